@@ -1,0 +1,187 @@
+/*
+ * kvd.h -- C ABI of libkvd, the MI355X (gfx950) library for KV-Direct's hot
+ * path: recompute attention keys and values from checkpointed residual-stream
+ * vectors, then run grouped-query decode attention over them.
+ *
+ * The operations follow the paper's statement of the problem:
+ *   - RMSNorm, Sec. 3.1, Eqs. (rmsnorm), (rms_def);
+ *   - the per-head projections, Sec. 3.1, Eqs. (q_proj), (k_proj), (v_proj);
+ *   - RoPE, Sec. 3.2, Eqs. (rope_cos), (rope_sin);
+ *   - the reconstruction identity, Sec. 3.2, Eqs. (k_recon), (v_recon);
+ *   - attention, Sec. 3.1, Eqs. (attn_weights), (head_output);
+ *   - one KV-Direct decode step, Sec. 3.4, Algorithm 1 (RECOMPUTE_KV, CONCAT,
+ *     ATTENTION) at cache budget 0, optionally with a stored tail of keys.
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ * Memory.   Every tensor pointer is a DEVICE pointer, owned by the caller and
+ *           aligned to 16 bytes.  The library never allocates, frees or
+ *           synchronises: each call validates its arguments on the host,
+ *           enqueues its kernels on `stream` (a hipStream_t; NULL means the
+ *           null stream) and returns.  Outputs must not alias inputs.
+ * Dtype.    shape->dtype (KVD_F32 or KVD_BF16) is the element type of every
+ *           tensor a call reads or writes, except `pos*` (int32) and the
+ *           workspace (opaque).  Arithmetic accumulates in fp32; K, V and q are
+ *           rounded once (round-to-nearest-even) to the dtype after RoPE.
+ * Layouts.  Row-major, innermost index last:
+ *             residuals  h      [B][h_ld][d_model]   rows 0..T-1 of each sequence used
+ *             gamma             [d_model]
+ *             W_q               [n_q_heads  * head_dim][d_model]   ([out][in])
+ *             W_k, W_v          [n_kv_heads * head_dim][d_model]   ([out][in])
+ *             q, attention out  [B][n_q_heads][head_dim]
+ *             K/V store         [B][n_kv_heads][t_cap][head_dim]   (kvd_kv_view)
+ *           Weights are stored [out][in], the transpose of the paper's
+ *           row-vector W (h W), so head h owns rows h*head_dim ..
+ *           (h+1)*head_dim-1.
+ * Norm.     hbar = h / sqrt(mean(h^2) + rms_eps) * gamma.
+ * RoPE.     Consecutive pairs (2i, 2i+1), 0-based, are rotated by
+ *           +p * rope_theta^(-2i/head_dim), p the token's absolute position.
+ * GQA.      Query head h reads KV head h / (n_q_heads / n_kv_heads).
+ * Scale.    Scores are q.k / sqrt(head_dim); softmax subtracts the maximum.
+ * Positions pos0[b] (int32, device): residual row t of sequence b sits at
+ *           absolute position pos0[b] + t.
+ * Errors.   Validation happens before any HIP call and returns a status; no
+ *           call aborts or throws.  KVD_ERR_DEVICE reports a failed launch.
+ *           kvd_last_error() returns a thread-local description of the last
+ *           non-OK status on the calling thread.
+ */
+#ifndef KVD_H
+#define KVD_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define KVD_ABI_VERSION 1
+
+typedef enum {
+  KVD_OK = 0,
+  KVD_ERR_NULL = 1,         /* a required pointer is NULL */
+  KVD_ERR_SHAPE = 2,        /* inconsistent or out-of-range sizes */
+  KVD_ERR_UNSUPPORTED = 3,  /* valid arguments this build has no kernel for */
+  KVD_ERR_WORKSPACE = 4,    /* workspace NULL or smaller than required */
+  KVD_ERR_ALIGN = 5,        /* a tensor pointer is not 16-byte aligned */
+  KVD_ERR_DEVICE = 6        /* the HIP runtime reported an error */
+} kvd_status;
+
+typedef enum { KVD_F32 = 0, KVD_BF16 = 1 } kvd_dtype;
+
+/* Operations whose workspace size kvd_workspace_bytes reports. */
+typedef enum { KVD_OP_DECODE_ATTN = 0, KVD_OP_CACHED_ATTN = 1, KVD_OP_FUSED = 2 } kvd_op;
+
+/* One attention layer's shape.
+ *   d_model     residual width; a positive multiple of 64.
+ *   n_q_heads   query heads; a positive multiple of n_kv_heads, with
+ *               n_q_heads / n_kv_heads <= 16.
+ *   n_kv_heads  key/value heads, >= 1.
+ *   head_dim    64, 128 or 256.
+ *   rms_eps     RMSNorm epsilon, finite and >= 0.
+ *   rope_theta  RoPE base, finite and > 0.
+ *   dtype       a kvd_dtype.                                                */
+typedef struct {
+  int32_t d_model;
+  int32_t n_q_heads;
+  int32_t n_kv_heads;
+  int32_t head_dim;
+  float rms_eps;
+  double rope_theta;
+  int32_t dtype;
+} kvd_attn_shape;
+
+/* A stored K/V block: k and v each [B][n_kv_heads][t_cap][head_dim] in the
+ * shape dtype.  A call touches rows t_off .. t_off+T-1 of every (b, head),
+ * which requires 0 <= t_off and t_off + T <= t_cap.                          */
+typedef struct {
+  void* k;
+  void* v;
+  int32_t t_cap;
+  int32_t t_off;
+} kvd_kv_view;
+
+/* RECOMPUTE_KV (Algorithm 1; Eqs. k_recon, v_recon): for each sequence b < B
+ * and residual row t < T,
+ *   K[b][j][t_off+t] = RoPE(hbar W_k^(j), pos0[b]+t),  V[b][j][t_off+t] = hbar W_v^(j),
+ * hbar = RMSNorm(h[b][t]).  This is also the prefill path (the K/V a cache
+ * would have stored); the same kernel produces them, so prefill, recompute,
+ * kvd_project_qkv's K/V and the fused kernel's K/V are bit-identical for the
+ * same residual row and position (Prop. reconstruction).
+ *   h     [B][h_ld][d_model], h_ld >= T.      pos0  [B] int32.
+ *   out   K/V view written at rows out->t_off .. out->t_off+T-1.
+ * B == 0 or T == 0 is a no-op.                                                */
+kvd_status kvd_recompute_kv(const kvd_attn_shape* shape, const void* h, int32_t h_ld,
+                            const void* gamma, const void* w_k, const void* w_v,
+                            const int32_t* pos0, int32_t B, int32_t T,
+                            const kvd_kv_view* out, void* stream);
+
+/* Current-token projections of a decode step (Algorithm 1; Eqs. q_proj,
+ * k_proj, v_proj): for each sequence b,
+ *   q_out[b][h] = RoPE(hbar W_q^(h), pos[b]),  hbar = RMSNorm(h_new[b]),
+ * and, if kv_out is not NULL, the token's own K and V written at row
+ * kv_out->t_off (exactly what kvd_recompute_kv gives for that row).
+ *   h_new [B][d_model].   pos [B] int32.   q_out [B][n_q_heads][head_dim].   */
+kvd_status kvd_project_qkv(const kvd_attn_shape* shape, const void* h_new, const void* gamma,
+                           const void* w_q, const void* w_k, const void* w_v,
+                           const int32_t* pos, int32_t B, void* q_out,
+                           const kvd_kv_view* kv_out, void* stream);
+
+/* ATTENTION for one decode query per sequence and head (Eqs. attn_weights,
+ * head_output) over T >= 1 stored keys: rows kv->t_off .. kv->t_off+T-1.
+ * Split-K: partial softmax states go to the workspace and a second kernel
+ * merges them.  ws (256-byte aligned) must hold kvd_workspace_bytes(shape,
+ * KVD_OP_DECODE_ATTN, B, T, 0) bytes; its contents on entry are ignored, and
+ * calls sharing one workspace must be ordered on one stream.
+ *   q [B][n_q_heads][head_dim].   out [B][n_q_heads][head_dim].               */
+kvd_status kvd_decode_attn(const kvd_attn_shape* shape, const void* q, const kvd_kv_view* kv,
+                           int32_t B, int32_t T, void* out, void* ws, size_t ws_bytes,
+                           void* stream);
+
+/* The cached-K/V baseline: a standard KV-cache decode step's attention, which
+ * reads every key and value from a persistent bf16 cache in HBM (the
+ * B_read = 2 N n_kv d_head b bytes of Eq. read_bytes).  Same arguments and
+ * kernels as kvd_decode_attn; shape->dtype must be KVD_BF16.  Workspace:
+ * kvd_workspace_bytes(shape, KVD_OP_CACHED_ATTN, B, T, 0).                    */
+kvd_status kvd_cached_attn(const kvd_attn_shape* shape, const void* q, const kvd_kv_view* kv,
+                           int32_t B, int32_t T, void* out, void* ws, size_t ws_bytes,
+                           void* stream);
+
+/* One KV-Direct decode step's attention at cache budget 0 (Algorithm 1:
+ * RECOMPUTE_KV, CONCAT, ATTENTION): keys and values are recomputed from the
+ * checkpointed residuals h rows 0..T_rec-1 (positions pos0[b]+t) inside the
+ * kernel and attended from LDS without being written to HBM, then
+ * concatenated with T_tail stored keys (tail rows tail->t_off ..
+ * tail->t_off+T_tail-1; typically the current token's own K/V from
+ * kvd_project_qkv, or a window of cached recent keys).
+ *   T_rec >= 0, T_tail >= 0, T_rec + T_tail >= 1; tail may be NULL iff T_tail == 0.
+ *   ws: kvd_workspace_bytes(shape, KVD_OP_FUSED, B, T_rec, T_tail) bytes.
+ *   kv_debug: NULL in production.  If not NULL, the recomputed K/V are also
+ *   written to it at rows kv_debug->t_off .. +T_rec-1 (for bit-identity checks).
+ * Supports both dtypes.                                                       */
+kvd_status kvd_fused_recompute_attn(const kvd_attn_shape* shape, const void* q, const void* h,
+                                    int32_t h_ld, const void* gamma, const void* w_k,
+                                    const void* w_v, const int32_t* pos0, int32_t B,
+                                    int32_t T_rec, const kvd_kv_view* tail, int32_t T_tail,
+                                    void* out, void* ws, size_t ws_bytes,
+                                    const kvd_kv_view* kv_debug, void* stream);
+
+/* Workspace bytes an attention call needs (0 on invalid arguments).  For
+ * KVD_OP_DECODE_ATTN / KVD_OP_CACHED_ATTN, T_main is T and T_tail must be 0;
+ * for KVD_OP_FUSED they are T_rec and T_tail.                                 */
+size_t kvd_workspace_bytes(const kvd_attn_shape* shape, int32_t op, int32_t B, int32_t T_main,
+                           int32_t T_tail);
+
+/* Number of split-K partitions an attention call uses (0 on invalid arguments). */
+int32_t kvd_num_splits(const kvd_attn_shape* shape, int32_t op, int32_t B, int32_t T_main,
+                       int32_t T_tail);
+
+const char* kvd_status_str(kvd_status status);
+const char* kvd_last_error(void);
+int kvd_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* KVD_H */

@@ -1,0 +1,348 @@
+// C ABI of libkvd: argument validation (host only, before any HIP call), the
+// split policy and workspace sizing, and kernel launches.  See include/kvd.h.
+#include "kvd.h"
+
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <string>
+
+#include "kvd_launch.h"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+kvd_status fail(kvd_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return st;
+}
+
+#define KVD_TRY(expr)               \
+  do {                              \
+    kvd_status _st = (expr);        \
+    if (_st != KVD_OK) return _st;  \
+  } while (0)
+
+size_t elem_size(const kvd_attn_shape* s) { return s->dtype == KVD_BF16 ? 2 : 4; }
+
+kvd_status check_shape(const kvd_attn_shape* s) {
+  if (s == nullptr) return fail(KVD_ERR_NULL, "shape is NULL");
+  if (s->dtype != KVD_F32 && s->dtype != KVD_BF16) return fail(KVD_ERR_UNSUPPORTED, "dtype %d is not KVD_F32 or KVD_BF16", s->dtype);
+  if (s->d_model <= 0 || s->d_model % kvd::kKT != 0)
+    return fail(KVD_ERR_SHAPE, "d_model=%d must be a positive multiple of %d", s->d_model, kvd::kKT);
+  if (s->head_dim != 64 && s->head_dim != 128 && s->head_dim != 256)
+    return fail(KVD_ERR_UNSUPPORTED, "head_dim=%d is not 64, 128 or 256", s->head_dim);
+  if (s->n_kv_heads < 1 || s->n_q_heads < 1) return fail(KVD_ERR_SHAPE, "n_q_heads=%d n_kv_heads=%d must be >= 1", s->n_q_heads, s->n_kv_heads);
+  if (s->n_kv_heads > 65535) return fail(KVD_ERR_SHAPE, "n_kv_heads=%d exceeds 65535", s->n_kv_heads);
+  if (s->n_q_heads % s->n_kv_heads != 0)
+    return fail(KVD_ERR_SHAPE, "n_q_heads=%d is not a multiple of n_kv_heads=%d", s->n_q_heads, s->n_kv_heads);
+  if (s->n_q_heads / s->n_kv_heads > kvd::kMaxGroup)
+    return fail(KVD_ERR_UNSUPPORTED, "group size %d exceeds %d", s->n_q_heads / s->n_kv_heads, kvd::kMaxGroup);
+  if (!std::isfinite(s->rms_eps) || s->rms_eps < 0.0f) return fail(KVD_ERR_SHAPE, "rms_eps must be finite and >= 0");
+  if (!std::isfinite(s->rope_theta) || s->rope_theta <= 0.0) return fail(KVD_ERR_SHAPE, "rope_theta must be finite and > 0");
+  return KVD_OK;
+}
+
+kvd_status check_ptr(const void* p, const char* name) {
+  if (p == nullptr) return fail(KVD_ERR_NULL, "%s is NULL", name);
+  if ((reinterpret_cast<uintptr_t>(p) & 15u) != 0) return fail(KVD_ERR_ALIGN, "%s is not 16-byte aligned", name);
+  return KVD_OK;
+}
+
+kvd_status check_view(const kvd_kv_view* v, int32_t T, const char* name) {
+  if (v == nullptr) return fail(KVD_ERR_NULL, "%s is NULL", name);
+  std::string nk = std::string(name) + "->k", nv = std::string(name) + "->v";
+  KVD_TRY(check_ptr(v->k, nk.c_str()));
+  KVD_TRY(check_ptr(v->v, nv.c_str()));
+  if (v->t_off < 0 || v->t_cap < 1 || (int64_t)v->t_off + T > v->t_cap)
+    return fail(KVD_ERR_SHAPE, "%s rows t_off=%d .. t_off+%d exceed t_cap=%d", name, v->t_off, T, v->t_cap);
+  return KVD_OK;
+}
+
+kvd_status check_batch(int32_t B) {
+  if (B < 0 || B > 65535) return fail(KVD_ERR_SHAPE, "B=%d must be in [0, 65535]", B);
+  return KVD_OK;
+}
+
+void fill_rev(const kvd_attn_shape* s, double* rev) {
+  const int pairs = s->head_dim / 2;
+  for (int i = 0; i < kvd::kMaxPairs; ++i)
+    rev[i] = i < pairs ? std::pow(s->rope_theta, -2.0 * i / s->head_dim) / (2.0 * M_PI) : 0.0;
+}
+
+int32_t ceil_div(int64_t a, int64_t b) { return (int32_t)((a + b - 1) / b); }
+
+int32_t splits(int32_t op, int32_t T_main, int32_t T_tail) {
+  if (op == KVD_OP_FUSED) return ceil_div(T_main, kvd::kMtBf16) + ceil_div(T_tail, kvd::kMtBf16);
+  return ceil_div(T_main, kvd::kTile);
+}
+
+size_t ws_acc_bytes(const kvd_attn_shape* s, int32_t B, int32_t S) {
+  return kvd::align_up((size_t)B * s->n_q_heads * S * s->head_dim * sizeof(float), 256);
+}
+size_t ws_total(const kvd_attn_shape* s, int32_t B, int32_t S) {
+  return ws_acc_bytes(s, B, S) + kvd::align_up((size_t)B * s->n_q_heads * S * 2 * sizeof(float), 256);
+}
+
+kvd_status check_ws(const kvd_attn_shape* s, int32_t B, int32_t S, void* ws, size_t ws_bytes) {
+  const size_t need = ws_total(s, B, S);
+  if (ws == nullptr) return fail(KVD_ERR_WORKSPACE, "workspace is NULL (%zu bytes needed)", need);
+  if ((reinterpret_cast<uintptr_t>(ws) & 255u) != 0) return fail(KVD_ERR_ALIGN, "workspace is not 256-byte aligned");
+  if (ws_bytes < need) return fail(KVD_ERR_WORKSPACE, "workspace holds %zu bytes, %zu needed", ws_bytes, need);
+  return KVD_OK;
+}
+
+constexpr size_t kLdsLimit = 160 * 1024;  // LDS per workgroup on gfx950
+
+template <typename T>
+size_t attn_lds_need(const kvd_attn_shape* s, bool fused) {
+  const int g = s->n_q_heads / s->n_kv_heads;
+  const int hd = s->head_dim;
+  return fused ? kvd::fused_lds_bytes<T>(g, hd, sizeof(T) == 2 ? kvd::kMtBf16 : kvd::kMtF32)
+               : kvd::decode_lds_bytes<T>(g, hd);
+}
+
+kvd_status check_lds(const kvd_attn_shape* s, bool fused) {
+  const size_t need = s->dtype == KVD_BF16 ? attn_lds_need<uint16_t>(s, fused) : attn_lds_need<float>(s, fused);
+  if (need > kLdsLimit)
+    return fail(KVD_ERR_UNSUPPORTED, "head_dim=%d with group size %d needs %zu bytes of LDS (limit %zu)", s->head_dim,
+                s->n_q_heads / s->n_kv_heads, need, kLdsLimit);
+  return KVD_OK;
+}
+
+kvd_status device_status(hipError_t e, const char* what) {
+  if (e == hipSuccess) return KVD_OK;
+  return fail(KVD_ERR_DEVICE, "%s: %s", what, hipGetErrorString(e));
+}
+
+kvd_status attn_common(const kvd_attn_shape* shape, const void* q, const kvd_kv_view* kv, int32_t B, int32_t T,
+                       void* out, void* ws, size_t ws_bytes, void* stream, bool cached) {
+  KVD_TRY(check_shape(shape));
+  if (cached && shape->dtype != KVD_BF16) return fail(KVD_ERR_UNSUPPORTED, "kvd_cached_attn reads a bf16 cache; dtype must be KVD_BF16");
+  KVD_TRY(check_batch(B));
+  if (T < 1) return fail(KVD_ERR_SHAPE, "T=%d: attention needs at least one key", T);
+  KVD_TRY(check_lds(shape, false));
+  if (B == 0) return KVD_OK;
+  KVD_TRY(check_ptr(q, "q"));
+  KVD_TRY(check_ptr(out, "out"));
+  KVD_TRY(check_view(kv, T, "kv"));
+  const int32_t S = splits(KVD_OP_DECODE_ATTN, T, 0);
+  KVD_TRY(check_ws(shape, B, S, ws, ws_bytes));
+  kvd::AttnArgs a{};
+  a.q = q;
+  a.k = kv->k;
+  a.v = kv->v;
+  a.t_cap = kv->t_cap;
+  a.t_off = kv->t_off;
+  a.out = out;
+  a.ws_acc = static_cast<float*>(ws);
+  a.ws_ml = reinterpret_cast<float*>(static_cast<char*>(ws) + ws_acc_bytes(shape, B, S));
+  a.B = B;
+  a.T = T;
+  a.n_q = shape->n_q_heads;
+  a.n_kv = shape->n_kv_heads;
+  a.S = S;
+  return device_status(kvd::launch_decode(a, shape->dtype == KVD_BF16, shape->head_dim, (hipStream_t)stream),
+                       cached ? "kvd_cached_attn launch" : "kvd_decode_attn launch");
+}
+
+}  // namespace
+
+extern "C" {
+
+int kvd_abi_version(void) { return KVD_ABI_VERSION; }
+
+const char* kvd_status_str(kvd_status st) {
+  switch (st) {
+    case KVD_OK: return "KVD_OK";
+    case KVD_ERR_NULL: return "KVD_ERR_NULL";
+    case KVD_ERR_SHAPE: return "KVD_ERR_SHAPE";
+    case KVD_ERR_UNSUPPORTED: return "KVD_ERR_UNSUPPORTED";
+    case KVD_ERR_WORKSPACE: return "KVD_ERR_WORKSPACE";
+    case KVD_ERR_ALIGN: return "KVD_ERR_ALIGN";
+    case KVD_ERR_DEVICE: return "KVD_ERR_DEVICE";
+  }
+  return "KVD_ERR_UNKNOWN";
+}
+
+const char* kvd_last_error(void) { return g_last_error.c_str(); }
+
+kvd_status kvd_recompute_kv(const kvd_attn_shape* shape, const void* h, int32_t h_ld, const void* gamma,
+                            const void* w_k, const void* w_v, const int32_t* pos0, int32_t B, int32_t T,
+                            const kvd_kv_view* out, void* stream) {
+  KVD_TRY(check_shape(shape));
+  KVD_TRY(check_batch(B));
+  if (T < 0) return fail(KVD_ERR_SHAPE, "T=%d must be >= 0", T);
+  if (B == 0 || T == 0) return KVD_OK;
+  if (h_ld < T) return fail(KVD_ERR_SHAPE, "h_ld=%d is smaller than T=%d", h_ld, T);
+  KVD_TRY(check_ptr(h, "h"));
+  KVD_TRY(check_ptr(gamma, "gamma"));
+  KVD_TRY(check_ptr(w_k, "w_k"));
+  KVD_TRY(check_ptr(w_v, "w_v"));
+  if (pos0 == nullptr) return fail(KVD_ERR_NULL, "pos0 is NULL");
+  KVD_TRY(check_view(out, T, "out"));
+  kvd::ProjArgs a{};
+  a.h = h;
+  a.gamma = gamma;
+  a.w_k = w_k;
+  a.w_v = w_v;
+  a.pos0 = pos0;
+  a.k_out = out->k;
+  a.v_out = out->v;
+  a.h_ld = h_ld;
+  a.kv_t_cap = out->t_cap;
+  a.kv_t_off = out->t_off;
+  a.d = shape->d_model;
+  a.n_q = shape->n_q_heads;
+  a.n_kv = shape->n_kv_heads;
+  a.B = B;
+  a.T = T;
+  a.n_kv_units = shape->n_kv_heads;
+  a.eps = shape->rms_eps;
+  fill_rev(shape, a.rev);
+  return device_status(kvd::launch_proj(a, shape->dtype == KVD_BF16, shape->head_dim, a.n_kv_units, (hipStream_t)stream),
+                       "kvd_recompute_kv launch");
+}
+
+kvd_status kvd_project_qkv(const kvd_attn_shape* shape, const void* h_new, const void* gamma, const void* w_q,
+                           const void* w_k, const void* w_v, const int32_t* pos, int32_t B, void* q_out,
+                           const kvd_kv_view* kv_out, void* stream) {
+  KVD_TRY(check_shape(shape));
+  KVD_TRY(check_batch(B));
+  if (B == 0) return KVD_OK;
+  KVD_TRY(check_ptr(h_new, "h_new"));
+  KVD_TRY(check_ptr(gamma, "gamma"));
+  KVD_TRY(check_ptr(w_q, "w_q"));
+  KVD_TRY(check_ptr(q_out, "q_out"));
+  if (pos == nullptr) return fail(KVD_ERR_NULL, "pos is NULL");
+  if (kv_out != nullptr) {
+    KVD_TRY(check_ptr(w_k, "w_k"));
+    KVD_TRY(check_ptr(w_v, "w_v"));
+    KVD_TRY(check_view(kv_out, 1, "kv_out"));
+  }
+  kvd::ProjArgs a{};
+  a.h = h_new;
+  a.gamma = gamma;
+  a.w_q = w_q;
+  a.w_k = w_k;
+  a.w_v = w_v;
+  a.pos0 = pos;
+  a.q_out = q_out;
+  if (kv_out) {
+    a.k_out = kv_out->k;
+    a.v_out = kv_out->v;
+    a.kv_t_cap = kv_out->t_cap;
+    a.kv_t_off = kv_out->t_off;
+  }
+  a.h_ld = 1;
+  a.d = shape->d_model;
+  a.n_q = shape->n_q_heads;
+  a.n_kv = shape->n_kv_heads;
+  a.B = B;
+  a.T = 1;
+  a.n_kv_units = kv_out ? shape->n_kv_heads : 0;
+  a.eps = shape->rms_eps;
+  fill_rev(shape, a.rev);
+  const int units = a.n_kv_units + (shape->n_q_heads + 1) / 2;
+  return device_status(kvd::launch_proj(a, shape->dtype == KVD_BF16, shape->head_dim, units, (hipStream_t)stream),
+                       "kvd_project_qkv launch");
+}
+
+kvd_status kvd_decode_attn(const kvd_attn_shape* shape, const void* q, const kvd_kv_view* kv, int32_t B, int32_t T,
+                           void* out, void* ws, size_t ws_bytes, void* stream) {
+  return attn_common(shape, q, kv, B, T, out, ws, ws_bytes, stream, false);
+}
+
+kvd_status kvd_cached_attn(const kvd_attn_shape* shape, const void* q, const kvd_kv_view* kv, int32_t B, int32_t T,
+                           void* out, void* ws, size_t ws_bytes, void* stream) {
+  return attn_common(shape, q, kv, B, T, out, ws, ws_bytes, stream, true);
+}
+
+kvd_status kvd_fused_recompute_attn(const kvd_attn_shape* shape, const void* q, const void* h, int32_t h_ld,
+                                    const void* gamma, const void* w_k, const void* w_v, const int32_t* pos0,
+                                    int32_t B, int32_t T_rec, const kvd_kv_view* tail, int32_t T_tail, void* out,
+                                    void* ws, size_t ws_bytes, const kvd_kv_view* kv_debug, void* stream) {
+  KVD_TRY(check_shape(shape));
+  KVD_TRY(check_batch(B));
+  if (T_rec < 0 || T_tail < 0 || (int64_t)T_rec + T_tail < 1)
+    return fail(KVD_ERR_SHAPE, "T_rec=%d T_tail=%d: need T_rec, T_tail >= 0 and at least one key", T_rec, T_tail);
+  KVD_TRY(check_lds(shape, true));
+  if (B == 0) return KVD_OK;
+  KVD_TRY(check_ptr(q, "q"));
+  KVD_TRY(check_ptr(out, "out"));
+  if (T_rec > 0) {
+    if (h_ld < T_rec) return fail(KVD_ERR_SHAPE, "h_ld=%d is smaller than T_rec=%d", h_ld, T_rec);
+    KVD_TRY(check_ptr(h, "h"));
+    KVD_TRY(check_ptr(gamma, "gamma"));
+    KVD_TRY(check_ptr(w_k, "w_k"));
+    KVD_TRY(check_ptr(w_v, "w_v"));
+    if (pos0 == nullptr) return fail(KVD_ERR_NULL, "pos0 is NULL");
+    if (kv_debug != nullptr) KVD_TRY(check_view(kv_debug, T_rec, "kv_debug"));
+  }
+  if (T_tail > 0) KVD_TRY(check_view(tail, T_tail, "tail"));
+  const int32_t S = splits(KVD_OP_FUSED, T_rec, T_tail);
+  KVD_TRY(check_ws(shape, B, S, ws, ws_bytes));
+  kvd::FusedArgs a{};
+  a.q = q;
+  a.h = h;
+  a.h_ld = h_ld;
+  a.gamma = gamma;
+  a.w_k = w_k;
+  a.w_v = w_v;
+  a.pos0 = pos0;
+  if (T_tail > 0) {
+    a.tk = tail->k;
+    a.tv = tail->v;
+    a.tail_t_cap = tail->t_cap;
+    a.tail_t_off = tail->t_off;
+  }
+  a.T_tail = T_tail;
+  if (kv_debug != nullptr && T_rec > 0) {
+    a.dbg_k = kv_debug->k;
+    a.dbg_v = kv_debug->v;
+    a.dbg_t_cap = kv_debug->t_cap;
+    a.dbg_t_off = kv_debug->t_off;
+  }
+  a.ws_acc = static_cast<float*>(ws);
+  a.ws_ml = reinterpret_cast<float*>(static_cast<char*>(ws) + ws_acc_bytes(shape, B, S));
+  a.out = out;
+  a.d = shape->d_model;
+  a.n_q = shape->n_q_heads;
+  a.n_kv = shape->n_kv_heads;
+  a.B = B;
+  a.T_rec = T_rec;
+  a.n_rec = ceil_div(T_rec, kvd::kMtBf16);
+  a.S = S;
+  a.eps = shape->rms_eps;
+  fill_rev(shape, a.rev);
+  return device_status(kvd::launch_fused(a, shape->dtype == KVD_BF16, shape->head_dim, (hipStream_t)stream),
+                       "kvd_fused_recompute_attn launch");
+}
+
+int32_t kvd_num_splits(const kvd_attn_shape* shape, int32_t op, int32_t B, int32_t T_main, int32_t T_tail) {
+  if (check_shape(shape) != KVD_OK || B < 0 || T_main < 0 || T_tail < 0) return 0;
+  if (op == KVD_OP_FUSED) {
+    if ((int64_t)T_main + T_tail < 1) return 0;
+  } else if (op == KVD_OP_DECODE_ATTN || op == KVD_OP_CACHED_ATTN) {
+    if (T_main < 1 || T_tail != 0) return 0;
+  } else {
+    return 0;
+  }
+  return splits(op, T_main, T_tail);
+}
+
+size_t kvd_workspace_bytes(const kvd_attn_shape* shape, int32_t op, int32_t B, int32_t T_main, int32_t T_tail) {
+  const int32_t S = kvd_num_splits(shape, op, B, T_main, T_tail);
+  if (S == 0) return 0;
+  return ws_total(shape, B, S);
+}
+
+}  // extern "C"

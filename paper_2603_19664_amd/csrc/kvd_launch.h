@@ -1,0 +1,73 @@
+// Kernel argument blocks and launcher entry points shared by the C ABI layer
+// (kvd_api.cpp) and the kernels (kvd_kernels.hip).  Internal to libkvd.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "kvd_layout.h"
+
+namespace kvd {
+
+// RMSNorm + projection + RoPE of B*T token rows.  grid.y enumerates units:
+// y < n_kv_units -> KV head y (its K rows get RoPE, V rows do not, written to
+// k_out / v_out); otherwise query heads 2u, 2u+1 (u = y - n_kv_units), written to
+// q_out [B][n_q][HD] (T must then be 1).
+struct ProjArgs {
+  const void* h;
+  const void* gamma;
+  const void* w_k;
+  const void* w_v;
+  const void* w_q;
+  const int32_t* pos0;
+  void* k_out;
+  void* v_out;
+  void* q_out;
+  long long h_ld;
+  int kv_t_cap, kv_t_off;
+  int d, n_q, n_kv, B, T, n_kv_units;
+  float eps;
+  double rev[kMaxPairs];  // RoPE frequency of pair i in revolutions per position
+};
+
+// Fused recompute + attention.  grid = (S, n_kv, B) with S = n_rec + n_tail
+// chunks of the tile size; chunk s < n_rec recomputes residual rows
+// s*MT .. s*MT+MT-1, the rest attend stored tail rows.
+struct FusedArgs {
+  const void* q;
+  const void* h;
+  long long h_ld;
+  const void* gamma;
+  const void* w_k;
+  const void* w_v;
+  const int32_t* pos0;
+  const void* tk;
+  const void* tv;
+  int tail_t_cap, tail_t_off, T_tail;
+  void* dbg_k;
+  void* dbg_v;
+  int dbg_t_cap, dbg_t_off;
+  float* ws_acc;
+  float* ws_ml;
+  void* out;
+  int d, n_q, n_kv, B, T_rec, n_rec, S;
+  float eps;
+  double rev[kMaxPairs];
+};
+
+// Split-K attention over stored K/V: S = ceil(T / kTile) chunks.
+struct AttnArgs {
+  const void* q;
+  const void* k;
+  const void* v;
+  int t_cap, t_off;
+  void* out;
+  float* ws_acc;
+  float* ws_ml;
+  int B, T, n_q, n_kv, S;
+};
+
+hipError_t launch_proj(const ProjArgs& a, int dtype_bf16, int hd, int n_units, hipStream_t st);
+hipError_t launch_fused(const FusedArgs& a, int dtype_bf16, int hd, hipStream_t st);
+hipError_t launch_decode(const AttnArgs& a, int dtype_bf16, int hd, hipStream_t st);
+
+}  // namespace kvd

@@ -1,0 +1,80 @@
+// Launch geometry and LDS carve-up shared by the host launchers and the
+// kernels of libkvd.  Plain constexpr arithmetic, usable on host and device.
+#pragma once
+#include <stddef.h>
+#include <stdint.h>
+
+namespace kvd {
+
+constexpr int kThreads = 256;   // every kernel: 4 wave64 waves
+constexpr int kKT = 64;         // d-elements per K-step of the projection GEMM
+constexpr int kTile = 64;       // keys per attention tile (one split-K partial)
+constexpr int kMaxGroup = 16;   // max query heads per KV head
+constexpr int kMaxPairs = 128;  // head_dim / 2 for head_dim <= 256
+
+// Tokens per workgroup of the projection engines.
+constexpr int kMtBf16 = 64;
+constexpr int kMtF32 = 64;
+
+constexpr size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+// Row strides (elements) of the LDS tiles; the +8 / +4 padding keeps the
+// 16-byte row reads of a wave on distinct LDS banks.
+template <typename T> struct Pad;
+template <> struct Pad<uint16_t> { static constexpr int kv = 8; static constexpr int h = 8; };
+template <> struct Pad<float> { static constexpr int kv = 4; static constexpr int h = 4; };
+
+template <typename T>
+constexpr int kv_ld(int hd) { return 2 * hd + Pad<T>::kv; }
+template <typename T>
+constexpr int h_ld(void) { return kKT + Pad<T>::h; }
+
+// LDS layout of the attention part (decode / fused kernels); g = group size.
+struct AttnLds {
+  size_t q, s, red, ml, acc, end;
+};
+constexpr size_t red_floats(int g, int hd) {
+  return (size_t)(g * hd > 2048 ? g * hd : 2048);
+}
+constexpr AttnLds attn_lds(size_t base, int g, int hd, int rows) {
+  AttnLds L{};
+  L.q = align_up(base, 16);
+  L.s = align_up(L.q + sizeof(float) * g * hd, 16);
+  L.red = align_up(L.s + sizeof(float) * g * rows, 16);
+  L.ml = align_up(L.red + sizeof(float) * red_floats(g, hd), 16);
+  L.acc = align_up(L.ml + sizeof(float) * 2 * g, 16);
+  L.end = align_up(L.acc + sizeof(float) * g * hd, 16);
+  return L;
+}
+
+// LDS layout of the projection engine: staged h-bar tiles (2 buffers), the
+// K/V tile, and per-token 1/rms and positions, plus the RoPE frequency table.
+struct ProjLds {
+  size_t hst, kv, rinv, pos, rev, end;
+};
+template <typename T>
+constexpr ProjLds proj_lds(int hd, int mt) {
+  ProjLds L{};
+  L.rev = 0;                                                       // double[kMaxPairs]
+  L.rinv = align_up(L.rev + sizeof(double) * kMaxPairs, 16);        // float[mt]
+  L.pos = align_up(L.rinv + sizeof(float) * mt, 16);                // int[mt]
+  L.hst = align_up(L.pos + sizeof(int) * mt, 16);                   // T[2][mt][h_ld]
+  size_t hst_end = L.hst + sizeof(T) * 2 * mt * h_ld<T>();
+  L.kv = align_up(L.pos + sizeof(int) * mt, 16);                    // T[mt][kv_ld] (aliases hst)
+  size_t kv_end = L.kv + sizeof(T) * mt * kv_ld<T>(hd);
+  L.end = align_up(hst_end > kv_end ? hst_end : kv_end, 16);
+  return L;
+}
+
+template <typename T>
+constexpr size_t decode_lds_bytes(int g, int hd) {
+  // K/V tile followed by the attention scratch.
+  return attn_lds(align_up(sizeof(T) * kTile * kv_ld<T>(hd), 16), g, hd, kTile).end;
+}
+
+template <typename T>
+constexpr size_t fused_lds_bytes(int g, int hd, int mt) {
+  return attn_lds(proj_lds<T>(hd, mt).end, g, hd, mt).end;
+}
+
+}  // namespace kvd

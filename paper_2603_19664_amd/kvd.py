@@ -1,0 +1,225 @@
+"""Python binding of libkvd (include/kvd.h): argument marshalling only.
+
+Each function has the name of the C entry point it calls, takes torch tensors
+that live on the GPU, checks their device / dtype / layout, passes raw pointers
+and torch's current HIP stream through ctypes, and raises KvdError on a non-OK
+status.  Every step of the computation runs in the HIP kernels of libkvd; there
+is no fallback.  Importing this module fails loudly if libkvd.so is not built.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+from dataclasses import dataclass
+
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libkvd.so")
+HEADER_PATH = os.path.join(os.path.dirname(_PKG), "include", "kvd.h")
+
+KVD_OK, KVD_ERR_NULL, KVD_ERR_SHAPE, KVD_ERR_UNSUPPORTED, KVD_ERR_WORKSPACE, KVD_ERR_ALIGN, KVD_ERR_DEVICE = range(7)
+KVD_F32, KVD_BF16 = 0, 1
+KVD_OP_DECODE_ATTN, KVD_OP_CACHED_ATTN, KVD_OP_FUSED = 0, 1, 2
+
+_DTYPES = {KVD_F32: torch.float32, KVD_BF16: torch.bfloat16}
+
+
+class KvdError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"{status_str(status)}: {msg}")
+        self.status = status
+
+
+class AttnShape(ctypes.Structure):
+    _fields_ = [
+        ("d_model", ctypes.c_int32),
+        ("n_q_heads", ctypes.c_int32),
+        ("n_kv_heads", ctypes.c_int32),
+        ("head_dim", ctypes.c_int32),
+        ("rms_eps", ctypes.c_float),
+        ("rope_theta", ctypes.c_double),
+        ("dtype", ctypes.c_int32),
+    ]
+
+
+class KvView(ctypes.Structure):
+    _fields_ = [("k", ctypes.c_void_p), ("v", ctypes.c_void_p), ("t_cap", ctypes.c_int32), ("t_off", ctypes.c_int32)]
+
+
+def _load() -> ctypes.CDLL:
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is not built; run `python -m paper_2603_19664_amd.build` "
+                          "(or __graft_entry__.build()) first")
+    lib = ctypes.CDLL(LIB_PATH)
+    P, I32, SZ, VP = ctypes.POINTER, ctypes.c_int32, ctypes.c_size_t, ctypes.c_void_p
+    S, V = P(AttnShape), P(KvView)
+    sig = {
+        "kvd_recompute_kv": [S, VP, I32, VP, VP, VP, VP, I32, I32, V, VP],
+        "kvd_project_qkv": [S, VP, VP, VP, VP, VP, VP, I32, VP, V, VP],
+        "kvd_decode_attn": [S, VP, V, I32, I32, VP, VP, SZ, VP],
+        "kvd_cached_attn": [S, VP, V, I32, I32, VP, VP, SZ, VP],
+        "kvd_fused_recompute_attn": [S, VP, VP, I32, VP, VP, VP, VP, I32, I32, V, I32, VP, VP, SZ, V, VP],
+    }
+    for name, args in sig.items():
+        f = getattr(lib, name)
+        f.argtypes = args
+        f.restype = ctypes.c_int
+    lib.kvd_workspace_bytes.argtypes = [S, I32, I32, I32, I32]
+    lib.kvd_workspace_bytes.restype = SZ
+    lib.kvd_num_splits.argtypes = [S, I32, I32, I32, I32]
+    lib.kvd_num_splits.restype = I32
+    lib.kvd_status_str.argtypes = [ctypes.c_int]
+    lib.kvd_status_str.restype = ctypes.c_char_p
+    lib.kvd_last_error.argtypes = []
+    lib.kvd_last_error.restype = ctypes.c_char_p
+    lib.kvd_abi_version.argtypes = []
+    lib.kvd_abi_version.restype = ctypes.c_int
+    return lib
+
+
+lib = _load()
+
+
+def header_symbols(path: str = HEADER_PATH) -> list:
+    """Names of the functions include/kvd.h declares."""
+    with open(path) as f:
+        src = f.read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(kvd_[a-z_]+)\s*\(", src)))
+
+
+def status_str(status: int) -> str:
+    return lib.kvd_status_str(status).decode()
+
+
+def last_error() -> str:
+    return lib.kvd_last_error().decode()
+
+
+def abi_version() -> int:
+    return lib.kvd_abi_version()
+
+
+@dataclass(frozen=True)
+class Shape:
+    """One attention layer's shape (kvd_attn_shape)."""
+    d_model: int
+    n_q_heads: int
+    n_kv_heads: int
+    head_dim: int
+    rms_eps: float
+    rope_theta: float
+    dtype: int
+
+    @property
+    def torch_dtype(self) -> torch.dtype:
+        return _DTYPES[self.dtype]
+
+    def c(self) -> AttnShape:
+        return AttnShape(self.d_model, self.n_q_heads, self.n_kv_heads, self.head_dim, self.rms_eps,
+                         self.rope_theta, self.dtype)
+
+
+def shape_of(wl) -> Shape:
+    """The Shape of a configs.Workload."""
+    return Shape(wl.d_model, wl.n_q, wl.n_kv, wl.head_dim, wl.rms_eps, wl.rope_theta,
+                 KVD_BF16 if wl.dtype == "bf16" else KVD_F32)
+
+
+def _check(st: int):
+    if st != KVD_OK:
+        raise KvdError(st, last_error())
+
+
+def _ptr(t, name, dtype=None, ndim=None):
+    if t is None:
+        return None
+    if not isinstance(t, torch.Tensor) or t.device.type != "cuda":
+        raise ValueError(f"{name} must be a torch tensor on the GPU")
+    if dtype is not None and t.dtype != dtype:
+        raise ValueError(f"{name} has dtype {t.dtype}, expected {dtype}")
+    if ndim is not None and t.dim() != ndim:
+        raise ValueError(f"{name} has {t.dim()} dims, expected {ndim}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return t.data_ptr()
+
+
+def _stream():
+    return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def _view(k, v, t_off, name, dt):
+    if k is None and v is None:
+        return None
+    if k is None or v is None or k.shape != v.shape or k.dim() != 4:
+        raise ValueError(f"{name}: k and v must both be [B, n_kv, t_cap, head_dim] tensors")
+    return KvView(_ptr(k, name + "_k", dt), _ptr(v, name + "_v", dt), k.shape[2], t_off)
+
+
+def kvd_workspace_bytes(shape: Shape, op: int, B: int, T_main: int, T_tail: int = 0) -> int:
+    return lib.kvd_workspace_bytes(ctypes.byref(shape.c()), op, B, T_main, T_tail)
+
+
+def kvd_num_splits(shape: Shape, op: int, B: int, T_main: int, T_tail: int = 0) -> int:
+    return lib.kvd_num_splits(ctypes.byref(shape.c()), op, B, T_main, T_tail)
+
+
+def workspace(shape: Shape, op: int, B: int, T_main: int, T_tail: int = 0, device="cuda") -> torch.Tensor:
+    """A device buffer of kvd_workspace_bytes bytes (torch allocations are 256-byte aligned)."""
+    n = kvd_workspace_bytes(shape, op, B, T_main, T_tail)
+    return torch.empty(max(n, 256), dtype=torch.uint8, device=device)
+
+
+def kvd_recompute_kv(shape: Shape, h, gamma, w_k, w_v, pos0, T: int, k_out, v_out, t_off: int = 0):
+    """K/V of residual rows 0..T-1 of h [B, h_ld, d] into k_out/v_out [B, n_kv, t_cap, hd] at rows t_off.."""
+    dt = shape.torch_dtype
+    B, h_ld = h.shape[0], h.shape[1]
+    view = _view(k_out, v_out, t_off, "out", dt)
+    _check(lib.kvd_recompute_kv(ctypes.byref(shape.c()), _ptr(h, "h", dt, 3), h_ld, _ptr(gamma, "gamma", dt),
+                                _ptr(w_k, "w_k", dt), _ptr(w_v, "w_v", dt), _ptr(pos0, "pos0", torch.int32), B, T,
+                                ctypes.byref(view) if view is not None else None, _stream()))
+
+
+def kvd_project_qkv(shape: Shape, h_new, gamma, w_q, w_k, w_v, pos, q_out, k_out=None, v_out=None, t_off: int = 0):
+    """q (and, if k_out/v_out are given, the token's K/V at row t_off) of h_new [B, d]."""
+    dt = shape.torch_dtype
+    view = _view(k_out, v_out, t_off, "kv_out", dt)
+    _check(lib.kvd_project_qkv(ctypes.byref(shape.c()), _ptr(h_new, "h_new", dt, 2), _ptr(gamma, "gamma", dt),
+                               _ptr(w_q, "w_q", dt), _ptr(w_k, "w_k", dt), _ptr(w_v, "w_v", dt),
+                               _ptr(pos, "pos", torch.int32), h_new.shape[0], _ptr(q_out, "q_out", dt, 3),
+                               ctypes.byref(view) if view is not None else None, _stream()))
+
+
+def _attn(fn, shape, q, k, v, T, out, ws, t_off):
+    dt = shape.torch_dtype
+    view = _view(k, v, t_off, "kv", dt)
+    _check(fn(ctypes.byref(shape.c()), _ptr(q, "q", dt, 3), ctypes.byref(view), q.shape[0], T,
+              _ptr(out, "out", dt, 3), _ptr(ws, "ws"), ws.numel() * ws.element_size(), _stream()))
+
+
+def kvd_decode_attn(shape: Shape, q, k, v, T: int, out, ws, t_off: int = 0):
+    """Decode attention of q [B, n_q, hd] over stored K/V rows t_off..t_off+T-1 into out."""
+    _attn(lib.kvd_decode_attn, shape, q, k, v, T, out, ws, t_off)
+
+
+def kvd_cached_attn(shape: Shape, q, k, v, T: int, out, ws, t_off: int = 0):
+    """The cached-K/V baseline (bf16 cache): same as kvd_decode_attn."""
+    _attn(lib.kvd_cached_attn, shape, q, k, v, T, out, ws, t_off)
+
+
+def kvd_fused_recompute_attn(shape: Shape, q, h, T_rec: int, gamma, w_k, w_v, pos0, out, ws,
+                             tail_k=None, tail_v=None, T_tail: int = 0, tail_t_off: int = 0,
+                             dbg_k=None, dbg_v=None, dbg_t_off: int = 0):
+    """Attention of q over K/V recomputed from h rows 0..T_rec-1, followed by T_tail stored tail rows."""
+    dt = shape.torch_dtype
+    tail = _view(tail_k, tail_v, tail_t_off, "tail", dt)
+    dbg = _view(dbg_k, dbg_v, dbg_t_off, "kv_debug", dt)
+    _check(lib.kvd_fused_recompute_attn(
+        ctypes.byref(shape.c()), _ptr(q, "q", dt, 3), _ptr(h, "h", dt, 3), h.shape[1] if h is not None else 0,
+        _ptr(gamma, "gamma", dt),
+        _ptr(w_k, "w_k", dt), _ptr(w_v, "w_v", dt), _ptr(pos0, "pos0", torch.int32), q.shape[0], T_rec,
+        ctypes.byref(tail) if tail is not None else None, T_tail, _ptr(out, "out", dt, 3), _ptr(ws, "ws"),
+        ws.numel() * ws.element_size(), ctypes.byref(dbg) if dbg is not None else None, _stream()))

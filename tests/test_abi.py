@@ -1,0 +1,147 @@
+"""The C-ABI library on the CPU: it loads, exports every symbol include/kvd.h
+declares, and every validation error is returned as the documented status
+before any HIP call (no GPU is touched: every call here fails validation)."""
+import ctypes
+
+import pytest
+
+kvd = pytest.importorskip("paper_2603_19664_amd.kvd")
+lib = kvd.lib
+
+FAKE = 0x10000          # aligned, never dereferenced (validation fails first)
+MISALIGNED = 0x10008
+
+
+def shape(**kw):
+    base = dict(d_model=2560, n_q_heads=8, n_kv_heads=4, head_dim=256, rms_eps=1e-6, rope_theta=1e4,
+                dtype=kvd.KVD_BF16)
+    base.update(kw)
+    return kvd.AttnShape(**base)
+
+
+def view(t_cap=16, t_off=0, k=FAKE, v=FAKE):
+    return kvd.KvView(k, v, t_cap, t_off)
+
+
+def test_loads_and_version():
+    assert kvd.abi_version() == 1
+    assert kvd.status_str(kvd.KVD_ERR_ALIGN) == "KVD_ERR_ALIGN"
+
+
+def test_exports_every_header_symbol():
+    names = kvd.header_symbols()
+    assert {"kvd_recompute_kv", "kvd_decode_attn", "kvd_fused_recompute_attn", "kvd_cached_attn",
+            "kvd_project_qkv", "kvd_workspace_bytes"} <= set(names)
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def recompute(s, h=FAKE, h_ld=16, gamma=FAKE, wk=FAKE, wv=FAKE, pos=FAKE, B=1, T=16, out=None):
+    out = view() if out is None else out
+    return lib.kvd_recompute_kv(ctypes.byref(s) if s is not None else None, h, h_ld, gamma, wk, wv, pos, B, T,
+                                ctypes.byref(out), None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(d_model=100), kvd.KVD_ERR_SHAPE),
+    (dict(d_model=0), kvd.KVD_ERR_SHAPE),
+    (dict(head_dim=96), kvd.KVD_ERR_UNSUPPORTED),
+    (dict(n_q_heads=6, n_kv_heads=4), kvd.KVD_ERR_SHAPE),
+    (dict(n_q_heads=34, n_kv_heads=2), kvd.KVD_ERR_UNSUPPORTED),
+    (dict(n_kv_heads=0), kvd.KVD_ERR_SHAPE),
+    (dict(rms_eps=-1.0), kvd.KVD_ERR_SHAPE),
+    (dict(rms_eps=float("nan")), kvd.KVD_ERR_SHAPE),
+    (dict(rope_theta=0.0), kvd.KVD_ERR_SHAPE),
+    (dict(dtype=7), kvd.KVD_ERR_UNSUPPORTED),
+])
+def test_shape_validation(kw, status):
+    assert recompute(shape(**kw)) == status
+    assert kvd.last_error()
+
+
+def test_recompute_argument_validation():
+    s = shape()
+    assert recompute(None) == kvd.KVD_ERR_NULL
+    assert recompute(s, h=None) == kvd.KVD_ERR_NULL
+    assert recompute(s, h=MISALIGNED) == kvd.KVD_ERR_ALIGN
+    assert recompute(s, gamma=None) == kvd.KVD_ERR_NULL
+    assert recompute(s, wv=MISALIGNED) == kvd.KVD_ERR_ALIGN
+    assert recompute(s, pos=None) == kvd.KVD_ERR_NULL
+    assert recompute(s, h_ld=8) == kvd.KVD_ERR_SHAPE
+    assert recompute(s, B=-1) == kvd.KVD_ERR_SHAPE
+    assert recompute(s, T=-3) == kvd.KVD_ERR_SHAPE
+    assert recompute(s, out=view(t_cap=20, t_off=5)) == kvd.KVD_ERR_SHAPE
+    assert recompute(s, out=view(k=0)) == kvd.KVD_ERR_NULL
+    # empty inputs are a no-op: OK without touching the device or the pointers
+    assert recompute(s, B=0) == kvd.KVD_OK
+    assert recompute(s, T=0, h=None) == kvd.KVD_OK
+
+
+def attn(fn, s, q=FAKE, kv=None, B=1, T=16, out=FAKE, ws=FAKE, ws_bytes=1 << 30):
+    kv = view() if kv is None else kv
+    return fn(ctypes.byref(s), q, ctypes.byref(kv), B, T, out, ws, ws_bytes, None)
+
+
+def test_attention_validation():
+    s = shape()
+    for fn in (lib.kvd_decode_attn, lib.kvd_cached_attn):
+        assert attn(fn, s, T=0) == kvd.KVD_ERR_SHAPE
+        assert attn(fn, s, q=None) == kvd.KVD_ERR_NULL
+        assert attn(fn, s, out=MISALIGNED) == kvd.KVD_ERR_ALIGN
+        assert attn(fn, s, kv=view(t_cap=15)) == kvd.KVD_ERR_SHAPE
+        assert attn(fn, s, ws=None) == kvd.KVD_ERR_WORKSPACE
+        assert attn(fn, s, ws_bytes=16) == kvd.KVD_ERR_WORKSPACE
+        assert attn(fn, s, ws=FAKE + 16) == kvd.KVD_ERR_ALIGN
+    assert attn(lib.kvd_cached_attn, shape(dtype=kvd.KVD_F32)) == kvd.KVD_ERR_UNSUPPORTED
+
+
+def fused(s, q=FAKE, h=FAKE, h_ld=64, T_rec=64, tail=None, T_tail=1, ws_bytes=1 << 30, dbg=None, B=1):
+    tail = view() if tail is None else tail
+    return lib.kvd_fused_recompute_attn(ctypes.byref(s), q, h, h_ld, FAKE, FAKE, FAKE, FAKE, B, T_rec,
+                                        ctypes.byref(tail), T_tail, FAKE, FAKE, ws_bytes,
+                                        ctypes.byref(dbg) if dbg is not None else None, None)
+
+
+def test_fused_validation():
+    s = shape()
+    assert fused(s, T_rec=0, T_tail=0) == kvd.KVD_ERR_SHAPE
+    assert fused(s, T_rec=-1) == kvd.KVD_ERR_SHAPE
+    assert fused(s, h_ld=32) == kvd.KVD_ERR_SHAPE
+    assert fused(s, h=None) == kvd.KVD_ERR_NULL
+    assert fused(s, tail=view(t_cap=4, t_off=4)) == kvd.KVD_ERR_SHAPE
+    assert fused(s, ws_bytes=100) == kvd.KVD_ERR_WORKSPACE
+    assert fused(s, dbg=view(t_cap=10)) == kvd.KVD_ERR_SHAPE
+    assert fused(s, B=70000) == kvd.KVD_ERR_SHAPE
+    assert lib.kvd_fused_recompute_attn(ctypes.byref(s), FAKE, FAKE, 64, FAKE, FAKE, FAKE, FAKE, 1, 64, None, 1,
+                                        FAKE, FAKE, 1 << 30, None, None) == kvd.KVD_ERR_NULL
+
+
+def test_project_validation():
+    s = shape()
+    f = lib.kvd_project_qkv
+    assert f(ctypes.byref(s), FAKE, FAKE, FAKE, FAKE, FAKE, None, 1, FAKE, None, None) == kvd.KVD_ERR_NULL
+    assert f(ctypes.byref(s), FAKE, FAKE, None, FAKE, FAKE, FAKE, 1, FAKE, None, None) == kvd.KVD_ERR_NULL
+    bad = view(t_cap=3, t_off=3)
+    assert f(ctypes.byref(s), FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 1, FAKE, ctypes.byref(bad), None) == kvd.KVD_ERR_SHAPE
+
+
+def test_split_policy_and_workspace():
+    s = shape()
+    # one 64-key split per tile; the fused kernel adds the tail's tiles
+    assert lib.kvd_num_splits(ctypes.byref(s), kvd.KVD_OP_DECODE_ATTN, 1, 4097, 0) == 65
+    assert lib.kvd_num_splits(ctypes.byref(s), kvd.KVD_OP_FUSED, 1, 4096, 1) == 65
+    assert lib.kvd_num_splits(ctypes.byref(s), kvd.KVD_OP_FUSED, 1, 0, 1) == 1
+    assert lib.kvd_num_splits(ctypes.byref(s), kvd.KVD_OP_DECODE_ATTN, 1, 0, 0) == 0
+    n = lib.kvd_workspace_bytes(ctypes.byref(s), kvd.KVD_OP_DECODE_ATTN, 2, 100, 0)
+    S = 2
+    acc = -(-2 * 8 * S * 256 * 4 // 256) * 256
+    ml = -(-2 * 8 * S * 2 * 4 // 256) * 256
+    assert n == acc + ml
+    assert lib.kvd_workspace_bytes(ctypes.byref(s), 9, 1, 10, 0) == 0
+
+
+def test_lds_limit_is_validated():
+    # fp32, head_dim 256 and 16 query heads per KV head exceed one workgroup's LDS
+    s = shape(dtype=kvd.KVD_F32, n_q_heads=64, n_kv_heads=4, d_model=512)
+    assert fused(s) == kvd.KVD_ERR_UNSUPPORTED
+    assert attn(lib.kvd_decode_attn, s) == kvd.KVD_ERR_UNSUPPORTED
