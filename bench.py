@@ -1,0 +1,371 @@
+#!/usr/bin/env python3
+"""Decode-step benchmark of the KV-Direct hot path on one MI355X.
+
+A step is one decode token of a Gemma-3-4B-shaped model (d=2560, 8 query / 4 KV
+heads, head_dim 256, 34 layers, bf16), batch 1, 4096 checkpointed context
+tokens per layer, with synthetic seeded residuals and random-init weights.
+Per layer the step runs the whole hot path through libkvd's C ABI:
+
+  kvd_project_qkv           q and the current token's K_t/V_t (RMSNorm, W_q/W_k/W_v, RoPE)
+  kvd_fused_recompute_attn  K/V of the 4096 context tokens recomputed from the residual
+                            checkpoints (RMSNorm, W_k/W_v GEMM, RoPE) into LDS, split-K
+                            attention over [context || current token]  (partials)
+  kvd_combine               merge of the split-K partials
+
+Printed: ONE JSON line (tokens/s of the step, ms per step, the roofline of the
+fused kernel from HIP events over the timed region, the per-op us/layer, the
+cached-K/V and unfused baselines, the recompute-vs-cached-read crossover over
+batch size, and the CPU oracle baseline).
+"""
+from __future__ import annotations
+
+import argparse
+import ctypes
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+MI355X_BF16_PEAK_TFLOPS = 2500.0   # dense bf16 MFMA
+MI355X_HBM_PEAK_GBS = 8000.0
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "fused_kernel_traffic.json")
+KERNEL_SOURCES = ["kvd_device.hpp", "kvd_kernels.hip", "kvd_layout.h"]
+
+
+def parse():
+    p = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=20)
+    p.add_argument("--warmup", type=int, default=5)
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--no-crossover", action="store_true")
+    p.add_argument("--no-baselines", action="store_true", help="skip the cached / unfused per-op timings")
+    p.add_argument("--cpu-seconds", type=float, default=12.0, help="CPU oracle time budget")
+    p.add_argument("--sweep-batches", default="1,2,4,8,16,32,64")
+    return p.parse_args()
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def source_hash():
+    h = hashlib.sha256()
+    for s in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, "paper_2603_19664_amd", "csrc", s), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+class Call:
+    """A libkvd entry point with its ctypes arguments built once (keeps host overhead per launch small)."""
+
+    def __init__(self, fn, *args):
+        self.fn, self.args = fn, args
+
+    def __call__(self):
+        st = self.fn(*self.args)
+        if st != 0:
+            from paper_2603_19664_amd import kvd
+            raise kvd.KvdError(st, kvd.last_error())
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only: this build has no multi-GPU path (asked for --gpus {args.gpus}). "
+              "The KV-Direct hot path shards over sequences, KV heads or keys with one exchange of split-K "
+              "partials per layer; that exchange is not built.", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2603_19664_amd import accounting as acc
+    from paper_2603_19664_amd import configs, inputs
+    from paper_2603_19664_amd import kvd
+
+    torch.cuda.set_device(0)
+    dev = "cuda"
+    wl = configs.GEMMA3_4B
+    s = kvd.shape_of(wl)
+    sc = s.c()
+    L, B, T = wl.layers, wl.batch, wl.ctx
+    d, nq, nkv, hd = wl.d_model, wl.n_q, wl.n_kv, wl.head_dim
+    lib = kvd.lib
+    stream = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    P = lambda t: ctypes.c_void_p(t.data_ptr())  # noqa: E731
+
+    log(f"[bench] workload {wl.name}: generating {L} layers of weights and residual checkpoints")
+    layers = []
+    for l in range(L):
+        gamma, w_q, w_k, w_v = inputs.weights(wl, l, 0, dev)
+        h, h_new = inputs.residuals(wl, l, B, T, 0, dev)
+        layers.append(dict(gamma=gamma, w_q=w_q, w_k=w_k, w_v=w_v, h=h, h_new=h_new))
+    pos0 = torch.zeros((B,), dtype=torch.int32, device=dev)
+    pos_new = torch.full((B,), T, dtype=torch.int32, device=dev)
+    q = torch.empty((B, nq, hd), dtype=torch.bfloat16, device=dev)
+    out = torch.empty_like(q)
+    tk = torch.zeros((B, nkv, 1, hd), dtype=torch.bfloat16, device=dev)
+    tv = torch.zeros_like(tk)
+    tail = kvd.KvView(tk.data_ptr(), tv.data_ptr(), 1, 0)
+    S_f = kvd.kvd_num_splits(s, kvd.KVD_OP_FUSED, B, T, 1)
+    ws_f = kvd.workspace(s, kvd.KVD_OP_FUSED, B, T, 1)
+    wsb_f = ws_f.numel()
+
+    proj, fused, comb = [], [], []
+    for ly in layers:
+        proj.append(Call(lib.kvd_project_qkv, ctypes.byref(sc), P(ly["h_new"]), P(ly["gamma"]), P(ly["w_q"]),
+                         P(ly["w_k"]), P(ly["w_v"]), P(pos_new), B, P(q), ctypes.byref(tail), stream))
+        fused.append(Call(lib.kvd_fused_recompute_attn, ctypes.byref(sc), P(q), P(ly["h"]), T, P(ly["gamma"]),
+                          P(ly["w_k"]), P(ly["w_v"]), P(pos0), B, T, ctypes.byref(tail), 1, None, P(ws_f), wsb_f,
+                          None, stream))
+        comb.append(Call(lib.kvd_combine, ctypes.byref(sc), B, S_f, P(ws_f), wsb_f, P(out), stream))
+
+    def step(events=None, i=0):
+        for l in range(L):
+            proj[l]()
+            if events is not None:
+                events[i][l][0].record()
+            fused[l]()
+            if events is not None:
+                events[i][l][1].record()
+            comb[l]()
+
+    # ---------------------------------------------------------------- timed region
+    K, W = args.steps, args.warmup
+    log(f"[bench] warmup {W} steps")
+    for _ in range(W):
+        step()
+    torch.cuda.synchronize()
+    ev = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(L)]
+          for _ in range(K)]
+    t_start, t_end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    log(f"[bench] timing {K} steps")
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    t_start.record()
+    for i in range(K):
+        step(ev, i)
+    t_end.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_step = t_start.elapsed_time(t_end) / K
+    fused_ms = float(np.mean([a.elapsed_time(b) for row in ev for (a, b) in row]))
+    log(f"[bench] {ms_step:.3f} ms/step (wall {1e3 * wall / K:.3f}), fused kernel {1e3 * fused_ms:.1f} us/launch")
+
+    flops = acc.fused_flops(B, T, 1, nq, nkv, d, hd)
+    achieved = flops / (fused_ms * 1e-3) / 1e12
+    traffic = None
+    if os.path.exists(TRAFFIC_FILE):
+        with open(TRAFFIC_FILE) as f:
+            tr = json.load(f)
+        if tr.get("source_hash") == source_hash() and tr.get("workload") == wl.name:
+            traffic = tr.get("bytes_per_launch")
+
+    # ---------------------------------------------------------------- per-op us/layer and baselines
+    def op_time(fn, iters=None, warm=2, flush=None):
+        """Average device time of fn() over iters calls, HIP events around each call."""
+        iters = iters or max(3, K)
+        for _ in range(warm):
+            fn()
+        times = []
+        for _ in range(iters):
+            if flush is not None:
+                flush()
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            fn()
+            b.record()
+            times.append((a, b))
+        torch.cuda.synchronize()
+        return float(np.mean([a.elapsed_time(b) for a, b in times])) * 1e3  # us
+
+    per_op = {}
+    baselines = {}
+    if not args.no_baselines:
+        log("[bench] per-op timings (cycling the 34 layers)")
+        cyc = lambda calls: (lambda c=[0]: (calls[c[0] % L](), c.__setitem__(0, c[0] + 1)))  # noqa: E731
+        per_op["project_qkv_us"] = op_time(cyc(proj), iters=2 * L)
+        per_op["fused_recompute_attn_us"] = op_time(cyc(fused), iters=2 * L)
+        per_op["combine_us"] = op_time(cyc(comb), iters=2 * L)
+
+        # cached-K/V baseline: a persistent bf16 cache per layer, prefilled once by the library
+        log("[bench] cached-K/V baseline: prefilling 34 layers of bf16 K/V")
+        S_c = kvd.kvd_num_splits(s, kvd.KVD_OP_CACHED_ATTN, B, T + 1)
+        ws_c = kvd.workspace(s, kvd.KVD_OP_CACHED_ATTN, B, T + 1)
+        cached, cproj, ccomb = [], [], []
+        caches = []
+        for ly in layers:
+            Kc = torch.empty((B, nkv, T + 1, hd), dtype=torch.bfloat16, device=dev)
+            Vc = torch.empty_like(Kc)
+            kvd.kvd_recompute_kv(s, ly["h"], ly["gamma"], ly["w_k"], ly["w_v"], pos0, T, Kc, Vc, 0)
+            caches.append((Kc, Vc))
+            vrow = kvd.KvView(Kc.data_ptr(), Vc.data_ptr(), T + 1, T)
+            vall = kvd.KvView(Kc.data_ptr(), Vc.data_ptr(), T + 1, 0)
+            caches.append((vrow, vall))
+            cproj.append(Call(lib.kvd_project_qkv, ctypes.byref(sc), P(ly["h_new"]), P(ly["gamma"]), P(ly["w_q"]),
+                              P(ly["w_k"]), P(ly["w_v"]), P(pos_new), B, P(q), ctypes.byref(vrow), stream))
+            cached.append(Call(lib.kvd_cached_attn, ctypes.byref(sc), P(q), ctypes.byref(vall), B, T + 1, None,
+                               P(ws_c), ws_c.numel(), stream))
+            ccomb.append(Call(lib.kvd_combine, ctypes.byref(sc), B, S_c, P(ws_c), ws_c.numel(), P(out), stream))
+        per_op["cached_attn_us"] = op_time(cyc(cached), iters=2 * L)
+        per_op["cached_combine_us"] = op_time(cyc(ccomb), iters=2 * L)
+
+        def cached_step():
+            for l in range(L):
+                cproj[l]()
+                cached[l]()
+                ccomb[l]()
+        cached_ms = op_time(cached_step, iters=max(3, K // 2)) / 1e3
+        baselines["cached_kv_ms_per_step"] = cached_ms
+        baselines["cached_kv_tok_s"] = B / (cached_ms * 1e-3)
+        cbytes = acc.cached_bytes(B, T + 1, nq, nkv, hd, 2, S_c)
+        baselines["cached_attn_hbm_gbs"] = cbytes / (per_op["cached_attn_us"] * 1e-6) / 1e9
+        baselines["cached_attn_hbm_frac"] = baselines["cached_attn_hbm_gbs"] / MI355X_HBM_PEAK_GBS
+
+        # unfused recompute: recompute_kv writes K/V to HBM, decode_attn reads them back
+        log("[bench] unfused recompute baseline")
+        Ku = torch.empty((B, nkv, T + 1, hd), dtype=torch.bfloat16, device=dev)
+        Vu = torch.empty_like(Ku)
+        urow = kvd.KvView(Ku.data_ptr(), Vu.data_ptr(), T + 1, T)
+        uall = kvd.KvView(Ku.data_ptr(), Vu.data_ptr(), T + 1, 0)
+        uproj, urec, udec = [], [], []
+        for ly in layers:
+            uproj.append(Call(lib.kvd_project_qkv, ctypes.byref(sc), P(ly["h_new"]), P(ly["gamma"]), P(ly["w_q"]),
+                              P(ly["w_k"]), P(ly["w_v"]), P(pos_new), B, P(q), ctypes.byref(urow), stream))
+            urec.append(Call(lib.kvd_recompute_kv, ctypes.byref(sc), P(ly["h"]), T, P(ly["gamma"]), P(ly["w_k"]),
+                             P(ly["w_v"]), P(pos0), B, T, ctypes.byref(uall), stream))
+            udec.append(Call(lib.kvd_decode_attn, ctypes.byref(sc), P(q), ctypes.byref(uall), B, T + 1, P(out),
+                             P(ws_c), ws_c.numel(), stream))
+        per_op["recompute_kv_us"] = op_time(cyc(urec), iters=2 * L)
+        per_op["decode_attn_with_combine_us"] = op_time(cyc(udec), iters=2 * L)
+
+        def unfused_step():
+            for l in range(L):
+                uproj[l]()
+                urec[l]()
+                udec[l]()
+        unf_ms = op_time(unfused_step, iters=max(3, K // 2)) / 1e3
+        baselines["unfused_ms_per_step"] = unf_ms
+        baselines["unfused_tok_s"] = B / (unf_ms * 1e-3)
+        rflops = acc.recompute_flops(B * T, nkv, d, hd)
+        per_op["recompute_kv_tflops"] = rflops / (per_op["recompute_kv_us"] * 1e-6) / 1e12
+        del caches
+
+    # ---------------------------------------------------------------- crossover over batch size
+    crossover = None
+    if not args.no_crossover:
+        crossover = run_crossover(args, torch, np, kvd, acc, configs, inputs, op_time, log)
+
+    # ---------------------------------------------------------------- CPU oracle baseline
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = run_cpu_baseline(args, np, wl, layers, T, B, inputs, log)
+
+    res = {
+        "metric": "decode tok/s + µs/layer: recompute-K/V attn vs cached-KV read; MFMA% / HBM%",
+        "value": B / (ms_step * 1e-3),
+        "unit": "tok/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": W,
+        "ms_per_step": ms_step,
+        "us_per_layer": 1e3 * ms_step / L,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded N(0,1) residuals scaled per layer by U(0.5,4); random-init N(0,0.02) weights)",
+        "config": {"workload": wl.name, "layers": L, "batch": B, "ctx": T, "keys_per_query": T + 1,
+                   "d_model": d, "n_q_heads": nq, "n_kv_heads": nkv, "head_dim": hd,
+                   "step": "per layer: kvd_project_qkv + kvd_fused_recompute_attn (partials) + kvd_combine"},
+        "roofline": {"bound": "mfma", "kernel": "fused_kernel<bf16,256,64>", "achieved": achieved,
+                     "peak": MI355X_BF16_PEAK_TFLOPS, "unit": "TFLOP/s", "frac": achieved / MI355X_BF16_PEAK_TFLOPS,
+                     "traffic": traffic, "flops_per_launch": flops, "us_per_launch": 1e3 * fused_ms},
+        "per_op_us": per_op,
+        "baselines": baselines,
+        "crossover": crossover,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(res), flush=True)
+
+
+def run_crossover(args, torch, np, kvd, acc, configs, inputs, op_time, log):
+    """Fused recompute-attention vs cached-K/V attention (each with its combine) for one
+    Gemma-3-4B-shaped layer, context 2048 + current token, over batch size.  Each
+    measurement runs after a 512 MiB write that evicts L2 and the Infinity Cache, so
+    both sides read their inputs from HBM."""
+    wl = configs.GEMMA3_SWEEP
+    s = kvd.shape_of(wl)
+    T = wl.ctx
+    flush_buf = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
+    flush = lambda: flush_buf.fill_(1)  # noqa: E731
+    rows = []
+    for B in [int(x) for x in args.sweep_batches.split(",")]:
+        log(f"[bench] crossover B={B}")
+        gamma, w_q, w_k, w_v = inputs.weights(wl, 0, 0, "cuda")
+        h, h_new = inputs.residuals(wl, 0, B, T, 0, "cuda")
+        pos0 = torch.zeros((B,), dtype=torch.int32, device="cuda")
+        pos_new = torch.full((B,), T, dtype=torch.int32, device="cuda")
+        q = torch.empty((B, wl.n_q, wl.head_dim), dtype=torch.bfloat16, device="cuda")
+        out = torch.empty_like(q)
+        Kc = torch.empty((B, wl.n_kv, T + 1, wl.head_dim), dtype=torch.bfloat16, device="cuda")
+        Vc = torch.empty_like(Kc)
+        kvd.kvd_recompute_kv(s, h, gamma, w_k, w_v, pos0, T, Kc, Vc, 0)
+        kvd.kvd_project_qkv(s, h_new, gamma, w_q, w_k, w_v, pos_new, q, Kc, Vc, T)
+        tk, tv = Kc[:, :, T:T + 1].contiguous(), Vc[:, :, T:T + 1].contiguous()
+        ws_f = kvd.workspace(s, kvd.KVD_OP_FUSED, B, T, 1)
+        ws_c = kvd.workspace(s, kvd.KVD_OP_CACHED_ATTN, B, T + 1)
+        fz = lambda: kvd.kvd_fused_recompute_attn(s, q, h, T, gamma, w_k, w_v, pos0, out, ws_f, tk, tv, 1)  # noqa
+        cz = lambda: kvd.kvd_cached_attn(s, q, Kc, Vc, T + 1, out, ws_c)  # noqa: E731
+        it = 10
+        f_us = op_time(fz, iters=it, flush=flush)
+        c_us = op_time(cz, iters=it, flush=flush)
+        fl = acc.fused_flops(B, T, 1, wl.n_q, wl.n_kv, wl.d_model, wl.head_dim)
+        cb = acc.cached_bytes(B, T + 1, wl.n_q, wl.n_kv, wl.head_dim, 2, kvd.kvd_num_splits(
+            s, kvd.KVD_OP_CACHED_ATTN, B, T + 1))
+        rows.append({"B": B, "fused_us": f_us, "cached_us": c_us, "ratio_fused_over_cached": f_us / c_us,
+                     "fused_tflops": fl / (f_us * 1e-6) / 1e12, "cached_gbs": cb / (c_us * 1e-6) / 1e9})
+        del h, Kc, Vc
+        torch.cuda.empty_cache()
+    faster = [r["B"] for r in rows if r["ratio_fused_over_cached"] < 1.0]
+    return {"workload": wl.name, "ctx": T, "rows": rows, "batches_where_recompute_wins": faster,
+            "note": "each op timed with HIP events after a 512 MiB cache-evicting write; both include their combine"}
+
+
+def run_cpu_baseline(args, np, wl, layers, T, B, inputs, log):
+    """The fp64 oracle on the host cores: whole layers of the same decode step, until
+    the time budget is spent, scaled to tokens/s of the full 34-layer step."""
+    import threadpoolctl
+
+    import oracle as O
+
+    f = inputs.to_f64
+    done, spent = 0, 0.0
+    pos = np.arange(T)[None, :]
+    for ly in layers:
+        hx, hn = f(ly["h"]), f(ly["h_new"])
+        g, wq, wk, wv = f(ly["gamma"]), f(ly["w_q"]), f(ly["w_k"]), f(ly["w_v"])
+        t0 = time.perf_counter()
+        qo, kt, vt = O.project_qkv(hn, g, wq, wk, wv, np.array([T]), wl.n_q, wl.n_kv, wl.head_dim, wl.rms_eps,
+                                   wl.rope_theta)
+        O.kv_direct_decode(qo, hx, g, wk, wv, pos, kt[:, :, None], vt[:, :, None], wl.n_kv, wl.head_dim,
+                           wl.rms_eps, wl.rope_theta)
+        spent += time.perf_counter() - t0
+        done += 1
+        if spent >= args.cpu_seconds:
+            break
+    cores = max([i.get("num_threads", 1) for i in threadpoolctl.threadpool_info()] + [1])
+    log(f"[bench] cpu oracle: {done} layers in {spent:.1f} s on {cores} threads")
+    return {"value": B * (done / wl.layers) / spent, "unit": "tok/s", "cores": cores, "kind": "oracle",
+            "sample": f"{done} of {wl.layers} layers of one decode step (B={B}, {T} context tokens + current "
+                      f"token), fp64 numpy oracle, scaled to the full step; {spent:.1f} s"}
+
+
+if __name__ == "__main__":
+    main()

@@ -132,7 +132,8 @@ kvd_status kvd_project_qkv(const kvd_attn_shape* shape, const void* h_new, const
  * Split-K: partial softmax states go to the workspace and a second kernel
  * merges them.  ws (256-byte aligned) must hold kvd_workspace_bytes(shape,
  * KVD_OP_DECODE_ATTN, B, T, 0) bytes; its contents on entry are ignored, and
- * calls sharing one workspace must be ordered on one stream.
+ * calls sharing one workspace must be ordered on one stream.  With out == NULL
+ * only the partials are written (see kvd_combine).
  *   q [B][n_q_heads][head_dim].   out [B][n_q_heads][head_dim].               */
 kvd_status kvd_decode_attn(const kvd_attn_shape* shape, const void* q, const kvd_kv_view* kv,
                            int32_t B, int32_t T, void* out, void* ws, size_t ws_bytes,
@@ -158,6 +159,7 @@ kvd_status kvd_cached_attn(const kvd_attn_shape* shape, const void* q, const kvd
  *   ws: kvd_workspace_bytes(shape, KVD_OP_FUSED, B, T_rec, T_tail) bytes.
  *   kv_debug: NULL in production.  If not NULL, the recomputed K/V are also
  *   written to it at rows kv_debug->t_off .. +T_rec-1 (for bit-identity checks).
+ * out == NULL writes only the split-K partials (see kvd_combine).
  * Supports both dtypes.                                                       */
 kvd_status kvd_fused_recompute_attn(const kvd_attn_shape* shape, const void* q, const void* h,
                                     int32_t h_ld, const void* gamma, const void* w_k,
@@ -165,6 +167,15 @@ kvd_status kvd_fused_recompute_attn(const kvd_attn_shape* shape, const void* q, 
                                     int32_t T_rec, const kvd_kv_view* tail, int32_t T_tail,
                                     void* out, void* ws, size_t ws_bytes,
                                     const kvd_kv_view* kv_debug, void* stream);
+
+/* Merge step of split-K attention: out[b][h] = sum_s w_s acc_s / sum_s w_s l_s
+ * with w_s = 2^(m_s - max_s m_s), over the S partial softmax states that a
+ * preceding kvd_decode_attn / kvd_cached_attn / kvd_fused_recompute_attn call
+ * (with out == NULL) left in ws, in split order (deterministic).  S is that
+ * call's kvd_num_splits.  Lets a caller time or schedule the two kernels
+ * separately; the attention calls with out != NULL run it themselves.        */
+kvd_status kvd_combine(const kvd_attn_shape* shape, int32_t B, int32_t S, const void* ws,
+                       size_t ws_bytes, void* out, void* stream);
 
 /* Workspace bytes an attention call needs (0 on invalid arguments).  For
  * KVD_OP_DECODE_ATTN / KVD_OP_CACHED_ATTN, T_main is T and T_tail must be 0;

@@ -132,7 +132,7 @@ kvd_status attn_common(const kvd_attn_shape* shape, const void* q, const kvd_kv_
   KVD_TRY(check_lds(shape, false));
   if (B == 0) return KVD_OK;
   KVD_TRY(check_ptr(q, "q"));
-  KVD_TRY(check_ptr(out, "out"));
+  if (out != nullptr) KVD_TRY(check_ptr(out, "out"));
   KVD_TRY(check_view(kv, T, "kv"));
   const int32_t S = splits(KVD_OP_DECODE_ATTN, T, 0);
   KVD_TRY(check_ws(shape, B, S, ws, ws_bytes));
@@ -277,7 +277,7 @@ kvd_status kvd_fused_recompute_attn(const kvd_attn_shape* shape, const void* q, 
   KVD_TRY(check_lds(shape, true));
   if (B == 0) return KVD_OK;
   KVD_TRY(check_ptr(q, "q"));
-  KVD_TRY(check_ptr(out, "out"));
+  if (out != nullptr) KVD_TRY(check_ptr(out, "out"));
   if (T_rec > 0) {
     if (h_ld < T_rec) return fail(KVD_ERR_SHAPE, "h_ld=%d is smaller than T_rec=%d", h_ld, T_rec);
     KVD_TRY(check_ptr(h, "h"));
@@ -325,6 +325,21 @@ kvd_status kvd_fused_recompute_attn(const kvd_attn_shape* shape, const void* q, 
   fill_rev(shape, a.rev);
   return device_status(kvd::launch_fused(a, shape->dtype == KVD_BF16, shape->head_dim, (hipStream_t)stream),
                        "kvd_fused_recompute_attn launch");
+}
+
+kvd_status kvd_combine(const kvd_attn_shape* shape, int32_t B, int32_t S, const void* ws, size_t ws_bytes, void* out,
+                       void* stream) {
+  KVD_TRY(check_shape(shape));
+  KVD_TRY(check_batch(B));
+  if (S < 1) return fail(KVD_ERR_SHAPE, "S=%d must be >= 1", S);
+  if (B == 0) return KVD_OK;
+  KVD_TRY(check_ptr(out, "out"));
+  KVD_TRY(check_ws(shape, B, S, const_cast<void*>(ws), ws_bytes));
+  const float* acc = static_cast<const float*>(ws);
+  const float* ml = reinterpret_cast<const float*>(static_cast<const char*>(ws) + ws_acc_bytes(shape, B, S));
+  return device_status(kvd::launch_combine(acc, ml, out, shape->n_q_heads, B, S, shape->dtype == KVD_BF16,
+                                           shape->head_dim, (hipStream_t)stream),
+                       "kvd_combine launch");
 }
 
 int32_t kvd_num_splits(const kvd_attn_shape* shape, int32_t op, int32_t B, int32_t T_main, int32_t T_tail) {

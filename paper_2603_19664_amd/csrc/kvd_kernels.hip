@@ -243,7 +243,7 @@ static hipError_t attn_t(const AttnArgs& a, hipStream_t st) {
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(k, dim3(a.S, a.n_kv, a.B), dim3(kThreads), bytes, st, a);
   e = hipGetLastError();
-  if (e != hipSuccess) return e;
+  if (e != hipSuccess || a.out == nullptr) return e;
   hipLaunchKernelGGL((combine_kernel<T, HD>), dim3(a.n_q, a.B), dim3(HD), 0, st, a.ws_acc, a.ws_ml,
                      static_cast<T*>(a.out), a.n_q, a.S);
   return hipGetLastError();
@@ -288,9 +288,14 @@ hipError_t launch_fused(const FusedArgs& a, int dtype_bf16, int hd, hipStream_t 
   e = [&]() -> hipError_t { KVD_DISPATCH(dtype_bf16, hd, FB, FF) }();
 #undef FB
 #undef FF
-  if (e != hipSuccess) return e;
-#define CB(H) combine_t<uint16_t, H>(a.ws_acc, a.ws_ml, a.out, a.n_q, a.B, a.S, st)
-#define CF(H) combine_t<float, H>(a.ws_acc, a.ws_ml, a.out, a.n_q, a.B, a.S, st)
+  if (e != hipSuccess || a.out == nullptr) return e;
+  return launch_combine(a.ws_acc, a.ws_ml, a.out, a.n_q, a.B, a.S, dtype_bf16, hd, st);
+}
+
+hipError_t launch_combine(const float* ws_acc, const float* ws_ml, void* out, int n_q, int B, int S, int dtype_bf16,
+                          int hd, hipStream_t st) {
+#define CB(H) combine_t<uint16_t, H>(ws_acc, ws_ml, out, n_q, B, S, st)
+#define CF(H) combine_t<float, H>(ws_acc, ws_ml, out, n_q, B, S, st)
   KVD_DISPATCH(dtype_bf16, hd, CB, CF)
 #undef CB
 #undef CF

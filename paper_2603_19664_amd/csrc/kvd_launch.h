@@ -54,7 +54,8 @@ struct FusedArgs {
   double rev[kMaxPairs];
 };
 
-// Split-K attention over stored K/V: S = ceil(T / kTile) chunks.
+// Split-K attention over stored K/V: S = ceil(T / kTile) chunks.  out == nullptr:
+// partials only (no combine launch); the same holds for FusedArgs::out.
 struct AttnArgs {
   const void* q;
   const void* k;
@@ -69,5 +70,7 @@ struct AttnArgs {
 hipError_t launch_proj(const ProjArgs& a, int dtype_bf16, int hd, int n_units, hipStream_t st);
 hipError_t launch_fused(const FusedArgs& a, int dtype_bf16, int hd, hipStream_t st);
 hipError_t launch_decode(const AttnArgs& a, int dtype_bf16, int hd, hipStream_t st);
+hipError_t launch_combine(const float* ws_acc, const float* ws_ml, void* out, int n_q, int B, int S, int dtype_bf16,
+                          int hd, hipStream_t st);
 
 }  // namespace kvd

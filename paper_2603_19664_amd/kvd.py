@@ -66,6 +66,8 @@ def _load() -> ctypes.CDLL:
         f = getattr(lib, name)
         f.argtypes = args
         f.restype = ctypes.c_int
+    lib.kvd_combine.argtypes = [S, I32, I32, VP, SZ, VP, VP]
+    lib.kvd_combine.restype = ctypes.c_int
     lib.kvd_workspace_bytes.argtypes = [S, I32, I32, I32, I32]
     lib.kvd_workspace_bytes.restype = SZ
     lib.kvd_num_splits.argtypes = [S, I32, I32, I32, I32]
@@ -200,8 +202,15 @@ def _attn(fn, shape, q, k, v, T, out, ws, t_off):
               _ptr(out, "out", dt, 3), _ptr(ws, "ws"), ws.numel() * ws.element_size(), _stream()))
 
 
+def kvd_combine(shape: Shape, B: int, S: int, ws, out):
+    """Merge the S split-K partials an attention call (with out=None) left in ws into out."""
+    _check(lib.kvd_combine(ctypes.byref(shape.c()), B, S, _ptr(ws, "ws"), ws.numel() * ws.element_size(),
+                           _ptr(out, "out", shape.torch_dtype, 3), _stream()))
+
+
 def kvd_decode_attn(shape: Shape, q, k, v, T: int, out, ws, t_off: int = 0):
-    """Decode attention of q [B, n_q, hd] over stored K/V rows t_off..t_off+T-1 into out."""
+    """Decode attention of q [B, n_q, hd] over stored K/V rows t_off..t_off+T-1 into out
+    (out=None: partials only, merged later by kvd_combine)."""
     _attn(lib.kvd_decode_attn, shape, q, k, v, T, out, ws, t_off)
 
 
@@ -213,7 +222,8 @@ def kvd_cached_attn(shape: Shape, q, k, v, T: int, out, ws, t_off: int = 0):
 def kvd_fused_recompute_attn(shape: Shape, q, h, T_rec: int, gamma, w_k, w_v, pos0, out, ws,
                              tail_k=None, tail_v=None, T_tail: int = 0, tail_t_off: int = 0,
                              dbg_k=None, dbg_v=None, dbg_t_off: int = 0):
-    """Attention of q over K/V recomputed from h rows 0..T_rec-1, followed by T_tail stored tail rows."""
+    """Attention of q over K/V recomputed from h rows 0..T_rec-1, followed by T_tail stored tail rows
+    (out=None: partials only, merged later by kvd_combine)."""
     dt = shape.torch_dtype
     tail = _view(tail_k, tail_v, tail_t_off, "tail", dt)
     dbg = _view(dbg_k, dbg_v, dbg_t_off, "kv_debug", dt)
@@ -221,5 +231,6 @@ def kvd_fused_recompute_attn(shape: Shape, q, h, T_rec: int, gamma, w_k, w_v, po
         ctypes.byref(shape.c()), _ptr(q, "q", dt, 3), _ptr(h, "h", dt, 3), h.shape[1] if h is not None else 0,
         _ptr(gamma, "gamma", dt),
         _ptr(w_k, "w_k", dt), _ptr(w_v, "w_v", dt), _ptr(pos0, "pos0", torch.int32), q.shape[0], T_rec,
-        ctypes.byref(tail) if tail is not None else None, T_tail, _ptr(out, "out", dt, 3), _ptr(ws, "ws"),
+        ctypes.byref(tail) if tail is not None else None, T_tail, _ptr(out, "out", dt, 3) if out is not None else None,
+        _ptr(ws, "ws"),
         ws.numel() * ws.element_size(), ctypes.byref(dbg) if dbg is not None else None, _stream()))

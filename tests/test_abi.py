@@ -145,3 +145,12 @@ def test_lds_limit_is_validated():
     s = shape(dtype=kvd.KVD_F32, n_q_heads=64, n_kv_heads=4, d_model=512)
     assert fused(s) == kvd.KVD_ERR_UNSUPPORTED
     assert attn(lib.kvd_decode_attn, s) == kvd.KVD_ERR_UNSUPPORTED
+
+
+def test_combine_validation():
+    s = shape()
+    f = lib.kvd_combine
+    assert f(ctypes.byref(s), 1, 0, FAKE, 1 << 30, FAKE, None) == kvd.KVD_ERR_SHAPE
+    assert f(ctypes.byref(s), 1, 4, FAKE, 1 << 30, None, None) == kvd.KVD_ERR_NULL
+    assert f(ctypes.byref(s), 1, 4, FAKE, 64, FAKE, None) == kvd.KVD_ERR_WORKSPACE
+    assert f(ctypes.byref(s), 1, 4, FAKE + 64, 1 << 30, FAKE, None) == kvd.KVD_ERR_ALIGN

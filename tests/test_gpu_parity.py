@@ -235,3 +235,22 @@ def test_cached_attn_matches_decode_attn():
     kvd.kvd_cached_attn(L.shape, q, K, V, L.T + 1, outc, ws)
     assert torch.equal(_bits(outc), _bits(out))
     check("cached vs oracle", outc, oracle_decode(L), 2e-2)
+
+
+def test_partials_then_combine_equals_one_call():
+    # out=None leaves the split-K partials in the workspace; kvd_combine merges them
+    # exactly as the one-call form does.
+    L = make_layer(C.GEMMA3_4B, B=2, T=333, seed=25, d_model=512)
+    q, (tk, tv), out1, _ = gpu_fused(L)
+    s = L.shape
+    ws = kvd.workspace(s, kvd.KVD_OP_FUSED, L.B, L.T, 1)
+    kvd.kvd_fused_recompute_attn(s, q, L.h, L.T, L.gamma, L.w_k, L.w_v, L.pos0, None, ws, tk, tv, 1)
+    out2 = torch.empty_like(out1)
+    kvd.kvd_combine(s, L.B, kvd.kvd_num_splits(s, kvd.KVD_OP_FUSED, L.B, L.T, 1), ws, out2)
+    assert torch.equal(_bits(out1), _bits(out2))
+    q, K, V, outd = gpu_unfused(L)
+    wsd = kvd.workspace(s, kvd.KVD_OP_DECODE_ATTN, L.B, L.T + 1)
+    kvd.kvd_decode_attn(s, q, K, V, L.T + 1, None, wsd)
+    out3 = torch.empty_like(outd)
+    kvd.kvd_combine(s, L.B, kvd.kvd_num_splits(s, kvd.KVD_OP_DECODE_ATTN, L.B, L.T + 1), wsd, out3)
+    assert torch.equal(_bits(outd), _bits(out3))
