@@ -92,7 +92,7 @@ def main():
     torch.cuda.set_device(0)
     dev = "cuda"
     wl = configs.GEMMA3_4B
-    s = kvd.shape_of(wl)
+    s = kvd.shape_of(wl).packed()   # weights in the packed MFMA layout (packed once, outside the step)
     sc = s.c()
     L, B, T = wl.layers, wl.batch, wl.ctx
     d, nq, nkv, hd = wl.d_model, wl.n_q, wl.n_kv, wl.head_dim
@@ -105,7 +105,8 @@ def main():
     for l in range(L):
         gamma, w_q, w_k, w_v = inputs.weights(wl, l, 0, dev)
         h, h_new = inputs.residuals(wl, l, B, T, 0, dev)
-        layers.append(dict(gamma=gamma, w_q=w_q, w_k=w_k, w_v=w_v, h=h, h_new=h_new))
+        layers.append(dict(gamma=gamma, w_q=kvd.kvd_pack_weights(s, w_q), w_k=kvd.kvd_pack_weights(s, w_k),
+                           w_v=kvd.kvd_pack_weights(s, w_v), h=h, h_new=h_new, rw_k=w_k, rw_v=w_v, rw_q=w_q))
     pos0 = torch.zeros((B,), dtype=torch.int32, device=dev)
     pos_new = torch.full((B,), T, dtype=torch.int32, device=dev)
     q = torch.empty((B, nq, hd), dtype=torch.bfloat16, device=dev)
@@ -301,14 +302,15 @@ def run_crossover(args, torch, np, kvd, acc, configs, inputs, op_time, log):
     measurement runs after a 512 MiB write that evicts L2 and the Infinity Cache, so
     both sides read their inputs from HBM."""
     wl = configs.GEMMA3_SWEEP
-    s = kvd.shape_of(wl)
+    s = kvd.shape_of(wl).packed()
     T = wl.ctx
     flush_buf = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
     flush = lambda: flush_buf.fill_(1)  # noqa: E731
     rows = []
     for B in [int(x) for x in args.sweep_batches.split(",")]:
         log(f"[bench] crossover B={B}")
-        gamma, w_q, w_k, w_v = inputs.weights(wl, 0, 0, "cuda")
+        gamma, w_q, w_k, w_v = (inputs.weights(wl, 0, 0, "cuda")[0],
+                                *(kvd.kvd_pack_weights(s, w) for w in inputs.weights(wl, 0, 0, "cuda")[1:]))
         h, h_new = inputs.residuals(wl, 0, B, T, 0, "cuda")
         pos0 = torch.zeros((B,), dtype=torch.int32, device="cuda")
         pos_new = torch.full((B,), T, dtype=torch.int32, device="cuda")
@@ -350,7 +352,7 @@ def run_cpu_baseline(args, np, wl, layers, T, B, inputs, log):
     pos = np.arange(T)[None, :]
     for ly in layers:
         hx, hn = f(ly["h"]), f(ly["h_new"])
-        g, wq, wk, wv = f(ly["gamma"]), f(ly["w_q"]), f(ly["w_k"]), f(ly["w_v"])
+        g, wq, wk, wv = f(ly["gamma"]), f(ly["rw_q"]), f(ly["rw_k"]), f(ly["rw_v"])
         t0 = time.perf_counter()
         qo, kt, vt = O.project_qkv(hn, g, wq, wk, wv, np.array([T]), wl.n_q, wl.n_kv, wl.head_dim, wl.rms_eps,
                                    wl.rope_theta)

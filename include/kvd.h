@@ -32,7 +32,10 @@
  *             K/V store         [B][n_kv_heads][t_cap][head_dim]   (kvd_kv_view)
  *           Weights are stored [out][in], the transpose of the paper's
  *           row-vector W (h W), so head h owns rows h*head_dim ..
- *           (h+1)*head_dim-1.
+ *           (h+1)*head_dim-1.  shape->w_layout selects how each weight matrix
+ *           is laid out in memory: KVD_W_ROWMAJOR (as above) or KVD_W_PACKED
+ *           (the MFMA operand order written by kvd_pack_weights; bf16 only).
+ *           Both layouts hold the same values and give bit-identical results.
  * Norm.     hbar = h / sqrt(mean(h^2) + rms_eps) * gamma.
  * RoPE.     Consecutive pairs (2i, 2i+1), 0-based, are rotated by
  *           +p * rope_theta^(-2i/head_dim), p the token's absolute position.
@@ -55,7 +58,7 @@
 extern "C" {
 #endif
 
-#define KVD_ABI_VERSION 1
+#define KVD_ABI_VERSION 2
 
 typedef enum {
   KVD_OK = 0,
@@ -69,6 +72,9 @@ typedef enum {
 
 typedef enum { KVD_F32 = 0, KVD_BF16 = 1 } kvd_dtype;
 
+/* Memory layout of W_q / W_k / W_v (see kvd_pack_weights). */
+typedef enum { KVD_W_ROWMAJOR = 0, KVD_W_PACKED = 1 } kvd_weight_layout;
+
 /* Operations whose workspace size kvd_workspace_bytes reports. */
 typedef enum { KVD_OP_DECODE_ATTN = 0, KVD_OP_CACHED_ATTN = 1, KVD_OP_FUSED = 2 } kvd_op;
 
@@ -80,7 +86,8 @@ typedef enum { KVD_OP_DECODE_ATTN = 0, KVD_OP_CACHED_ATTN = 1, KVD_OP_FUSED = 2 
  *   head_dim    64, 128 or 256.
  *   rms_eps     RMSNorm epsilon, finite and >= 0.
  *   rope_theta  RoPE base, finite and > 0.
- *   dtype       a kvd_dtype.                                                */
+ *   dtype       a kvd_dtype.
+ *   w_layout    a kvd_weight_layout; KVD_W_PACKED requires KVD_BF16.        */
 typedef struct {
   int32_t d_model;
   int32_t n_q_heads;
@@ -89,6 +96,7 @@ typedef struct {
   float rms_eps;
   double rope_theta;
   int32_t dtype;
+  int32_t w_layout;
 } kvd_attn_shape;
 
 /* A stored K/V block: k and v each [B][n_kv_heads][t_cap][head_dim] in the
@@ -167,6 +175,19 @@ kvd_status kvd_fused_recompute_attn(const kvd_attn_shape* shape, const void* q, 
                                     int32_t T_rec, const kvd_kv_view* tail, int32_t T_tail,
                                     void* out, void* ws, size_t ws_bytes,
                                     const kvd_kv_view* kv_debug, void* stream);
+
+/* Weight packing (done once per frozen weight matrix; the weights of the paper's
+ * projections are fixed at inference, Sec. 3.2): rewrites a row-major
+ * [rows][d_model] bf16 matrix into the order the MFMA kernels read it in, so
+ * that every 64-lane load of a weight operand is one contiguous 1 KiB block:
+ * block (r, c), r < rows/32, c < d_model/16, is 512 elements at offset
+ * (r * d_model/16 + c) * 512, and its element 8*l + e (lane l < 64, e < 8) is
+ * W[32 r + l % 32][16 c + 8 (l / 32) + e].  A head's rows start at the same
+ * element offset (head * head_dim * d_model) as in the row-major matrix.
+ * rows must be a positive multiple of 32; packed holds rows * d_model bf16 and
+ * must not alias w.  shape->dtype must be KVD_BF16 (w_layout is ignored).    */
+kvd_status kvd_pack_weights(const kvd_attn_shape* shape, const void* w, int32_t rows, void* packed,
+                            void* stream);
 
 /* Merge step of split-K attention: out[b][h] = sum_s w_s acc_s / sum_s w_s l_s
  * with w_s = 2^(m_s - max_s m_s), over the S partial softmax states that a

@@ -47,6 +47,10 @@ kvd_status check_shape(const kvd_attn_shape* s) {
   if (s->n_q_heads / s->n_kv_heads > kvd::kMaxGroup)
     return fail(KVD_ERR_UNSUPPORTED, "group size %d exceeds %d", s->n_q_heads / s->n_kv_heads, kvd::kMaxGroup);
   if (!std::isfinite(s->rms_eps) || s->rms_eps < 0.0f) return fail(KVD_ERR_SHAPE, "rms_eps must be finite and >= 0");
+  if (s->w_layout != KVD_W_ROWMAJOR && s->w_layout != KVD_W_PACKED)
+    return fail(KVD_ERR_UNSUPPORTED, "w_layout %d is not KVD_W_ROWMAJOR or KVD_W_PACKED", s->w_layout);
+  if (s->w_layout == KVD_W_PACKED && s->dtype != KVD_BF16)
+    return fail(KVD_ERR_UNSUPPORTED, "packed weights are bf16 only");
   if (!std::isfinite(s->rope_theta) || s->rope_theta <= 0.0) return fail(KVD_ERR_SHAPE, "rope_theta must be finite and > 0");
   return KVD_OK;
 }
@@ -111,11 +115,30 @@ size_t attn_lds_need(const kvd_attn_shape* s, bool fused) {
 }
 
 kvd_status check_lds(const kvd_attn_shape* s, bool fused) {
-  const size_t need = s->dtype == KVD_BF16 ? attn_lds_need<uint16_t>(s, fused) : attn_lds_need<float>(s, fused);
+  const size_t need = (s->dtype == KVD_BF16 ? attn_lds_need<uint16_t>(s, fused) : attn_lds_need<float>(s, fused)) +
+                      (fused ? kvd::gamma_lds_bytes(s->d_model) : 0);
   if (need > kLdsLimit)
     return fail(KVD_ERR_UNSUPPORTED, "head_dim=%d with group size %d needs %zu bytes of LDS (limit %zu)", s->head_dim,
                 s->n_q_heads / s->n_kv_heads, need, kLdsLimit);
   return KVD_OK;
+}
+
+kvd_status check_lds_bytes(size_t need, const char* what) {
+  if (need > kLdsLimit)
+    return fail(KVD_ERR_UNSUPPORTED, "%s needs %zu bytes of LDS for this shape (limit %zu)", what, need, kLdsLimit);
+  return KVD_OK;
+}
+
+size_t recompute_lds(const kvd_attn_shape* s) {
+  const int hd = s->head_dim;
+  const size_t base = s->dtype == KVD_BF16
+                          ? (hd == 64 ? kvd::proj_lds<uint16_t>(64, kvd::kMtBf16).end
+                                      : hd == 128 ? kvd::proj_lds<uint16_t>(128, kvd::kMtBf16).end
+                                                  : kvd::proj_lds<uint16_t>(256, kvd::kMtBf16).end)
+                          : (hd == 64 ? kvd::proj_lds<float>(64, kvd::kMtF32).end
+                                      : hd == 128 ? kvd::proj_lds<float>(128, kvd::kMtF32).end
+                                                  : kvd::proj_lds<float>(256, kvd::kMtF32).end);
+  return base + kvd::gamma_lds_bytes(s->d_model);
 }
 
 kvd_status device_status(hipError_t e, const char* what) {
@@ -183,6 +206,7 @@ kvd_status kvd_recompute_kv(const kvd_attn_shape* shape, const void* h, int32_t 
   if (T < 0) return fail(KVD_ERR_SHAPE, "T=%d must be >= 0", T);
   if (B == 0 || T == 0) return KVD_OK;
   if (h_ld < T) return fail(KVD_ERR_SHAPE, "h_ld=%d is smaller than T=%d", h_ld, T);
+  KVD_TRY(check_lds_bytes(recompute_lds(shape), "kvd_recompute_kv"));
   KVD_TRY(check_ptr(h, "h"));
   KVD_TRY(check_ptr(gamma, "gamma"));
   KVD_TRY(check_ptr(w_k, "w_k"));
@@ -208,7 +232,8 @@ kvd_status kvd_recompute_kv(const kvd_attn_shape* shape, const void* h, int32_t 
   a.n_kv_units = shape->n_kv_heads;
   a.eps = shape->rms_eps;
   fill_rev(shape, a.rev);
-  return device_status(kvd::launch_proj(a, shape->dtype == KVD_BF16, shape->head_dim, a.n_kv_units, (hipStream_t)stream),
+  return device_status(kvd::launch_proj(a, shape->dtype == KVD_BF16, shape->head_dim, shape->w_layout == KVD_W_PACKED,
+                                        a.n_kv_units, (hipStream_t)stream),
                        "kvd_recompute_kv launch");
 }
 
@@ -217,6 +242,8 @@ kvd_status kvd_project_qkv(const kvd_attn_shape* shape, const void* h_new, const
                            const kvd_kv_view* kv_out, void* stream) {
   KVD_TRY(check_shape(shape));
   KVD_TRY(check_batch(B));
+  KVD_TRY(check_lds_bytes(shape->dtype == KVD_BF16 ? kvd::stream_lds(shape->d_model).end : recompute_lds(shape),
+                          "kvd_project_qkv"));
   if (B == 0) return KVD_OK;
   KVD_TRY(check_ptr(h_new, "h_new"));
   KVD_TRY(check_ptr(gamma, "gamma"));
@@ -252,8 +279,10 @@ kvd_status kvd_project_qkv(const kvd_attn_shape* shape, const void* h_new, const
   a.eps = shape->rms_eps;
   fill_rev(shape, a.rev);
   const int units = a.n_kv_units + (shape->n_q_heads + 1) / 2;
-  return device_status(kvd::launch_proj(a, shape->dtype == KVD_BF16, shape->head_dim, units, (hipStream_t)stream),
-                       "kvd_project_qkv launch");
+  return device_status(
+      kvd::launch_project_current(a, shape->dtype == KVD_BF16, shape->head_dim, shape->w_layout == KVD_W_PACKED, units,
+                                  (hipStream_t)stream),
+      "kvd_project_qkv launch");
 }
 
 kvd_status kvd_decode_attn(const kvd_attn_shape* shape, const void* q, const kvd_kv_view* kv, int32_t B, int32_t T,
@@ -323,8 +352,25 @@ kvd_status kvd_fused_recompute_attn(const kvd_attn_shape* shape, const void* q, 
   a.S = S;
   a.eps = shape->rms_eps;
   fill_rev(shape, a.rev);
-  return device_status(kvd::launch_fused(a, shape->dtype == KVD_BF16, shape->head_dim, (hipStream_t)stream),
+  return device_status(kvd::launch_fused(a, shape->dtype == KVD_BF16, shape->head_dim,
+                                         shape->w_layout == KVD_W_PACKED, (hipStream_t)stream),
                        "kvd_fused_recompute_attn launch");
+}
+
+kvd_status kvd_pack_weights(const kvd_attn_shape* shape, const void* w, int32_t rows, void* packed, void* stream) {
+  if (shape == nullptr) return fail(KVD_ERR_NULL, "shape is NULL");
+  kvd_attn_shape s = *shape;
+  s.w_layout = KVD_W_ROWMAJOR;
+  KVD_TRY(check_shape(&s));
+  if (s.dtype != KVD_BF16) return fail(KVD_ERR_UNSUPPORTED, "kvd_pack_weights packs bf16 weights");
+  if (rows < 32 || rows % 32 != 0) return fail(KVD_ERR_SHAPE, "rows=%d must be a positive multiple of 32", rows);
+  KVD_TRY(check_ptr(w, "w"));
+  KVD_TRY(check_ptr(packed, "packed"));
+  const size_t bytes = (size_t)rows * s.d_model * 2;
+  const char* a = static_cast<const char*>(w);
+  const char* b = static_cast<const char*>(packed);
+  if (a < b + bytes && b < a + bytes) return fail(KVD_ERR_SHAPE, "packed must not overlap w");
+  return device_status(kvd::launch_pack(w, packed, rows, s.d_model, (hipStream_t)stream), "kvd_pack_weights launch");
 }
 
 kvd_status kvd_combine(const kvd_attn_shape* shape, int32_t B, int32_t S, const void* ws, size_t ws_bytes, void* out,

@@ -118,8 +118,9 @@ __device__ __forceinline__ uint4 stage_chunk_bf16(uint4 hv, uint4 gv, float& ss)
 
 // Per-token 1/rms from the per-thread partial sums: thread (row, sub) holds the
 // sum over its chunk column sub = tid & 7; the 8 partials of a row sit in 8
-// consecutive lanes and are added by a fixed xor tree.
-template <int CPT>
+// consecutive lanes and are added by a fixed xor tree.  Rows of thread tid are
+// (tid >> 3) + (NT / 8) * r.
+template <int NT, int CPT>
 __device__ __forceinline__ void finish_rms(const float (&ss)[CPT], const bool (&valid)[CPT], int d, float eps,
                                            float* rinv) {
   const int tid = threadIdx.x;
@@ -129,62 +130,85 @@ __device__ __forceinline__ void finish_rms(const float (&ss)[CPT], const bool (&
     v += __shfl_xor(v, 1, 64);
     v += __shfl_xor(v, 2, 64);
     v += __shfl_xor(v, 4, 64);
-    if ((tid & 7) == 0) rinv[(tid >> 3) + 32 * r] = valid[r] ? 1.0f / sqrtf(v / (float)d + eps) : 0.0f;
+    if ((tid & 7) == 0) rinv[(tid >> 3) + (NT / 8) * r] = valid[r] ? 1.0f / sqrtf(v / (float)d + eps) : 0.0f;
   }
 }
 
-// One half (head_dim rows) of a projection tile: the weight block it reads, whether
-// its rows get RoPE, and its column offset in the LDS K/V tile (0 or head_dim).
+// One half (head_dim rows) of a projection tile: the weight block it reads and
+// whether its rows get RoPE.  Column offset in the LDS K/V tile: half * head_dim.
 struct Half {
   const void* w;  // first row of a [head_dim][d] block, or nullptr (rows absent -> zeros)
   int rope;
 };
 
+__device__ __forceinline__ int wave_id() { return __builtin_amdgcn_readfirstlane(threadIdx.x >> 6); }
+
+// Element offset of the MFMA A operand chunk (K-step s, 16-wide substep u) from a
+// lane's base pointer.  Row-major: base = row (row0 + lane % 32), column 8 (lane / 32);
+// packed (kvd_pack_weights): base = block row row0 + lane * 8, one 512-element
+// block per 16 columns.
+template <bool PACKED>
+__device__ __forceinline__ size_t w_off(int s, int u) {
+  return PACKED ? ((size_t)s * (kKT / 16) + u) * 512 : (size_t)s * kKT + 16 * u;
+}
+
 // ------------------------------------------------------------------ bf16 MFMA tile
 
-template <int HD, int MT>
+// 8 waves (512 threads) compute a [2*HD features] x [MT tokens] tile.  Waves are
+// arranged WF (features) x WT (tokens); each owns NB_F 32-row blocks and NB_T
+// 32-token blocks.  head_dim 256: every wave owns 32 K rows and the same 32 V
+// rows (RoPE work balanced); head_dim 128 / 64: waves own one 32-row block of
+// either half.  Weights stream from global memory straight into MFMA A-operand
+// registers (each weight byte is used by exactly one wave), kDepth K-steps
+// ahead; gamma-scaled residuals are staged through LDS (shared by all waves),
+// double buffered.
+template <int HD, int MT, bool PACKED>
 struct MfmaTile {
-  static constexpr int NB_F = HD >= 128 ? HD / 64 : 1;  // 32-row blocks per wave
-  static constexpr int NB_T = MT / 32;                  // 32-token blocks
-  static constexpr int CPT = MT / 32;                   // staged chunks per thread per K-step
+  static constexpr int NT = kNtTile;
+  static constexpr int NW = NT / 64;
+  static constexpr int WF = HD == 64 ? 4 : 8;
+  static constexpr int WT = NW / WF;
+  static constexpr int NB_F = (2 * HD / WF) / 32;
+  static constexpr int TOK_W = MT / WT;
+  static constexpr int NB_T = TOK_W / 32;
+  static constexpr int CPT = MT * 8 / NT;  // staged 8-element chunks per thread per K-step
   static constexpr int HLD = h_ld<uint16_t>();
   static constexpr int KLD = kv_ld<uint16_t>(HD);
+  static_assert(NB_F >= 1 && NB_T >= 1 && CPT >= 1, "tile shape");
 
-  // Rows covered by block bf of wave w: which half (K/first = 0, V/second = 1) and
-  // the first row inside that half.  head_dim >= 128: every wave owns head_dim/4
-  // rows of each half; head_dim == 64: waves 0-1 own the first half, 2-3 the second.
-  static __device__ __forceinline__ void block_rows(int wave, int bf, int& half, int& row0) {
-    if (HD == 64) {
-      half = wave >> 1;
-      row0 = 32 * (wave & 1);
+  static __device__ __forceinline__ void block_rows(int fw, int bf, int& half, int& row0) {
+    if (NB_F == 2) {
+      half = bf;
+      row0 = 32 * fw;
     } else {
-      constexpr int hb = NB_F / 2;
-      half = bf / hb;
-      row0 = (HD / 4) * wave + 32 * (bf % hb);
+      half = fw / (WF / 2);
+      row0 = 32 * (fw % (WF / 2));
     }
   }
 
-  // Computes the tile into `kv` (LDS, [MT][KLD] bf16): rows of half 0 at columns
-  // 0..HD-1, half 1 at HD..2HD-1.  hrow[r]: residual row of staged token
-  // (tid>>3)+32r, already offset by 8*(tid&7), or nullptr for a padding token.
-  // pos (LDS [MT]) and rev (LDS [HD/2]) feed RoPE; rinv is LDS scratch [MT].
-  static __device__ void run(const uint16_t* const (&hrow)[CPT], const uint16_t* gamma, int d, float eps,
-                             const Half (&halves)[2], uint16_t* hst, float* rinv, const int* pos,
+  // Computes the tile into `kv` (LDS, [MT][KLD] bf16).  hrow[r]: residual row of
+  // staged token (tid>>3)+64r, offset by 8*(tid&7) (any readable row if !valid[r]).
+  // gam: gamma in LDS ([d] bf16).
+  static __device__ void run(const uint16_t* const (&hrow)[CPT], const bool (&valid)[CPT], const uint16_t* gam,
+                             int d, float eps, const Half (&halves)[2], uint16_t* hst, float* rinv, const int* pos,
                              const double* rev, uint16_t* kv) {
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, sub = tid & 7;
+    const int tid = threadIdx.x, lane = tid & 63, sub = tid & 7;
+    const int wave = wave_id();
+    const int fw = wave % WF, tw = wave / WF;
     const int nsteps = d / kKT;
 
     const uint16_t* wrow[NB_F];
+    bool wok[NB_F];
 #pragma unroll
     for (int bf = 0; bf < NB_F; ++bf) {
       int half, row0;
-      block_rows(wave, bf, half, row0);
-      const uint16_t* w = static_cast<const uint16_t*>(halves[half].w);
-      wrow[bf] = w ? w + (size_t)(row0 + (lane & 31)) * d + 8 * (lane >> 5) : nullptr;
+      block_rows(fw, bf, half, row0);
+      const uint16_t* w = static_cast<const uint16_t*>(half ? halves[1].w : halves[0].w);
+      wok[bf] = w != nullptr;  // uniform per wave
+      const uint16_t* wb = wok[bf] ? w : static_cast<const uint16_t*>(halves[0].w);
+      wrow[bf] = PACKED ? wb + (size_t)row0 * d + 8 * lane
+                        : wb + (size_t)(row0 + (lane & 31)) * d + 8 * (lane >> 5);
     }
-    bool valid[CPT];
-#pragma unroll
-    for (int r = 0; r < CPT; ++r) valid[r] = hrow[r] != nullptr;
 
     f32x16_t acc[NB_F][NB_T];
 #pragma unroll
@@ -194,90 +218,94 @@ struct MfmaTile {
 #pragma unroll
         for (int i = 0; i < 16; ++i) acc[bf][bt][i] = 0.0f;
 
-    bf16x8_t a[2][NB_F][4];
-    uint4 hv[CPT];
-    uint4 gv;
+    // Ring of kDepth K-steps in flight: slot U holds the weights and residual
+    // chunks of step s with s % kDepth == U.  Step s is staged into LDS buffer
+    // s & 1 one iteration before it is consumed.
+    constexpr int D = kDepth;
+    bf16x8_t A[D][NB_F][4];
+    uint4 H[D][CPT];
     float ss[CPT];
 #pragma unroll
     for (int r = 0; r < CPT; ++r) ss[r] = 0.0f;
 
-    auto load_h = [&](int s) {
+    auto load_step = [&](auto slot_c, int s) {
+      constexpr int U = decltype(slot_c)::value;
 #pragma unroll
-      for (int r = 0; r < CPT; ++r)
-        hv[r] = valid[r] ? *reinterpret_cast<const uint4*>(hrow[r] + (size_t)s * kKT) : make_uint4(0, 0, 0, 0);
-      gv = *reinterpret_cast<const uint4*>(gamma + (size_t)s * kKT + 8 * sub);
-    };
-    auto store_h = [&](int buf) {
-#pragma unroll
-      for (int r = 0; r < CPT; ++r) {
-        const uint4 o = stage_chunk_bf16(hv[r], gv, ss[r]);
-        *reinterpret_cast<uint4*>(hst + ((size_t)buf * MT + (tid >> 3) + 32 * r) * HLD + 8 * sub) = o;
-      }
-    };
-    auto load_a = [&](auto buf_c, int s) {
-      constexpr int B = decltype(buf_c)::value;
+      for (int r = 0; r < CPT; ++r) H[U][r] = *reinterpret_cast<const uint4*>(hrow[r] + (size_t)s * kKT);
 #pragma unroll
       for (int bf = 0; bf < NB_F; ++bf)
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          if (wrow[bf]) {
-            a[B][bf][u] = *reinterpret_cast<const bf16x8_t*>(wrow[bf] + (size_t)s * kKT + 16 * u);
-          } else {
-#pragma unroll
-            for (int i = 0; i < 8; ++i) a[B][bf][u][i] = (__bf16)0.0f;
-          }
-        }
+        for (int u = 0; u < 4; ++u)
+          A[U][bf][u] = *reinterpret_cast<const bf16x8_t*>(wrow[bf] + w_off<PACKED>(s, u));
     };
-    auto kstep = [&](auto cur_c, int s) {
-      constexpr int C = decltype(cur_c)::value;
-      const bool more = s + 1 < nsteps;
-      if (more) {
-        load_h(s + 1);
-        load_a(IC<C ^ 1>{}, s + 1);
+    auto stage = [&](auto slot_c, int s, int buf) {
+      constexpr int U = decltype(slot_c)::value;
+      const uint4 gv = *reinterpret_cast<const uint4*>(gam + (size_t)s * kKT + 8 * sub);
+#pragma unroll
+      for (int r = 0; r < CPT; ++r) {
+        const uint4 x = valid[r] ? H[U][r] : make_uint4(0, 0, 0, 0);
+        const uint4 o = stage_chunk_bf16(x, gv, ss[r]);
+        *reinterpret_cast<uint4*>(hst + ((size_t)buf * MT + (tid >> 3) + (NT / 8) * r) * HLD + 8 * sub) = o;
       }
+    };
+    auto compute = [&](auto slot_c, auto buf_c) {
+      constexpr int U = decltype(slot_c)::value;
+      constexpr int C = decltype(buf_c)::value;
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
         bf16x8_t bv[NB_T];
 #pragma unroll
         for (int bt = 0; bt < NB_T; ++bt)
           bv[bt] = *reinterpret_cast<const bf16x8_t*>(
-              hst + ((size_t)C * MT + 32 * bt + (lane & 31)) * HLD + 16 * u + 8 * (lane >> 5));
+              hst + ((size_t)C * MT + tw * TOK_W + 32 * bt + (lane & 31)) * HLD + 16 * u + 8 * (lane >> 5));
 #pragma unroll
         for (int bf = 0; bf < NB_F; ++bf)
 #pragma unroll
           for (int bt = 0; bt < NB_T; ++bt)
-            acc[bf][bt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[C][bf][u], bv[bt], acc[bf][bt], 0, 0, 0);
+            acc[bf][bt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(A[U][bf][u], bv[bt], acc[bf][bt], 0, 0, 0);
       }
-      if (more) store_h(C ^ 1);
+    };
+    // one iteration: consume step s from slot U, refill slot U with step s + D,
+    // stage step s + 1 (slot (U + 1) % D) into the other LDS buffer.
+    auto iter = [&](auto slot_c, int s) {
+      constexpr int U = decltype(slot_c)::value;
+      compute(slot_c, IC<U & 1>{});
+      if (s + D < nsteps) load_step(slot_c, s + D);
+      if (s + 1 < nsteps) stage(IC<(U + 1) % D>{}, s + 1, (U + 1) & 1);
       __syncthreads();
     };
 
-    load_h(0);
-    load_a(IC<0>{}, 0);
-    store_h(0);
+    static_assert(D == 4, "the unrolled loop below assumes four slots");
+    load_step(IC<0>{}, 0);
+    if (1 < nsteps) load_step(IC<1>{}, 1);
+    if (2 < nsteps) load_step(IC<2>{}, 2);
+    if (3 < nsteps) load_step(IC<3>{}, 3);
+    stage(IC<0>{}, 0, 0);
     __syncthreads();
-    for (int s = 0; s < nsteps; s += 2) {
-      kstep(IC<0>{}, s);
-      if (s + 1 < nsteps) kstep(IC<1>{}, s + 1);
+    for (int s0 = 0; s0 < nsteps; s0 += D) {
+      iter(IC<0>{}, s0);
+      if (s0 + 1 < nsteps) iter(IC<1>{}, s0 + 1);
+      if (s0 + 2 < nsteps) iter(IC<2>{}, s0 + 2);
+      if (s0 + 3 < nsteps) iter(IC<3>{}, s0 + 3);
     }
 
-    finish_rms<CPT>(ss, valid, d, eps, rinv);
+    finish_rms<NT, CPT>(ss, valid, d, eps, rinv);
     __syncthreads();
 
     // epilogue: row scale, RoPE on rotated halves, one RNE rounding, LDS tile.
 #pragma unroll
     for (int bt = 0; bt < NB_T; ++bt) {
-      const int tok = 32 * bt + (lane & 31);
+      const int tok = tw * TOK_W + 32 * bt + (lane & 31);
       const float ri = rinv[tok];
       const int p = pos[tok];
 #pragma unroll
       for (int bf = 0; bf < NB_F; ++bf) {
         int half, row0;
-        block_rows(wave, bf, half, row0);
+        block_rows(fw, bf, half, row0);
         float v[16];
 #pragma unroll
-        for (int r = 0; r < 16; ++r) v[r] = acc[bf][bt][r] * ri;
-        if (halves[half].rope) {
+        for (int r = 0; r < 16; ++r) v[r] = wok[bf] ? acc[bf][bt][r] * ri : 0.0f;
+        if (half ? halves[1].rope : halves[0].rope) {
 #pragma unroll
           for (int r = 0; r < 16; r += 2) {
             const int f = row0 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
@@ -299,29 +327,29 @@ struct MfmaTile {
 
 // ------------------------------------------------------------------ fp32 VALU tile
 
+// The same contraction in fp32 on the vector ALUs: thread (pair p, token group)
+// accumulates rows 2p, 2p+1 of the 2*HD rows for TPT tokens, in d order.
 template <int HD, int MT>
 struct F32Tile {
-  static constexpr int TG = kThreads / HD;   // token groups
+  static constexpr int NT = kNtTile;
+  static constexpr int TG = NT / HD;         // token groups
   static constexpr int TPT = MT / TG;        // tokens per thread
-  static constexpr int CPT = MT / 32;
+  static constexpr int CPT = MT * 8 / NT;
   static constexpr int HLD = h_ld<float>();
   static constexpr int KLD = kv_ld<float>(HD);
 
-  static __device__ void run(const float* const (&hrow)[CPT], const float* gamma, int d, float eps,
-                             const Half (&halves)[2], float* hst, float* rinv, const int* pos, const double* rev,
-                             float* kv) {
+  static __device__ void run(const float* const (&hrow)[CPT], const bool (&valid)[CPT], const float* gamma, int d,
+                             float eps, const Half (&halves)[2], float* hst, float* rinv, const int* pos,
+                             const double* rev, float* kv) {
     const int tid = threadIdx.x, sub = tid & 7;
-    const int p = tid % HD;            // feature pair: rows 2p, 2p+1 of the 2*HD rows
+    const int p = tid % HD;
     const int tg = tid / HD;
     const int half = (2 * p) / HD;
     const int r0 = (2 * p) % HD;
-    const float* w = static_cast<const float*>(halves[half].w);
+    const float* w = static_cast<const float*>(half ? halves[1].w : halves[0].w);
     const float* w0 = w ? w + (size_t)r0 * d : nullptr;
     const int nsteps = d / kKT;
 
-    bool valid[CPT];
-#pragma unroll
-    for (int r = 0; r < CPT; ++r) valid[r] = hrow[r] != nullptr;
     float ss[CPT];
 #pragma unroll
     for (int r = 0; r < CPT; ++r) ss[r] = 0.0f;
@@ -335,17 +363,13 @@ struct F32Tile {
 #pragma unroll
       for (int r = 0; r < CPT; ++r) {
         float x[8];
-        if (valid[r]) {
-          load8(hrow[r] + (size_t)s * kKT, x);
-        } else {
-#pragma unroll
-          for (int e = 0; e < 8; ++e) x[e] = 0.0f;
-        }
-        float* dst = hst + (size_t)((tid >> 3) + 32 * r) * HLD + 8 * sub;
+        load8(hrow[r] + (size_t)s * kKT, x);
+        float* dst = hst + (size_t)((tid >> 3) + (NT / 8) * r) * HLD + 8 * sub;
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
-          ss[r] = fmaf(x[e], x[e], ss[r]);
-          dst[e] = x[e] * g[e];
+          const float xe = valid[r] ? x[e] : 0.0f;
+          ss[r] = fmaf(xe, xe, ss[r]);
+          dst[e] = xe * g[e];
         }
       }
       __syncthreads();
@@ -371,7 +395,7 @@ struct F32Tile {
       __syncthreads();
     }
 
-    finish_rms<CPT>(ss, valid, d, eps, rinv);
+    finish_rms<NT, CPT>(ss, valid, d, eps, rinv);
     __syncthreads();
 
 #pragma unroll
@@ -379,7 +403,7 @@ struct F32Tile {
       const int tok = tg * TPT + t;
       const float ri = rinv[tok];
       float v0 = acc0[t] * ri, v1 = acc1[t] * ri;
-      if (halves[half].rope) rope_rotate(v0, v1, pos[tok], rev[r0 >> 1]);
+      if (half ? halves[1].rope : halves[0].rope) rope_rotate(v0, v1, pos[tok], rev[r0 >> 1]);
       *reinterpret_cast<float2*>(kv + (size_t)tok * KLD + half * HD + r0) = make_float2(v0, v1);
     }
   }
@@ -389,74 +413,108 @@ struct F32Tile {
 
 // q heads j*g .. j*g+g-1 of sequence b into LDS (fp32), pre-multiplied by
 // log2(e)/sqrt(head_dim).
-template <typename T, int HD>
+template <typename T, int HD, int NT>
 __device__ __forceinline__ void load_q(const T* q, int b, int n_q, int j, int g, float* qs) {
+  constexpr int CH = 16 / sizeof(T);
   const T* src = q + ((size_t)b * n_q + (size_t)j * g) * HD;
-  for (int i = threadIdx.x; i < g * HD; i += kThreads) qs[i] = to_f<T>(src[i]) * ScoreScale<HD>::v;
+  for (int c = threadIdx.x; c < g * HD / CH; c += NT) {
+    float x[8];
+    if constexpr (CH == 8) {
+      load8(src + CH * c, x);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) qs[CH * c + e] = x[e] * ScoreScale<HD>::v;
+    } else {
+      const float4 v = *reinterpret_cast<const float4*>(src + CH * c);
+      qs[CH * c + 0] = v.x * ScoreScale<HD>::v;
+      qs[CH * c + 1] = v.y * ScoreScale<HD>::v;
+      qs[CH * c + 2] = v.z * ScoreScale<HD>::v;
+      qs[CH * c + 3] = v.w * ScoreScale<HD>::v;
+    }
+  }
 }
 
-// Rows t0 .. t0+n-1 of a stored K/V block ([B][n_kv][t_cap][HD], head j of
-// sequence b, rows counted from t_off) into the LDS tile [kTile][K | V].
-template <typename T, int HD>
+// Rows row0 .. row0+n-1 (n <= kTile) of a stored K/V block ([B][n_kv][t_cap][HD],
+// head j of sequence b) into the LDS tile [kTile][K | V].  All loads of a thread
+// are issued before its LDS stores.
+template <typename T, int HD, int NT>
 __device__ __forceinline__ void load_kv_tile(const T* K, const T* V, int b, int n_kv, int j, int t_cap, int row0,
                                              int n, T* kv) {
   constexpr int KLD = kv_ld<T>(HD);
-  constexpr int CH = 16 / sizeof(T);  // elements per 16-byte chunk
-  constexpr int CPR = HD / CH;        // chunks per K (or V) row
+  constexpr int CH = 16 / sizeof(T);         // elements per 16-byte chunk
+  constexpr int CPR = HD / CH;               // chunks per K (or V) row
+  constexpr int HALF = kTile * CPR / NT;     // chunks per thread for the K (or V) half of a full tile
+  static_assert(HALF * NT == kTile * CPR, "tile split");
   const size_t base = ((size_t)b * n_kv + j) * t_cap + row0;
-  for (int c = threadIdx.x; c < 2 * n * CPR; c += kThreads) {
-    const int which = c / (n * CPR);  // 0: K, 1: V
-    const int rem = c - which * n * CPR;
-    const int t = rem / CPR, ch = rem - t * CPR;
-    const T* src = (which ? V : K) + (base + t) * HD + ch * CH;
-    *reinterpret_cast<uint4*>(kv + (size_t)t * KLD + which * HD + ch * CH) = *reinterpret_cast<const uint4*>(src);
+  uint4 v[2 * HALF];
+#pragma unroll
+  for (int i = 0; i < 2 * HALF; ++i) {
+    const int rem = threadIdx.x + NT * (i % HALF);
+    const int t = rem / CPR, ch = rem % CPR;
+    const T* src = (i < HALF ? K : V) + (base + (t < n ? t : 0)) * HD + ch * CH;
+    v[i] = *reinterpret_cast<const uint4*>(src);
+  }
+#pragma unroll
+  for (int i = 0; i < 2 * HALF; ++i) {
+    const int rem = threadIdx.x + NT * (i % HALF);
+    const int t = rem / CPR, ch = rem % CPR;
+    if (t < n) *reinterpret_cast<uint4*>(kv + (size_t)t * KLD + (i < HALF ? 0 : HD) + ch * CH) = v[i];
   }
 }
 
 // Softmax partial state of keys 0..n-1 of an LDS K/V tile (rows stride KLD,
 // K at columns 0..HD-1, V at HD..2HD-1) for g query heads:
 //   m_h = max_t s_ht,  l_h = sum_t 2^(s_ht - m_h),  acc_h = sum_t 2^(s_ht - m_h) V_t,
-// with s_ht = log2(e) q_h.K_t / sqrt(HD).  Results in LDS (L.ml, L.acc).
-template <typename T, int HD>
+// with s_ht = log2(e) q_h.K_t / sqrt(HD).  Results in LDS (L.ml, L.acc).  The
+// arithmetic (task split and summation order) does not depend on the thread
+// count NT, so every kernel that attends a tile gets identical bits.
+template <typename T, int HD, int NT>
 __device__ void attend_tile(const T* kv, int n, int rows, int g, char* lds, const AttnLds& L) {
   constexpr int KLD = kv_ld<T>(HD);
   constexpr int C8 = HD / 8;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = wave_id();
   const float* qs = reinterpret_cast<const float*>(lds + L.q);
   float* S = reinterpret_cast<float*>(lds + L.s);
   float* red = reinterpret_cast<float*>(lds + L.red);
   float* ml = reinterpret_cast<float*>(lds + L.ml);
   float* acc = reinterpret_cast<float*>(lds + L.acc);
 
-  for (int task = tid; task < g * rows; task += kThreads) {
+  for (int task = tid; task < g * rows; task += NT) {
     const int h = task / rows, t = task - h * rows;
     float s = -INFINITY;
     if (t < n) {
       const T* krow = kv + (size_t)t * KLD;
       const float* qh = qs + h * HD;
-      float dot = 0.0f;
-#pragma unroll 4
-      for (int c = 0; c < C8; ++c) {
+      float d0 = 0.0f, d1 = 0.0f, d2 = 0.0f, d3 = 0.0f;
+      auto dot8 = [&](int c, float x) {
         float k8[8];
         load8(krow + 8 * c, k8);
         const float4 qa = *reinterpret_cast<const float4*>(qh + 8 * c);
         const float4 qb = *reinterpret_cast<const float4*>(qh + 8 * c + 4);
-        dot = fmaf(qa.x, k8[0], dot);
-        dot = fmaf(qa.y, k8[1], dot);
-        dot = fmaf(qa.z, k8[2], dot);
-        dot = fmaf(qa.w, k8[3], dot);
-        dot = fmaf(qb.x, k8[4], dot);
-        dot = fmaf(qb.y, k8[5], dot);
-        dot = fmaf(qb.z, k8[6], dot);
-        dot = fmaf(qb.w, k8[7], dot);
+        x = fmaf(qa.x, k8[0], x);
+        x = fmaf(qa.y, k8[1], x);
+        x = fmaf(qa.z, k8[2], x);
+        x = fmaf(qa.w, k8[3], x);
+        x = fmaf(qb.x, k8[4], x);
+        x = fmaf(qb.y, k8[5], x);
+        x = fmaf(qb.z, k8[6], x);
+        x = fmaf(qb.w, k8[7], x);
+        return x;
+      };
+#pragma unroll 2
+      for (int c = 0; c < C8; c += 4) {
+        d0 = dot8(c, d0);
+        d1 = dot8(c + 1, d1);
+        d2 = dot8(c + 2, d2);
+        d3 = dot8(c + 3, d3);
       }
-      s = dot;
+      s = (d0 + d1) + (d2 + d3);
     }
     S[h * rows + t] = s;
   }
   __syncthreads();
 
-  for (int h = wave; h < g; h += kThreads / 64) {
+  for (int h = wave; h < g; h += NT / 64) {
     float m = -INFINITY;
     for (int t = lane; t < n; t += 64) m = fmaxf(m, S[h * rows + t]);
     m = wave_max(m);
@@ -475,8 +533,8 @@ __device__ void attend_tile(const T* kv, int n, int rows, int g, char* lds, cons
   __syncthreads();
 
   const int per = g * C8;
-  const int TS = per >= kThreads ? 1 : kThreads / per;
-  for (int task = tid; task < TS * per; task += kThreads) {
+  const int TS = per >= kAttnTasks ? 1 : kAttnTasks / per;
+  for (int task = tid; task < TS * per; task += NT) {
     const int c8 = task % C8;
     const int rest = task / C8;
     const int h = rest % g, ts = rest / g;
@@ -493,7 +551,7 @@ __device__ void attend_tile(const T* kv, int n, int rows, int g, char* lds, cons
     for (int e = 0; e < 8; ++e) dst[e] = a8[e];
   }
   __syncthreads();
-  for (int idx = tid; idx < g * HD; idx += kThreads) {
+  for (int idx = tid; idx < g * HD; idx += NT) {
     float s = 0.0f;
     for (int ts = 0; ts < TS; ++ts) s += red[(size_t)ts * g * HD + idx];
     acc[idx] = s;
@@ -503,18 +561,20 @@ __device__ void attend_tile(const T* kv, int n, int rows, int g, char* lds, cons
 
 // Split-K partial of (b, KV head j, split s) into the workspace:
 // acc [B][n_q][S][HD] fp32 followed by ml [B][n_q][S][2] fp32.
-template <int HD>
+template <int HD, int NT>
 __device__ __forceinline__ void write_partial(const char* lds, const AttnLds& L, float* ws_acc, float* ws_ml, int b,
                                               int n_q, int j, int g, int S, int s) {
   const float* acc = reinterpret_cast<const float*>(lds + L.acc);
   const float* ml = reinterpret_cast<const float*>(lds + L.ml);
-  for (int idx = threadIdx.x; idx < g * HD; idx += kThreads) {
-    const int h = idx / HD, c = idx - h * HD;
-    ws_acc[(((size_t)b * n_q + (size_t)j * g + h) * S + s) * HD + c] = acc[idx];
+  for (int c4 = threadIdx.x; c4 < g * HD / 4; c4 += NT) {
+    const int h = (4 * c4) / HD, c = 4 * c4 - h * HD;
+    *reinterpret_cast<float4*>(ws_acc + (((size_t)b * n_q + (size_t)j * g + h) * S + s) * HD + c) =
+        *reinterpret_cast<const float4*>(acc + 4 * c4);
   }
-  if (threadIdx.x < 2 * g) {
-    const int h = threadIdx.x >> 1, k = threadIdx.x & 1;
-    ws_ml[(((size_t)b * n_q + (size_t)j * g + h) * S + s) * 2 + k] = ml[threadIdx.x];
+  if (threadIdx.x < g) {
+    const int h = threadIdx.x;
+    *reinterpret_cast<float2*>(ws_ml + (((size_t)b * n_q + (size_t)j * g + h) * S + s) * 2) =
+        make_float2(ml[2 * h], ml[2 * h + 1]);
   }
 }
 

@@ -1,12 +1,15 @@
 // Kernels and launchers of libkvd (gfx950).
 //
-//   proj_kernel     RMSNorm + projection + RoPE of token tiles (RECOMPUTE_KV /
-//                   prefill, and the current token's q, K_t, V_t of a decode step).
-//   fused_kernel    per (b, KV head, 64-key chunk): recompute K/V of the chunk
-//                   into LDS and emit its split-K softmax partial without writing
-//                   K/V to HBM; extra chunks attend a stored tail (CONCAT).
-//   decode_kernel   per (b, KV head, 64-key chunk) of stored K/V: split-K partial.
-//   combine_kernel  merges the partials of each (b, query head) in split order.
+//   proj_kernel         RMSNorm + projection + RoPE of token tiles (RECOMPUTE_KV /
+//                       prefill; also the fp32 current-token projection).
+//   stream_proj_kernel  bf16 current-token q, K_t, V_t of a decode step: one wave per
+//                       32 weight rows streams its rows with deep prefetch (a GEMV
+//                       shape), on the same per-element arithmetic as proj_kernel.
+//   fused_kernel        per (b, KV head, 64-key chunk): recompute K/V of the chunk
+//                       into LDS and emit its split-K softmax partial without writing
+//                       K/V to HBM; stored tail tiles (CONCAT) ride along.
+//   decode_kernel       per (b, KV head, 64-key chunk) of stored K/V: split-K partial.
+//   combine_kernel      merges the partials of each (b, query head) in split order.
 #include <hip/hip_runtime.h>
 
 #include "kvd_device.hpp"
@@ -14,15 +17,23 @@
 
 namespace kvd {
 
-// ------------------------------------------------------------------ projection
+// ------------------------------------------------------------------ recompute / prefill
 
-template <typename T, int HD, int MT>
-__global__ __launch_bounds__(kThreads, 1) void proj_kernel(ProjArgs a) {
+// grid: xcd_map(n_units * n_tiles) workgroups; item = unit * n_tiles + tile, so
+// the token tiles of one KV head (which share W_k / W_v) run on one XCD.
+template <typename T, int HD, int MT, bool PACKED>
+__global__ __launch_bounds__(kNtTile, 1) void proj_kernel(ProjArgs a, int per_xcd, int n_tiles, int n_units) {
   extern __shared__ __align__(16) char lds[];
+  constexpr int NT = kNtTile;
   constexpr ProjLds PL = proj_lds<T>(HD, MT);
-  constexpr int CPT = MT / 32;
+  constexpr int CPT = MT * 8 / NT;
   constexpr int KLD = kv_ld<T>(HD);
   const int tid = threadIdx.x;
+  const long long item = (long long)(blockIdx.x % kXcds) * per_xcd + blockIdx.x / kXcds;
+  if (item >= (long long)n_units * n_tiles) return;
+  const int unit = (int)(item / n_tiles);
+  const int tile = (int)(item - (long long)unit * n_tiles);
+
   double* rev = reinterpret_cast<double*>(lds + PL.rev);
   float* rinv = reinterpret_cast<float*>(lds + PL.rinv);
   int* pos = reinterpret_cast<int*>(lds + PL.pos);
@@ -30,8 +41,7 @@ __global__ __launch_bounds__(kThreads, 1) void proj_kernel(ProjArgs a) {
   T* kv = reinterpret_cast<T*>(lds + PL.kv);
 
   const long long ntok = (long long)a.B * a.T;
-  const long long n0 = (long long)blockIdx.x * MT;
-  const int unit = blockIdx.y;
+  const long long n0 = (long long)tile * MT;
   const bool kv_mode = unit < a.n_kv_units;
   const size_t hd_d = (size_t)HD * a.d;
 
@@ -50,6 +60,11 @@ __global__ __launch_bounds__(kThreads, 1) void proj_kernel(ProjArgs a) {
   }
 
   if (tid < HD / 2) rev[tid] = a.rev[tid];
+  uint16_t* gam = reinterpret_cast<uint16_t*>(lds + PL.end);
+  if constexpr (sizeof(T) == 2) {
+    for (int c = tid; c < a.d / 8; c += NT)
+      *reinterpret_cast<uint4*>(gam + 8 * c) = *reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(a.gamma) + 8 * c);
+  }
   if (tid < MT) {
     const long long n = n0 + tid;
     int p = 0;
@@ -60,95 +75,270 @@ __global__ __launch_bounds__(kThreads, 1) void proj_kernel(ProjArgs a) {
     pos[tid] = p;
   }
   const T* hrow[CPT];
+  bool valid[CPT];
 #pragma unroll
   for (int r = 0; r < CPT; ++r) {
-    const long long n = n0 + (tid >> 3) + 32 * r;
-    if (n < ntok) {
-      const int b = (int)(n / a.T), t = (int)(n - (long long)b * a.T);
-      hrow[r] = static_cast<const T*>(a.h) + ((size_t)b * a.h_ld + t) * a.d + 8 * (tid & 7);
-    } else {
-      hrow[r] = nullptr;
-    }
+    long long n = n0 + (tid >> 3) + (NT / 8) * r;
+    valid[r] = n < ntok;
+    if (!valid[r]) n = n0;  // any readable row; its values are replaced by zeros
+    const int b = (int)(n / a.T), t = (int)(n - (long long)b * a.T);
+    hrow[r] = static_cast<const T*>(a.h) + ((size_t)b * a.h_ld + t) * a.d + 8 * (tid & 7);
   }
   __syncthreads();
 
   if constexpr (sizeof(T) == 2) {
-    MfmaTile<HD, MT>::run(hrow, static_cast<const uint16_t*>(a.gamma), a.d, a.eps, halves, hst, rinv, pos, rev, kv);
+    MfmaTile<HD, MT, PACKED>::run(hrow, valid, gam, a.d, a.eps, halves, hst, rinv, pos, rev, kv);
   } else {
-    F32Tile<HD, MT>::run(hrow, static_cast<const float*>(a.gamma), a.d, a.eps, halves, hst, rinv, pos, rev, kv);
+    F32Tile<HD, MT>::run(hrow, valid, static_cast<const float*>(a.gamma), a.d, a.eps, halves, hst, rinv, pos, rev,
+                         kv);
   }
   __syncthreads();
 
   // store: 16-byte chunks of each valid token row of each present half.
   constexpr int CH = 16 / sizeof(T);
   constexpr int CPR = HD / CH;
-  for (int c = tid; c < 2 * MT * CPR; c += kThreads) {
+  for (int c = tid; c < 2 * MT * CPR; c += NT) {
     const int half = c / (MT * CPR);
     const int rem = c - half * MT * CPR;
     const int row = rem / CPR, ch = rem - row * CPR;
     const long long n = n0 + row;
-    if (n >= ntok || halves[half].w == nullptr) continue;
+    const bool present = half ? halves[1].w != nullptr : halves[0].w != nullptr;
+    if (n >= ntok || !present) continue;
     const int b = (int)(n / a.T), t = (int)(n - (long long)b * a.T);
+    const int head = half ? heads[1] : heads[0];
     T* dst;
     if (kv_mode) {
       T* base = static_cast<T*>(half ? a.v_out : a.k_out);
-      dst = base + (((size_t)b * a.n_kv + heads[half]) * a.kv_t_cap + a.kv_t_off + t) * HD;
+      dst = base + (((size_t)b * a.n_kv + head) * a.kv_t_cap + a.kv_t_off + t) * HD;
     } else {
-      dst = static_cast<T*>(a.q_out) + ((size_t)b * a.n_q + heads[half]) * HD;
+      dst = static_cast<T*>(a.q_out) + ((size_t)b * a.n_q + head) * HD;
     }
     *reinterpret_cast<uint4*>(dst + ch * CH) =
         *reinterpret_cast<const uint4*>(kv + (size_t)row * KLD + half * HD + ch * CH);
   }
 }
 
+// ------------------------------------------------------------------ streaming current-token projection
+
+// One wave per workgroup.  blockIdx.x: a 32-row block of [W_q rows | W_k rows |
+// W_v rows]; blockIdx.y: a group of kProjTok sequences.  The group's gamma-scaled
+// residuals (and 1/rms) are staged into LDS once; the wave then streams its 32
+// weight rows with kProjPrefetch K-steps in flight.  Per output element the
+// arithmetic is MfmaTile's (same MFMA chain over d, same 1/rms, same epilogue),
+// so K_t / V_t equal what recompute gives for the same row.
+template <int HD, bool PACKED>
+__global__ __launch_bounds__(64) void stream_proj_kernel(ProjArgs a, int q_blocks, int k_blocks) {
+  extern __shared__ __align__(16) char lds[];
+  constexpr int PD = kProjPrefetch;
+  const int lane = threadIdx.x, sub = lane & 7;
+  const int d = a.d;
+  const StreamLds SL = stream_lds(d);
+  const int HLD = stream_h_ld(d);
+  double* rev = reinterpret_cast<double*>(lds + SL.rev);
+  float* rinv = reinterpret_cast<float*>(lds + SL.rinv);
+  int* pos = reinterpret_cast<int*>(lds + SL.pos);
+  uint16_t* hb = reinterpret_cast<uint16_t*>(lds + SL.hb);
+
+  const int blk = blockIdx.x;
+  const int b0 = blockIdx.y * kProjTok;
+  const int nt = min(kProjTok, a.B - b0);
+  const uint16_t* W;
+  int row0, rope, mat;  // mat: 0 q, 1 k, 2 v
+  if (blk < q_blocks) {
+    W = static_cast<const uint16_t*>(a.w_q); row0 = 32 * blk; rope = 1; mat = 0;
+  } else if (blk < q_blocks + k_blocks) {
+    W = static_cast<const uint16_t*>(a.w_k); row0 = 32 * (blk - q_blocks); rope = 1; mat = 1;
+  } else {
+    W = static_cast<const uint16_t*>(a.w_v); row0 = 32 * (blk - q_blocks - k_blocks); rope = 0; mat = 2;
+  }
+
+  for (int i = lane; i < HD / 2; i += 64) rev[i] = a.rev[i];
+  for (int r = lane; r < kProjTok; r += 64) pos[r] = r < nt ? a.pos0[b0 + r] : 0;
+
+  // stage gamma * h (bf16) and the sum of squares: lane -> rows (lane>>3) + 8r, column chunk sub
+  {
+    const int nsteps = d / kKT;
+    const uint16_t* g = static_cast<const uint16_t*>(a.gamma) + 8 * sub;
+    const uint16_t* hr[2];
+    bool ok[2];
+    float ss[2] = {0.0f, 0.0f};
+#pragma unroll
+    for (int r = 0; r < 2; ++r) {
+      const int row = (lane >> 3) + 8 * r;
+      ok[r] = row < nt;
+      hr[r] = static_cast<const uint16_t*>(a.h) + (size_t)(b0 + (ok[r] ? row : 0)) * d + 8 * sub;
+    }
+    for (int s0 = 0; s0 < nsteps; s0 += 4) {
+      uint4 hv[4][2], gv[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int s = min(s0 + u, nsteps - 1);
+        gv[u] = *reinterpret_cast<const uint4*>(g + (size_t)s * kKT);
+#pragma unroll
+        for (int r = 0; r < 2; ++r) hv[u][r] = *reinterpret_cast<const uint4*>(hr[r] + (size_t)s * kKT);
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int s = s0 + u;
+        if (s < nsteps) {
+#pragma unroll
+          for (int r = 0; r < 2; ++r) {
+            const uint4 x = ok[r] ? hv[u][r] : make_uint4(0, 0, 0, 0);
+            const uint4 o = stage_chunk_bf16(x, gv[u], ss[r]);
+            *reinterpret_cast<uint4*>(hb + (size_t)((lane >> 3) + 8 * r) * HLD + (size_t)s * kKT + 8 * sub) = o;
+          }
+        }
+      }
+    }
+#pragma unroll
+    for (int r = 0; r < 2; ++r) {
+      float v = ss[r];
+      v += __shfl_xor(v, 1, 64);
+      v += __shfl_xor(v, 2, 64);
+      v += __shfl_xor(v, 4, 64);
+      if (sub == 0) rinv[(lane >> 3) + 8 * r] = ok[r] ? 1.0f / sqrtf(v / (float)d + a.eps) : 0.0f;
+    }
+  }
+  __syncthreads();
+
+  // MFMA over d: A = 32 weight rows, B = the group's tokens (columns >= kProjTok are zero)
+  const uint16_t* wrow = PACKED ? W + (size_t)row0 * d + 8 * lane : W + (size_t)(row0 + (lane & 31)) * d + 8 * (lane >> 5);
+  const int col = lane & 31;
+  const bool col_ok = col < kProjTok;
+  const uint16_t* hcol = hb + (size_t)(col_ok ? col : 0) * HLD + 8 * (lane >> 5);
+  const int nsteps = d / kKT;
+  f32x16_t acc;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) acc[i] = 0.0f;
+  bf16x8_t ring[PD][4];
+#pragma unroll
+  for (int u = 0; u < PD; ++u)
+#pragma unroll
+    for (int k = 0; k < 4; ++k)
+      ring[u][k] = *reinterpret_cast<const bf16x8_t*>(wrow + w_off<PACKED>(min(u, nsteps - 1), k));
+  bf16x8_t zero;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) zero[i] = (__bf16)0.0f;
+  for (int s0 = 0; s0 < nsteps; s0 += PD) {
+#pragma unroll
+    for (int u = 0; u < PD; ++u) {
+      const int s = s0 + u;
+      if (s < nsteps) {
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          const bf16x8_t bv = col_ok ? *reinterpret_cast<const bf16x8_t*>(hcol + (size_t)s * kKT + 16 * k) : zero;
+          acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ring[u][k], bv, acc, 0, 0, 0);
+        }
+        if (s + PD < nsteps) {
+#pragma unroll
+          for (int k = 0; k < 4; ++k)
+            ring[u][k] = *reinterpret_cast<const bf16x8_t*>(wrow + w_off<PACKED>(s + PD, k));
+        }
+      }
+    }
+  }
+
+  if (col >= nt) return;
+  const float ri = rinv[col];
+  const int p = pos[col];
+  const int b = b0 + col;
+  float v[16];
+#pragma unroll
+  for (int r = 0; r < 16; ++r) v[r] = acc[r] * ri;
+  const int head = row0 / HD, f0 = row0 % HD;
+  if (rope) {
+#pragma unroll
+    for (int r = 0; r < 16; r += 2) {
+      const int f = f0 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+      rope_rotate(v[r], v[r + 1], p, rev[f >> 1]);
+    }
+  }
+  uint16_t* dst;
+  if (mat == 0) {
+    dst = static_cast<uint16_t*>(a.q_out) + ((size_t)b * a.n_q + head) * HD;
+  } else {
+    uint16_t* base = static_cast<uint16_t*>(mat == 1 ? a.k_out : a.v_out);
+    dst = base + (((size_t)b * a.n_kv + head) * a.kv_t_cap + a.kv_t_off) * HD;
+  }
+#pragma unroll
+  for (int g4 = 0; g4 < 4; ++g4) {
+    const int f = f0 + 8 * g4 + 4 * (lane >> 5);
+    uint2 o;
+    o.x = pack_bf16x2(v[4 * g4 + 0], v[4 * g4 + 1]);
+    o.y = pack_bf16x2(v[4 * g4 + 2], v[4 * g4 + 3]);
+    *reinterpret_cast<uint2*>(dst + f) = o;
+  }
+}
+
 // ------------------------------------------------------------------ fused recompute + attention
 
-template <typename T, int HD, int MT>
-__global__ __launch_bounds__(kThreads, 1) void fused_kernel(FusedArgs a) {
+// grid: xcd_map(n_kv * B * C) workgroups, item = (j * B + b) * C + c (the chunks of
+// one KV head, which share W_k / W_v, run on one XCD).  C = n_rec, or n_tail when
+// nothing is recomputed.  Chunk c < n_rec recomputes residual rows c*MT..c*MT+MT-1
+// and writes partial c; tail tile k (partial n_rec + k) is attended by chunk
+// n_rec - 1 - (k % n_rec) after its own chunk.
+template <typename T, int HD, int MT, bool PACKED>
+__global__ __launch_bounds__(kNtTile, 1) void fused_kernel(FusedArgs a, int per_xcd) {
   extern __shared__ __align__(16) char lds[];
+  constexpr int NT = kNtTile;
   constexpr ProjLds PL = proj_lds<T>(HD, MT);
-  constexpr int CPT = MT / 32;
+  constexpr int CPT = MT * 8 / NT;
   constexpr int KLD = kv_ld<T>(HD);
+  static_assert(MT == kTile, "fused chunks are attention tiles");
   const int tid = threadIdx.x;
-  const int s = blockIdx.x, j = blockIdx.y, b = blockIdx.z;
+  const int n_tail = (a.T_tail + kTile - 1) / kTile;
+  const int C = a.n_rec > 0 ? a.n_rec : n_tail;
+  const long long item = (long long)(blockIdx.x % kXcds) * per_xcd + blockIdx.x / kXcds;
+  if (item >= (long long)a.n_kv * a.B * C) return;
+  const int c = (int)(item % C);
+  const int unit = (int)(item / C);
+  const int j = unit / a.B, b = unit - j * a.B;
   const int g = a.n_q / a.n_kv;
   const AttnLds AL = attn_lds(PL.end, g, HD, MT);
   T* kv = reinterpret_cast<T*>(lds + PL.kv);
 
-  load_q<T, HD>(static_cast<const T*>(a.q), b, a.n_q, j, g, reinterpret_cast<float*>(lds + AL.q));
+  load_q<T, HD, NT>(static_cast<const T*>(a.q), b, a.n_q, j, g, reinterpret_cast<float*>(lds + AL.q));
 
-  int n;
-  if (s < a.n_rec) {
-    const int t0 = s * MT;
-    n = min(MT, a.T_rec - t0);
+  if (a.n_rec > 0) {
+    const int t0 = c * MT;
+    const int n = min(MT, a.T_rec - t0);
     double* rev = reinterpret_cast<double*>(lds + PL.rev);
     float* rinv = reinterpret_cast<float*>(lds + PL.rinv);
     int* pos = reinterpret_cast<int*>(lds + PL.pos);
     T* hst = reinterpret_cast<T*>(lds + PL.hst);
     if (tid < HD / 2) rev[tid] = a.rev[tid];
     if (tid < MT) pos[tid] = a.pos0[b] + t0 + tid;
+    uint16_t* gam = reinterpret_cast<uint16_t*>(lds + AL.end);
+    if constexpr (sizeof(T) == 2) {
+      for (int i = tid; i < a.d / 8; i += NT)
+        *reinterpret_cast<uint4*>(gam + 8 * i) =
+            *reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(a.gamma) + 8 * i);
+    }
     const T* hrow[CPT];
+    bool valid[CPT];
 #pragma unroll
     for (int r = 0; r < CPT; ++r) {
-      const int t = (tid >> 3) + 32 * r;
-      hrow[r] = t < n ? static_cast<const T*>(a.h) + ((size_t)b * a.h_ld + t0 + t) * a.d + 8 * (tid & 7) : nullptr;
+      const int t = (tid >> 3) + (NT / 8) * r;
+      valid[r] = t < n;
+      hrow[r] = static_cast<const T*>(a.h) + ((size_t)b * a.h_ld + t0 + (valid[r] ? t : 0)) * a.d + 8 * (tid & 7);
     }
     const size_t hd_d = (size_t)HD * a.d;
     const Half halves[2] = {Half{static_cast<const T*>(a.w_k) + j * hd_d, 1},
                             Half{static_cast<const T*>(a.w_v) + j * hd_d, 0}};
     __syncthreads();
     if constexpr (sizeof(T) == 2) {
-      MfmaTile<HD, MT>::run(hrow, static_cast<const uint16_t*>(a.gamma), a.d, a.eps, halves, hst, rinv, pos, rev, kv);
+      MfmaTile<HD, MT, PACKED>::run(hrow, valid, gam, a.d, a.eps, halves, hst, rinv, pos, rev, kv);
     } else {
-      F32Tile<HD, MT>::run(hrow, static_cast<const float*>(a.gamma), a.d, a.eps, halves, hst, rinv, pos, rev, kv);
+      F32Tile<HD, MT>::run(hrow, valid, static_cast<const float*>(a.gamma), a.d, a.eps, halves, hst, rinv, pos, rev,
+                           kv);
     }
     __syncthreads();
     if (a.dbg_k != nullptr) {
       constexpr int CH = 16 / sizeof(T);
       constexpr int CPR = HD / CH;
-      for (int c = tid; c < 2 * n * CPR; c += kThreads) {
-        const int half = c / (n * CPR);
-        const int rem = c - half * n * CPR;
+      for (int i = tid; i < 2 * n * CPR; i += NT) {
+        const int half = i / (n * CPR);
+        const int rem = i - half * n * CPR;
         const int row = rem / CPR, ch = rem - row * CPR;
         T* base = static_cast<T*>(half ? a.dbg_v : a.dbg_k);
         T* dst = base + (((size_t)b * a.n_kv + j) * a.dbg_t_cap + a.dbg_t_off + t0 + row) * HD;
@@ -156,53 +346,129 @@ __global__ __launch_bounds__(kThreads, 1) void fused_kernel(FusedArgs a) {
             *reinterpret_cast<const uint4*>(kv + (size_t)row * KLD + half * HD + ch * CH);
       }
     }
+    attend_tile<T, HD, NT>(kv, n, MT, g, lds, AL);
+    write_partial<HD, NT>(lds, AL, a.ws_acc, a.ws_ml, b, a.n_q, j, g, a.S, c);
+    // stored tail tiles assigned to this chunk
+    for (int k = a.n_rec - 1 - c; k < n_tail; k += a.n_rec) {
+      const int r0 = k * kTile;
+      const int nk = min(kTile, a.T_tail - r0);
+      __syncthreads();
+      load_kv_tile<T, HD, NT>(static_cast<const T*>(a.tk), static_cast<const T*>(a.tv), b, a.n_kv, j, a.tail_t_cap,
+                              a.tail_t_off + r0, nk, kv);
+      __syncthreads();
+      attend_tile<T, HD, NT>(kv, nk, MT, g, lds, AL);
+      write_partial<HD, NT>(lds, AL, a.ws_acc, a.ws_ml, b, a.n_q, j, g, a.S, a.n_rec + k);
+    }
   } else {
-    const int t0 = (s - a.n_rec) * MT;
-    n = min(MT, a.T_tail - t0);
-    load_kv_tile<T, HD>(static_cast<const T*>(a.tk), static_cast<const T*>(a.tv), b, a.n_kv, j, a.tail_t_cap,
-                        a.tail_t_off + t0, n, kv);
+    const int r0 = c * kTile;
+    const int nk = min(kTile, a.T_tail - r0);
+    load_kv_tile<T, HD, NT>(static_cast<const T*>(a.tk), static_cast<const T*>(a.tv), b, a.n_kv, j, a.tail_t_cap,
+                            a.tail_t_off + r0, nk, kv);
     __syncthreads();
+    attend_tile<T, HD, NT>(kv, nk, MT, g, lds, AL);
+    write_partial<HD, NT>(lds, AL, a.ws_acc, a.ws_ml, b, a.n_q, j, g, a.S, c);
   }
-
-  attend_tile<T, HD>(kv, n, MT, g, lds, AL);
-  write_partial<HD>(lds, AL, a.ws_acc, a.ws_ml, b, a.n_q, j, g, a.S, s);
 }
 
 // ------------------------------------------------------------------ stored-K/V attention
 
 template <typename T, int HD>
-__global__ __launch_bounds__(kThreads) void decode_kernel(AttnArgs a) {
+__global__ __launch_bounds__(kNtAttn) void decode_kernel(AttnArgs a) {
   extern __shared__ __align__(16) char lds[];
+  constexpr int NT = kNtAttn;
   const int s = blockIdx.x, j = blockIdx.y, b = blockIdx.z;
   const int g = a.n_q / a.n_kv;
   const AttnLds AL = attn_lds(align_up(sizeof(T) * kTile * kv_ld<T>(HD), 16), g, HD, kTile);
   T* kv = reinterpret_cast<T*>(lds);
   const int t0 = s * kTile;
   const int n = min(kTile, a.T - t0);
-  load_q<T, HD>(static_cast<const T*>(a.q), b, a.n_q, j, g, reinterpret_cast<float*>(lds + AL.q));
-  load_kv_tile<T, HD>(static_cast<const T*>(a.k), static_cast<const T*>(a.v), b, a.n_kv, j, a.t_cap, a.t_off + t0,
-                      n, kv);
+  load_kv_tile<T, HD, NT>(static_cast<const T*>(a.k), static_cast<const T*>(a.v), b, a.n_kv, j, a.t_cap,
+                          a.t_off + t0, n, kv);
+  load_q<T, HD, NT>(static_cast<const T*>(a.q), b, a.n_q, j, g, reinterpret_cast<float*>(lds + AL.q));
   __syncthreads();
-  attend_tile<T, HD>(kv, n, kTile, g, lds, AL);
-  write_partial<HD>(lds, AL, a.ws_acc, a.ws_ml, b, a.n_q, j, g, a.S, s);
+  attend_tile<T, HD, NT>(kv, n, kTile, g, lds, AL);
+  write_partial<HD, NT>(lds, AL, a.ws_acc, a.ws_ml, b, a.n_q, j, g, a.S, s);
 }
 
-// out[b][h] = sum_s 2^(m_s - M) acc_s / sum_s 2^(m_s - M) l_s, M = max_s m_s, in split order.
+// out[b][h] = sum_s w_s acc_s / sum_s w_s l_s, w_s = 2^(m_s - M), M = max_s m_s.
+// One workgroup per (b, h); the weights of a block of 256 splits are computed in
+// parallel into LDS, then each thread sums its column over the block in split order.
 template <typename T, int HD>
-__global__ __launch_bounds__(HD) void combine_kernel(const float* ws_acc, const float* ws_ml, T* out, int n_q, int S) {
-  const int h = blockIdx.x, b = blockIdx.y, c = threadIdx.x;
+__global__ __launch_bounds__(kNtAttn) void combine_kernel(const float* ws_acc, const float* ws_ml, T* out, int n_q,
+                                                          int S) {
+  constexpr int NT = kNtAttn;
+  __shared__ float wsh[NT];
+  __shared__ float red[NT / 64];
+  const int h = blockIdx.x, b = blockIdx.y, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const size_t row = (size_t)b * n_q + h;
   const float* ml = ws_ml + row * S * 2;
   const float* acc = ws_acc + row * S * HD;
-  float M = -INFINITY;
-  for (int s = 0; s < S; ++s) M = fmaxf(M, ml[2 * s]);
-  float L = 0.0f, o = 0.0f;
-  for (int s = 0; s < S; ++s) {
-    const float w = exp2f(ml[2 * s] - M);
-    L = fmaf(ml[2 * s + 1], w, L);
-    o = fmaf(acc[(size_t)s * HD + c], w, o);
+
+  float m = -INFINITY;
+  for (int s = tid; s < S; s += NT) m = fmaxf(m, ml[2 * s]);
+  m = wave_max(m);
+  if (lane == 0) red[wave] = m;
+  __syncthreads();
+  float M = red[0];
+#pragma unroll
+  for (int w = 1; w < NT / 64; ++w) M = fmaxf(M, red[w]);
+  __syncthreads();
+
+  float lsum = 0.0f, o = 0.0f;
+  for (int s0 = 0; s0 < S; s0 += NT) {
+    const int s = s0 + tid;
+    float w = 0.0f;
+    if (s < S) {
+      const float2 v = *reinterpret_cast<const float2*>(ml + 2 * s);
+      w = exp2f(v.x - M);
+      lsum = fmaf(v.y, w, lsum);
+    }
+    wsh[tid] = w;
+    __syncthreads();
+    const int cnt = min(NT, S - s0);
+    if (tid < HD) {
+      const float* ap = acc + (size_t)s0 * HD + tid;
+      int i = 0;
+      for (; i + 8 <= cnt; i += 8) {
+        float x[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) x[e] = ap[(size_t)(i + e) * HD];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) o = fmaf(x[e], wsh[i + e], o);
+      }
+      for (; i < cnt; ++i) o = fmaf(ap[(size_t)i * HD], wsh[i], o);
+    }
+    __syncthreads();
   }
-  out[row * HD + c] = from_f<T>(o / L);
+  lsum = wave_sum(lsum);
+  if (lane == 0) red[wave] = lsum;
+  __syncthreads();
+  float L = red[0];
+#pragma unroll
+  for (int w = 1; w < NT / 64; ++w) L += red[w];
+  if (tid < HD) out[row * HD + tid] = from_f<T>(o / L);
+}
+
+// ------------------------------------------------------------------ weight packing
+
+// One thread per 16-byte chunk of the packed matrix (see kvd_pack_weights).
+__global__ __launch_bounds__(256) void pack_kernel(const uint16_t* w, uint16_t* out, int rows, int d) {
+  const long long chunk = (long long)blockIdx.x * 256 + threadIdx.x;
+  const long long n = (long long)rows * d / 8;
+  if (chunk >= n) return;
+  const int l = (int)(chunk % 64);
+  const long long blk = chunk / 64;
+  const int kb = (int)(blk % (d / 16));
+  const long long rb = blk / (d / 16);
+  const uint16_t* src = w + (size_t)(rb * 32 + l % 32) * d + 16 * kb + 8 * (l / 32);
+  *reinterpret_cast<uint4*>(out + (size_t)chunk * 8) = *reinterpret_cast<const uint4*>(src);
+}
+
+hipError_t launch_pack(const void* w, void* out, int rows, int d, hipStream_t st) {
+  const long long n = (long long)rows * d / 8;
+  hipLaunchKernelGGL(pack_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, static_cast<const uint16_t*>(w),
+                     static_cast<uint16_t*>(out), rows, d);
+  return hipGetLastError();
 }
 
 // ------------------------------------------------------------------ launchers
@@ -213,38 +479,70 @@ static hipError_t set_lds(K kernel, size_t bytes) {
                              (int)bytes);
 }
 
-template <typename T, int HD>
-static hipError_t proj_t(const ProjArgs& a, dim3 grid, hipStream_t st) {
+// Raise the kernel's dynamic-LDS limit once per process (per kernel and size).
+template <typename K>
+static hipError_t ensure_lds(K kernel, size_t bytes, size_t& done) {
+  if (bytes <= done) return hipSuccess;
+  hipError_t e = set_lds(kernel, bytes);
+  if (e == hipSuccess) done = bytes;
+  return e;
+}
+
+template <typename T, int HD, bool PACKED>
+static hipError_t proj_t(const ProjArgs& a, int n_units, hipStream_t st) {
   constexpr int MT = sizeof(T) == 2 ? kMtBf16 : kMtF32;
-  constexpr size_t bytes = proj_lds<T>(HD, MT).end;
-  auto k = proj_kernel<T, HD, MT>;
-  hipError_t e = set_lds(k, bytes);
+  const size_t bytes = proj_lds<T>(HD, MT).end + gamma_lds_bytes(a.d);
+  static size_t done = 0;
+  auto k = proj_kernel<T, HD, MT, PACKED>;
+  hipError_t e = ensure_lds(k, bytes, done);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k, grid, dim3(kThreads), bytes, st, a);
+  const long long ntok = (long long)a.B * a.T;
+  const int n_tiles = (int)((ntok + MT - 1) / MT);
+  const XcdMap m = xcd_map((long long)n_units * n_tiles);
+  hipLaunchKernelGGL(k, dim3(m.grid), dim3(kNtTile), bytes, st, a, m.per, n_tiles, n_units);
   return hipGetLastError();
 }
 
-template <typename T, int HD>
-static hipError_t fused_t(const FusedArgs& a, dim3 grid, hipStream_t st) {
-  constexpr int MT = sizeof(T) == 2 ? kMtBf16 : kMtF32;
-  const size_t bytes = fused_lds_bytes<T>(a.n_q / a.n_kv, HD, MT);
-  auto k = fused_kernel<T, HD, MT>;
-  hipError_t e = set_lds(k, bytes);
+template <int HD, bool PACKED>
+static hipError_t stream_t(const ProjArgs& a, hipStream_t st) {
+  const size_t bytes = stream_lds(a.d).end;
+  static size_t done = 0;
+  auto k = stream_proj_kernel<HD, PACKED>;
+  hipError_t e = ensure_lds(k, bytes, done);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k, grid, dim3(kThreads), bytes, st, a);
+  const int qb = a.n_q * HD / 32;
+  const int kb = a.n_kv_units ? a.n_kv * HD / 32 : 0;
+  dim3 grid(qb + 2 * kb, (a.B + kProjTok - 1) / kProjTok);
+  hipLaunchKernelGGL(k, grid, dim3(64), bytes, st, a, qb, kb);
+  return hipGetLastError();
+}
+
+template <typename T, int HD, bool PACKED>
+static hipError_t fused_t(const FusedArgs& a, hipStream_t st) {
+  constexpr int MT = sizeof(T) == 2 ? kMtBf16 : kMtF32;
+  const size_t bytes = fused_lds_bytes<T>(a.n_q / a.n_kv, HD, MT) + gamma_lds_bytes(a.d);
+  static size_t done = 0;
+  auto k = fused_kernel<T, HD, MT, PACKED>;
+  hipError_t e = ensure_lds(k, bytes, done);
+  if (e != hipSuccess) return e;
+  const int n_tail = (a.T_tail + kTile - 1) / kTile;
+  const int C = a.n_rec > 0 ? a.n_rec : n_tail;
+  const XcdMap m = xcd_map((long long)a.n_kv * a.B * C);
+  hipLaunchKernelGGL(k, dim3(m.grid), dim3(kNtTile), bytes, st, a, m.per);
   return hipGetLastError();
 }
 
 template <typename T, int HD>
 static hipError_t attn_t(const AttnArgs& a, hipStream_t st) {
   const size_t bytes = decode_lds_bytes<T>(a.n_q / a.n_kv, HD);
+  static size_t done = 0;
   auto k = decode_kernel<T, HD>;
-  hipError_t e = set_lds(k, bytes);
+  hipError_t e = ensure_lds(k, bytes, done);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k, dim3(a.S, a.n_kv, a.B), dim3(kThreads), bytes, st, a);
+  hipLaunchKernelGGL(k, dim3(a.S, a.n_kv, a.B), dim3(kNtAttn), bytes, st, a);
   e = hipGetLastError();
   if (e != hipSuccess || a.out == nullptr) return e;
-  hipLaunchKernelGGL((combine_kernel<T, HD>), dim3(a.n_q, a.B), dim3(HD), 0, st, a.ws_acc, a.ws_ml,
+  hipLaunchKernelGGL((combine_kernel<T, HD>), dim3(a.n_q, a.B), dim3(kNtAttn), 0, st, a.ws_acc, a.ws_ml,
                      static_cast<T*>(a.out), a.n_q, a.S);
   return hipGetLastError();
 }
@@ -252,8 +550,8 @@ static hipError_t attn_t(const AttnArgs& a, hipStream_t st) {
 template <typename T, int HD>
 static hipError_t combine_t(const float* ws_acc, const float* ws_ml, void* out, int n_q, int B, int S,
                             hipStream_t st) {
-  hipLaunchKernelGGL((combine_kernel<T, HD>), dim3(n_q, B), dim3(HD), 0, st, ws_acc, ws_ml, static_cast<T*>(out),
-                     n_q, S);
+  hipLaunchKernelGGL((combine_kernel<T, HD>), dim3(n_q, B), dim3(kNtAttn), 0, st, ws_acc, ws_ml,
+                     static_cast<T*>(out), n_q, S);
   return hipGetLastError();
 }
 
@@ -269,22 +567,29 @@ static hipError_t combine_t(const float* ws_acc, const float* ws_ml, void* out, 
       return hipErrorInvalidValue;                         \
   }
 
-hipError_t launch_proj(const ProjArgs& a, int dtype_bf16, int hd, int n_units, hipStream_t st) {
-  const int MT = dtype_bf16 ? kMtBf16 : kMtF32;
-  const long long ntok = (long long)a.B * a.T;
-  dim3 grid((unsigned)((ntok + MT - 1) / MT), (unsigned)n_units);
-#define PB(H) proj_t<uint16_t, H>(a, grid, st)
-#define PF(H) proj_t<float, H>(a, grid, st)
+hipError_t launch_proj(const ProjArgs& a, int dtype_bf16, int hd, int packed, int n_units, hipStream_t st) {
+#define PB(H) (packed ? proj_t<uint16_t, H, true>(a, n_units, st) : proj_t<uint16_t, H, false>(a, n_units, st))
+#define PF(H) proj_t<float, H, false>(a, n_units, st)
   KVD_DISPATCH(dtype_bf16, hd, PB, PF)
 #undef PB
 #undef PF
 }
 
-hipError_t launch_fused(const FusedArgs& a, int dtype_bf16, int hd, hipStream_t st) {
-  dim3 grid((unsigned)a.S, (unsigned)a.n_kv, (unsigned)a.B);
+hipError_t launch_project_current(const ProjArgs& a, int dtype_bf16, int hd, int packed, int n_units,
+                                  hipStream_t st) {
+  if (!dtype_bf16) return launch_proj(a, 0, hd, 0, n_units, st);
+  switch (hd) {
+    case 64: return packed ? stream_t<64, true>(a, st) : stream_t<64, false>(a, st);
+    case 128: return packed ? stream_t<128, true>(a, st) : stream_t<128, false>(a, st);
+    case 256: return packed ? stream_t<256, true>(a, st) : stream_t<256, false>(a, st);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+hipError_t launch_fused(const FusedArgs& a, int dtype_bf16, int hd, int packed, hipStream_t st) {
   hipError_t e;
-#define FB(H) fused_t<uint16_t, H>(a, grid, st)
-#define FF(H) fused_t<float, H>(a, grid, st)
+#define FB(H) (packed ? fused_t<uint16_t, H, true>(a, st) : fused_t<uint16_t, H, false>(a, st))
+#define FF(H) fused_t<float, H, false>(a, st)
   e = [&]() -> hipError_t { KVD_DISPATCH(dtype_bf16, hd, FB, FF) }();
 #undef FB
 #undef FF

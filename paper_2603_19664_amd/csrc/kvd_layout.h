@@ -6,15 +6,23 @@
 
 namespace kvd {
 
-constexpr int kThreads = 256;   // every kernel: 4 wave64 waves
+constexpr int kNtTile = 512;    // threads of the recompute / fused kernels (8 wave64 waves)
+constexpr int kNtAttn = 256;    // threads of the stored-K/V attention and combine kernels
+constexpr int kAttnTasks = 256; // fixed task split of the attention arithmetic (independent of thread count)
 constexpr int kKT = 64;         // d-elements per K-step of the projection GEMM
 constexpr int kTile = 64;       // keys per attention tile (one split-K partial)
 constexpr int kMaxGroup = 16;   // max query heads per KV head
 constexpr int kMaxPairs = 128;  // head_dim / 2 for head_dim <= 256
+constexpr int kXcds = 8;        // MI355X: workgroups are dispatched round-robin over 8 XCDs
+constexpr int kDepth = 4;       // K-steps of weights / residuals in flight in the recompute GEMM
 
-// Tokens per workgroup of the projection engines.
+// Tokens per workgroup of the recompute engines.
 constexpr int kMtBf16 = 64;
 constexpr int kMtF32 = 64;
+
+// Streaming projection (current-token q/K/V): tokens per workgroup.
+constexpr int kProjTok = 16;
+constexpr int kProjPrefetch = 8;  // K-steps of weights in flight per wave
 
 constexpr size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
@@ -47,8 +55,9 @@ constexpr AttnLds attn_lds(size_t base, int g, int hd, int rows) {
   return L;
 }
 
-// LDS layout of the projection engine: staged h-bar tiles (2 buffers), the
-// K/V tile, and per-token 1/rms and positions, plus the RoPE frequency table.
+// LDS layout of the recompute engine: staged h-bar tiles (2 buffers), the
+// K/V tile (aliases the staging buffers), per-token 1/rms and positions, and
+// the RoPE frequency table.
 struct ProjLds {
   size_t hst, kv, rinv, pos, rev, end;
 };
@@ -60,11 +69,14 @@ constexpr ProjLds proj_lds(int hd, int mt) {
   L.pos = align_up(L.rinv + sizeof(float) * mt, 16);                // int[mt]
   L.hst = align_up(L.pos + sizeof(int) * mt, 16);                   // T[2][mt][h_ld]
   size_t hst_end = L.hst + sizeof(T) * 2 * mt * h_ld<T>();
-  L.kv = align_up(L.pos + sizeof(int) * mt, 16);                    // T[mt][kv_ld] (aliases hst)
+  L.kv = L.hst;                                                     // T[mt][kv_ld]
   size_t kv_end = L.kv + sizeof(T) * mt * kv_ld<T>(hd);
   L.end = align_up(hst_end > kv_end ? hst_end : kv_end, 16);
   return L;
 }
+
+// gamma (bf16, [d]) of the bf16 recompute engine sits after a kernel's other LDS.
+constexpr size_t gamma_lds_bytes(int d) { return align_up((size_t)2 * d, 16); }
 
 template <typename T>
 constexpr size_t decode_lds_bytes(int g, int hd) {
@@ -75,6 +87,36 @@ constexpr size_t decode_lds_bytes(int g, int hd) {
 template <typename T>
 constexpr size_t fused_lds_bytes(int g, int hd, int mt) {
   return attn_lds(proj_lds<T>(hd, mt).end, g, hd, mt).end;
+}
+
+// Streaming projection: h-bar of kProjTok tokens for the whole d, plus 1/rms,
+// positions and the RoPE table.
+struct StreamLds {
+  size_t rev, rinv, pos, hb, end;
+};
+constexpr int stream_h_ld(int d) { return d + 8; }
+constexpr StreamLds stream_lds(int d) {
+  StreamLds L{};
+  L.rev = 0;
+  L.rinv = align_up(L.rev + sizeof(double) * kMaxPairs, 16);
+  L.pos = align_up(L.rinv + sizeof(float) * kProjTok, 16);
+  L.hb = align_up(L.pos + sizeof(int) * kProjTok, 16);
+  L.end = align_up(L.hb + sizeof(uint16_t) * kProjTok * stream_h_ld(d), 16);
+  return L;
+}
+
+// Workgroup -> work item remap that keeps the items of one XCD contiguous:
+// hardware dispatch sends workgroup w to XCD w % 8, so XCD x runs items
+// x*per .. x*per+per-1, and units that share weights land on the same L2.
+struct XcdMap {
+  int per;    // items per XCD
+  int grid;   // workgroups to launch (kXcds * per)
+};
+constexpr XcdMap xcd_map(long long n_items) {
+  XcdMap m{};
+  m.per = (int)((n_items + kXcds - 1) / kXcds);
+  m.grid = kXcds * m.per;
+  return m;
 }
 
 }  // namespace kvd

@@ -9,6 +9,7 @@ is no fallback.  Importing this module fails loudly if libkvd.so is not built.
 from __future__ import annotations
 
 import ctypes
+import dataclasses
 import os
 import re
 from dataclasses import dataclass
@@ -21,6 +22,7 @@ HEADER_PATH = os.path.join(os.path.dirname(_PKG), "include", "kvd.h")
 
 KVD_OK, KVD_ERR_NULL, KVD_ERR_SHAPE, KVD_ERR_UNSUPPORTED, KVD_ERR_WORKSPACE, KVD_ERR_ALIGN, KVD_ERR_DEVICE = range(7)
 KVD_F32, KVD_BF16 = 0, 1
+KVD_W_ROWMAJOR, KVD_W_PACKED = 0, 1
 KVD_OP_DECODE_ATTN, KVD_OP_CACHED_ATTN, KVD_OP_FUSED = 0, 1, 2
 
 _DTYPES = {KVD_F32: torch.float32, KVD_BF16: torch.bfloat16}
@@ -41,6 +43,7 @@ class AttnShape(ctypes.Structure):
         ("rms_eps", ctypes.c_float),
         ("rope_theta", ctypes.c_double),
         ("dtype", ctypes.c_int32),
+        ("w_layout", ctypes.c_int32),
     ]
 
 
@@ -66,6 +69,8 @@ def _load() -> ctypes.CDLL:
         f = getattr(lib, name)
         f.argtypes = args
         f.restype = ctypes.c_int
+    lib.kvd_pack_weights.argtypes = [S, VP, I32, VP, VP]
+    lib.kvd_pack_weights.restype = ctypes.c_int
     lib.kvd_combine.argtypes = [S, I32, I32, VP, SZ, VP, VP]
     lib.kvd_combine.restype = ctypes.c_int
     lib.kvd_workspace_bytes.argtypes = [S, I32, I32, I32, I32]
@@ -114,6 +119,7 @@ class Shape:
     rms_eps: float
     rope_theta: float
     dtype: int
+    w_layout: int = KVD_W_ROWMAJOR
 
     @property
     def torch_dtype(self) -> torch.dtype:
@@ -121,7 +127,11 @@ class Shape:
 
     def c(self) -> AttnShape:
         return AttnShape(self.d_model, self.n_q_heads, self.n_kv_heads, self.head_dim, self.rms_eps,
-                         self.rope_theta, self.dtype)
+                         self.rope_theta, self.dtype, self.w_layout)
+
+    def packed(self) -> "Shape":
+        """The same shape with weights in the packed MFMA layout (kvd_pack_weights)."""
+        return dataclasses.replace(self, w_layout=KVD_W_PACKED)
 
 
 def shape_of(wl) -> Shape:
@@ -200,6 +210,14 @@ def _attn(fn, shape, q, k, v, T, out, ws, t_off):
     view = _view(k, v, t_off, "kv", dt)
     _check(fn(ctypes.byref(shape.c()), _ptr(q, "q", dt, 3), ctypes.byref(view), q.shape[0], T,
               _ptr(out, "out", dt, 3), _ptr(ws, "ws"), ws.numel() * ws.element_size(), _stream()))
+
+
+def kvd_pack_weights(shape: Shape, w):
+    """A packed copy (MFMA operand order) of a row-major [rows, d_model] bf16 weight matrix."""
+    out = torch.empty_like(w)
+    _check(lib.kvd_pack_weights(ctypes.byref(shape.c()), _ptr(w, "w", torch.bfloat16, 2), w.shape[0],
+                                _ptr(out, "packed", torch.bfloat16, 2), _stream()))
+    return out
 
 
 def kvd_combine(shape: Shape, B: int, S: int, ws, out):

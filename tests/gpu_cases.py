@@ -44,17 +44,29 @@ class Layer:
     w_v: torch.Tensor
     pos0: torch.Tensor      # [B] int32 (device)
     pos_new: torch.Tensor   # [B] int32 (device) = pos0 + T
+    lw_q: torch.Tensor = None   # the weights as the library receives them (packed or row-major)
+    lw_k: torch.Tensor = None
+    lw_v: torch.Tensor = None
 
 
-def make_layer(wl, B, T, seed=0, layer=0, w_q_std=None, pos0=None, t_cap=None, **over) -> Layer:
+def make_layer(wl, B, T, seed=0, layer=0, w_q_std=None, pos0=None, t_cap=None, packed=None, **over) -> Layer:
+    """Seeded inputs of one layer.  bf16 weights go to the library in the packed MFMA
+    layout unless packed=False (the oracle always gets the row-major values)."""
     if over:
         wl = dataclasses.replace(wl, **over)
     dev = "cuda"
     gamma, w_q, w_k, w_v = inputs.weights(wl, layer, seed, dev, w_std=w_q_std)
     h, h_new = inputs.residuals(wl, layer, B, T, seed, dev, t_cap=t_cap)
     p0 = inputs.positions(wl, B, seed) if pos0 is None else torch.as_tensor(pos0, dtype=torch.int32)
-    return Layer(wl, kvd.shape_of(wl), B, T, h, h_new, gamma, w_q, w_k, w_v, p0.to(dev),
-                 (p0 + T).to(torch.int32).to(dev))
+    shape = kvd.shape_of(wl)
+    if packed is None:
+        packed = shape.dtype == kvd.KVD_BF16
+    lw = (w_q, w_k, w_v)
+    if packed:
+        shape = shape.packed()
+        lw = tuple(kvd.kvd_pack_weights(shape, w) for w in lw)
+    return Layer(wl, shape, B, T, h, h_new, gamma, w_q, w_k, w_v, p0.to(dev), (p0 + T).to(torch.int32).to(dev),
+                 *lw)
 
 
 def empty_kv(L: Layer, t_cap: int):
@@ -67,7 +79,7 @@ def empty_kv(L: Layer, t_cap: int):
 
 def gpu_recompute(L: Layer, t_cap=None, t_off=0):
     K, V = empty_kv(L, t_cap or (L.T + t_off))
-    kvd.kvd_recompute_kv(L.shape, L.h, L.gamma, L.w_k, L.w_v, L.pos0, L.T, K, V, t_off)
+    kvd.kvd_recompute_kv(L.shape, L.h, L.gamma, L.lw_k, L.lw_v, L.pos0, L.T, K, V, t_off)
     return K, V
 
 
@@ -75,7 +87,7 @@ def gpu_project(L: Layer, kv=None, t_off=0):
     s = L.shape
     q = torch.empty((L.B, s.n_q_heads, s.head_dim), dtype=s.torch_dtype, device="cuda")
     k, v = kv if kv is not None else (None, None)
-    kvd.kvd_project_qkv(s, L.h_new, L.gamma, L.w_q, L.w_k, L.w_v, L.pos_new, q, k, v, t_off)
+    kvd.kvd_project_qkv(s, L.h_new, L.gamma, L.lw_q, L.lw_k, L.lw_v, L.pos_new, q, k, v, t_off)
     return q
 
 
@@ -102,7 +114,7 @@ def gpu_fused(L: Layer, q=None, kv_debug=False, with_current=True):
     dk = dv = None
     if kv_debug:
         dk, dv = empty_kv(L, max(L.T, 1))
-    kvd.kvd_fused_recompute_attn(s, q, L.h, L.T, L.gamma, L.w_k, L.w_v, L.pos0, out, ws,
+    kvd.kvd_fused_recompute_attn(s, q, L.h, L.T, L.gamma, L.lw_k, L.lw_v, L.pos0, out, ws,
                                  tk if with_current else None, tv if with_current else None, T_tail, 0, dk, dv, 0)
     return q, (tk, tv), out, (dk, dv)
 

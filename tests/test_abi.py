@@ -24,7 +24,7 @@ def view(t_cap=16, t_off=0, k=FAKE, v=FAKE):
 
 
 def test_loads_and_version():
-    assert kvd.abi_version() == 1
+    assert kvd.abi_version() == 2
     assert kvd.status_str(kvd.KVD_ERR_ALIGN) == "KVD_ERR_ALIGN"
 
 
@@ -154,3 +154,22 @@ def test_combine_validation():
     assert f(ctypes.byref(s), 1, 4, FAKE, 1 << 30, None, None) == kvd.KVD_ERR_NULL
     assert f(ctypes.byref(s), 1, 4, FAKE, 64, FAKE, None) == kvd.KVD_ERR_WORKSPACE
     assert f(ctypes.byref(s), 1, 4, FAKE + 64, 1 << 30, FAKE, None) == kvd.KVD_ERR_ALIGN
+
+
+def test_lds_limit_of_projection_is_validated():
+    # the current-token projection stages d_model * 16 bf16 values in LDS
+    s = shape(d_model=8192)
+    f = lib.kvd_project_qkv
+    assert f(ctypes.byref(s), FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 1, FAKE, None, None) == kvd.KVD_ERR_UNSUPPORTED
+    assert "LDS" in kvd.last_error()
+
+
+def test_weight_layout_validation():
+    assert recompute(shape(w_layout=5)) == kvd.KVD_ERR_UNSUPPORTED
+    assert recompute(shape(w_layout=kvd.KVD_W_PACKED, dtype=kvd.KVD_F32)) == kvd.KVD_ERR_UNSUPPORTED
+    f = lib.kvd_pack_weights
+    s = shape()
+    assert f(ctypes.byref(s), FAKE, 48, FAKE + (1 << 24), None) == kvd.KVD_ERR_SHAPE       # rows % 32
+    assert f(ctypes.byref(s), FAKE, 64, FAKE + 4096, None) == kvd.KVD_ERR_SHAPE            # overlap
+    assert f(ctypes.byref(s), None, 64, FAKE, None) == kvd.KVD_ERR_NULL
+    assert f(ctypes.byref(shape(dtype=kvd.KVD_F32)), FAKE, 64, FAKE + (1 << 24), None) == kvd.KVD_ERR_UNSUPPORTED

@@ -244,7 +244,7 @@ def test_partials_then_combine_equals_one_call():
     q, (tk, tv), out1, _ = gpu_fused(L)
     s = L.shape
     ws = kvd.workspace(s, kvd.KVD_OP_FUSED, L.B, L.T, 1)
-    kvd.kvd_fused_recompute_attn(s, q, L.h, L.T, L.gamma, L.w_k, L.w_v, L.pos0, None, ws, tk, tv, 1)
+    kvd.kvd_fused_recompute_attn(s, q, L.h, L.T, L.gamma, L.lw_k, L.lw_v, L.pos0, None, ws, tk, tv, 1)
     out2 = torch.empty_like(out1)
     kvd.kvd_combine(s, L.B, kvd.kvd_num_splits(s, kvd.KVD_OP_FUSED, L.B, L.T, 1), ws, out2)
     assert torch.equal(_bits(out1), _bits(out2))
@@ -254,3 +254,19 @@ def test_partials_then_combine_equals_one_call():
     out3 = torch.empty_like(outd)
     kvd.kvd_combine(s, L.B, kvd.kvd_num_splits(s, kvd.KVD_OP_DECODE_ATTN, L.B, L.T + 1), wsd, out3)
     assert torch.equal(_bits(outd), _bits(out3))
+
+
+@pytest.mark.parametrize("hd", [64, 128, 256])
+def test_packed_weights_bitwise_equal_rowmajor(hd):
+    # the packed MFMA layout holds the same values and feeds the same arithmetic
+    kw = dict(B=2, T=150, seed=26, d_model=512, n_q=4, n_kv=2, head_dim=hd, pos0=[3, 700])
+    Lr = make_layer(C.GEMMA3_4B, packed=False, **kw)
+    Lp = make_layer(C.GEMMA3_4B, packed=True, **kw)
+    assert Lp.shape.w_layout == kvd.KVD_W_PACKED and not torch.equal(Lp.lw_k, Lp.w_k)
+    for a, b in zip(gpu_recompute(Lr), gpu_recompute(Lp)):
+        assert torch.equal(_bits(a), _bits(b))
+    qr, (tkr, tvr), outr, (dkr, dvr) = gpu_fused(Lr, kv_debug=True)
+    qp, (tkp, tvp), outp, (dkp, dvp) = gpu_fused(Lp, kv_debug=True)
+    for a, b in [(qr, qp), (tkr, tkp), (tvr, tvp), (outr, outp), (dkr, dkp), (dvr, dvp)]:
+        assert torch.equal(_bits(a), _bits(b))
+    check("out fused (row-major weights)", outr, oracle_decode(Lr), 2e-2)
