@@ -266,8 +266,18 @@ struct MfmaTile {
       }
     };
     // one iteration: consume step s from slot U, refill slot U with step s + D,
-    // stage step s + 1 (slot (U + 1) % D) into the other LDS buffer.
-    auto iter = [&](auto slot_c, int s) {
+    // stage step s + 1 (slot (U + 1) % D) into the other LDS buffer.  The steady
+    // state issues its loads unconditionally so that the compiler can count the
+    // loads in flight across the loop back-edge (a conditional refill makes it
+    // drain the whole ring at every trip).
+    auto iter_full = [&](auto slot_c, int s) {
+      constexpr int U = decltype(slot_c)::value;
+      compute(slot_c, IC<U & 1>{});
+      load_step(slot_c, s + D);
+      stage(IC<(U + 1) % D>{}, s + 1, (U + 1) & 1);
+      __syncthreads();
+    };
+    auto iter_tail = [&](auto slot_c, int s) {
       constexpr int U = decltype(slot_c)::value;
       compute(slot_c, IC<U & 1>{});
       if (s + D < nsteps) load_step(slot_c, s + D);
@@ -275,18 +285,25 @@ struct MfmaTile {
       __syncthreads();
     };
 
-    static_assert(D == 4, "the unrolled loop below assumes four slots");
+    static_assert(D == 4, "the unrolled loops below assume four slots");
     load_step(IC<0>{}, 0);
-    if (1 < nsteps) load_step(IC<1>{}, 1);
-    if (2 < nsteps) load_step(IC<2>{}, 2);
-    if (3 < nsteps) load_step(IC<3>{}, 3);
+    load_step(IC<1>{}, min(1, nsteps - 1));
+    load_step(IC<2>{}, min(2, nsteps - 1));
+    load_step(IC<3>{}, min(3, nsteps - 1));
     stage(IC<0>{}, 0, 0);
     __syncthreads();
-    for (int s0 = 0; s0 < nsteps; s0 += D) {
-      iter(IC<0>{}, s0);
-      if (s0 + 1 < nsteps) iter(IC<1>{}, s0 + 1);
-      if (s0 + 2 < nsteps) iter(IC<2>{}, s0 + 2);
-      if (s0 + 3 < nsteps) iter(IC<3>{}, s0 + 3);
+    int s0 = 0;
+    for (; s0 + 2 * D <= nsteps; s0 += D) {
+      iter_full(IC<0>{}, s0);
+      iter_full(IC<1>{}, s0 + 1);
+      iter_full(IC<2>{}, s0 + 2);
+      iter_full(IC<3>{}, s0 + 3);
+    }
+    for (; s0 < nsteps; s0 += D) {
+      iter_tail(IC<0>{}, s0);
+      if (s0 + 1 < nsteps) iter_tail(IC<1>{}, s0 + 1);
+      if (s0 + 2 < nsteps) iter_tail(IC<2>{}, s0 + 2);
+      if (s0 + 3 < nsteps) iter_tail(IC<3>{}, s0 + 3);
     }
 
     finish_rms<NT, CPT>(ss, valid, d, eps, rinv);

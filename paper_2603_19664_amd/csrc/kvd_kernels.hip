@@ -219,16 +219,30 @@ __global__ __launch_bounds__(64) void stream_proj_kernel(ProjArgs a, int q_block
   bf16x8_t zero;
 #pragma unroll
   for (int i = 0; i < 8; ++i) zero[i] = (__bf16)0.0f;
-  for (int s0 = 0; s0 < nsteps; s0 += PD) {
+  auto consume = [&](int u, int s) {
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const bf16x8_t bv = col_ok ? *reinterpret_cast<const bf16x8_t*>(hcol + (size_t)s * kKT + 16 * k) : zero;
+      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ring[u][k], bv, acc, 0, 0, 0);
+    }
+  };
+  // steady state: unconditional refills keep PD K-steps in flight across the back-edge
+  int s0 = 0;
+  for (; s0 + 2 * PD <= nsteps; s0 += PD) {
+#pragma unroll
+    for (int u = 0; u < PD; ++u) {
+      consume(u, s0 + u);
+#pragma unroll
+      for (int k = 0; k < 4; ++k)
+        ring[u][k] = *reinterpret_cast<const bf16x8_t*>(wrow + w_off<PACKED>(s0 + u + PD, k));
+    }
+  }
+  for (; s0 < nsteps; s0 += PD) {
 #pragma unroll
     for (int u = 0; u < PD; ++u) {
       const int s = s0 + u;
       if (s < nsteps) {
-#pragma unroll
-        for (int k = 0; k < 4; ++k) {
-          const bf16x8_t bv = col_ok ? *reinterpret_cast<const bf16x8_t*>(hcol + (size_t)s * kKT + 16 * k) : zero;
-          acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ring[u][k], bv, acc, 0, 0, 0);
-        }
+        consume(u, s);
         if (s + PD < nsteps) {
 #pragma unroll
           for (int k = 0; k < 4; ++k)
