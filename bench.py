@@ -46,6 +46,8 @@ def parse():
     p.add_argument("--no-baselines", action="store_true", help="skip the cached / unfused per-op timings")
     p.add_argument("--cpu-seconds", type=float, default=12.0, help="CPU oracle time budget")
     p.add_argument("--sweep-batches", default="1,2,4,8,16,32,64")
+    p.add_argument("--calibration-copy-mib", type=int, default=256,
+                   help="size of one untimed device-to-device copy whose HBM counters calibrate the traffic figure")
     return p.parse_args()
 
 
@@ -136,6 +138,16 @@ def main():
             if events is not None:
                 events[i][l][1].record()
             comb[l]()
+
+    # one plain copy of known size (untimed): its FETCH_SIZE / WRITE_SIZE in a
+    # counter run scale the fused kernel's counters to bytes
+    if args.calibration_copy_mib > 0:
+        src = torch.empty(args.calibration_copy_mib << 20, dtype=torch.uint8, device=dev).fill_(1)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
 
     # ---------------------------------------------------------------- timed region
     K, W = args.steps, args.warmup
