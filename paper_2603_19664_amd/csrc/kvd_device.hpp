@@ -30,6 +30,7 @@ namespace kvd {
 
 typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8_t;
 typedef __attribute__((__vector_size__(16 * sizeof(float)))) float f32x16_t;
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 
 template <int N> struct IC { static constexpr int value = N; };
 
@@ -113,6 +114,26 @@ __device__ __forceinline__ uint4 stage_chunk_bf16(uint4 hv, uint4 gv, float& ss)
     ss = fmaf(h1, h1, ss);
     o[i] = pack_bf16x2(h0 * bf_lo(gw[i]), h1 * bf_hi(gw[i]));
   }
+  return make_uint4(o[0], o[1], o[2], o[3]);
+}
+
+// The two halves of stage_chunk_bf16, with the same arithmetic: the sum of squares
+// of one chunk in element order, and bf16(h * gamma) of one chunk.
+__device__ __forceinline__ void sumsq_chunk_bf16(uint4 hv, float& ss) {
+  const uint32_t hw[4] = {hv.x, hv.y, hv.z, hv.w};
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const float h0 = bf_lo(hw[i]), h1 = bf_hi(hw[i]);
+    ss = fmaf(h0, h0, ss);
+    ss = fmaf(h1, h1, ss);
+  }
+}
+__device__ __forceinline__ uint4 scale_chunk_bf16(uint4 hv, uint4 gv) {
+  const uint32_t hw[4] = {hv.x, hv.y, hv.z, hv.w};
+  const uint32_t gw[4] = {gv.x, gv.y, gv.z, gv.w};
+  uint32_t o[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) o[i] = pack_bf16x2(bf_lo(hw[i]) * bf_lo(gw[i]), bf_hi(hw[i]) * bf_hi(gw[i]));
   return make_uint4(o[0], o[1], o[2], o[3]);
 }
 

@@ -126,7 +126,7 @@ __global__ __launch_bounds__(kNtTile, 1) void proj_kernel(ProjArgs a, int per_xc
 // weight rows with kProjPrefetch K-steps in flight.  Per output element the
 // arithmetic is MfmaTile's (same MFMA chain over d, same 1/rms, same epilogue),
 // so K_t / V_t equal what recompute gives for the same row.
-template <int HD, bool PACKED>
+template <int HD, bool PACKED, int NS>
 __global__ __launch_bounds__(64) void stream_proj_kernel(ProjArgs a, int q_blocks, int k_blocks) {
   extern __shared__ __align__(16) char lds[];
   constexpr int PD = kProjPrefetch;
@@ -152,43 +152,78 @@ __global__ __launch_bounds__(64) void stream_proj_kernel(ProjArgs a, int q_block
     W = static_cast<const uint16_t*>(a.w_v); row0 = 32 * (blk - q_blocks - k_blocks); rope = 0; mat = 2;
   }
 
-  for (int i = lane; i < HD / 2; i += 64) rev[i] = a.rev[i];
-  for (int r = lane; r < kProjTok; r += 64) pos[r] = r < nt ? a.pos0[b0 + r] : 0;
+  const uint16_t* wrow = PACKED ? W + (size_t)row0 * d + 8 * lane : W + (size_t)(row0 + (lane & 31)) * d + 8 * (lane >> 5);
+  const int nsteps = NS > 0 ? NS : d / kKT;  // NS > 0: K-step count fixed at compile time (straight-line loop)
+  bf16x8_t ring[PD][4];
 
-  // stage gamma * h (bf16) and the sum of squares: lane -> rows (lane>>3) + 8r, column chunk sub
+  // Stage the group's raw residual rows and gamma into LDS with every lane and
+  // all loads of a batch in flight, then form gamma * h (bf16) and the sums of
+  // squares in place: lane -> rows (lane>>3) + 8r, column chunk sub, K-steps in
+  // order (the same per-element arithmetic and summation order as the tile engine).
+  uint16_t* gl = reinterpret_cast<uint16_t*>(lds + SL.gam);
   {
-    const int nsteps = d / kKT;
-    const uint16_t* g = static_cast<const uint16_t*>(a.gamma) + 8 * sub;
-    const uint16_t* hr[2];
-    bool ok[2];
+    const int cpr = d / 8;                 // 16-byte chunks per row
+    const int n_h = nt * cpr, total = n_h + cpr;
+    // chunk i of [rows of present tokens | gamma]; lanes past the end repeat the last chunk
+    struct Chunk { const uint16_t* src; uint16_t* dst; };
+    auto locate = [&](int i) {
+      i = min(i, total - 1);
+      const int r = i / cpr, ch = i - r * cpr;  // gamma chunks: r == nt, ch == i - n_h
+      const bool is_h = r < nt;
+      return Chunk{is_h ? static_cast<const uint16_t*>(a.h) + (size_t)(b0 + r) * d + 8 * ch
+                        : static_cast<const uint16_t*>(a.gamma) + 8 * ch,
+                   is_h ? hb + (size_t)r * HLD + 8 * ch : gl + 8 * ch};
+    };
+    // first batch, then the weight ring's first PD K-steps (independent of the
+    // residuals; issued after the batch so that waiting for the batch does not
+    // wait for them), then the rest
+    constexpr int B0 = 10, BATCH = 8;
+    {
+      u32x4_t v[B0];
+#pragma unroll
+      for (int k = 0; k < B0; ++k) v[k] = *reinterpret_cast<const u32x4_t*>(locate(64 * k + lane).src);
+#pragma unroll
+      for (int u = 0; u < PD; ++u)
+#pragma unroll
+        for (int k = 0; k < 4; ++k)
+          ring[u][k] = *reinterpret_cast<const bf16x8_t*>(wrow + w_off<PACKED>(min(u, nsteps - 1), k));
+#pragma unroll
+      for (int k = 0; k < B0; ++k) *reinterpret_cast<u32x4_t*>(locate(64 * k + lane).dst) = v[k];
+    }
+    for (int i0 = 64 * B0; i0 < total; i0 += 64 * BATCH) {
+      u32x4_t v[BATCH];
+#pragma unroll
+      for (int k = 0; k < BATCH; ++k) v[k] = *reinterpret_cast<const u32x4_t*>(locate(i0 + 64 * k + lane).src);
+#pragma unroll
+      for (int k = 0; k < BATCH; ++k) *reinterpret_cast<u32x4_t*>(locate(i0 + 64 * k + lane).dst) = v[k];
+      // all of the batch's loads before its LDS writes
+      __builtin_amdgcn_sched_group_barrier(0x020, BATCH, 0);
+      __builtin_amdgcn_sched_group_barrier(0x200, BATCH, 0);
+    }
+    __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): the wave's own LDS writes are done
+    // sums of squares: lane -> rows (lane>>3) + 8r of present tokens, column chunk sub,
+    // K-steps in order (the tile engine's per-thread chain), read from the raw rows
     float ss[2] = {0.0f, 0.0f};
+    const uint16_t* hrow0 = hb + (size_t)(lane >> 3) * HLD + 8 * sub;
 #pragma unroll
     for (int r = 0; r < 2; ++r) {
-      const int row = (lane >> 3) + 8 * r;
-      ok[r] = row < nt;
-      hr[r] = static_cast<const uint16_t*>(a.h) + (size_t)(b0 + (ok[r] ? row : 0)) * d + 8 * sub;
-    }
-    for (int s0 = 0; s0 < nsteps; s0 += 4) {
-      uint4 hv[4][2], gv[4];
+      if ((lane >> 3) + 8 * r < nt) {
+        const uint16_t* hr = hrow0 + (size_t)(8 * r) * HLD;
+        for (int s0 = 0; s0 < nsteps; s0 += 8) {
+          uint4 x[8];
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const int s = min(s0 + u, nsteps - 1);
-        gv[u] = *reinterpret_cast<const uint4*>(g + (size_t)s * kKT);
+          for (int j = 0; j < 8; ++j) x[j] = *reinterpret_cast<const uint4*>(hr + (size_t)min(s0 + j, nsteps - 1) * kKT);
 #pragma unroll
-        for (int r = 0; r < 2; ++r) hv[u][r] = *reinterpret_cast<const uint4*>(hr[r] + (size_t)s * kKT);
-      }
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const int s = s0 + u;
-        if (s < nsteps) {
-#pragma unroll
-          for (int r = 0; r < 2; ++r) {
-            const uint4 x = ok[r] ? hv[u][r] : make_uint4(0, 0, 0, 0);
-            const uint4 o = stage_chunk_bf16(x, gv[u], ss[r]);
-            *reinterpret_cast<uint4*>(hb + (size_t)((lane >> 3) + 8 * r) * HLD + (size_t)s * kKT + 8 * sub) = o;
-          }
+          for (int j = 0; j < 8; ++j)
+            if (s0 + j < nsteps) sumsq_chunk_bf16(x[j], ss[r]);
         }
       }
+    }
+    // gamma * h -> bf16 in place, spread over all lanes (present rows only)
+    for (int i = lane; i < n_h; i += 64) {
+      const int r = i / cpr, ch = i - r * cpr;
+      uint4* ptr = reinterpret_cast<uint4*>(hb + (size_t)r * HLD + 8 * ch);
+      *ptr = scale_chunk_bf16(*ptr, *reinterpret_cast<const uint4*>(gl + 8 * ch));
     }
 #pragma unroll
     for (int r = 0; r < 2; ++r) {
@@ -196,36 +231,49 @@ __global__ __launch_bounds__(64) void stream_proj_kernel(ProjArgs a, int q_block
       v += __shfl_xor(v, 1, 64);
       v += __shfl_xor(v, 2, 64);
       v += __shfl_xor(v, 4, 64);
-      if (sub == 0) rinv[(lane >> 3) + 8 * r] = ok[r] ? 1.0f / sqrtf(v / (float)d + a.eps) : 0.0f;
+      const int row = (lane >> 3) + 8 * r;
+      if (sub == 0) rinv[row] = row < nt ? 1.0f / sqrtf(v / (float)d + a.eps) : 0.0f;
     }
   }
+  for (int i = lane; i < HD / 2; i += 64) rev[i] = a.rev[i];
+  for (int r = lane; r < kProjTok; r += 64) pos[r] = r < nt ? a.pos0[b0 + r] : 0;
   __syncthreads();
 
-  // MFMA over d: A = 32 weight rows, B = the group's tokens (columns >= kProjTok are zero)
-  const uint16_t* wrow = PACKED ? W + (size_t)row0 * d + 8 * lane : W + (size_t)(row0 + (lane & 31)) * d + 8 * (lane >> 5);
+  // MFMA over d: A = 32 weight rows, B = the group's tokens.  Columns >= kProjTok
+  // repeat columns col - kProjTok and columns of absent tokens hold unused values:
+  // MFMA output columns are independent and only those of present tokens are stored.
   const int col = lane & 31;
-  const bool col_ok = col < kProjTok;
-  const uint16_t* hcol = hb + (size_t)(col_ok ? col : 0) * HLD + 8 * (lane >> 5);
-  const int nsteps = d / kKT;
+  const uint16_t* hcol = hb + (size_t)(col % kProjTok) * HLD + 8 * (lane >> 5);
   f32x16_t acc;
 #pragma unroll
   for (int i = 0; i < 16; ++i) acc[i] = 0.0f;
-  bf16x8_t ring[PD][4];
+  // B fragments of the next K-step are read while the current step's MFMAs run.
+  bf16x8_t bcur[4], bnxt[4];
+  auto read_b = [&](bf16x8_t (&bv)[4], int s) {
 #pragma unroll
-  for (int u = 0; u < PD; ++u)
-#pragma unroll
-    for (int k = 0; k < 4; ++k)
-      ring[u][k] = *reinterpret_cast<const bf16x8_t*>(wrow + w_off<PACKED>(min(u, nsteps - 1), k));
-  bf16x8_t zero;
-#pragma unroll
-  for (int i = 0; i < 8; ++i) zero[i] = (__bf16)0.0f;
-  auto consume = [&](int u, int s) {
-#pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      const bf16x8_t bv = col_ok ? *reinterpret_cast<const bf16x8_t*>(hcol + (size_t)s * kKT + 16 * k) : zero;
-      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ring[u][k], bv, acc, 0, 0, 0);
-    }
+    for (int k = 0; k < 4; ++k) bv[k] = *reinterpret_cast<const bf16x8_t*>(hcol + (size_t)s * kKT + 16 * k);
   };
+  auto consume = [&](int u, int s) {
+    read_b(bnxt, min(s + 1, nsteps - 1));
+#pragma unroll
+    for (int k = 0; k < 4; ++k) acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ring[u][k], bcur[k], acc, 0, 0, 0);
+#pragma unroll
+    for (int k = 0; k < 4; ++k) bcur[k] = bnxt[k];
+  };
+  read_b(bcur, 0);
+  if constexpr (NS > 0) {
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+      consume(s % PD, s);
+      if (s + PD < NS) {
+#pragma unroll
+        for (int k = 0; k < 4; ++k)
+          ring[s % PD][k] = *reinterpret_cast<const bf16x8_t*>(wrow + w_off<PACKED>(s + PD, k));
+      }
+      // keep each step's refill where it is issued (PD steps ahead of its use)
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  } else {
   // steady state: unconditional refills keep PD K-steps in flight across the back-edge
   int s0 = 0;
   for (; s0 + 2 * PD <= nsteps; s0 += PD) {
@@ -250,6 +298,7 @@ __global__ __launch_bounds__(64) void stream_proj_kernel(ProjArgs a, int q_block
         }
       }
     }
+  }
   }
 
   if (col >= nt) return;
@@ -517,11 +566,11 @@ static hipError_t proj_t(const ProjArgs& a, int n_units, hipStream_t st) {
   return hipGetLastError();
 }
 
-template <int HD, bool PACKED>
+template <int HD, bool PACKED, int NS>
 static hipError_t stream_t(const ProjArgs& a, hipStream_t st) {
   const size_t bytes = stream_lds(a.d).end;
   static size_t done = 0;
-  auto k = stream_proj_kernel<HD, PACKED>;
+  auto k = stream_proj_kernel<HD, PACKED, NS>;
   hipError_t e = ensure_lds(k, bytes, done);
   if (e != hipSuccess) return e;
   const int qb = a.n_q * HD / 32;
@@ -589,13 +638,23 @@ hipError_t launch_proj(const ProjArgs& a, int dtype_bf16, int hd, int packed, in
 #undef PF
 }
 
+// d = 2560 (Gemma-3-4B) and 1536 (Qwen2.5-1.5B) get a straight-line K-loop.
+template <int HD, bool PACKED>
+static hipError_t stream_ns(const ProjArgs& a, hipStream_t st) {
+  switch (a.d / kKT) {
+    case 40: return stream_t<HD, PACKED, 40>(a, st);
+    case 24: return stream_t<HD, PACKED, 24>(a, st);
+    default: return stream_t<HD, PACKED, 0>(a, st);
+  }
+}
+
 hipError_t launch_project_current(const ProjArgs& a, int dtype_bf16, int hd, int packed, int n_units,
                                   hipStream_t st) {
   if (!dtype_bf16) return launch_proj(a, 0, hd, 0, n_units, st);
   switch (hd) {
-    case 64: return packed ? stream_t<64, true>(a, st) : stream_t<64, false>(a, st);
-    case 128: return packed ? stream_t<128, true>(a, st) : stream_t<128, false>(a, st);
-    case 256: return packed ? stream_t<256, true>(a, st) : stream_t<256, false>(a, st);
+    case 64: return packed ? stream_ns<64, true>(a, st) : stream_ns<64, false>(a, st);
+    case 128: return packed ? stream_ns<128, true>(a, st) : stream_ns<128, false>(a, st);
+    case 256: return packed ? stream_ns<256, true>(a, st) : stream_ns<256, false>(a, st);
     default: return hipErrorInvalidValue;
   }
 }

@@ -89,10 +89,10 @@ constexpr size_t fused_lds_bytes(int g, int hd, int mt) {
   return attn_lds(proj_lds<T>(hd, mt).end, g, hd, mt).end;
 }
 
-// Streaming projection: h-bar of kProjTok tokens for the whole d, plus 1/rms,
+// Streaming projection: h-bar of kProjTok tokens for the whole d, gamma, 1/rms,
 // positions and the RoPE table.
 struct StreamLds {
-  size_t rev, rinv, pos, hb, end;
+  size_t rev, rinv, pos, gam, hb, end;
 };
 constexpr int stream_h_ld(int d) { return d + 8; }
 constexpr StreamLds stream_lds(int d) {
@@ -100,7 +100,8 @@ constexpr StreamLds stream_lds(int d) {
   L.rev = 0;
   L.rinv = align_up(L.rev + sizeof(double) * kMaxPairs, 16);
   L.pos = align_up(L.rinv + sizeof(float) * kProjTok, 16);
-  L.hb = align_up(L.pos + sizeof(int) * kProjTok, 16);
+  L.gam = align_up(L.pos + sizeof(int) * kProjTok, 16);
+  L.hb = align_up(L.gam + sizeof(uint16_t) * d, 16);
   L.end = align_up(L.hb + sizeof(uint16_t) * kProjTok * stream_h_ld(d), 16);
   return L;
 }
