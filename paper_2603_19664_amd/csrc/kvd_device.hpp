@@ -39,10 +39,12 @@ template <int N> struct IC { static constexpr int value = N; };
 __device__ __forceinline__ float bf_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
 
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+
+// Two floats -> two bf16 (round to nearest even) in one 32-bit word, a in the low half.
 __device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
-  __bf16 x = (__bf16)a;  // round to nearest even
-  __bf16 y = (__bf16)b;
-  return (uint32_t)__builtin_bit_cast(uint16_t, x) | ((uint32_t)__builtin_bit_cast(uint16_t, y) << 16);
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t){a, b}, bf16x2_t));
 }
 
 __device__ __forceinline__ void load8(const uint16_t* p, float (&x)[8]) {
@@ -239,93 +241,134 @@ struct MfmaTile {
 #pragma unroll
         for (int i = 0; i < 16; ++i) acc[bf][bt][i] = 0.0f;
 
-    // Ring of kDepth K-steps in flight: slot U holds the weights and residual
-    // chunks of step s with s % kDepth == U.  Step s is staged into LDS buffer
-    // s & 1 one iteration before it is consumed.
-    constexpr int D = kDepth;
+    // K-loop.  Weights: a ring of D = 4 K-steps in A-operand registers, each
+    // 16-wide substep refilled right after its MFMAs.  Residuals: loaded D - 1
+    // steps ahead into registers, staged (gamma * h -> bf16, sum of squares) one
+    // step ahead into an LDS ring of D slots laid out in MFMA B-fragment order
+    // (fragment f = 4 * token block + substep, 64 lanes x 8 elements), so every
+    // wave reads its B operands as contiguous 1 KB blocks.  One barrier per step,
+    // in its middle: before it the step's first two substeps; after it the next
+    // step's fragments are valid, so the next step's first fragments are read
+    // during the last two substeps.  Per accumulator the MFMA chain is in K order.
+    static_assert(CPT == 1 && MT == 64, "one staged chunk per thread, two 32-token blocks");
+    constexpr int D = 4;
+    constexpr int SLOT = 8 * 512;  // elements per LDS slot
     bf16x8_t A[D][NB_F][4];
-    uint4 H[D][CPT];
-    float ss[CPT];
-#pragma unroll
-    for (int r = 0; r < CPT; ++r) ss[r] = 0.0f;
+    uint4 H[D];
+    float ss[CPT] = {0.0f};
+    const int row = tid >> 3;
+    const int lofs = ((row >> 5) * 4 + (sub >> 1)) * 512 + 8 * ((row & 31) + 32 * (sub & 1));
+    const int bt0 = NB_T == 2 ? 0 : tw;  // first absolute token block of this wave
 
-    auto load_step = [&](auto slot_c, int s) {
-      constexpr int U = decltype(slot_c)::value;
+    auto load_wu = [&](int slot, int s, int u) {
 #pragma unroll
-      for (int r = 0; r < CPT; ++r) H[U][r] = *reinterpret_cast<const uint4*>(hrow[r] + (size_t)s * kKT);
+      for (int bf = 0; bf < NB_F; ++bf)
+        A[slot][bf][u] = *reinterpret_cast<const bf16x8_t*>(wrow[bf] + w_off<PACKED>(s, u));
+    };
+    auto load_h = [&](int slot, int s) { H[slot] = *reinterpret_cast<const uint4*>(hrow[0] + (size_t)s * kKT); };
+    // Tokens past the end of a ragged tile stage a readable row's values: their
+    // MFMA columns are independent of the others and their 1/rms is zero.
+    auto put_h = [&](int slot, int s) {
+      const uint4 gv = *reinterpret_cast<const uint4*>(gam + (size_t)s * kKT + 8 * sub);
+      *reinterpret_cast<uint4*>(hst + (size_t)slot * SLOT + lofs) = stage_chunk_bf16(H[slot], gv, ss[0]);
+    };
+    auto rd = [&](bf16x8_t (&bv)[NB_T], int slot, int u) {
+#pragma unroll
+      for (int bt = 0; bt < NB_T; ++bt)
+        bv[bt] = *reinterpret_cast<const bf16x8_t*>(hst + (size_t)slot * SLOT + ((bt0 + bt) * 4 + u) * 512 + 8 * lane);
+    };
+    auto mma = [&](int slot, int u, const bf16x8_t (&bv)[NB_T]) {
 #pragma unroll
       for (int bf = 0; bf < NB_F; ++bf)
 #pragma unroll
-        for (int u = 0; u < 4; ++u)
-          A[U][bf][u] = *reinterpret_cast<const bf16x8_t*>(wrow[bf] + w_off<PACKED>(s, u));
-    };
-    auto stage = [&](auto slot_c, int s, int buf) {
-      constexpr int U = decltype(slot_c)::value;
-      const uint4 gv = *reinterpret_cast<const uint4*>(gam + (size_t)s * kKT + 8 * sub);
-#pragma unroll
-      for (int r = 0; r < CPT; ++r) {
-        const uint4 x = valid[r] ? H[U][r] : make_uint4(0, 0, 0, 0);
-        const uint4 o = stage_chunk_bf16(x, gv, ss[r]);
-        *reinterpret_cast<uint4*>(hst + ((size_t)buf * MT + (tid >> 3) + (NT / 8) * r) * HLD + 8 * sub) = o;
-      }
-    };
-    auto compute = [&](auto slot_c, auto buf_c) {
-      constexpr int U = decltype(slot_c)::value;
-      constexpr int C = decltype(buf_c)::value;
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        bf16x8_t bv[NB_T];
-#pragma unroll
         for (int bt = 0; bt < NB_T; ++bt)
-          bv[bt] = *reinterpret_cast<const bf16x8_t*>(
-              hst + ((size_t)C * MT + tw * TOK_W + 32 * bt + (lane & 31)) * HLD + 16 * u + 8 * (lane >> 5));
+          acc[bf][bt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(A[slot][bf][u], bv[bt], acc[bf][bt], 0, 0, 0);
+    };
+    // interleave of one substep: its B reads, then MFMAs and weight refills alternating
+    auto sched_substep = [&]() {
+      __builtin_amdgcn_sched_group_barrier(0x100, NB_T, 0);  // DS read
 #pragma unroll
-        for (int bf = 0; bf < NB_F; ++bf)
-#pragma unroll
-          for (int bt = 0; bt < NB_T; ++bt)
-            acc[bf][bt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(A[U][bf][u], bv[bt], acc[bf][bt], 0, 0, 0);
+      for (int i = 0; i < NB_F; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, NB_T, 0);  // MFMA
+        __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);     // VMEM read
       }
     };
-    // one iteration: consume step s from slot U, refill slot U with step s + D,
-    // stage step s + 1 (slot (U + 1) % D) into the other LDS buffer.  The steady
-    // state issues its loads unconditionally so that the compiler can count the
-    // loads in flight across the loop back-edge (a conditional refill makes it
-    // drain the whole ring at every trip).
-    auto iter_full = [&](auto slot_c, int s) {
-      constexpr int U = decltype(slot_c)::value;
-      compute(slot_c, IC<U & 1>{});
-      load_step(slot_c, s + D);
-      stage(IC<(U + 1) % D>{}, s + 1, (U + 1) & 1);
-      __syncthreads();
-    };
-    auto iter_tail = [&](auto slot_c, int s) {
-      constexpr int U = decltype(slot_c)::value;
-      compute(slot_c, IC<U & 1>{});
-      if (s + D < nsteps) load_step(slot_c, s + D);
-      if (s + 1 < nsteps) stage(IC<(U + 1) % D>{}, s + 1, (U + 1) & 1);
-      __syncthreads();
+    bf16x8_t b0[NB_T];
+    // iteration s (slot L = s % D): GUARD = false for the steady state (every
+    // step index below is in range), true for the last iterations.
+    auto iter = [&](auto lc, int s, auto guard_c) {
+      constexpr int L = decltype(lc)::value;
+      constexpr bool GUARD = decltype(guard_c)::value;
+      const int sw = GUARD ? min(s + D, nsteps - 1) : s + D;
+      __builtin_amdgcn_sched_barrier(0);
+      if (!GUARD || s + 1 < nsteps) put_h((L + 1) % D, s + 1);
+      bf16x8_t b1[NB_T], b2[NB_T], b3[NB_T];
+      rd(b1, L, 1);
+      mma(L, 0, b0);
+      load_wu(L, sw, 0);
+      mma(L, 1, b1);
+      load_wu(L, sw, 1);
+      if (!GUARD) {
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // gamma
+        __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);  // staged chunk
+        __builtin_amdgcn_sched_group_barrier(0x100, NB_T, 0);
+#pragma unroll
+        for (int i = 0; i < NB_F; ++i) {
+          __builtin_amdgcn_sched_group_barrier(0x008, NB_T, 0);
+          __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+        }
+#pragma unroll
+        for (int i = 0; i < NB_F; ++i) {
+          __builtin_amdgcn_sched_group_barrier(0x008, NB_T, 0);
+          __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+        }
+      }
+      __builtin_amdgcn_sched_barrier(0);
+      __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): this wave's staged chunk is in LDS
+      __builtin_amdgcn_s_barrier();
+      __builtin_amdgcn_sched_barrier(0);
+      rd(b2, L, 2);
+      rd(b3, L, 3);
+      load_h(L, GUARD ? min(s + D, nsteps - 1) : s + D);
+      mma(L, 2, b2);
+      load_wu(L, sw, 2);
+      rd(b0, (L + 1) % D, 0);
+      mma(L, 3, b3);
+      load_wu(L, sw, 3);
+      if (!GUARD) {
+        __builtin_amdgcn_sched_group_barrier(0x100, 2 * NB_T, 0);
+        __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // residual load
+        sched_substep();
+        sched_substep();
+      }
     };
 
-    static_assert(D == 4, "the unrolled loops below assume four slots");
-    load_step(IC<0>{}, 0);
-    load_step(IC<1>{}, min(1, nsteps - 1));
-    load_step(IC<2>{}, min(2, nsteps - 1));
-    load_step(IC<3>{}, min(3, nsteps - 1));
-    stage(IC<0>{}, 0, 0);
+    // prologue: residual steps 0..D-1 and weight steps 0..D-1 in flight, step 0 staged
+#pragma unroll
+    for (int i = 0; i < D; ++i) load_h(i, min(i, nsteps - 1));
+#pragma unroll
+    for (int i = 0; i < D; ++i)
+#pragma unroll
+      for (int u = 0; u < 4; ++u) load_wu(i, min(i, nsteps - 1), u);
+    put_h(0, 0);
+    load_h(0, min(D, nsteps - 1));
     __syncthreads();
+    rd(b0, 0, 0);
     int s0 = 0;
+    // steady state: iterations s0..s0+3 all have s + D < nsteps
     for (; s0 + 2 * D <= nsteps; s0 += D) {
-      iter_full(IC<0>{}, s0);
-      iter_full(IC<1>{}, s0 + 1);
-      iter_full(IC<2>{}, s0 + 2);
-      iter_full(IC<3>{}, s0 + 3);
+      iter(IC<0>{}, s0, IC<0>{});
+      iter(IC<1>{}, s0 + 1, IC<0>{});
+      iter(IC<2>{}, s0 + 2, IC<0>{});
+      iter(IC<3>{}, s0 + 3, IC<0>{});
     }
     for (; s0 < nsteps; s0 += D) {
-      iter_tail(IC<0>{}, s0);
-      if (s0 + 1 < nsteps) iter_tail(IC<1>{}, s0 + 1);
-      if (s0 + 2 < nsteps) iter_tail(IC<2>{}, s0 + 2);
-      if (s0 + 3 < nsteps) iter_tail(IC<3>{}, s0 + 3);
+      iter(IC<0>{}, s0, IC<1>{});
+      if (s0 + 1 < nsteps) iter(IC<1>{}, s0 + 1, IC<1>{});
+      if (s0 + 2 < nsteps) iter(IC<2>{}, s0 + 2, IC<1>{});
+      if (s0 + 3 < nsteps) iter(IC<3>{}, s0 + 3, IC<1>{});
     }
+    __syncthreads();
 
     finish_rms<NT, CPT>(ss, valid, d, eps, rinv);
     __syncthreads();
@@ -499,16 +542,40 @@ __device__ __forceinline__ void load_kv_tile(const T* K, const T* V, int b, int 
   }
 }
 
-// Softmax partial state of keys 0..n-1 of an LDS K/V tile (rows stride KLD,
-// K at columns 0..HD-1, V at HD..2HD-1) for g query heads:
-//   m_h = max_t s_ht,  l_h = sum_t 2^(s_ht - m_h),  acc_h = sum_t 2^(s_ht - m_h) V_t,
-// with s_ht = log2(e) q_h.K_t / sqrt(HD).  Results in LDS (L.ml, L.acc).  The
-// arithmetic (task split and summation order) does not depend on the thread
-// count NT, so every kernel that attends a tile gets identical bits.
+// E consecutive elements of a K/V row as floats (E = head_dim / 64).
+template <int E> __device__ __forceinline__ void load_e(const uint16_t* p, float (&x)[E]) {
+  if constexpr (E == 4) {
+    const uint2 v = *reinterpret_cast<const uint2*>(p);
+    x[0] = bf_lo(v.x); x[1] = bf_hi(v.x); x[2] = bf_lo(v.y); x[3] = bf_hi(v.y);
+  } else if constexpr (E == 2) {
+    const uint32_t v = *reinterpret_cast<const uint32_t*>(p);
+    x[0] = bf_lo(v); x[1] = bf_hi(v);
+  } else {
+    x[0] = to_f<uint16_t>(*p);
+  }
+}
+template <int E> __device__ __forceinline__ void load_e(const float* p, float (&x)[E]) {
+#pragma unroll
+  for (int e = 0; e < E; ++e) x[e] = p[e];
+}
+
+// Softmax partial state of one tile of up to 64 keys (rows of `kv`: K in
+// columns [0, HD), V in [HD, 2 HD)) for the g query heads of one KV head, from
+// the pre-scaled q in LDS: ml = (max, sum of exp2) per head, acc = sum of
+// exp2(s - max) V (Eqs. attn_weights / head_output, restricted to the tile).
+// Work is split into wave-level tasks whose count depends on g and head_dim
+// only, never on the thread count, so every kernel that attends a tile performs
+// the same additions in the same order.
+//  1. partial scores: task (head h, 64-dim part p), lane = key;
+//  2. per head: parts summed in order, max, exp2, sum (one wave per head);
+//  3. P V: task (head h, key split ts of attn_ts(g)), lane = head_dim / 64
+//     consecutive output columns; the key splits are then summed in order.
 template <typename T, int HD, int NT>
 __device__ void attend_tile(const T* kv, int n, int rows, int g, char* lds, const AttnLds& L) {
   constexpr int KLD = kv_ld<T>(HD);
-  constexpr int C8 = HD / 8;
+  constexpr int NW = NT / 64;
+  constexpr int P = HD / 64;  // 64-dim parts of a score
+  constexpr int E = HD / 64;  // output columns per lane
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = wave_id();
   const float* qs = reinterpret_cast<const float*>(lds + L.q);
@@ -517,18 +584,20 @@ __device__ void attend_tile(const T* kv, int n, int rows, int g, char* lds, cons
   float* ml = reinterpret_cast<float*>(lds + L.ml);
   float* acc = reinterpret_cast<float*>(lds + L.acc);
 
-  for (int task = tid; task < g * rows; task += NT) {
-    const int h = task / rows, t = task - h * rows;
-    float s = -INFINITY;
-    if (t < n) {
-      const T* krow = kv + (size_t)t * KLD;
-      const float* qh = qs + h * HD;
-      float d0 = 0.0f, d1 = 0.0f, d2 = 0.0f, d3 = 0.0f;
-      auto dot8 = [&](int c, float x) {
+  for (int task = wave; task < g * P; task += NW) {
+    const int h = task / P, p = task - h * P;
+    float s = 0.0f;
+    if (lane < n) {
+      const T* krow = kv + (size_t)lane * KLD + 64 * p;
+      const float* qh = qs + h * HD + 64 * p;
+      float d[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+      for (int c = 0; c < 8; ++c) {
         float k8[8];
         load8(krow + 8 * c, k8);
         const float4 qa = *reinterpret_cast<const float4*>(qh + 8 * c);
         const float4 qb = *reinterpret_cast<const float4*>(qh + 8 * c + 4);
+        float x = d[c & 3];
         x = fmaf(qa.x, k8[0], x);
         x = fmaf(qa.y, k8[1], x);
         x = fmaf(qa.z, k8[2], x);
@@ -537,32 +606,25 @@ __device__ void attend_tile(const T* kv, int n, int rows, int g, char* lds, cons
         x = fmaf(qb.y, k8[5], x);
         x = fmaf(qb.z, k8[6], x);
         x = fmaf(qb.w, k8[7], x);
-        return x;
-      };
-#pragma unroll 2
-      for (int c = 0; c < C8; c += 4) {
-        d0 = dot8(c, d0);
-        d1 = dot8(c + 1, d1);
-        d2 = dot8(c + 2, d2);
-        d3 = dot8(c + 3, d3);
+        d[c & 3] = x;
       }
-      s = (d0 + d1) + (d2 + d3);
+      s = (d[0] + d[1]) + (d[2] + d[3]);
     }
-    S[h * rows + t] = s;
+    red[task * 64 + lane] = s;
   }
   __syncthreads();
 
-  for (int h = wave; h < g; h += NT / 64) {
-    float m = -INFINITY;
-    for (int t = lane; t < n; t += 64) m = fmaxf(m, S[h * rows + t]);
-    m = wave_max(m);
-    float l = 0.0f;
-    for (int t = lane; t < rows; t += 64) {
-      const float p = t < n ? exp2f(S[h * rows + t] - m) : 0.0f;
-      S[h * rows + t] = p;
-      l += p;
+  for (int h = wave; h < g; h += NW) {
+    float s = -INFINITY;
+    if (lane < n) {
+      s = red[(h * P) * 64 + lane];
+#pragma unroll
+      for (int p = 1; p < P; ++p) s += red[(h * P + p) * 64 + lane];
     }
-    l = wave_sum(l);
+    const float m = wave_max(s);
+    const float pr = lane < n ? exp2f(s - m) : 0.0f;
+    const float l = wave_sum(pr);
+    if (lane < rows) S[h * rows + lane] = pr;
     if (lane == 0) {
       ml[2 * h] = m;
       ml[2 * h + 1] = l;
@@ -570,23 +632,22 @@ __device__ void attend_tile(const T* kv, int n, int rows, int g, char* lds, cons
   }
   __syncthreads();
 
-  const int per = g * C8;
-  const int TS = per >= kAttnTasks ? 1 : kAttnTasks / per;
-  for (int task = tid; task < TS * per; task += NT) {
-    const int c8 = task % C8;
-    const int rest = task / C8;
-    const int h = rest % g, ts = rest / g;
-    float a8[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+  const int TS = attn_ts(g);
+  for (int task = wave; task < g * TS; task += NW) {
+    const int h = task % g, ts = task / g;
+    float a[E];
+#pragma unroll
+    for (int e = 0; e < E; ++e) a[e] = 0.0f;
     for (int t = ts; t < n; t += TS) {
-      const float p = S[h * rows + t];
-      float v8[8];
-      load8(kv + (size_t)t * KLD + HD + 8 * c8, v8);
+      const float pr = S[h * rows + t];
+      float v[E];
+      load_e<E>(kv + (size_t)t * KLD + HD + E * lane, v);
 #pragma unroll
-      for (int e = 0; e < 8; ++e) a8[e] = fmaf(p, v8[e], a8[e]);
+      for (int e = 0; e < E; ++e) a[e] = fmaf(pr, v[e], a[e]);
     }
-    float* dst = red + ((size_t)ts * g + h) * HD + 8 * c8;
+    float* dst = red + ((size_t)ts * g + h) * HD + E * lane;
 #pragma unroll
-    for (int e = 0; e < 8; ++e) dst[e] = a8[e];
+    for (int e = 0; e < E; ++e) dst[e] = a[e];
   }
   __syncthreads();
   for (int idx = tid; idx < g * HD; idx += NT) {

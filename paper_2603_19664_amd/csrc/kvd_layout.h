@@ -8,7 +8,6 @@ namespace kvd {
 
 constexpr int kNtTile = 512;    // threads of the recompute / fused kernels (8 wave64 waves)
 constexpr int kNtAttn = 256;    // threads of the stored-K/V attention and combine kernels
-constexpr int kAttnTasks = 256; // fixed task split of the attention arithmetic (independent of thread count)
 constexpr int kKT = 64;         // d-elements per K-step of the projection GEMM
 constexpr int kTile = 64;       // keys per attention tile (one split-K partial)
 constexpr int kMaxGroup = 16;   // max query heads per KV head
@@ -41,9 +40,10 @@ constexpr int h_ld(void) { return kKT + Pad<T>::h; }
 struct AttnLds {
   size_t q, s, red, ml, acc, end;
 };
-constexpr size_t red_floats(int g, int hd) {
-  return (size_t)(g * hd > 2048 ? g * hd : 2048);
-}
+// Key splits of the P V phase of a tile's attention: fixed by the group size
+// alone, so that kernels with different thread counts add in the same order.
+constexpr int attn_ts(int g) { return g >= 8 ? 1 : 8 / g; }
+constexpr size_t red_floats(int g, int hd) { return (size_t)attn_ts(g) * g * hd; }
 constexpr AttnLds attn_lds(size_t base, int g, int hd, int rows) {
   AttnLds L{};
   L.q = align_up(base, 16);
@@ -55,9 +55,10 @@ constexpr AttnLds attn_lds(size_t base, int g, int hd, int rows) {
   return L;
 }
 
-// LDS layout of the recompute engine: staged h-bar tiles (2 buffers), the
-// K/V tile (aliases the staging buffers), per-token 1/rms and positions, and
-// the RoPE frequency table.
+// LDS layout of the recompute engine: staged h-bar tiles, the K/V tile (aliases
+// the staging buffers), per-token 1/rms and positions, and the RoPE frequency
+// table.  bf16: a ring of kDepth K-steps of mt tokens x kKT in MFMA B-fragment
+// order; fp32: one [mt][h_ld] tile.
 struct ProjLds {
   size_t hst, kv, rinv, pos, rev, end;
 };
@@ -67,8 +68,8 @@ constexpr ProjLds proj_lds(int hd, int mt) {
   L.rev = 0;                                                       // double[kMaxPairs]
   L.rinv = align_up(L.rev + sizeof(double) * kMaxPairs, 16);        // float[mt]
   L.pos = align_up(L.rinv + sizeof(float) * mt, 16);                // int[mt]
-  L.hst = align_up(L.pos + sizeof(int) * mt, 16);                   // T[2][mt][h_ld]
-  size_t hst_end = L.hst + sizeof(T) * 2 * mt * h_ld<T>();
+  L.hst = align_up(L.pos + sizeof(int) * mt, 16);
+  size_t hst_end = L.hst + (sizeof(T) == 2 ? sizeof(T) * kDepth * mt * kKT : sizeof(T) * 2 * mt * h_ld<T>());
   L.kv = L.hst;                                                     // T[mt][kv_ld]
   size_t kv_end = L.kv + sizeof(T) * mt * kv_ld<T>(hd);
   L.end = align_up(hst_end > kv_end ? hst_end : kv_end, 16);
