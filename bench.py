@@ -9,8 +9,8 @@ Per layer the step runs the whole hot path through libkvd's C ABI:
   kvd_project_qkv           q and the current token's K_t/V_t (RMSNorm, W_q/W_k/W_v, RoPE)
   kvd_fused_recompute_attn  K/V of the 4096 context tokens recomputed from the residual
                             checkpoints (RMSNorm, W_k/W_v GEMM, RoPE) into LDS, split-K
-                            attention over [context || current token]  (partials)
-  kvd_combine               merge of the split-K partials
+                            attention over [context || current token]; the workgroup that
+                            completes a (sequence, KV head) merges its partials in-kernel
 
 Printed: ONE JSON line (tokens/s of the step, ms per step, the roofline of the
 fused kernel from HIP events over the timed region, the per-op us/layer, the
@@ -116,18 +116,16 @@ def main():
     tk = torch.zeros((B, nkv, 1, hd), dtype=torch.bfloat16, device=dev)
     tv = torch.zeros_like(tk)
     tail = kvd.KvView(tk.data_ptr(), tv.data_ptr(), 1, 0)
-    S_f = kvd.kvd_num_splits(s, kvd.KVD_OP_FUSED, B, T, 1)
     ws_f = kvd.workspace(s, kvd.KVD_OP_FUSED, B, T, 1)
     wsb_f = ws_f.numel()
 
-    proj, fused, comb = [], [], []
+    proj, fused = [], []
     for ly in layers:
         proj.append(Call(lib.kvd_project_qkv, ctypes.byref(sc), P(ly["h_new"]), P(ly["gamma"]), P(ly["w_q"]),
                          P(ly["w_k"]), P(ly["w_v"]), P(pos_new), B, P(q), ctypes.byref(tail), stream))
         fused.append(Call(lib.kvd_fused_recompute_attn, ctypes.byref(sc), P(q), P(ly["h"]), T, P(ly["gamma"]),
-                          P(ly["w_k"]), P(ly["w_v"]), P(pos0), B, T, ctypes.byref(tail), 1, None, P(ws_f), wsb_f,
+                          P(ly["w_k"]), P(ly["w_v"]), P(pos0), B, T, ctypes.byref(tail), 1, P(out), P(ws_f), wsb_f,
                           None, stream))
-        comb.append(Call(lib.kvd_combine, ctypes.byref(sc), B, S_f, P(ws_f), wsb_f, P(out), stream))
 
     def step(events=None, i=0):
         for l in range(L):
@@ -137,7 +135,6 @@ def main():
             fused[l]()
             if events is not None:
                 events[i][l][1].record()
-            comb[l]()
 
     # one plain copy of known size (untimed): its FETCH_SIZE / WRITE_SIZE in a
     # counter run scale the fused kernel's counters to bytes
@@ -205,13 +202,12 @@ def main():
         cyc = lambda calls: (lambda c=[0]: (calls[c[0] % L](), c.__setitem__(0, c[0] + 1)))  # noqa: E731
         per_op["project_qkv_us"] = op_time(cyc(proj), iters=2 * L)
         per_op["fused_recompute_attn_us"] = op_time(cyc(fused), iters=2 * L)
-        per_op["combine_us"] = op_time(cyc(comb), iters=2 * L)
 
         # cached-K/V baseline: a persistent bf16 cache per layer, prefilled once by the library
         log("[bench] cached-K/V baseline: prefilling 34 layers of bf16 K/V")
         S_c = kvd.kvd_num_splits(s, kvd.KVD_OP_CACHED_ATTN, B, T + 1)
         ws_c = kvd.workspace(s, kvd.KVD_OP_CACHED_ATTN, B, T + 1)
-        cached, cproj, ccomb = [], [], []
+        cached, cproj = [], []
         caches = []
         for ly in layers:
             Kc = torch.empty((B, nkv, T + 1, hd), dtype=torch.bfloat16, device=dev)
@@ -223,17 +219,14 @@ def main():
             caches.append((vrow, vall))
             cproj.append(Call(lib.kvd_project_qkv, ctypes.byref(sc), P(ly["h_new"]), P(ly["gamma"]), P(ly["w_q"]),
                               P(ly["w_k"]), P(ly["w_v"]), P(pos_new), B, P(q), ctypes.byref(vrow), stream))
-            cached.append(Call(lib.kvd_cached_attn, ctypes.byref(sc), P(q), ctypes.byref(vall), B, T + 1, None,
+            cached.append(Call(lib.kvd_cached_attn, ctypes.byref(sc), P(q), ctypes.byref(vall), B, T + 1, P(out),
                                P(ws_c), ws_c.numel(), stream))
-            ccomb.append(Call(lib.kvd_combine, ctypes.byref(sc), B, S_c, P(ws_c), ws_c.numel(), P(out), stream))
         per_op["cached_attn_us"] = op_time(cyc(cached), iters=2 * L)
-        per_op["cached_combine_us"] = op_time(cyc(ccomb), iters=2 * L)
 
         def cached_step():
             for l in range(L):
                 cproj[l]()
                 cached[l]()
-                ccomb[l]()
         cached_ms = op_time(cached_step, iters=max(3, K // 2)) / 1e3
         baselines["cached_kv_ms_per_step"] = cached_ms
         baselines["cached_kv_tok_s"] = B / (cached_ms * 1e-3)
@@ -256,7 +249,7 @@ def main():
             udec.append(Call(lib.kvd_decode_attn, ctypes.byref(sc), P(q), ctypes.byref(uall), B, T + 1, P(out),
                              P(ws_c), ws_c.numel(), stream))
         per_op["recompute_kv_us"] = op_time(cyc(urec), iters=2 * L)
-        per_op["decode_attn_with_combine_us"] = op_time(cyc(udec), iters=2 * L)
+        per_op["decode_attn_us"] = op_time(cyc(udec), iters=2 * L)
 
         def unfused_step():
             for l in range(L):
@@ -296,7 +289,7 @@ def main():
         "data": "synthetic (seeded N(0,1) residuals scaled per layer by U(0.5,4); random-init N(0,0.02) weights)",
         "config": {"workload": wl.name, "layers": L, "batch": B, "ctx": T, "keys_per_query": T + 1,
                    "d_model": d, "n_q_heads": nq, "n_kv_heads": nkv, "head_dim": hd,
-                   "step": "per layer: kvd_project_qkv + kvd_fused_recompute_attn (partials) + kvd_combine"},
+                   "step": "per layer: kvd_project_qkv + kvd_fused_recompute_attn (split-K merge in-kernel)"},
         "roofline": {"bound": "mfma", "kernel": "fused_kernel<bf16,256,64>", "achieved": achieved,
                      "peak": MI355X_BF16_PEAK_TFLOPS, "unit": "TFLOP/s", "frac": achieved / MI355X_BF16_PEAK_TFLOPS,
                      "traffic": traffic, "flops_per_launch": flops, "us_per_launch": 1e3 * fused_ms},
@@ -309,7 +302,7 @@ def main():
 
 
 def run_crossover(args, torch, np, kvd, acc, configs, inputs, op_time, log):
-    """Fused recompute-attention vs cached-K/V attention (each with its combine) for one
+    """Fused recompute-attention vs cached-K/V attention (each with its split-K merge) for one
     Gemma-3-4B-shaped layer, context 2048 + current token, over batch size.  Each
     measurement runs after a 512 MiB write that evicts L2 and the Infinity Cache, so
     both sides read their inputs from HBM."""
@@ -349,7 +342,7 @@ def run_crossover(args, torch, np, kvd, acc, configs, inputs, op_time, log):
         torch.cuda.empty_cache()
     faster = [r["B"] for r in rows if r["ratio_fused_over_cached"] < 1.0]
     return {"workload": wl.name, "ctx": T, "rows": rows, "batches_where_recompute_wins": faster,
-            "note": "each op timed with HIP events after a 512 MiB cache-evicting write; both include their combine"}
+            "note": "each op timed with HIP events after a 512 MiB cache-evicting write; both include their split-K merge"}
 
 
 def run_cpu_baseline(args, np, wl, layers, T, B, inputs, log):

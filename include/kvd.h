@@ -58,7 +58,7 @@
 extern "C" {
 #endif
 
-#define KVD_ABI_VERSION 2
+#define KVD_ABI_VERSION 3
 
 typedef enum {
   KVD_OK = 0,
@@ -137,11 +137,16 @@ kvd_status kvd_project_qkv(const kvd_attn_shape* shape, const void* h_new, const
 
 /* ATTENTION for one decode query per sequence and head (Eqs. attn_weights,
  * head_output) over T >= 1 stored keys: rows kv->t_off .. kv->t_off+T-1.
- * Split-K: partial softmax states go to the workspace and a second kernel
- * merges them.  ws (256-byte aligned) must hold kvd_workspace_bytes(shape,
- * KVD_OP_DECODE_ATTN, B, T, 0) bytes; its contents on entry are ignored, and
- * calls sharing one workspace must be ordered on one stream.  With out == NULL
- * only the partials are written (see kvd_combine).
+ * Split-K: partial softmax states go to the workspace; the workgroup that
+ * writes the last partial of a (sequence, KV head) merges them into out in the
+ * same kernel (an atomic split counter in the workspace; no spin-waits).
+ * ws (256-byte aligned) must hold kvd_workspace_bytes(shape, KVD_OP_DECODE_ATTN,
+ * B, T, 0) bytes.  Workspace contract: its last kvd_workspace_bytes - (partials)
+ * bytes hold split counters that must be zero before the first call with
+ * out != NULL (allocate the workspace zero-filled once); every call leaves them
+ * zero.  The rest of the workspace is overwritten.  Calls sharing one workspace
+ * must be ordered on one stream.  With out == NULL only the partials are
+ * written (see kvd_combine) and the counters are not touched.
  *   q [B][n_q_heads][head_dim].   out [B][n_q_heads][head_dim].               */
 kvd_status kvd_decode_attn(const kvd_attn_shape* shape, const void* q, const kvd_kv_view* kv,
                            int32_t B, int32_t T, void* out, void* ws, size_t ws_bytes,
@@ -192,9 +197,10 @@ kvd_status kvd_pack_weights(const kvd_attn_shape* shape, const void* w, int32_t 
 /* Merge step of split-K attention: out[b][h] = sum_s w_s acc_s / sum_s w_s l_s
  * with w_s = 2^(m_s - max_s m_s), over the S partial softmax states that a
  * preceding kvd_decode_attn / kvd_cached_attn / kvd_fused_recompute_attn call
- * (with out == NULL) left in ws, in split order (deterministic).  S is that
- * call's kvd_num_splits.  Lets a caller time or schedule the two kernels
- * separately; the attention calls with out != NULL run it themselves.        */
+ * (with out == NULL) left in ws, in a fixed order (deterministic; the same
+ * arithmetic as the merge those calls run themselves when out != NULL).  S is
+ * that call's kvd_num_splits.  Lets a caller time or schedule the merge
+ * separately.                                                                 */
 kvd_status kvd_combine(const kvd_attn_shape* shape, int32_t B, int32_t S, const void* ws,
                        size_t ws_bytes, void* out, void* stream);
 

@@ -92,8 +92,19 @@ int32_t splits(int32_t op, int32_t T_main, int32_t T_tail) {
 size_t ws_acc_bytes(const kvd_attn_shape* s, int32_t B, int32_t S) {
   return kvd::align_up((size_t)B * s->n_q_heads * S * s->head_dim * sizeof(float), 256);
 }
+size_t ws_ml_bytes(const kvd_attn_shape* s, int32_t B, int32_t S) {
+  return kvd::align_up((size_t)B * s->n_q_heads * S * 2 * sizeof(float), 256);
+}
+// Workspace: partial accumulators [B][n_q][S][hd] fp32, partial (max, sum)
+// [B][n_q][S][2] fp32, split counters [B][n_kv] int32 (zero between calls).
 size_t ws_total(const kvd_attn_shape* s, int32_t B, int32_t S) {
-  return ws_acc_bytes(s, B, S) + kvd::align_up((size_t)B * s->n_q_heads * S * 2 * sizeof(float), 256);
+  return ws_acc_bytes(s, B, S) + ws_ml_bytes(s, B, S) + kvd::align_up((size_t)B * s->n_kv_heads * sizeof(int32_t), 256);
+}
+float* ws_ml_ptr(const kvd_attn_shape* s, int32_t B, int32_t S, void* ws) {
+  return reinterpret_cast<float*>(static_cast<char*>(ws) + ws_acc_bytes(s, B, S));
+}
+int* ws_done_ptr(const kvd_attn_shape* s, int32_t B, int32_t S, void* ws) {
+  return reinterpret_cast<int*>(static_cast<char*>(ws) + ws_acc_bytes(s, B, S) + ws_ml_bytes(s, B, S));
 }
 
 kvd_status check_ws(const kvd_attn_shape* s, int32_t B, int32_t S, void* ws, size_t ws_bytes) {
@@ -167,7 +178,8 @@ kvd_status attn_common(const kvd_attn_shape* shape, const void* q, const kvd_kv_
   a.t_off = kv->t_off;
   a.out = out;
   a.ws_acc = static_cast<float*>(ws);
-  a.ws_ml = reinterpret_cast<float*>(static_cast<char*>(ws) + ws_acc_bytes(shape, B, S));
+  a.ws_ml = ws_ml_ptr(shape, B, S, ws);
+  a.ws_done = ws_done_ptr(shape, B, S, ws);
   a.B = B;
   a.T = T;
   a.n_q = shape->n_q_heads;
@@ -341,7 +353,8 @@ kvd_status kvd_fused_recompute_attn(const kvd_attn_shape* shape, const void* q, 
     a.dbg_t_off = kv_debug->t_off;
   }
   a.ws_acc = static_cast<float*>(ws);
-  a.ws_ml = reinterpret_cast<float*>(static_cast<char*>(ws) + ws_acc_bytes(shape, B, S));
+  a.ws_ml = ws_ml_ptr(shape, B, S, ws);
+  a.ws_done = ws_done_ptr(shape, B, S, ws);
   a.out = out;
   a.d = shape->d_model;
   a.n_q = shape->n_q_heads;

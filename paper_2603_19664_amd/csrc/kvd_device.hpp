@@ -658,6 +658,16 @@ __device__ void attend_tile(const T* kv, int n, int rows, int g, char* lds, cons
   __syncthreads();
 }
 
+// Device-scope (coherent across the XCDs' L2 caches) 32-bit store / load: the
+// split-K partials cross workgroups on different XCDs, so they are written
+// through and read past the per-XCD L2 instead of fencing whole caches.
+__device__ __forceinline__ void store_dev(float* p, float v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float load_dev(const float* p) {
+  return __hip_atomic_load(const_cast<float*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
 // Split-K partial of (b, KV head j, split s) into the workspace:
 // acc [B][n_q][S][HD] fp32 followed by ml [B][n_q][S][2] fp32.
 template <int HD, int NT>
@@ -665,16 +675,109 @@ __device__ __forceinline__ void write_partial(const char* lds, const AttnLds& L,
                                               int n_q, int j, int g, int S, int s) {
   const float* acc = reinterpret_cast<const float*>(lds + L.acc);
   const float* ml = reinterpret_cast<const float*>(lds + L.ml);
-  for (int c4 = threadIdx.x; c4 < g * HD / 4; c4 += NT) {
-    const int h = (4 * c4) / HD, c = 4 * c4 - h * HD;
-    *reinterpret_cast<float4*>(ws_acc + (((size_t)b * n_q + (size_t)j * g + h) * S + s) * HD + c) =
-        *reinterpret_cast<const float4*>(acc + 4 * c4);
+  for (int i = threadIdx.x; i < g * HD; i += NT) {
+    const int h = i / HD, c = i - h * HD;
+    store_dev(ws_acc + (((size_t)b * n_q + (size_t)j * g + h) * S + s) * HD + c, acc[i]);
   }
-  if (threadIdx.x < g) {
-    const int h = threadIdx.x;
-    *reinterpret_cast<float2*>(ws_ml + (((size_t)b * n_q + (size_t)j * g + h) * S + s) * 2) =
-        make_float2(ml[2 * h], ml[2 * h + 1]);
+  if (threadIdx.x < 2 * g) {
+    const int h = threadIdx.x >> 1;
+    store_dev(ws_ml + (((size_t)b * n_q + (size_t)j * g + h) * S + s) * 2 + (threadIdx.x & 1), ml[threadIdx.x]);
   }
+}
+
+// Merge of the S split-K partial states of rows row0 .. row0+nrows-1 (row =
+// b * n_q + query head) into out (Eqs. attn_weights / head_output over all
+// splits): M = max_s m_s, w_s = 2^(m_s - M), out = sum_s w_s acc_s / sum_s w_s l_s.
+// Every sum has a fixed order that does not depend on NT: each output column
+// adds its splits in split order; the denominator is accumulated per lane over
+// splits s = lane, lane + 64, ... and then summed by a fixed wave tree.  NT / HD
+// rows are merged per pass.  lds: cmb_floats(NT, HD) floats.
+template <typename T, int HD, int NT>
+__device__ void combine_rows(const float* ws_acc, const float* ws_ml, T* out, size_t row0, int nrows, int S,
+                             float* lds) {
+  constexpr int RPP = NT / HD;
+  static_assert(RPP >= 1 && RPP <= NT / 64, "rows per pass");
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = wave_id();
+  const int rr = tid / HD, c = tid - rr * HD;
+  float* wsh = lds;             // [RPP][64] weights of the current block of splits
+  float* mL = lds + RPP * 64;   // [RPP][2] max, denominator
+  for (int r0 = 0; r0 < nrows; r0 += RPP) {
+    const bool mine = wave < RPP && r0 + wave < nrows;  // this wave owns the weights of row r0 + wave
+    const bool rv = rr < RPP && r0 + rr < nrows;         // this thread owns column c of row r0 + rr
+    const float* mlw = ws_ml + (row0 + r0 + wave) * (size_t)S * 2;
+    if (mine) {
+      float m = -INFINITY;
+      for (int s = lane; s < S; s += 64) m = fmaxf(m, load_dev(mlw + 2 * s));
+      m = wave_max(m);
+      if (lane == 0) mL[2 * wave] = m;
+    }
+    __syncthreads();
+    float o = 0.0f, lsum = 0.0f;
+    const float* ap = ws_acc + (row0 + r0 + rr) * (size_t)S * HD + c;
+    for (int s0 = 0; s0 < S; s0 += 64) {
+      if (mine) {
+        const int s = s0 + lane;
+        float w = 0.0f;
+        if (s < S) {
+          w = exp2f(load_dev(mlw + 2 * s) - mL[2 * wave]);
+          lsum = fmaf(load_dev(mlw + 2 * s + 1), w, lsum);
+        }
+        wsh[wave * 64 + lane] = w;
+      }
+      __syncthreads();
+      if (rv) {
+        const int cnt = min(64, S - s0);
+        const float* a = ap + (size_t)s0 * HD;
+        const float* wp = wsh + rr * 64;
+        int i = 0;
+        if (cnt == 64) {  // a whole block: all 64 loads in flight, then the sums in split order
+          float x[64];
+#pragma unroll
+          for (int e = 0; e < 64; ++e) x[e] = load_dev(a + (size_t)e * HD);
+#pragma unroll
+          for (int e = 0; e < 64; ++e) o = fmaf(x[e], wp[e], o);
+          i = 64;
+        }
+        for (; i + 16 <= cnt; i += 16) {
+          float x[16];
+#pragma unroll
+          for (int e = 0; e < 16; ++e) x[e] = load_dev(a + (size_t)(i + e) * HD);
+#pragma unroll
+          for (int e = 0; e < 16; ++e) o = fmaf(x[e], wp[i + e], o);
+        }
+        for (; i < cnt; ++i) o = fmaf(load_dev(a + (size_t)i * HD), wp[i], o);
+      }
+      __syncthreads();
+    }
+    if (mine) {
+      lsum = wave_sum(lsum);
+      if (lane == 0) mL[2 * wave + 1] = lsum;
+    }
+    __syncthreads();
+    if (rv) out[(row0 + r0 + rr) * HD + c] = from_f<T>(o / mL[2 * rr + 1]);
+    __syncthreads();
+  }
+}
+
+// After a workgroup has written `count` partials of (b, KV head j) with
+// store_dev: returns true in the one workgroup whose partials complete the S of
+// (b, j) (the counter in the workspace is then reset for the next call).  Every
+// thread waits for its device-scope stores to complete before the workgroup
+// counts, so a workgroup that sees the final count and reads with load_dev sees
+// every partial.  No cache-wide write-back or invalidate is needed: other
+// workgroups streaming weights through the same L2 keep them.
+__device__ __forceinline__ bool last_of_splits(int* done, int count, int S, int* flag) {
+  __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0): this thread's partial stores are complete
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const int before = __hip_atomic_fetch_add(done, count, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const bool last = before + count == S;
+    if (last) __hip_atomic_store(done, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    *flag = last;
+  }
+  __syncthreads();
+  return *flag != 0;
 }
 
 }  // namespace kvd

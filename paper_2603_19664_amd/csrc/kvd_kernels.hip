@@ -411,6 +411,7 @@ __global__ __launch_bounds__(kNtTile, 1) void fused_kernel(FusedArgs a, int per_
     }
     attend_tile<T, HD, NT>(kv, n, MT, g, lds, AL);
     write_partial<HD, NT>(lds, AL, a.ws_acc, a.ws_ml, b, a.n_q, j, g, a.S, c);
+    int count = 1;
     // stored tail tiles assigned to this chunk
     for (int k = a.n_rec - 1 - c; k < n_tail; k += a.n_rec) {
       const int r0 = k * kTile;
@@ -421,7 +422,12 @@ __global__ __launch_bounds__(kNtTile, 1) void fused_kernel(FusedArgs a, int per_
       __syncthreads();
       attend_tile<T, HD, NT>(kv, nk, MT, g, lds, AL);
       write_partial<HD, NT>(lds, AL, a.ws_acc, a.ws_ml, b, a.n_q, j, g, a.S, a.n_rec + k);
+      ++count;
     }
+    if (a.out != nullptr &&
+        last_of_splits(a.ws_done + (size_t)b * a.n_kv + j, count, a.S, reinterpret_cast<int*>(lds + AL.cmb)))
+      combine_rows<T, HD, NT>(a.ws_acc, a.ws_ml, static_cast<T*>(a.out), (size_t)b * a.n_q + (size_t)j * g, g, a.S,
+                              reinterpret_cast<float*>(lds + AL.cmb));
   } else {
     const int r0 = c * kTile;
     const int nk = min(kTile, a.T_tail - r0);
@@ -430,6 +436,10 @@ __global__ __launch_bounds__(kNtTile, 1) void fused_kernel(FusedArgs a, int per_
     __syncthreads();
     attend_tile<T, HD, NT>(kv, nk, MT, g, lds, AL);
     write_partial<HD, NT>(lds, AL, a.ws_acc, a.ws_ml, b, a.n_q, j, g, a.S, c);
+    if (a.out != nullptr &&
+        last_of_splits(a.ws_done + (size_t)b * a.n_kv + j, 1, a.S, reinterpret_cast<int*>(lds + AL.cmb)))
+      combine_rows<T, HD, NT>(a.ws_acc, a.ws_ml, static_cast<T*>(a.out), (size_t)b * a.n_q + (size_t)j * g, g, a.S,
+                              reinterpret_cast<float*>(lds + AL.cmb));
   }
 }
 
@@ -451,65 +461,19 @@ __global__ __launch_bounds__(kNtAttn) void decode_kernel(AttnArgs a) {
   __syncthreads();
   attend_tile<T, HD, NT>(kv, n, kTile, g, lds, AL);
   write_partial<HD, NT>(lds, AL, a.ws_acc, a.ws_ml, b, a.n_q, j, g, a.S, s);
+  if (a.out != nullptr &&
+      last_of_splits(a.ws_done + (size_t)b * a.n_kv + j, 1, a.S, reinterpret_cast<int*>(lds + AL.cmb)))
+    combine_rows<T, HD, NT>(a.ws_acc, a.ws_ml, static_cast<T*>(a.out), (size_t)b * a.n_q + (size_t)j * g, g, a.S,
+                            reinterpret_cast<float*>(lds + AL.cmb));
 }
 
-// out[b][h] = sum_s w_s acc_s / sum_s w_s l_s, w_s = 2^(m_s - M), M = max_s m_s.
-// One workgroup per (b, h); the weights of a block of 256 splits are computed in
-// parallel into LDS, then each thread sums its column over the block in split order.
+// Standalone merge (kvd_combine): one workgroup per (b, query head), the same
+// arithmetic as the merge the attention kernels run in their last workgroup.
 template <typename T, int HD>
 __global__ __launch_bounds__(kNtAttn) void combine_kernel(const float* ws_acc, const float* ws_ml, T* out, int n_q,
                                                           int S) {
-  constexpr int NT = kNtAttn;
-  __shared__ float wsh[NT];
-  __shared__ float red[NT / 64];
-  const int h = blockIdx.x, b = blockIdx.y, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const size_t row = (size_t)b * n_q + h;
-  const float* ml = ws_ml + row * S * 2;
-  const float* acc = ws_acc + row * S * HD;
-
-  float m = -INFINITY;
-  for (int s = tid; s < S; s += NT) m = fmaxf(m, ml[2 * s]);
-  m = wave_max(m);
-  if (lane == 0) red[wave] = m;
-  __syncthreads();
-  float M = red[0];
-#pragma unroll
-  for (int w = 1; w < NT / 64; ++w) M = fmaxf(M, red[w]);
-  __syncthreads();
-
-  float lsum = 0.0f, o = 0.0f;
-  for (int s0 = 0; s0 < S; s0 += NT) {
-    const int s = s0 + tid;
-    float w = 0.0f;
-    if (s < S) {
-      const float2 v = *reinterpret_cast<const float2*>(ml + 2 * s);
-      w = exp2f(v.x - M);
-      lsum = fmaf(v.y, w, lsum);
-    }
-    wsh[tid] = w;
-    __syncthreads();
-    const int cnt = min(NT, S - s0);
-    if (tid < HD) {
-      const float* ap = acc + (size_t)s0 * HD + tid;
-      int i = 0;
-      for (; i + 8 <= cnt; i += 8) {
-        float x[8];
-#pragma unroll
-        for (int e = 0; e < 8; ++e) x[e] = ap[(size_t)(i + e) * HD];
-#pragma unroll
-        for (int e = 0; e < 8; ++e) o = fmaf(x[e], wsh[i + e], o);
-      }
-      for (; i < cnt; ++i) o = fmaf(ap[(size_t)i * HD], wsh[i], o);
-    }
-    __syncthreads();
-  }
-  lsum = wave_sum(lsum);
-  if (lane == 0) red[wave] = lsum;
-  __syncthreads();
-  float L = red[0];
-#pragma unroll
-  for (int w = 1; w < NT / 64; ++w) L += red[w];
-  if (tid < HD) out[row * HD + tid] = from_f<T>(o / L);
+  __shared__ float cmb[cmb_floats(kNtAttn, HD)];
+  combine_rows<T, HD, kNtAttn>(ws_acc, ws_ml, out, (size_t)blockIdx.y * n_q + blockIdx.x, 1, S, cmb);
 }
 
 // ------------------------------------------------------------------ weight packing
@@ -603,10 +567,6 @@ static hipError_t attn_t(const AttnArgs& a, hipStream_t st) {
   hipError_t e = ensure_lds(k, bytes, done);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(k, dim3(a.S, a.n_kv, a.B), dim3(kNtAttn), bytes, st, a);
-  e = hipGetLastError();
-  if (e != hipSuccess || a.out == nullptr) return e;
-  hipLaunchKernelGGL((combine_kernel<T, HD>), dim3(a.n_q, a.B), dim3(kNtAttn), 0, st, a.ws_acc, a.ws_ml,
-                     static_cast<T*>(a.out), a.n_q, a.S);
   return hipGetLastError();
 }
 
@@ -666,8 +626,7 @@ hipError_t launch_fused(const FusedArgs& a, int dtype_bf16, int hd, int packed, 
   e = [&]() -> hipError_t { KVD_DISPATCH(dtype_bf16, hd, FB, FF) }();
 #undef FB
 #undef FF
-  if (e != hipSuccess || a.out == nullptr) return e;
-  return launch_combine(a.ws_acc, a.ws_ml, a.out, a.n_q, a.B, a.S, dtype_bf16, hd, st);
+  return e;
 }
 
 hipError_t launch_combine(const float* ws_acc, const float* ws_ml, void* out, int n_q, int B, int S, int dtype_bf16,

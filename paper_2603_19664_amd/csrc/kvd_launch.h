@@ -48,6 +48,7 @@ struct FusedArgs {
   int dbg_t_cap, dbg_t_off;
   float* ws_acc;
   float* ws_ml;
+  int* ws_done;  // [B][n_kv] split counters (zero between calls)
   void* out;
   int d, n_q, n_kv, B, T_rec, n_rec, S;
   float eps;
@@ -55,7 +56,8 @@ struct FusedArgs {
 };
 
 // Split-K attention over stored K/V: S = ceil(T / kTile) chunks.  out == nullptr:
-// partials only (no combine launch); the same holds for FusedArgs::out.
+// partials only; otherwise the workgroup that completes the splits of (b, KV
+// head) merges them into out.  The same holds for FusedArgs::out.
 struct AttnArgs {
   const void* q;
   const void* k;
@@ -64,6 +66,7 @@ struct AttnArgs {
   void* out;
   float* ws_acc;
   float* ws_ml;
+  int* ws_done;
   int B, T, n_q, n_kv, S;
 };
 

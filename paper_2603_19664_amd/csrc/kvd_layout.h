@@ -38,8 +38,10 @@ constexpr int h_ld(void) { return kKT + Pad<T>::h; }
 
 // LDS layout of the attention part (decode / fused kernels); g = group size.
 struct AttnLds {
-  size_t q, s, red, ml, acc, end;
+  size_t q, s, red, ml, acc, cmb, end;
 };
+// LDS floats of the split merge (combine_rows): rows-per-pass x (64 weights + 2).
+constexpr size_t cmb_floats(int nt, int hd) { return (size_t)(nt / hd) * 66; }
 // Key splits of the P V phase of a tile's attention: fixed by the group size
 // alone, so that kernels with different thread counts add in the same order.
 constexpr int attn_ts(int g) { return g >= 8 ? 1 : 8 / g; }
@@ -51,7 +53,8 @@ constexpr AttnLds attn_lds(size_t base, int g, int hd, int rows) {
   L.red = align_up(L.s + sizeof(float) * g * rows, 16);
   L.ml = align_up(L.red + sizeof(float) * red_floats(g, hd), 16);
   L.acc = align_up(L.ml + sizeof(float) * 2 * g, 16);
-  L.end = align_up(L.acc + sizeof(float) * g * hd, 16);
+  L.cmb = align_up(L.acc + sizeof(float) * g * hd, 16);
+  L.end = align_up(L.cmb + sizeof(float) * cmb_floats(512, hd), 16);
   return L;
 }
 

@@ -180,9 +180,10 @@ def kvd_num_splits(shape: Shape, op: int, B: int, T_main: int, T_tail: int = 0) 
 
 
 def workspace(shape: Shape, op: int, B: int, T_main: int, T_tail: int = 0, device="cuda") -> torch.Tensor:
-    """A device buffer of kvd_workspace_bytes bytes (torch allocations are 256-byte aligned)."""
+    """A zero-filled device buffer of kvd_workspace_bytes bytes (torch allocations are
+    256-byte aligned; the split counters at its end must start at zero)."""
     n = kvd_workspace_bytes(shape, op, B, T_main, T_tail)
-    return torch.empty(max(n, 256), dtype=torch.uint8, device=device)
+    return torch.zeros(max(n, 256), dtype=torch.uint8, device=device)
 
 
 def kvd_recompute_kv(shape: Shape, h, gamma, w_k, w_v, pos0, T: int, k_out, v_out, t_off: int = 0):

@@ -24,7 +24,7 @@ def view(t_cap=16, t_off=0, k=FAKE, v=FAKE):
 
 
 def test_loads_and_version():
-    assert kvd.abi_version() == 2
+    assert kvd.abi_version() == 3
     assert kvd.status_str(kvd.KVD_ERR_ALIGN) == "KVD_ERR_ALIGN"
 
 
@@ -136,7 +136,8 @@ def test_split_policy_and_workspace():
     S = 2
     acc = -(-2 * 8 * S * 256 * 4 // 256) * 256
     ml = -(-2 * 8 * S * 2 * 4 // 256) * 256
-    assert n == acc + ml
+    done = -(-2 * 4 * 4 // 256) * 256  # split counters [B][n_kv] int32
+    assert n == acc + ml + done
     assert lib.kvd_workspace_bytes(ctypes.byref(s), 9, 1, 10, 0) == 0
 
 
