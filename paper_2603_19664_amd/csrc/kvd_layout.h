@@ -7,7 +7,7 @@
 namespace kvd {
 
 constexpr int kNtTile = 512;    // threads of the recompute / fused kernels (8 wave64 waves)
-constexpr int kNtAttn = 256;    // threads of the stored-K/V attention and combine kernels
+constexpr int kNtAttn = 512;    // threads of the stored-K/V attention and combine kernels
 constexpr int kKT = 64;         // d-elements per K-step of the projection GEMM
 constexpr int kTile = 64;       // keys per attention tile (one split-K partial)
 constexpr int kMaxGroup = 16;   // max query heads per KV head
