@@ -48,6 +48,10 @@ def parse():
     p.add_argument("--sweep-batches", default="1,2,4,8,16,32,64")
     p.add_argument("--calibration-copy-mib", type=int, default=256,
                    help="size of one untimed device-to-device copy whose HBM counters calibrate the traffic figure")
+    p.add_argument("--extra", action="store_true",
+                   help="also measure the Qwen-1.5B-shaped step (28 layers, B=8, 16384 ctx; fused vs cached) and "
+                        "the multi-turn conversation (Gemma 3-4B shape, B=16, a decode step at each of 20 turn "
+                        "boundaries of 256 tokens) into extra_workloads")
     return p.parse_args()
 
 
@@ -298,6 +302,10 @@ def main():
         "crossover": crossover,
         "cpu_baseline": cpu,
     }
+    if args.extra:
+        del layers
+        torch.cuda.empty_cache()
+        res["extra_workloads"] = run_extra(args, torch, np, kvd, acc, configs, inputs, log)
     print(json.dumps(res), flush=True)
 
 
@@ -343,6 +351,131 @@ def run_crossover(args, torch, np, kvd, acc, configs, inputs, op_time, log):
     faster = [r["B"] for r in rows if r["ratio_fused_over_cached"] < 1.0]
     return {"workload": wl.name, "ctx": T, "rows": rows, "batches_where_recompute_wins": faster,
             "note": "each op timed with HIP events after a 512 MiB cache-evicting write; both include their split-K merge"}
+
+
+def _step_timer(torch, step, steps, warmup):
+    """ms per call of step(), HIP events around `steps` back-to-back calls after `warmup`."""
+    for _ in range(warmup):
+        step()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    a.record()
+    for _ in range(steps):
+        step()
+    b.record()
+    torch.cuda.synchronize()
+    return a.elapsed_time(b) / steps
+
+
+def _model_layers(wl, s, kvd, inputs, L, B, T_cap, dev):
+    layers = []
+    for l in range(L):
+        gamma, w_q, w_k, w_v = inputs.weights(wl, l, 0, dev)
+        h, h_new = inputs.residuals(wl, l, B, T_cap, 0, dev)
+        layers.append(dict(gamma=gamma, w_q=kvd.kvd_pack_weights(s, w_q), w_k=kvd.kvd_pack_weights(s, w_k),
+                           w_v=kvd.kvd_pack_weights(s, w_v), h=h, h_new=h_new))
+        del w_q, w_k, w_v
+    return layers
+
+
+def run_extra(args, torch, np, kvd, acc, configs, inputs, log):
+    """Full decode steps of the two other workloads, through the same C ABI calls as
+    the headline step (per layer: kvd_project_qkv, then kvd_fused_recompute_attn with
+    the current token as a one-row tail and the split-K merge in-kernel)."""
+    lib, dev = kvd.lib, "cuda"
+    stream = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    P = lambda t: ctypes.c_void_p(t.data_ptr())  # noqa: E731
+    res = {}
+
+    def fused_calls(s, sc, layers, B, T, h_ld, pos0, pos_new, q, out, tail, ws):
+        calls = []
+        for ly in layers:
+            calls.append(Call(lib.kvd_project_qkv, ctypes.byref(sc), P(ly["h_new"]), P(ly["gamma"]), P(ly["w_q"]),
+                              P(ly["w_k"]), P(ly["w_v"]), P(pos_new), B, P(q), ctypes.byref(tail), stream))
+            calls.append(Call(lib.kvd_fused_recompute_attn, ctypes.byref(sc), P(q), P(ly["h"]), h_ld,
+                              P(ly["gamma"]), P(ly["w_k"]), P(ly["w_v"]), P(pos0), B, T, ctypes.byref(tail), 1,
+                              P(out), P(ws), ws.numel(), None, stream))
+        return calls
+
+    # ---- Qwen-1.5B shape: 28 layers, B = 8, 16384 checkpointed tokens + current token
+    wl = configs.QWEN_1_5B
+    s = kvd.shape_of(wl).packed()
+    sc = s.c()
+    L, B, T = wl.layers, wl.batch, wl.ctx
+    log(f"[bench] extra: {wl.name}: generating {L} layers")
+    layers = _model_layers(wl, s, kvd, inputs, L, B, T, dev)
+    pos0 = inputs.positions(wl, B).to(dev)
+    pos_new = (pos0 + T).to(torch.int32)
+    q = torch.empty((B, wl.n_q, wl.head_dim), dtype=torch.bfloat16, device=dev)
+    out = torch.empty_like(q)
+    tk = torch.zeros((B, wl.n_kv, 1, wl.head_dim), dtype=torch.bfloat16, device=dev)
+    tv = torch.zeros_like(tk)
+    tail = kvd.KvView(tk.data_ptr(), tv.data_ptr(), 1, 0)
+    ws = kvd.workspace(s, kvd.KVD_OP_FUSED, B, T, 1)
+    calls = fused_calls(s, sc, layers, B, T, T, pos0, pos_new, q, out, tail, ws)
+    ms = _step_timer(torch, lambda: [c() for c in calls], steps=10, warmup=2)
+    flops = L * acc.fused_flops(B, T, 1, wl.n_q, wl.n_kv, wl.d_model, wl.head_dim)
+    entry = {"workload": wl.name, "layers": L, "batch": B, "ctx": T, "ms_per_step": ms, "tok_s": B / (ms * 1e-3),
+             "us_per_layer": 1e3 * ms / L, "fused_path_tflops": flops / (ms * 1e-3) / 1e12}
+    log(f"[bench] extra: {wl.name}: fused step {ms:.3f} ms")
+    # cached-K/V step on the same inputs: per-layer bf16 caches prefilled by the library
+    wsc = kvd.workspace(s, kvd.KVD_OP_CACHED_ATTN, B, T + 1)
+    ccalls, caches = [], []
+    for ly in layers:
+        Kc = torch.empty((B, wl.n_kv, T + 1, wl.head_dim), dtype=torch.bfloat16, device=dev)
+        Vc = torch.empty_like(Kc)
+        kvd.kvd_recompute_kv(s, ly["h"], ly["gamma"], ly["w_k"], ly["w_v"], pos0, T, Kc, Vc, 0)
+        vrow = kvd.KvView(Kc.data_ptr(), Vc.data_ptr(), T + 1, T)
+        vall = kvd.KvView(Kc.data_ptr(), Vc.data_ptr(), T + 1, 0)
+        caches.append((Kc, Vc, vrow, vall))
+        ccalls.append(Call(lib.kvd_project_qkv, ctypes.byref(sc), P(ly["h_new"]), P(ly["gamma"]), P(ly["w_q"]),
+                           P(ly["w_k"]), P(ly["w_v"]), P(pos_new), B, P(q), ctypes.byref(vrow), stream))
+        ccalls.append(Call(lib.kvd_cached_attn, ctypes.byref(sc), P(q), ctypes.byref(vall), B, T + 1, P(out),
+                           P(wsc), wsc.numel(), stream))
+    cms = _step_timer(torch, lambda: [c() for c in ccalls], steps=10, warmup=2)
+    cbytes = L * acc.cached_bytes(B, T + 1, wl.n_q, wl.n_kv, wl.head_dim, 2,
+                                  kvd.kvd_num_splits(s, kvd.KVD_OP_CACHED_ATTN, B, T + 1))
+    entry.update({"cached_ms_per_step": cms, "cached_tok_s": B / (cms * 1e-3),
+                  "cached_path_gbs": cbytes / (cms * 1e-3) / 1e9,
+                  "checkpoint_bytes": L * B * T * wl.d_model * 2,
+                  "kv_cache_bytes": L * B * (T + 1) * 2 * wl.n_kv * wl.head_dim * 2})
+    log(f"[bench] extra: {wl.name}: cached step {cms:.3f} ms")
+    res["qwen_1_5b"] = entry
+    del layers, caches, calls, ccalls
+    torch.cuda.empty_cache()
+
+    # ---- multi-turn conversation: Gemma 3-4B shape, 34 layers, B = 16, 20 turns of 256 tokens
+    wl = configs.GEMMA3_MULTITURN
+    s = kvd.shape_of(wl).packed()
+    sc = s.c()
+    L, B, Tmax = wl.layers, wl.batch, wl.turns * wl.turn_tokens
+    log(f"[bench] extra: {wl.name}: generating {L} layers of {Tmax}-token checkpoints")
+    layers = _model_layers(wl, s, kvd, inputs, L, B, Tmax, dev)
+    pos0 = torch.zeros((B,), dtype=torch.int32, device=dev)
+    q = torch.empty((B, wl.n_q, wl.head_dim), dtype=torch.bfloat16, device=dev)
+    out = torch.empty_like(q)
+    tk = torch.zeros((B, wl.n_kv, 1, wl.head_dim), dtype=torch.bfloat16, device=dev)
+    tv = torch.zeros_like(tk)
+    tail = kvd.KvView(tk.data_ptr(), tv.data_ptr(), 1, 0)
+    turns = []
+    for k in range(1, wl.turns + 1):
+        T = k * wl.turn_tokens
+        pos_new = torch.full((B,), T, dtype=torch.int32, device=dev)
+        ws = kvd.workspace(s, kvd.KVD_OP_FUSED, B, T, 1)
+        calls = fused_calls(s, sc, layers, B, T, Tmax, pos0, pos_new, q, out, tail, ws)
+        ms = _step_timer(torch, lambda: [c() for c in calls], steps=3, warmup=1)
+        flops = L * acc.fused_flops(B, T, 1, wl.n_q, wl.n_kv, wl.d_model, wl.head_dim)
+        turns.append({"turn": k, "ctx": T, "ms_per_step": ms, "tok_s": B / (ms * 1e-3), "us_per_layer": 1e3 * ms / L,
+                      "fused_path_tflops": flops / (ms * 1e-3) / 1e12,
+                      "checkpoint_bytes": L * B * T * wl.d_model * 2,
+                      "kv_cache_equiv_bytes": L * B * T * 2 * wl.n_kv * wl.head_dim * 2,
+                      "single_checkpoint_bytes": B * T * wl.d_model * 2,
+                      "workspace_bytes": ws.numel()})
+        log(f"[bench] extra: turn {k} ctx {T}: {ms:.3f} ms/step")
+    res["multiturn"] = {"workload": wl.name, "layers": L, "batch": B, "turn_tokens": wl.turn_tokens, "turns": turns}
+    del layers
+    torch.cuda.empty_cache()
+    return res
 
 
 def run_cpu_baseline(args, np, wl, layers, T, B, inputs, log):
