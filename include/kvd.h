@@ -58,7 +58,7 @@
 extern "C" {
 #endif
 
-#define KVD_ABI_VERSION 3
+#define KVD_ABI_VERSION 4
 
 typedef enum {
   KVD_OK = 0,
@@ -142,11 +142,11 @@ kvd_status kvd_project_qkv(const kvd_attn_shape* shape, const void* h_new, const
  * same kernel (an atomic split counter in the workspace; no spin-waits).
  * ws (256-byte aligned) must hold kvd_workspace_bytes(shape, KVD_OP_DECODE_ATTN,
  * B, T, 0) bytes.  Workspace contract: its last kvd_workspace_bytes - (partials)
- * bytes hold split counters that must be zero before the first call with
- * out != NULL (allocate the workspace zero-filled once); every call leaves them
- * zero.  The rest of the workspace is overwritten.  Calls sharing one workspace
- * must be ordered on one stream.  With out == NULL only the partials are
- * written (see kvd_combine) and the counters are not touched.
+ * bytes hold split counters ([B][n_kv_heads] uint64) that must be zero before
+ * the first call that uses them (allocate the workspace zero-filled once);
+ * every call leaves them zero.  The rest of the workspace is overwritten.  Calls
+ * sharing one workspace must be ordered on one stream.  With out == NULL only
+ * the partials are written (see kvd_combine) and the counters are not touched.
  *   q [B][n_q_heads][head_dim].   out [B][n_q_heads][head_dim].               */
 kvd_status kvd_decode_attn(const kvd_attn_shape* shape, const void* q, const kvd_kv_view* kv,
                            int32_t B, int32_t T, void* out, void* ws, size_t ws_bytes,
@@ -172,6 +172,14 @@ kvd_status kvd_cached_attn(const kvd_attn_shape* shape, const void* q, const kvd
  *   ws: kvd_workspace_bytes(shape, KVD_OP_FUSED, B, T_rec, T_tail) bytes.
  *   kv_debug: NULL in production.  If not NULL, the recomputed K/V are also
  *   written to it at rows kv_debug->t_off .. +T_rec-1 (for bit-identity checks).
+ * Split-K as in kvd_decode_attn, one split per 64-token tile of the
+ * recomputed rows.  With bf16, T_rec >= 1 and T_tail <= 4 (a decode step's
+ * current token) the tail joins the last tile's split: its rows are copied into
+ * LDS while that tile is recomputed.  Otherwise the tail adds one split per
+ * 64-row tile, each attended by one of the first recompute workgroups of its
+ * (sequence, KV head) to finish, handed out by the workspace's split counter
+ * (same zero-before-use contract as kvd_decode_attn), which is then used even
+ * with out == NULL.  kvd_num_splits gives the count.
  * out == NULL writes only the split-K partials (see kvd_combine).
  * Supports both dtypes.                                                       */
 kvd_status kvd_fused_recompute_attn(const kvd_attn_shape* shape, const void* q, const void* h,

@@ -84,9 +84,13 @@ void fill_rev(const kvd_attn_shape* s, double* rev) {
 
 int32_t ceil_div(int64_t a, int64_t b) { return (int32_t)((a + b - 1) / b); }
 
-int32_t splits(int32_t op, int32_t T_main, int32_t T_tail) {
-  if (op == KVD_OP_FUSED) return ceil_div(T_main, kvd::kMtBf16) + ceil_div(T_tail, kvd::kMtBf16);
-  return ceil_div(T_main, kvd::kTile);
+int32_t splits(const kvd_attn_shape* s, int32_t op, int32_t T_main, int32_t T_tail) {
+  if (op == KVD_OP_FUSED) {
+    const int32_t n_rec = ceil_div(T_main, kvd::kMtBf16);
+    return n_rec + (s->dtype == KVD_BF16 ? kvd::fused_tail_tiles<uint16_t>(n_rec, T_tail)
+                                         : kvd::fused_tail_tiles<float>(n_rec, T_tail));
+  }
+  return s->dtype == KVD_BF16 ? kvd::decode_splits<uint16_t>(T_main) : kvd::decode_splits<float>(T_main);
 }
 
 size_t ws_acc_bytes(const kvd_attn_shape* s, int32_t B, int32_t S) {
@@ -96,15 +100,15 @@ size_t ws_ml_bytes(const kvd_attn_shape* s, int32_t B, int32_t S) {
   return kvd::align_up((size_t)B * s->n_q_heads * S * 2 * sizeof(float), 256);
 }
 // Workspace: partial accumulators [B][n_q][S][hd] fp32, partial (max, sum)
-// [B][n_q][S][2] fp32, split counters [B][n_kv] int32 (zero between calls).
+// [B][n_q][S][2] fp32, split counters [B][n_kv] uint64 (zero between calls).
 size_t ws_total(const kvd_attn_shape* s, int32_t B, int32_t S) {
-  return ws_acc_bytes(s, B, S) + ws_ml_bytes(s, B, S) + kvd::align_up((size_t)B * s->n_kv_heads * sizeof(int32_t), 256);
+  return ws_acc_bytes(s, B, S) + ws_ml_bytes(s, B, S) + kvd::align_up((size_t)B * s->n_kv_heads * sizeof(uint64_t), 256);
 }
 float* ws_ml_ptr(const kvd_attn_shape* s, int32_t B, int32_t S, void* ws) {
   return reinterpret_cast<float*>(static_cast<char*>(ws) + ws_acc_bytes(s, B, S));
 }
-int* ws_done_ptr(const kvd_attn_shape* s, int32_t B, int32_t S, void* ws) {
-  return reinterpret_cast<int*>(static_cast<char*>(ws) + ws_acc_bytes(s, B, S) + ws_ml_bytes(s, B, S));
+unsigned long long* ws_done_ptr(const kvd_attn_shape* s, int32_t B, int32_t S, void* ws) {
+  return reinterpret_cast<unsigned long long*>(static_cast<char*>(ws) + ws_acc_bytes(s, B, S) + ws_ml_bytes(s, B, S));
 }
 
 kvd_status check_ws(const kvd_attn_shape* s, int32_t B, int32_t S, void* ws, size_t ws_bytes) {
@@ -168,7 +172,7 @@ kvd_status attn_common(const kvd_attn_shape* shape, const void* q, const kvd_kv_
   KVD_TRY(check_ptr(q, "q"));
   if (out != nullptr) KVD_TRY(check_ptr(out, "out"));
   KVD_TRY(check_view(kv, T, "kv"));
-  const int32_t S = splits(KVD_OP_DECODE_ATTN, T, 0);
+  const int32_t S = splits(shape, KVD_OP_DECODE_ATTN, T, 0);
   KVD_TRY(check_ws(shape, B, S, ws, ws_bytes));
   kvd::AttnArgs a{};
   a.q = q;
@@ -329,7 +333,7 @@ kvd_status kvd_fused_recompute_attn(const kvd_attn_shape* shape, const void* q, 
     if (kv_debug != nullptr) KVD_TRY(check_view(kv_debug, T_rec, "kv_debug"));
   }
   if (T_tail > 0) KVD_TRY(check_view(tail, T_tail, "tail"));
-  const int32_t S = splits(KVD_OP_FUSED, T_rec, T_tail);
+  const int32_t S = splits(shape, KVD_OP_FUSED, T_rec, T_tail);
   KVD_TRY(check_ws(shape, B, S, ws, ws_bytes));
   kvd::FusedArgs a{};
   a.q = q;
@@ -410,7 +414,7 @@ int32_t kvd_num_splits(const kvd_attn_shape* shape, int32_t op, int32_t B, int32
   } else {
     return 0;
   }
-  return splits(op, T_main, T_tail);
+  return splits(shape, op, T_main, T_tail);
 }
 
 size_t kvd_workspace_bytes(const kvd_attn_shape* shape, int32_t op, int32_t B, int32_t T_main, int32_t T_tail) {

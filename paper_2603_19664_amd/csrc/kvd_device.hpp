@@ -69,15 +69,31 @@ template <> __device__ __forceinline__ uint16_t from_f<uint16_t>(float v) {
 }
 template <> __device__ __forceinline__ float from_f<float>(float v) { return v; }
 
+// Wave-wide reductions on DPP lane moves (VALU only, no LDS round trips), in a
+// fixed order: pairs and quads (quad_perm), 16-lane rows (row_ror 4, 8), then
+// rows into lane 63 (row_bcast 15, 31); the result is broadcast from lane 63.
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ float dpp_mov(float old, float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(__builtin_bit_cast(int, old), __builtin_bit_cast(int, v),
+                                                               CTRL, ROW_MASK, 0xf, false));
+}
 __device__ __forceinline__ float wave_max(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
-  return v;
+  v = fmaxf(v, dpp_mov<0xB1, 0xf>(v, v));          // quad_perm [1,0,3,2]
+  v = fmaxf(v, dpp_mov<0x4E, 0xf>(v, v));          // quad_perm [2,3,0,1]
+  v = fmaxf(v, dpp_mov<0x124, 0xf>(v, v));         // row_ror 4
+  v = fmaxf(v, dpp_mov<0x128, 0xf>(v, v));         // row_ror 8
+  v = fmaxf(v, dpp_mov<0x142, 0xa>(-INFINITY, v)); // row_bcast 15
+  v = fmaxf(v, dpp_mov<0x143, 0xc>(-INFINITY, v)); // row_bcast 31
+  return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 63));
 }
 __device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
-  return v;
+  v += dpp_mov<0xB1, 0xf>(v, v);
+  v += dpp_mov<0x4E, 0xf>(v, v);
+  v += dpp_mov<0x124, 0xf>(v, v);
+  v += dpp_mov<0x128, 0xf>(v, v);
+  v += dpp_mov<0x142, 0xa>(0.0f, v);
+  v += dpp_mov<0x143, 0xc>(0.0f, v);
+  return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 63));
 }
 
 // 1 / (log2(e)^-1 sqrt(head_dim)): scores are kept in the log2 domain.
@@ -212,7 +228,7 @@ struct MfmaTile {
   // Computes the tile into `kv` (LDS, [MT][KLD] bf16).  hrow[r]: residual row of
   // staged token (tid>>3)+64r, offset by 8*(tid&7) (any readable row if !valid[r]).
   // gam: gamma in LDS ([d] bf16).
-  static __device__ void run(const uint16_t* const (&hrow)[CPT], const bool (&valid)[CPT], const uint16_t* gam,
+  static __device__ __forceinline__ void run(const uint16_t* const (&hrow)[CPT], const bool (&valid)[CPT], const uint16_t* gam,
                              int d, float eps, const Half (&halves)[2], uint16_t* hst, float* rinv, const int* pos,
                              const double* rev, uint16_t* kv) {
     const int tid = threadIdx.x, lane = tid & 63, sub = tid & 7;
@@ -419,7 +435,7 @@ struct F32Tile {
   static constexpr int HLD = h_ld<float>();
   static constexpr int KLD = kv_ld<float>(HD);
 
-  static __device__ void run(const float* const (&hrow)[CPT], const bool (&valid)[CPT], const float* gamma, int d,
+  static __device__ __forceinline__ void run(const float* const (&hrow)[CPT], const bool (&valid)[CPT], const float* gamma, int d,
                              float eps, const Half (&halves)[2], float* hst, float* rinv, const int* pos,
                              const double* rev, float* kv) {
     const int tid = threadIdx.x, sub = tid & 7;
@@ -559,19 +575,63 @@ template <int E> __device__ __forceinline__ void load_e(const float* p, float (&
   for (int e = 0; e < E; ++e) x[e] = p[e];
 }
 
-// Softmax partial state of one tile of up to 64 keys (rows of `kv`: K in
+// Stored K/V rows row0 .. row0 + n - 1 (n <= NT / 64) of (b, KV head j) copied
+// straight into LDS rows 0 .. n - 1 of `dst` (the K|V row layout of the
+// attention tile) by global-to-LDS loads: one wave per row, 16 bytes per lane,
+// no registers held, so the copy overlaps whatever the workgroup does next.
+// The issuing waves wait for their vector memory counter and the workgroup
+// synchronises before the rows are read.
+template <typename T, int HD>
+__device__ __forceinline__ void prefetch_rows_lds(const T* K, const T* V, size_t row0, int n, T* dst) {
+  constexpr int KLD = kv_ld<T>(HD);
+  constexpr int CH = 16 / sizeof(T);
+  constexpr int CPR = HD / CH;  // 16-byte chunks of a K (or V) row
+  const int w = wave_id(), lane = threadIdx.x & 63;
+  if (w >= n) return;
+#pragma unroll
+  for (int c0 = 0; c0 < 2 * CPR; c0 += 64) {
+    const int ch = c0 + lane;
+    if (ch < 2 * CPR) {
+      const T* src = ch < CPR ? K + (row0 + w) * HD + ch * CH : V + (row0 + w) * HD + (ch - CPR) * CH;
+      __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)src,
+                                       (__attribute__((address_space(3))) void*)(dst + (size_t)w * KLD + c0 * CH),
+                                       16, 0, 0);
+    }
+  }
+}
+
+// Moves n <= kMax K|V rows of the LDS tile from row `from` to row `to` (the
+// ranges may overlap): everything is read before anything is written.
+template <typename T, int HD, int NT, int kMax>
+__device__ __forceinline__ void move_rows(T* kv, int from, int to, int n) {
+  constexpr int KLD = kv_ld<T>(HD);
+  constexpr int CH = 16 / sizeof(T);
+  constexpr int CPR2 = 2 * HD / CH;  // 16-byte chunks of a K|V row
+  static_assert(kMax * CPR2 <= NT, "one chunk per thread");
+  const int r = threadIdx.x / CPR2, ch = threadIdx.x - r * CPR2;
+  uint4 v{};
+  if (r < n) v = *reinterpret_cast<const uint4*>(kv + (size_t)(from + r) * KLD + ch * CH);
+  __syncthreads();
+  if (r < n) *reinterpret_cast<uint4*>(kv + (size_t)(to + r) * KLD + ch * CH) = v;
+  __syncthreads();
+}
+
+// Softmax partial state of one tile of up to 64 * KPL keys (rows of `kv`: K in
 // columns [0, HD), V in [HD, 2 HD)) for the g query heads of one KV head, from
 // the pre-scaled q in LDS: ml = (max, sum of exp2) per head, acc = sum of
 // exp2(s - max) V (Eqs. attn_weights / head_output, restricted to the tile).
 // Work is split into wave-level tasks whose count depends on g and head_dim
 // only, never on the thread count, so every kernel that attends a tile performs
 // the same additions in the same order.
-//  1. partial scores: task (head h, 64-dim part p), lane = key;
+//  1. partial scores: task (head h, 64-dim part p), lane = key (and key + 64);
 //  2. per head: parts summed in order, max, exp2, sum (one wave per head);
 //  3. P V: task (head h, key split ts of attn_ts(g)), lane = head_dim / 64
 //     consecutive output columns; the key splits are then summed in order.
-template <typename T, int HD, int NT>
-__device__ void attend_tile(const T* kv, int n, int rows, int g, char* lds, const AttnLds& L) {
+// For n <= 64 the second key slot adds exact zeros (max with -inf, sum with
+// 0), so KPL = 1 and KPL = 2 give bit-identical results.  rows >= n is the
+// stride of the probabilities in LDS.
+template <typename T, int HD, int NT, int KPL>
+__device__ __forceinline__ void attend_tile(const T* kv, int n, int rows, int g, char* lds, const AttnLds& L) {
   constexpr int KLD = kv_ld<T>(HD);
   constexpr int NW = NT / 64;
   constexpr int P = HD / 64;  // 64-dim parts of a score
@@ -584,47 +644,65 @@ __device__ void attend_tile(const T* kv, int n, int rows, int g, char* lds, cons
   float* ml = reinterpret_cast<float*>(lds + L.ml);
   float* acc = reinterpret_cast<float*>(lds + L.acc);
 
-  for (int task = wave; task < g * P; task += NW) {
-    const int h = task / P, p = task - h * P;
-    float s = 0.0f;
-    if (lane < n) {
-      const T* krow = kv + (size_t)lane * KLD + 64 * p;
-      const float* qh = qs + h * HD + 64 * p;
-      float d[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+  static_assert(KPL == 1 || KPL == 2, "keys per lane");
+  for (int kk = 0; kk < KPL && 64 * kk < n; ++kk) {  // key slot: keys 64 kk + lane
+    for (int task = wave; task < g * P; task += NW) {
+      const int h = task / P, p = task - h * P;
+      const int key = 64 * kk + lane;
+      float s = 0.0f;
+      if (key < n) {
+        const T* krow = kv + (size_t)key * KLD + 64 * p;
+        const float* qh = qs + h * HD + 64 * p;
+        float d[4] = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
-      for (int c = 0; c < 8; ++c) {
-        float k8[8];
-        load8(krow + 8 * c, k8);
-        const float4 qa = *reinterpret_cast<const float4*>(qh + 8 * c);
-        const float4 qb = *reinterpret_cast<const float4*>(qh + 8 * c + 4);
-        float x = d[c & 3];
-        x = fmaf(qa.x, k8[0], x);
-        x = fmaf(qa.y, k8[1], x);
-        x = fmaf(qa.z, k8[2], x);
-        x = fmaf(qa.w, k8[3], x);
-        x = fmaf(qb.x, k8[4], x);
-        x = fmaf(qb.y, k8[5], x);
-        x = fmaf(qb.z, k8[6], x);
-        x = fmaf(qb.w, k8[7], x);
-        d[c & 3] = x;
+        for (int c = 0; c < 8; ++c) {
+          float k8[8];
+          load8(krow + 8 * c, k8);
+          const float4 qa = *reinterpret_cast<const float4*>(qh + 8 * c);
+          const float4 qb = *reinterpret_cast<const float4*>(qh + 8 * c + 4);
+          float x = d[c & 3];
+          x = fmaf(qa.x, k8[0], x);
+          x = fmaf(qa.y, k8[1], x);
+          x = fmaf(qa.z, k8[2], x);
+          x = fmaf(qa.w, k8[3], x);
+          x = fmaf(qb.x, k8[4], x);
+          x = fmaf(qb.y, k8[5], x);
+          x = fmaf(qb.z, k8[6], x);
+          x = fmaf(qb.w, k8[7], x);
+          d[c & 3] = x;
+        }
+        s = (d[0] + d[1]) + (d[2] + d[3]);
       }
-      s = (d[0] + d[1]) + (d[2] + d[3]);
+      red[(kk * g * P + task) * 64 + lane] = s;
     }
-    red[task * 64 + lane] = s;
   }
   __syncthreads();
 
   for (int h = wave; h < g; h += NW) {
-    float s = -INFINITY;
-    if (lane < n) {
-      s = red[(h * P) * 64 + lane];
+    float sk[KPL], pk[KPL];
 #pragma unroll
-      for (int p = 1; p < P; ++p) s += red[(h * P + p) * 64 + lane];
+    for (int kk = 0; kk < KPL; ++kk) {
+      const float* r = red + (size_t)(kk * g * P + h * P) * 64 + lane;
+      sk[kk] = -INFINITY;
+      if (64 * kk + lane < n) {
+        sk[kk] = r[0];
+#pragma unroll
+        for (int p = 1; p < P; ++p) sk[kk] += r[64 * p];
+      }
     }
-    const float m = wave_max(s);
-    const float pr = lane < n ? exp2f(s - m) : 0.0f;
-    const float l = wave_sum(pr);
-    if (lane < rows) S[h * rows + lane] = pr;
+    float mx = sk[0];
+#pragma unroll
+    for (int kk = 1; kk < KPL; ++kk) mx = fmaxf(mx, sk[kk]);
+    const float m = wave_max(mx);
+#pragma unroll
+    for (int kk = 0; kk < KPL; ++kk) pk[kk] = 64 * kk + lane < n ? exp2f(sk[kk] - m) : 0.0f;
+    float ps = pk[0];
+#pragma unroll
+    for (int kk = 1; kk < KPL; ++kk) ps += pk[kk];
+    const float l = wave_sum(ps);
+#pragma unroll
+    for (int kk = 0; kk < KPL; ++kk)
+      if (64 * kk + lane < rows) S[h * rows + 64 * kk + lane] = pk[kk];
     if (lane == 0) {
       ml[2 * h] = m;
       ml[2 * h + 1] = l;
@@ -638,7 +716,20 @@ __device__ void attend_tile(const T* kv, int n, int rows, int g, char* lds, cons
     float a[E];
 #pragma unroll
     for (int e = 0; e < E; ++e) a[e] = 0.0f;
-    for (int t = ts; t < n; t += TS) {
+    int t = ts;
+    for (; t + 3 * TS < n; t += 4 * TS) {  // four keys' reads in flight, then their sums in key order
+      float pr[4], v[4][E];
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        pr[k] = S[h * rows + t + k * TS];
+        load_e<E>(kv + (size_t)(t + k * TS) * KLD + HD + E * lane, v[k]);
+      }
+#pragma unroll
+      for (int k = 0; k < 4; ++k)
+#pragma unroll
+        for (int e = 0; e < E; ++e) a[e] = fmaf(pr[k], v[k][e], a[e]);
+    }
+    for (; t < n; t += TS) {
       const float pr = S[h * rows + t];
       float v[E];
       load_e<E>(kv + (size_t)t * KLD + HD + E * lane, v);
@@ -690,12 +781,17 @@ __device__ __forceinline__ void write_partial(const char* lds, const AttnLds& L,
 // splits): M = max_s m_s, w_s = 2^(m_s - M), out = sum_s w_s acc_s / sum_s w_s l_s.
 // Every sum has a fixed order that does not depend on NT: each output column
 // adds its splits in split order; the denominator is accumulated per lane over
-// splits s = lane, lane + 64, ... and then summed by a fixed wave tree.  NT / HD
-// rows are merged per pass.  lds: cmb_floats(NT, HD) floats.
+// splits s = lane, lane + 64, ... and then summed by the fixed wave tree.  NT / HD
+// rows are merged per pass, splits in blocks of 64.  The (max, sum) pairs of the
+// first kCmbKeep blocks are loaded once and kept in registers, and the waves
+// that own no weights request a block's accumulators while the others compute
+// its weights, so a merge of S <= 64 splits costs about two round trips.
+// lds: cmb_floats(NT, HD) floats.
 template <typename T, int HD, int NT>
-__device__ void combine_rows(const float* ws_acc, const float* ws_ml, T* out, size_t row0, int nrows, int S,
-                             float* lds) {
+__device__ __forceinline__ void combine_rows(const float* ws_acc, const float* ws_ml, T* out, size_t row0, int nrows,
+                                             int S, float* lds) {
   constexpr int RPP = NT / HD;
+  constexpr int KEEP = kCmbKeep;
   static_assert(RPP >= 1 && RPP <= NT / 64, "rows per pass");
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = wave_id();
@@ -706,47 +802,67 @@ __device__ void combine_rows(const float* ws_acc, const float* ws_ml, T* out, si
     const bool mine = wave < RPP && r0 + wave < nrows;  // this wave owns the weights of row r0 + wave
     const bool rv = rr < RPP && r0 + rr < nrows;         // this thread owns column c of row r0 + rr
     const float* mlw = ws_ml + (row0 + r0 + wave) * (size_t)S * 2;
+    // accumulators: a uniform base per block plus a 32-bit per-lane offset
+    const float* abase = ws_acc + (row0 + r0) * (size_t)S * HD;
+    const unsigned aoff = (unsigned)(rr * S * HD + c);
+    float mv[KEEP], lv[KEEP];
+    float M = -INFINITY;
     if (mine) {
-      float m = -INFINITY;
-      for (int s = lane; s < S; s += 64) m = fmaxf(m, load_dev(mlw + 2 * s));
-      m = wave_max(m);
-      if (lane == 0) mL[2 * wave] = m;
+#pragma unroll
+      for (int k = 0; k < KEEP; ++k) {
+        const int s = 64 * k + lane;
+        mv[k] = s < S ? load_dev(mlw + 2 * s) : -INFINITY;
+        lv[k] = s < S ? load_dev(mlw + 2 * s + 1) : 0.0f;
+      }
     }
-    __syncthreads();
     float o = 0.0f, lsum = 0.0f;
-    const float* ap = ws_acc + (row0 + r0 + rr) * (size_t)S * HD + c;
-    for (int s0 = 0; s0 < S; s0 += 64) {
+    for (int s0 = 0, blk = 0; s0 < S; s0 += 64, ++blk) {
+      const int cnt = min(64, S - s0);
+      const float* a = abase + (size_t)s0 * HD;
       if (mine) {
-        const int s = s0 + lane;
-        float w = 0.0f;
-        if (s < S) {
-          w = exp2f(load_dev(mlw + 2 * s) - mL[2 * wave]);
-          lsum = fmaf(load_dev(mlw + 2 * s + 1), w, lsum);
+        if (blk == 0) {  // the maximum over all splits, before the first weight
+          float m = mv[0];
+#pragma unroll
+          for (int k = 1; k < KEEP; ++k) m = fmaxf(m, mv[k]);
+          for (int s = 64 * KEEP + lane; s < S; s += 64) m = fmaxf(m, load_dev(mlw + 2 * s));
+          M = wave_max(m);
         }
+        const int s = s0 + lane;
+        float mk = -INFINITY, lk = 0.0f;
+#pragma unroll
+        for (int k = 0; k < KEEP; ++k)
+          if (blk == k) mk = mv[k], lk = lv[k];
+        if (blk >= KEEP && s < S) mk = load_dev(mlw + 2 * s), lk = load_dev(mlw + 2 * s + 1);
+        const float w = s < S ? exp2f(mk - M) : 0.0f;
+        lsum = fmaf(lk, w, lsum);
         wsh[wave * 64 + lane] = w;
       }
-      __syncthreads();
-      if (rv) {
-        const int cnt = min(64, S - s0);
-        const float* a = ap + (size_t)s0 * HD;
-        const float* wp = wsh + rr * 64;
-        int i = 0;
-        if (cnt == 64) {  // a whole block: all 64 loads in flight, then the sums in split order
-          float x[64];
+      const float* wp = wsh + rr * 64;
+      if (cnt == 64) {  // (uniform) a whole block: all 64 loads in flight before any wait;
+                        // the waves that own no weights reach them at once
+        float x[64];
+        if (rv) {
 #pragma unroll
-          for (int e = 0; e < 64; ++e) x[e] = load_dev(a + (size_t)e * HD);
+          for (int e = 0; e < 64; ++e) x[e] = load_dev(a + (size_t)e * HD + aoff);
+        }
+        __syncthreads();
+        if (rv) {
 #pragma unroll
           for (int e = 0; e < 64; ++e) o = fmaf(x[e], wp[e], o);
-          i = 64;
         }
-        for (; i + 16 <= cnt; i += 16) {
-          float x[16];
+      } else {
+        __syncthreads();
+        if (rv) {
+          int i = 0;
+          for (; i + 16 <= cnt; i += 16) {
+            float y[16];
 #pragma unroll
-          for (int e = 0; e < 16; ++e) x[e] = load_dev(a + (size_t)(i + e) * HD);
+            for (int e = 0; e < 16; ++e) y[e] = load_dev(a + (size_t)(i + e) * HD + aoff);
 #pragma unroll
-          for (int e = 0; e < 16; ++e) o = fmaf(x[e], wp[i + e], o);
+            for (int e = 0; e < 16; ++e) o = fmaf(y[e], wp[i + e], o);
+          }
+          for (; i < cnt; ++i) o = fmaf(load_dev(a + (size_t)i * HD + aoff), wp[i], o);
         }
-        for (; i < cnt; ++i) o = fmaf(load_dev(a + (size_t)i * HD), wp[i], o);
       }
       __syncthreads();
     }
@@ -760,24 +876,32 @@ __device__ void combine_rows(const float* ws_acc, const float* ws_ml, T* out, si
   }
 }
 
-// After a workgroup has written `count` partials of (b, KV head j) with
-// store_dev: returns true in the one workgroup whose partials complete the S of
-// (b, j) (the counter in the workspace is then reset for the next call).  Every
-// thread waits for its device-scope stores to complete before the workgroup
-// counts, so a workgroup that sees the final count and reads with load_dev sees
-// every partial.  No cache-wide write-back or invalidate is needed: other
-// workgroups streaming weights through the same L2 keep them.
-__device__ __forceinline__ bool last_of_splits(int* done, int count, int S, int* flag) {
-  __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0): this thread's partial stores are complete
+// Split-K completion counter of (b, KV head j): one 64-bit word in the
+// workspace.  The low 32 bits count the splits whose partials are written; the
+// high 32 bits count the recompute workgroups that have arrived, and that
+// arrival order hands out the stored tail tiles of a fused call.  Every thread
+// first waits for its own device-scope partial stores to complete; then one
+// thread adds `add` and the value before the add is broadcast to the workgroup.
+// No cache-wide write-back or invalidate is needed, so other workgroups that
+// stream weights through the same L2 keep them.
+__device__ __forceinline__ unsigned long long split_arrive(unsigned long long* ctr, unsigned long long add,
+                                                           unsigned long long* bcast) {
+  __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0)
   __syncthreads();
-  if (threadIdx.x == 0) {
-    const int before = __hip_atomic_fetch_add(done, count, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    const bool last = before + count == S;
-    if (last) __hip_atomic_store(done, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    *flag = last;
-  }
+  if (threadIdx.x == 0) *bcast = __hip_atomic_fetch_add(ctr, add, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   __syncthreads();
-  return *flag != 0;
+  return *bcast;
+}
+
+// True in the one workgroup whose add of `added` completed splits brought the
+// count to S: every partial is then written, and reads with load_dev see them.
+// That workgroup resets the word for the next call (no add can follow: all S
+// splits, hence all arrivals, are counted).
+__device__ __forceinline__ bool split_complete(unsigned long long* ctr, unsigned long long before, unsigned added,
+                                               int S) {
+  const bool last = (unsigned)(before & 0xffffffffull) + added == (unsigned)S;
+  if (last && threadIdx.x == 0) __hip_atomic_store(ctr, 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  return last;
 }
 
 }  // namespace kvd

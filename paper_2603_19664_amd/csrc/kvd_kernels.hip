@@ -344,12 +344,14 @@ template <typename T, int HD, int MT, bool PACKED>
 __global__ __launch_bounds__(kNtTile, 1) void fused_kernel(FusedArgs a, int per_xcd) {
   extern __shared__ __align__(16) char lds[];
   constexpr int NT = kNtTile;
-  constexpr ProjLds PL = proj_lds<T>(HD, MT);
+  constexpr int FR = fold_rows<T>();
+  constexpr ProjLds PL = proj_lds<T>(HD, MT, FR);
   constexpr int CPT = MT * 8 / NT;
   constexpr int KLD = kv_ld<T>(HD);
   static_assert(MT == kTile, "fused chunks are attention tiles");
   const int tid = threadIdx.x;
-  const int n_tail = (a.T_tail + kTile - 1) / kTile;
+  const bool fold = fold_tail<T>(a.n_rec, a.T_tail);
+  const int n_tail = fused_tail_tiles<T>(a.n_rec, a.T_tail);
   const int C = a.n_rec > 0 ? a.n_rec : n_tail;
   const long long item = (long long)(blockIdx.x % kXcds) * per_xcd + blockIdx.x / kXcds;
   if (item >= (long long)a.n_kv * a.B * C) return;
@@ -357,8 +359,18 @@ __global__ __launch_bounds__(kNtTile, 1) void fused_kernel(FusedArgs a, int per_
   const int unit = (int)(item / C);
   const int j = unit / a.B, b = unit - j * a.B;
   const int g = a.n_q / a.n_kv;
-  const AttnLds AL = attn_lds(PL.end, g, HD, MT);
+  const AttnLds AL = attn_lds(PL.end, g, HD, MT + FR);
   T* kv = reinterpret_cast<T*>(lds + PL.kv);
+
+  // A folded tail goes to the last recomputed tile's workgroup: its rows land
+  // in LDS rows MT.. while the tile is being recomputed.
+  const bool tail_here = fold && c == a.n_rec - 1;
+  if constexpr (FR > 0) {
+    if (tail_here)
+      prefetch_rows_lds<T, HD>(static_cast<const T*>(a.tk), static_cast<const T*>(a.tv),
+                               ((size_t)b * a.n_kv + j) * a.tail_t_cap + a.tail_t_off, a.T_tail,
+                               kv + (size_t)MT * KLD);
+  }
 
   load_q<T, HD, NT>(static_cast<const T*>(a.q), b, a.n_q, j, g, reinterpret_cast<float*>(lds + AL.q));
 
@@ -409,62 +421,95 @@ __global__ __launch_bounds__(kNtTile, 1) void fused_kernel(FusedArgs a, int per_
             *reinterpret_cast<const uint4*>(kv + (size_t)row * KLD + half * HD + ch * CH);
       }
     }
-    attend_tile<T, HD, NT>(kv, n, MT, g, lds, AL);
-    write_partial<HD, NT>(lds, AL, a.ws_acc, a.ws_ml, b, a.n_q, j, g, a.S, c);
-    int count = 1;
-    // stored tail tiles assigned to this chunk
-    for (int k = a.n_rec - 1 - c; k < n_tail; k += a.n_rec) {
-      const int r0 = k * kTile;
-      const int nk = min(kTile, a.T_tail - r0);
-      __syncthreads();
-      load_kv_tile<T, HD, NT>(static_cast<const T*>(a.tk), static_cast<const T*>(a.tv), b, a.n_kv, j, a.tail_t_cap,
-                              a.tail_t_off + r0, nk, kv);
-      __syncthreads();
-      attend_tile<T, HD, NT>(kv, nk, MT, g, lds, AL);
-      write_partial<HD, NT>(lds, AL, a.ws_acc, a.ws_ml, b, a.n_q, j, g, a.S, a.n_rec + k);
-      ++count;
+    int nk = n;
+    if constexpr (FR > 0) {
+      if (tail_here) {
+        __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0): this wave's tail row is in LDS
+        __syncthreads();
+        if (n < MT) move_rows<T, HD, NT, FR>(kv, MT, n, a.T_tail);
+        nk = n + a.T_tail;
+      }
     }
-    if (a.out != nullptr &&
-        last_of_splits(a.ws_done + (size_t)b * a.n_kv + j, count, a.S, reinterpret_cast<int*>(lds + AL.cmb)))
-      combine_rows<T, HD, NT>(a.ws_acc, a.ws_ml, static_cast<T*>(a.out), (size_t)b * a.n_q + (size_t)j * g, g, a.S,
-                              reinterpret_cast<float*>(lds + AL.cmb));
+    attend_tile<T, HD, NT, tile_kpl<T>()>(kv, nk, MT + FR, g, lds, AL);
+    write_partial<HD, NT>(lds, AL, a.ws_acc, a.ws_ml, b, a.n_q, j, g, a.S, c);
+    if (a.out != nullptr || n_tail > 0) {
+      // The stored tail tiles go to the first recompute workgroups of (b, j) to
+      // finish: arrival r takes tail tiles r, r + n_rec, ...
+      unsigned long long* ctr = a.ws_done + (size_t)b * a.n_kv + j;
+      auto* bc = reinterpret_cast<unsigned long long*>(lds + AL.ctr);
+      unsigned long long before = split_arrive(ctr, (1ull << 32) + 1, bc);
+      unsigned added = 1;
+      unsigned mine = 0;
+      for (int k = (int)(before >> 32); k < n_tail; k += a.n_rec) {
+        const int r0 = k * kTile;
+        const int nk = min(kTile, a.T_tail - r0);
+        __syncthreads();
+        load_kv_tile<T, HD, NT>(static_cast<const T*>(a.tk), static_cast<const T*>(a.tv), b, a.n_kv, j, a.tail_t_cap,
+                                a.tail_t_off + r0, nk, kv);
+        __syncthreads();
+        attend_tile<T, HD, NT, tile_kpl<T>()>(kv, nk, MT + FR, g, lds, AL);
+        write_partial<HD, NT>(lds, AL, a.ws_acc, a.ws_ml, b, a.n_q, j, g, a.S, a.n_rec + k);
+        ++mine;
+      }
+      if (mine > 0) {
+        before = split_arrive(ctr, mine, bc);
+        added = mine;
+      }
+      if (split_complete(ctr, before, added, a.S) && a.out != nullptr)
+        combine_rows<T, HD, NT>(a.ws_acc, a.ws_ml, static_cast<T*>(a.out), (size_t)b * a.n_q + (size_t)j * g, g,
+                                a.S, reinterpret_cast<float*>(lds + AL.cmb));
+    }
   } else {
     const int r0 = c * kTile;
     const int nk = min(kTile, a.T_tail - r0);
     load_kv_tile<T, HD, NT>(static_cast<const T*>(a.tk), static_cast<const T*>(a.tv), b, a.n_kv, j, a.tail_t_cap,
                             a.tail_t_off + r0, nk, kv);
     __syncthreads();
-    attend_tile<T, HD, NT>(kv, nk, MT, g, lds, AL);
+    attend_tile<T, HD, NT, tile_kpl<T>()>(kv, nk, MT + FR, g, lds, AL);
     write_partial<HD, NT>(lds, AL, a.ws_acc, a.ws_ml, b, a.n_q, j, g, a.S, c);
-    if (a.out != nullptr &&
-        last_of_splits(a.ws_done + (size_t)b * a.n_kv + j, 1, a.S, reinterpret_cast<int*>(lds + AL.cmb)))
-      combine_rows<T, HD, NT>(a.ws_acc, a.ws_ml, static_cast<T*>(a.out), (size_t)b * a.n_q + (size_t)j * g, g, a.S,
-                              reinterpret_cast<float*>(lds + AL.cmb));
+    if (a.out != nullptr) {
+      unsigned long long* ctr = a.ws_done + (size_t)b * a.n_kv + j;
+      const unsigned long long before = split_arrive(ctr, 1, reinterpret_cast<unsigned long long*>(lds + AL.ctr));
+      if (split_complete(ctr, before, 1, a.S))
+        combine_rows<T, HD, NT>(a.ws_acc, a.ws_ml, static_cast<T*>(a.out), (size_t)b * a.n_q + (size_t)j * g, g,
+                                a.S, reinterpret_cast<float*>(lds + AL.cmb));
+    }
   }
 }
 
 // ------------------------------------------------------------------ stored-K/V attention
 
 template <typename T, int HD>
-__global__ __launch_bounds__(kNtAttn) void decode_kernel(AttnArgs a) {
+__global__ __launch_bounds__(kNtAttn) __attribute__((amdgpu_waves_per_eu(4))) void decode_kernel(AttnArgs a) {
   extern __shared__ __align__(16) char lds[];
   constexpr int NT = kNtAttn;
   const int s = blockIdx.x, j = blockIdx.y, b = blockIdx.z;
   const int g = a.n_q / a.n_kv;
-  const AttnLds AL = attn_lds(align_up(sizeof(T) * kTile * kv_ld<T>(HD), 16), g, HD, kTile);
+  constexpr int FR = fold_rows<T>();
+  const AttnLds AL = attn_lds(align_up(sizeof(T) * (kTile + FR) * kv_ld<T>(HD), 16), g, HD, kTile + FR);
   T* kv = reinterpret_cast<T*>(lds);
   const int t0 = s * kTile;
-  const int n = min(kTile, a.T - t0);
+  const int n = s == a.S - 1 ? a.T - t0 : kTile;  // the last tile may hold a folded remainder
+  if constexpr (FR > 0) {
+    if (n > kTile)
+      prefetch_rows_lds<T, HD>(static_cast<const T*>(a.k), static_cast<const T*>(a.v),
+                               ((size_t)b * a.n_kv + j) * a.t_cap + a.t_off + t0 + kTile, n - kTile,
+                               kv + (size_t)kTile * kv_ld<T>(HD));
+  }
   load_kv_tile<T, HD, NT>(static_cast<const T*>(a.k), static_cast<const T*>(a.v), b, a.n_kv, j, a.t_cap,
-                          a.t_off + t0, n, kv);
+                          a.t_off + t0, min(n, kTile), kv);
   load_q<T, HD, NT>(static_cast<const T*>(a.q), b, a.n_q, j, g, reinterpret_cast<float*>(lds + AL.q));
+  if constexpr (FR > 0) __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0): the remainder rows are in LDS
   __syncthreads();
-  attend_tile<T, HD, NT>(kv, n, kTile, g, lds, AL);
+  attend_tile<T, HD, NT, tile_kpl<T>()>(kv, n, kTile + FR, g, lds, AL);
   write_partial<HD, NT>(lds, AL, a.ws_acc, a.ws_ml, b, a.n_q, j, g, a.S, s);
-  if (a.out != nullptr &&
-      last_of_splits(a.ws_done + (size_t)b * a.n_kv + j, 1, a.S, reinterpret_cast<int*>(lds + AL.cmb)))
-    combine_rows<T, HD, NT>(a.ws_acc, a.ws_ml, static_cast<T*>(a.out), (size_t)b * a.n_q + (size_t)j * g, g, a.S,
-                            reinterpret_cast<float*>(lds + AL.cmb));
+  if (a.out != nullptr) {
+    unsigned long long* ctr = a.ws_done + (size_t)b * a.n_kv + j;
+    const unsigned long long before = split_arrive(ctr, 1, reinterpret_cast<unsigned long long*>(lds + AL.ctr));
+    if (split_complete(ctr, before, 1, a.S))
+      combine_rows<T, HD, NT>(a.ws_acc, a.ws_ml, static_cast<T*>(a.out), (size_t)b * a.n_q + (size_t)j * g, g, a.S,
+                              reinterpret_cast<float*>(lds + AL.cmb));
+  }
 }
 
 // Standalone merge (kvd_combine): one workgroup per (b, query head), the same

@@ -48,7 +48,7 @@ struct FusedArgs {
   int dbg_t_cap, dbg_t_off;
   float* ws_acc;
   float* ws_ml;
-  int* ws_done;  // [B][n_kv] split counters (zero between calls)
+  unsigned long long* ws_done;  // [B][n_kv] split counters (zero between calls)
   void* out;
   int d, n_q, n_kv, B, T_rec, n_rec, S;
   float eps;
@@ -66,7 +66,7 @@ struct AttnArgs {
   void* out;
   float* ws_acc;
   float* ws_ml;
-  int* ws_done;
+  unsigned long long* ws_done;
   int B, T, n_q, n_kv, S;
 };
 

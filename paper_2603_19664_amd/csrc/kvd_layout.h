@@ -19,6 +19,34 @@ constexpr int kDepth = 4;       // K-steps of weights / residuals in flight in t
 constexpr int kMtBf16 = 64;
 constexpr int kMtF32 = 64;
 
+// A stored tail of at most fold_rows<T>() rows (a decode step's current token)
+// joins the split of the last recomputed tile of a fused call: the rows are
+// copied into LDS while that tile is recomputed and attended with its keys.
+// Longer tails get one split per 64-row tile.  bf16 only: the fp32 engine's
+// K/V tile leaves no LDS for the extra rows at head_dim 256.
+template <typename T>
+constexpr int fold_rows() { return sizeof(T) == 2 ? 4 : 0; }
+template <typename T>
+constexpr bool fold_tail(int n_rec, int T_tail) { return n_rec > 0 && T_tail > 0 && T_tail <= fold_rows<T>(); }
+// Splits of a stored-K/V attention call over Tk keys: one per 64-key tile, and
+// a remainder of at most fold_rows<T>() keys joins the tile before it (so that a
+// context that is a multiple of 64 plus the current token fills its grid
+// exactly and is chunked as the fused kernel chunks it).
+template <typename T>
+constexpr int decode_splits(int Tk) {
+  const int r = Tk % kTile;
+  return Tk > kTile && r > 0 && r <= fold_rows<T>() ? Tk / kTile : (Tk + kTile - 1) / kTile;
+}
+// Keys per lane of the attention tiles (up to 64 + fold_rows<T>() keys).
+template <typename T>
+constexpr int tile_kpl() { return kTile + fold_rows<T>() > 64 ? 2 : 1; }
+// Splits of a fused call: one per recomputed tile, plus one per tail tile
+// unless the tail is folded.
+template <typename T>
+constexpr int fused_tail_tiles(int n_rec, int T_tail) {
+  return fold_tail<T>(n_rec, T_tail) ? 0 : (T_tail + kTile - 1) / kTile;
+}
+
 // Streaming projection (current-token q/K/V): tokens per workgroup.
 constexpr int kProjTok = 16;
 constexpr int kProjPrefetch = 8;  // K-steps of weights in flight per wave
@@ -38,23 +66,38 @@ constexpr int h_ld(void) { return kKT + Pad<T>::h; }
 
 // LDS layout of the attention part (decode / fused kernels); g = group size.
 struct AttnLds {
-  size_t q, s, red, ml, acc, cmb, end;
+  size_t q, s, red, ml, acc, cmb, ctr, end;
 };
-// LDS floats of the split merge (combine_rows): rows-per-pass x (64 weights + 2).
+// Split merge (combine_rows): blocks of 64 splits; the (max, sum) pairs of the
+// first kCmbKeep blocks stay in registers.  LDS floats: rows-per-pass x (64
+// weights + max and sum).
+constexpr int kCmbKeep = 2;
 constexpr size_t cmb_floats(int nt, int hd) { return (size_t)(nt / hd) * 66; }
 // Key splits of the P V phase of a tile's attention: fixed by the group size
 // alone, so that kernels with different thread counts add in the same order.
 constexpr int attn_ts(int g) { return g >= 8 ? 1 : 8 / g; }
-constexpr size_t red_floats(int g, int hd) { return (size_t)attn_ts(g) * g * hd; }
-constexpr AttnLds attn_lds(size_t base, int g, int hd, int rows) {
+// Scratch of a tile's attention: the scores of up to 64 keys per (head, 64-dim
+// part) per pass over `rows`, then the P V partial sums of the key splits.
+constexpr size_t red_floats(int g, int hd, int rows) {
+  const size_t sc = (size_t)((rows + 63) / 64) * g * hd;
+  const size_t pv = (size_t)attn_ts(g) * g * hd;
+  return sc > pv ? sc : pv;
+}
+// q, probabilities, the scratch `red` (scores, then P V partial sums), (max,
+// sum), the split counter's broadcast.  The tile's output `acc` is the first
+// slice of `red` (its final sum reads every slice of a column before writing
+// it), and the split merge, which runs after all tiles, reuses `red` as well.
+__attribute__((always_inline)) constexpr AttnLds attn_lds(size_t base, int g, int hd, int rows) {
   AttnLds L{};
   L.q = align_up(base, 16);
   L.s = align_up(L.q + sizeof(float) * g * hd, 16);
   L.red = align_up(L.s + sizeof(float) * g * rows, 16);
-  L.ml = align_up(L.red + sizeof(float) * red_floats(g, hd), 16);
-  L.acc = align_up(L.ml + sizeof(float) * 2 * g, 16);
-  L.cmb = align_up(L.acc + sizeof(float) * g * hd, 16);
-  L.end = align_up(L.cmb + sizeof(float) * cmb_floats(512, hd), 16);
+  const size_t rf = red_floats(g, hd, rows), cf = cmb_floats(512, hd);
+  L.acc = L.red;
+  L.cmb = L.red;
+  L.ml = align_up(L.red + sizeof(float) * (rf > cf ? rf : cf), 16);
+  L.ctr = align_up(L.ml + sizeof(float) * 2 * g, 16);  // split counter broadcast
+  L.end = align_up(L.ctr + sizeof(unsigned long long), 16);
   return L;
 }
 
@@ -65,16 +108,19 @@ constexpr AttnLds attn_lds(size_t base, int g, int hd, int rows) {
 struct ProjLds {
   size_t hst, kv, rinv, pos, rev, end;
 };
+// `extra` rows after the tile's mt are filled during the K-loop (a folded tail),
+// so the tile is placed to keep them clear of the staging buffers.
 template <typename T>
-constexpr ProjLds proj_lds(int hd, int mt) {
+constexpr ProjLds proj_lds(int hd, int mt, int extra = 0) {
   ProjLds L{};
   L.rev = 0;                                                       // double[kMaxPairs]
   L.rinv = align_up(L.rev + sizeof(double) * kMaxPairs, 16);        // float[mt]
   L.pos = align_up(L.rinv + sizeof(float) * mt, 16);                // int[mt]
   L.hst = align_up(L.pos + sizeof(int) * mt, 16);
   size_t hst_end = L.hst + (sizeof(T) == 2 ? sizeof(T) * kDepth * mt * kKT : sizeof(T) * 2 * mt * h_ld<T>());
-  L.kv = L.hst;                                                     // T[mt][kv_ld]
-  size_t kv_end = L.kv + sizeof(T) * mt * kv_ld<T>(hd);
+  const size_t row = sizeof(T) * kv_ld<T>(hd);
+  L.kv = extra > 0 && L.hst + mt * row < hst_end ? hst_end - mt * row : L.hst;  // T[mt + extra][kv_ld]
+  size_t kv_end = L.kv + row * (mt + extra);
   L.end = align_up(hst_end > kv_end ? hst_end : kv_end, 16);
   return L;
 }
@@ -84,13 +130,13 @@ constexpr size_t gamma_lds_bytes(int d) { return align_up((size_t)2 * d, 16); }
 
 template <typename T>
 constexpr size_t decode_lds_bytes(int g, int hd) {
-  // K/V tile followed by the attention scratch.
-  return attn_lds(align_up(sizeof(T) * kTile * kv_ld<T>(hd), 16), g, hd, kTile).end;
+  // K/V tile (with room for a folded remainder) followed by the attention scratch.
+  return attn_lds(align_up(sizeof(T) * (kTile + fold_rows<T>()) * kv_ld<T>(hd), 16), g, hd, kTile + fold_rows<T>()).end;
 }
 
 template <typename T>
 constexpr size_t fused_lds_bytes(int g, int hd, int mt) {
-  return attn_lds(proj_lds<T>(hd, mt).end, g, hd, mt).end;
+  return attn_lds(proj_lds<T>(hd, mt, fold_rows<T>()).end, g, hd, mt + fold_rows<T>()).end;
 }
 
 // Streaming projection: h-bar of kProjTok tokens for the whole d, gamma, 1/rms,

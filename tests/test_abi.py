@@ -24,7 +24,7 @@ def view(t_cap=16, t_off=0, k=FAKE, v=FAKE):
 
 
 def test_loads_and_version():
-    assert kvd.abi_version() == 3
+    assert kvd.abi_version() == 4
     assert kvd.status_str(kvd.KVD_ERR_ALIGN) == "KVD_ERR_ALIGN"
 
 
@@ -127,16 +127,27 @@ def test_project_validation():
 
 def test_split_policy_and_workspace():
     s = shape()
-    # one 64-key split per tile; the fused kernel adds the tail's tiles
-    assert lib.kvd_num_splits(ctypes.byref(s), kvd.KVD_OP_DECODE_ATTN, 1, 4097, 0) == 65
-    assert lib.kvd_num_splits(ctypes.byref(s), kvd.KVD_OP_FUSED, 1, 4096, 1) == 65
-    assert lib.kvd_num_splits(ctypes.byref(s), kvd.KVD_OP_FUSED, 1, 0, 1) == 1
+    # one 64-key split per tile; a bf16 tail of <= 4 rows joins the fused kernel's
+    # last recomputed tile, a longer one (or any fp32 tail) adds its own tiles
+    ns = lambda sh, op, T, Tt: lib.kvd_num_splits(ctypes.byref(sh), op, 1, T, Tt)
+    assert ns(s, kvd.KVD_OP_DECODE_ATTN, 4097, 0) == 64      # 1..4 remaining keys join the last tile (bf16)
+    assert ns(s, kvd.KVD_OP_DECODE_ATTN, 4100, 0) == 64
+    assert ns(s, kvd.KVD_OP_DECODE_ATTN, 4101, 0) == 65
+    assert ns(s, kvd.KVD_OP_DECODE_ATTN, 4, 0) == 1
+    assert ns(s, kvd.KVD_OP_DECODE_ATTN, 68, 0) == 1
+    assert ns(shape(dtype=kvd.KVD_F32), kvd.KVD_OP_DECODE_ATTN, 4097, 0) == 65
+    assert ns(s, kvd.KVD_OP_FUSED, 4096, 1) == 64
+    assert ns(s, kvd.KVD_OP_FUSED, 4096, 4) == 64
+    assert ns(s, kvd.KVD_OP_FUSED, 4096, 5) == 65
+    assert ns(s, kvd.KVD_OP_FUSED, 4000, 70) == 65
+    assert ns(shape(dtype=kvd.KVD_F32), kvd.KVD_OP_FUSED, 4096, 1) == 65
+    assert ns(s, kvd.KVD_OP_FUSED, 0, 1) == 1
     assert lib.kvd_num_splits(ctypes.byref(s), kvd.KVD_OP_DECODE_ATTN, 1, 0, 0) == 0
     n = lib.kvd_workspace_bytes(ctypes.byref(s), kvd.KVD_OP_DECODE_ATTN, 2, 100, 0)
     S = 2
     acc = -(-2 * 8 * S * 256 * 4 // 256) * 256
     ml = -(-2 * 8 * S * 2 * 4 // 256) * 256
-    done = -(-2 * 4 * 4 // 256) * 256  # split counters [B][n_kv] int32
+    done = -(-2 * 4 * 8 // 256) * 256  # split counters [B][n_kv] uint64
     assert n == acc + ml + done
     assert lib.kvd_workspace_bytes(ctypes.byref(s), 9, 1, 10, 0) == 0
 

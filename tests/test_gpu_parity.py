@@ -219,12 +219,20 @@ def test_fused_and_decode_time_kv_bitwise(dtype):
 
 
 def test_fused_equals_unfused_bitwise_on_shared_chunking():
-    # with the context a multiple of the 64-key tile, both paths attend identical
-    # K/V in identical chunks, so the outputs agree bit for bit.
+    # Recomputing rows 0..191 and reading rows 192..256 (the last context tile
+    # plus the current token) as a stored tail gives the fused kernel the same
+    # 64-key chunks as decode_attn over all 257 keys: identical arithmetic, so the
+    # outputs agree bit for bit.
     L = make_layer(C.GEMMA3_4B, B=2, T=256, seed=23, d_model=512)
-    q, _, _, out = gpu_unfused(L)
-    _, _, outf, _ = gpu_fused(L)
+    q, K, V, out = gpu_unfused(L)
+    ws = kvd.workspace(L.shape, kvd.KVD_OP_FUSED, L.B, 192, 65)
+    outf = torch.empty_like(out)
+    kvd.kvd_fused_recompute_attn(L.shape, q, L.h, 192, L.gamma, L.lw_k, L.lw_v, L.pos0, outf, ws, K, V, 65, 192)
     assert torch.equal(_bits(out), _bits(outf))
+    # budget 0: the current token joins the last 64-key tile on both paths
+    _, _, outc, _ = gpu_fused(L, q=q)
+    assert kvd.kvd_num_splits(L.shape, kvd.KVD_OP_DECODE_ATTN, L.B, 257) == 4
+    assert torch.equal(_bits(out), _bits(outc))
 
 
 def test_cached_attn_matches_decode_attn():
@@ -254,6 +262,45 @@ def test_partials_then_combine_equals_one_call():
     out3 = torch.empty_like(outd)
     kvd.kvd_combine(s, L.B, kvd.kvd_num_splits(s, kvd.KVD_OP_DECODE_ATTN, L.B, L.T + 1), wsd, out3)
     assert torch.equal(_bits(outd), _bits(out3))
+
+
+@pytest.mark.parametrize("dtype", [BF, F32])
+@pytest.mark.parametrize("T_rec,T", [(130, 430), (0, 200), (64, 384), (200, 260), (126, 129), (128, 131), (61, 64),
+                                     (64, 66)])
+def test_hybrid_budget_stored_window(dtype, T_rec, T):
+    # Algorithm 1 with a cache budget: the T - T_rec most recent context tokens
+    # keep stored K/V (the library's own, bit-identical to what prefill stores)
+    # and form the tail with the current token; the older T_rec are recomputed
+    # in the kernel.  (130, 430) has more tail tiles than recompute tiles, so
+    # some workgroups attend two tail tiles; (0, 200) is tail-only.  Tails of
+    # <= 4 rows join the last recomputed tile in bf16: after a full tile
+    # (128, 131), or moved down over a partial one, overlapping (126, 129) or not
+    # (61, 64), (64, 66).
+    kw = dict(d_model=512) if dtype == BF else dict(d_model=512, n_q=8, n_kv=4, head_dim=64)
+    L = make_layer(C.GEMMA3_4B if dtype == BF else C.SMOLLM_FP32, B=2, T=T, seed=40 + T_rec, pos0=[3, 250], **kw)
+    s, tol = L.shape, TOL[dtype]
+    q, K, V, out_u = gpu_unfused(L)   # K/V rows 0..T-1 recomputed, row T the current token
+    T_tail = T - T_rec + 1
+
+    def fused(out, ws):
+        kvd.kvd_fused_recompute_attn(s, q, L.h, T_rec, L.gamma, L.lw_k, L.lw_v, L.pos0, out, ws, K, V, T_tail, T_rec)
+
+    ws = kvd.workspace(s, kvd.KVD_OP_FUSED, L.B, T_rec, T_tail)
+    out = torch.empty_like(q)
+    fused(out, ws)
+    check("hybrid fused vs oracle", out, oracle_decode(L), tol)
+    check("hybrid fused vs unfused", out, f64(out_u), tol)
+    if T_rec % 64 == 0 and kvd.kvd_num_splits(s, kvd.KVD_OP_FUSED, L.B, T_rec, T_tail) == -(-(T + 1) // 64):
+        assert torch.equal(_bits(out), _bits(out_u))  # identical 64-key chunking: identical arithmetic
+    out2 = torch.empty_like(q)
+    fused(out2, ws)  # the workspace's counters were left zero
+    assert torch.equal(_bits(out), _bits(out2))
+    fused(None, ws)  # partials only (the tail tiles still handed out by arrival)
+    out3 = torch.empty_like(q)
+    kvd.kvd_combine(s, L.B, kvd.kvd_num_splits(s, kvd.KVD_OP_FUSED, L.B, T_rec, T_tail), ws, out3)
+    assert torch.equal(_bits(out), _bits(out3))
+    ctr_bytes = -(-L.B * s.n_kv_heads * 8 // 256) * 256  # the split counters close the workspace
+    assert int(torch.count_nonzero(ws[-ctr_bytes:])) == 0
 
 
 @pytest.mark.parametrize("hd", [64, 128, 256])
