@@ -119,7 +119,7 @@ kvd_status check_ws(const kvd_attn_shape* s, int32_t B, int32_t S, void* ws, siz
   return KVD_OK;
 }
 
-constexpr size_t kLdsLimit = 160 * 1024;  // LDS per workgroup on gfx950
+constexpr size_t kLdsLimit = kvd::kLdsPerGroup;
 
 template <typename T>
 size_t attn_lds_need(const kvd_attn_shape* s, bool fused) {
@@ -258,8 +258,14 @@ kvd_status kvd_project_qkv(const kvd_attn_shape* shape, const void* h_new, const
                            const kvd_kv_view* kv_out, void* stream) {
   KVD_TRY(check_shape(shape));
   KVD_TRY(check_batch(B));
-  KVD_TRY(check_lds_bytes(shape->dtype == KVD_BF16 ? kvd::stream_lds(shape->d_model).end : recompute_lds(shape),
-                          "kvd_project_qkv"));
+  if (shape->dtype == KVD_BF16) {
+    // the streaming kernel holds its weight ring and at least one residual row
+    if (B > 0 && kvd::stream_group(shape->d_model, B, kLdsLimit) < 1)
+      return fail(KVD_ERR_UNSUPPORTED, "kvd_project_qkv needs %zu bytes of LDS for d_model=%d (limit %zu)",
+                  kvd::stream_lds(shape->d_model, 1).end, shape->d_model, kLdsLimit);
+  } else {
+    KVD_TRY(check_lds_bytes(recompute_lds(shape), "kvd_project_qkv"));
+  }
   if (B == 0) return KVD_OK;
   KVD_TRY(check_ptr(h_new, "h_new"));
   KVD_TRY(check_ptr(gamma, "gamma"));

@@ -182,6 +182,10 @@ struct Half {
 
 __device__ __forceinline__ int wave_id() { return __builtin_amdgcn_readfirstlane(threadIdx.x >> 6); }
 
+// s_waitcnt immediate that waits until at most n (< 64) vector memory operations
+// of the wave are outstanding (expcnt and lgkmcnt left unconstrained).
+constexpr int vmcnt_imm(int n) { return (n & 15) | ((n >> 4) << 14) | 0x0f70; }
+
 // Element offset of the MFMA A operand chunk (K-step s, 16-wide substep u) from a
 // lane's base pointer.  Row-major: base = row (row0 + lane % 32), column 8 (lane / 32);
 // packed (kvd_pack_weights): base = block row row0 + lane * 8, one 512-element

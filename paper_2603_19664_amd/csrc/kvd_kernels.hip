@@ -2,9 +2,10 @@
 //
 //   proj_kernel         RMSNorm + projection + RoPE of token tiles (RECOMPUTE_KV /
 //                       prefill; also the fp32 current-token projection).
-//   stream_proj_kernel  bf16 current-token q, K_t, V_t of a decode step: one wave per
-//                       32 weight rows streams its rows with deep prefetch (a GEMV
-//                       shape), on the same per-element arithmetic as proj_kernel.
+//   stream_proj_kernel  bf16 current-token q, K_t, V_t of a decode step (a GEMV
+//                       shape): four waves per 32 weight rows stream them into an
+//                       LDS ring, one runs the MFMA chain; the same per-element
+//                       arithmetic as proj_kernel.
 //   fused_kernel        per (b, KV head, 64-key chunk): recompute K/V of the chunk
 //                       into LDS and emit its split-K softmax partial without writing
 //                       K/V to HBM; stored tail tiles (CONCAT) ride along.
@@ -120,28 +121,44 @@ __global__ __launch_bounds__(kNtTile, 1) void proj_kernel(ProjArgs a, int per_xc
 
 // ------------------------------------------------------------------ streaming current-token projection
 
-// One wave per workgroup.  blockIdx.x: a 32-row block of [W_q rows | W_k rows |
-// W_v rows]; blockIdx.y: a group of kProjTok sequences.  The group's gamma-scaled
-// residuals (and 1/rms) are staged into LDS once; the wave then streams its 32
-// weight rows with kProjPrefetch K-steps in flight.  Per output element the
-// arithmetic is MfmaTile's (same MFMA chain over d, same 1/rms, same epilogue),
-// so K_t / V_t equal what recompute gives for the same row.
-template <int HD, bool PACKED, int NS>
-__global__ __launch_bounds__(64) void stream_proj_kernel(ProjArgs a, int q_blocks, int k_blocks) {
+// One workgroup of kStreamWaves waves per 32 weight rows.  blockIdx.x: a 32-row
+// block of [W_q rows | W_k rows | W_v rows]; blockIdx.y: a group of G sequences.
+// Waves 1.. (the loaders) each keep their share of kStreamDepth chunks of the
+// rows' MFMA A fragments (1 KiB each) in flight in registers; wave 0 runs the
+// MFMA chain over d and issues no global loads in its loop.  Barrier c: the
+// loaders have written chunk c + 1 into the LDS ring (slot (c + 1) % NR, whose
+// previous chunk wave 0 read before barrier c - 2); after it wave 0 reads chunk
+// c + 1 while chunk c's MFMAs run.  The loaders also carry the tokens' sums of
+// squares along, chunk by chunk, and write 1/rms before the last barrier: only
+// the epilogue needs it.  Per output element the arithmetic is MfmaTile's (the
+// same MFMA chain over d, the same sum-of-squares chain, 1/rms and epilogue), so
+// K_t / V_t equal what recompute gives for the same row.  NCH > 0: the chunk
+// count, fixed at compile time so that the loaders' loop is straight-line code
+// (their memory-counter waits then keep every chunk in flight).
+template <int HD, bool PACKED, int NCH>
+__global__ __launch_bounds__(64 * kStreamWaves) void stream_proj_kernel(ProjArgs a, int q_blocks, int k_blocks,
+                                                                        int G) {
   extern __shared__ __align__(16) char lds[];
-  constexpr int PD = kProjPrefetch;
-  const int lane = threadIdx.x, sub = lane & 7;
+  constexpr int NW = kStreamWaves, CK = kStreamChunk, NR = kStreamSlots, D = kStreamDepth;
+  constexpr int FPC = 4 * CK;          // A fragments per chunk
+  constexpr int LPW = FPC / (NW - 1);  // fragments per loader wave per chunk
+  static_assert(FPC % (NW - 1) == 0 && NR >= 3, "ring");
+  static_assert(8 * (NW - 1) >= kProjTok, "a sum-of-squares row per 8 loader lanes");
+  const int tid = threadIdx.x, lane = tid & 63, w = wave_id();
   const int d = a.d;
-  const StreamLds SL = stream_lds(d);
+  const StreamLds SL = stream_lds(d, G);
   const int HLD = stream_h_ld(d);
   double* rev = reinterpret_cast<double*>(lds + SL.rev);
   float* rinv = reinterpret_cast<float*>(lds + SL.rinv);
   int* pos = reinterpret_cast<int*>(lds + SL.pos);
+  uint16_t* gl = reinterpret_cast<uint16_t*>(lds + SL.gam);
+  uint16_t* ring = reinterpret_cast<uint16_t*>(lds + SL.ring);
   uint16_t* hb = reinterpret_cast<uint16_t*>(lds + SL.hb);
+  uint16_t* hs = reinterpret_cast<uint16_t*>(lds + SL.hs);
 
   const int blk = blockIdx.x;
-  const int b0 = blockIdx.y * kProjTok;
-  const int nt = min(kProjTok, a.B - b0);
+  const int b0 = blockIdx.y * G;
+  const int nt = min(G, a.B - b0);
   const uint16_t* W;
   int row0, rope, mat;  // mat: 0 q, 1 k, 2 v
   if (blk < q_blocks) {
@@ -151,154 +168,169 @@ __global__ __launch_bounds__(64) void stream_proj_kernel(ProjArgs a, int q_block
   } else {
     W = static_cast<const uint16_t*>(a.w_v); row0 = 32 * (blk - q_blocks - k_blocks); rope = 0; mat = 2;
   }
-
+  // lane l's 16 bytes of A fragment (K-step s, substep k): row l % 32, columns
+  // 16 k + 8 (l / 32) of the K-step (packed: the fragment's contiguous 1 KiB)
   const uint16_t* wrow = PACKED ? W + (size_t)row0 * d + 8 * lane : W + (size_t)(row0 + (lane & 31)) * d + 8 * (lane >> 5);
-  const int nsteps = NS > 0 ? NS : d / kKT;  // NS > 0: K-step count fixed at compile time (straight-line loop)
-  bf16x8_t ring[PD][4];
-
-  // Stage the group's raw residual rows and gamma into LDS with every lane and
-  // all loads of a batch in flight, then form gamma * h (bf16) and the sums of
-  // squares in place: lane -> rows (lane>>3) + 8r, column chunk sub, K-steps in
-  // order (the same per-element arithmetic and summation order as the tile engine).
-  uint16_t* gl = reinterpret_cast<uint16_t*>(lds + SL.gam);
-  {
-    const int cpr = d / 8;                 // 16-byte chunks per row
-    const int n_h = nt * cpr, total = n_h + cpr;
-    // chunk i of [rows of present tokens | gamma]; lanes past the end repeat the last chunk
-    struct Chunk { const uint16_t* src; uint16_t* dst; };
-    auto locate = [&](int i) {
-      i = min(i, total - 1);
-      const int r = i / cpr, ch = i - r * cpr;  // gamma chunks: r == nt, ch == i - n_h
-      const bool is_h = r < nt;
-      return Chunk{is_h ? static_cast<const uint16_t*>(a.h) + (size_t)(b0 + r) * d + 8 * ch
-                        : static_cast<const uint16_t*>(a.gamma) + 8 * ch,
-                   is_h ? hb + (size_t)r * HLD + 8 * ch : gl + 8 * ch};
-    };
-    // first batch, then the weight ring's first PD K-steps (independent of the
-    // residuals; issued after the batch so that waiting for the batch does not
-    // wait for them), then the rest
-    constexpr int B0 = 10, BATCH = 8;
-    {
-      u32x4_t v[B0];
+  const int nsteps = d / kKT;
+  const int nchunks = NCH > 0 ? NCH : (nsteps + CK - 1) / CK;
+  const int ld = w - 1;  // loader index (waves 1..)
+  u32x4_t wr[D][LPW];    // loaders: chunks in flight, chunk c in wr[c % D]
+  auto load_chunk = [&](u32x4_t (&rv)[LPW], int c) {
 #pragma unroll
-      for (int k = 0; k < B0; ++k) v[k] = *reinterpret_cast<const u32x4_t*>(locate(64 * k + lane).src);
-#pragma unroll
-      for (int u = 0; u < PD; ++u)
-#pragma unroll
-        for (int k = 0; k < 4; ++k)
-          ring[u][k] = *reinterpret_cast<const bf16x8_t*>(wrow + w_off<PACKED>(min(u, nsteps - 1), k));
-#pragma unroll
-      for (int k = 0; k < B0; ++k) *reinterpret_cast<u32x4_t*>(locate(64 * k + lane).dst) = v[k];
+    for (int i = 0; i < LPW; ++i) {
+      const int f = min(c * FPC + ld * LPW + i, 4 * nsteps - 1);
+      rv[i] = *reinterpret_cast<const u32x4_t*>(wrow + w_off<PACKED>(f >> 2, f & 3));
     }
-    for (int i0 = 64 * B0; i0 < total; i0 += 64 * BATCH) {
-      u32x4_t v[BATCH];
+  };
+  auto store_chunk = [&](const u32x4_t (&rv)[LPW], int c) {
+    uint16_t* slot = ring + (size_t)(c % NR) * FPC * 512 + 8 * lane;
 #pragma unroll
-      for (int k = 0; k < BATCH; ++k) v[k] = *reinterpret_cast<const u32x4_t*>(locate(i0 + 64 * k + lane).src);
-#pragma unroll
-      for (int k = 0; k < BATCH; ++k) *reinterpret_cast<u32x4_t*>(locate(i0 + 64 * k + lane).dst) = v[k];
-      // all of the batch's loads before its LDS writes
-      __builtin_amdgcn_sched_group_barrier(0x020, BATCH, 0);
-      __builtin_amdgcn_sched_group_barrier(0x200, BATCH, 0);
-    }
-    __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): the wave's own LDS writes are done
-    // sums of squares: lane -> rows (lane>>3) + 8r of present tokens, column chunk sub,
-    // K-steps in order (the tile engine's per-thread chain), read from the raw rows
-    float ss[2] = {0.0f, 0.0f};
-    const uint16_t* hrow0 = hb + (size_t)(lane >> 3) * HLD + 8 * sub;
-#pragma unroll
-    for (int r = 0; r < 2; ++r) {
-      if ((lane >> 3) + 8 * r < nt) {
-        const uint16_t* hr = hrow0 + (size_t)(8 * r) * HLD;
-        for (int s0 = 0; s0 < nsteps; s0 += 8) {
-          uint4 x[8];
-#pragma unroll
-          for (int j = 0; j < 8; ++j) x[j] = *reinterpret_cast<const uint4*>(hr + (size_t)min(s0 + j, nsteps - 1) * kKT);
-#pragma unroll
-          for (int j = 0; j < 8; ++j)
-            if (s0 + j < nsteps) sumsq_chunk_bf16(x[j], ss[r]);
-        }
-      }
-    }
-    // gamma * h -> bf16 in place, spread over all lanes (present rows only)
-    for (int i = lane; i < n_h; i += 64) {
+    for (int i = 0; i < LPW; ++i)
+      *reinterpret_cast<u32x4_t*>(slot + (ld * LPW + i) * 512) = rv[i];
+  };
+  // gamma * h -> bf16 into hs (present rows only), by wave 0
+  auto scale_rows = [&]() {
+    const int cpr = d / 8;
+    for (int i = lane; i < nt * cpr; i += 64) {
       const int r = i / cpr, ch = i - r * cpr;
-      uint4* ptr = reinterpret_cast<uint4*>(hb + (size_t)r * HLD + 8 * ch);
-      *ptr = scale_chunk_bf16(*ptr, *reinterpret_cast<const uint4*>(gl + 8 * ch));
+      *reinterpret_cast<uint4*>(hs + (size_t)r * HLD + 8 * ch) =
+          scale_chunk_bf16(*reinterpret_cast<const uint4*>(hb + (size_t)r * HLD + 8 * ch),
+                           *reinterpret_cast<const uint4*>(gl + 8 * ch));
     }
-#pragma unroll
-    for (int r = 0; r < 2; ++r) {
-      float v = ss[r];
-      v += __shfl_xor(v, 1, 64);
-      v += __shfl_xor(v, 2, 64);
-      v += __shfl_xor(v, 4, 64);
-      const int row = (lane >> 3) + 8 * r;
-      if (sub == 0) rinv[row] = row < nt ? 1.0f / sqrtf(v / (float)d + a.eps) : 0.0f;
-    }
-  }
-  for (int i = lane; i < HD / 2; i += 64) rev[i] = a.rev[i];
-  for (int r = lane; r < kProjTok; r += 64) pos[r] = r < nt ? a.pos0[b0 + r] : 0;
-  __syncthreads();
-
-  // MFMA over d: A = 32 weight rows, B = the group's tokens.  Columns >= kProjTok
-  // repeat columns col - kProjTok and columns of absent tokens hold unused values:
-  // MFMA output columns are independent and only those of present tokens are stored.
-  const int col = lane & 31;
-  const uint16_t* hcol = hb + (size_t)(col % kProjTok) * HLD + 8 * (lane >> 5);
+  };
   f32x16_t acc;
 #pragma unroll
   for (int i = 0; i < 16; ++i) acc[i] = 0.0f;
-  // B fragments of the next K-step are read while the current step's MFMAs run.
-  bf16x8_t bcur[4], bnxt[4];
-  auto read_b = [&](bf16x8_t (&bv)[4], int s) {
-#pragma unroll
-    for (int k = 0; k < 4; ++k) bv[k] = *reinterpret_cast<const bf16x8_t*>(hcol + (size_t)s * kKT + 16 * k);
-  };
-  auto consume = [&](int u, int s) {
-    read_b(bnxt, min(s + 1, nsteps - 1));
-#pragma unroll
-    for (int k = 0; k < 4; ++k) acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ring[u][k], bcur[k], acc, 0, 0, 0);
-#pragma unroll
-    for (int k = 0; k < 4; ++k) bcur[k] = bnxt[k];
-  };
-  read_b(bcur, 0);
-  if constexpr (NS > 0) {
-#pragma unroll
-    for (int s = 0; s < NS; ++s) {
-      consume(s % PD, s);
-      if (s + PD < NS) {
-#pragma unroll
-        for (int k = 0; k < 4; ++k)
-          ring[s % PD][k] = *reinterpret_cast<const bf16x8_t*>(wrow + w_off<PACKED>(s + PD, k));
+
+  // The two roles run separate code paths with the same sequence of barriers, so
+  // that the loaders' memory-counter waits are exact.
+  if (w > 0) {
+    // The residual rows of the group and gamma straight into LDS (global-to-LDS,
+    // one instruction per 1 KiB of a row, rows spread over the loaders), then the
+    // first two chunks of weights.  A barrier after global-to-LDS copies waits
+    // for every outstanding load, so the remaining chunks are issued after it
+    // (while wave 0 scales the rows).
+    {
+      const int cpr = d / 8;  // 16-byte chunks per row
+      for (int r = ld; r <= nt; r += NW - 1) {
+        const uint16_t* src = (r < nt ? static_cast<const uint16_t*>(a.h) + (size_t)(b0 + r) * d
+                                      : static_cast<const uint16_t*>(a.gamma)) + 8 * lane;
+        uint16_t* dst = r < nt ? hb + (size_t)r * HLD : gl;
+        for (int ch0 = 0; ch0 < cpr; ch0 += 64)
+          if (ch0 + lane < cpr)
+            __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)(src + 8 * ch0),
+                                             (__attribute__((address_space(3))) void*)(dst + 8 * ch0), 16, 0, 0);
       }
-      // keep each step's refill where it is issued (PD steps ahead of its use)
-      __builtin_amdgcn_sched_barrier(0);
     }
-  } else {
-  // steady state: unconditional refills keep PD K-steps in flight across the back-edge
-  int s0 = 0;
-  for (; s0 + 2 * PD <= nsteps; s0 += PD) {
+    load_chunk(wr[0], 0);
+    if (1 < nchunks) load_chunk(wr[1], 1);
+    __syncthreads();
 #pragma unroll
-    for (int u = 0; u < PD; ++u) {
-      consume(u, s0 + u);
+    for (int u = 2; u < D; ++u)
+      if (u < nchunks) load_chunk(wr[u], u);
+    store_chunk(wr[0], 0);
+    if (D < nchunks) load_chunk(wr[0], D);
+    __syncthreads();
+    // sums of squares: row 8 ld + (lane >> 3), column chunk lane & 7, K-steps in
+    // order (the tile engine's per-thread chain), one chunk of K-steps per
+    // iteration; the 8 lanes' sums by the xor tree and 1/rms before the last barrier
+    const int srow = 8 * ld + (lane >> 3), sub = lane & 7;
+    const uint16_t* hr = hb + (size_t)(srow < nt ? srow : 0) * HLD + 8 * sub;
+    float ss = 0.0f;
+    uint4 xs[CK];  // the next chunk's residual values, read one iteration ahead
+    auto ss_read = [&](int c) {
 #pragma unroll
-      for (int k = 0; k < 4; ++k)
-        ring[u][k] = *reinterpret_cast<const bf16x8_t*>(wrow + w_off<PACKED>(s0 + u + PD, k));
-    }
-  }
-  for (; s0 < nsteps; s0 += PD) {
+      for (int kk = 0; kk < CK; ++kk) xs[kk] = *reinterpret_cast<const uint4*>(hr + (size_t)min(c * CK + kk, nsteps - 1) * kKT);
+    };
+    auto ss_chunk = [&](int c) {
+      uint4 x[CK];
 #pragma unroll
-    for (int u = 0; u < PD; ++u) {
-      const int s = s0 + u;
-      if (s < nsteps) {
-        consume(u, s);
-        if (s + PD < nsteps) {
+      for (int kk = 0; kk < CK; ++kk) x[kk] = xs[kk];
+      if (c + 1 < nchunks) ss_read(c + 1);
+      if (srow < nt) {
 #pragma unroll
-          for (int k = 0; k < 4; ++k)
-            ring[u][k] = *reinterpret_cast<const bf16x8_t*>(wrow + w_off<PACKED>(s + PD, k));
+        for (int kk = 0; kk < CK; ++kk)
+          if (c * CK + kk < nsteps) sumsq_chunk_bf16(x[kk], ss);
+      }
+    };
+    ss_read(0);
+    auto finish_ss = [&]() {
+      ss += __shfl_xor(ss, 1, 64);
+      ss += __shfl_xor(ss, 2, 64);
+      ss += __shfl_xor(ss, 4, 64);
+      if (sub == 0 && srow < kProjTok) rinv[srow] = srow < nt ? 1.0f / sqrtf(ss / (float)d + a.eps) : 0.0f;
+    };
+    // iteration c: the sums of squares of chunk c, write chunk c + 1 (loaded D
+    // chunks earlier), refill its registers with chunk c + 1 + D, barrier c
+    if constexpr (NCH > 0) {
+#pragma unroll
+      for (int c = 0; c < NCH; ++c) {
+        ss_chunk(c);
+        if (c + 1 < NCH) {
+          store_chunk(wr[(c + 1) % D], c + 1);
+          if (c + 1 + D < NCH) load_chunk(wr[(c + 1) % D], c + 1 + D);
+        } else {
+          finish_ss();
+        }
+        __syncthreads();
+      }
+    } else {
+      for (int c0 = 0; c0 < nchunks; c0 += D) {
+#pragma unroll
+        for (int u = 0; u < D; ++u) {
+          const int c = c0 + u;
+          if (c < nchunks) {
+            ss_chunk(c);
+            if (c + 1 < nchunks) {
+              store_chunk(wr[(u + 1) % D], c + 1);
+              if (c + 1 + D < nchunks) load_chunk(wr[(u + 1) % D], c + 1 + D);
+            } else {
+              finish_ss();
+            }
+            __syncthreads();
+          }
         }
       }
     }
+    return;
   }
+
+  // wave 0: the RoPE table and positions, then (while the loaders issue their
+  // weights) gamma * h for all rows, then the MFMA chain
+  for (int i = lane; i < HD / 2; i += 64) rev[i] = a.rev[i];
+  if (lane < kProjTok) pos[lane] = lane < nt ? a.pos0[b0 + lane] : 0;
+  __syncthreads();
+  scale_rows();
+  __syncthreads();
+  // MFMA over d: A = 32 weight rows (from the ring), B = the group's tokens.
+  // Columns of absent tokens read row 0 and hold unused values: MFMA output
+  // columns are independent and only those of present tokens are stored.
+  const int col = lane & 31;
+  const uint16_t* hcol = hs + (size_t)(col < nt ? col : 0) * HLD + 8 * (lane >> 5);
+  {
+    bf16x8_t a0[FPC], b0f[FPC], a1[FPC], b1f[FPC];  // chunk c's fragments and chunk c + 1's
+    auto read_chunk = [&](bf16x8_t (&av)[FPC], bf16x8_t (&bv)[FPC], int c) {
+      const uint16_t* slot = ring + (size_t)(c % NR) * FPC * 512 + 8 * lane;
+#pragma unroll
+      for (int f = 0; f < FPC; ++f) {
+        const int s = min(c * CK + (f >> 2), nsteps - 1);
+        av[f] = *reinterpret_cast<const bf16x8_t*>(slot + f * 512);
+        bv[f] = *reinterpret_cast<const bf16x8_t*>(hcol + (size_t)s * kKT + 16 * (f & 3));
+      }
+    };
+    auto step = [&](int c, bf16x8_t (&ac)[FPC], bf16x8_t (&bc)[FPC], bf16x8_t (&an)[FPC], bf16x8_t (&bn)[FPC]) {
+      __syncthreads();
+      if (c + 1 < nchunks) read_chunk(an, bn, c + 1);
+      const int nk = min(CK, nsteps - c * CK);
+#pragma unroll
+      for (int f = 0; f < FPC; ++f)
+        if ((f >> 2) < nk) acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ac[f], bc[f], acc, 0, 0, 0);
+    };
+    read_chunk(a0, b0f, 0);
+    for (int c = 0; c < nchunks; c += 2) {
+      step(c, a0, b0f, a1, b1f);
+      if (c + 1 < nchunks) step(c + 1, a1, b1f, a0, b0f);
+    }
   }
 
   if (col >= nt) return;
@@ -338,8 +370,10 @@ __global__ __launch_bounds__(64) void stream_proj_kernel(ProjArgs a, int q_block
 // grid: xcd_map(n_kv * B * C) workgroups, item = (j * B + b) * C + c (the chunks of
 // one KV head, which share W_k / W_v, run on one XCD).  C = n_rec, or n_tail when
 // nothing is recomputed.  Chunk c < n_rec recomputes residual rows c*MT..c*MT+MT-1
-// and writes partial c; tail tile k (partial n_rec + k) is attended by chunk
-// n_rec - 1 - (k % n_rec) after its own chunk.
+// and writes partial c.  A folded tail (<= fold_rows<T>() rows) is attended with
+// the last chunk's keys; otherwise tail tile k (partial n_rec + k) goes to the
+// recompute workgroup of (b, j) that arrives k-th, k + n_rec-th, ... at the
+// split counter.
 template <typename T, int HD, int MT, bool PACKED>
 __global__ __launch_bounds__(kNtTile, 1) void fused_kernel(FusedArgs a, int per_xcd) {
   extern __shared__ __align__(16) char lds[];
@@ -575,17 +609,19 @@ static hipError_t proj_t(const ProjArgs& a, int n_units, hipStream_t st) {
   return hipGetLastError();
 }
 
-template <int HD, bool PACKED, int NS>
+template <int HD, bool PACKED, int NCH>
 static hipError_t stream_t(const ProjArgs& a, hipStream_t st) {
-  const size_t bytes = stream_lds(a.d).end;
+  const int G = stream_group(a.d, a.B, kLdsPerGroup);
+  if (G < 1) return hipErrorInvalidValue;  // validated by the caller
+  const size_t bytes = stream_lds(a.d, G).end;
   static size_t done = 0;
-  auto k = stream_proj_kernel<HD, PACKED, NS>;
+  auto k = stream_proj_kernel<HD, PACKED, NCH>;
   hipError_t e = ensure_lds(k, bytes, done);
   if (e != hipSuccess) return e;
   const int qb = a.n_q * HD / 32;
   const int kb = a.n_kv_units ? a.n_kv * HD / 32 : 0;
-  dim3 grid(qb + 2 * kb, (a.B + kProjTok - 1) / kProjTok);
-  hipLaunchKernelGGL(k, grid, dim3(64), bytes, st, a, qb, kb);
+  dim3 grid(qb + 2 * kb, (a.B + G - 1) / G);
+  hipLaunchKernelGGL(k, grid, dim3(64 * kStreamWaves), bytes, st, a, qb, kb, G);
   return hipGetLastError();
 }
 
@@ -643,23 +679,24 @@ hipError_t launch_proj(const ProjArgs& a, int dtype_bf16, int hd, int packed, in
 #undef PF
 }
 
-// d = 2560 (Gemma-3-4B) and 1536 (Qwen2.5-1.5B) get a straight-line K-loop.
+// d = 2560 (Gemma-3-4B) and 1536 (Qwen2.5-1.5B) get a compile-time chunk count.
 template <int HD, bool PACKED>
-static hipError_t stream_ns(const ProjArgs& a, hipStream_t st) {
-  switch (a.d / kKT) {
-    case 40: return stream_t<HD, PACKED, 40>(a, st);
-    case 24: return stream_t<HD, PACKED, 24>(a, st);
-    default: return stream_t<HD, PACKED, 0>(a, st);
+static hipError_t stream_nch(const ProjArgs& a, hipStream_t st) {
+  switch (a.d / (kKT * kStreamChunk)) {
+    case 20: if (a.d == 20 * kKT * kStreamChunk) return stream_t<HD, PACKED, 20>(a, st); break;
+    case 12: if (a.d == 12 * kKT * kStreamChunk) return stream_t<HD, PACKED, 12>(a, st); break;
+    default: break;
   }
+  return stream_t<HD, PACKED, 0>(a, st);
 }
 
 hipError_t launch_project_current(const ProjArgs& a, int dtype_bf16, int hd, int packed, int n_units,
                                   hipStream_t st) {
   if (!dtype_bf16) return launch_proj(a, 0, hd, 0, n_units, st);
   switch (hd) {
-    case 64: return packed ? stream_ns<64, true>(a, st) : stream_ns<64, false>(a, st);
-    case 128: return packed ? stream_ns<128, true>(a, st) : stream_ns<128, false>(a, st);
-    case 256: return packed ? stream_ns<256, true>(a, st) : stream_ns<256, false>(a, st);
+    case 64: return packed ? stream_nch<64, true>(a, st) : stream_nch<64, false>(a, st);
+    case 128: return packed ? stream_nch<128, true>(a, st) : stream_nch<128, false>(a, st);
+    case 256: return packed ? stream_nch<256, true>(a, st) : stream_nch<256, false>(a, st);
     default: return hipErrorInvalidValue;
   }
 }

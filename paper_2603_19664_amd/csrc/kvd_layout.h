@@ -49,9 +49,9 @@ constexpr int fused_tail_tiles(int n_rec, int T_tail) {
 
 // Streaming projection (current-token q/K/V): tokens per workgroup.
 constexpr int kProjTok = 16;
-constexpr int kProjPrefetch = 8;  // K-steps of weights in flight per wave
 
 constexpr size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+constexpr size_t kLdsPerGroup = 160 * 1024;  // LDS a workgroup may use on gfx950
 
 // Row strides (elements) of the LDS tiles; the +8 / +4 padding keeps the
 // 16-byte row reads of a wave on distinct LDS banks.
@@ -139,21 +139,41 @@ constexpr size_t fused_lds_bytes(int g, int hd, int mt) {
   return attn_lds(proj_lds<T>(hd, mt, fold_rows<T>()).end, g, hd, mt + fold_rows<T>()).end;
 }
 
-// Streaming projection: h-bar of kProjTok tokens for the whole d, gamma, 1/rms,
-// positions and the RoPE table.
+// Streaming projection (current-token q/K/V): one workgroup of kStreamWaves
+// waves per 32 weight rows.  Waves 1.. keep kStreamDepth chunks of the rows'
+// MFMA A fragments in flight in registers and write each chunk (kStreamChunk
+// K-steps: 32 rows x 64 x bf16 = 4 KiB per K-step) into an LDS ring of
+// kStreamSlots slots one chunk ahead of its use; wave 0 runs the MFMA chain.
+// LDS: RoPE table, 1/rms and positions of up to kProjTok tokens, gamma, the ring,
+// then the raw residual rows of the workgroup's token group (G rows, for the sums
+// of squares) and the same rows scaled by gamma (the MFMA B operand).
+constexpr int kStreamWaves = 5;
+constexpr int kStreamChunk = 2;
+constexpr int kStreamSlots = 4;
+constexpr int kStreamDepth = 10;
+constexpr size_t kStreamSlotBytes = (size_t)32 * kKT * 2 * kStreamChunk;
 struct StreamLds {
-  size_t rev, rinv, pos, gam, hb, end;
+  size_t rev, rinv, pos, gam, ring, hb, hs, end;
 };
 constexpr int stream_h_ld(int d) { return d + 8; }
-constexpr StreamLds stream_lds(int d) {
+constexpr StreamLds stream_lds(int d, int G) {
   StreamLds L{};
   L.rev = 0;
   L.rinv = align_up(L.rev + sizeof(double) * kMaxPairs, 16);
   L.pos = align_up(L.rinv + sizeof(float) * kProjTok, 16);
   L.gam = align_up(L.pos + sizeof(int) * kProjTok, 16);
-  L.hb = align_up(L.gam + sizeof(uint16_t) * d, 16);
-  L.end = align_up(L.hb + sizeof(uint16_t) * kProjTok * stream_h_ld(d), 16);
+  L.ring = align_up(L.gam + sizeof(uint16_t) * d, 16);
+  L.hb = L.ring + kStreamSlotBytes * kStreamSlots;
+  L.hs = align_up(L.hb + sizeof(uint16_t) * G * stream_h_ld(d), 16);
+  L.end = align_up(L.hs + sizeof(uint16_t) * G * stream_h_ld(d), 16);
   return L;
+}
+// Tokens per workgroup of the streaming projection: up to kProjTok, as many as
+// the LDS left after the ring holds (0: not even one row fits).
+constexpr int stream_group(int d, int B, size_t lds_limit) {
+  int G = B < kProjTok ? B : kProjTok;
+  while (G > 0 && stream_lds(d, G).end > lds_limit) --G;
+  return G;
 }
 
 // Workgroup -> work item remap that keeps the items of one XCD contiguous:

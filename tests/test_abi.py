@@ -169,11 +169,14 @@ def test_combine_validation():
 
 
 def test_lds_limit_of_projection_is_validated():
-    # the current-token projection stages d_model * 16 bf16 values in LDS
-    s = shape(d_model=8192)
+    # the current-token projection holds gamma, its weight ring and at least one
+    # residual row in LDS (fewer tokens per workgroup as d_model grows)
     f = lib.kvd_project_qkv
+    s = shape(d_model=40960)
     assert f(ctypes.byref(s), FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 1, FAKE, None, None) == kvd.KVD_ERR_UNSUPPORTED
     assert "LDS" in kvd.last_error()
+    s = shape(d_model=8192)  # fits: validation goes on to the NULL q_out (nothing is launched)
+    assert f(ctypes.byref(s), FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 1, None, None, None) == kvd.KVD_ERR_NULL
 
 
 def test_weight_layout_validation():
