@@ -123,20 +123,25 @@ def main():
     ws_f = kvd.workspace(s, kvd.KVD_OP_FUSED, B, T, 1)
     wsb_f = ws_f.numel()
 
-    proj, fused = [], []
-    for ly in layers:
-        proj.append(Call(lib.kvd_project_qkv, ctypes.byref(sc), P(ly["h_new"]), P(ly["gamma"]), P(ly["w_q"]),
-                         P(ly["w_k"]), P(ly["w_v"]), P(pos_new), B, P(q), ctypes.byref(tail), stream))
-        fused.append(Call(lib.kvd_fused_recompute_attn, ctypes.byref(sc), P(q), P(ly["h"]), T, P(ly["gamma"]),
-                          P(ly["w_k"]), P(ly["w_v"]), P(pos0), B, T, ctypes.byref(tail), 1, P(out), P(ws_f), wsb_f,
-                          None, stream))
+    def calls_on(st):
+        """The step's launches (per layer: project_qkv, fused) on stream st."""
+        pj, fz = [], []
+        for ly in layers:
+            pj.append(Call(lib.kvd_project_qkv, ctypes.byref(sc), P(ly["h_new"]), P(ly["gamma"]), P(ly["w_q"]),
+                           P(ly["w_k"]), P(ly["w_v"]), P(pos_new), B, P(q), ctypes.byref(tail), st))
+            fz.append(Call(lib.kvd_fused_recompute_attn, ctypes.byref(sc), P(q), P(ly["h"]), T, P(ly["gamma"]),
+                           P(ly["w_k"]), P(ly["w_v"]), P(pos0), B, T, ctypes.byref(tail), 1, P(out), P(ws_f), wsb_f,
+                           None, st))
+        return pj, fz
 
-    def step(events=None, i=0):
+    proj, fused = calls_on(stream)
+
+    def step(events=None, i=0, pj=proj, fz=fused):
         for l in range(L):
-            proj[l]()
+            pj[l]()
             if events is not None:
                 events[i][l][0].record()
-            fused[l]()
+            fz[l]()
             if events is not None:
                 events[i][l][1].record()
 
@@ -151,26 +156,56 @@ def main():
         del src, dst
 
     # ---------------------------------------------------------------- timed region
+    # value: the K timed steps are captured once as a HIP graph and replayed (the
+    # same launches in the same order as eager steps; the replay is checked
+    # bitwise against an eager step first).  The fused kernel's duration for the
+    # roofline: HIP events around every fused launch over K eager steps on the
+    # launch stream (events recorded inside a graph are not refreshed by replays,
+    # and recorded eagerly they widen every kernel boundary by a few us, so the
+    # two are measured in separate passes).
     K, W = args.steps, args.warmup
     log(f"[bench] warmup {W} steps")
     for _ in range(W):
         step()
     torch.cuda.synchronize()
-    ev = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(L)]
-          for _ in range(K)]
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        cst = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+        gp, gf = calls_on(cst)
+        for i in range(K):
+            step(None, i, gp, gf)
+    graph.replay()  # untimed: first launch of the graph
+    torch.cuda.synchronize()
+    out_graph = out.clone()
+    step()
+    torch.cuda.synchronize()
+    if not torch.equal(out_graph.view(torch.int16), out.view(torch.int16)):
+        raise RuntimeError("graph replay of the step differs from the eager step")
     t_start, t_end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    log(f"[bench] timing {K} steps")
+    log(f"[bench] timing {K} steps (one graph replay)")
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     t_start.record()
-    for i in range(K):
-        step(ev, i)
+    graph.replay()
     t_end.record()
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     ms_step = t_start.elapsed_time(t_end) / K
+    del graph
+    log(f"[bench] timing the fused kernel: {K} eager steps with events around each launch")
+    ev = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(L)]
+          for _ in range(K)]
+    e_start, e_end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e_start.record()
+    for i in range(K):
+        step(ev, i)
+    e_end.record()
+    torch.cuda.synchronize()
+    ms_step_events = e_start.elapsed_time(e_end) / K
     fused_ms = float(np.mean([a.elapsed_time(b) for row in ev for (a, b) in row]))
-    log(f"[bench] {ms_step:.3f} ms/step (wall {1e3 * wall / K:.3f}), fused kernel {1e3 * fused_ms:.1f} us/launch")
+    log(f"[bench] {ms_step:.3f} ms/step (wall {1e3 * wall / K:.3f}); with per-launch events "
+        f"{ms_step_events:.3f} ms/step, fused kernel {1e3 * fused_ms:.1f} us/launch")
 
     flops = acc.fused_flops(B, T, 1, nq, nkv, d, hd)
     achieved = flops / (fused_ms * 1e-3) / 1e12
@@ -293,7 +328,9 @@ def main():
         "data": "synthetic (seeded N(0,1) residuals scaled per layer by U(0.5,4); random-init N(0,0.02) weights)",
         "config": {"workload": wl.name, "layers": L, "batch": B, "ctx": T, "keys_per_query": T + 1,
                    "d_model": d, "n_q_heads": nq, "n_kv_heads": nkv, "head_dim": hd,
-                   "step": "per layer: kvd_project_qkv + kvd_fused_recompute_attn (split-K merge in-kernel)"},
+                   "step": "per layer: kvd_project_qkv + kvd_fused_recompute_attn (split-K merge in-kernel)",
+                   "launch": "the K timed steps captured once as a HIP graph and replayed"},
+        "eager_ms_per_step_with_events": ms_step_events,
         "roofline": {"bound": "mfma", "kernel": "fused_kernel<bf16,256,64>", "achieved": achieved,
                      "peak": MI355X_BF16_PEAK_TFLOPS, "unit": "TFLOP/s", "frac": achieved / MI355X_BF16_PEAK_TFLOPS,
                      "traffic": traffic, "flops_per_launch": flops, "us_per_launch": 1e3 * fused_ms},
