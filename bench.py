@@ -48,6 +48,8 @@ def parse():
     p.add_argument("--sweep-batches", default="1,2,4,8,16,32,64")
     p.add_argument("--calibration-copy-mib", type=int, default=256,
                    help="size of one untimed device-to-device copy whose HBM counters calibrate the traffic figure")
+    p.add_argument("--next", action="store_true",
+                   help="also measure the hybrid cache budget sweep and the recompute-vs-transfer sweep over evicted tokens")
     p.add_argument("--extra", action="store_true",
                    help="also measure the Qwen-1.5B-shaped step (28 layers, B=8, 16384 ctx; fused vs cached) and "
                         "the multi-turn conversation (Gemma 3-4B shape, B=16, a decode step at each of 20 turn "
@@ -217,8 +219,8 @@ def main():
             traffic = tr.get("bytes_per_launch")
 
     # ---------------------------------------------------------------- per-op us/layer and baselines
-    def op_time(fn, iters=None, warm=2, flush=None):
-        """Average device time of fn() over iters calls, HIP events around each call."""
+    def op_time(fn, iters=None, warm=2, flush=None, median=False):
+        """Average (or median) device time of fn() over iters calls, HIP events around each call."""
         iters = iters or max(3, K)
         for _ in range(warm):
             fn()
@@ -232,7 +234,8 @@ def main():
             b.record()
             times.append((a, b))
         torch.cuda.synchronize()
-        return float(np.mean([a.elapsed_time(b) for a, b in times])) * 1e3  # us
+        v = [a.elapsed_time(b) for a, b in times]
+        return float(np.median(v) if median else np.mean(v)) * 1e3  # us
 
     per_op = {}
     baselines = {}
@@ -339,9 +342,12 @@ def main():
         "crossover": crossover,
         "cpu_baseline": cpu,
     }
-    if args.extra:
+    if args.extra or args.next:
         del layers
         torch.cuda.empty_cache()
+    if args.next:
+        res["next"] = run_next(args, torch, np, kvd, configs, inputs, op_time, log)
+    if args.extra:
         res["extra_workloads"] = run_extra(args, torch, np, kvd, acc, configs, inputs, log)
     print(json.dumps(res), flush=True)
 
@@ -388,6 +394,101 @@ def run_crossover(args, torch, np, kvd, acc, configs, inputs, op_time, log):
     faster = [r["B"] for r in rows if r["ratio_fused_over_cached"] < 1.0]
     return {"workload": wl.name, "ctx": T, "rows": rows, "batches_where_recompute_wins": faster,
             "note": "each op timed with HIP events after a 512 MiB cache-evicting write; both include their split-K merge"}
+
+
+def run_next(args, torch, np, kvd, configs, inputs, op_time, log):
+    """Two measurements on one Gemma-3-4B-shaped layer (context 4096 + the current token),
+    each op timed with HIP events after a 512 MiB write that evicts L2 and the Infinity Cache:
+
+    hybrid_budget: Algorithm 1 with a cache budget of W tokens.  The W most recent context
+      tokens keep stored bf16 K/V and form the fused kernel's tail with the current token;
+      the older T - W are recomputed from their checkpoints in the kernel.  Every token keeps
+      its checkpoint (STORE_RESIDUAL), so memory = checkpoints of T tokens + K/V of W + 1.
+      The per-token costs are the slopes of the fused time in the recomputed and the stored
+      token counts.
+
+    evicted_tokens: N evicted tokens' K/V made available again, three ways: recomputed from
+      their checkpoints (kvd_recompute_kv), copied from a bf16 copy in HBM, and copied from a
+      bf16 copy in pinned host memory over PCIe (token-major, so each is one contiguous copy).
+      Medians of 11 calls (a PCIe copy occasionally takes far longer)."""
+    wl = configs.GEMMA3_4B
+    s = kvd.shape_of(wl).packed()
+    T, d, nkv, hd = wl.ctx, wl.d_model, wl.n_kv, wl.head_dim
+    flush_buf = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
+    flush = lambda: flush_buf.fill_(1)  # noqa: E731
+    gamma, w_q, w_k, w_v = inputs.weights(wl, 0, 0, "cuda")
+    w_q, w_k, w_v = (kvd.kvd_pack_weights(s, w) for w in (w_q, w_k, w_v))
+    res = {}
+
+    rows = []
+    for B in (1, 8):
+        log(f"[bench] next: hybrid budget B={B}")
+        h, h_new = inputs.residuals(wl, 0, B, T, 0, "cuda")
+        pos0 = torch.zeros((B,), dtype=torch.int32, device="cuda")
+        pos_new = torch.full((B,), T, dtype=torch.int32, device="cuda")
+        q = torch.empty((B, wl.n_q, hd), dtype=torch.bfloat16, device="cuda")
+        out = torch.empty_like(q)
+        Kc = torch.empty((B, nkv, T + 1, hd), dtype=torch.bfloat16, device="cuda")
+        Vc = torch.empty_like(Kc)
+        kvd.kvd_recompute_kv(s, h, gamma, w_k, w_v, pos0, T, Kc, Vc, 0)
+        kvd.kvd_project_qkv(s, h_new, gamma, w_q, w_k, w_v, pos_new, q, Kc, Vc, T)
+        for W in (0, 256, 1024, 2048, 3072, 4096):
+            T_rec, T_tail = T - W, W + 1
+            ws = kvd.workspace(s, kvd.KVD_OP_FUSED, B, T_rec, T_tail)
+            fz = lambda: kvd.kvd_fused_recompute_attn(s, q, h, T_rec, gamma, w_k, w_v, pos0, out, ws,  # noqa: E731
+                                                     Kc, Vc, T_tail, T_rec)
+            us = op_time(fz, iters=10, flush=flush)
+            rows.append({"B": B, "budget_tokens": W, "recomputed_tokens": T_rec, "stored_rows": T_tail,
+                         "fused_us": us, "checkpoint_bytes": B * T * d * 2,
+                         "kv_bytes": B * T_tail * 2 * nkv * hd * 2})
+            del ws
+        del h, h_new, Kc, Vc
+        torch.cuda.empty_cache()
+    slopes = {}
+    for B in (1, 8):
+        r = [x for x in rows if x["B"] == B]
+        W = np.array([x["budget_tokens"] for x in r], dtype=np.float64)
+        t = np.array([x["fused_us"] for x in r])
+        a, b = np.polyfit(W, t, 1)[::-1]  # t ~ a + b W
+        read_per_token = r[-1]["fused_us"] / (T + 1)  # W = T: every key is read
+        slopes[str(B)] = {"us_per_recomputed_minus_stored_token": -b, "fit_intercept_us": a,
+                          "us_per_stored_token_read": read_per_token,
+                          "us_per_recomputed_token": read_per_token - b}
+    res["hybrid_budget"] = {"workload": "gemma3-4b layer, ctx 4096 + current token", "rows": rows,
+                            "per_token_costs": slopes}
+
+    log("[bench] next: evicted tokens, recompute vs HBM copy vs host copy")
+    B = 1
+    h, _ = inputs.residuals(wl, 0, B, T, 0, "cuda")
+    pos0 = torch.zeros((B,), dtype=torch.int32, device="cuda")
+    Kc = torch.empty((B, nkv, T, hd), dtype=torch.bfloat16, device="cuda")
+    Vc = torch.empty_like(Kc)
+    kvd.kvd_recompute_kv(s, h, gamma, w_k, w_v, pos0, T, Kc, Vc, 0)
+    kv_dev = torch.stack([Kc[0].transpose(0, 1), Vc[0].transpose(0, 1)], dim=1).contiguous()  # [T][2][n_kv][hd]
+    kv_host = torch.empty(kv_dev.shape, dtype=kv_dev.dtype, pin_memory=True)
+    kv_host.copy_(kv_dev)
+    erows = []
+    for N in (1, 2, 4, 8, 16, 32, 64, 128, 256, 512, 1024, 2048, 4096):
+        Kr = torch.empty((B, nkv, N, hd), dtype=torch.bfloat16, device="cuda")
+        Vr = torch.empty_like(Kr)
+        dst = torch.empty((N,) + tuple(kv_dev.shape[1:]), dtype=kv_dev.dtype, device="cuda")
+        rec = lambda: kvd.kvd_recompute_kv(s, h, gamma, w_k, w_v, pos0, N, Kr, Vr, 0)  # noqa: E731
+        hbm = lambda: dst.copy_(kv_dev[:N])  # noqa: E731
+        host = lambda: dst.copy_(kv_host[:N], non_blocking=True)  # noqa: E731
+        e = {"N": N, "kv_bytes": N * 2 * nkv * hd * 2,
+             "recompute_us": op_time(rec, iters=11, flush=flush, median=True),
+             "hbm_copy_us": op_time(hbm, iters=11, flush=flush, median=True),
+             "host_copy_us": op_time(host, iters=11, flush=flush, median=True)}
+        erows.append(e)
+        log(f"[bench] next: N={N}: recompute {e['recompute_us']:.1f} us, HBM copy {e['hbm_copy_us']:.1f} us, "
+            f"host copy {e['host_copy_us']:.1f} us")
+    res["evicted_tokens"] = {
+        "workload": "gemma3-4b layer, B=1; K/V of N evicted tokens (N * 4 KiB)", "rows": erows,
+        "recompute_faster_than_hbm_copy": [e["N"] for e in erows if e["recompute_us"] < e["hbm_copy_us"]],
+        "recompute_faster_than_host_copy": [e["N"] for e in erows if e["recompute_us"] < e["host_copy_us"]]}
+    del h, Kc, Vc, kv_dev, kv_host, flush_buf
+    torch.cuda.empty_cache()
+    return res
 
 
 def _step_timer(torch, step, steps, warmup):

@@ -113,9 +113,12 @@ typedef struct {
  * and residual row t < T,
  *   K[b][j][t_off+t] = RoPE(hbar W_k^(j), pos0[b]+t),  V[b][j][t_off+t] = hbar W_v^(j),
  * hbar = RMSNorm(h[b][t]).  This is also the prefill path (the K/V a cache
- * would have stored); the same kernel produces them, so prefill, recompute,
- * kvd_project_qkv's K/V and the fused kernel's K/V are bit-identical for the
- * same residual row and position (Prop. reconstruction).
+ * would have stored).  Every producer runs the same arithmetic (one MFMA chain
+ * over d_model per output element, one sum-of-squares order), so prefill,
+ * recompute, kvd_project_qkv's K/V and the fused kernel's K/V are bit-identical
+ * for the same residual row and position (Prop. reconstruction).  A bf16 call of
+ * at most 64 rows (B * T) runs on the current-token projection's kernel, which
+ * serves a few rows at far lower latency than the 64-row tile engine.
  *   h     [B][h_ld][d_model], h_ld >= T.      pos0  [B] int32.
  *   out   K/V view written at rows out->t_off .. out->t_off+T-1.
  * B == 0 or T == 0 is a no-op.                                                */
@@ -176,10 +179,9 @@ kvd_status kvd_cached_attn(const kvd_attn_shape* shape, const void* q, const kvd
  * recomputed rows.  With bf16, T_rec >= 1 and T_tail <= 4 (a decode step's
  * current token) the tail joins the last tile's split: its rows are copied into
  * LDS while that tile is recomputed.  Otherwise the tail adds one split per
- * 64-row tile, each attended by one of the first recompute workgroups of its
- * (sequence, KV head) to finish, handed out by the workspace's split counter
- * (same zero-before-use contract as kvd_decode_attn), which is then used even
- * with out == NULL.  kvd_num_splits gives the count.
+ * 64-row tile, each attended by a workgroup of its own (the hybrid cache budget:
+ * recent tokens stored, older ones recomputed).  kvd_num_splits gives the count.
+ * The workspace's split counters follow kvd_decode_attn's contract.
  * out == NULL writes only the split-K partials (see kvd_combine).
  * Supports both dtypes.                                                       */
 kvd_status kvd_fused_recompute_attn(const kvd_attn_shape* shape, const void* q, const void* h,

@@ -881,11 +881,10 @@ __device__ __forceinline__ void combine_rows(const float* ws_acc, const float* w
 }
 
 // Split-K completion counter of (b, KV head j): one 64-bit word in the
-// workspace.  The low 32 bits count the splits whose partials are written; the
-// high 32 bits count the recompute workgroups that have arrived, and that
-// arrival order hands out the stored tail tiles of a fused call.  Every thread
-// first waits for its own device-scope partial stores to complete; then one
-// thread adds `add` and the value before the add is broadcast to the workgroup.
+// workspace whose low 32 bits count the splits whose partials are written (the
+// high 32 bits are reserved and stay zero).  Every thread first waits for its own
+// device-scope partial stores to complete; then one thread adds `add` and the
+// value before the add is broadcast to the workgroup.
 // No cache-wide write-back or invalidate is needed, so other workgroups that
 // stream weights through the same L2 keep them.
 __device__ __forceinline__ unsigned long long split_arrive(unsigned long long* ctr, unsigned long long add,

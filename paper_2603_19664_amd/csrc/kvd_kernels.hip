@@ -122,7 +122,9 @@ __global__ __launch_bounds__(kNtTile, 1) void proj_kernel(ProjArgs a, int per_xc
 // ------------------------------------------------------------------ streaming current-token projection
 
 // One workgroup of kStreamWaves waves per 32 weight rows.  blockIdx.x: a 32-row
-// block of [W_q rows | W_k rows | W_v rows]; blockIdx.y: a group of G sequences.
+// block of [W_q rows | W_k rows | W_v rows] (no W_q rows without q_out);
+// blockIdx.y: a group of G of the B * T tokens (T = 1 for a decode step's
+// current tokens; the few rows of a short recompute otherwise).
 // Waves 1.. (the loaders) each keep their share of kStreamDepth chunks of the
 // rows' MFMA A fragments (1 KiB each) in flight in registers; wave 0 runs the
 // MFMA chain over d and issues no global loads in its loop.  Barrier c: the
@@ -157,8 +159,9 @@ __global__ __launch_bounds__(64 * kStreamWaves) void stream_proj_kernel(ProjArgs
   uint16_t* hs = reinterpret_cast<uint16_t*>(lds + SL.hs);
 
   const int blk = blockIdx.x;
-  const int b0 = blockIdx.y * G;
-  const int nt = min(G, a.B - b0);
+  // tokens n0 .. n0 + nt - 1 of the B * T: token n is row t = n % T of sequence b = n / T
+  const int n0 = blockIdx.y * G;
+  const int nt = min(G, a.B * a.T - n0);
   const uint16_t* W;
   int row0, rope, mat;  // mat: 0 q, 1 k, 2 v
   if (blk < q_blocks) {
@@ -213,7 +216,8 @@ __global__ __launch_bounds__(64 * kStreamWaves) void stream_proj_kernel(ProjArgs
     {
       const int cpr = d / 8;  // 16-byte chunks per row
       for (int r = ld; r <= nt; r += NW - 1) {
-        const uint16_t* src = (r < nt ? static_cast<const uint16_t*>(a.h) + (size_t)(b0 + r) * d
+        const int nb = (n0 + r) / a.T, ntk = n0 + r - nb * a.T;
+        const uint16_t* src = (r < nt ? static_cast<const uint16_t*>(a.h) + ((size_t)nb * a.h_ld + ntk) * d
                                       : static_cast<const uint16_t*>(a.gamma)) + 8 * lane;
         uint16_t* dst = r < nt ? hb + (size_t)r * HLD : gl;
         for (int ch0 = 0; ch0 < cpr; ch0 += 64)
@@ -298,7 +302,10 @@ __global__ __launch_bounds__(64 * kStreamWaves) void stream_proj_kernel(ProjArgs
   // wave 0: the RoPE table and positions, then (while the loaders issue their
   // weights) gamma * h for all rows, then the MFMA chain
   for (int i = lane; i < HD / 2; i += 64) rev[i] = a.rev[i];
-  if (lane < kProjTok) pos[lane] = lane < nt ? a.pos0[b0 + lane] : 0;
+  if (lane < kProjTok) {
+    const int nb = (n0 + lane) / a.T, ntk = n0 + lane - nb * a.T;
+    pos[lane] = lane < nt ? a.pos0[nb] + ntk : 0;
+  }
   __syncthreads();
   scale_rows();
   __syncthreads();
@@ -336,7 +343,7 @@ __global__ __launch_bounds__(64 * kStreamWaves) void stream_proj_kernel(ProjArgs
   if (col >= nt) return;
   const float ri = rinv[col];
   const int p = pos[col];
-  const int b = b0 + col;
+  const int b = (n0 + col) / a.T, t = n0 + col - b * a.T;
   float v[16];
 #pragma unroll
   for (int r = 0; r < 16; ++r) v[r] = acc[r] * ri;
@@ -353,7 +360,7 @@ __global__ __launch_bounds__(64 * kStreamWaves) void stream_proj_kernel(ProjArgs
     dst = static_cast<uint16_t*>(a.q_out) + ((size_t)b * a.n_q + head) * HD;
   } else {
     uint16_t* base = static_cast<uint16_t*>(mat == 1 ? a.k_out : a.v_out);
-    dst = base + (((size_t)b * a.n_kv + head) * a.kv_t_cap + a.kv_t_off) * HD;
+    dst = base + (((size_t)b * a.n_kv + head) * a.kv_t_cap + a.kv_t_off + t) * HD;
   }
 #pragma unroll
   for (int g4 = 0; g4 < 4; ++g4) {
@@ -368,12 +375,11 @@ __global__ __launch_bounds__(64 * kStreamWaves) void stream_proj_kernel(ProjArgs
 // ------------------------------------------------------------------ fused recompute + attention
 
 // grid: xcd_map(n_kv * B * C) workgroups, item = (j * B + b) * C + c (the chunks of
-// one KV head, which share W_k / W_v, run on one XCD).  C = n_rec, or n_tail when
-// nothing is recomputed.  Chunk c < n_rec recomputes residual rows c*MT..c*MT+MT-1
-// and writes partial c.  A folded tail (<= fold_rows<T>() rows) is attended with
-// the last chunk's keys; otherwise tail tile k (partial n_rec + k) goes to the
-// recompute workgroup of (b, j) that arrives k-th, k + n_rec-th, ... at the
-// split counter.
+// one KV head, which share W_k / W_v, run on one XCD), C = n_tail + n_rec.  Items
+// c < n_tail attend stored tail tile c (64 rows; partial n_rec + c) and come first,
+// as they are short; item n_tail + r recomputes residual rows r*MT..r*MT+MT-1
+// (partial r).  A folded tail (<= fold_rows<T>() rows, n_tail = 0) is attended
+// with the last recomputed chunk's keys.
 template <typename T, int HD, int MT, bool PACKED>
 __global__ __launch_bounds__(kNtTile, 1) void fused_kernel(FusedArgs a, int per_xcd) {
   extern __shared__ __align__(16) char lds[];
@@ -386,10 +392,11 @@ __global__ __launch_bounds__(kNtTile, 1) void fused_kernel(FusedArgs a, int per_
   const int tid = threadIdx.x;
   const bool fold = fold_tail<T>(a.n_rec, a.T_tail);
   const int n_tail = fused_tail_tiles<T>(a.n_rec, a.T_tail);
-  const int C = a.n_rec > 0 ? a.n_rec : n_tail;
+  const int C = n_tail + a.n_rec;
   const long long item = (long long)(blockIdx.x % kXcds) * per_xcd + blockIdx.x / kXcds;
   if (item >= (long long)a.n_kv * a.B * C) return;
   const int c = (int)(item % C);
+  const int rc = c - n_tail;  // recomputed chunk (c >= n_tail)
   const int unit = (int)(item / C);
   const int j = unit / a.B, b = unit - j * a.B;
   const int g = a.n_q / a.n_kv;
@@ -398,7 +405,7 @@ __global__ __launch_bounds__(kNtTile, 1) void fused_kernel(FusedArgs a, int per_
 
   // A folded tail goes to the last recomputed tile's workgroup: its rows land
   // in LDS rows MT.. while the tile is being recomputed.
-  const bool tail_here = fold && c == a.n_rec - 1;
+  const bool tail_here = fold && rc == a.n_rec - 1;
   if constexpr (FR > 0) {
     if (tail_here)
       prefetch_rows_lds<T, HD>(static_cast<const T*>(a.tk), static_cast<const T*>(a.tv),
@@ -408,8 +415,8 @@ __global__ __launch_bounds__(kNtTile, 1) void fused_kernel(FusedArgs a, int per_
 
   load_q<T, HD, NT>(static_cast<const T*>(a.q), b, a.n_q, j, g, reinterpret_cast<float*>(lds + AL.q));
 
-  if (a.n_rec > 0) {
-    const int t0 = c * MT;
+  if (c >= n_tail) {
+    const int t0 = rc * MT;
     const int n = min(MT, a.T_rec - t0);
     double* rev = reinterpret_cast<double*>(lds + PL.rev);
     float* rinv = reinterpret_cast<float*>(lds + PL.rinv);
@@ -465,34 +472,7 @@ __global__ __launch_bounds__(kNtTile, 1) void fused_kernel(FusedArgs a, int per_
       }
     }
     attend_tile<T, HD, NT, tile_kpl<T>()>(kv, nk, MT + FR, g, lds, AL);
-    write_partial<HD, NT>(lds, AL, a.ws_acc, a.ws_ml, b, a.n_q, j, g, a.S, c);
-    if (a.out != nullptr || n_tail > 0) {
-      // The stored tail tiles go to the first recompute workgroups of (b, j) to
-      // finish: arrival r takes tail tiles r, r + n_rec, ...
-      unsigned long long* ctr = a.ws_done + (size_t)b * a.n_kv + j;
-      auto* bc = reinterpret_cast<unsigned long long*>(lds + AL.ctr);
-      unsigned long long before = split_arrive(ctr, (1ull << 32) + 1, bc);
-      unsigned added = 1;
-      unsigned mine = 0;
-      for (int k = (int)(before >> 32); k < n_tail; k += a.n_rec) {
-        const int r0 = k * kTile;
-        const int nk = min(kTile, a.T_tail - r0);
-        __syncthreads();
-        load_kv_tile<T, HD, NT>(static_cast<const T*>(a.tk), static_cast<const T*>(a.tv), b, a.n_kv, j, a.tail_t_cap,
-                                a.tail_t_off + r0, nk, kv);
-        __syncthreads();
-        attend_tile<T, HD, NT, tile_kpl<T>()>(kv, nk, MT + FR, g, lds, AL);
-        write_partial<HD, NT>(lds, AL, a.ws_acc, a.ws_ml, b, a.n_q, j, g, a.S, a.n_rec + k);
-        ++mine;
-      }
-      if (mine > 0) {
-        before = split_arrive(ctr, mine, bc);
-        added = mine;
-      }
-      if (split_complete(ctr, before, added, a.S) && a.out != nullptr)
-        combine_rows<T, HD, NT>(a.ws_acc, a.ws_ml, static_cast<T*>(a.out), (size_t)b * a.n_q + (size_t)j * g, g,
-                                a.S, reinterpret_cast<float*>(lds + AL.cmb));
-    }
+    write_partial<HD, NT>(lds, AL, a.ws_acc, a.ws_ml, b, a.n_q, j, g, a.S, rc);
   } else {
     const int r0 = c * kTile;
     const int nk = min(kTile, a.T_tail - r0);
@@ -500,14 +480,14 @@ __global__ __launch_bounds__(kNtTile, 1) void fused_kernel(FusedArgs a, int per_
                             a.tail_t_off + r0, nk, kv);
     __syncthreads();
     attend_tile<T, HD, NT, tile_kpl<T>()>(kv, nk, MT + FR, g, lds, AL);
-    write_partial<HD, NT>(lds, AL, a.ws_acc, a.ws_ml, b, a.n_q, j, g, a.S, c);
-    if (a.out != nullptr) {
-      unsigned long long* ctr = a.ws_done + (size_t)b * a.n_kv + j;
-      const unsigned long long before = split_arrive(ctr, 1, reinterpret_cast<unsigned long long*>(lds + AL.ctr));
-      if (split_complete(ctr, before, 1, a.S))
-        combine_rows<T, HD, NT>(a.ws_acc, a.ws_ml, static_cast<T*>(a.out), (size_t)b * a.n_q + (size_t)j * g, g,
-                                a.S, reinterpret_cast<float*>(lds + AL.cmb));
-    }
+    write_partial<HD, NT>(lds, AL, a.ws_acc, a.ws_ml, b, a.n_q, j, g, a.S, a.n_rec + c);
+  }
+  if (a.out != nullptr) {
+    unsigned long long* ctr = a.ws_done + (size_t)b * a.n_kv + j;
+    const unsigned long long before = split_arrive(ctr, 1, reinterpret_cast<unsigned long long*>(lds + AL.ctr));
+    if (split_complete(ctr, before, 1, a.S))
+      combine_rows<T, HD, NT>(a.ws_acc, a.ws_ml, static_cast<T*>(a.out), (size_t)b * a.n_q + (size_t)j * g, g, a.S,
+                              reinterpret_cast<float*>(lds + AL.cmb));
   }
 }
 
@@ -611,16 +591,16 @@ static hipError_t proj_t(const ProjArgs& a, int n_units, hipStream_t st) {
 
 template <int HD, bool PACKED, int NCH>
 static hipError_t stream_t(const ProjArgs& a, hipStream_t st) {
-  const int G = stream_group(a.d, a.B, kLdsPerGroup);
+  const int G = stream_group(a.d, a.B * a.T, kLdsPerGroup);
   if (G < 1) return hipErrorInvalidValue;  // validated by the caller
   const size_t bytes = stream_lds(a.d, G).end;
   static size_t done = 0;
   auto k = stream_proj_kernel<HD, PACKED, NCH>;
   hipError_t e = ensure_lds(k, bytes, done);
   if (e != hipSuccess) return e;
-  const int qb = a.n_q * HD / 32;
+  const int qb = a.q_out ? a.n_q * HD / 32 : 0;
   const int kb = a.n_kv_units ? a.n_kv * HD / 32 : 0;
-  dim3 grid(qb + 2 * kb, (a.B + G - 1) / G);
+  dim3 grid(qb + 2 * kb, (a.B * a.T + G - 1) / G);
   hipLaunchKernelGGL(k, grid, dim3(64 * kStreamWaves), bytes, st, a, qb, kb, G);
   return hipGetLastError();
 }
@@ -633,8 +613,7 @@ static hipError_t fused_t(const FusedArgs& a, hipStream_t st) {
   auto k = fused_kernel<T, HD, MT, PACKED>;
   hipError_t e = ensure_lds(k, bytes, done);
   if (e != hipSuccess) return e;
-  const int n_tail = (a.T_tail + kTile - 1) / kTile;
-  const int C = a.n_rec > 0 ? a.n_rec : n_tail;
+  const int C = fused_tail_tiles<T>(a.n_rec, a.T_tail) + a.n_rec;
   const XcdMap m = xcd_map((long long)a.n_kv * a.B * C);
   hipLaunchKernelGGL(k, dim3(m.grid), dim3(kNtTile), bytes, st, a, m.per);
   return hipGetLastError();

@@ -151,6 +151,10 @@ constexpr int kStreamWaves = 5;
 constexpr int kStreamChunk = 2;
 constexpr int kStreamSlots = 4;
 constexpr int kStreamDepth = 10;
+// A bf16 recompute of at most this many token rows runs on the streaming
+// projection (its MFMA chain is the tile engine's, so the K/V are identical):
+// the tile engine takes a whole K-loop per 64-token tile whatever the count.
+constexpr int kStreamRecomputeMaxTokens = 64;
 constexpr size_t kStreamSlotBytes = (size_t)32 * kKT * 2 * kStreamChunk;
 struct StreamLds {
   size_t rev, rinv, pos, gam, ring, hb, hs, end;

@@ -189,12 +189,16 @@ def test_prefill_equals_recompute_bitwise(dtype):
     wl = dataclasses.replace(C.GEMMA3_4B, d_model=512, dtype="bf16" if dtype == BF else "f32")
     L = make_layer(wl, B=3, T=300, seed=21, pos0=[0, 17, 4000])
     Kp, Vp = gpu_recompute(L)                     # prefill: every token at once
-    # recompute of sub-ranges with odd lengths, at other offsets and capacities
-    for a, b in [(0, 1), (1, 66), (66, 67), (67, 299), (299, 300), (5, 250)]:
+    # recompute of sub-ranges with odd lengths, at other offsets and capacities (in bf16,
+    # B * T <= 64 rows run on the streaming kernel, longer ones on the tile engine)
+    for a, b in [(0, 1), (1, 66), (66, 67), (67, 299), (299, 300), (5, 250), (100, 120)]:
         Lr = dataclasses.replace(L, h=L.h[:, a:b].contiguous(), T=b - a, pos0=(L.pos0 + a).to(torch.int32))
         K, V = gpu_recompute(Lr, t_cap=b - a + 9, t_off=7)
         assert torch.equal(_bits(K[:, :, 7:7 + b - a]), _bits(Kp[:, :, a:b])), (a, b)
         assert torch.equal(_bits(V[:, :, 7:7 + b - a]), _bits(Vp[:, :, a:b])), (a, b)
+    # a short recompute reading its rows out of a longer checkpoint buffer (h_ld > T)
+    K, V = gpu_recompute(dataclasses.replace(L, T=20))
+    assert torch.equal(_bits(K), _bits(Kp[:, :, :20])) and torch.equal(_bits(V), _bits(Vp[:, :, :20]))
     # one sequence alone vs inside the batch
     Lb = dataclasses.replace(L, B=1, h=L.h[2:3].contiguous(), pos0=L.pos0[2:3].contiguous())
     K, V = gpu_recompute(Lb)
@@ -271,8 +275,8 @@ def test_hybrid_budget_stored_window(dtype, T_rec, T):
     # Algorithm 1 with a cache budget: the T - T_rec most recent context tokens
     # keep stored K/V (the library's own, bit-identical to what prefill stores)
     # and form the tail with the current token; the older T_rec are recomputed
-    # in the kernel.  (130, 430) has more tail tiles than recompute tiles, so
-    # some workgroups attend two tail tiles; (0, 200) is tail-only.  Tails of
+    # in the kernel.  (130, 430) has more tail tiles than recompute tiles;
+    # (0, 200) is tail-only.  Tails of
     # <= 4 rows join the last recomputed tile in bf16: after a full tile
     # (128, 131), or moved down over a partial one, overlapping (126, 129) or not
     # (61, 64), (64, 66).
@@ -295,7 +299,7 @@ def test_hybrid_budget_stored_window(dtype, T_rec, T):
     out2 = torch.empty_like(q)
     fused(out2, ws)  # the workspace's counters were left zero
     assert torch.equal(_bits(out), _bits(out2))
-    fused(None, ws)  # partials only (the tail tiles still handed out by arrival)
+    fused(None, ws)  # partials only
     out3 = torch.empty_like(q)
     kvd.kvd_combine(s, L.B, kvd.kvd_num_splits(s, kvd.KVD_OP_FUSED, L.B, T_rec, T_tail), ws, out3)
     assert torch.equal(_bits(out), _bits(out3))
