@@ -231,10 +231,14 @@ struct MfmaTile {
 
   // Computes the tile into `kv` (LDS, [MT][KLD] bf16).  hrow[r]: residual row of
   // staged token (tid>>3)+64r, offset by 8*(tid&7) (any readable row if !valid[r]).
-  // gam: gamma in LDS ([d] bf16).
+  // gam: gamma in LDS ([d] bf16), gam_g: the same in global memory.  setup():
+  // the caller's LDS writes of gam, pos and rev (and anything else it needs),
+  // run after the K-loop's first loads are issued so that the latency of the
+  // caller's own loads overlaps theirs; no barrier may precede it.
+  template <class Setup>
   static __device__ __forceinline__ void run(const uint16_t* const (&hrow)[CPT], const bool (&valid)[CPT], const uint16_t* gam,
-                             int d, float eps, const Half (&halves)[2], uint16_t* hst, float* rinv, const int* pos,
-                             const double* rev, uint16_t* kv) {
+                             const uint16_t* gam_g, int d, float eps, const Half (&halves)[2], uint16_t* hst,
+                             float* rinv, const int* pos, const double* rev, uint16_t* kv, const Setup& setup) {
     const int tid = threadIdx.x, lane = tid & 63, sub = tid & 7;
     const int wave = wave_id();
     const int fw = wave % WF, tw = wave / WF;
@@ -288,10 +292,10 @@ struct MfmaTile {
     auto load_h = [&](int slot, int s) { H[slot] = *reinterpret_cast<const uint4*>(hrow[0] + (size_t)s * kKT); };
     // Tokens past the end of a ragged tile stage a readable row's values: their
     // MFMA columns are independent of the others and their 1/rms is zero.
-    auto put_h = [&](int slot, int s) {
-      const uint4 gv = *reinterpret_cast<const uint4*>(gam + (size_t)s * kKT + 8 * sub);
+    auto put_hv = [&](int slot, const uint4& gv) {
       *reinterpret_cast<uint4*>(hst + (size_t)slot * SLOT + lofs) = stage_chunk_bf16(H[slot], gv, ss[0]);
     };
+    auto put_h = [&](int slot, int s) { put_hv(slot, *reinterpret_cast<const uint4*>(gam + (size_t)s * kKT + 8 * sub)); };
     auto rd = [&](bf16x8_t (&bv)[NB_T], int slot, int u) {
 #pragma unroll
       for (int bt = 0; bt < NB_T; ++bt)
@@ -363,14 +367,19 @@ struct MfmaTile {
       }
     };
 
-    // prologue: residual steps 0..D-1 and weight steps 0..D-1 in flight, step 0 staged
+    // prologue: residual steps 0..D-1 and weight steps 0..D-1 in flight, the
+    // caller's setup written, step 0 staged (its gamma chunk read from global
+    // memory: the LDS copy is complete only after the barrier)
 #pragma unroll
     for (int i = 0; i < D; ++i) load_h(i, min(i, nsteps - 1));
+    const uint4 g0 = *reinterpret_cast<const uint4*>(gam_g + 8 * sub);
+    __builtin_amdgcn_sched_barrier(0);  // keep it ahead of the weight loads (in-order waits)
 #pragma unroll
     for (int i = 0; i < D; ++i)
 #pragma unroll
       for (int u = 0; u < 4; ++u) load_wu(i, min(i, nsteps - 1), u);
-    put_h(0, 0);
+    setup();
+    put_hv(0, g0);
     load_h(0, min(D, nsteps - 1));
     __syncthreads();
     rd(b0, 0, 0);
@@ -439,9 +448,13 @@ struct F32Tile {
   static constexpr int HLD = h_ld<float>();
   static constexpr int KLD = kv_ld<float>(HD);
 
+  // setup(): the caller's LDS writes of pos and rev (read after the K-loop's
+  // barriers), run first.
+  template <class Setup>
   static __device__ __forceinline__ void run(const float* const (&hrow)[CPT], const bool (&valid)[CPT], const float* gamma, int d,
                              float eps, const Half (&halves)[2], float* hst, float* rinv, const int* pos,
-                             const double* rev, float* kv) {
+                             const double* rev, float* kv, const Setup& setup) {
+    setup();
     const int tid = threadIdx.x, sub = tid & 7;
     const int p = tid % HD;
     const int tg = tid / HD;
@@ -534,6 +547,69 @@ __device__ __forceinline__ void load_q(const T* q, int b, int n_q, int j, int g,
   }
 }
 
+// Setup values of a recomputed tile: the KV group's query rows (WITH_Q; as load_q
+// stores them), gamma (bf16 only: the fp32 engine reads it from global memory) and the
+// RoPE inverse frequencies.  The constructor issues the loads of a thread's
+// first chunks into registers with clamped indexes, unconditionally; store()
+// writes the in-range ones to LDS and copies what is left over (more than one q
+// chunk or two gamma chunks per thread) with plain loops.  Constructed before a
+// tile engine's first loads, stored by its setup(): the two latencies overlap.
+template <typename T, int HD, int NT, bool WITH_Q>
+struct TileSetup {
+  static constexpr int CH = 16 / sizeof(T);
+  const T* qsrc;
+  const uint16_t* gsrc;
+  int nqc, ngc;
+  u32x4_t qv, gv0, gv1;
+  double rv;
+
+  __device__ __forceinline__ TileSetup(const T* q, int b, int n_q, int j, int g, const void* gamma, int d,
+                                       const double* rev) {
+    const int tid = threadIdx.x;
+    if constexpr (WITH_Q) {
+      qsrc = q + ((size_t)b * n_q + (size_t)j * g) * HD;
+      nqc = g * HD / CH;
+      qv = *reinterpret_cast<const u32x4_t*>(qsrc + CH * min(tid, nqc - 1));
+    }
+    rv = rev[min(tid, HD / 2 - 1)];
+    if constexpr (sizeof(T) == 2) {
+      gsrc = static_cast<const uint16_t*>(gamma);
+      ngc = d / 8;
+      gv0 = *reinterpret_cast<const u32x4_t*>(gsrc + 8 * min(tid, ngc - 1));
+      gv1 = *reinterpret_cast<const u32x4_t*>(gsrc + 8 * min(tid + NT, ngc - 1));
+    }
+  }
+
+  __device__ __forceinline__ void store(float* qs, uint16_t* gam, double* revs) const {
+    const int tid = threadIdx.x;
+    auto put_q = [&](int c, u32x4_t v) {
+      float* dst = qs + CH * c;
+      if constexpr (CH == 8) {
+        const float x[8] = {bf_lo(v.x), bf_hi(v.x), bf_lo(v.y), bf_hi(v.y),
+                            bf_lo(v.z), bf_hi(v.z), bf_lo(v.w), bf_hi(v.w)};
+#pragma unroll
+        for (int e = 0; e < 8; ++e) dst[e] = x[e] * ScoreScale<HD>::v;
+      } else {
+        dst[0] = __uint_as_float(v.x) * ScoreScale<HD>::v;
+        dst[1] = __uint_as_float(v.y) * ScoreScale<HD>::v;
+        dst[2] = __uint_as_float(v.z) * ScoreScale<HD>::v;
+        dst[3] = __uint_as_float(v.w) * ScoreScale<HD>::v;
+      }
+    };
+    if constexpr (WITH_Q) {
+      if (tid < nqc) put_q(tid, qv);
+      for (int c = tid + NT; c < nqc; c += NT) put_q(c, *reinterpret_cast<const u32x4_t*>(qsrc + CH * c));
+    }
+    if (tid < HD / 2) revs[tid] = rv;
+    if constexpr (sizeof(T) == 2) {
+      if (tid < ngc) *reinterpret_cast<u32x4_t*>(gam + 8 * tid) = gv0;
+      if (tid + NT < ngc) *reinterpret_cast<u32x4_t*>(gam + 8 * (tid + NT)) = gv1;
+      for (int c = tid + 2 * NT; c < ngc; c += NT)
+        *reinterpret_cast<uint4*>(gam + 8 * c) = *reinterpret_cast<const uint4*>(gsrc + 8 * c);
+    }
+  }
+};
+
 // Rows row0 .. row0+n-1 (n <= kTile) of a stored K/V block ([B][n_kv][t_cap][HD],
 // head j of sequence b) into the LDS tile [kTile][K | V].  All loads of a thread
 // are issued before its LDS stores.
@@ -546,19 +622,19 @@ __device__ __forceinline__ void load_kv_tile(const T* K, const T* V, int b, int 
   constexpr int HALF = kTile * CPR / NT;     // chunks per thread for the K (or V) half of a full tile
   static_assert(HALF * NT == kTile * CPR, "tile split");
   const size_t base = ((size_t)b * n_kv + j) * t_cap + row0;
-  uint4 v[2 * HALF];
+  u32x4_t v[2 * HALF];
 #pragma unroll
   for (int i = 0; i < 2 * HALF; ++i) {
     const int rem = threadIdx.x + NT * (i % HALF);
     const int t = rem / CPR, ch = rem % CPR;
     const T* src = (i < HALF ? K : V) + (base + (t < n ? t : 0)) * HD + ch * CH;
-    v[i] = *reinterpret_cast<const uint4*>(src);
+    v[i] = *reinterpret_cast<const u32x4_t*>(src);
   }
 #pragma unroll
   for (int i = 0; i < 2 * HALF; ++i) {
     const int rem = threadIdx.x + NT * (i % HALF);
     const int t = rem / CPR, ch = rem % CPR;
-    if (t < n) *reinterpret_cast<uint4*>(kv + (size_t)t * KLD + (i < HALF ? 0 : HD) + ch * CH) = v[i];
+    if (t < n) *reinterpret_cast<u32x4_t*>(kv + (size_t)t * KLD + (i < HALF ? 0 : HD) + ch * CH) = v[i];
   }
 }
 

@@ -60,21 +60,20 @@ __global__ __launch_bounds__(kNtTile, 1) void proj_kernel(ProjArgs a, int per_xc
     halves[1] = Half{heads[1] < a.n_q ? static_cast<const T*>(a.w_q) + heads[1] * hd_d : nullptr, 1};
   }
 
-  if (tid < HD / 2) rev[tid] = a.rev[tid];
+  // gamma, rev and the positions reach LDS while the K-loop's first loads are in flight
   uint16_t* gam = reinterpret_cast<uint16_t*>(lds + PL.end);
-  if constexpr (sizeof(T) == 2) {
-    for (int c = tid; c < a.d / 8; c += NT)
-      *reinterpret_cast<uint4*>(gam + 8 * c) = *reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(a.gamma) + 8 * c);
-  }
-  if (tid < MT) {
-    const long long n = n0 + tid;
-    int p = 0;
-    if (n < ntok) {
-      const int b = (int)(n / a.T), t = (int)(n - (long long)b * a.T);
-      p = a.pos0[b] + t;
-    }
-    pos[tid] = p;
-  }
+  const TileSetup<T, HD, NT, false> su(nullptr, 0, 0, 0, 0, a.gamma, a.d, a.rev);
+  // position of staged token tid (tid < MT): pos0[b] + t, 0 past the end; the
+  // load is issued here and its value used in setup()
+  const long long pn = n0 + min(tid, MT - 1);
+  const bool pok = pn < ntok;
+  const int pb = pok ? (int)(pn / a.T) : 0;
+  const int pt = pok ? (int)(pn - (long long)pb * a.T) : 0;
+  const int pbase = a.pos0[pb];
+  auto setup = [&]() {
+    su.store(nullptr, gam, rev);
+    if (tid < MT) pos[tid] = pok ? pbase + pt : 0;
+  };
   const T* hrow[CPT];
   bool valid[CPT];
 #pragma unroll
@@ -85,13 +84,13 @@ __global__ __launch_bounds__(kNtTile, 1) void proj_kernel(ProjArgs a, int per_xc
     const int b = (int)(n / a.T), t = (int)(n - (long long)b * a.T);
     hrow[r] = static_cast<const T*>(a.h) + ((size_t)b * a.h_ld + t) * a.d + 8 * (tid & 7);
   }
-  __syncthreads();
 
   if constexpr (sizeof(T) == 2) {
-    MfmaTile<HD, MT, PACKED>::run(hrow, valid, gam, a.d, a.eps, halves, hst, rinv, pos, rev, kv);
+    MfmaTile<HD, MT, PACKED>::run(hrow, valid, gam, static_cast<const uint16_t*>(a.gamma), a.d, a.eps, halves, hst,
+                                  rinv, pos, rev, kv, setup);
   } else {
     F32Tile<HD, MT>::run(hrow, valid, static_cast<const float*>(a.gamma), a.d, a.eps, halves, hst, rinv, pos, rev,
-                         kv);
+                         kv, setup);
   }
   __syncthreads();
 
@@ -403,17 +402,22 @@ __global__ __launch_bounds__(kNtTile, 1) void fused_kernel(FusedArgs a, int per_
   const AttnLds AL = attn_lds(PL.end, g, HD, MT + FR);
   T* kv = reinterpret_cast<T*>(lds + PL.kv);
 
-  // A folded tail goes to the last recomputed tile's workgroup: its rows land
-  // in LDS rows MT.. while the tile is being recomputed.
+  // A folded tail goes to the last recomputed tile's workgroup: its rows are
+  // loaded with the setup values (one 16-byte chunk of a K | V row per thread;
+  // other threads load q, which is always readable) and land in LDS rows MT..
+  // while the tile is being recomputed.
   const bool tail_here = fold && rc == a.n_rec - 1;
+  constexpr int TCH = 2 * HD * (int)sizeof(T) / 16;  // chunks per K | V row
+  static_assert(FR * TCH <= NT, "one folded-tail chunk per thread");
+  const int tr = tid / TCH, tch = tid - tr * TCH;
+  const bool tail_mine = FR > 0 && tail_here && tr < a.T_tail;
+  u32x4_t tail_v;
   if constexpr (FR > 0) {
-    if (tail_here)
-      prefetch_rows_lds<T, HD>(static_cast<const T*>(a.tk), static_cast<const T*>(a.tv),
-                               ((size_t)b * a.n_kv + j) * a.tail_t_cap + a.tail_t_off, a.T_tail,
-                               kv + (size_t)MT * KLD);
+    const size_t trow = ((size_t)b * a.n_kv + j) * a.tail_t_cap + a.tail_t_off + tr;
+    const T* src = tch < TCH / 2 ? static_cast<const T*>(a.tk) + trow * HD + tch * (16 / sizeof(T))
+                                 : static_cast<const T*>(a.tv) + trow * HD + (tch - TCH / 2) * (16 / sizeof(T));
+    tail_v = *reinterpret_cast<const u32x4_t*>(tail_mine ? src : static_cast<const T*>(a.q));
   }
-
-  load_q<T, HD, NT>(static_cast<const T*>(a.q), b, a.n_q, j, g, reinterpret_cast<float*>(lds + AL.q));
 
   if (c >= n_tail) {
     const int t0 = rc * MT;
@@ -422,14 +426,17 @@ __global__ __launch_bounds__(kNtTile, 1) void fused_kernel(FusedArgs a, int per_
     float* rinv = reinterpret_cast<float*>(lds + PL.rinv);
     int* pos = reinterpret_cast<int*>(lds + PL.pos);
     T* hst = reinterpret_cast<T*>(lds + PL.hst);
-    if (tid < HD / 2) rev[tid] = a.rev[tid];
-    if (tid < MT) pos[tid] = a.pos0[b] + t0 + tid;
     uint16_t* gam = reinterpret_cast<uint16_t*>(lds + AL.end);
-    if constexpr (sizeof(T) == 2) {
-      for (int i = tid; i < a.d / 8; i += NT)
-        *reinterpret_cast<uint4*>(gam + 8 * i) =
-            *reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(a.gamma) + 8 * i);
-    }
+    // q, gamma and rev reach LDS while the K-loop's first loads are in flight
+    const TileSetup<T, HD, NT, true> su(static_cast<const T*>(a.q), b, a.n_q, j, g, a.gamma, a.d, a.rev);
+    const int p0 = a.pos0[b] + t0;
+    auto setup = [&]() {
+      su.store(reinterpret_cast<float*>(lds + AL.q), gam, rev);
+      if (tid < MT) pos[tid] = p0 + tid;
+      if constexpr (FR > 0) {
+        if (tail_mine) *reinterpret_cast<u32x4_t*>(kv + (size_t)(MT + tr) * KLD + tch * (16 / sizeof(T))) = tail_v;
+      }
+    };
     const T* hrow[CPT];
     bool valid[CPT];
 #pragma unroll
@@ -441,12 +448,12 @@ __global__ __launch_bounds__(kNtTile, 1) void fused_kernel(FusedArgs a, int per_
     const size_t hd_d = (size_t)HD * a.d;
     const Half halves[2] = {Half{static_cast<const T*>(a.w_k) + j * hd_d, 1},
                             Half{static_cast<const T*>(a.w_v) + j * hd_d, 0}};
-    __syncthreads();
     if constexpr (sizeof(T) == 2) {
-      MfmaTile<HD, MT, PACKED>::run(hrow, valid, gam, a.d, a.eps, halves, hst, rinv, pos, rev, kv);
+      MfmaTile<HD, MT, PACKED>::run(hrow, valid, gam, static_cast<const uint16_t*>(a.gamma), a.d, a.eps, halves, hst,
+                                    rinv, pos, rev, kv, setup);
     } else {
       F32Tile<HD, MT>::run(hrow, valid, static_cast<const float*>(a.gamma), a.d, a.eps, halves, hst, rinv, pos, rev,
-                           kv);
+                           kv, setup);
     }
     __syncthreads();
     if (a.dbg_k != nullptr) {
@@ -465,8 +472,6 @@ __global__ __launch_bounds__(kNtTile, 1) void fused_kernel(FusedArgs a, int per_
     int nk = n;
     if constexpr (FR > 0) {
       if (tail_here) {
-        __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0): this wave's tail row is in LDS
-        __syncthreads();
         if (n < MT) move_rows<T, HD, NT, FR>(kv, MT, n, a.T_tail);
         nk = n + a.T_tail;
       }
@@ -476,6 +481,7 @@ __global__ __launch_bounds__(kNtTile, 1) void fused_kernel(FusedArgs a, int per_
   } else {
     const int r0 = c * kTile;
     const int nk = min(kTile, a.T_tail - r0);
+    load_q<T, HD, NT>(static_cast<const T*>(a.q), b, a.n_q, j, g, reinterpret_cast<float*>(lds + AL.q));
     load_kv_tile<T, HD, NT>(static_cast<const T*>(a.tk), static_cast<const T*>(a.tv), b, a.n_kv, j, a.tail_t_cap,
                             a.tail_t_off + r0, nk, kv);
     __syncthreads();
