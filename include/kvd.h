@@ -58,7 +58,7 @@
 extern "C" {
 #endif
 
-#define KVD_ABI_VERSION 4
+#define KVD_ABI_VERSION 5
 
 typedef enum {
   KVD_OK = 0,
@@ -144,11 +144,14 @@ kvd_status kvd_project_qkv(const kvd_attn_shape* shape, const void* h_new, const
  * writes the last partial of a (sequence, KV head) merges them into out in the
  * same kernel (an atomic split counter in the workspace; no spin-waits).
  * ws (256-byte aligned) must hold kvd_workspace_bytes(shape, KVD_OP_DECODE_ATTN,
- * B, T, 0) bytes.  Workspace contract: its last kvd_workspace_bytes - (partials)
- * bytes hold split counters ([B][n_kv_heads] uint64) that must be zero before
- * the first call that uses them (allocate the workspace zero-filled once);
- * every call leaves them zero.  The rest of the workspace is overwritten.  Calls
- * sharing one workspace must be ordered on one stream.  With out == NULL only
+ * B, T, 0) bytes.  Workspace contract: its first bytes hold split counters
+ * ([B][n_kv_heads] uint64, padded to 256 bytes) that must be zero before the
+ * first call that uses them (allocate the workspace zero-filled once); every
+ * call leaves them zero.  The rest of the workspace is overwritten.  Their
+ * place depends on B only, so attention calls of any key count and op (decode,
+ * cached, fused) with the same B can share one workspace sized for the largest
+ * of them, as a decode loop whose context grows does.  Calls sharing one
+ * workspace must be ordered on one stream.  With out == NULL only
  * the partials are written (see kvd_combine) and the counters are not touched.
  *   q [B][n_q_heads][head_dim].   out [B][n_q_heads][head_dim].               */
 kvd_status kvd_decode_attn(const kvd_attn_shape* shape, const void* q, const kvd_kv_view* kv,

@@ -99,17 +99,23 @@ size_t ws_acc_bytes(const kvd_attn_shape* s, int32_t B, int32_t S) {
 size_t ws_ml_bytes(const kvd_attn_shape* s, int32_t B, int32_t S) {
   return kvd::align_up((size_t)B * s->n_q_heads * S * 2 * sizeof(float), 256);
 }
-// Workspace: partial accumulators [B][n_q][S][hd] fp32, partial (max, sum)
-// [B][n_q][S][2] fp32, split counters [B][n_kv] uint64 (zero between calls).
+size_t ws_done_bytes(const kvd_attn_shape* s, int32_t B) {
+  return kvd::align_up((size_t)B * s->n_kv_heads * sizeof(uint64_t), 256);
+}
+// Workspace: split counters [B][n_kv] uint64 first (zero between calls; their
+// place depends on B only, so calls with any key count can share one
+// workspace), then partial accumulators [B][n_q][S][hd] fp32 and partial
+// (max, sum) [B][n_q][S][2] fp32.
 size_t ws_total(const kvd_attn_shape* s, int32_t B, int32_t S) {
-  return ws_acc_bytes(s, B, S) + ws_ml_bytes(s, B, S) + kvd::align_up((size_t)B * s->n_kv_heads * sizeof(uint64_t), 256);
+  return ws_done_bytes(s, B) + ws_acc_bytes(s, B, S) + ws_ml_bytes(s, B, S);
+}
+float* ws_acc_ptr(const kvd_attn_shape* s, int32_t B, void* ws) {
+  return reinterpret_cast<float*>(static_cast<char*>(ws) + ws_done_bytes(s, B));
 }
 float* ws_ml_ptr(const kvd_attn_shape* s, int32_t B, int32_t S, void* ws) {
-  return reinterpret_cast<float*>(static_cast<char*>(ws) + ws_acc_bytes(s, B, S));
+  return reinterpret_cast<float*>(static_cast<char*>(ws) + ws_done_bytes(s, B) + ws_acc_bytes(s, B, S));
 }
-unsigned long long* ws_done_ptr(const kvd_attn_shape* s, int32_t B, int32_t S, void* ws) {
-  return reinterpret_cast<unsigned long long*>(static_cast<char*>(ws) + ws_acc_bytes(s, B, S) + ws_ml_bytes(s, B, S));
-}
+unsigned long long* ws_done_ptr(void* ws) { return static_cast<unsigned long long*>(ws); }
 
 kvd_status check_ws(const kvd_attn_shape* s, int32_t B, int32_t S, void* ws, size_t ws_bytes) {
   const size_t need = ws_total(s, B, S);
@@ -181,9 +187,9 @@ kvd_status attn_common(const kvd_attn_shape* shape, const void* q, const kvd_kv_
   a.t_cap = kv->t_cap;
   a.t_off = kv->t_off;
   a.out = out;
-  a.ws_acc = static_cast<float*>(ws);
+  a.ws_acc = ws_acc_ptr(shape, B, ws);
   a.ws_ml = ws_ml_ptr(shape, B, S, ws);
-  a.ws_done = ws_done_ptr(shape, B, S, ws);
+  a.ws_done = ws_done_ptr(ws);
   a.B = B;
   a.T = T;
   a.n_q = shape->n_q_heads;
@@ -367,9 +373,9 @@ kvd_status kvd_fused_recompute_attn(const kvd_attn_shape* shape, const void* q, 
     a.dbg_t_cap = kv_debug->t_cap;
     a.dbg_t_off = kv_debug->t_off;
   }
-  a.ws_acc = static_cast<float*>(ws);
+  a.ws_acc = ws_acc_ptr(shape, B, ws);
   a.ws_ml = ws_ml_ptr(shape, B, S, ws);
-  a.ws_done = ws_done_ptr(shape, B, S, ws);
+  a.ws_done = ws_done_ptr(ws);
   a.out = out;
   a.d = shape->d_model;
   a.n_q = shape->n_q_heads;
@@ -409,8 +415,8 @@ kvd_status kvd_combine(const kvd_attn_shape* shape, int32_t B, int32_t S, const 
   if (B == 0) return KVD_OK;
   KVD_TRY(check_ptr(out, "out"));
   KVD_TRY(check_ws(shape, B, S, const_cast<void*>(ws), ws_bytes));
-  const float* acc = static_cast<const float*>(ws);
-  const float* ml = reinterpret_cast<const float*>(static_cast<const char*>(ws) + ws_acc_bytes(shape, B, S));
+  const float* acc = ws_acc_ptr(shape, B, const_cast<void*>(ws));
+  const float* ml = ws_ml_ptr(shape, B, S, const_cast<void*>(ws));
   return device_status(kvd::launch_combine(acc, ml, out, shape->n_q_heads, B, S, shape->dtype == KVD_BF16,
                                            shape->head_dim, (hipStream_t)stream),
                        "kvd_combine launch");

@@ -181,7 +181,7 @@ def kvd_num_splits(shape: Shape, op: int, B: int, T_main: int, T_tail: int = 0) 
 
 def workspace(shape: Shape, op: int, B: int, T_main: int, T_tail: int = 0, device="cuda") -> torch.Tensor:
     """A zero-filled device buffer of kvd_workspace_bytes bytes (torch allocations are
-    256-byte aligned; the split counters at its end must start at zero)."""
+    256-byte aligned; the split counters at its start must be zero before first use)."""
     n = kvd_workspace_bytes(shape, op, B, T_main, T_tail)
     return torch.zeros(max(n, 256), dtype=torch.uint8, device=device)
 

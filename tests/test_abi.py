@@ -24,7 +24,7 @@ def view(t_cap=16, t_off=0, k=FAKE, v=FAKE):
 
 
 def test_loads_and_version():
-    assert kvd.abi_version() == 4
+    assert kvd.abi_version() == 5
     assert kvd.status_str(kvd.KVD_ERR_ALIGN) == "KVD_ERR_ALIGN"
 
 

@@ -303,8 +303,41 @@ def test_hybrid_budget_stored_window(dtype, T_rec, T):
     out3 = torch.empty_like(q)
     kvd.kvd_combine(s, L.B, kvd.kvd_num_splits(s, kvd.KVD_OP_FUSED, L.B, T_rec, T_tail), ws, out3)
     assert torch.equal(_bits(out), _bits(out3))
-    ctr_bytes = -(-L.B * s.n_kv_heads * 8 // 256) * 256  # the split counters close the workspace
-    assert int(torch.count_nonzero(ws[-ctr_bytes:])) == 0
+    ctr_bytes = -(-L.B * s.n_kv_heads * 8 // 256) * 256  # the split counters open the workspace
+    assert int(torch.count_nonzero(ws[:ctr_bytes])) == 0
+
+
+def test_workspace_shared_across_key_counts_and_ops():
+    # a decode loop keeps one workspace (sized for its largest call) while its
+    # context grows or restarts: the split counters sit at a place that depends
+    # on B only, so every call finds them zero whatever the previous call's split
+    # count was.  Each output equals the one computed with a fresh workspace.
+    L = make_layer(C.GEMMA3_4B, B=2, T=330, seed=77, d_model=512)
+    s = L.shape
+    q, K, V, _ = gpu_unfused(L)   # K/V rows 0..329 recomputed, row 330 the current token
+    def fused(T_rec, T_tail, ws):
+        out = torch.empty_like(q)
+        kvd.kvd_fused_recompute_attn(s, q, L.h, T_rec, L.gamma, L.lw_k, L.lw_v, L.pos0, out, ws, K, V, T_tail, T_rec)
+        return out
+
+    def decode(T, ws):
+        out = torch.empty_like(q)
+        kvd.kvd_decode_attn(s, q, K, V, T, out, ws, 331 - T)
+        return out
+
+    calls = [(fused, (330, 1)), (fused, (65, 1)), (decode, (331,)), (fused, (1, 1)), (fused, (260, 71)),
+             (decode, (5,)), (fused, (200, 131)), (fused, (330, 1))]
+    op_of = lambda fn: kvd.KVD_OP_DECODE_ATTN if fn is decode else kvd.KVD_OP_FUSED
+    big = max(kvd.kvd_workspace_bytes(s, op_of(fn), L.B, *args) for fn, args in calls)
+    shared = torch.zeros(big, dtype=torch.uint8, device="cuda")
+    for fn, args in calls:
+        fresh = kvd.workspace(s, op_of(fn), L.B, *args)
+        ref = fn(*args, fresh)
+        got = fn(*args, shared)
+        note(f"    {fn.__name__}{args}")
+        assert torch.equal(_bits(got), _bits(ref)), (fn.__name__, args)
+    ctr_bytes = -(-L.B * s.n_kv_heads * 8 // 256) * 256
+    assert int(torch.count_nonzero(shared[:ctr_bytes])) == 0
 
 
 @pytest.mark.parametrize("hd", [64, 128, 256])
