@@ -45,6 +45,8 @@ __all__ = [
     "project_qkv",
     "decode_attention",
     "kv_direct_decode",
+    "window_start",
+    "sliding_window_decode",
 ]
 
 
@@ -181,4 +183,35 @@ def kv_direct_decode(q, h_ctx, gamma, w_k, w_v, pos_ctx, k_tail, v_tail,
     if k_tail is not None:
         K = np.concatenate([K, _f64(k_tail)], axis=2)
         V = np.concatenate([V, _f64(v_tail)], axis=2)
+    return decode_attention(q, K, V)
+
+
+def window_start(n_keys, window):
+    """Index w of the oldest key a sliding window of `window` keys keeps out of
+    n_keys keys (the newest are kept): w = max(0, n_keys - window)."""
+    if window < 1:
+        raise ValueError("window must be >= 1")
+    return max(0, n_keys - window)
+
+
+def sliding_window_decode(h_new, h_ctx, gamma, w_q, w_k, w_v, window, n_q, n_kv, head_dim, eps, theta):
+    """One decode step of a sliding-window layer (Sec. 3.2, the sliding-window
+    boundary paragraph and Eq. sw_error; Sec. 5, the sliding-window limitation:
+    window-relative rotation plus a local attention mask).
+
+    The keys are the T checkpointed context rows h_ctx [B, T, d] followed by the
+    current token h_new [B, d] (key T).  Only the newest `window` of these T + 1
+    keys are attended (the local attention mask): keys j >= w = window_start(T + 1,
+    window).  Each kept key is rotated by R_{j-w}, its index inside the window,
+    instead of R_j, and the query by R_{T-w} (its own index in the window); V
+    carries no rotation.  K and V are recomputed from the residuals of the kept
+    rows exactly as in recompute_kv.
+    """
+    h_ctx, h_new = _f64(h_ctx), _f64(h_new)
+    B, T, _ = h_ctx.shape
+    w = window_start(T + 1, window)
+    rows = np.concatenate([h_ctx[:, w:T], h_new[:, None, :]], axis=1)   # keys w .. T
+    local = np.broadcast_to(np.arange(T + 1 - w, dtype=np.float64), (B, T + 1 - w))
+    K, V = recompute_kv(rows, gamma, w_k, w_v, local, n_kv, head_dim, eps, theta)
+    q, _, _ = project_qkv(h_new, gamma, w_q, w_k, w_v, np.full(B, float(T - w)), n_q, n_kv, head_dim, eps, theta)
     return decode_attention(q, K, V)

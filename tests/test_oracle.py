@@ -120,6 +120,83 @@ def test_sliding_window_error_closed_form():
     assert lhs > 1e-3
 
 
+def _sw_layer(B=2, T=13, d=32, n_q=4, n_kv=2, hd=8, seed=7):
+    r = np.random.default_rng(seed)
+    h_ctx = r.normal(0, 1, (B, T, d))
+    h_new = r.normal(0, 1, (B, d))
+    gamma = r.normal(1, 0.1, d)
+    wq, wk, wv = (r.normal(0, 0.3, (n * hd, d)) for n in (n_q, n_kv, n_kv))
+    return h_ctx, h_new, gamma, wq, wk, wv, n_q, n_kv, hd
+
+
+def test_sliding_window_start():
+    assert O.window_start(10, 4) == 6 and O.window_start(10, 10) == 0 and O.window_start(3, 1024) == 0
+    assert O.window_start(5, 1) == 4
+    with pytest.raises(ValueError):
+        O.window_start(5, 0)
+
+
+def test_sliding_window_wide_window_is_global_attention():
+    # A window holding every key (w = 0) is plain global attention at positions 0..T.
+    h_ctx, h_new, gamma, wq, wk, wv, n_q, n_kv, hd = _sw_layer()
+    B, T, _ = h_ctx.shape
+    rows = np.concatenate([h_ctx, h_new[:, None]], axis=1)
+    K, V = O.recompute_kv(rows, gamma, wk, wv, np.tile(np.arange(T + 1.0), (B, 1)), n_kv, hd, 1e-6, 1e4)
+    q = O.project_qkv(h_new, gamma, wq, wk, wv, np.full(B, float(T)), n_q, n_kv, hd, 1e-6, 1e4)[0]
+    ref = O.decode_attention(q, K, V)
+    for window in (T + 1, T + 50):
+        out = O.sliding_window_decode(h_new, h_ctx, gamma, wq, wk, wv, window, n_q, n_kv, hd, 1e-6, 1e4)
+        np.testing.assert_allclose(out, ref, rtol=1e-13, atol=1e-15)
+
+
+def test_sliding_window_rotation_offset_cancels_in_scores():
+    # Window-relative rotation of keys (R_{j-w}) and query (R_{T-w}) gives the same
+    # scores as absolute rotation over the same keys (R_j, R_T): <R_a x, R_b y> depends
+    # on b - a only.  A query and keys rotated with different offsets would not.
+    h_ctx, h_new, gamma, wq, wk, wv, n_q, n_kv, hd = _sw_layer(T=21)
+    B, T, _ = h_ctx.shape
+    for window in (1, 5, 9, 21):
+        w = O.window_start(T + 1, window)
+        rows = np.concatenate([h_ctx[:, w:], h_new[:, None]], axis=1)
+        K, V = O.recompute_kv(rows, gamma, wk, wv, np.tile(np.arange(w, T + 1.0), (B, 1)), n_kv, hd, 1e-6, 1e4)
+        q = O.project_qkv(h_new, gamma, wq, wk, wv, np.full(B, float(T)), n_q, n_kv, hd, 1e-6, 1e4)[0]
+        out = O.sliding_window_decode(h_new, h_ctx, gamma, wq, wk, wv, window, n_q, n_kv, hd, 1e-6, 1e4)
+        np.testing.assert_allclose(out, O.decode_attention(q, K, V), rtol=1e-9, atol=1e-12)
+
+
+def test_sliding_window_of_one_returns_current_value():
+    # window = 1 keeps only the current token: softmax over one key is 1, so every
+    # query head returns its KV head's V_t = RMSNorm(h_new) W_v (brute-force loops).
+    h_ctx, h_new, gamma, wq, wk, wv, n_q, n_kv, hd = _sw_layer()
+    B, T, d = h_ctx.shape
+    out = O.sliding_window_decode(h_new, h_ctx, gamma, wq, wk, wv, 1, n_q, n_kv, hd, 1e-6, 1e4)
+    g = n_q // n_kv
+    for b in range(B):
+        r = 1.0 / math.sqrt(sum(x * x for x in h_new[b]) / d + 1e-6)
+        for h in range(n_q):
+            j = h // g
+            for c in range(hd):
+                v = sum(wv[j * hd + c, i] * h_new[b, i] * r * gamma[i] for i in range(d))
+                assert abs(out[b, h, c] - v) <= 1e-12 * max(1.0, abs(v))
+
+
+def test_sliding_window_masks_older_keys():
+    # Keys older than the window do not take part: changing their residuals leaves
+    # the output bit-identical, changing the oldest kept key does not.
+    h_ctx, h_new, gamma, wq, wk, wv, n_q, n_kv, hd = _sw_layer(T=17)
+    window = 6
+    w = O.window_start(18, window)
+    base = O.sliding_window_decode(h_new, h_ctx, gamma, wq, wk, wv, window, n_q, n_kv, hd, 1e-6, 1e4)
+    h2 = h_ctx.copy()
+    h2[:, :w] = rng.normal(0, 3, h2[:, :w].shape)
+    assert np.array_equal(O.sliding_window_decode(h_new, h2, gamma, wq, wk, wv, window, n_q, n_kv, hd, 1e-6, 1e4),
+                          base)
+    h3 = h_ctx.copy()
+    h3[:, w] += 1.0
+    assert np.max(np.abs(O.sliding_window_decode(h_new, h3, gamma, wq, wk, wv, window, n_q, n_kv, hd, 1e-6, 1e4)
+                         - base)) > 1e-6
+
+
 # ---------------------------------------------------------------- projection (Eqs. k_proj / v_proj)
 
 def test_projection_brute_force_loops():
