@@ -488,7 +488,95 @@ def run_next(args, torch, np, kvd, configs, inputs, op_time, log):
         "recompute_faster_than_host_copy": [e["N"] for e in erows if e["recompute_us"] < e["host_copy_us"]]}
     del h, Kc, Vc, kv_dev, kv_host, flush_buf
     torch.cuda.empty_cache()
+    res["sliding_window"] = run_sliding(torch, kvd, configs, inputs, log)
     return res
+
+
+def run_sliding(torch, kvd, configs, inputs, log, window=1024):
+    """Sliding-window layers: a Gemma-3-4B-shaped decode step (34 layers, context 4096 + the
+    current token) whose layers l with l % 6 != 5 are sliding-window layers (29 of 34; the
+    window is a stand-in, the paper does not give its size) against the all-global step on
+    the same inputs, for B = 1 and 8.  Recompute path: kvd_project_qkv (the current token at
+    its window index on sliding layers) + kvd_fused_window_attn, which recomputes only the
+    window's residual rows.  Cached path: kvd_project_qkv into the cache + kvd_cached_attn
+    over all T + 1 rows (global layers) or over a window-sized buffer (sliding layers).
+    Eager steps of prebuilt C-ABI calls; HIP events around 10 steps after 2 warm-up steps."""
+    wl = configs.GEMMA3_4B
+    s = kvd.shape_of(wl).packed()
+    sc = s.c()
+    L, T, nq, nkv, hd = wl.layers, wl.ctx, wl.n_q, wl.n_kv, wl.head_dim
+    lib, dev = kvd.lib, "cuda"
+    stream = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    P = lambda t: ctypes.c_void_p(t.data_ptr())  # noqa: E731
+    sliding = [l % 6 != 5 for l in range(L)]
+    W = window
+    rows = []
+    for B in (1, 8):
+        log(f"[bench] next: sliding-window layers, B={B}")
+        layers = _model_layers(wl, s, kvd, inputs, L, B, T, dev)
+        pos0 = torch.zeros((B,), dtype=torch.int32, device=dev)
+        pos_g = torch.full((B,), T, dtype=torch.int32, device=dev)
+        pos_w = torch.full((B,), W - 1, dtype=torch.int32, device=dev)
+        q = torch.empty((B, nq, hd), dtype=torch.bfloat16, device=dev)
+        out = torch.empty_like(q)
+        tk = torch.zeros((B, nkv, 1, hd), dtype=torch.bfloat16, device=dev)
+        tv = torch.zeros_like(tk)
+        tail = kvd.KvView(tk.data_ptr(), tv.data_ptr(), 1, 0)
+        ws = kvd.workspace(s, kvd.KVD_OP_FUSED, B, T, 1)   # suffices for every call below
+
+        def fused_step(use_window):
+            calls = []
+            for ly, sw in zip(layers, sliding):
+                sw = sw and use_window
+                calls.append(Call(lib.kvd_project_qkv, ctypes.byref(sc), P(ly["h_new"]), P(ly["gamma"]),
+                                  P(ly["w_q"]), P(ly["w_k"]), P(ly["w_v"]), P(pos_w if sw else pos_g), B, P(q),
+                                  ctypes.byref(tail), stream))
+                if sw:
+                    calls.append(Call(lib.kvd_fused_window_attn, ctypes.byref(sc), P(q), P(ly["h"]), T,
+                                      P(ly["gamma"]), P(ly["w_k"]), P(ly["w_v"]), B, T, ctypes.byref(tail), 1, W,
+                                      P(out), P(ws), ws.numel(), stream))
+                else:
+                    calls.append(Call(lib.kvd_fused_recompute_attn, ctypes.byref(sc), P(q), P(ly["h"]), T,
+                                      P(ly["gamma"]), P(ly["w_k"]), P(ly["w_v"]), P(pos0), B, T,
+                                      ctypes.byref(tail), 1, P(out), P(ws), ws.numel(), None, stream))
+            return lambda: [c() for c in calls]
+
+        ms_fg = _step_timer(torch, fused_step(False), steps=10, warmup=2)
+        ms_fw = _step_timer(torch, fused_step(True), steps=10, warmup=2)
+        # cached: a full (T + 1)-row cache per global layer, a W-row buffer per sliding layer
+        wsc = kvd.workspace(s, kvd.KVD_OP_CACHED_ATTN, B, T + 1)
+        caches = []
+        for ly, sw in zip(layers, sliding):
+            Kc = torch.empty((B, nkv, T + 1, hd), dtype=torch.bfloat16, device=dev)
+            Vc = torch.empty_like(Kc)
+            kvd.kvd_recompute_kv(s, ly["h"], ly["gamma"], ly["w_k"], ly["w_v"], pos0, T, Kc, Vc, 0)
+            caches.append((Kc, Vc, kvd.KvView(Kc.data_ptr(), Vc.data_ptr(), T + 1, T),
+                           kvd.KvView(Kc.data_ptr(), Vc.data_ptr(), T + 1, 0),
+                           kvd.KvView(Kc.data_ptr(), Vc.data_ptr(), T + 1, T + 1 - W)))
+
+        def cached_step(use_window):
+            calls = []
+            for ly, sw, (_, _, vrow, vall, vwin) in zip(layers, sliding, caches):
+                sw = sw and use_window
+                calls.append(Call(lib.kvd_project_qkv, ctypes.byref(sc), P(ly["h_new"]), P(ly["gamma"]),
+                                  P(ly["w_q"]), P(ly["w_k"]), P(ly["w_v"]), P(pos_g), B, P(q),
+                                  ctypes.byref(vrow), stream))
+                calls.append(Call(lib.kvd_cached_attn, ctypes.byref(sc), P(q), ctypes.byref(vwin if sw else vall),
+                                  B, W if sw else T + 1, P(out), P(wsc), wsc.numel(), stream))
+            return lambda: [c() for c in calls]
+
+        ms_cg = _step_timer(torch, cached_step(False), steps=10, warmup=2)
+        ms_cw = _step_timer(torch, cached_step(True), steps=10, warmup=2)
+        rows.append({"B": B, "fused_all_global_ms": ms_fg, "fused_sliding_ms": ms_fw,
+                     "cached_all_global_ms": ms_cg, "cached_sliding_ms": ms_cw,
+                     "fused_sliding_tok_s": B / (ms_fw * 1e-3), "cached_sliding_tok_s": B / (ms_cw * 1e-3)})
+        log(f"[bench] next: sliding B={B}: fused {ms_fg:.3f} -> {ms_fw:.3f} ms/step, "
+            f"cached {ms_cg:.3f} -> {ms_cw:.3f} ms/step")
+        del layers, caches, ws, wsc
+        torch.cuda.empty_cache()
+    return {"workload": "gemma3-4b, 34 layers, ctx 4096 + current token", "window": W,
+            "sliding_layers": int(sum(sliding)), "global_layers": [l for l in range(L) if not sliding[l]],
+            "rows": rows}
 
 
 def _step_timer(torch, step, steps, warmup):

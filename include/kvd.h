@@ -58,7 +58,7 @@
 extern "C" {
 #endif
 
-#define KVD_ABI_VERSION 5
+#define KVD_ABI_VERSION 6
 
 typedef enum {
   KVD_OK = 0,
@@ -193,6 +193,28 @@ kvd_status kvd_fused_recompute_attn(const kvd_attn_shape* shape, const void* q, 
                                     int32_t T_rec, const kvd_kv_view* tail, int32_t T_tail,
                                     void* out, void* ws, size_t ws_bytes,
                                     const kvd_kv_view* kv_debug, void* stream);
+
+/* A sliding-window layer's decode-step attention (Sec. 3.2, the sliding-window
+ * boundary and Eq. sw_error; Sec. 5, the sliding-window limitation): of the
+ * T = T_rec + T_tail keys that kvd_fused_recompute_attn would attend (residual
+ * rows 0..T_rec-1 recomputed, then the stored tail rows), only the newest
+ * min(T, window) take part (the local attention mask), and the key with index i
+ * inside that window (i = 0 for the oldest kept key) is rotated by R_i, not by
+ * its absolute position (window-relative RoPE).  The max(0, T - window) oldest
+ * keys are dropped, recomputed rows first: the first kept residual row is
+ * recomputed at position 0, the next at 1, and so on.  Stored tail rows that are
+ * kept must carry the same window-relative rotation (e.g. the current token's K
+ * from kvd_project_qkv at position min(T, window) - 1), and so must q.
+ *   window >= 1.  Other arguments as in kvd_fused_recompute_attn (no pos0: the
+ *   positions are window indices; no kv_debug).
+ *   ws: kvd_workspace_bytes(shape, KVD_OP_FUSED, B, T_rec', T_tail') for the
+ *   kept counts; the value for (T_rec, T_tail) always suffices.  Split counters
+ *   as in kvd_decode_attn.                                                    */
+kvd_status kvd_fused_window_attn(const kvd_attn_shape* shape, const void* q, const void* h,
+                                 int32_t h_ld, const void* gamma, const void* w_k,
+                                 const void* w_v, int32_t B, int32_t T_rec,
+                                 const kvd_kv_view* tail, int32_t T_tail, int32_t window,
+                                 void* out, void* ws, size_t ws_bytes, void* stream);
 
 /* Weight packing (done once per frozen weight matrix; the weights of the paper's
  * projections are fixed at inference, Sec. 3.2): rewrites a row-major

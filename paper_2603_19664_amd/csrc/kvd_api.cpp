@@ -4,6 +4,7 @@
 
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -328,10 +329,11 @@ kvd_status kvd_cached_attn(const kvd_attn_shape* shape, const void* q, const kvd
   return attn_common(shape, q, kv, B, T, out, ws, ws_bytes, stream, true);
 }
 
-kvd_status kvd_fused_recompute_attn(const kvd_attn_shape* shape, const void* q, const void* h, int32_t h_ld,
-                                    const void* gamma, const void* w_k, const void* w_v, const int32_t* pos0,
-                                    int32_t B, int32_t T_rec, const kvd_kv_view* tail, int32_t T_tail, void* out,
-                                    void* ws, size_t ws_bytes, const kvd_kv_view* kv_debug, void* stream) {
+namespace {
+
+kvd_status check_fused_args(const kvd_attn_shape* shape, const void* q, const void* h, int32_t h_ld,
+                            const void* gamma, const void* w_k, const void* w_v, int32_t B, int32_t T_rec,
+                            const kvd_kv_view* tail, int32_t T_tail, void* out) {
   KVD_TRY(check_shape(shape));
   KVD_TRY(check_batch(B));
   if (T_rec < 0 || T_tail < 0 || (int64_t)T_rec + T_tail < 1)
@@ -346,10 +348,17 @@ kvd_status kvd_fused_recompute_attn(const kvd_attn_shape* shape, const void* q, 
     KVD_TRY(check_ptr(gamma, "gamma"));
     KVD_TRY(check_ptr(w_k, "w_k"));
     KVD_TRY(check_ptr(w_v, "w_v"));
-    if (pos0 == nullptr) return fail(KVD_ERR_NULL, "pos0 is NULL");
-    if (kv_debug != nullptr) KVD_TRY(check_view(kv_debug, T_rec, "kv_debug"));
   }
   if (T_tail > 0) KVD_TRY(check_view(tail, T_tail, "tail"));
+  return KVD_OK;
+}
+
+// The fused launch on validated arguments.  pos0 == nullptr: residual row 0 of
+// every sequence is at position 0.
+kvd_status fused_launch(const kvd_attn_shape* shape, const void* q, const void* h, int32_t h_ld, const void* gamma,
+                        const void* w_k, const void* w_v, const int32_t* pos0, int32_t B, int32_t T_rec,
+                        const kvd_kv_view* tail, int32_t T_tail, void* out, void* ws, size_t ws_bytes,
+                        const kvd_kv_view* kv_debug, void* stream, const char* name) {
   const int32_t S = splits(shape, KVD_OP_FUSED, T_rec, T_tail);
   KVD_TRY(check_ws(shape, B, S, ws, ws_bytes));
   kvd::FusedArgs a{};
@@ -388,7 +397,48 @@ kvd_status kvd_fused_recompute_attn(const kvd_attn_shape* shape, const void* q, 
   fill_rev(shape, a.rev);
   return device_status(kvd::launch_fused(a, shape->dtype == KVD_BF16, shape->head_dim,
                                          shape->w_layout == KVD_W_PACKED, (hipStream_t)stream),
-                       "kvd_fused_recompute_attn launch");
+                       name);
+}
+
+}  // namespace
+
+kvd_status kvd_fused_recompute_attn(const kvd_attn_shape* shape, const void* q, const void* h, int32_t h_ld,
+                                    const void* gamma, const void* w_k, const void* w_v, const int32_t* pos0,
+                                    int32_t B, int32_t T_rec, const kvd_kv_view* tail, int32_t T_tail, void* out,
+                                    void* ws, size_t ws_bytes, const kvd_kv_view* kv_debug, void* stream) {
+  KVD_TRY(check_fused_args(shape, q, h, h_ld, gamma, w_k, w_v, B, T_rec, tail, T_tail, out));
+  if (B == 0) return KVD_OK;
+  if (T_rec > 0) {
+    if (pos0 == nullptr) return fail(KVD_ERR_NULL, "pos0 is NULL");
+    if (kv_debug != nullptr) KVD_TRY(check_view(kv_debug, T_rec, "kv_debug"));
+  }
+  return fused_launch(shape, q, h, h_ld, gamma, w_k, w_v, pos0, B, T_rec, tail, T_tail, out, ws, ws_bytes, kv_debug,
+                      stream, "kvd_fused_recompute_attn launch");
+}
+
+kvd_status kvd_fused_window_attn(const kvd_attn_shape* shape, const void* q, const void* h, int32_t h_ld,
+                                 const void* gamma, const void* w_k, const void* w_v, int32_t B, int32_t T_rec,
+                                 const kvd_kv_view* tail, int32_t T_tail, int32_t window, void* out, void* ws,
+                                 size_t ws_bytes, void* stream) {
+  KVD_TRY(check_fused_args(shape, q, h, h_ld, gamma, w_k, w_v, B, T_rec, tail, T_tail, out));
+  if (window < 1) return fail(KVD_ERR_SHAPE, "window=%d must be >= 1", window);
+  if (B == 0) return KVD_OK;
+  // the oldest keys beyond the window go, recomputed rows first; the first kept
+  // recomputed row is window index 0
+  const int64_t drop = std::max<int64_t>(0, (int64_t)T_rec + T_tail - window);
+  const int32_t drop_rec = (int32_t)std::min<int64_t>(drop, T_rec);
+  const int32_t drop_tail = (int32_t)(drop - drop_rec);
+  const int32_t keep_rec = T_rec - drop_rec, keep_tail = T_tail - drop_tail;
+  const size_t elem = shape->dtype == KVD_BF16 ? 2 : 4;
+  const void* h_kept = keep_rec > 0 ? static_cast<const char*>(h) + (size_t)drop_rec * shape->d_model * elem : h;
+  kvd_kv_view tail_kept{};
+  if (keep_tail > 0) {
+    tail_kept = *tail;
+    tail_kept.t_off += drop_tail;
+  }
+  return fused_launch(shape, q, h_kept, h_ld, gamma, w_k, w_v, nullptr, B, keep_rec,
+                      keep_tail > 0 ? &tail_kept : nullptr, keep_tail, out, ws, ws_bytes, nullptr, stream,
+                      "kvd_fused_window_attn launch");
 }
 
 kvd_status kvd_pack_weights(const kvd_attn_shape* shape, const void* w, int32_t rows, void* packed, void* stream) {

@@ -429,7 +429,7 @@ __global__ __launch_bounds__(kNtTile, 1) void fused_kernel(FusedArgs a, int per_
     uint16_t* gam = reinterpret_cast<uint16_t*>(lds + AL.end);
     // q, gamma and rev reach LDS while the K-loop's first loads are in flight
     const TileSetup<T, HD, NT, true> su(static_cast<const T*>(a.q), b, a.n_q, j, g, a.gamma, a.d, a.rev);
-    const int p0 = a.pos0[b] + t0;
+    const int p0 = (a.pos0 != nullptr ? a.pos0[b] : 0) + t0;
     auto setup = [&]() {
       su.store(reinterpret_cast<float*>(lds + AL.q), gam, rev);
       if (tid < MT) pos[tid] = p0 + tid;

@@ -39,7 +39,7 @@ struct FusedArgs {
   const void* gamma;
   const void* w_k;
   const void* w_v;
-  const int32_t* pos0;
+  const int32_t* pos0;  // [B] position of residual row 0; nullptr: 0 for every sequence
   const void* tk;
   const void* tv;
   int tail_t_cap, tail_t_off, T_tail;

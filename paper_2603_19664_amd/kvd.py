@@ -64,6 +64,7 @@ def _load() -> ctypes.CDLL:
         "kvd_decode_attn": [S, VP, V, I32, I32, VP, VP, SZ, VP],
         "kvd_cached_attn": [S, VP, V, I32, I32, VP, VP, SZ, VP],
         "kvd_fused_recompute_attn": [S, VP, VP, I32, VP, VP, VP, VP, I32, I32, V, I32, VP, VP, SZ, V, VP],
+        "kvd_fused_window_attn": [S, VP, VP, I32, VP, VP, VP, I32, I32, V, I32, I32, VP, VP, SZ, VP],
     }
     for name, args in sig.items():
         f = getattr(lib, name)
@@ -253,3 +254,17 @@ def kvd_fused_recompute_attn(shape: Shape, q, h, T_rec: int, gamma, w_k, w_v, po
         ctypes.byref(tail) if tail is not None else None, T_tail, _ptr(out, "out", dt, 3) if out is not None else None,
         _ptr(ws, "ws"),
         ws.numel() * ws.element_size(), ctypes.byref(dbg) if dbg is not None else None, _stream()))
+
+
+def kvd_fused_window_attn(shape: Shape, q, h, T_rec: int, gamma, w_k, w_v, window: int, out, ws,
+                          tail_k=None, tail_v=None, T_tail: int = 0, tail_t_off: int = 0):
+    """Sliding-window attention of q over the newest `window` of [h rows 0..T_rec-1 recomputed || T_tail stored
+    tail rows], each kept key rotated by its index inside the window (out=None: partials only)."""
+    dt = shape.torch_dtype
+    tail = _view(tail_k, tail_v, tail_t_off, "tail", dt)
+    _check(lib.kvd_fused_window_attn(
+        ctypes.byref(shape.c()), _ptr(q, "q", dt, 3), _ptr(h, "h", dt, 3), h.shape[1] if h is not None else 0,
+        _ptr(gamma, "gamma", dt), _ptr(w_k, "w_k", dt), _ptr(w_v, "w_v", dt), q.shape[0], T_rec,
+        ctypes.byref(tail) if tail is not None else None, T_tail, window,
+        _ptr(out, "out", dt, 3) if out is not None else None, _ptr(ws, "ws"), ws.numel() * ws.element_size(),
+        _stream()))

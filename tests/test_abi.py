@@ -24,7 +24,7 @@ def view(t_cap=16, t_off=0, k=FAKE, v=FAKE):
 
 
 def test_loads_and_version():
-    assert kvd.abi_version() == 5
+    assert kvd.abi_version() == 6
     assert kvd.status_str(kvd.KVD_ERR_ALIGN) == "KVD_ERR_ALIGN"
 
 
@@ -114,6 +114,27 @@ def test_fused_validation():
     assert fused(s, B=70000) == kvd.KVD_ERR_SHAPE
     assert lib.kvd_fused_recompute_attn(ctypes.byref(s), FAKE, FAKE, 64, FAKE, FAKE, FAKE, FAKE, 1, 64, None, 1,
                                         FAKE, FAKE, 1 << 30, None, None) == kvd.KVD_ERR_NULL
+
+
+def window_call(s, q=FAKE, h=FAKE, h_ld=64, T_rec=64, tail=None, T_tail=1, window=16, ws_bytes=1 << 30):
+    tail = view() if tail is None else tail
+    return lib.kvd_fused_window_attn(ctypes.byref(s), q, h, h_ld, FAKE, FAKE, FAKE, 1, T_rec, ctypes.byref(tail),
+                                     T_tail, window, FAKE, FAKE, ws_bytes, None)
+
+
+def test_window_validation():
+    s = shape()
+    assert window_call(s, window=0) == kvd.KVD_ERR_SHAPE
+    assert window_call(s, window=-3) == kvd.KVD_ERR_SHAPE
+    assert window_call(s, T_rec=0, T_tail=0) == kvd.KVD_ERR_SHAPE
+    assert window_call(s, h_ld=32) == kvd.KVD_ERR_SHAPE
+    assert window_call(s, h=None) == kvd.KVD_ERR_NULL
+    assert window_call(s, q=None) == kvd.KVD_ERR_NULL
+    assert window_call(s, tail=view(t_cap=4, t_off=4)) == kvd.KVD_ERR_SHAPE
+    assert window_call(s, ws_bytes=100) == kvd.KVD_ERR_WORKSPACE
+    # the kept rows set the split count: 16 kept keys need one split
+    need = lib.kvd_workspace_bytes(ctypes.byref(s), kvd.KVD_OP_FUSED, 1, 15, 1)
+    assert window_call(s, ws_bytes=need - 1) == kvd.KVD_ERR_WORKSPACE
 
 
 def test_project_validation():
