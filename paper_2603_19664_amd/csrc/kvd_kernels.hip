@@ -190,10 +190,10 @@ __global__ __launch_bounds__(64 * kStreamWaves) void stream_proj_kernel(ProjArgs
     for (int i = 0; i < LPW; ++i)
       *reinterpret_cast<u32x4_t*>(slot + (ld * LPW + i) * 512) = rv[i];
   };
-  // gamma * h -> bf16 into hs (present rows only), by wave 0
+  // gamma * h -> bf16 into hs (present rows only), by all waves between barriers A and C
   auto scale_rows = [&]() {
     const int cpr = d / 8;
-    for (int i = lane; i < nt * cpr; i += 64) {
+    for (int i = tid; i < nt * cpr; i += 64 * NW) {
       const int r = i / cpr, ch = i - r * cpr;
       *reinterpret_cast<uint4*>(hs + (size_t)r * HLD + 8 * ch) =
           scale_chunk_bf16(*reinterpret_cast<const uint4*>(hb + (size_t)r * HLD + 8 * ch),
@@ -211,7 +211,7 @@ __global__ __launch_bounds__(64 * kStreamWaves) void stream_proj_kernel(ProjArgs
     // one instruction per 1 KiB of a row, rows spread over the loaders), then the
     // first two chunks of weights.  A barrier after global-to-LDS copies waits
     // for every outstanding load, so the remaining chunks are issued after it
-    // (while wave 0 scales the rows).
+    // (with their share of the row scaling).
     {
       const int cpr = d / 8;  // 16-byte chunks per row
       for (int r = ld; r <= nt; r += NW - 1) {
@@ -231,6 +231,7 @@ __global__ __launch_bounds__(64 * kStreamWaves) void stream_proj_kernel(ProjArgs
 #pragma unroll
     for (int u = 2; u < D; ++u)
       if (u < nchunks) load_chunk(wr[u], u);
+    scale_rows();
     store_chunk(wr[0], 0);
     if (D < nchunks) load_chunk(wr[0], D);
     __syncthreads();
@@ -298,8 +299,8 @@ __global__ __launch_bounds__(64 * kStreamWaves) void stream_proj_kernel(ProjArgs
     return;
   }
 
-  // wave 0: the RoPE table and positions, then (while the loaders issue their
-  // weights) gamma * h for all rows, then the MFMA chain
+  // wave 0: the RoPE table and positions, then its share of gamma * h (while the
+  // loaders issue their weights and scale theirs), then the MFMA chain
   for (int i = lane; i < HD / 2; i += 64) rev[i] = a.rev[i];
   if (lane < kProjTok) {
     const int nb = (n0 + lane) / a.T, ntk = n0 + lane - nb * a.T;
