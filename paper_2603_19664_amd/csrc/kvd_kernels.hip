@@ -374,14 +374,13 @@ __global__ __launch_bounds__(64 * kStreamWaves) void stream_proj_kernel(ProjArgs
 
 // ------------------------------------------------------------------ fused recompute + attention
 
-// grid: xcd_map(n_kv * B * C) workgroups, item = (j * B + b) * C + c (the chunks of
-// one KV head, which share W_k / W_v, run on one XCD), C = n_tail + n_rec.  Items
-// c < n_tail attend stored tail tile c (64 rows; partial n_rec + c) and come first,
-// as they are short; item n_tail + r recomputes residual rows r*MT..r*MT+MT-1
-// (partial r).  A folded tail (<= fold_rows<T>() rows, n_tail = 0) is attended
+// grid: xcd_map(n_kv * B * C) workgroups, one per (KV head j, sequence b, chunk c),
+// C = n_tail + n_rec.  Chunks c < n_tail attend stored tail tile c (64 rows;
+// partial n_rec + c) and come first, as they are short; chunk n_tail + r
+// recomputes residual rows r*MT..r*MT+MT-1 (partial r).  A folded tail (<= fold_rows<T>() rows, n_tail = 0) is attended
 // with the last recomputed chunk's keys.
 template <typename T, int HD, int MT, bool PACKED>
-__global__ __launch_bounds__(kNtTile, 1) void fused_kernel(FusedArgs a, int per_xcd) {
+__global__ __launch_bounds__(kNtTile, 1) void fused_kernel(FusedArgs a, int per_xcd, int hg) {
   extern __shared__ __align__(16) char lds[];
   constexpr int NT = kNtTile;
   constexpr int FR = fold_rows<T>();
@@ -395,10 +394,17 @@ __global__ __launch_bounds__(kNtTile, 1) void fused_kernel(FusedArgs a, int per_
   const int C = n_tail + a.n_rec;
   const long long item = (long long)(blockIdx.x % kXcds) * per_xcd + blockIdx.x / kXcds;
   if (item >= (long long)a.n_kv * a.B * C) return;
-  const int c = (int)(item % C);
+  // Items in XCD order: KV heads in groups of hg (a power of two dividing n_kv) of
+  // one sequence, the group's chunks in order, its heads alternating.  An XCD's
+  // run of per_xcd items then spans hg heads and per_xcd / hg chunks; it pulls
+  // each of those residual tiles and each of those heads' weights into its own
+  // L2 once.  The host picks hg to balance the two streams (fused_head_group).
+  const long long gi = item / ((long long)hg * C), rem = item - gi * hg * C;  // group index jg * B + b
+  const int jg = (int)(gi / a.B);
+  const int b = (int)(gi - (long long)jg * a.B);
+  const int c = (int)(rem / hg);
+  const int j = jg * hg + (int)(rem - (long long)c * hg);
   const int rc = c - n_tail;  // recomputed chunk (c >= n_tail)
-  const int unit = (int)(item / C);
-  const int j = unit / a.B, b = unit - j * a.B;
   const int g = a.n_q / a.n_kv;
   const AttnLds AL = attn_lds(PL.end, g, HD, MT + FR);
   T* kv = reinterpret_cast<T*>(lds + PL.kv);
@@ -622,7 +628,7 @@ static hipError_t fused_t(const FusedArgs& a, hipStream_t st) {
   if (e != hipSuccess) return e;
   const int C = fused_tail_tiles<T>(a.n_rec, a.T_tail) + a.n_rec;
   const XcdMap m = xcd_map((long long)a.n_kv * a.B * C);
-  hipLaunchKernelGGL(k, dim3(m.grid), dim3(kNtTile), bytes, st, a, m.per);
+  hipLaunchKernelGGL(k, dim3(m.grid), dim3(kNtTile), bytes, st, a, m.per, fused_head_group(a.n_kv, HD, m.per));
   return hipGetLastError();
 }
 

@@ -194,4 +194,15 @@ constexpr XcdMap xcd_map(long long n_items) {
   return m;
 }
 
+// Heads per group in the fused kernel's item order: per XCD, per items are hg
+// heads x per / hg chunks, and the XCD's L2 takes (per / hg) residual tiles of
+// 64 d-vectors plus hg heads' W_k | W_v (2 hd d-vectors each).  Their sum is
+// least at hg^2 = 32 per / hd; the largest power of two at or below that which
+// divides n_kv.
+constexpr int fused_head_group(int n_kv, int hd, int per) {
+  int hg = 1;
+  while (n_kv % (2 * hg) == 0 && (long long)(2 * hg) * (2 * hg) * hd <= 32LL * per) hg *= 2;
+  return hg;
+}
+
 }  // namespace kvd
