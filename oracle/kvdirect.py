@@ -47,6 +47,11 @@ __all__ = [
     "kv_direct_decode",
     "window_start",
     "sliding_window_decode",
+    "silu",
+    "swiglu_mlp",
+    "causal_attention",
+    "block_forward",
+    "recompute_residual",
 ]
 
 
@@ -215,3 +220,69 @@ def sliding_window_decode(h_new, h_ctx, gamma, w_q, w_k, w_v, window, n_q, n_kv,
     K, V = recompute_kv(rows, gamma, w_k, w_v, local, n_kv, head_dim, eps, theta)
     q, _, _ = project_qkv(h_new, gamma, w_q, w_k, w_v, np.full(B, float(T - w)), n_q, n_kv, head_dim, eps, theta)
     return decode_attention(q, K, V)
+
+
+# ---------------------------------------------------------------- single-checkpoint scheme
+
+def silu(x):
+    """SiLU(x) = x * sigmoid(x) = x / (1 + e^-x)."""
+    x = _f64(x)
+    return x / (1.0 + np.exp(-x))
+
+
+def swiglu_mlp(x, w_gate, w_up, w_down):
+    """The MLP of Eq. mlp_sublayer.  The paper leaves its form open; the reading is
+    the gated SiLU MLP of the LLaMA and Qwen families the paper evaluates:
+    MLP(x) = (SiLU(x W_gate) * (x W_up)) W_down, weights stored [out][in]."""
+    x = _f64(x)
+    return (silu(x @ _f64(w_gate).T) * (x @ _f64(w_up).T)) @ _f64(w_down).T
+
+
+def causal_attention(q, K, V):
+    """Attention of every position over itself and the positions before it
+    (Eqs. attn_weights / head_output with the decoder's causal order: position p
+    attends keys j <= p).  q [B, n_q, T, hd]; K, V [B, n_kv, T, hd]; query head h
+    reads KV head floor(h / g).  Returns [B, T, n_q * hd] (heads concatenated, the
+    input of W_o in Eq. attn_sublayer)."""
+    q, K, V = _f64(q), _f64(K), _f64(V)
+    B, n_q, T, hd = q.shape
+    g = n_q // K.shape[1]
+    out = np.empty((B, T, n_q * hd), dtype=np.float64)
+    for b in range(B):
+        for h in range(n_q):
+            Kh, Vh = K[b, h // g], V[b, h // g]
+            for p in range(T):
+                s = Kh[:p + 1] @ q[b, h, p] / math.sqrt(hd)
+                e = np.exp(s - np.max(s))
+                out[b, p, h * hd:(h + 1) * hd] = (e / np.sum(e)) @ Vh[:p + 1]
+    return out
+
+
+def block_forward(h, pos, gamma_attn, w_q, w_k, w_v, w_o, gamma_mlp, w_gate, w_up, w_down,
+                  n_q, n_kv, head_dim, eps, theta):
+    """One pre-norm transformer block over all T positions of each sequence
+    (Sec. 3.1, Eqs. q_proj .. mlp_sublayer): h [B, T, d] at positions pos [B, T]
+    -> h^(l+1) [B, T, d].
+
+    hbar = RMSNorm(h; gamma_attn); q, K, V per Eqs. q_proj / k_proj / v_proj (RoPE
+    on q and K); heads by causal attention; hhat = h + [heads] W_o (Eq.
+    attn_sublayer); h' = hhat + MLP(RMSNorm(hhat; gamma_mlp)) (Eq. mlp_sublayer).
+    W_o is stored [d][n_q * head_dim]."""
+    h = _f64(h)
+    hbar = rms_normalize(h, gamma_attn, eps)
+    q = apply_rope(project_heads(hbar, w_q, n_q, head_dim), _f64(pos)[..., None], theta)
+    K, V = recompute_kv(h, gamma_attn, w_k, w_v, pos, n_kv, head_dim, eps, theta)
+    heads = causal_attention(q.transpose(0, 2, 1, 3), K, V)
+    hhat = h + heads @ _f64(w_o).T
+    return hhat + swiglu_mlp(rms_normalize(hhat, gamma_mlp, eps), w_gate, w_up, w_down)
+
+
+def recompute_residual(h0, pos, layers, n_layers, n_q, n_kv, head_dim, eps, theta):
+    """The single-checkpoint scheme (Eq. res_mem: one residual vector per token
+    serves every layer): h^(l) for l = n_layers, from the checkpoint h^(0) by
+    running blocks 0 .. n_layers - 1 over all positions.  layers[i] holds block i's
+    (gamma_attn, w_q, w_k, w_v, w_o, gamma_mlp, w_gate, w_up, w_down)."""
+    h = _f64(h0)
+    for i in range(n_layers):
+        h = block_forward(h, pos, *layers[i], n_q, n_kv, head_dim, eps, theta)
+    return h

@@ -344,3 +344,125 @@ def test_decode_step_concat_and_current_token():
     out2 = O.kv_direct_decode(q2, h[:, :T], gamma, wk, wv, pos[:, :T] + 1000, kt2[:, :, None],
                               vt2[:, :, None], n_kv, hd, 1e-6, 1e4)
     np.testing.assert_allclose(out2, out, rtol=1e-9, atol=1e-12)
+
+
+# ---------------------------------------------------------------- single-checkpoint scheme (Sec. 3.1 block)
+
+def test_silu_closed_forms():
+    x = rng.normal(0, 3, 50)
+    np.testing.assert_allclose(O.silu(x) - O.silu(-x), x, rtol=1e-14, atol=1e-14)  # x s(x) + x s(-x) = x
+    assert O.silu(0.0) == 0.0
+    np.testing.assert_allclose(O.silu(1.0), 1.0 / (1.0 + math.exp(-1.0)), rtol=1e-15)
+    np.testing.assert_allclose(O.silu(40.0), 40.0, rtol=1e-15)
+
+
+def _block_params(d, n_q, n_kv, hd, dff, r):
+    return (r.normal(1, 0.1, d), r.normal(0, 0.3, (n_q * hd, d)), r.normal(0, 0.3, (n_kv * hd, d)),
+            r.normal(0, 0.3, (n_kv * hd, d)), r.normal(0, 0.3, (d, n_q * hd)), r.normal(1, 0.1, d),
+            r.normal(0, 0.3, (dff, d)), r.normal(0, 0.3, (dff, d)), r.normal(0, 0.3, (d, dff)))
+
+
+def test_swiglu_mlp_brute_force():
+    r = np.random.default_rng(3)
+    d, dff = 5, 7
+    x = r.normal(0, 1, (2, d))
+    wg, wu, wd = r.normal(0, 1, (dff, d)), r.normal(0, 1, (dff, d)), r.normal(0, 1, (d, dff))
+    out = O.swiglu_mlp(x, wg, wu, wd)
+    for b in range(2):
+        for o in range(d):
+            acc = 0.0
+            for f in range(dff):
+                gt = sum(wg[f, i] * x[b, i] for i in range(d))
+                ut = sum(wu[f, i] * x[b, i] for i in range(d))
+                acc += wd[o, f] * gt / (1.0 + math.exp(-gt)) * ut
+            assert abs(out[b, o] - acc) <= 1e-12 * max(1.0, abs(acc))
+
+
+def test_causal_attention_first_position_causality_and_last_position():
+    r = np.random.default_rng(4)
+    B, n_q, n_kv, T, hd = 2, 4, 2, 9, 8
+    q = r.normal(0, 1, (B, n_q, T, hd))
+    K, V = r.normal(0, 1, (B, n_kv, T, hd)), r.normal(0, 1, (B, n_kv, T, hd))
+    out = O.causal_attention(q, K, V)
+    # position 0 has one key: its output is V_0 of its KV head
+    for h in range(n_q):
+        np.testing.assert_allclose(out[:, 0, h * hd:(h + 1) * hd], V[:, h // 2, 0], rtol=1e-14)
+    # keys after p do not reach p
+    K2, V2 = K.copy(), V.copy()
+    K2[:, :, 5:] += 3.0
+    V2[:, :, 5:] -= 2.0
+    assert np.array_equal(O.causal_attention(q, K2, V2)[:, :5], out[:, :5])
+    # the last position sees every key: the decode attention of its query
+    last = O.decode_attention(q[:, :, T - 1], K, V)
+    np.testing.assert_allclose(out[:, T - 1].reshape(B, n_q, hd), last, rtol=1e-12, atol=1e-14)
+
+
+def test_block_with_zero_output_projections_is_identity():
+    # Eqs. attn_sublayer / mlp_sublayer add to the residual: with W_o = 0 and W_down = 0
+    # both sub-layers add exactly zero.
+    r = np.random.default_rng(5)
+    B, T, d, n_q, n_kv, hd, dff = 2, 6, 16, 4, 2, 4, 24
+    p = list(_block_params(d, n_q, n_kv, hd, dff, r))
+    p[4] = np.zeros_like(p[4])
+    p[8] = np.zeros_like(p[8])
+    h = r.normal(0, 1, (B, T, d))
+    pos = np.tile(np.arange(T), (B, 1))
+    assert np.array_equal(O.block_forward(h, pos, *p, n_q, n_kv, hd, 1e-6, 1e4), h)
+
+
+def test_block_brute_force_tiny():
+    # The whole block written out with scalar loops (math.cos / math.sin RoPE on
+    # consecutive pairs, explicit causal softmax, SiLU-gated MLP).
+    r = np.random.default_rng(6)
+    T, d, n_q, n_kv, hd, dff, eps, theta = 4, 6, 2, 1, 4, 5, 1e-6, 100.0
+    ga, wq, wk, wv, wo, gm, wg, wu, wd = _block_params(d, n_q, n_kv, hd, dff, r)
+    h = r.normal(0, 1, (1, T, d))
+    pos = np.array([[3, 4, 5, 6]])
+    got = O.block_forward(h, pos, ga, wq, wk, wv, wo, gm, wg, wu, wd, n_q, n_kv, hd, eps, theta)[0]
+
+    def norm(x, g):
+        ms = sum(v * v for v in x) / len(x)
+        return [x[i] / math.sqrt(ms + eps) * g[i] for i in range(len(x))]
+
+    def rope(v, p):
+        o = list(v)
+        for i in range(len(v) // 2):
+            a = p * theta ** (-2.0 * i / len(v))
+            o[2 * i] = v[2 * i] * math.cos(a) - v[2 * i + 1] * math.sin(a)
+            o[2 * i + 1] = v[2 * i] * math.sin(a) + v[2 * i + 1] * math.cos(a)
+        return o
+
+    def mat(W, x, r0, n):
+        return [sum(W[r0 + o, i] * x[i] for i in range(len(x))) for o in range(n)]
+
+    x = [list(h[0, t]) for t in range(T)]
+    xb = [norm(x[t], ga) for t in range(T)]
+    Q = [[rope(mat(wq, xb[t], hh * hd, hd), pos[0, t]) for hh in range(n_q)] for t in range(T)]
+    Kt = [rope(mat(wk, xb[t], 0, hd), pos[0, t]) for t in range(T)]
+    Vt = [mat(wv, xb[t], 0, hd) for t in range(T)]
+    for t in range(T):
+        heads = []
+        for hh in range(n_q):
+            s = [sum(Q[t][hh][c] * Kt[j][c] for c in range(hd)) / math.sqrt(hd) for j in range(t + 1)]
+            m = max(s)
+            e = [math.exp(v - m) for v in s]
+            z = sum(e)
+            heads += [sum(e[j] / z * Vt[j][c] for j in range(t + 1)) for c in range(hd)]
+        hhat = [x[t][o] + sum(wo[o, i] * heads[i] for i in range(n_q * hd)) for o in range(d)]
+        hn = norm(hhat, gm)
+        gu = [(mat(wg, hn, f, 1)[0], mat(wu, hn, f, 1)[0]) for f in range(dff)]
+        act = [gv / (1.0 + math.exp(-gv)) * uv for gv, uv in gu]
+        ref = [hhat[o] + sum(wd[o, f] * act[f] for f in range(dff)) for o in range(d)]
+        np.testing.assert_allclose(got[t], ref, rtol=1e-12, atol=1e-12)
+
+
+def test_recompute_residual_composes_blocks():
+    r = np.random.default_rng(7)
+    B, T, d, n_q, n_kv, hd, dff = 1, 5, 8, 2, 1, 4, 12
+    layers = [_block_params(d, n_q, n_kv, hd, dff, r) for _ in range(3)]
+    h0 = r.normal(0, 1, (B, T, d))
+    pos = np.tile(np.arange(T), (B, 1))
+    assert np.array_equal(O.recompute_residual(h0, pos, layers, 0, n_q, n_kv, hd, 1e-6, 1e4), h0)
+    h2 = O.block_forward(O.block_forward(h0, pos, *layers[0], n_q, n_kv, hd, 1e-6, 1e4), pos, *layers[1],
+                         n_q, n_kv, hd, 1e-6, 1e4)
+    assert np.array_equal(O.recompute_residual(h0, pos, layers, 2, n_q, n_kv, hd, 1e-6, 1e4), h2)
