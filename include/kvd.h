@@ -58,7 +58,7 @@
 extern "C" {
 #endif
 
-#define KVD_ABI_VERSION 6
+#define KVD_ABI_VERSION 7
 
 typedef enum {
   KVD_OK = 0,
@@ -228,6 +228,54 @@ kvd_status kvd_fused_window_attn(const kvd_attn_shape* shape, const void* q, con
  * must not alias w.  shape->dtype must be KVD_BF16 (w_layout is ignored).    */
 kvd_status kvd_pack_weights(const kvd_attn_shape* shape, const void* w, int32_t rows, void* packed,
                             void* stream);
+
+/* kvd_pack_weights for any bf16 matrix [rows][cols] (rows % 32 == 0,
+ * cols % 16 == 0): block (r, c) of 32 rows x 16 columns is 512 elements at
+ * offset (r * cols/16 + c) * 512 in MFMA A-operand lane order.  Used for the
+ * block forward's W_o [d_model][n_q*head_dim] and W_down [d_model][d_ff], whose
+ * rows are not d_model long.  packed must not alias w.                       */
+kvd_status kvd_pack_matrix(const void* w, int32_t rows, int32_t cols, void* packed, void* stream);
+
+/* The single-checkpoint scheme (Eq. res_mem: one residual vector per token
+ * serves all layers; Algorithm 1 otherwise stores a residual per layer):
+ * h^(l+1) of every position from h^(l), by one pre-norm transformer block
+ * (Sec. 3.1, Eqs. q_proj, k_proj, v_proj, attn_weights, head_output,
+ * attn_sublayer, mlp_sublayer).  Running it for layers 0 .. l-1 recomputes h^(l)
+ * from the checkpoint h^(0).  For each sequence b and position t (at pos0[b]+t):
+ *   hbar = RMSNorm(h; gamma_attn); q, K, V as kvd_recompute_kv / kvd_project_qkv
+ *   compute them (the same tile engine and arithmetic); heads = causal attention
+ *   (position t attends positions <= t); hhat = h + heads W_o^T;
+ *   h_out = hhat + (SiLU(xbar W_gate^T) * (xbar W_up^T)) W_down^T,
+ *   xbar = RMSNorm(hhat; gamma_mlp).
+ * The MLP's form is not given by the paper; this is the SiLU-gated MLP of the
+ * LLaMA and Qwen families it evaluates.  Weights are [out][in]: W_q
+ * [n_q*hd][d], W_k/W_v [n_kv*hd][d], W_o [d][n_q*hd], W_gate/W_up [d_ff][d],
+ * W_down [d][d_ff]; shape->w_layout applies to all of them (packed: each
+ * through kvd_pack_weights / kvd_pack_matrix).  bf16 only; head_dim 128 or
+ * 256; d_model % 512 == 0; d_ff % 256 == 0.  q, K, V, the heads, hhat and the
+ * MLP activation are rounded to bf16 between kernels (RNE), accumulation fp32.
+ *   h_in, h_out [B][T][d_model] (must not overlap).   pos0 [B] int32.
+ *   ws: kvd_block_workspace_bytes(shape, d_ff, B, T) bytes, 256-byte aligned,
+ *   overwritten.  B == 0 or T == 0 is a no-op.                                */
+typedef struct {
+  const void* gamma_attn;
+  const void* w_q;
+  const void* w_k;
+  const void* w_v;
+  const void* w_o;
+  const void* gamma_mlp;
+  const void* w_gate;
+  const void* w_up;
+  const void* w_down;
+  int32_t d_ff;
+} kvd_block_weights;
+
+kvd_status kvd_block_forward(const kvd_attn_shape* shape, const kvd_block_weights* w,
+                             const void* h_in, void* h_out, const int32_t* pos0, int32_t B,
+                             int32_t T, void* ws, size_t ws_bytes, void* stream);
+
+/* Workspace bytes of kvd_block_forward (0 on invalid arguments).              */
+size_t kvd_block_workspace_bytes(const kvd_attn_shape* shape, int32_t d_ff, int32_t B, int32_t T);
 
 /* Merge step of split-K attention: out[b][h] = sum_s w_s acc_s / sum_s w_s l_s
  * with w_s = 2^(m_s - max_s m_s), over the S partial softmax states that a

@@ -13,7 +13,7 @@ INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libkvd.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
-SOURCES = ["kvd_api.cpp", "kvd_kernels.hip"]
+SOURCES = ["kvd_api.cpp", "kvd_kernels.hip", "kvd_block.hip"]
 FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++20", "-fPIC", "-shared",
     # no packed-fp32 instructions in generated code

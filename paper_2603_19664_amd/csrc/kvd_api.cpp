@@ -441,6 +441,173 @@ kvd_status kvd_fused_window_attn(const kvd_attn_shape* shape, const void* q, con
                       "kvd_fused_window_attn launch");
 }
 
+kvd_status kvd_pack_matrix(const void* w, int32_t rows, int32_t cols, void* packed, void* stream) {
+  if (rows < 32 || rows % 32 != 0) return fail(KVD_ERR_SHAPE, "rows=%d must be a positive multiple of 32", rows);
+  if (cols < 16 || cols % 16 != 0) return fail(KVD_ERR_SHAPE, "cols=%d must be a positive multiple of 16", cols);
+  KVD_TRY(check_ptr(w, "w"));
+  KVD_TRY(check_ptr(packed, "packed"));
+  const size_t bytes = (size_t)rows * cols * 2;
+  const char* a = static_cast<const char*>(w);
+  const char* b = static_cast<const char*>(packed);
+  if (a < b + bytes && b < a + bytes) return fail(KVD_ERR_SHAPE, "packed must not overlap w");
+  return device_status(kvd::launch_pack(w, packed, rows, cols, (hipStream_t)stream), "kvd_pack_matrix launch");
+}
+
+namespace {
+
+// Block-forward workspace: q [B][T][n_q][hd], K and V [B][n_kv][T][hd], attention
+// heads [B][T][n_q hd], hhat [B][T][d], the MLP activation [B][T][d_ff] (bf16),
+// and a vector of ones (the staged operand of the unnormalised projections).
+struct BlockWs {
+  size_t q, k, v, heads, hhat, u, ones, end;
+};
+BlockWs block_ws(const kvd_attn_shape* s, int32_t d_ff, int32_t B, int32_t T) {
+  const size_t bt = (size_t)B * T, qd = (size_t)s->n_q_heads * s->head_dim;
+  BlockWs L{};
+  L.q = 0;
+  L.k = kvd::align_up(L.q + 2 * bt * qd, 256);
+  L.v = kvd::align_up(L.k + 2 * bt * s->n_kv_heads * s->head_dim, 256);
+  L.heads = kvd::align_up(L.v + 2 * bt * s->n_kv_heads * s->head_dim, 256);
+  L.hhat = kvd::align_up(L.heads + 2 * bt * qd, 256);
+  L.u = kvd::align_up(L.hhat + 2 * bt * s->d_model, 256);
+  L.ones = kvd::align_up(L.u + 2 * bt * d_ff, 256);
+  L.end = kvd::align_up(L.ones + 2 * (size_t)std::max<int64_t>((int64_t)qd, d_ff), 256);
+  return L;
+}
+
+kvd_status check_block(const kvd_attn_shape* shape, int32_t d_ff, int32_t B, int32_t T) {
+  KVD_TRY(check_shape(shape));
+  KVD_TRY(check_batch(B));
+  if (shape->dtype != KVD_BF16) return fail(KVD_ERR_UNSUPPORTED, "the block forward runs in bf16");
+  if (shape->head_dim != 128 && shape->head_dim != 256)
+    return fail(KVD_ERR_UNSUPPORTED, "the block forward supports head_dim 128 and 256 (got %d)", shape->head_dim);
+  if (shape->d_model % 512 != 0)
+    return fail(KVD_ERR_UNSUPPORTED, "the block forward needs d_model %% 512 == 0 (got %d)", shape->d_model);
+  if (d_ff < 256 || d_ff % 256 != 0) return fail(KVD_ERR_SHAPE, "d_ff=%d must be a positive multiple of 256", d_ff);
+  if ((shape->n_q_heads * shape->head_dim) % kvd::kKT != 0)
+    return fail(KVD_ERR_UNSUPPORTED, "n_q_heads * head_dim must be a multiple of %d", kvd::kKT);
+  if (T < 0) return fail(KVD_ERR_SHAPE, "T=%d must be >= 0", T);
+  if ((int64_t)B * T > INT32_MAX / 2) return fail(KVD_ERR_SHAPE, "B * T = %lld is too large", (long long)B * T);
+  KVD_TRY(check_lds_bytes(recompute_lds(shape), "kvd_block_forward (projections)"));
+  KVD_TRY(check_lds_bytes(kvd::gemm_lds_bytes(std::max(d_ff, shape->n_q_heads * shape->head_dim)),
+                          "kvd_block_forward (output projections)"));
+  KVD_TRY(check_lds_bytes(kvd::prefill_lds_bytes(shape->head_dim), "kvd_block_forward (attention)"));
+  return KVD_OK;
+}
+
+}  // namespace
+
+size_t kvd_block_workspace_bytes(const kvd_attn_shape* shape, int32_t d_ff, int32_t B, int32_t T) {
+  if (check_block(shape, d_ff, B, T) != KVD_OK) return 0;
+  return block_ws(shape, d_ff, B, T).end;
+}
+
+kvd_status kvd_block_forward(const kvd_attn_shape* shape, const kvd_block_weights* w, const void* h_in, void* h_out,
+                             const int32_t* pos0, int32_t B, int32_t T, void* ws, size_t ws_bytes, void* stream) {
+  if (w == nullptr) return fail(KVD_ERR_NULL, "w is NULL");
+  KVD_TRY(check_block(shape, w->d_ff, B, T));
+  if (B == 0 || T == 0) return KVD_OK;
+  KVD_TRY(check_ptr(h_in, "h_in"));
+  KVD_TRY(check_ptr(h_out, "h_out"));
+  const void* mats[] = {w->gamma_attn, w->w_q, w->w_k, w->w_v, w->w_o, w->gamma_mlp, w->w_gate, w->w_up, w->w_down};
+  const char* names[] = {"gamma_attn", "w_q", "w_k", "w_v", "w_o", "gamma_mlp", "w_gate", "w_up", "w_down"};
+  for (int i = 0; i < 9; ++i) KVD_TRY(check_ptr(mats[i], names[i]));
+  if (pos0 == nullptr) return fail(KVD_ERR_NULL, "pos0 is NULL");
+  const size_t hbytes = (size_t)B * T * shape->d_model * 2;
+  {
+    const char* a = static_cast<const char*>(h_in);
+    const char* b = static_cast<const char*>(h_out);
+    if (a < b + hbytes && b < a + hbytes) return fail(KVD_ERR_SHAPE, "h_out must not overlap h_in");
+  }
+  const BlockWs L = block_ws(shape, w->d_ff, B, T);
+  if (ws == nullptr) return fail(KVD_ERR_WORKSPACE, "workspace is NULL (%zu bytes needed)", L.end);
+  if ((reinterpret_cast<uintptr_t>(ws) & 255u) != 0) return fail(KVD_ERR_ALIGN, "workspace is not 256-byte aligned");
+  if (ws_bytes < L.end) return fail(KVD_ERR_WORKSPACE, "workspace holds %zu bytes, %zu needed", ws_bytes, L.end);
+  char* base = static_cast<char*>(ws);
+  const hipStream_t st = (hipStream_t)stream;
+  const int packed = shape->w_layout == KVD_W_PACKED;
+  const int qd = shape->n_q_heads * shape->head_dim;
+  hipError_t e = kvd::launch_fill_ones_bf16(base + L.ones, std::max(qd, w->d_ff), st);
+  if (e != hipSuccess) return device_status(e, "kvd_block_forward launch");
+  // RMSNorm + Q, K, V of every position (Eqs. q_proj .. v_proj)
+  kvd::ProjArgs p{};
+  p.h = h_in;
+  p.gamma = w->gamma_attn;
+  p.w_q = w->w_q;
+  p.w_k = w->w_k;
+  p.w_v = w->w_v;
+  p.pos0 = pos0;
+  p.k_out = base + L.k;
+  p.v_out = base + L.v;
+  p.q_out = base + L.q;
+  p.h_ld = T;
+  p.kv_t_cap = T;
+  p.kv_t_off = 0;
+  p.d = shape->d_model;
+  p.n_q = shape->n_q_heads;
+  p.n_kv = shape->n_kv_heads;
+  p.B = B;
+  p.T = T;
+  p.n_kv_units = shape->n_kv_heads;
+  p.eps = shape->rms_eps;
+  fill_rev(shape, p.rev);
+  e = kvd::launch_proj(p, 1, shape->head_dim, packed, p.n_kv_units + (shape->n_q_heads + 1) / 2, st);
+  if (e != hipSuccess) return device_status(e, "kvd_block_forward launch");
+  // causal attention (Eqs. attn_weights / head_output)
+  kvd::PrefillArgs at{};
+  at.q = base + L.q;
+  at.k = base + L.k;
+  at.v = base + L.v;
+  at.out = base + L.heads;
+  at.B = B;
+  at.T = T;
+  at.n_q = shape->n_q_heads;
+  at.n_kv = shape->n_kv_heads;
+  e = kvd::launch_prefill_attn(at, shape->head_dim, st);
+  if (e != hipSuccess) return device_status(e, "kvd_block_forward launch");
+  // hhat = h + heads W_o (Eq. attn_sublayer)
+  kvd::GemmArgs g{};
+  g.x = base + L.heads;
+  g.gamma = base + L.ones;
+  g.w = w->w_o;
+  g.res = h_in;
+  g.out = base + L.hhat;
+  g.M = B * T;
+  g.K = qd;
+  g.N = shape->d_model;
+  g.norm = 0;
+  g.eps = shape->rms_eps;
+  e = kvd::launch_gemm(g, kvd::kEpiResidual, packed, st);
+  if (e != hipSuccess) return device_status(e, "kvd_block_forward launch");
+  // u = SiLU(xbar W_gate) * (xbar W_up), xbar = RMSNorm(hhat; gamma_mlp)
+  g = kvd::GemmArgs{};
+  g.x = base + L.hhat;
+  g.gamma = w->gamma_mlp;
+  g.w = w->w_gate;
+  g.w2 = w->w_up;
+  g.out = base + L.u;
+  g.M = B * T;
+  g.K = shape->d_model;
+  g.N = w->d_ff;
+  g.norm = 1;
+  g.eps = shape->rms_eps;
+  e = kvd::launch_gemm(g, kvd::kEpiSwiglu, packed, st);
+  if (e != hipSuccess) return device_status(e, "kvd_block_forward launch");
+  // h_out = hhat + u W_down (Eq. mlp_sublayer)
+  g = kvd::GemmArgs{};
+  g.x = base + L.u;
+  g.gamma = base + L.ones;
+  g.w = w->w_down;
+  g.res = base + L.hhat;
+  g.out = h_out;
+  g.M = B * T;
+  g.K = w->d_ff;
+  g.N = shape->d_model;
+  g.norm = 0;
+  g.eps = shape->rms_eps;
+  return device_status(kvd::launch_gemm(g, kvd::kEpiResidual, packed, st), "kvd_block_forward launch");
+}
+
 kvd_status kvd_pack_weights(const kvd_attn_shape* shape, const void* w, int32_t rows, void* packed, void* stream) {
   if (shape == nullptr) return fail(KVD_ERR_NULL, "shape is NULL");
   kvd_attn_shape s = *shape;

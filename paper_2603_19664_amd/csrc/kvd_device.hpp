@@ -239,6 +239,58 @@ struct MfmaTile {
   static __device__ __forceinline__ void run(const uint16_t* const (&hrow)[CPT], const bool (&valid)[CPT], const uint16_t* gam,
                              const uint16_t* gam_g, int d, float eps, const Half (&halves)[2], uint16_t* hst,
                              float* rinv, const int* pos, const double* rev, uint16_t* kv, const Setup& setup) {
+    run_with(hrow, valid, gam, gam_g, d, eps, halves, hst, rinv, setup,
+             [&](const f32x16_t (&acc)[NB_F][NB_T], const bool (&wok)[NB_F]) {
+               store_kv(acc, wok, halves, rinv, pos, rev, kv);
+             });
+  }
+
+  // Epilogue of run(): row scale, RoPE on rotated halves, one RNE rounding, LDS tile.
+  static __device__ __forceinline__ void store_kv(const f32x16_t (&acc)[NB_F][NB_T], const bool (&wok)[NB_F],
+                                                  const Half (&halves)[2], const float* rinv, const int* pos,
+                                                  const double* rev, uint16_t* kv) {
+    const int lane = threadIdx.x & 63, wave = wave_id();
+    const int fw = wave % WF, tw = wave / WF;
+#pragma unroll
+    for (int bt = 0; bt < NB_T; ++bt) {
+      const int tok = tw * TOK_W + 32 * bt + (lane & 31);
+      const float ri = rinv[tok];
+      const int p = pos[tok];
+#pragma unroll
+      for (int bf = 0; bf < NB_F; ++bf) {
+        int half, row0;
+        block_rows(fw, bf, half, row0);
+        float v[16];
+#pragma unroll
+        for (int r = 0; r < 16; ++r) v[r] = wok[bf] ? acc[bf][bt][r] * ri : 0.0f;
+        if (half ? halves[1].rope : halves[0].rope) {
+#pragma unroll
+          for (int r = 0; r < 16; r += 2) {
+            const int f = row0 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+            rope_rotate(v[r], v[r + 1], p, rev[f >> 1]);
+          }
+        }
+#pragma unroll
+        for (int g4 = 0; g4 < 4; ++g4) {
+          const int col = half * HD + row0 + 8 * g4 + 4 * (lane >> 5);
+          uint2 o;
+          o.x = pack_bf16x2(v[4 * g4 + 0], v[4 * g4 + 1]);
+          o.y = pack_bf16x2(v[4 * g4 + 2], v[4 * g4 + 3]);
+          *reinterpret_cast<uint2*>(kv + (size_t)tok * KLD + col) = o;
+        }
+      }
+    }
+  }
+
+  // The K-loop and the tokens' 1/rms (in rinv), then epi(acc, wok) with the
+  // fp32 accumulators: acc[bf][bt][r] is feature row0(bf) + 8 (r / 4) +
+  // 4 (lane / 32) + r % 4 of half(bf) (block_rows) for token tw TOK_W + 32 bt +
+  // lane % 32, wok[bf] whether that half's weights are present.
+  template <class Setup, class Epi>
+  static __device__ __forceinline__ void run_with(const uint16_t* const (&hrow)[CPT], const bool (&valid)[CPT],
+                                                  const uint16_t* gam, const uint16_t* gam_g, int d, float eps,
+                                                  const Half (&halves)[2], uint16_t* hst, float* rinv,
+                                                  const Setup& setup, const Epi& epi) {
     const int tid = threadIdx.x, lane = tid & 63, sub = tid & 7;
     const int wave = wave_id();
     const int fw = wave % WF, tw = wave / WF;
@@ -402,36 +454,7 @@ struct MfmaTile {
     finish_rms<NT, CPT>(ss, valid, d, eps, rinv);
     __syncthreads();
 
-    // epilogue: row scale, RoPE on rotated halves, one RNE rounding, LDS tile.
-#pragma unroll
-    for (int bt = 0; bt < NB_T; ++bt) {
-      const int tok = tw * TOK_W + 32 * bt + (lane & 31);
-      const float ri = rinv[tok];
-      const int p = pos[tok];
-#pragma unroll
-      for (int bf = 0; bf < NB_F; ++bf) {
-        int half, row0;
-        block_rows(fw, bf, half, row0);
-        float v[16];
-#pragma unroll
-        for (int r = 0; r < 16; ++r) v[r] = wok[bf] ? acc[bf][bt][r] * ri : 0.0f;
-        if (half ? halves[1].rope : halves[0].rope) {
-#pragma unroll
-          for (int r = 0; r < 16; r += 2) {
-            const int f = row0 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-            rope_rotate(v[r], v[r + 1], p, rev[f >> 1]);
-          }
-        }
-#pragma unroll
-        for (int g4 = 0; g4 < 4; ++g4) {
-          const int col = half * HD + row0 + 8 * g4 + 4 * (lane >> 5);
-          uint2 o;
-          o.x = pack_bf16x2(v[4 * g4 + 0], v[4 * g4 + 1]);
-          o.y = pack_bf16x2(v[4 * g4 + 2], v[4 * g4 + 3]);
-          *reinterpret_cast<uint2*>(kv + (size_t)tok * KLD + col) = o;
-        }
-      }
-    }
+    epi(acc, wok);
   }
 };
 

@@ -111,7 +111,7 @@ __global__ __launch_bounds__(kNtTile, 1) void proj_kernel(ProjArgs a, int per_xc
       T* base = static_cast<T*>(half ? a.v_out : a.k_out);
       dst = base + (((size_t)b * a.n_kv + head) * a.kv_t_cap + a.kv_t_off + t) * HD;
     } else {
-      dst = static_cast<T*>(a.q_out) + ((size_t)b * a.n_q + head) * HD;
+      dst = static_cast<T*>(a.q_out) + (((size_t)b * a.T + t) * a.n_q + head) * HD;  // [B][T][n_q][hd]
     }
     *reinterpret_cast<uint4*>(dst + ch * CH) =
         *reinterpret_cast<const uint4*>(kv + (size_t)row * KLD + half * HD + ch * CH);

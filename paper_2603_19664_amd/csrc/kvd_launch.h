@@ -21,7 +21,7 @@ struct ProjArgs {
   const int32_t* pos0;
   void* k_out;
   void* v_out;
-  void* q_out;
+  void* q_out;  // [B][T][n_q][hd] (q units)
   long long h_ld;
   int kv_t_cap, kv_t_off;
   int d, n_q, n_kv, B, T, n_kv_units;
@@ -69,6 +69,45 @@ struct AttnArgs {
   unsigned long long* ws_done;
   int B, T, n_q, n_kv, S;
 };
+
+// Block-forward projection on the tile engine (bf16): out = epilogue(x W^T) for
+// the M = B * T token rows of x [M][K], 512 output features per workgroup.
+//   kEpiResidual: out[m][n] = res[m][n] + (x W^T)[m][n], W [N][K] (N % 512 == 0);
+//   kEpiSwiglu:   out[m][f] = SiLU(g) * u with g = (xbar W^T)[m][f], u = (xbar W2^T)[m][f],
+//                 W, W2 [N][K] (N % 256 == 0), xbar = RMSNorm(x; gamma).
+// norm: the activation rows are RMS-normalised with gamma (1/rms on the
+// accumulators, gamma on the staged operand); otherwise gamma is a vector of ones.
+enum { kEpiResidual = 0, kEpiSwiglu = 1 };
+struct GemmArgs {
+  const void* x;
+  const void* gamma;
+  const void* w;
+  const void* w2;
+  const void* res;
+  void* out;
+  int M, K, N;
+  int norm;
+  float eps;
+};
+hipError_t launch_gemm(const GemmArgs& a, int epi, int packed, hipStream_t st);
+
+// Causal prefill attention (bf16): out[b][t][h*hd .. h*hd+hd-1] = sum over keys
+// j <= t of softmax_j(q[b][t][h] . K[b][h/g][j] / sqrt(hd)) V[b][h/g][j].
+//   q [B][T][n_q][hd]; K, V [B][n_kv][T][hd]; out [B][T][n_q * hd].
+struct PrefillArgs {
+  const void* q;
+  const void* k;
+  const void* v;
+  void* out;
+  int B, T, n_q, n_kv;
+};
+hipError_t launch_prefill_attn(const PrefillArgs& a, int hd, hipStream_t st);
+
+// dst[i] = 1.0 (bf16) for i < n.
+hipError_t launch_fill_ones_bf16(void* dst, int n, hipStream_t st);
+// LDS bytes of the two block-forward kernels (for host-side validation).
+size_t gemm_lds_bytes(int K);
+size_t prefill_lds_bytes(int hd);
 
 hipError_t launch_proj(const ProjArgs& a, int dtype_bf16, int hd, int packed, int n_units, hipStream_t st);
 // Current-token projection (T == 1): the streaming kernel for bf16, proj_kernel for fp32.

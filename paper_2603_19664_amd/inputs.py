@@ -14,6 +14,7 @@ import torch
 
 # tensor ids (part of the seed)
 T_H, T_HNEW, T_GAMMA, T_WQ, T_WK, T_WV, T_POS, T_SCALE = range(8)
+T_WO, T_GAMMA_MLP, T_WGATE, T_WUP, T_WDOWN = range(8, 13)
 
 _DT = {"f32": torch.float32, "bf16": torch.bfloat16}
 
@@ -67,6 +68,22 @@ def weights(wl, layer: int, seed: int = 0, device="cpu", w_std=None):
     w_k = normal((wl.n_kv * hd, d), wl.w_std, device, *ids, T_WK).to(dt)
     w_v = normal((wl.n_kv * hd, d), wl.w_std, device, *ids, T_WV).to(dt)
     return gamma, w_q, w_k, w_v
+
+
+def block_weights(wl, layer: int, d_ff: int, seed: int = 0, device="cpu", w_std=None):
+    """The rest of a transformer block's parameters: W_o [d, n_q*hd], gamma_mlp [d],
+    W_gate / W_up [d_ff, d], W_down [d, d_ff], in the workload dtype (N(0, w_std^2);
+    gamma 1 + N(0, gamma_std^2))."""
+    dt = _DT[wl.dtype]
+    d, qd = wl.d_model, wl.n_q * wl.head_dim
+    std = wl.w_std if w_std is None else w_std
+    ids = (seed, wl.cfg_id, layer)
+    w_o = normal((d, qd), std, device, *ids, T_WO).to(dt)
+    gamma_mlp = normal((d,), wl.gamma_std, device, *ids, T_GAMMA_MLP, mean=1.0).to(dt)
+    w_gate = normal((d_ff, d), std, device, *ids, T_WGATE).to(dt)
+    w_up = normal((d_ff, d), std, device, *ids, T_WUP).to(dt)
+    w_down = normal((d, d_ff), std, device, *ids, T_WDOWN).to(dt)
+    return w_o, gamma_mlp, w_gate, w_up, w_down
 
 
 def residuals(wl, layer: int, B: int, T: int, seed: int = 0, device="cpu", t_cap=None):

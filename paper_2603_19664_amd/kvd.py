@@ -51,6 +51,11 @@ class KvView(ctypes.Structure):
     _fields_ = [("k", ctypes.c_void_p), ("v", ctypes.c_void_p), ("t_cap", ctypes.c_int32), ("t_off", ctypes.c_int32)]
 
 
+class BlockWeights(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in ("gamma_attn", "w_q", "w_k", "w_v", "w_o", "gamma_mlp", "w_gate",
+                                               "w_up", "w_down")] + [("d_ff", ctypes.c_int32)]
+
+
 def _load() -> ctypes.CDLL:
     if not os.path.exists(LIB_PATH):
         raise ImportError(f"{LIB_PATH} is not built; run `python -m paper_2603_19664_amd.build` "
@@ -72,6 +77,12 @@ def _load() -> ctypes.CDLL:
         f.restype = ctypes.c_int
     lib.kvd_pack_weights.argtypes = [S, VP, I32, VP, VP]
     lib.kvd_pack_weights.restype = ctypes.c_int
+    lib.kvd_pack_matrix.argtypes = [VP, I32, I32, VP, VP]
+    lib.kvd_pack_matrix.restype = ctypes.c_int
+    lib.kvd_block_forward.argtypes = [S, P(BlockWeights), VP, VP, VP, I32, I32, VP, SZ, VP]
+    lib.kvd_block_forward.restype = ctypes.c_int
+    lib.kvd_block_workspace_bytes.argtypes = [S, I32, I32, I32]
+    lib.kvd_block_workspace_bytes.restype = SZ
     lib.kvd_combine.argtypes = [S, I32, I32, VP, SZ, VP, VP]
     lib.kvd_combine.restype = ctypes.c_int
     lib.kvd_workspace_bytes.argtypes = [S, I32, I32, I32, I32]
@@ -268,3 +279,31 @@ def kvd_fused_window_attn(shape: Shape, q, h, T_rec: int, gamma, w_k, w_v, windo
         ctypes.byref(tail) if tail is not None else None, T_tail, window,
         _ptr(out, "out", dt, 3) if out is not None else None, _ptr(ws, "ws"), ws.numel() * ws.element_size(),
         _stream()))
+
+
+def kvd_pack_matrix(w):
+    """A packed copy (MFMA operand order) of a row-major [rows, cols] bf16 matrix."""
+    out = torch.empty_like(w)
+    _check(lib.kvd_pack_matrix(_ptr(w, "w", torch.bfloat16, 2), w.shape[0], w.shape[1],
+                               _ptr(out, "packed", torch.bfloat16, 2), _stream()))
+    return out
+
+
+def kvd_block_workspace_bytes(shape: Shape, d_ff: int, B: int, T: int) -> int:
+    return lib.kvd_block_workspace_bytes(ctypes.byref(shape.c()), d_ff, B, T)
+
+
+def block_weights(gamma_attn, w_q, w_k, w_v, w_o, gamma_mlp, w_gate, w_up, w_down) -> BlockWeights:
+    """The kvd_block_weights of one block (device bf16 tensors, kept alive by the caller)."""
+    ts = (gamma_attn, w_q, w_k, w_v, w_o, gamma_mlp, w_gate, w_up, w_down)
+    names = ("gamma_attn", "w_q", "w_k", "w_v", "w_o", "gamma_mlp", "w_gate", "w_up", "w_down")
+    ptrs = [_ptr(t, n, torch.bfloat16) for t, n in zip(ts, names)]
+    return BlockWeights(*ptrs, w_gate.shape[0])
+
+
+def kvd_block_forward(shape: Shape, weights: BlockWeights, h_in, h_out, pos0, ws):
+    """h_out [B, T, d] = one pre-norm transformer block over every position of h_in [B, T, d]."""
+    B, T = h_in.shape[0], h_in.shape[1]
+    _check(lib.kvd_block_forward(ctypes.byref(shape.c()), ctypes.byref(weights), _ptr(h_in, "h_in", torch.bfloat16, 3),
+                                 _ptr(h_out, "h_out", torch.bfloat16, 3), _ptr(pos0, "pos0", torch.int32), B, T,
+                                 _ptr(ws, "ws"), ws.numel() * ws.element_size(), _stream()))

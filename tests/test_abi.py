@@ -24,7 +24,7 @@ def view(t_cap=16, t_off=0, k=FAKE, v=FAKE):
 
 
 def test_loads_and_version():
-    assert kvd.abi_version() == 6
+    assert kvd.abi_version() == 7
     assert kvd.status_str(kvd.KVD_ERR_ALIGN) == "KVD_ERR_ALIGN"
 
 
@@ -209,3 +209,41 @@ def test_weight_layout_validation():
     assert f(ctypes.byref(s), FAKE, 64, FAKE + 4096, None) == kvd.KVD_ERR_SHAPE            # overlap
     assert f(ctypes.byref(s), None, 64, FAKE, None) == kvd.KVD_ERR_NULL
     assert f(ctypes.byref(shape(dtype=kvd.KVD_F32)), FAKE, 64, FAKE + (1 << 24), None) == kvd.KVD_ERR_UNSUPPORTED
+
+
+def block_call(s, h_in=FAKE, h_out=FAKE + (1 << 24), pos=FAKE, B=1, T=64, d_ff=1024, ws_bytes=1 << 30, nullw=None):
+    ptrs = [FAKE] * 9
+    if nullw is not None:
+        ptrs[nullw] = None
+    w = kvd.BlockWeights(*ptrs, d_ff)
+    return lib.kvd_block_forward(ctypes.byref(s), ctypes.byref(w), h_in, h_out, pos, B, T, FAKE, ws_bytes, None)
+
+
+def test_block_forward_validation():
+    s = shape(d_model=1024, n_q_heads=8, n_kv_heads=4, head_dim=128)
+    assert block_call(shape(d_model=1024, n_q_heads=8, n_kv_heads=4, head_dim=128, dtype=kvd.KVD_F32)) == \
+        kvd.KVD_ERR_UNSUPPORTED
+    assert block_call(shape(d_model=1024, n_q_heads=8, n_kv_heads=4, head_dim=64)) == kvd.KVD_ERR_UNSUPPORTED
+    assert block_call(shape(d_model=768, n_q_heads=8, n_kv_heads=4, head_dim=128)) == kvd.KVD_ERR_UNSUPPORTED
+    assert block_call(s, d_ff=100) == kvd.KVD_ERR_SHAPE
+    assert block_call(s, T=-1) == kvd.KVD_ERR_SHAPE
+    assert block_call(s, h_in=None) == kvd.KVD_ERR_NULL
+    assert block_call(s, pos=None) == kvd.KVD_ERR_NULL
+    for i in range(9):
+        assert block_call(s, nullw=i) == kvd.KVD_ERR_NULL
+    assert block_call(s, h_out=FAKE) == kvd.KVD_ERR_SHAPE          # aliasing
+    assert block_call(s, ws_bytes=100) == kvd.KVD_ERR_WORKSPACE
+    assert lib.kvd_block_forward(ctypes.byref(s), None, FAKE, FAKE, FAKE, 1, 1, FAKE, 1 << 30, None) == kvd.KVD_ERR_NULL
+    n = lib.kvd_block_workspace_bytes(ctypes.byref(s), 1024, 2, 100)
+    qd, kvd_ = 8 * 128, 4 * 128
+    parts = [2 * 200 * qd, 2 * 200 * kvd_, 2 * 200 * kvd_, 2 * 200 * qd, 2 * 200 * 1024, 2 * 200 * 1024, 2 * 1024]
+    assert n == sum(-(-p // 256) * 256 for p in parts)
+    assert lib.kvd_block_workspace_bytes(ctypes.byref(s), 100, 2, 100) == 0
+
+
+def test_pack_matrix_validation():
+    f = lib.kvd_pack_matrix
+    assert f(FAKE, 33, 64, FAKE + (1 << 24), None) == kvd.KVD_ERR_SHAPE
+    assert f(FAKE, 64, 24, FAKE + (1 << 24), None) == kvd.KVD_ERR_SHAPE
+    assert f(None, 64, 64, FAKE, None) == kvd.KVD_ERR_NULL
+    assert f(FAKE, 64, 64, FAKE + 64, None) == kvd.KVD_ERR_SHAPE     # overlap

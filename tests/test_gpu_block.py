@@ -1,0 +1,154 @@
+"""GPU parity of the single-checkpoint scheme (Eq. res_mem): kvd_block_forward
+runs one pre-norm transformer block over every position (Sec. 3.1, Eqs. q_proj
+.. mlp_sublayer), and chaining it recomputes h^(l) from the one stored residual
+h^(0).  Checked against the fp64 oracle's block_forward / recompute_residual on
+the same bf16 values, both on h_out and on what the block adds to the residual
+stream (h_out - h_in), and bit for bit between packed and row-major weights.
+
+Tolerance (max |gpu - oracle| / max |oracle| per tensor): 2e-2 (bf16) on h_out.
+What a block adds to the residual stream is compared with 2e-2 plus the two
+bf16 roundings (unit roundoff u = 2^-8) each block makes at the residual's own
+scale (hhat and h_out are stored in bf16): 2 L u max|h| / max|h_out - h_in| for
+L blocks."""
+import dataclasses
+
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+from paper_2603_19664_amd import configs as C
+from paper_2603_19664_amd import inputs, kvd
+
+from gpu_cases import err, f64, note
+
+pytestmark = pytest.mark.gpu
+
+TOL = 2e-2
+
+
+@pytest.fixture(autouse=True)
+def _announce(request):
+    note(f"[gpu] {request.node.nodeid}")
+    yield
+    torch.cuda.synchronize()
+
+
+U = 2.0 ** -8
+
+
+def _delta_tol(h_in, ref, n_layers):
+    return TOL + 2 * n_layers * U * float(np.max(np.abs(f64(h_in)))) / float(np.max(np.abs(ref - f64(h_in))))
+
+
+def _check(name, x, ref, tol=TOL):
+    e = err(x, ref)
+    note(f"    {name}: err {e:.3e} (tol {tol:g})")
+    assert e < tol, f"{name}: err {e:.3e} >= {tol:g}"
+
+
+class Model:
+    """Seeded weights of n_layers blocks (row-major for the oracle, and as the library gets them)."""
+
+    def __init__(self, wl, n_layers, d_ff, packed, seed=0):
+        self.wl, self.d_ff = wl, d_ff
+        self.shape = kvd.shape_of(wl)
+        if packed:
+            self.shape = self.shape.packed()
+        self.rows, self.lib, self.wts = [], [], []
+        for l in range(n_layers):
+            gamma, w_q, w_k, w_v = inputs.weights(wl, l, seed, "cuda")
+            w_o, gamma_mlp, w_gate, w_up, w_down = inputs.block_weights(wl, l, d_ff, seed, "cuda")
+            rm = (gamma, w_q, w_k, w_v, w_o, gamma_mlp, w_gate, w_up, w_down)
+            self.rows.append(rm)
+            if packed:
+                pw = lambda w: kvd.kvd_pack_weights(self.shape, w)  # noqa: E731
+                lw = (gamma, pw(w_q), pw(w_k), pw(w_v), kvd.kvd_pack_matrix(w_o), gamma_mlp, pw(w_gate), pw(w_up),
+                      kvd.kvd_pack_matrix(w_down))
+            else:
+                lw = rm
+            self.lib.append(lw)
+            self.wts.append(kvd.block_weights(*lw))
+
+    def oracle_layers(self):
+        return [tuple(f64(t) for t in rm) for rm in self.rows]
+
+    def forward(self, h, pos0, n_layers):
+        B, T = h.shape[0], h.shape[1]
+        ws = torch.empty(kvd.kvd_block_workspace_bytes(self.shape, self.d_ff, B, T), dtype=torch.uint8,
+                         device="cuda")
+        x = h
+        for l in range(n_layers):
+            y = torch.empty_like(x)
+            kvd.kvd_block_forward(self.shape, self.wts[l], x, y, pos0, ws)
+            x = y
+        return x
+
+
+def _wl(hd):
+    # d_model 512 (a multiple of the 512-row output tile), heads of 128 or 256; unit
+    # residual scale, so that what a block adds is not small next to the stream
+    if hd == 128:
+        return dataclasses.replace(C.GEMMA3_4B, d_model=512, n_q=8, n_kv=4, head_dim=128, layer_scale=(1.0, 1.0))
+    return dataclasses.replace(C.GEMMA3_4B, d_model=512, n_q=4, n_kv=2, head_dim=256, layer_scale=(1.0, 1.0))
+
+
+def _inputs(wl, B, T, seed):
+    h, _ = inputs.residuals(wl, 0, B, T, seed, "cuda")
+    pos0 = torch.tensor([3, 100][:B], dtype=torch.int32, device="cuda")
+    return h.contiguous(), pos0
+
+
+def _oracle(M, h, pos0, n_layers):
+    s = M.shape
+    T = h.shape[1]
+    pos = f64(pos0)[:, None] + np.arange(T)[None, :]
+    return O.recompute_residual(f64(h), pos, M.oracle_layers(), n_layers, s.n_q_heads, s.n_kv_heads, s.head_dim,
+                                s.rms_eps, s.rope_theta)
+
+
+@pytest.mark.parametrize("hd", [128, 256])
+@pytest.mark.parametrize("T", [1, 63, 64, 130])
+def test_block_forward_vs_oracle(hd, T):
+    wl = _wl(hd)
+    M = Model(wl, 1, d_ff=1024, packed=True, seed=hd + T)
+    h, pos0 = _inputs(wl, 2, T, seed=T)
+    out = M.forward(h, pos0, 1)
+    ref = _oracle(M, h, pos0, 1)
+    _check("h_out", f64(out), ref)
+    _check("h_out - h_in (what the block adds)", f64(out) - f64(h), ref - f64(h), _delta_tol(h, ref, 1))
+    assert torch.isfinite(out.float()).all()
+
+
+def test_single_checkpoint_recompute_three_layers():
+    # h^(3) from h^(0): three blocks in a row (the residual stream recomputed from one checkpoint)
+    wl = _wl(256)
+    M = Model(wl, 3, d_ff=1024, packed=True, seed=11)
+    h, pos0 = _inputs(wl, 2, 96, seed=12)
+    out = M.forward(h, pos0, 3)
+    ref = _oracle(M, h, pos0, 3)
+    _check("h^(3)", f64(out), ref)
+    _check("h^(3) - h^(0)", f64(out) - f64(h), ref - f64(h), _delta_tol(h, ref, 3))
+
+
+def test_packed_and_rowmajor_weights_bitwise_equal():
+    wl = _wl(128)
+    Mp = Model(wl, 1, d_ff=512, packed=True, seed=21)
+    Mr = Model(wl, 1, d_ff=512, packed=False, seed=21)
+    h, pos0 = _inputs(wl, 2, 77, seed=22)
+    a, b = Mp.forward(h, pos0, 1), Mr.forward(h, pos0, 1)
+    assert torch.equal(a.view(torch.int16), b.view(torch.int16))
+
+
+def test_block_causality_on_gpu():
+    # positions before t do not see rows after t: changing the last rows leaves the
+    # first rows' outputs bit-identical
+    wl = _wl(256)
+    M = Model(wl, 1, d_ff=512, packed=True, seed=31)
+    h, pos0 = _inputs(wl, 1, 150, seed=32)
+    a = M.forward(h, pos0, 1)
+    h2 = h.clone()
+    h2[:, 100:] = (h2[:, 100:].float() * -1.5).to(h.dtype)
+    b = M.forward(h2, pos0, 1)
+    assert torch.equal(a[:, :100].view(torch.int16), b[:, :100].view(torch.int16))
+    assert not torch.equal(a[:, 100:], b[:, 100:])
