@@ -50,6 +50,9 @@ def parse():
                    help="size of one untimed device-to-device copy whose HBM counters calibrate the traffic figure")
     p.add_argument("--next", action="store_true",
                    help="also measure the hybrid cache budget sweep and the recompute-vs-transfer sweep over evicted tokens")
+    p.add_argument("--only", choices=["single_checkpoint", "sliding_window"],
+                   help="run only this one of the --next measurements and print its JSON (no headline line; "
+                        "for profiling its kernels)")
     p.add_argument("--extra", action="store_true",
                    help="also measure the Qwen-1.5B-shaped step (28 layers, B=8, 16384 ctx; fused vs cached) and "
                         "the multi-turn conversation (Gemma 3-4B shape, B=16, a decode step at each of 20 turn "
@@ -98,6 +101,11 @@ def main():
     from paper_2603_19664_amd import kvd
 
     torch.cuda.set_device(0)
+    if args.only:
+        fn = {"single_checkpoint": lambda: run_single_checkpoint(torch, np, kvd, configs, inputs, log),
+              "sliding_window": lambda: run_sliding(torch, kvd, configs, inputs, log)}[args.only]
+        print(json.dumps({args.only: fn()}), flush=True)
+        return
     dev = "cuda"
     wl = configs.GEMMA3_4B
     s = kvd.shape_of(wl).packed()   # weights in the packed MFMA layout (packed once, outside the step)
@@ -489,7 +497,68 @@ def run_next(args, torch, np, kvd, configs, inputs, op_time, log):
     del h, Kc, Vc, kv_dev, kv_host, flush_buf
     torch.cuda.empty_cache()
     res["sliding_window"] = run_sliding(torch, kvd, configs, inputs, log)
+    res["single_checkpoint"] = run_single_checkpoint(torch, np, kvd, configs, inputs, log)
     return res
+
+
+def block_flops(B, T, d, n_q, n_kv, hd, d_ff):
+    """Algorithmic flops of one pre-norm block over B sequences of T positions: the
+    Q/K/V, W_o and MLP products plus causal attention (scores and weighted sum over
+    t + 1 keys at position t)."""
+    proj = 2 * B * T * d * (n_q + 2 * n_kv) * hd + 2 * B * T * n_q * hd * d + 2 * B * T * 3 * d * d_ff
+    attn = 4 * B * n_q * hd * (T * (T + 1) // 2)
+    return proj + attn
+
+
+def run_single_checkpoint(torch, np, kvd, configs, inputs, log, d_ff=10240, n_distinct=4):
+    """The single-checkpoint scheme (one residual per token for all layers): recomputing
+    h^(l) means running blocks 0 .. l-1 over every position (kvd_block_forward).  A
+    Gemma-3-4B-shaped block (d 2560, 8 q / 4 KV heads of 256; d_ff 10240 is a stand-in,
+    the paper does not give the MLP width), B = 1, T = 1024 and 4096: one block's time,
+    and the 34 blocks that recompute every layer's residuals once (n_distinct layers of
+    weights cycled), HIP events around the calls."""
+    wl = configs.GEMMA3_4B
+    s = kvd.shape_of(wl).packed()
+    L, d, nq, nkv, hd = wl.layers, wl.d_model, wl.n_q, wl.n_kv, wl.head_dim
+    blocks = []
+    for l in range(n_distinct):
+        gamma, w_q, w_k, w_v = inputs.weights(wl, l, 0, "cuda")
+        w_o, gamma_mlp, w_gate, w_up, w_down = inputs.block_weights(wl, l, d_ff, 0, "cuda")
+        pw = lambda w: kvd.kvd_pack_weights(s, w)  # noqa: E731
+        lw = (gamma, pw(w_q), pw(w_k), pw(w_v), kvd.kvd_pack_matrix(w_o), gamma_mlp, pw(w_gate), pw(w_up),
+              kvd.kvd_pack_matrix(w_down))
+        del w_q, w_k, w_v, w_o, w_gate, w_up, w_down
+        blocks.append((lw, kvd.block_weights(*lw)))
+    rows = []
+    for T in (1024, 4096):
+        B = 1
+        log(f"[bench] next: single checkpoint, block forward T={T}")
+        h, _ = inputs.residuals(wl, 0, B, T, 0, "cuda")
+        h = h.contiguous()
+        bufs = [h, torch.empty_like(h)]
+        pos0 = torch.zeros((B,), dtype=torch.int32, device="cuda")
+        ws = torch.empty(kvd.kvd_block_workspace_bytes(s, d_ff, B, T), dtype=torch.uint8, device="cuda")
+        sc = s.c()
+        P = lambda t: ctypes.c_void_p(t.data_ptr())  # noqa: E731
+        st = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+        calls = [Call(kvd.lib.kvd_block_forward, ctypes.byref(sc), ctypes.byref(blocks[i % n_distinct][1]),
+                      P(bufs[i % 2]), P(bufs[(i + 1) % 2]), P(pos0), B, T, P(ws), ws.numel(), st)
+                 for i in range(L)]
+        one = _step_timer(torch, calls[0], steps=10, warmup=2)
+        # the recompute of all L layers' residuals: L blocks in a row (ping-pong buffers)
+        full = _step_timer(torch, lambda: [c() for c in calls], steps=3, warmup=1)
+        fl = block_flops(B, T, d, nq, nkv, hd, d_ff)
+        rows.append({"B": B, "T": T, "block_ms": one, "block_tflops": fl / (one * 1e-3) / 1e12,
+                     "all_layers_ms": full, "all_layers_tflops": L * fl / (full * 1e-3) / 1e12,
+                     "single_checkpoint_bytes": B * T * d * 2, "per_layer_checkpoint_bytes": L * B * T * d * 2,
+                     "kv_cache_bytes": L * B * T * 2 * nkv * hd * 2})
+        log(f"[bench] next: single checkpoint T={T}: block {one:.3f} ms ({rows[-1]['block_tflops']:.0f} TFLOP/s), "
+            f"{L} blocks {full:.2f} ms")
+        del h, bufs, ws
+        torch.cuda.empty_cache()
+    del blocks
+    torch.cuda.empty_cache()
+    return {"workload": f"gemma3-4b-shaped block (d_ff {d_ff}), {L} layers, B=1", "rows": rows}
 
 
 def run_sliding(torch, kvd, configs, inputs, log, window=1024):

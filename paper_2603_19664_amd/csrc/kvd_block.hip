@@ -143,19 +143,26 @@ constexpr PrefillLds prefill_lds(int hd) {
   return L;
 }
 
-// grid (ceil(T / 64) query blocks, n_q, B), 256 threads (4 waves).  A workgroup
-// takes 64 query rows of one head through the key blocks 0 .. its own (flash
-// order: scores, running max / sum, rescaled accumulators).  Wave w computes the
-// 32 x 32 score block (query half w / 2, key half w % 2) with its query rows in
-// registers, and the output columns [w % 2 * hd / 2, + hd / 2) of query half w / 2.
-// Scores are in the log2 domain (log2(e) / sqrt(hd) folded into the scale).
+// grid: xcd_map(B * n_q * nqb) workgroups, nqb = ceil(T / 64), 256 threads (4
+// waves).  Items are ordered (sequence, KV head, query block from the last,
+// query head of the group), so an XCD's workgroups share one KV head's keys and
+// values in its L2 and the longest rows start first.  A workgroup takes 64 query
+// rows of one head through the key blocks 0 .. its own (flash order: scores,
+// running max / sum, rescaled accumulators), loading key block kb + 1 into
+// registers while block kb is computed.  Wave w computes the 32 x 32 score block
+// (query half w / 2, key half w % 2) with its query rows in registers, and the
+// output columns [w % 2 * hd / 2, + hd / 2) of query half w / 2.  Scores are in
+// the log2 domain (log2(e) / sqrt(hd) folded into the scale).
 template <int HD>
-__global__ __launch_bounds__(256) void prefill_attn_kernel(PrefillArgs a) {
+__global__ __launch_bounds__(256) void prefill_attn_kernel(PrefillArgs a, int per_xcd) {
   extern __shared__ __align__(16) char lds[];
   constexpr PrefillLds PL = prefill_lds(HD);
   constexpr int KS = HD / 16;   // 16-wide k-steps of a score block
   constexpr int DBW = HD / 64;  // 32-wide output column blocks per wave
   constexpr int KLDS = HD + 8, VLD = 64 + 8, SLD = 65, PLD = 64 + 8;
+  constexpr int CPR = HD / 8;              // 16-byte chunks per key row
+  constexpr int KCH = 64 * CPR / 256;      // key chunks per thread
+  constexpr int VGR = 16 * CPR / 256;      // value groups (4 keys x 8 columns) per thread
   uint16_t* Ks = reinterpret_cast<uint16_t*>(lds + PL.ks);
   uint16_t* Vt = reinterpret_cast<uint16_t*>(lds + PL.vt);
   float* Ss = reinterpret_cast<float*>(lds + PL.ss);
@@ -166,9 +173,15 @@ __global__ __launch_bounds__(256) void prefill_attn_kernel(PrefillArgs a) {
 
   const int tid = threadIdx.x, lane = tid & 63, w = wave_id();
   const int nqb = (a.T + 63) / 64;
-  const int qb = nqb - 1 - (int)blockIdx.x;  // the longest rows first
-  const int h = blockIdx.y, b = blockIdx.z;
-  const int j = h / (a.n_q / a.n_kv);
+  const int g = a.n_q / a.n_kv;
+  const long long item = (long long)(blockIdx.x % kXcds) * per_xcd + blockIdx.x / kXcds;
+  if (item >= (long long)a.B * a.n_q * nqb) return;
+  const int hh = (int)(item % g);
+  const long long r1 = item / g;
+  const int qb = nqb - 1 - (int)(r1 % nqb);  // the longest rows first
+  const long long r2 = r1 / nqb;
+  const int j = (int)(r2 % a.n_kv), b = (int)(r2 / a.n_kv);
+  const int h = j * g + hh;
   const int qi = w >> 1, kj = w & 1;
   const float scale = ScoreScale<HD>::v;
   const uint16_t* kbase = static_cast<const uint16_t*>(a.k) + ((size_t)b * a.n_kv + j) * a.T * HD;
@@ -192,64 +205,68 @@ __global__ __launch_bounds__(256) void prefill_attn_kernel(PrefillArgs a) {
 #pragma unroll
     for (int i = 0; i < 16; ++i) o[db][i] = 0.0f;
 
+  // key / value block kb into registers (rows clamped to T - 1: masked below)
+  u32x4_t kc[KCH], vc[VGR][4];
+  auto load_kv = [&](int kb) {
+#pragma unroll
+    for (int i = 0; i < KCH; ++i) {
+      const int c = tid + 256 * i, row = c / CPR, ch = c - row * CPR;
+      const int t = min(64 * kb + row, a.T - 1);
+      kc[i] = *reinterpret_cast<const u32x4_t*>(kbase + (size_t)t * HD + 8 * ch);
+    }
+#pragma unroll
+    for (int i = 0; i < VGR; ++i) {
+      const int gidx = tid + 256 * i, k4 = gidx & 15, ch = gidx >> 4;
+#pragma unroll
+      for (int kk = 0; kk < 4; ++kk) {
+        const int t = min(64 * kb + 4 * k4 + kk, a.T - 1);
+        vc[i][kk] = *reinterpret_cast<const u32x4_t*>(vbase + (size_t)t * HD + 8 * ch);
+      }
+    }
+  };
+  load_kv(0);
+
   for (int kb = 0; kb <= qb; ++kb) {
-    // K tile (rows clamped to T - 1: masked below) and V tile, transposed
-    {
-      constexpr int CPR = HD / 8;
-      u32x4_t kc[64 * CPR / 256];
+    // the registers into LDS: K as is, V transposed ([column][key])
 #pragma unroll
-      for (int i = 0; i < 64 * CPR / 256; ++i) {
-        const int c = tid + 256 * i, row = c / CPR, ch = c - row * CPR;
-        const int t = min(64 * kb + row, a.T - 1);
-        kc[i] = *reinterpret_cast<const u32x4_t*>(kbase + (size_t)t * HD + 8 * ch);
-      }
-      constexpr int VG = 16 * CPR;  // groups of 4 keys x 8 columns
-      u32x4_t vc[VG / 256][4];
+    for (int i = 0; i < KCH; ++i) {
+      const int c = tid + 256 * i, row = c / CPR, ch = c - row * CPR;
+      *reinterpret_cast<u32x4_t*>(Ks + row * KLDS + 8 * ch) = kc[i];
+    }
 #pragma unroll
-      for (int i = 0; i < VG / 256; ++i) {
-        const int gidx = tid + 256 * i, k4 = gidx & 15, ch = gidx >> 4;
+    for (int i = 0; i < VGR; ++i) {
+      const int gidx = tid + 256 * i, k4 = gidx & 15, ch = gidx >> 4;
 #pragma unroll
-        for (int kk = 0; kk < 4; ++kk) {
-          const int t = min(64 * kb + 4 * k4 + kk, a.T - 1);
-          vc[i][kk] = *reinterpret_cast<const u32x4_t*>(vbase + (size_t)t * HD + 8 * ch);
-        }
-      }
-#pragma unroll
-      for (int i = 0; i < 64 * CPR / 256; ++i) {
-        const int c = tid + 256 * i, row = c / CPR, ch = c - row * CPR;
-        *reinterpret_cast<u32x4_t*>(Ks + row * KLDS + 8 * ch) = kc[i];
-      }
-#pragma unroll
-      for (int i = 0; i < VG / 256; ++i) {
-        const int gidx = tid + 256 * i, k4 = gidx & 15, ch = gidx >> 4;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const int word = e >> 1, sh = (e & 1) * 16;
-          uint2 pk;
-          pk.x = ((vc[i][0][word] >> sh) & 0xffffu) | (((vc[i][1][word] >> sh) & 0xffffu) << 16);
-          pk.y = ((vc[i][2][word] >> sh) & 0xffffu) | (((vc[i][3][word] >> sh) & 0xffffu) << 16);
-          *reinterpret_cast<uint2*>(Vt + (8 * ch + e) * VLD + 4 * k4) = pk;
-        }
+      for (int e = 0; e < 8; ++e) {
+        const int word = e >> 1, sh = (e & 1) * 16;
+        uint2 pk;
+        pk.x = ((vc[i][0][word] >> sh) & 0xffffu) | (((vc[i][1][word] >> sh) & 0xffffu) << 16);
+        pk.y = ((vc[i][2][word] >> sh) & 0xffffu) | (((vc[i][3][word] >> sh) & 0xffffu) << 16);
+        *reinterpret_cast<uint2*>(Vt + (8 * ch + e) * VLD + 4 * k4) = pk;
       }
     }
     __syncthreads();
+    if (kb < qb) load_kv(kb + 1);  // in flight while this block is computed
 
-    // scores of block (qi, kj), masked, into LDS
+    // scores of block (qi, kj), masked, into LDS (two accumulators halve the chain)
     {
-      f32x16_t s;
+      f32x16_t s0, s1;
 #pragma unroll
-      for (int i = 0; i < 16; ++i) s[i] = 0.0f;
+      for (int i = 0; i < 16; ++i) s0[i] = s1[i] = 0.0f;
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks) {
-        const bf16x8_t kf = *reinterpret_cast<const bf16x8_t*>(Ks + (32 * kj + (lane & 31)) * KLDS + 16 * ks + 8 * (lane >> 5));
-        s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qf[ks], kf, s, 0, 0, 0);
+      for (int ks = 0; ks < KS; ks += 2) {
+        const uint16_t* kr = Ks + (32 * kj + (lane & 31)) * KLDS + 8 * (lane >> 5);
+        const bf16x8_t k0 = *reinterpret_cast<const bf16x8_t*>(kr + 16 * ks);
+        const bf16x8_t k1 = *reinterpret_cast<const bf16x8_t*>(kr + 16 * ks + 16);
+        s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qf[ks], k0, s0, 0, 0, 0);
+        s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qf[ks + 1], k1, s1, 0, 0, 0);
       }
       const int key = 64 * kb + 32 * kj + (lane & 31);
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int rl = 32 * qi + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
         const int query = 64 * qb + rl;
-        float v = s[r] * scale;
+        float v = (s0[r] + s1[r]) * scale;
         if (query >= a.T) v = 0.0f;  // rows past the end: finite, never stored
         else if (key > query) v = -INFINITY;
         Ss[rl * SLD + 32 * kj + (lane & 31)] = v;
@@ -371,7 +388,8 @@ static hipError_t prefill_t(const PrefillArgs& a, hipStream_t st) {
   auto k = prefill_attn_kernel<HD>;
   hipError_t e = set_lds_once(k, bytes, done);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k, dim3((a.T + 63) / 64, a.n_q, a.B), dim3(256), bytes, st, a);
+  const XcdMap m = xcd_map((long long)a.B * a.n_q * ((a.T + 63) / 64));
+  hipLaunchKernelGGL(k, dim3(m.grid), dim3(256), bytes, st, a, m.per);
   return hipGetLastError();
 }
 
