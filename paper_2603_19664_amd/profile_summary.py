@@ -1,6 +1,7 @@
 """Condense rocprofv3 CSV output into the short text summaries kept under profiles/.
 
     python -m paper_2603_19664_amd.profile_summary stats <run_kernel_stats.csv> "<command>" > profiles/X.md
+    python -m paper_2603_19664_amd.profile_summary trace <run_kernel_trace.csv> "<command>" > profiles/X.md
     python -m paper_2603_19664_amd.profile_summary pmc <dir with p*/run_counter_collection.csv> <kernel substring> "<command>"
     python -m paper_2603_19664_amd.profile_summary traffic <fetch dir> <write dir> <kernel> <copy kernel> <copy bytes> <workload> "<command>"
 """
@@ -21,6 +22,23 @@ def stats(path: str, command: str, top: int = 12) -> str:
         name = r["Name"].split("(")[0][:80]
         out.append(f"| `{name}` | {r['Calls']} | {float(r['AverageNs']) / 1e3:.2f} | {float(r['MinNs']) / 1e3:.2f} | "
                    f"{float(r['MaxNs']) / 1e3:.2f} | {float(r['Percentage']):.1f} |")
+    return "\n".join(out) + "\n"
+
+
+def trace(path: str, command: str, top: int = 12) -> str:
+    """Per (kernel, grid size) launch durations from a --kernel-trace CSV: kernels
+    launched at several shapes get a row per shape."""
+    groups = collections.defaultdict(list)
+    for r in csv.DictReader(open(path)):
+        grid = r.get("Grid_Size_X") or r.get("Grid_Size") or "?"
+        wg = r.get("Workgroup_Size_X") or r.get("Workgroup_Size") or "1"
+        groups[(r["Kernel_Name"].split("(")[0][:80], int(grid) // max(int(wg), 1))].append(
+            (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3)
+    out = ["# rocprofv3 kernel trace, per kernel and grid", "", "Command (repository root, one MI355X):", "", "```",
+           command, "```", "", "| kernel | workgroups | launches | average (us) | min (us) | max (us) |",
+           "|---|---|---|---|---|---|"]
+    for (name, wgs), v in sorted(groups.items(), key=lambda x: -sum(x[1]))[:top]:
+        out.append(f"| `{name}` | {wgs} | {len(v)} | {sum(v) / len(v):.1f} | {min(v):.1f} | {max(v):.1f} |")
     return "\n".join(out) + "\n"
 
 
@@ -71,6 +89,8 @@ if __name__ == "__main__":
     mode = sys.argv[1]
     if mode == "stats":
         sys.stdout.write(stats(sys.argv[2], sys.argv[3]))
+    elif mode == "trace":
+        sys.stdout.write(trace(sys.argv[2], sys.argv[3]))
     elif mode == "pmc":
         sys.stdout.write(pmc(sys.argv[2], sys.argv[3], sys.argv[4]))
     elif mode == "traffic":
