@@ -63,3 +63,63 @@ def test_multiturn_final_turn_full_size_b16_ctx5120():
     # Gemma 3-4B layer at the last turn boundary of the 20 x 256-token conversation
     wl = C.GEMMA3_MULTITURN
     _full_size_case(wl, B=wl.batch, T=wl.turns * wl.turn_tokens, sampled=(0, wl.batch - 1), layer=17)
+
+
+def test_sliding_window_full_size_gemma_ctx4096_window1024():
+    # Gemma 3-4B layer shape at the headline context (4096 checkpointed tokens + the
+    # current one), a 1024-key sliding window: only the window's rows are recomputed
+    import oracle as O
+    wl = C.GEMMA3_4B
+    L = make_layer(wl, B=1, T=wl.ctx, layer=9)
+    s = L.shape
+    W = 1024
+    q = torch.empty((1, s.n_q_heads, s.head_dim), dtype=s.torch_dtype, device="cuda")
+    tk = torch.zeros((1, s.n_kv_heads, 1, s.head_dim), dtype=s.torch_dtype, device="cuda")
+    tv = torch.zeros_like(tk)
+    pos = torch.full((1,), W - 1, dtype=torch.int32, device="cuda")
+    kvd.kvd_project_qkv(s, L.h_new, L.gamma, L.lw_q, L.lw_k, L.lw_v, pos, q, tk, tv, 0)
+    out = torch.empty_like(q)
+    ws = kvd.workspace(s, kvd.KVD_OP_FUSED, 1, W - 1, 1)
+    kvd.kvd_fused_window_attn(s, q, L.h, wl.ctx, L.gamma, L.lw_k, L.lw_v, W, out, ws, tk, tv, 1)
+    ref = O.sliding_window_decode(f64(L.h_new), f64(L.h), f64(L.gamma), f64(L.w_q), f64(L.w_k), f64(L.w_v), W,
+                                  s.n_q_heads, s.n_kv_heads, s.head_dim, s.rms_eps, s.rope_theta)
+    check("sliding window out vs oracle", out, ref, TOL)
+
+
+def test_block_forward_full_size_gemma_t4096_sampled_rows():
+    # one Gemma-3-4B-shaped block (d_ff 10240) over 4096 positions, in the launch
+    # configuration the benchmark times; the oracle computes sampled output rows one by
+    # one from its pinned pieces (K/V of every earlier position, decode attention over
+    # keys 0..p, W_o, the SiLU-gated MLP)
+    import oracle as O
+    from paper_2603_19664_amd import inputs
+    wl = C.GEMMA3_4B
+    d_ff, T = 10240, wl.ctx
+    s = kvd.shape_of(wl).packed()
+    gamma, w_q, w_k, w_v = inputs.weights(wl, 2, 0, "cuda")
+    w_o, gamma_mlp, w_gate, w_up, w_down = inputs.block_weights(wl, 2, d_ff, 0, "cuda")
+    pw = lambda w: kvd.kvd_pack_weights(s, w)  # noqa: E731
+    lw = (gamma, pw(w_q), pw(w_k), pw(w_v), kvd.kvd_pack_matrix(w_o), gamma_mlp, pw(w_gate), pw(w_up),
+          kvd.kvd_pack_matrix(w_down))
+    h, _ = inputs.residuals(wl, 2, 1, T, 0, "cuda")
+    h = h.contiguous()
+    pos0 = torch.zeros((1,), dtype=torch.int32, device="cuda")
+    out = torch.empty_like(h)
+    ws = torch.empty(kvd.kvd_block_workspace_bytes(s, d_ff, 1, T), dtype=torch.uint8, device="cuda")
+    kvd.kvd_block_forward(s, kvd.block_weights(*lw), h, out, pos0, ws)
+    torch.cuda.synchronize()
+    rows = [0, 1, 63, 64, 1000, 2047, 4095]
+    hx = f64(h)[0]
+    g_a, wq, wk, wv, wo, g_m, wg, wu, wd = (f64(t) for t in (gamma, w_q, w_k, w_v, w_o, gamma_mlp, w_gate, w_up,
+                                                                w_down))
+    last = max(rows) + 1
+    K, V = O.recompute_kv(hx[None, :last], g_a, wk, wv, np.arange(last)[None, :], s.n_kv_heads, s.head_dim,
+                          s.rms_eps, s.rope_theta)
+    got = f64(out)[0]
+    for p in rows:
+        hb = O.rms_normalize(hx[p], g_a, s.rms_eps)
+        qp = O.apply_rope(O.project_heads(hb[None], wq, s.n_q_heads, s.head_dim), float(p), s.rope_theta)
+        heads = O.decode_attention(qp, K[:, :, :p + 1], V[:, :, :p + 1]).reshape(-1)
+        hhat = hx[p] + heads @ wo.T
+        ref = hhat + O.swiglu_mlp(O.rms_normalize(hhat, g_m, s.rms_eps)[None], wg, wu, wd)[0]
+        check(f"block row {p} vs oracle", got[p], ref, TOL)
