@@ -239,15 +239,16 @@ struct MfmaTile {
   static __device__ __forceinline__ void run(const uint16_t* const (&hrow)[CPT], const bool (&valid)[CPT], const uint16_t* gam,
                              const uint16_t* gam_g, int d, float eps, const Half (&halves)[2], uint16_t* hst,
                              float* rinv, const int* pos, const double* rev, uint16_t* kv, const Setup& setup) {
+    const int rope0 = halves[0].rope, rope1 = halves[1].rope;
     run_with(hrow, valid, gam, gam_g, d, eps, halves, hst, rinv, setup,
              [&](const f32x16_t (&acc)[NB_F][NB_T], const bool (&wok)[NB_F]) {
-               store_kv(acc, wok, halves, rinv, pos, rev, kv);
+               store_kv(acc, wok, rope0, rope1, rinv, pos, rev, kv);
              });
   }
 
   // Epilogue of run(): row scale, RoPE on rotated halves, one RNE rounding, LDS tile.
   static __device__ __forceinline__ void store_kv(const f32x16_t (&acc)[NB_F][NB_T], const bool (&wok)[NB_F],
-                                                  const Half (&halves)[2], const float* rinv, const int* pos,
+                                                  int rope0, int rope1, const float* rinv, const int* pos,
                                                   const double* rev, uint16_t* kv) {
     const int lane = threadIdx.x & 63, wave = wave_id();
     const int fw = wave % WF, tw = wave / WF;
@@ -263,7 +264,7 @@ struct MfmaTile {
         float v[16];
 #pragma unroll
         for (int r = 0; r < 16; ++r) v[r] = wok[bf] ? acc[bf][bt][r] * ri : 0.0f;
-        if (half ? halves[1].rope : halves[0].rope) {
+        if (half ? rope1 : rope0) {
 #pragma unroll
           for (int r = 0; r < 16; r += 2) {
             const int f = row0 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
@@ -296,15 +297,19 @@ struct MfmaTile {
     const int fw = wave % WF, tw = wave / WF;
     const int nsteps = d / kKT;
 
+    // the halves' weight pointers as values (a runtime choice between two array
+    // elements would keep the array in scratch memory)
+    const void* const hw0 = halves[0].w;
+    const void* const hw1 = halves[1].w;
     const uint16_t* wrow[NB_F];
     bool wok[NB_F];
 #pragma unroll
     for (int bf = 0; bf < NB_F; ++bf) {
       int half, row0;
       block_rows(fw, bf, half, row0);
-      const uint16_t* w = static_cast<const uint16_t*>(half ? halves[1].w : halves[0].w);
+      const uint16_t* w = static_cast<const uint16_t*>(half ? hw1 : hw0);
       wok[bf] = w != nullptr;  // uniform per wave
-      const uint16_t* wb = wok[bf] ? w : static_cast<const uint16_t*>(halves[0].w);
+      const uint16_t* wb = wok[bf] ? w : static_cast<const uint16_t*>(hw0);
       wrow[bf] = PACKED ? wb + (size_t)row0 * d + 8 * lane
                         : wb + (size_t)(row0 + (lane & 31)) * d + 8 * (lane >> 5);
     }
