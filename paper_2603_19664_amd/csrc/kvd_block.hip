@@ -124,55 +124,54 @@ __global__ __launch_bounds__(kNtTile, 1) void gemm_kernel(GemmArgs a, int per_xc
 
 // ------------------------------------------------------------------ causal prefill attention
 
-// LDS of prefill_attn_kernel (bytes): the key tile [64][HD + 8] bf16, the value
-// tile transposed [HD][64 + 8] bf16, scores [64][65] fp32, probabilities
-// [64][64 + 8] bf16, and per query row the running max, sum and rescale factor.
+// LDS of prefill_attn_kernel (bytes): the workgroup's query rows [128][HD + 8],
+// the key tile [64][HD + 8] and the value tile transposed [HD][64 + 8], bf16.
 struct PrefillLds {
-  size_t ks, vt, ss, ps, m, l, al, end;
+  size_t qs, ks, vt, end;
 };
 constexpr PrefillLds prefill_lds(int hd) {
   PrefillLds L{};
-  L.ks = 0;
+  L.qs = 0;
+  L.ks = L.qs + (size_t)2 * 128 * (hd + 8);
   L.vt = L.ks + (size_t)2 * 64 * (hd + 8);
-  L.ss = L.vt + (size_t)2 * hd * (64 + 8);
-  L.ps = L.ss + (size_t)4 * 64 * 65;
-  L.m = L.ps + (size_t)2 * 64 * (64 + 8);
-  L.l = L.m + 4 * 64;
-  L.al = L.l + 4 * 64;
-  L.end = L.al + 4 * 64;
+  L.end = L.vt + (size_t)2 * hd * (64 + 8);
   return L;
 }
 
-// grid: xcd_map(B * n_q * nqb) workgroups, nqb = ceil(T / 64), 256 threads (4
+// grid: xcd_map(B * n_q * nqb) workgroups, nqb = ceil(T / 128), 256 threads (4
 // waves).  Items are ordered (sequence, KV head, query block from the last,
 // query head of the group), so an XCD's workgroups share one KV head's keys and
-// values in its L2 and the longest rows start first.  A workgroup takes 64 query
-// rows of one head through the key blocks 0 .. its own (flash order: scores,
-// running max / sum, rescaled accumulators), loading key block kb + 1 into
-// registers while block kb is computed.  Wave w computes the 32 x 32 score block
-// (query half w / 2, key half w % 2) with its query rows in registers, and the
-// output columns [w % 2 * hd / 2, + hd / 2) of query half w / 2.  Scores are in
-// the log2 domain (log2(e) / sqrt(hd) folded into the scale).
+// values in its L2 and the longest rows start first.  A workgroup takes 128 query
+// rows of one head, 32 per wave, through the key blocks of 64 up to its last row
+// (flash order), loading block kb + 1 into registers while block kb is computed.
+//
+// Scores are computed transposed, S^T = K Q^T: A = 32 keys from the LDS tile,
+// B = the wave's 32 query rows (registers), so that a lane holds one query's
+// scores in its registers and the softmax needs no LDS: the running max and sum
+// of a query live in the two lanes (l, l ^ 32) that hold its keys, and the max
+// used for the weights moves only in steps of more than 2^8 (rescaling then).  The output is
+// accumulated transposed too, O^T += V^T P^T, with P^T straight from the score
+// registers: for the 16 keys of an MFMA step, lane half h supplies the keys its
+// score registers hold (32 kh + 16 (t & 1) + 4 h + {0..3, 8..11}), and the V^T
+// operand takes the same keys, so both operands agree on the reduction order.
+// Scores are in the log2 domain (log2(e) / sqrt(hd) folded into the scale).
 template <int HD>
 __global__ __launch_bounds__(256) void prefill_attn_kernel(PrefillArgs a, int per_xcd) {
   extern __shared__ __align__(16) char lds[];
   constexpr PrefillLds PL = prefill_lds(HD);
-  constexpr int KS = HD / 16;   // 16-wide k-steps of a score block
-  constexpr int DBW = HD / 64;  // 32-wide output column blocks per wave
-  constexpr int KLDS = HD + 8, VLD = 64 + 8, SLD = 65, PLD = 64 + 8;
+  constexpr int KS = HD / 16;              // 16-wide k-steps of a score block
+  constexpr int DB = HD / 32;              // 32-row blocks of O^T (head_dim rows)
+  constexpr int KLDS = HD + 8, VLD = 64 + 8;
   constexpr int CPR = HD / 8;              // 16-byte chunks per key row
   constexpr int KCH = 64 * CPR / 256;      // key chunks per thread
   constexpr int VGR = 16 * CPR / 256;      // value groups (4 keys x 8 columns) per thread
+  uint16_t* Qs = reinterpret_cast<uint16_t*>(lds + PL.qs);
   uint16_t* Ks = reinterpret_cast<uint16_t*>(lds + PL.ks);
   uint16_t* Vt = reinterpret_cast<uint16_t*>(lds + PL.vt);
-  float* Ss = reinterpret_cast<float*>(lds + PL.ss);
-  uint16_t* Ps = reinterpret_cast<uint16_t*>(lds + PL.ps);
-  float* mrow = reinterpret_cast<float*>(lds + PL.m);
-  float* lrow = reinterpret_cast<float*>(lds + PL.l);
-  float* arow = reinterpret_cast<float*>(lds + PL.al);
 
   const int tid = threadIdx.x, lane = tid & 63, w = wave_id();
-  const int nqb = (a.T + 63) / 64;
+  const int hl = lane >> 5;  // lane half
+  const int nqb = (a.T + 127) / 128;
   const int g = a.n_q / a.n_kv;
   const long long item = (long long)(blockIdx.x % kXcds) * per_xcd + blockIdx.x / kXcds;
   if (item >= (long long)a.B * a.n_q * nqb) return;
@@ -182,28 +181,27 @@ __global__ __launch_bounds__(256) void prefill_attn_kernel(PrefillArgs a, int pe
   const long long r2 = r1 / nqb;
   const int j = (int)(r2 % a.n_kv), b = (int)(r2 / a.n_kv);
   const int h = j * g + hh;
-  const int qi = w >> 1, kj = w & 1;
+  const int q0 = 128 * qb + 32 * w;          // this wave's first query row
+  const int query = q0 + (lane & 31);        // this lane's query row
   const float scale = ScoreScale<HD>::v;
   const uint16_t* kbase = static_cast<const uint16_t*>(a.k) + ((size_t)b * a.n_kv + j) * a.T * HD;
   const uint16_t* vbase = static_cast<const uint16_t*>(a.v) + ((size_t)b * a.n_kv + j) * a.T * HD;
 
-  // this wave's query rows as MFMA A operands: row 64 qb + 32 qi + lane % 32
-  bf16x8_t qf[KS];
-  {
-    const int t = min(64 * qb + 32 * qi + (lane & 31), a.T - 1);
-    const uint16_t* qrow = static_cast<const uint16_t*>(a.q) + (((size_t)b * a.T + t) * a.n_q + h) * HD + 8 * (lane >> 5);
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) qf[ks] = *reinterpret_cast<const bf16x8_t*>(qrow + 16 * ks);
+  // the wave's query rows into LDS (its own 32 rows; read back as MFMA B
+  // operands: column = query, 8 dims per lane half)
+  for (int c = lane; c < 32 * CPR; c += 64) {
+    const int row = c / CPR, ch = c - row * CPR;
+    const int t = min(q0 + row, a.T - 1);
+    *reinterpret_cast<u32x4_t*>(Qs + (32 * w + row) * KLDS + 8 * ch) = *reinterpret_cast<const u32x4_t*>(
+        static_cast<const uint16_t*>(a.q) + (((size_t)b * a.T + t) * a.n_q + h) * HD + 8 * ch);
   }
-  if (tid < 64) {
-    mrow[tid] = -INFINITY;
-    lrow[tid] = 0.0f;
-  }
-  f32x16_t o[DBW];
+  const uint16_t* qrow = Qs + (32 * w + (lane & 31)) * KLDS + 8 * hl;
+  f32x16_t o[DB];
 #pragma unroll
-  for (int db = 0; db < DBW; ++db)
+  for (int db = 0; db < DB; ++db)
 #pragma unroll
     for (int i = 0; i < 16; ++i) o[db][i] = 0.0f;
+  float m_run = -INFINITY, l_run = 0.0f;
 
   // key / value block kb into registers (rows clamped to T - 1: masked below)
   u32x4_t kc[KCH], vc[VGR][4];
@@ -224,9 +222,11 @@ __global__ __launch_bounds__(256) void prefill_attn_kernel(PrefillArgs a, int pe
       }
     }
   };
+  const int last_row = min(128 * qb + 127, a.T - 1);
+  const int nkb = last_row / 64 + 1;  // key blocks 0 .. nkb - 1
   load_kv(0);
 
-  for (int kb = 0; kb <= qb; ++kb) {
+  for (int kb = 0; kb < nkb; ++kb) {
     // the registers into LDS: K as is, V transposed ([column][key])
 #pragma unroll
     for (int i = 0; i < KCH; ++i) {
@@ -246,99 +246,105 @@ __global__ __launch_bounds__(256) void prefill_attn_kernel(PrefillArgs a, int pe
       }
     }
     __syncthreads();
-    if (kb < qb) load_kv(kb + 1);  // in flight while this block is computed
+    if (kb + 1 < nkb) load_kv(kb + 1);  // in flight while this block is computed
 
-    // scores of block (qi, kj), masked, into LDS (two accumulators halve the chain)
-    {
-      f32x16_t s0, s1;
+    // a wave whose rows all precede the block (or lie past T) skips it
+    if (64 * kb <= q0 + 31 && q0 < a.T) {
+      // S^T for key halves kh = 0, 1: four independent accumulator chains
+      f32x16_t st[2], sx[2];
 #pragma unroll
-      for (int i = 0; i < 16; ++i) s0[i] = s1[i] = 0.0f;
+      for (int kh = 0; kh < 2; ++kh)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) st[kh][i] = sx[kh][i] = 0.0f;
 #pragma unroll
       for (int ks = 0; ks < KS; ks += 2) {
-        const uint16_t* kr = Ks + (32 * kj + (lane & 31)) * KLDS + 8 * (lane >> 5);
-        const bf16x8_t k0 = *reinterpret_cast<const bf16x8_t*>(kr + 16 * ks);
-        const bf16x8_t k1 = *reinterpret_cast<const bf16x8_t*>(kr + 16 * ks + 16);
-        s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qf[ks], k0, s0, 0, 0, 0);
-        s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qf[ks + 1], k1, s1, 0, 0, 0);
-      }
-      const int key = 64 * kb + 32 * kj + (lane & 31);
+        const bf16x8_t q0f = *reinterpret_cast<const bf16x8_t*>(qrow + 16 * ks);
+        const bf16x8_t q1f = *reinterpret_cast<const bf16x8_t*>(qrow + 16 * ks + 16);
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int rl = 32 * qi + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-        const int query = 64 * qb + rl;
-        float v = (s0[r] + s1[r]) * scale;
-        if (query >= a.T) v = 0.0f;  // rows past the end: finite, never stored
-        else if (key > query) v = -INFINITY;
-        Ss[rl * SLD + 32 * kj + (lane & 31)] = v;
+        for (int kh = 0; kh < 2; ++kh) {
+          const uint16_t* kr = Ks + (32 * kh + (lane & 31)) * KLDS + 8 * hl + 16 * ks;
+          const bf16x8_t k0 = *reinterpret_cast<const bf16x8_t*>(kr);
+          const bf16x8_t k1 = *reinterpret_cast<const bf16x8_t*>(kr + 16);
+          st[kh] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k0, q0f, st[kh], 0, 0, 0);
+          sx[kh] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k1, q1f, sx[kh], 0, 0, 0);
+        }
       }
-    }
-    __syncthreads();
-
-    // running softmax: 4 threads per query row, 16 keys each
-    {
-      const int row = tid >> 2, part = tid & 3;
-      float x[16];
+#pragma unroll
+      for (int kh = 0; kh < 2; ++kh)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int key = 64 * kb + 32 * kh + 8 * (r >> 2) + 4 * hl + (r & 3);
+          float v = (st[kh][r] + sx[kh][r]) * scale;
+          if (query >= a.T) v = 0.0f;  // rows past the end: finite, never stored
+          else if (key > query) v = -INFINITY;
+          st[kh][r] = v;
+        }
+      // running softmax of this lane's query: its 32 scores here and 32 in lane ^ 32
       float mx = -INFINITY;
 #pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        x[e] = Ss[row * SLD + 16 * part + e];
-        mx = fmaxf(mx, x[e]);
+      for (int kh = 0; kh < 2; ++kh)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, st[kh][r]);
+      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+      // The reference max moves only when the block's max exceeds it by more than 8
+      // (log2 units): the weights 2^(s - m) stay <= 2^8, and O and l are rescaled
+      // (accumulators held in AGPRs) only in the few blocks where it moves.
+      const bool grow = mx > m_run + 8.0f;
+      if (__any(grow)) {
+        const float m_new = grow ? mx : m_run;
+        const float alpha = exp2f(m_run - m_new);
+        m_run = m_new;
+        l_run *= alpha;
+#pragma unroll
+        for (int db = 0; db < DB; ++db)
+#pragma unroll
+          for (int i = 0; i < 16; ++i) o[db][i] *= alpha;
       }
-      mx = fmaxf(mx, __shfl_xor(mx, 1, 64));
-      mx = fmaxf(mx, __shfl_xor(mx, 2, 64));
-      const float m_old = mrow[row];
-      const float m_new = fmaxf(m_old, mx);
+      bf16x8_t pf[4];  // P^T operands of the four 16-key MFMA steps
       float sum = 0.0f;
-      uint32_t pw[8];
 #pragma unroll
-      for (int e = 0; e < 16; e += 2) {
-        const float p0 = exp2f(x[e] - m_new), p1 = exp2f(x[e + 1] - m_new);
-        pw[e >> 1] = pack_bf16x2(p0, p1);
-        sum += bf_lo(pw[e >> 1]) + bf_hi(pw[e >> 1]);  // the rounded weights the MFMA uses
+      for (int t = 0; t < 4; ++t) {
+        uint32_t pw[4];
+#pragma unroll
+        for (int e = 0; e < 8; e += 2) {
+          const int r = 8 * (t & 1) + e;
+          pw[e >> 1] = pack_bf16x2(exp2f(st[t >> 1][r] - m_run), exp2f(st[t >> 1][r + 1] - m_run));
+          sum += bf_lo(pw[e >> 1]) + bf_hi(pw[e >> 1]);  // the rounded weights the MFMA uses
+        }
+        pf[t] = __builtin_bit_cast(bf16x8_t, make_uint4(pw[0], pw[1], pw[2], pw[3]));
       }
-      *reinterpret_cast<uint4*>(Ps + row * PLD + 16 * part) = make_uint4(pw[0], pw[1], pw[2], pw[3]);
-      *reinterpret_cast<uint4*>(Ps + row * PLD + 16 * part + 8) = make_uint4(pw[4], pw[5], pw[6], pw[7]);
-      sum += __shfl_xor(sum, 1, 64);
-      sum += __shfl_xor(sum, 2, 64);
-      if (part == 0) {
-        const float al = exp2f(m_old - m_new);
-        arow[row] = al;
-        lrow[row] = lrow[row] * al + sum;
-        mrow[row] = m_new;
-      }
-    }
-    __syncthreads();
-
-    // o = o * alpha + P V over this key block
+      sum += __shfl_xor(sum, 32, 64);
+      l_run += sum;
+      // O^T += V^T P^T: per 16-key step, the DB accumulators are independent
 #pragma unroll
-    for (int db = 0; db < DBW; ++db) {
-      const int col0 = 32 * (DBW * kj + db);
+      for (int t = 0; t < 4; ++t) {
+        const int k0 = 32 * (t >> 1) + 16 * (t & 1);
 #pragma unroll
-      for (int r = 0; r < 16; ++r) o[db][r] *= arow[32 * qi + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3)];
-#pragma unroll
-      for (int ks = 0; ks < 4; ++ks) {
-        const bf16x8_t pf = *reinterpret_cast<const bf16x8_t*>(Ps + (32 * qi + (lane & 31)) * PLD + 16 * ks + 8 * (lane >> 5));
-        const bf16x8_t vf = *reinterpret_cast<const bf16x8_t*>(Vt + (col0 + (lane & 31)) * VLD + 16 * ks + 8 * (lane >> 5));
-        o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(pf, vf, o[db], 0, 0, 0);
+        for (int db = 0; db < DB; ++db) {
+          const uint16_t* vr = Vt + (32 * db + (lane & 31)) * VLD + 4 * hl + k0;
+          const uint2 lo = *reinterpret_cast<const uint2*>(vr);
+          const uint2 hi = *reinterpret_cast<const uint2*>(vr + 8);
+          const bf16x8_t vf = __builtin_bit_cast(bf16x8_t, make_uint4(lo.x, lo.y, hi.x, hi.y));
+          o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[t], o[db], 0, 0, 0);
+        }
       }
     }
     __syncthreads();
   }
 
-  // out = o / l, one RNE rounding
-  uint16_t* out = static_cast<uint16_t*>(a.out);
+  // out = O / l, one RNE rounding: lane = query, rows = dims 32 db + 8 (r / 4) + 4 hl + r % 4
+  if (query < a.T) {
+    const float inv = 1.0f / l_run;
+    uint16_t* orow = static_cast<uint16_t*>(a.out) + ((size_t)b * a.T + query) * a.n_q * HD + (size_t)h * HD;
 #pragma unroll
-  for (int r = 0; r < 16; ++r) {
-    const int rl = 32 * qi + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-    const int t = 64 * qb + rl;
-    if (t >= a.T) continue;
-    const float inv = 1.0f / lrow[rl];
+    for (int db = 0; db < DB; ++db)
 #pragma unroll
-    for (int db = 0; db < DBW; ++db) {
-      const int col = 32 * (DBW * kj + db) + (lane & 31);
-      out[((size_t)b * a.T + t) * a.n_q * HD + (size_t)h * HD + col] =
-          (uint16_t)(pack_bf16x2(o[db][r] * inv, 0.0f) & 0xffffu);
-    }
+      for (int g4 = 0; g4 < 4; ++g4) {
+        uint2 v;
+        v.x = pack_bf16x2(o[db][4 * g4 + 0] * inv, o[db][4 * g4 + 1] * inv);
+        v.y = pack_bf16x2(o[db][4 * g4 + 2] * inv, o[db][4 * g4 + 3] * inv);
+        *reinterpret_cast<uint2*>(orow + 32 * db + 8 * g4 + 4 * hl) = v;
+      }
   }
 }
 
@@ -388,7 +394,7 @@ static hipError_t prefill_t(const PrefillArgs& a, hipStream_t st) {
   auto k = prefill_attn_kernel<HD>;
   hipError_t e = set_lds_once(k, bytes, done);
   if (e != hipSuccess) return e;
-  const XcdMap m = xcd_map((long long)a.B * a.n_q * ((a.T + 63) / 64));
+  const XcdMap m = xcd_map((long long)a.B * a.n_q * ((a.T + 127) / 128));
   hipLaunchKernelGGL(k, dim3(m.grid), dim3(256), bytes, st, a, m.per);
   return hipGetLastError();
 }
