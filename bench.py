@@ -50,7 +50,7 @@ def parse():
                    help="size of one untimed device-to-device copy whose HBM counters calibrate the traffic figure")
     p.add_argument("--next", action="store_true",
                    help="also measure the hybrid cache budget sweep and the recompute-vs-transfer sweep over evicted tokens")
-    p.add_argument("--only", choices=["single_checkpoint", "sliding_window"],
+    p.add_argument("--only", choices=["single_checkpoint", "sliding_window", "hybrid_budget", "evicted_tokens"],
                    help="run only this one of the --next measurements and print its JSON (no headline line; "
                         "for profiling its kernels)")
     p.add_argument("--extra", action="store_true",
@@ -58,6 +58,28 @@ def parse():
                         "the multi-turn conversation (Gemma 3-4B shape, B=16, a decode step at each of 20 turn "
                         "boundaries of 256 tokens) into extra_workloads")
     return p.parse_args()
+
+
+def op_timer(torch, np, default_iters):
+    """op_time(fn, ...): average (or median) device time of fn() in us over iters calls, HIP
+    events around each call, optionally after flush() (a cache-evicting write)."""
+    def op_time(fn, iters=None, warm=2, flush=None, median=False):
+        iters = iters or default_iters
+        for _ in range(warm):
+            fn()
+        times = []
+        for _ in range(iters):
+            if flush is not None:
+                flush()
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            fn()
+            b.record()
+            times.append((a, b))
+        torch.cuda.synchronize()
+        v = [a.elapsed_time(b) for a, b in times]
+        return float(np.median(v) if median else np.mean(v)) * 1e3
+    return op_time
 
 
 def log(msg):
@@ -102,8 +124,12 @@ def main():
 
     torch.cuda.set_device(0)
     if args.only:
+        op_time = op_timer(torch, np, 3)
         fn = {"single_checkpoint": lambda: run_single_checkpoint(torch, np, kvd, configs, inputs, log),
-              "sliding_window": lambda: run_sliding(torch, kvd, configs, inputs, log)}[args.only]
+              "sliding_window": lambda: run_sliding(torch, kvd, configs, inputs, log),
+              "hybrid_budget": lambda: run_hybrid(torch, np, kvd, configs, inputs, op_time, log),
+              "evicted_tokens": lambda: run_evicted(torch, np, kvd, configs, inputs, op_time, log)[
+                  "evicted_tokens"]}[args.only]
         print(json.dumps({args.only: fn()}), flush=True)
         return
     dev = "cuda"
@@ -227,23 +253,7 @@ def main():
             traffic = tr.get("bytes_per_launch")
 
     # ---------------------------------------------------------------- per-op us/layer and baselines
-    def op_time(fn, iters=None, warm=2, flush=None, median=False):
-        """Average (or median) device time of fn() over iters calls, HIP events around each call."""
-        iters = iters or max(3, K)
-        for _ in range(warm):
-            fn()
-        times = []
-        for _ in range(iters):
-            if flush is not None:
-                flush()
-            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            a.record()
-            fn()
-            b.record()
-            times.append((a, b))
-        torch.cuda.synchronize()
-        v = [a.elapsed_time(b) for a, b in times]
-        return float(np.median(v) if median else np.mean(v)) * 1e3  # us
+    op_time = op_timer(torch, np, max(3, K))
 
     per_op = {}
     baselines = {}
@@ -419,15 +429,27 @@ def run_next(args, torch, np, kvd, configs, inputs, op_time, log):
       their checkpoints (kvd_recompute_kv), copied from a bf16 copy in HBM, and copied from a
       bf16 copy in pinned host memory over PCIe (token-major, so each is one contiguous copy).
       Medians of 11 calls (a PCIe copy occasionally takes far longer)."""
+    res = {"hybrid_budget": run_hybrid(torch, np, kvd, configs, inputs, op_time, log)}
+    res.update(run_evicted(torch, np, kvd, configs, inputs, op_time, log))
+    res["sliding_window"] = run_sliding(torch, kvd, configs, inputs, log)
+    res["single_checkpoint"] = run_single_checkpoint(torch, np, kvd, configs, inputs, log)
+    return res
+
+
+def _next_setup(torch, kvd, configs, inputs):
     wl = configs.GEMMA3_4B
     s = kvd.shape_of(wl).packed()
-    T, d, nkv, hd = wl.ctx, wl.d_model, wl.n_kv, wl.head_dim
     flush_buf = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
-    flush = lambda: flush_buf.fill_(1)  # noqa: E731
     gamma, w_q, w_k, w_v = inputs.weights(wl, 0, 0, "cuda")
     w_q, w_k, w_v = (kvd.kvd_pack_weights(s, w) for w in (w_q, w_k, w_v))
-    res = {}
+    return wl, s, flush_buf, gamma, w_q, w_k, w_v
 
+
+def run_hybrid(torch, np, kvd, configs, inputs, op_time, log):
+    """The hybrid cache budget sweep (see run_next)."""
+    wl, s, flush_buf, gamma, w_q, w_k, w_v = _next_setup(torch, kvd, configs, inputs)
+    flush = lambda: flush_buf.fill_(1)  # noqa: E731
+    T, d, nkv, hd = wl.ctx, wl.d_model, wl.n_kv, wl.head_dim
     rows = []
     for B in (1, 8):
         log(f"[bench] next: hybrid budget B={B}")
@@ -462,9 +484,15 @@ def run_next(args, torch, np, kvd, configs, inputs, op_time, log):
         slopes[str(B)] = {"us_per_recomputed_minus_stored_token": -b, "fit_intercept_us": a,
                           "us_per_stored_token_read": read_per_token,
                           "us_per_recomputed_token": read_per_token - b}
-    res["hybrid_budget"] = {"workload": "gemma3-4b layer, ctx 4096 + current token", "rows": rows,
-                            "per_token_costs": slopes}
+    return {"workload": "gemma3-4b layer, ctx 4096 + current token", "rows": rows, "per_token_costs": slopes}
 
+
+def run_evicted(torch, np, kvd, configs, inputs, op_time, log):
+    """Recompute vs copy of N evicted tokens' K/V (see run_next)."""
+    wl, s, flush_buf, gamma, w_q, w_k, w_v = _next_setup(torch, kvd, configs, inputs)
+    flush = lambda: flush_buf.fill_(1)  # noqa: E731
+    T, nkv, hd = wl.ctx, wl.n_kv, wl.head_dim
+    res = {}
     log("[bench] next: evicted tokens, recompute vs HBM copy vs host copy")
     B = 1
     h, _ = inputs.residuals(wl, 0, B, T, 0, "cuda")
@@ -496,8 +524,6 @@ def run_next(args, torch, np, kvd, configs, inputs, op_time, log):
         "recompute_faster_than_host_copy": [e["N"] for e in erows if e["recompute_us"] < e["host_copy_us"]]}
     del h, Kc, Vc, kv_dev, kv_host, flush_buf
     torch.cuda.empty_cache()
-    res["sliding_window"] = run_sliding(torch, kvd, configs, inputs, log)
-    res["single_checkpoint"] = run_single_checkpoint(torch, np, kvd, configs, inputs, log)
     return res
 
 

@@ -626,9 +626,14 @@ static hipError_t fused_t(const FusedArgs& a, hipStream_t st) {
   auto k = fused_kernel<T, HD, MT, PACKED>;
   hipError_t e = ensure_lds(k, bytes, done);
   if (e != hipSuccess) return e;
-  const int C = fused_tail_tiles<T>(a.n_rec, a.T_tail) + a.n_rec;
+  const int n_tail = fused_tail_tiles<T>(a.n_rec, a.T_tail);
+  const int C = n_tail + a.n_rec;
   const XcdMap m = xcd_map((long long)a.n_kv * a.B * C);
-  hipLaunchKernelGGL(k, dim3(m.grid), dim3(kNtTile), bytes, st, a, m.per, fused_head_group(a.n_kv, HD, m.per));
+  // With stored tail tiles (short items that go first in each head's run) one
+  // head per XCD run keeps short items in most runs, so that a grid a little
+  // larger than the chip starts its last items on CUs the short ones free.
+  const int hg = n_tail > 0 ? 1 : fused_head_group(a.n_kv, HD, m.per);
+  hipLaunchKernelGGL(k, dim3(m.grid), dim3(kNtTile), bytes, st, a, m.per, hg);
   return hipGetLastError();
 }
 
