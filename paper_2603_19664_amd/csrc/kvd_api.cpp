@@ -360,6 +360,10 @@ kvd_status fused_launch(const kvd_attn_shape* shape, const void* q, const void* 
                         const kvd_kv_view* tail, int32_t T_tail, void* out, void* ws, size_t ws_bytes,
                         const kvd_kv_view* kv_debug, void* stream, const char* name) {
   const int32_t S = splits(shape, KVD_OP_FUSED, T_rec, T_tail);
+  // one workgroup per (KV head, sequence, split), indexed in 32 bits
+  if ((int64_t)shape->n_kv_heads * B * S > INT32_MAX - 8)
+    return fail(KVD_ERR_SHAPE, "%s: n_kv_heads * B * splits = %lld workgroups is too many", name,
+                (long long)shape->n_kv_heads * B * S);
   KVD_TRY(check_ws(shape, B, S, ws, ws_bytes));
   kvd::FusedArgs a{};
   a.q = q;

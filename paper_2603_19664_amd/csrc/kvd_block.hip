@@ -25,10 +25,11 @@ __global__ __launch_bounds__(kNtTile, 1) void gemm_kernel(GemmArgs a, int per_xc
   using Tile = MfmaTile<HD, MT, PACKED>;
   static_assert(Tile::NB_F == 2 && Tile::WT == 1 && Tile::NB_T == 2, "wave fw owns rows 32 fw.. of both halves");
   const int tid = threadIdx.x;
-  const long long item = (long long)(blockIdx.x % kXcds) * per_xcd + blockIdx.x / kXcds;
-  if (item >= (long long)n_units * n_tiles) return;
-  const int unit = (int)(item / n_tiles);
-  const int tile = (int)(item - (long long)unit * n_tiles);
+  // 32-bit index arithmetic: the launch's grid bounds the item count
+  const unsigned item = (blockIdx.x % kXcds) * (unsigned)per_xcd + blockIdx.x / kXcds;
+  if (item >= (unsigned)n_units * (unsigned)n_tiles) return;
+  const int unit = (int)(item / (unsigned)n_tiles);
+  const int tile = (int)(item - (unsigned)unit * (unsigned)n_tiles);
   float* rinv = reinterpret_cast<float*>(lds + PL.rinv);
   uint16_t* hst = reinterpret_cast<uint16_t*>(lds + PL.hst);
   uint16_t* kv = reinterpret_cast<uint16_t*>(lds + PL.kv);
@@ -173,13 +174,14 @@ __global__ __launch_bounds__(256) void prefill_attn_kernel(PrefillArgs a, int pe
   const int hl = lane >> 5;  // lane half
   const int nqb = (a.T + 127) / 128;
   const int g = a.n_q / a.n_kv;
-  const long long item = (long long)(blockIdx.x % kXcds) * per_xcd + blockIdx.x / kXcds;
-  if (item >= (long long)a.B * a.n_q * nqb) return;
-  const int hh = (int)(item % g);
-  const long long r1 = item / g;
-  const int qb = nqb - 1 - (int)(r1 % nqb);  // the longest rows first
-  const long long r2 = r1 / nqb;
-  const int j = (int)(r2 % a.n_kv), b = (int)(r2 / a.n_kv);
+  // 32-bit index arithmetic: the launch's grid bounds the item count
+  const unsigned item = (blockIdx.x % kXcds) * (unsigned)per_xcd + blockIdx.x / kXcds;
+  if (item >= (unsigned)a.B * (unsigned)a.n_q * (unsigned)nqb) return;
+  const int hh = (int)(item % (unsigned)g);
+  const unsigned r1 = item / (unsigned)g;
+  const int qb = nqb - 1 - (int)(r1 % (unsigned)nqb);  // the longest rows first
+  const unsigned r2 = r1 / (unsigned)nqb;
+  const int j = (int)(r2 % (unsigned)a.n_kv), b = (int)(r2 / (unsigned)a.n_kv);
   const int h = j * g + hh;
   const int q0 = 128 * qb + 32 * w;          // this wave's first query row
   const int query = q0 + (lane & 31);        // this lane's query row

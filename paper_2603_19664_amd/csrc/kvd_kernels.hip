@@ -30,10 +30,11 @@ __global__ __launch_bounds__(kNtTile, 1) void proj_kernel(ProjArgs a, int per_xc
   constexpr int CPT = MT * 8 / NT;
   constexpr int KLD = kv_ld<T>(HD);
   const int tid = threadIdx.x;
-  const long long item = (long long)(blockIdx.x % kXcds) * per_xcd + blockIdx.x / kXcds;
-  if (item >= (long long)n_units * n_tiles) return;
-  const int unit = (int)(item / n_tiles);
-  const int tile = (int)(item - (long long)unit * n_tiles);
+  // 32-bit index arithmetic: the launch's grid bounds the item count
+  const unsigned item = (blockIdx.x % kXcds) * (unsigned)per_xcd + blockIdx.x / kXcds;
+  if (item >= (unsigned)n_units * (unsigned)n_tiles) return;
+  const int unit = (int)(item / (unsigned)n_tiles);
+  const int tile = (int)(item - (unsigned)unit * (unsigned)n_tiles);
 
   double* rev = reinterpret_cast<double*>(lds + PL.rev);
   float* rinv = reinterpret_cast<float*>(lds + PL.rinv);
@@ -392,18 +393,22 @@ __global__ __launch_bounds__(kNtTile, 1) void fused_kernel(FusedArgs a, int per_
   const bool fold = fold_tail<T>(a.n_rec, a.T_tail);
   const int n_tail = fused_tail_tiles<T>(a.n_rec, a.T_tail);
   const int C = n_tail + a.n_rec;
-  const long long item = (long long)(blockIdx.x % kXcds) * per_xcd + blockIdx.x / kXcds;
-  if (item >= (long long)a.n_kv * a.B * C) return;
+  // 32-bit index arithmetic (the item count is below 2^31, checked by the host):
+  // every wave runs it on the CU's one scalar unit before its first load.
+  const unsigned item = (blockIdx.x % kXcds) * (unsigned)per_xcd + blockIdx.x / kXcds;
+  if (item >= (unsigned)a.n_kv * (unsigned)a.B * (unsigned)C) return;
   // Items in XCD order: KV heads in groups of hg (a power of two dividing n_kv) of
   // one sequence, the group's chunks in order, its heads alternating.  An XCD's
   // run of per_xcd items then spans hg heads and per_xcd / hg chunks; it pulls
   // each of those residual tiles and each of those heads' weights into its own
   // L2 once.  The host picks hg to balance the two streams (fused_head_group).
-  const long long gi = item / ((long long)hg * C), rem = item - gi * hg * C;  // group index jg * B + b
-  const int jg = (int)(gi / a.B);
-  const int b = (int)(gi - (long long)jg * a.B);
-  const int c = (int)(rem / hg);
-  const int j = jg * hg + (int)(rem - (long long)c * hg);
+  const int hg_log2 = __builtin_ctz((unsigned)hg);
+  const unsigned hgC = (unsigned)C << hg_log2;
+  const unsigned gi = item / hgC, rem = item - gi * hgC;  // group index jg * B + b
+  const int jg = (int)(gi / (unsigned)a.B);
+  const int b = (int)(gi - (unsigned)jg * (unsigned)a.B);
+  const int c = (int)(rem >> hg_log2);
+  const int j = (jg << hg_log2) + (int)(rem & (unsigned)(hg - 1));
   const int rc = c - n_tail;  // recomputed chunk (c >= n_tail)
   const int g = a.n_q / a.n_kv;
   const AttnLds AL = attn_lds(PL.end, g, HD, MT + FR);
@@ -436,8 +441,10 @@ __global__ __launch_bounds__(kNtTile, 1) void fused_kernel(FusedArgs a, int per_
     uint16_t* gam = reinterpret_cast<uint16_t*>(lds + AL.end);
     // q, gamma and rev reach LDS while the K-loop's first loads are in flight
     const TileSetup<T, HD, NT, true> su(static_cast<const T*>(a.q), b, a.n_q, j, g, a.gamma, a.d, a.rev);
-    const int p0 = (a.pos0 != nullptr ? a.pos0[b] : 0) + t0;
+    // pos0[b] is read here, after the K-loop's first loads are issued: a scalar
+    // load read up front holds back every address computation behind its latency
     auto setup = [&]() {
+      const int p0 = (a.pos0 != nullptr ? a.pos0[b] : 0) + t0;
       su.store(reinterpret_cast<float*>(lds + AL.q), gam, rev);
       if (tid < MT) pos[tid] = p0 + tid;
       if constexpr (FR > 0) {
