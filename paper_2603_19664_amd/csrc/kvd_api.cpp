@@ -463,7 +463,8 @@ namespace {
 // heads [B][T][n_q hd], hhat [B][T][d], the MLP activation [B][T][d_ff] (bf16),
 // and a vector of ones (the staged operand of the unnormalised projections).
 struct BlockWs {
-  size_t q, k, v, heads, hhat, u, ones, end;
+  size_t q, k, v, heads, hhat, u, ones, part, ctr, end;
+  kvd::PrefillSplit split;
 };
 BlockWs block_ws(const kvd_attn_shape* s, int32_t d_ff, int32_t B, int32_t T) {
   const size_t bt = (size_t)B * T, qd = (size_t)s->n_q_heads * s->head_dim;
@@ -475,7 +476,13 @@ BlockWs block_ws(const kvd_attn_shape* s, int32_t d_ff, int32_t B, int32_t T) {
   L.hhat = kvd::align_up(L.heads + 2 * bt * qd, 256);
   L.u = kvd::align_up(L.hhat + 2 * bt * s->d_model, 256);
   L.ones = kvd::align_up(L.u + 2 * bt * d_ff, 256);
-  L.end = kvd::align_up(L.ones + 2 * (size_t)std::max<int64_t>((int64_t)qd, d_ff), 256);
+  // the causal attention's key-range parts and their arrival counters (only when it splits)
+  L.split = kvd::prefill_split(B, T, s->n_q_heads);
+  const size_t blocks = (size_t)B * s->n_q_heads * ((T + 127) / 128);
+  const bool split = L.split.NP > 1;
+  L.part = kvd::align_up(L.ones + 2 * (size_t)std::max<int64_t>((int64_t)qd, d_ff), 256);
+  L.ctr = kvd::align_up(L.part + (split ? 4 * blocks * L.split.NP * kvd::prefill_part_floats(s->head_dim) : 0), 256);
+  L.end = kvd::align_up(L.ctr + (split ? 8 * blocks : 0), 256);
   return L;
 }
 
@@ -492,6 +499,9 @@ kvd_status check_block(const kvd_attn_shape* shape, int32_t d_ff, int32_t B, int
     return fail(KVD_ERR_UNSUPPORTED, "n_q_heads * head_dim must be a multiple of %d", kvd::kKT);
   if (T < 0) return fail(KVD_ERR_SHAPE, "T=%d must be >= 0", T);
   if ((int64_t)B * T > INT32_MAX / 2) return fail(KVD_ERR_SHAPE, "B * T = %lld is too large", (long long)B * T);
+  const kvd::PrefillSplit sp = kvd::prefill_split(B, T, shape->n_q_heads);
+  if ((int64_t)B * shape->n_q_heads * ((T + 127) / 128) * sp.NP > INT32_MAX)
+    return fail(KVD_ERR_SHAPE, "B=%d T=%d n_q_heads=%d: too many attention workgroups", B, T, shape->n_q_heads);
   KVD_TRY(check_lds_bytes(recompute_lds(shape), "kvd_block_forward (projections)"));
   KVD_TRY(check_lds_bytes(kvd::gemm_lds_bytes(std::max(d_ff, shape->n_q_heads * shape->head_dim)),
                           "kvd_block_forward (output projections)"));
@@ -567,6 +577,15 @@ kvd_status kvd_block_forward(const kvd_attn_shape* shape, const kvd_block_weight
   at.T = T;
   at.n_q = shape->n_q_heads;
   at.n_kv = shape->n_kv_heads;
+  at.P = L.split.P;
+  at.NP = L.split.NP;
+  at.q1 = L.split.q1;
+  if (L.split.NP > 1) {
+    at.part = reinterpret_cast<float*>(base + L.part);
+    at.ctr = reinterpret_cast<unsigned long long*>(base + L.ctr);
+    e = kvd::launch_fill_zero_u64(at.ctr, B * shape->n_q_heads * ((T + 127) / 128), st);
+    if (e != hipSuccess) return device_status(e, "kvd_block_forward launch");
+  }
   e = kvd::launch_prefill_attn(at, shape->head_dim, st);
   if (e != hipSuccess) return device_status(e, "kvd_block_forward launch");
   // hhat = h + heads W_o (Eq. attn_sublayer)

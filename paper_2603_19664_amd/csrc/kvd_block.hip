@@ -6,6 +6,8 @@
 // MFMA tile engine with other epilogues, and causal prefill attention.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
+
 #include "kvd_device.hpp"
 #include "kvd_launch.h"
 
@@ -128,23 +130,28 @@ __global__ __launch_bounds__(kNtTile, 1) void gemm_kernel(GemmArgs a, int per_xc
 // LDS of prefill_attn_kernel (bytes): the workgroup's query rows [128][HD + 8],
 // the key tile [64][HD + 8] and the value tile transposed [HD][64 + 8], bf16.
 struct PrefillLds {
-  size_t qs, ks, vt, end;
+  size_t qs, ks, vt, ctr, end;
 };
 constexpr PrefillLds prefill_lds(int hd) {
   PrefillLds L{};
   L.qs = 0;
   L.ks = L.qs + (size_t)2 * 128 * (hd + 8);
   L.vt = L.ks + (size_t)2 * 64 * (hd + 8);
-  L.end = L.vt + (size_t)2 * hd * (64 + 8);
+  L.ctr = L.vt + (size_t)2 * hd * (64 + 8);  // split counter broadcast
+  L.end = L.ctr + 16;
   return L;
 }
 
-// grid: xcd_map(B * n_q * nqb) workgroups, nqb = ceil(T / 128), 256 threads (4
-// waves).  Items are ordered (sequence, KV head, query block from the last,
-// query head of the group), so an XCD's workgroups share one KV head's keys and
-// values in its L2 and the longest rows start first.  A workgroup takes 128 query
-// rows of one head, 32 per wave, through the key blocks of 64 up to its last row
-// (flash order), loading block kb + 1 into registers while block kb is computed.
+// grid: B * n_q * nqb * NP workgroups, nqb = ceil(T / 128), 256 threads (4
+// waves), item = blockIdx.x.  Items are ordered (query block rank, key part,
+// sequence, KV head, query head of the group): the ranks take the unsplit
+// blocks first, then the split ones, each from the last (the longest) down,
+// which starts the longest pieces of work first; consecutive items go to
+// different XCDs, so every XCD gets its share of each rank.  A workgroup takes
+// 128 query rows of one head, 32 per wave, through the key blocks of 64 of its
+// part of the range up to its last row (flash order), loading block kb + 1 into
+// registers while block kb is computed; items past their block's part count
+// exit at once.
 //
 // Scores are computed transposed, S^T = K Q^T: A = 32 keys from the LDS tile,
 // B = the wave's 32 query rows (registers), so that a lane holds one query's
@@ -157,7 +164,7 @@ constexpr PrefillLds prefill_lds(int hd) {
 // operand takes the same keys, so both operands agree on the reduction order.
 // Scores are in the log2 domain (log2(e) / sqrt(hd) folded into the scale).
 template <int HD>
-__global__ __launch_bounds__(256) void prefill_attn_kernel(PrefillArgs a, int per_xcd) {
+__global__ __launch_bounds__(256) void prefill_attn_kernel(PrefillArgs a) {
   extern __shared__ __align__(16) char lds[];
   constexpr PrefillLds PL = prefill_lds(HD);
   constexpr int KS = HD / 16;              // 16-wide k-steps of a score block
@@ -175,14 +182,23 @@ __global__ __launch_bounds__(256) void prefill_attn_kernel(PrefillArgs a, int pe
   const int nqb = (a.T + 127) / 128;
   const int g = a.n_q / a.n_kv;
   // 32-bit index arithmetic: the launch's grid bounds the item count
-  const unsigned item = (blockIdx.x % kXcds) * (unsigned)per_xcd + blockIdx.x / kXcds;
-  if (item >= (unsigned)a.B * (unsigned)a.n_q * (unsigned)nqb) return;
+  const unsigned item = blockIdx.x;
   const int hh = (int)(item % (unsigned)g);
-  const unsigned r1 = item / (unsigned)g;
-  const int qb = nqb - 1 - (int)(r1 % (unsigned)nqb);  // the longest rows first
-  const unsigned r2 = r1 / (unsigned)nqb;
-  const int j = (int)(r2 % (unsigned)a.n_kv), b = (int)(r2 / (unsigned)a.n_kv);
+  const unsigned r0 = item / (unsigned)g;
+  const unsigned bj = (unsigned)a.B * (unsigned)a.n_kv;
+  const int j = (int)(r0 % (unsigned)a.n_kv);
+  const int b = (int)((r0 / (unsigned)a.n_kv) % (unsigned)a.B);
+  const unsigned r1 = r0 / bj;
+  const int part = (int)(r1 % (unsigned)a.NP);
+  const int rank = (int)(r1 / (unsigned)a.NP);
+  if (rank >= nqb) return;
+  const int qb = rank < a.q1 ? a.q1 - 1 - rank : nqb - 1 - (rank - a.q1);
   const int h = j * g + hh;
+  const int last_row = min(128 * qb + 127, a.T - 1);
+  const int nkb = last_row / 64 + 1;        // key blocks 0 .. nkb - 1 reach this block's rows
+  const int np = (nkb + a.P - 1) / a.P;     // parts of the key range
+  if (part >= np) return;
+  const int kb0 = part * nkb / np, kb1 = (part + 1) * nkb / np;
   const int q0 = 128 * qb + 32 * w;          // this wave's first query row
   const int query = q0 + (lane & 31);        // this lane's query row
   const float scale = ScoreScale<HD>::v;
@@ -224,11 +240,9 @@ __global__ __launch_bounds__(256) void prefill_attn_kernel(PrefillArgs a, int pe
       }
     }
   };
-  const int last_row = min(128 * qb + 127, a.T - 1);
-  const int nkb = last_row / 64 + 1;  // key blocks 0 .. nkb - 1
-  load_kv(0);
+  load_kv(kb0);
 
-  for (int kb = 0; kb < nkb; ++kb) {
+  for (int kb = kb0; kb < kb1; ++kb) {
     // the registers into LDS: K as is, V transposed ([column][key])
 #pragma unroll
     for (int i = 0; i < KCH; ++i) {
@@ -248,7 +262,7 @@ __global__ __launch_bounds__(256) void prefill_attn_kernel(PrefillArgs a, int pe
       }
     }
     __syncthreads();
-    if (kb + 1 < nkb) load_kv(kb + 1);  // in flight while this block is computed
+    if (kb + 1 < kb1) load_kv(kb + 1);  // in flight while this block is computed
 
     // a wave whose rows all precede the block (or lie past T) skips it
     if (64 * kb <= q0 + 31 && q0 < a.T) {
@@ -334,6 +348,70 @@ __global__ __launch_bounds__(256) void prefill_attn_kernel(PrefillArgs a, int pe
     __syncthreads();
   }
 
+  if (np > 1) {
+    // This part's state into its slot (per wave: O as [db][r][lane], then the
+    // lane's max and sum), then the arrival; the last part merges every part's
+    // state in part order, so the result does not depend on which part arrives
+    // last.
+    constexpr size_t PF = 4 * (DB * 16 * 64 + 128);
+    const size_t blk = ((size_t)b * a.n_q + h) * nqb + qb;
+    float* slots = a.part + blk * a.NP * PF;
+    {
+      float* so = slots + (size_t)part * PF + (size_t)w * DB * 16 * 64 + lane;
+#pragma unroll
+      for (int db = 0; db < DB; ++db)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) store_dev(so + (db * 16 + r) * 64, o[db][r]);
+      float* sm = slots + (size_t)part * PF + 4 * DB * 16 * 64 + w * 128 + lane;
+      store_dev(sm, m_run);
+      store_dev(sm + 64, l_run);
+    }
+    unsigned long long* ctr = a.ctr + blk;
+    const unsigned long long before =
+        split_arrive(ctr, 1, reinterpret_cast<unsigned long long*>(lds + PL.ctr));
+    if (!split_complete(ctr, before, 1, np)) return;
+    // O = sum over parts p (in order) of 2^(m_p - M) O_p, the same for l; this
+    // part's own values come from its registers (they equal what it stored).
+    // The other parts' values are read in batches of 32 ahead of their use, so
+    // that their round trips overlap.
+    const float* sml = slots + 4 * DB * 16 * 64 + w * 128 + lane;
+    float M = m_run;
+    for (int p2 = 0; p2 < np; ++p2)
+      if (p2 != part) M = fmaxf(M, load_dev(sml + (size_t)p2 * PF));
+    float L = 0.0f;
+    for (int p2 = 0; p2 < np; ++p2) {
+      const float mq = p2 == part ? m_run : load_dev(sml + (size_t)p2 * PF);
+      const float lq = p2 == part ? l_run : load_dev(sml + (size_t)p2 * PF + 64);
+      L = fmaf(lq, exp2f(mq - M), L);
+    }
+    l_run = L;
+    const float w_own = exp2f(m_run - M);
+#pragma unroll
+    for (int db = 0; db < DB; db += 2) {
+      float acc[32];
+#pragma unroll
+      for (int i = 0; i < 32; ++i) acc[i] = 0.0f;
+      for (int p2 = 0; p2 < np; ++p2) {
+        float x[32];
+        float wq;
+        if (p2 == part) {
+#pragma unroll
+          for (int i = 0; i < 32; ++i) x[i] = o[db + (i >> 4)][i & 15];
+          wq = w_own;
+        } else {
+          const float* so = slots + (size_t)p2 * PF + (size_t)w * DB * 16 * 64 + (size_t)db * 16 * 64 + lane;
+#pragma unroll
+          for (int i = 0; i < 32; ++i) x[i] = load_dev(so + i * 64);
+          wq = exp2f(load_dev(sml + (size_t)p2 * PF) - M);
+        }
+#pragma unroll
+        for (int i = 0; i < 32; ++i) acc[i] = fmaf(x[i], wq, acc[i]);
+      }
+#pragma unroll
+      for (int i = 0; i < 32; ++i) o[db + (i >> 4)][i & 15] = acc[i];
+    }
+  }
+
   // out = O / l, one RNE rounding: lane = query, rows = dims 32 db + 8 (r / 4) + 4 hl + r % 4
   if (query < a.T) {
     const float inv = 1.0f / l_run;
@@ -353,6 +431,11 @@ __global__ __launch_bounds__(256) void prefill_attn_kernel(PrefillArgs a, int pe
 __global__ void fill_ones_kernel(uint16_t* dst, int n) {
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
   if (i < n) dst[i] = 0x3f80;  // 1.0 in bf16
+}
+
+__global__ void fill_zero_u64_kernel(unsigned long long* dst, int n) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) dst[i] = 0ull;
 }
 
 // ------------------------------------------------------------------ launchers
@@ -396,10 +479,36 @@ static hipError_t prefill_t(const PrefillArgs& a, hipStream_t st) {
   auto k = prefill_attn_kernel<HD>;
   hipError_t e = set_lds_once(k, bytes, done);
   if (e != hipSuccess) return e;
-  const XcdMap m = xcd_map((long long)a.B * a.n_q * ((a.T + 127) / 128));
-  hipLaunchKernelGGL(k, dim3(m.grid), dim3(256), bytes, st, a, m.per);
+  const long long items = (long long)a.B * a.n_q * ((a.T + 127) / 128) * a.NP;
+  hipLaunchKernelGGL(k, dim3((unsigned)items), dim3(256), bytes, st, a);
   return hipGetLastError();
 }
+
+// The split aims at about kPrefillTargetCus workgroups' worth of equal work:
+// P = max(8, ceil(total key blocks / target)) key blocks per part, so a launch
+// whose blocks already fill the chip (long batches, many heads) splits nothing.
+constexpr long long kPrefillTargetCus = 256;
+PrefillSplit prefill_split(int B, int T, int n_q) {
+  const int nqb = (T + 127) / 128;
+  PrefillSplit sp{1, 1, nqb};
+  if (B <= 0 || T <= 0) return sp;
+  long long per_head = 0;
+  for (int qb = 0; qb < nqb; ++qb) per_head += std::min(128LL * qb + 127, (long long)T - 1) / 64 + 1;
+  const long long total = per_head * B * n_q;
+  const long long P = std::max(8LL, (total + kPrefillTargetCus - 1) / kPrefillTargetCus);
+  const long long nkb_max = (long long)(T - 1) / 64 + 1;
+  sp.P = (int)std::min<long long>(P, nkb_max);
+  sp.NP = (int)((nkb_max + sp.P - 1) / sp.P);
+  // parts per block grow with the block's key count: the first block with two
+  for (int qb = 0; qb < nqb; ++qb)
+    if (std::min(128LL * qb + 127, (long long)T - 1) / 64 + 1 > sp.P) {
+      sp.q1 = qb;
+      break;
+    }
+  return sp;
+}
+
+size_t prefill_part_floats(int hd) { return (size_t)4 * ((hd / 32) * 16 * 64 + 128); }
 
 size_t prefill_lds_bytes(int hd) { return prefill_lds(hd).end; }
 size_t gemm_lds_bytes(int K) { return proj_lds<uint16_t>(256, kMtBf16).end + gamma_lds_bytes(K); }
@@ -414,6 +523,12 @@ hipError_t launch_prefill_attn(const PrefillArgs& a, int hd, hipStream_t st) {
 
 hipError_t launch_fill_ones_bf16(void* dst, int n, hipStream_t st) {
   hipLaunchKernelGGL(fill_ones_kernel, dim3((n + 255) / 256), dim3(256), 0, st, static_cast<uint16_t*>(dst), n);
+  return hipGetLastError();
+}
+
+hipError_t launch_fill_zero_u64(void* dst, int n, hipStream_t st) {
+  hipLaunchKernelGGL(fill_zero_u64_kernel, dim3((n + 255) / 256), dim3(256), 0, st,
+                     static_cast<unsigned long long*>(dst), n);
   return hipGetLastError();
 }
 

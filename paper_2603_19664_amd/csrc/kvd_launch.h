@@ -94,17 +94,35 @@ hipError_t launch_gemm(const GemmArgs& a, int epi, int packed, hipStream_t st);
 // Causal prefill attention (bf16): out[b][t][h*hd .. h*hd+hd-1] = sum over keys
 // j <= t of softmax_j(q[b][t][h] . K[b][h/g][j] / sqrt(hd)) V[b][h/g][j].
 //   q [B][T][n_q][hd]; K, V [B][n_kv][T][hd]; out [B][T][n_q * hd].
+// Query block qb (rows 128 qb ..) attends nkb = last row / 64 + 1 key blocks of
+// 64.  When the blocks are too few and too unequal to fill the chip, a block's
+// key range is split into np = ceil(nkb / P) parts of near-equal length, one
+// workgroup each; the parts' states (unnormalised O, running max and sum) meet in
+// `part`, and the last part to arrive (counter in `ctr`, zero before the launch)
+// merges them in part order.  P and NP (the most parts of any block) come from
+// prefill_split; with NP == 1 nothing is split and part / ctr are unused.
 struct PrefillArgs {
   const void* q;
   const void* k;
   const void* v;
   void* out;
   int B, T, n_q, n_kv;
+  int P, NP;
+  int q1;                    // first query block with more than one part (nqb if none)
+  float* part;               // [B][n_q][nqb][NP][prefill_part_floats(hd)]
+  unsigned long long* ctr;   // [B][n_q][nqb]
 };
+struct PrefillSplit {
+  int P, NP, q1;
+};
+PrefillSplit prefill_split(int B, int T, int n_q);
+size_t prefill_part_floats(int hd);
 hipError_t launch_prefill_attn(const PrefillArgs& a, int hd, hipStream_t st);
 
 // dst[i] = 1.0 (bf16) for i < n.
 hipError_t launch_fill_ones_bf16(void* dst, int n, hipStream_t st);
+// dst[i] = 0 (64-bit words) for i < n.
+hipError_t launch_fill_zero_u64(void* dst, int n, hipStream_t st);
 // LDS bytes of the two block-forward kernels (for host-side validation).
 size_t gemm_lds_bytes(int K);
 size_t prefill_lds_bytes(int hd);

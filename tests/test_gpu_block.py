@@ -152,3 +152,18 @@ def test_block_causality_on_gpu():
     b = M.forward(h2, pos0, 1)
     assert torch.equal(a[:, :100].view(torch.int16), b[:, :100].view(torch.int16))
     assert not torch.equal(a[:, 100:], b[:, 100:])
+
+
+@pytest.mark.parametrize("hd,T", [(256, 1100), (128, 777), (256, 2049)])
+def test_block_forward_split_key_ranges(hd, T):
+    # one sequence of several hundred positions: the causal attention splits the
+    # longer query blocks' key ranges over workgroups and merges the parts
+    wl = _wl(hd)
+    M = Model(wl, 1, d_ff=512, packed=True, seed=hd + T)
+    h, pos0 = _inputs(wl, 1, T, seed=T)
+    out = M.forward(h, pos0, 1)
+    ref = _oracle(M, h, pos0, 1)
+    _check("h_out", f64(out), ref)
+    _check("h_out - h_in (what the block adds)", f64(out) - f64(h), ref - f64(h), _delta_tol(h, ref, 1))
+    again = M.forward(h, pos0, 1)  # the merge order is fixed: the same bits on every run
+    assert torch.equal(out.view(torch.int16), again.view(torch.int16))
