@@ -500,7 +500,7 @@ kvd_status check_block(const kvd_attn_shape* shape, int32_t d_ff, int32_t B, int
   if (T < 0) return fail(KVD_ERR_SHAPE, "T=%d must be >= 0", T);
   if ((int64_t)B * T > INT32_MAX / 2) return fail(KVD_ERR_SHAPE, "B * T = %lld is too large", (long long)B * T);
   const kvd::PrefillSplit sp = kvd::prefill_split(B, T, shape->n_q_heads);
-  if ((int64_t)B * shape->n_q_heads * ((T + 127) / 128) * sp.NP > INT32_MAX)
+  if ((int64_t)B * shape->n_q_heads * (sp.n_order > 0 ? sp.n_order : (T + 127) / 128) > INT32_MAX)
     return fail(KVD_ERR_SHAPE, "B=%d T=%d n_q_heads=%d: too many attention workgroups", B, T, shape->n_q_heads);
   KVD_TRY(check_lds_bytes(recompute_lds(shape), "kvd_block_forward (projections)"));
   KVD_TRY(check_lds_bytes(kvd::gemm_lds_bytes(std::max(d_ff, shape->n_q_heads * shape->head_dim)),
@@ -579,7 +579,8 @@ kvd_status kvd_block_forward(const kvd_attn_shape* shape, const kvd_block_weight
   at.n_kv = shape->n_kv_heads;
   at.P = L.split.P;
   at.NP = L.split.NP;
-  at.q1 = L.split.q1;
+  at.n_order = L.split.n_order;
+  std::copy(L.split.order, L.split.order + L.split.n_order, at.order);
   if (L.split.NP > 1) {
     at.part = reinterpret_cast<float*>(base + L.part);
     at.ctr = reinterpret_cast<unsigned long long*>(base + L.ctr);

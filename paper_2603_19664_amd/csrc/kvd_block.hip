@@ -142,16 +142,15 @@ constexpr PrefillLds prefill_lds(int hd) {
   return L;
 }
 
-// grid: B * n_q * nqb * NP workgroups, nqb = ceil(T / 128), 256 threads (4
-// waves), item = blockIdx.x.  Items are ordered (query block rank, key part,
-// sequence, KV head, query head of the group): the ranks take the unsplit
-// blocks first, then the split ones, each from the last (the longest) down,
-// which starts the longest pieces of work first; consecutive items go to
-// different XCDs, so every XCD gets its share of each rank.  A workgroup takes
-// 128 query rows of one head, 32 per wave, through the key blocks of 64 of its
-// part of the range up to its last row (flash order), loading block kb + 1 into
-// registers while block kb is computed; items past their block's part count
-// exit at once.
+// grid: (pieces of one head) * B * n_q workgroups, 256 threads (4 waves), item =
+// blockIdx.x.  A piece is a (query block, key part) pair; the host lists them
+// longest first (order), and items run (piece rank, sequence, KV head, query head
+// of the group), so the longest pieces start first and consecutive items go to
+// different XCDs, which gives every XCD its share of each rank.  Without a list
+// (too many blocks, then nothing is split) rank r is query block nqb - 1 - r.  A
+// workgroup takes 128 query rows of one head, 32 per wave, through the key
+// blocks of 64 of its part of the range up to its last row (flash order),
+// loading block kb + 1 into registers while block kb is computed.
 //
 // Scores are computed transposed, S^T = K Q^T: A = 32 keys from the LDS tile,
 // B = the wave's 32 query rows (registers), so that a lane holds one query's
@@ -188,16 +187,13 @@ __global__ __launch_bounds__(256) void prefill_attn_kernel(PrefillArgs a) {
   const unsigned bj = (unsigned)a.B * (unsigned)a.n_kv;
   const int j = (int)(r0 % (unsigned)a.n_kv);
   const int b = (int)((r0 / (unsigned)a.n_kv) % (unsigned)a.B);
-  const unsigned r1 = r0 / bj;
-  const int part = (int)(r1 % (unsigned)a.NP);
-  const int rank = (int)(r1 / (unsigned)a.NP);
-  if (rank >= nqb) return;
-  const int qb = rank < a.q1 ? a.q1 - 1 - rank : nqb - 1 - (rank - a.q1);
+  const int rank = (int)(r0 / bj);
+  const unsigned piece = a.n_order > 0 ? a.order[rank] : (unsigned)(nqb - 1 - rank) << 8;
+  const int qb = (int)(piece >> 8), part = (int)(piece & 255u);
   const int h = j * g + hh;
   const int last_row = min(128 * qb + 127, a.T - 1);
   const int nkb = last_row / 64 + 1;        // key blocks 0 .. nkb - 1 reach this block's rows
   const int np = (nkb + a.P - 1) / a.P;     // parts of the key range
-  if (part >= np) return;
   const int kb0 = part * nkb / np, kb1 = (part + 1) * nkb / np;
   const int q0 = 128 * qb + 32 * w;          // this wave's first query row
   const int query = q0 + (lane & 31);        // this lane's query row
@@ -479,7 +475,8 @@ static hipError_t prefill_t(const PrefillArgs& a, hipStream_t st) {
   auto k = prefill_attn_kernel<HD>;
   hipError_t e = set_lds_once(k, bytes, done);
   if (e != hipSuccess) return e;
-  const long long items = (long long)a.B * a.n_q * ((a.T + 127) / 128) * a.NP;
+  const long long pieces = a.n_order > 0 ? a.n_order : (a.T + 127) / 128;
+  const long long items = (long long)a.B * a.n_q * pieces;
   hipLaunchKernelGGL(k, dim3((unsigned)items), dim3(256), bytes, st, a);
   return hipGetLastError();
 }
@@ -489,22 +486,40 @@ static hipError_t prefill_t(const PrefillArgs& a, hipStream_t st) {
 // whose blocks already fill the chip (long batches, many heads) splits nothing.
 constexpr long long kPrefillTargetCus = 256;
 PrefillSplit prefill_split(int B, int T, int n_q) {
-  const int nqb = (T + 127) / 128;
-  PrefillSplit sp{1, 1, nqb};
+  PrefillSplit sp{};
+  sp.P = 1;
+  sp.NP = 1;
   if (B <= 0 || T <= 0) return sp;
+  const int nqb = (T + 127) / 128;
+  auto nkb = [&](int qb) { return (int)(std::min(128LL * qb + 127, (long long)T - 1) / 64 + 1); };
   long long per_head = 0;
-  for (int qb = 0; qb < nqb; ++qb) per_head += std::min(128LL * qb + 127, (long long)T - 1) / 64 + 1;
+  for (int qb = 0; qb < nqb; ++qb) per_head += nkb(qb);
   const long long total = per_head * B * n_q;
-  const long long P = std::max(8LL, (total + kPrefillTargetCus - 1) / kPrefillTargetCus);
-  const long long nkb_max = (long long)(T - 1) / 64 + 1;
-  sp.P = (int)std::min<long long>(P, nkb_max);
+  const long long nkb_max = nkb(nqb - 1);
+  sp.P = (int)std::min<long long>(std::max(8LL, (total + kPrefillTargetCus - 1) / kPrefillTargetCus), nkb_max);
   sp.NP = (int)((nkb_max + sp.P - 1) / sp.P);
-  // parts per block grow with the block's key count: the first block with two
-  for (int qb = 0; qb < nqb; ++qb)
-    if (std::min(128LL * qb + 127, (long long)T - 1) / 64 + 1 > sp.P) {
-      sp.q1 = qb;
-      break;
+  // the pieces of one head, longest first (ties: the later block first)
+  struct Piece {
+    int len, qb, part;
+  };
+  Piece pc[kPrefillOrderMax];
+  int n = 0;
+  for (int qb = nqb - 1; qb >= 0; --qb) {
+    const int nk = nkb(qb), np = (nk + sp.P - 1) / sp.P;
+    for (int p = 0; p < np; ++p) {
+      if (n == kPrefillOrderMax || sp.NP > 255) {
+        // too many pieces to list: no split, blocks from the last
+        sp.P = (int)nkb_max;
+        sp.NP = 1;
+        sp.n_order = 0;
+        return sp;
+      }
+      pc[n++] = Piece{(p + 1) * nk / np - p * nk / np, qb, p};
     }
+  }
+  std::stable_sort(pc, pc + n, [](const Piece& x, const Piece& y) { return x.len > y.len; });
+  sp.n_order = n;
+  for (int i = 0; i < n; ++i) sp.order[i] = ((unsigned)pc[i].qb << 8) | (unsigned)pc[i].part;
   return sp;
 }
 

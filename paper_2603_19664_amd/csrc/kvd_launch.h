@@ -101,6 +101,12 @@ hipError_t launch_gemm(const GemmArgs& a, int epi, int packed, hipStream_t st);
 // `part`, and the last part to arrive (counter in `ctr`, zero before the launch)
 // merges them in part order.  P and NP (the most parts of any block) come from
 // prefill_split; with NP == 1 nothing is split and part / ctr are unused.
+constexpr int kPrefillOrderMax = 256;
+struct PrefillSplit {
+  int P, NP;
+  int n_order;  // entries of order (0: too many; rank r is then query block nqb - 1 - r, part 0, unsplit)
+  unsigned order[kPrefillOrderMax];  // (qb << 8) | part, longest part first
+};
 struct PrefillArgs {
   const void* q;
   const void* k;
@@ -108,12 +114,10 @@ struct PrefillArgs {
   void* out;
   int B, T, n_q, n_kv;
   int P, NP;
-  int q1;                    // first query block with more than one part (nqb if none)
   float* part;               // [B][n_q][nqb][NP][prefill_part_floats(hd)]
   unsigned long long* ctr;   // [B][n_q][nqb]
-};
-struct PrefillSplit {
-  int P, NP, q1;
+  int n_order;
+  unsigned order[kPrefillOrderMax];
 };
 PrefillSplit prefill_split(int B, int T, int n_q);
 size_t prefill_part_floats(int hd);
