@@ -112,6 +112,8 @@ def test_fused_validation():
     assert fused(s, ws_bytes=100) == kvd.KVD_ERR_WORKSPACE
     assert fused(s, dbg=view(t_cap=10)) == kvd.KVD_ERR_SHAPE
     assert fused(s, B=70000) == kvd.KVD_ERR_SHAPE
+    # one workgroup per (KV head, sequence, split) must stay below 2^31
+    assert fused(s, B=65535, T_rec=600000, h_ld=600000) == kvd.KVD_ERR_SHAPE
     assert lib.kvd_fused_recompute_attn(ctypes.byref(s), FAKE, FAKE, 64, FAKE, FAKE, FAKE, FAKE, 1, 64, None, 1,
                                         FAKE, FAKE, 1 << 30, None, None) == kvd.KVD_ERR_NULL
 
@@ -239,6 +241,30 @@ def test_block_forward_validation():
     parts = [2 * 200 * qd, 2 * 200 * kvd_, 2 * 200 * kvd_, 2 * 200 * qd, 2 * 200 * 1024, 2 * 200 * 1024, 2 * 1024]
     assert n == sum(-(-p // 256) * 256 for p in parts)
     assert lib.kvd_block_workspace_bytes(ctypes.byref(s), 100, 2, 100) == 0
+
+
+def _prefill_split(B, T, n_q, target=256):
+    # the causal attention's key-range split (host policy): parts of at most P key blocks
+    nqb = -(-T // 128)
+    nkb = [min(128 * qb + 127, T - 1) // 64 + 1 for qb in range(nqb)]
+    P = min(max(8, -(-sum(nkb) * B * n_q // target)), nkb[-1])
+    return P, -(-nkb[-1] // P), nqb
+
+
+@pytest.mark.parametrize("B,T", [(1, 4096), (1, 1100), (2, 777), (8, 4096), (1, 100)])
+def test_block_workspace_holds_the_attention_split(B, T):
+    s = shape(d_model=1024, n_q_heads=8, n_kv_heads=4, head_dim=128)
+    qd, kvd_, dff = 8 * 128, 4 * 128, 1024
+    bt = B * T
+    parts = [2 * bt * qd, 2 * bt * kvd_, 2 * bt * kvd_, 2 * bt * qd, 2 * bt * 1024, 2 * bt * dff, 2 * 1024]
+    P, NP, nqb = _prefill_split(B, T, 8)
+    if NP > 1:  # partial states (4 waves x (32 x 128 O + 128 max/sum) floats) and one counter per query block
+        parts += [4 * B * 8 * nqb * NP * 4 * (4 * 16 * 64 + 128), 8 * B * 8 * nqb]
+    assert lib.kvd_block_workspace_bytes(ctypes.byref(s), dff, B, T) == sum(-(-p // 256) * 256 for p in parts)
+    if (B, T) == (1, 4096):
+        assert (P, NP) == (33, 2)
+    if (B, T) == (8, 4096):
+        assert NP == 1  # enough blocks to fill the chip: nothing split
 
 
 def test_pack_matrix_validation():
