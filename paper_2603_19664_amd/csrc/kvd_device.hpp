@@ -726,15 +726,17 @@ __device__ __forceinline__ void move_rows(T* kv, int from, int to, int n) {
 
 // Softmax partial state of one tile of up to 64 * KPL keys (rows of `kv`: K in
 // columns [0, HD), V in [HD, 2 HD)) for the g query heads of one KV head, from
-// the pre-scaled q in LDS: ml = (max, sum of exp2) per head, acc = sum of
-// exp2(s - max) V (Eqs. attn_weights / head_output, restricted to the tile).
+// the pre-scaled q in LDS: ml = (max, sum of exp2) per head, and in `red` the
+// attn_ts(g) key splits' sums of exp2(s - max) V, whose sum in split order
+// (added by write_partial) is the tile's output (Eqs. attn_weights /
+// head_output, restricted to the tile).
 // Work is split into wave-level tasks whose count depends on g and head_dim
 // only, never on the thread count, so every kernel that attends a tile performs
 // the same additions in the same order.
 //  1. partial scores: task (head h, 64-dim part p), lane = key (and key + 64);
 //  2. per head: parts summed in order, max, exp2, sum (one wave per head);
 //  3. P V: task (head h, key split ts of attn_ts(g)), lane = head_dim / 64
-//     consecutive output columns; the key splits are then summed in order.
+//     consecutive output columns.
 // For n <= 64 the second key slot adds exact zeros (max with -inf, sum with
 // 0), so KPL = 1 and KPL = 2 give bit-identical results.  rows >= n is the
 // stride of the probabilities in LDS.
@@ -750,7 +752,6 @@ __device__ __forceinline__ void attend_tile(const T* kv, int n, int rows, int g,
   float* S = reinterpret_cast<float*>(lds + L.s);
   float* red = reinterpret_cast<float*>(lds + L.red);
   float* ml = reinterpret_cast<float*>(lds + L.ml);
-  float* acc = reinterpret_cast<float*>(lds + L.acc);
 
   static_assert(KPL == 1 || KPL == 2, "keys per lane");
   for (int kk = 0; kk < KPL && 64 * kk < n; ++kk) {  // key slot: keys 64 kk + lane
@@ -849,12 +850,6 @@ __device__ __forceinline__ void attend_tile(const T* kv, int n, int rows, int g,
     for (int e = 0; e < E; ++e) dst[e] = a[e];
   }
   __syncthreads();
-  for (int idx = tid; idx < g * HD; idx += NT) {
-    float s = 0.0f;
-    for (int ts = 0; ts < TS; ++ts) s += red[(size_t)ts * g * HD + idx];
-    acc[idx] = s;
-  }
-  __syncthreads();
 }
 
 // Device-scope (coherent across the XCDs' L2 caches) 32-bit store / load: the
@@ -868,15 +863,20 @@ __device__ __forceinline__ float load_dev(const float* p) {
 }
 
 // Split-K partial of (b, KV head j, split s) into the workspace:
-// acc [B][n_q][S][HD] fp32 followed by ml [B][n_q][S][2] fp32.
+// acc [B][n_q][S][HD] fp32 followed by ml [B][n_q][S][2] fp32.  The tile's
+// output is the sum, in key-split order, of attend_tile's attn_ts(g) P V
+// partial sums in `red`; it is added here as it is written out.
 template <int HD, int NT>
 __device__ __forceinline__ void write_partial(const char* lds, const AttnLds& L, float* ws_acc, float* ws_ml, int b,
                                               int n_q, int j, int g, int S, int s) {
-  const float* acc = reinterpret_cast<const float*>(lds + L.acc);
+  const float* red = reinterpret_cast<const float*>(lds + L.red);
   const float* ml = reinterpret_cast<const float*>(lds + L.ml);
+  const int TS = attn_ts(g);
   for (int i = threadIdx.x; i < g * HD; i += NT) {
     const int h = i / HD, c = i - h * HD;
-    store_dev(ws_acc + (((size_t)b * n_q + (size_t)j * g + h) * S + s) * HD + c, acc[i]);
+    float o = 0.0f;
+    for (int ts = 0; ts < TS; ++ts) o += red[(size_t)ts * g * HD + i];
+    store_dev(ws_acc + (((size_t)b * n_q + (size_t)j * g + h) * S + s) * HD + c, o);
   }
   if (threadIdx.x < 2 * g) {
     const int h = threadIdx.x >> 1;

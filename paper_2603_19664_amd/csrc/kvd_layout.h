@@ -66,7 +66,7 @@ constexpr int h_ld(void) { return kKT + Pad<T>::h; }
 
 // LDS layout of the attention part (decode / fused kernels); g = group size.
 struct AttnLds {
-  size_t q, s, red, ml, acc, cmb, ctr, end;
+  size_t q, s, red, ml, cmb, ctr, end;
 };
 // Split merge (combine_rows): blocks of 64 splits; the (max, sum) pairs of the
 // first kCmbKeep blocks stay in registers.  LDS floats: rows-per-pass x (64
@@ -83,17 +83,16 @@ constexpr size_t red_floats(int g, int hd, int rows) {
   const size_t pv = (size_t)attn_ts(g) * g * hd;
   return sc > pv ? sc : pv;
 }
-// q, probabilities, the scratch `red` (scores, then P V partial sums), (max,
-// sum), the split counter's broadcast.  The tile's output `acc` is the first
-// slice of `red` (its final sum reads every slice of a column before writing
-// it), and the split merge, which runs after all tiles, reuses `red` as well.
+// q, probabilities, the scratch `red` (scores, then the key splits' P V
+// partial sums, which write_partial adds as it writes the tile's output), (max,
+// sum), the split counter's broadcast.  The split merge, which runs after all
+// tiles, reuses `red` as well.
 __attribute__((always_inline)) constexpr AttnLds attn_lds(size_t base, int g, int hd, int rows) {
   AttnLds L{};
   L.q = align_up(base, 16);
   L.s = align_up(L.q + sizeof(float) * g * hd, 16);
   L.red = align_up(L.s + sizeof(float) * g * rows, 16);
   const size_t rf = red_floats(g, hd, rows), cf = cmb_floats(512, hd);
-  L.acc = L.red;
   L.cmb = L.red;
   L.ml = align_up(L.red + sizeof(float) * (rf > cf ? rf : cf), 16);
   L.ctr = align_up(L.ml + sizeof(float) * 2 * g, 16);  // split counter broadcast
