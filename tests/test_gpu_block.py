@@ -154,13 +154,13 @@ def test_block_causality_on_gpu():
     assert not torch.equal(a[:, 100:], b[:, 100:])
 
 
-@pytest.mark.parametrize("hd,T", [(256, 1100), (128, 777), (256, 2049)])
-def test_block_forward_split_key_ranges(hd, T):
-    # one sequence of several hundred positions: the causal attention splits the
+@pytest.mark.parametrize("hd,T,B", [(256, 1100, 1), (128, 777, 1), (256, 2049, 1), (128, 777, 2)])
+def test_block_forward_split_key_ranges(hd, T, B):
+    # sequences of several hundred positions: the causal attention splits the
     # longer query blocks' key ranges over workgroups and merges the parts
     wl = _wl(hd)
     M = Model(wl, 1, d_ff=512, packed=True, seed=hd + T)
-    h, pos0 = _inputs(wl, 1, T, seed=T)
+    h, pos0 = _inputs(wl, B, T, seed=T)
     out = M.forward(h, pos0, 1)
     ref = _oracle(M, h, pos0, 1)
     _check("h_out", f64(out), ref)
