@@ -138,8 +138,21 @@ kvd_status kvd_project_qkv(const kvd_attn_shape* shape, const void* h_new, const
                            const int32_t* pos, int32_t B, void* q_out,
                            const kvd_kv_view* kv_out, void* stream);
 
+/* The query projection alone (Sec. 3.1, Eq. q_proj; Algorithm 1's Q):
+ *   q_out[b][h] = RoPE(hbar W_q^(h), pos[b]),  hbar = RMSNorm(h_new[b]).
+ * The same call as kvd_project_qkv with kv_out == NULL (w_k / w_v unused), with
+ * the argument list of the plain problem statement.
+ *   h_new [B][d_model].   pos [B] int32.   q_out [B][n_q_heads][head_dim].   */
+kvd_status kvd_project_q(const kvd_attn_shape* shape, const void* h_new, const void* gamma,
+                         const void* w_q, const int32_t* pos, int32_t B, void* q_out, void* stream);
+
 /* ATTENTION for one decode query per sequence and head (Eqs. attn_weights,
  * head_output) over T >= 1 stored keys: rows kv->t_off .. kv->t_off+T-1.
+ * bf16: the keys of each (sequence, KV head) are cut into kvd_num_splits
+ * contiguous ranges (about kvd_set_attn_workgroups workgroups over the call),
+ * each streamed by one workgroup that keeps its next 16-key block's loads in
+ * flight (HBM-bound: the read is Eq. read_bytes).  fp32: one split per
+ * 64-key tile.
  * Split-K: partial softmax states go to the workspace; the workgroup that
  * writes the last partial of a (sequence, KV head) merges them into out in the
  * same kernel (an atomic split counter in the workspace; no spin-waits).
@@ -296,6 +309,16 @@ size_t kvd_workspace_bytes(const kvd_attn_shape* shape, int32_t op, int32_t B, i
 /* Number of split-K partitions an attention call uses (0 on invalid arguments). */
 int32_t kvd_num_splits(const kvd_attn_shape* shape, int32_t op, int32_t B, int32_t T_main,
                        int32_t T_tail);
+
+/* Tuning of the bf16 stored-K/V attention (kvd_decode_attn, kvd_cached_attn):
+ * the number of workgroups its split policy aims for over the whole call
+ * (B * n_kv_heads * splits; default 256, one per MI355X compute unit;
+ * target <= 0 restores the default).  Returns the previous value.  The setting
+ * is process-wide and changes kvd_num_splits / kvd_workspace_bytes of those
+ * ops: query workspace sizes after setting it, and do not change it while
+ * calls that share a workspace are in flight.  Results are exact for every
+ * setting (only the key ranges of the splits move).                          */
+int32_t kvd_set_attn_workgroups(int32_t target);
 
 const char* kvd_status_str(kvd_status status);
 const char* kvd_last_error(void);

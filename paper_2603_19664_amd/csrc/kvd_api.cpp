@@ -5,6 +5,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <atomic>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -85,13 +86,21 @@ void fill_rev(const kvd_attn_shape* s, double* rev) {
 
 int32_t ceil_div(int64_t a, int64_t b) { return (int32_t)((a + b - 1) / b); }
 
-int32_t splits(const kvd_attn_shape* s, int32_t op, int32_t T_main, int32_t T_tail) {
+// Workgroups the bf16 stored-K/V attention's split policy aims for
+// (kvd_set_attn_workgroups).
+std::atomic<int32_t> g_attn_target{kvd::kSaTargetWgs};
+
+kvd::SaSplit stream_split(const kvd_attn_shape* s, int32_t B, int32_t T) {
+  return kvd::sa_split((long long)B * s->n_kv_heads, T, g_attn_target.load(std::memory_order_relaxed));
+}
+
+int32_t splits(const kvd_attn_shape* s, int32_t op, int32_t B, int32_t T_main, int32_t T_tail) {
   if (op == KVD_OP_FUSED) {
     const int32_t n_rec = ceil_div(T_main, kvd::kMtBf16);
     return n_rec + (s->dtype == KVD_BF16 ? kvd::fused_tail_tiles<uint16_t>(n_rec, T_tail)
                                          : kvd::fused_tail_tiles<float>(n_rec, T_tail));
   }
-  return s->dtype == KVD_BF16 ? kvd::decode_splits<uint16_t>(T_main) : kvd::decode_splits<float>(T_main);
+  return s->dtype == KVD_BF16 ? stream_split(s, B, T_main).S : kvd::decode_splits<float>(T_main);
 }
 
 size_t ws_acc_bytes(const kvd_attn_shape* s, int32_t B, int32_t S) {
@@ -132,8 +141,8 @@ template <typename T>
 size_t attn_lds_need(const kvd_attn_shape* s, bool fused) {
   const int g = s->n_q_heads / s->n_kv_heads;
   const int hd = s->head_dim;
-  return fused ? kvd::fused_lds_bytes<T>(g, hd, sizeof(T) == 2 ? kvd::kMtBf16 : kvd::kMtF32)
-               : kvd::decode_lds_bytes<T>(g, hd);
+  if (fused) return kvd::fused_lds_bytes<T>(g, hd, sizeof(T) == 2 ? kvd::kMtBf16 : kvd::kMtF32);
+  return sizeof(T) == 2 ? kvd::sa_lds(hd, kvd::sa_group(g)).end : kvd::decode_lds_bytes<T>(g, hd);
 }
 
 kvd_status check_lds(const kvd_attn_shape* s, bool fused) {
@@ -179,9 +188,10 @@ kvd_status attn_common(const kvd_attn_shape* shape, const void* q, const kvd_kv_
   KVD_TRY(check_ptr(q, "q"));
   if (out != nullptr) KVD_TRY(check_ptr(out, "out"));
   KVD_TRY(check_view(kv, T, "kv"));
-  const int32_t S = splits(shape, KVD_OP_DECODE_ATTN, T, 0);
+  const int32_t S = splits(shape, KVD_OP_DECODE_ATTN, B, T, 0);
   KVD_TRY(check_ws(shape, B, S, ws, ws_bytes));
   kvd::AttnArgs a{};
+  if (shape->dtype == KVD_BF16) a.kps = stream_split(shape, B, T).kps;
   a.q = q;
   a.k = kv->k;
   a.v = kv->v;
@@ -319,6 +329,11 @@ kvd_status kvd_project_qkv(const kvd_attn_shape* shape, const void* h_new, const
       "kvd_project_qkv launch");
 }
 
+kvd_status kvd_project_q(const kvd_attn_shape* shape, const void* h_new, const void* gamma, const void* w_q,
+                         const int32_t* pos, int32_t B, void* q_out, void* stream) {
+  return kvd_project_qkv(shape, h_new, gamma, w_q, nullptr, nullptr, pos, B, q_out, nullptr, stream);
+}
+
 kvd_status kvd_decode_attn(const kvd_attn_shape* shape, const void* q, const kvd_kv_view* kv, int32_t B, int32_t T,
                            void* out, void* ws, size_t ws_bytes, void* stream) {
   return attn_common(shape, q, kv, B, T, out, ws, ws_bytes, stream, false);
@@ -359,7 +374,7 @@ kvd_status fused_launch(const kvd_attn_shape* shape, const void* q, const void* 
                         const void* w_k, const void* w_v, const int32_t* pos0, int32_t B, int32_t T_rec,
                         const kvd_kv_view* tail, int32_t T_tail, void* out, void* ws, size_t ws_bytes,
                         const kvd_kv_view* kv_debug, void* stream, const char* name) {
-  const int32_t S = splits(shape, KVD_OP_FUSED, T_rec, T_tail);
+  const int32_t S = splits(shape, KVD_OP_FUSED, B, T_rec, T_tail);
   // one workgroup per (KV head, sequence, split), indexed in 32 bits
   if ((int64_t)shape->n_kv_heads * B * S > INT32_MAX - 8)
     return fail(KVD_ERR_SHAPE, "%s: n_kv_heads * B * splits = %lld workgroups is too many", name,
@@ -672,7 +687,13 @@ int32_t kvd_num_splits(const kvd_attn_shape* shape, int32_t op, int32_t B, int32
   } else {
     return 0;
   }
-  return splits(shape, op, T_main, T_tail);
+  return splits(shape, op, B, T_main, T_tail);
+}
+
+int32_t kvd_set_attn_workgroups(int32_t target) {
+  if (target <= 0) target = kvd::kSaTargetWgs;
+  target = std::min<int32_t>(target, 1 << 22);
+  return g_attn_target.exchange(target, std::memory_order_relaxed);
 }
 
 size_t kvd_workspace_bytes(const kvd_attn_shape* shape, int32_t op, int32_t B, int32_t T_main, int32_t T_tail) {

@@ -6,6 +6,8 @@
 // MFMA tile engine with other epilogues, and causal prefill attention.
 #include <hip/hip_runtime.h>
 
+#include <atomic>
+
 #include <algorithm>
 
 #include "kvd_device.hpp"
@@ -436,19 +438,24 @@ __global__ void fill_zero_u64_kernel(unsigned long long* dst, int n) {
 
 // ------------------------------------------------------------------ launchers
 
+// Raise a kernel's dynamic-LDS limit once per process; `done` is the largest
+// size set so far (racing threads may both set the idempotent attribute).
 template <class Kern>
-static hipError_t set_lds_once(Kern k, size_t bytes, size_t& done) {
-  if (bytes <= done) return hipSuccess;
+static hipError_t set_lds_once(Kern k, size_t bytes, std::atomic<size_t>& done) {
+  if (bytes <= done.load(std::memory_order_acquire)) return hipSuccess;
   hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(k), hipFuncAttributeMaxDynamicSharedMemorySize,
                                      (int)bytes);
-  if (e == hipSuccess) done = bytes;
-  return e;
+  if (e != hipSuccess) return e;
+  size_t cur = done.load(std::memory_order_relaxed);
+  while (cur < bytes && !done.compare_exchange_weak(cur, bytes, std::memory_order_release)) {
+  }
+  return hipSuccess;
 }
 
 template <int EPI, bool NORM, bool PACKED>
 static hipError_t gemm_t(const GemmArgs& a, hipStream_t st) {
   const size_t bytes = proj_lds<uint16_t>(256, kMtBf16).end + gamma_lds_bytes(a.K);
-  static size_t done = 0;
+  static std::atomic<size_t> done{0};
   auto k = gemm_kernel<EPI, NORM, PACKED>;
   hipError_t e = set_lds_once(k, bytes, done);
   if (e != hipSuccess) return e;
@@ -471,7 +478,7 @@ hipError_t launch_gemm(const GemmArgs& a, int epi, int packed, hipStream_t st) {
 template <int HD>
 static hipError_t prefill_t(const PrefillArgs& a, hipStream_t st) {
   constexpr size_t bytes = prefill_lds(HD).end;
-  static size_t done = 0;
+  static std::atomic<size_t> done{0};
   auto k = prefill_attn_kernel<HD>;
   hipError_t e = set_lds_once(k, bytes, done);
   if (e != hipSuccess) return e;

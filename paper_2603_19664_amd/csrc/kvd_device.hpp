@@ -30,6 +30,7 @@ namespace kvd {
 
 typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8_t;
 typedef __attribute__((__vector_size__(16 * sizeof(float)))) float f32x16_t;
+typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4_t;
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 
 template <int N> struct IC { static constexpr int value = N; };
@@ -889,18 +890,24 @@ __device__ __forceinline__ void write_partial(const char* lds, const AttnLds& L,
 // splits): M = max_s m_s, w_s = 2^(m_s - M), out = sum_s w_s acc_s / sum_s w_s l_s.
 // Every sum has a fixed order that does not depend on NT: each output column
 // adds its splits in split order; the denominator is accumulated per lane over
-// splits s = lane, lane + 64, ... and then summed by the fixed wave tree.  NT / HD
-// rows are merged per pass, splits in blocks of 64.  The (max, sum) pairs of the
-// first kCmbKeep blocks are loaded once and kept in registers, and the waves
-// that own no weights request a block's accumulators while the others compute
-// its weights, so a merge of S <= 64 splits costs about two round trips.
+// splits s = lane, lane + 64, ... and then summed by the fixed wave tree.  A
+// pass merges RPP rows: each thread owns one column of CPT of them (CPT = 2
+// for head_dim >= 128), so a decode group's rows go in one pass; splits go in
+// blocks of 64.  The (max, sum) pairs of the first kCmbKeep blocks are loaded
+// once and kept in registers, and every thread issues all of a block's
+// accumulator loads (partial blocks included) before its first wait, while the
+// waves that own the rows' weights compute them: one round trip per block.
+// CPT2 asks for two columns per thread where the rows allow it (64 more
+// registers of accumulators in flight); the arithmetic is the same either way.
 // lds: cmb_floats(NT, HD) floats.
-template <typename T, int HD, int NT>
+template <typename T, int HD, int NT, bool CPT2 = false>
 __device__ __forceinline__ void combine_rows(const float* ws_acc, const float* ws_ml, T* out, size_t row0, int nrows,
                                              int S, float* lds) {
-  constexpr int RPP = NT / HD;
+  constexpr int RPH = NT / HD;                                  // rows per column set (one column per thread)
+  constexpr int CPT = CPT2 && 2 * RPH <= NT / 64 ? 2 : 1;      // columns per thread
+  constexpr int RPP = CPT * RPH;                                // rows per pass
   constexpr int KEEP = kCmbKeep;
-  static_assert(RPP >= 1 && RPP <= NT / 64, "rows per pass");
+  static_assert(RPH >= 1 && RPP <= NT / 64 && RPP * 66 <= (int)cmb_floats(NT, HD), "rows per pass");
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = wave_id();
   const int rr = tid / HD, c = tid - rr * HD;
@@ -908,11 +915,15 @@ __device__ __forceinline__ void combine_rows(const float* ws_acc, const float* w
   float* mL = lds + RPP * 64;   // [RPP][2] max, denominator
   for (int r0 = 0; r0 < nrows; r0 += RPP) {
     const bool mine = wave < RPP && r0 + wave < nrows;  // this wave owns the weights of row r0 + wave
-    const bool rv = rr < RPP && r0 + rr < nrows;         // this thread owns column c of row r0 + rr
+    bool rv[CPT];                                         // this thread owns column c of row r0 + rr + k RPH
+#pragma unroll
+    for (int k = 0; k < CPT; ++k) rv[k] = rr < RPH && r0 + rr + k * RPH < nrows;
     const float* mlw = ws_ml + (row0 + r0 + wave) * (size_t)S * 2;
     // accumulators: a uniform base per block plus a 32-bit per-lane offset
     const float* abase = ws_acc + (row0 + r0) * (size_t)S * HD;
-    const unsigned aoff = (unsigned)(rr * S * HD + c);
+    unsigned aoff[CPT];
+#pragma unroll
+    for (int k = 0; k < CPT; ++k) aoff[k] = (unsigned)((rr + k * RPH) * S * HD + c);
     float mv[KEEP], lv[KEEP];
     float M = -INFINITY;
     if (mine) {
@@ -923,10 +934,23 @@ __device__ __forceinline__ void combine_rows(const float* ws_acc, const float* w
         lv[k] = s < S ? load_dev(mlw + 2 * s + 1) : 0.0f;
       }
     }
-    float o = 0.0f, lsum = 0.0f;
+    float o[CPT], lsum = 0.0f;
+#pragma unroll
+    for (int k = 0; k < CPT; ++k) o[k] = 0.0f;
     for (int s0 = 0, blk = 0; s0 < S; s0 += 64, ++blk) {
       const int cnt = min(64, S - s0);
       const float* a = abase + (size_t)s0 * HD;
+      // the block's accumulators: every load in flight before any wait.  Past the
+      // last split the loads repeat split cnt - 1 (in bounds, finite): their
+      // weights below are zero, and the loads stay straight-line code.
+      float x[CPT][64];
+#pragma unroll
+      for (int k = 0; k < CPT; ++k) {
+        if (rv[k]) {
+#pragma unroll
+          for (int e = 0; e < 64; ++e) x[k][e] = load_dev(a + (size_t)min(e, cnt - 1) * HD + aoff[k]);
+        }
+      }
       if (mine) {
         if (blk == 0) {  // the maximum over all splits, before the first weight
           float m = mv[0];
@@ -945,31 +969,14 @@ __device__ __forceinline__ void combine_rows(const float* ws_acc, const float* w
         lsum = fmaf(lk, w, lsum);
         wsh[wave * 64 + lane] = w;
       }
-      const float* wp = wsh + rr * 64;
-      if (cnt == 64) {  // (uniform) a whole block: all 64 loads in flight before any wait;
-                        // the waves that own no weights reach them at once
-        float x[64];
-        if (rv) {
+      __syncthreads();
+      // w = 0 past the last split: those terms add an exact zero
 #pragma unroll
-          for (int e = 0; e < 64; ++e) x[e] = load_dev(a + (size_t)e * HD + aoff);
-        }
-        __syncthreads();
-        if (rv) {
+      for (int k = 0; k < CPT; ++k) {
+        if (rv[k]) {
+          const float* wp = wsh + (rr + k * RPH) * 64;
 #pragma unroll
-          for (int e = 0; e < 64; ++e) o = fmaf(x[e], wp[e], o);
-        }
-      } else {
-        __syncthreads();
-        if (rv) {
-          int i = 0;
-          for (; i + 16 <= cnt; i += 16) {
-            float y[16];
-#pragma unroll
-            for (int e = 0; e < 16; ++e) y[e] = load_dev(a + (size_t)(i + e) * HD + aoff);
-#pragma unroll
-            for (int e = 0; e < 16; ++e) o = fmaf(y[e], wp[i + e], o);
-          }
-          for (; i < cnt; ++i) o = fmaf(load_dev(a + (size_t)i * HD + aoff), wp[i], o);
+          for (int e = 0; e < 64; ++e) o[k] = fmaf(x[k][e], wp[e], o[k]);
         }
       }
       __syncthreads();
@@ -979,7 +986,9 @@ __device__ __forceinline__ void combine_rows(const float* ws_acc, const float* w
       if (lane == 0) mL[2 * wave + 1] = lsum;
     }
     __syncthreads();
-    if (rv) out[(row0 + r0 + rr) * HD + c] = from_f<T>(o / mL[2 * rr + 1]);
+#pragma unroll
+    for (int k = 0; k < CPT; ++k)
+      if (rv[k]) out[(row0 + r0 + rr + k * RPH) * HD + c] = from_f<T>(o[k] / mL[2 * (rr + k * RPH) + 1]);
     __syncthreads();
   }
 }

@@ -9,9 +9,14 @@
 //   fused_kernel        per (b, KV head, 64-key chunk): recompute K/V of the chunk
 //                       into LDS and emit its split-K softmax partial without writing
 //                       K/V to HBM; stored tail tiles (CONCAT) ride along.
-//   decode_kernel       per (b, KV head, 64-key chunk) of stored K/V: split-K partial.
+//   stream_attn_kernel  bf16 stored-K/V attention: per (key split, KV head, b) one
+//                       workgroup streams the split's keys in 16-key blocks, loads of
+//                       the next block in flight, and emits one split-K partial.
+//   decode_kernel       fp32 stored-K/V attention, per (b, KV head, 64-key chunk).
 //   combine_kernel      merges the partials of each (b, query head) in split order.
 #include <hip/hip_runtime.h>
+
+#include <atomic>
 
 #include "kvd_device.hpp"
 #include "kvd_launch.h"
@@ -514,7 +519,7 @@ __global__ __launch_bounds__(kNtTile, 1) void fused_kernel(FusedArgs a, int per_
 // ------------------------------------------------------------------ stored-K/V attention
 
 template <typename T, int HD>
-__global__ __launch_bounds__(kNtAttn) __attribute__((amdgpu_waves_per_eu(4))) void decode_kernel(AttnArgs a) {
+__global__ __launch_bounds__(kNtAttn) void decode_kernel(AttnArgs a) {
   extern __shared__ __align__(16) char lds[];
   constexpr int NT = kNtAttn;
   const int s = blockIdx.x, j = blockIdx.y, b = blockIdx.z;
@@ -543,6 +548,222 @@ __global__ __launch_bounds__(kNtAttn) __attribute__((amdgpu_waves_per_eu(4))) vo
     if (split_complete(ctr, before, 1, a.S))
       combine_rows<T, HD, NT>(a.ws_acc, a.ws_ml, static_cast<T*>(a.out), (size_t)b * a.n_q + (size_t)j * g, g, a.S,
                               reinterpret_cast<float*>(lds + AL.cmb));
+  }
+}
+
+// ------------------------------------------------------------------ streaming stored-K/V attention (bf16)
+
+// One workgroup of kSaWaves waves per (split s, KV head j, sequence b): keys
+// k0 = s * kps .. min(T, k0 + kps) - 1 of the stored K/V, in 16-key blocks,
+// block i to wave i % kSaWaves.  Memory traffic is the K/V rows read once
+// (Eq. read_bytes): HBM-bound, so the design keeps loads in flight rather than
+// counting flops.  Per block a wave
+//  - has the NEXT block's K and V already loading into registers (two
+//    register sets, unconditional loads with clamped rows, so the compiler's
+//    memory-counter waits stay static);
+//  - takes the scores S^T = K q^T on MFMA 16x16x32 bf16: K is the A operand
+//    straight from global memory (lane: key lane % 16, 8 dims at 32 c +
+//    8 (lane / 16)), q the B operand (lane: query head lane % 16, zero past g),
+//    so no cross-lane dot-product reduction is needed;
+//  - runs the online softmax in the log2 domain (Eqs. attn_weights /
+//    head_output split over keys): the block max over the 4 key lanes of each
+//    head by two xor shuffles, p = 2^(s - m), the running sum per lane;
+//  - P V on the vector ALUs: V rows are loaded as whole 16-byte chunks (one
+//    load instruction covers 64 / (hd / 8) consecutive rows, fully coalesced),
+//    each lane keeps fp32 accumulators for 8 columns of each head; the
+//    probabilities and the rescale factors pass through a wave-private LDS
+//    slot.
+// At the end the key groups of each wave are added by xor shuffles, the waves
+// merged through LDS (weights 2^(m_w - M), in wave order), and the split's
+// state written as a partial in the split-K workspace format, or, with one
+// split and out given, normalised straight into out.  The split merge is
+// combine_rows, as in every other attention kernel.
+template <int HD, int G>
+__global__ __launch_bounds__(64 * kSaWaves) __attribute__((amdgpu_waves_per_eu(2))) void stream_attn_kernel(
+    AttnArgs a) {
+  extern __shared__ __align__(16) char lds[];
+  constexpr int NW = kSaWaves, NT = 64 * NW;
+  constexpr int NC = HD / 32;    // MFMA K-steps of a score block = V loads per lane per block
+  constexpr int CPK = HD / 8;    // 16-byte chunks of a K or V row
+  constexpr int KPI = 64 / CPK;  // rows per V load instruction
+  static_assert(NC * KPI == kSaBlock, "a block's V rows: NC loads of KPI rows");
+  static_assert(G >= 1 && G <= 16, "query heads per KV head");
+  constexpr SaLds SL = sa_lds(HD, G);
+  const int tid = threadIdx.x, lane = tid & 63, w = wave_id();
+  const int s = blockIdx.x, j = blockIdx.y, b = blockIdx.z;
+  const int g = a.n_q / a.n_kv;
+  const int k0 = s * a.kps;
+  const int nk = min(a.T - k0, a.kps);              // keys of this split, >= 1
+  const int nblk = (nk + kSaBlock - 1) / kSaBlock;
+  const int nb = nblk > w ? (nblk - 1 - w) / NW + 1 : 0;  // this wave's blocks: w, w + NW, ...
+  const size_t row0 = ((size_t)b * a.n_kv + j) * a.t_cap + a.t_off + k0;
+  const uint16_t* Kp = static_cast<const uint16_t*>(a.k) + row0 * HD;
+  const uint16_t* Vp = static_cast<const uint16_t*>(a.v) + row0 * HD;
+  const int hq = lane & 15;  // query head of this lane's score column
+
+  // q as the MFMA B operand, bf16 as stored
+  bf16x8_t qf[NC];
+  {
+    const uint16_t* qs = static_cast<const uint16_t*>(a.q) + ((size_t)b * a.n_q + (size_t)j * g + min(hq, g - 1)) * HD +
+                         8 * (lane >> 4);
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+      u32x4_t v = *reinterpret_cast<const u32x4_t*>(qs + 32 * c);
+      if (hq >= g) v = u32x4_t{0u, 0u, 0u, 0u};
+      qf[c] = __builtin_bit_cast(bf16x8_t, v);
+    }
+  }
+
+  // the wave's i-th block (i clamped to its last block) into registers
+  auto load = [&](u32x4_t (&kr)[NC], u32x4_t (&vr)[NC], int i) {
+    const int kb = kSaBlock * (w + NW * min(i, nb - 1));
+    const uint16_t* kp = Kp + (size_t)min(kb + hq, nk - 1) * HD + 8 * (lane >> 4);
+#pragma unroll
+    for (int c = 0; c < NC; ++c) kr[c] = *reinterpret_cast<const u32x4_t*>(kp + 32 * c);
+#pragma unroll
+    for (int c = 0; c < NC; ++c)
+      vr[c] = *reinterpret_cast<const u32x4_t*>(Vp + (size_t)min(kb + KPI * c + lane / CPK, nk - 1) * HD +
+                                                8 * (lane % CPK));
+  };
+
+  float m_run = -INFINITY, l_run = 0.0f;
+  float acc[G][8];
+#pragma unroll
+  for (int h = 0; h < G; ++h)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc[h][e] = 0.0f;
+  float* Pw = reinterpret_cast<float*>(lds + SL.p) + w * (G + 1) * kSaBlock;  // [G][16] probabilities
+  float* Aw = Pw + G * kSaBlock;                                                // [G] rescale factors
+
+  auto attend = [&](const u32x4_t (&kr)[NC], const u32x4_t (&vr)[NC], int i) {
+    const int kb = kSaBlock * (w + NW * i);
+    f32x4_t sc = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+    for (int c = 0; c < NC; ++c)
+      sc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, kr[c]), qf[c], sc, 0, 0, 0);
+    // sc[r]: key kb + 4 (lane / 16) + r, query head hq
+    float sv[4], bm = -INFINITY;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      sv[r] = kb + 4 * (lane >> 4) + r < nk ? sc[r] * ScoreScale<HD>::v : -INFINITY;
+      bm = fmaxf(bm, sv[r]);
+    }
+    bm = fmaxf(bm, __shfl_xor(bm, 16, 64));
+    bm = fmaxf(bm, __shfl_xor(bm, 32, 64));
+    const float m_new = fmaxf(m_run, bm);  // finite: every attended block holds a key
+    const float alpha = exp2f(m_run - m_new);
+    float p[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) p[r] = exp2f(sv[r] - m_new);
+    l_run = fmaf(l_run, alpha, (p[0] + p[1]) + (p[2] + p[3]));
+    m_run = m_new;
+    if (hq < G) *reinterpret_cast<float4*>(Pw + hq * kSaBlock + 4 * (lane >> 4)) = make_float4(p[0], p[1], p[2], p[3]);
+    if (lane < G) Aw[lane] = alpha;
+    __builtin_amdgcn_wave_barrier();  // the wave's LDS writes are ordered before its reads below
+#pragma unroll
+    for (int h = 0; h < G; ++h) {
+      const float al = Aw[h];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) acc[h][e] *= al;
+    }
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+      const int kk = KPI * c + lane / CPK;  // key of this V chunk within the block
+      const uint32_t vw[4] = {vr[c].x, vr[c].y, vr[c].z, vr[c].w};
+      float v8[8];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        v8[2 * e] = bf_lo(vw[e]);
+        v8[2 * e + 1] = bf_hi(vw[e]);
+      }
+#pragma unroll
+      for (int h = 0; h < G; ++h) {
+        const float pr = Pw[h * kSaBlock + kk];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) acc[h][e] = fmaf(pr, v8[e], acc[h][e]);
+      }
+    }
+    __builtin_amdgcn_wave_barrier();  // reads of this block's slot before the next block's writes
+  };
+
+  // Blocks in pairs, the loop body straight-line (a branch out of its middle
+  // made the compiler's register reuse wait for every load in flight).  With
+  // an odd count the last pair's second block lies past the split: all its
+  // keys are masked, so it leaves the state unchanged (alpha = 1, p = 0).
+  // The scheduling barriers keep each refill after the last use of the
+  // registers it overwrites: hoisted above it, the refill got fresh registers
+  // and a copy back at the loop edge, which waited for every load in flight.
+  if (nb > 0) {
+    u32x4_t kr0[NC], vr0[NC], kr1[NC], vr1[NC];
+    load(kr0, vr0, 0);
+    for (int i = 0; i < nb; i += 2) {
+      __builtin_amdgcn_sched_barrier(0);
+      load(kr1, vr1, i + 1);
+      attend(kr0, vr0, i);
+      __builtin_amdgcn_sched_barrier(0);
+      load(kr0, vr0, i + 2);
+      attend(kr1, vr1, i + 1);
+    }
+  }
+
+  // the wave's state: sums over its key lanes (4 per head for l, KPI per column chunk for acc)
+  l_run += __shfl_xor(l_run, 16, 64);
+  l_run += __shfl_xor(l_run, 32, 64);
+#pragma unroll
+  for (int o = CPK; o < 64; o <<= 1)
+#pragma unroll
+    for (int h = 0; h < G; ++h)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) acc[h][e] += __shfl_xor(acc[h][e], o, 64);
+
+  float* ms = reinterpret_cast<float*>(lds + SL.ml);   // [NW][G][2]
+  float* as = reinterpret_cast<float*>(lds + SL.acc);  // [NW][G][HD]
+  if (lane < G) {
+    ms[(w * G + lane) * 2] = m_run;
+    ms[(w * G + lane) * 2 + 1] = l_run;
+  }
+  if (lane < CPK) {
+#pragma unroll
+    for (int h = 0; h < G; ++h) {
+      float* dst = as + ((size_t)w * G + h) * HD + 8 * lane;
+      *reinterpret_cast<float4*>(dst) = make_float4(acc[h][0], acc[h][1], acc[h][2], acc[h][3]);
+      *reinterpret_cast<float4*>(dst + 4) = make_float4(acc[h][4], acc[h][5], acc[h][6], acc[h][7]);
+    }
+  }
+  __syncthreads();
+
+  // merge of the waves (in wave order): the split's state, or with one split its output
+  const bool direct = a.S == 1 && a.out != nullptr;
+  for (int i = tid; i < g * HD; i += NT) {
+    const int h = i / HD, c = i - h * HD;
+    float M = -INFINITY;
+#pragma unroll
+    for (int v = 0; v < NW; ++v) M = fmaxf(M, ms[(v * G + h) * 2]);
+    float o = 0.0f, L = 0.0f;
+#pragma unroll
+    for (int v = 0; v < NW; ++v) {
+      const float wt = exp2f(ms[(v * G + h) * 2] - M);
+      o = fmaf(wt, as[((size_t)v * G + h) * HD + c], o);
+      L = fmaf(wt, ms[(v * G + h) * 2 + 1], L);
+    }
+    const size_t row = (size_t)b * a.n_q + (size_t)j * g + h;
+    if (direct) {
+      static_cast<uint16_t*>(a.out)[row * HD + c] = from_f<uint16_t>(o / L);
+    } else {
+      store_dev(a.ws_acc + (row * a.S + s) * HD + c, o);
+      if (c == 0) {
+        store_dev(a.ws_ml + (row * a.S + s) * 2, M);
+        store_dev(a.ws_ml + (row * a.S + s) * 2 + 1, L);
+      }
+    }
+  }
+  if (a.out != nullptr && a.S > 1) {
+    unsigned long long* ctr = a.ws_done + (size_t)b * a.n_kv + j;
+    const unsigned long long before = split_arrive(ctr, 1, reinterpret_cast<unsigned long long*>(lds + SL.ctr));
+    if (split_complete(ctr, before, 1, a.S))
+      combine_rows<uint16_t, HD, NT, (G <= 2)>(a.ws_acc, a.ws_ml, static_cast<uint16_t*>(a.out),
+                                               (size_t)b * a.n_q + (size_t)j * g, g, a.S,
+                                               reinterpret_cast<float*>(lds + SL.cmb));
   }
 }
 
@@ -586,19 +807,24 @@ static hipError_t set_lds(K kernel, size_t bytes) {
 }
 
 // Raise the kernel's dynamic-LDS limit once per process (per kernel and size).
+// `done` is the largest size already set; threads that race here may both set
+// the attribute, which is idempotent, and the atomic keeps the maximum.
 template <typename K>
-static hipError_t ensure_lds(K kernel, size_t bytes, size_t& done) {
-  if (bytes <= done) return hipSuccess;
+static hipError_t ensure_lds(K kernel, size_t bytes, std::atomic<size_t>& done) {
+  if (bytes <= done.load(std::memory_order_acquire)) return hipSuccess;
   hipError_t e = set_lds(kernel, bytes);
-  if (e == hipSuccess) done = bytes;
-  return e;
+  if (e != hipSuccess) return e;
+  size_t cur = done.load(std::memory_order_relaxed);
+  while (cur < bytes && !done.compare_exchange_weak(cur, bytes, std::memory_order_release)) {
+  }
+  return hipSuccess;
 }
 
 template <typename T, int HD, bool PACKED>
 static hipError_t proj_t(const ProjArgs& a, int n_units, hipStream_t st) {
   constexpr int MT = sizeof(T) == 2 ? kMtBf16 : kMtF32;
   const size_t bytes = proj_lds<T>(HD, MT).end + gamma_lds_bytes(a.d);
-  static size_t done = 0;
+  static std::atomic<size_t> done{0};
   auto k = proj_kernel<T, HD, MT, PACKED>;
   hipError_t e = ensure_lds(k, bytes, done);
   if (e != hipSuccess) return e;
@@ -614,7 +840,7 @@ static hipError_t stream_t(const ProjArgs& a, hipStream_t st) {
   const int G = stream_group(a.d, a.B * a.T, kLdsPerGroup);
   if (G < 1) return hipErrorInvalidValue;  // validated by the caller
   const size_t bytes = stream_lds(a.d, G).end;
-  static size_t done = 0;
+  static std::atomic<size_t> done{0};
   auto k = stream_proj_kernel<HD, PACKED, NCH>;
   hipError_t e = ensure_lds(k, bytes, done);
   if (e != hipSuccess) return e;
@@ -629,7 +855,7 @@ template <typename T, int HD, bool PACKED>
 static hipError_t fused_t(const FusedArgs& a, hipStream_t st) {
   constexpr int MT = sizeof(T) == 2 ? kMtBf16 : kMtF32;
   const size_t bytes = fused_lds_bytes<T>(a.n_q / a.n_kv, HD, MT) + gamma_lds_bytes(a.d);
-  static size_t done = 0;
+  static std::atomic<size_t> done{0};
   auto k = fused_kernel<T, HD, MT, PACKED>;
   hipError_t e = ensure_lds(k, bytes, done);
   if (e != hipSuccess) return e;
@@ -647,12 +873,37 @@ static hipError_t fused_t(const FusedArgs& a, hipStream_t st) {
 template <typename T, int HD>
 static hipError_t attn_t(const AttnArgs& a, hipStream_t st) {
   const size_t bytes = decode_lds_bytes<T>(a.n_q / a.n_kv, HD);
-  static size_t done = 0;
+  static std::atomic<size_t> done{0};
   auto k = decode_kernel<T, HD>;
   hipError_t e = ensure_lds(k, bytes, done);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(k, dim3(a.S, a.n_kv, a.B), dim3(kNtAttn), bytes, st, a);
   return hipGetLastError();
+}
+
+template <int HD, int G>
+static hipError_t stream_attn_t(const AttnArgs& a, hipStream_t st) {
+  constexpr size_t bytes = sa_lds(HD, G).end;
+  static std::atomic<size_t> done{0};
+  auto k = stream_attn_kernel<HD, G>;
+  hipError_t e = ensure_lds(k, bytes, done);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k, dim3(a.S, a.n_kv, a.B), dim3(64 * kSaWaves), bytes, st, a);
+  return hipGetLastError();
+}
+
+template <int HD>
+static hipError_t stream_attn_g(const AttnArgs& a, hipStream_t st) {
+  switch (sa_group(a.n_q / a.n_kv)) {
+    case 1: return stream_attn_t<HD, 1>(a, st);
+    case 2: return stream_attn_t<HD, 2>(a, st);
+    case 3: return stream_attn_t<HD, 3>(a, st);
+    case 4: return stream_attn_t<HD, 4>(a, st);
+    case 6: return stream_attn_t<HD, 6>(a, st);
+    case 8: return stream_attn_t<HD, 8>(a, st);
+    case 16: return stream_attn_t<HD, 16>(a, st);
+    default: return hipErrorInvalidValue;
+  }
 }
 
 template <typename T, int HD>
@@ -725,7 +976,7 @@ hipError_t launch_combine(const float* ws_acc, const float* ws_ml, void* out, in
 }
 
 hipError_t launch_decode(const AttnArgs& a, int dtype_bf16, int hd, hipStream_t st) {
-#define AB(H) attn_t<uint16_t, H>(a, st)
+#define AB(H) stream_attn_g<H>(a, st)
 #define AF(H) attn_t<float, H>(a, st)
   KVD_DISPATCH(dtype_bf16, hd, AB, AF)
 #undef AB

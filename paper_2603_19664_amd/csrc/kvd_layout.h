@@ -69,10 +69,10 @@ struct AttnLds {
   size_t q, s, red, ml, cmb, ctr, end;
 };
 // Split merge (combine_rows): blocks of 64 splits; the (max, sum) pairs of the
-// first kCmbKeep blocks stay in registers.  LDS floats: rows-per-pass x (64
-// weights + max and sum).
+// first kCmbKeep blocks stay in registers.  LDS floats: rows-per-pass (up to
+// two per nt / hd threads) x (64 weights + max and sum).
 constexpr int kCmbKeep = 2;
-constexpr size_t cmb_floats(int nt, int hd) { return (size_t)(nt / hd) * 66; }
+constexpr size_t cmb_floats(int nt, int hd) { return (size_t)(2 * (nt / hd)) * 66; }
 // Key splits of the P V phase of a tile's attention: fixed by the group size
 // alone, so that kernels with different thread counts add in the same order.
 constexpr int attn_ts(int g) { return g >= 8 ? 1 : 8 / g; }
@@ -177,6 +177,59 @@ constexpr int stream_group(int d, int B, size_t lds_limit) {
   int G = B < kProjTok ? B : kProjTok;
   while (G > 0 && stream_lds(d, G).end > lds_limit) --G;
   return G;
+}
+
+// Streaming stored-K/V attention (bf16 kvd_decode_attn / kvd_cached_attn):
+// kSaWaves waves per workgroup, one workgroup per (key split, KV head,
+// sequence).  A split's keys go in blocks of kSaBlock (one 16-key MFMA score
+// block), block i to wave i % kSaWaves; each wave keeps the next block's K/V
+// loads in flight while it attends the current one.
+constexpr int kSaWaves = 4;
+constexpr int kSaBlock = 16;
+// Workgroups the split policy aims for by default: one per CU.  Measured on
+// MI355X (Gemma-3-4B layer, B = 1..64): a larger target adds splits whose merge
+// (one remote round trip per block of 64, after an arrival per split) costs
+// more than the extra parallelism gains.
+constexpr int kSaTargetWgs = 256;
+// Query heads per KV head the kernel is compiled for: the smallest of 1, 2, 3,
+// 4, 6, 8, 16 that is >= g (heads g .. G-1 are computed on zero queries and
+// never stored).
+constexpr int sa_group(int g) { return g <= 4 ? g : g <= 6 ? 6 : g <= 8 ? 8 : 16; }
+// Keys per split (a multiple of kSaBlock) and the split count S for T keys and
+// `pairs` = B * n_kv (sequence, KV head) pairs: about `target` workgroups in
+// all, at most one split per block; every split holds at least one key.
+struct SaSplit {
+  int kps, S;
+};
+constexpr SaSplit sa_split(long long pairs, int T, int target) {
+  const int nblk = (T + kSaBlock - 1) / kSaBlock;
+  long long s = pairs > 0 ? (target + pairs - 1) / pairs : 1;
+  if (s < 1) s = 1;
+  if (s > nblk) s = nblk;
+  const int bps = (int)((nblk + s - 1) / s);  // blocks per split
+  SaSplit r{};
+  r.kps = bps * kSaBlock;
+  r.S = (T + r.kps - 1) / r.kps;
+  return r;
+}
+// LDS of the streaming kernel: per wave the block's probabilities [G][16] and
+// rescale factors [16]; the waves' states [kSaWaves][G][hd] and (max, sum)
+// [kSaWaves][G][2] for the workgroup merge; the split merge (combine_rows)
+// reuses the state area; the split counter's broadcast.
+struct SaLds {
+  size_t p, acc, ml, cmb, ctr, end;
+};
+constexpr SaLds sa_lds(int hd, int G) {
+  SaLds L{};
+  L.p = 0;
+  L.acc = align_up(L.p + sizeof(float) * kSaWaves * (G + 1) * kSaBlock, 16);
+  L.ml = align_up(L.acc + sizeof(float) * kSaWaves * G * hd, 16);
+  const size_t merge_end = align_up(L.ml + sizeof(float) * kSaWaves * G * 2, 16);
+  L.cmb = L.acc;
+  const size_t cmb_end = L.cmb + sizeof(float) * cmb_floats(64 * kSaWaves, hd);
+  L.ctr = align_up(merge_end > cmb_end ? merge_end : cmb_end, 16);
+  L.end = align_up(L.ctr + sizeof(unsigned long long), 16);
+  return L;
 }
 
 // Workgroup -> work item remap that keeps the items of one XCD contiguous:

@@ -66,6 +66,7 @@ def _load() -> ctypes.CDLL:
     sig = {
         "kvd_recompute_kv": [S, VP, I32, VP, VP, VP, VP, I32, I32, V, VP],
         "kvd_project_qkv": [S, VP, VP, VP, VP, VP, VP, I32, VP, V, VP],
+        "kvd_project_q": [S, VP, VP, VP, VP, I32, VP, VP],
         "kvd_decode_attn": [S, VP, V, I32, I32, VP, VP, SZ, VP],
         "kvd_cached_attn": [S, VP, V, I32, I32, VP, VP, SZ, VP],
         "kvd_fused_recompute_attn": [S, VP, VP, I32, VP, VP, VP, VP, I32, I32, V, I32, VP, VP, SZ, V, VP],
@@ -89,6 +90,8 @@ def _load() -> ctypes.CDLL:
     lib.kvd_workspace_bytes.restype = SZ
     lib.kvd_num_splits.argtypes = [S, I32, I32, I32, I32]
     lib.kvd_num_splits.restype = I32
+    lib.kvd_set_attn_workgroups.argtypes = [I32]
+    lib.kvd_set_attn_workgroups.restype = I32
     lib.kvd_status_str.argtypes = [ctypes.c_int]
     lib.kvd_status_str.restype = ctypes.c_char_p
     lib.kvd_last_error.argtypes = []
@@ -171,6 +174,49 @@ def _ptr(t, name, dtype=None, ndim=None):
     return t.data_ptr()
 
 
+def _extent(t, name, want):
+    """ValueError unless tensor t (if given) has exactly the extents `want` (a tuple); checked
+    before any pointer is taken, so a mismatched tensor never reaches a kernel."""
+    if t is None:
+        return
+    if not isinstance(t, torch.Tensor):
+        raise ValueError(f"{name} must be a torch tensor")
+    if tuple(t.shape) != tuple(want):
+        raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {tuple(want)}")
+
+
+def _kv_extent(k, v, name, B, shape: "Shape", min_rows: int, t_off: int):
+    """k, v: [B, n_kv, t_cap, head_dim] with rows t_off .. t_off + min_rows - 1 inside t_cap."""
+    if k is None and v is None:
+        return
+    if k is None or v is None or k.dim() != 4:
+        raise ValueError(f"{name}: k and v must both be [B, n_kv, t_cap, head_dim] tensors")
+    t_cap = k.shape[2]
+    _extent(k, name + "_k", (B, shape.n_kv_heads, t_cap, shape.head_dim))
+    _extent(v, name + "_v", (B, shape.n_kv_heads, t_cap, shape.head_dim))
+    if t_off < 0 or t_off + min_rows > t_cap:
+        raise ValueError(f"{name}: rows {t_off} .. {t_off + min_rows - 1} exceed t_cap {t_cap}")
+
+
+def _weights_extent(shape: "Shape", **mats):
+    """gamma [d]; w_q [n_q*hd, d]; w_k, w_v [n_kv*hd, d] (packed weights keep these extents)."""
+    d, hd = shape.d_model, shape.head_dim
+    want = {"gamma": (d,), "w_q": (shape.n_q_heads * hd, d), "w_k": (shape.n_kv_heads * hd, d),
+            "w_v": (shape.n_kv_heads * hd, d)}
+    for name, t in mats.items():
+        _extent(t, name, want[name])
+
+
+def _pos_extent(pos, name, B):
+    if pos is None:
+        raise ValueError(f"{name} is required")
+    _extent(pos, name, (B,))
+
+
+def _qo_extent(t, name, B, shape: "Shape"):
+    _extent(t, name, (B, shape.n_q_heads, shape.head_dim))
+
+
 def _stream():
     return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
 
@@ -191,6 +237,12 @@ def kvd_num_splits(shape: Shape, op: int, B: int, T_main: int, T_tail: int = 0) 
     return lib.kvd_num_splits(ctypes.byref(shape.c()), op, B, T_main, T_tail)
 
 
+def kvd_set_attn_workgroups(target: int) -> int:
+    """Workgroup target of the bf16 stored-K/V attention's split policy (0: the default);
+    returns the previous value.  Process-wide; size workspaces after setting it."""
+    return lib.kvd_set_attn_workgroups(int(target))
+
+
 def workspace(shape: Shape, op: int, B: int, T_main: int, T_tail: int = 0, device="cuda") -> torch.Tensor:
     """A zero-filled device buffer of kvd_workspace_bytes bytes (torch allocations are
     256-byte aligned; the split counters at its start must be zero before first use)."""
@@ -198,10 +250,22 @@ def workspace(shape: Shape, op: int, B: int, T_main: int, T_tail: int = 0, devic
     return torch.zeros(max(n, 256), dtype=torch.uint8, device=device)
 
 
+def _ws(ws):
+    if not isinstance(ws, torch.Tensor):
+        raise ValueError("ws must be a torch tensor")
+    return _ptr(ws, "ws"), ws.numel() * ws.element_size()
+
+
 def kvd_recompute_kv(shape: Shape, h, gamma, w_k, w_v, pos0, T: int, k_out, v_out, t_off: int = 0):
     """K/V of residual rows 0..T-1 of h [B, h_ld, d] into k_out/v_out [B, n_kv, t_cap, hd] at rows t_off.."""
     dt = shape.torch_dtype
+    if not isinstance(h, torch.Tensor) or h.dim() != 3:
+        raise ValueError("h must be a [B, h_ld, d_model] tensor")
     B, h_ld = h.shape[0], h.shape[1]
+    _extent(h, "h", (B, h_ld, shape.d_model))
+    _weights_extent(shape, gamma=gamma, w_k=w_k, w_v=w_v)
+    _pos_extent(pos0, "pos0", B)
+    _kv_extent(k_out, v_out, "out", B, shape, T, t_off)
     view = _view(k_out, v_out, t_off, "out", dt)
     _check(lib.kvd_recompute_kv(ctypes.byref(shape.c()), _ptr(h, "h", dt, 3), h_ld, _ptr(gamma, "gamma", dt),
                                 _ptr(w_k, "w_k", dt), _ptr(w_v, "w_v", dt), _ptr(pos0, "pos0", torch.int32), B, T,
@@ -211,22 +275,56 @@ def kvd_recompute_kv(shape: Shape, h, gamma, w_k, w_v, pos0, T: int, k_out, v_ou
 def kvd_project_qkv(shape: Shape, h_new, gamma, w_q, w_k, w_v, pos, q_out, k_out=None, v_out=None, t_off: int = 0):
     """q (and, if k_out/v_out are given, the token's K/V at row t_off) of h_new [B, d]."""
     dt = shape.torch_dtype
+    if not isinstance(h_new, torch.Tensor) or h_new.dim() != 2:
+        raise ValueError("h_new must be a [B, d_model] tensor")
+    B = h_new.shape[0]
+    _extent(h_new, "h_new", (B, shape.d_model))
+    _weights_extent(shape, gamma=gamma, w_q=w_q, w_k=w_k, w_v=w_v)
+    _pos_extent(pos, "pos", B)
+    _qo_extent(q_out, "q_out", B, shape)
+    _kv_extent(k_out, v_out, "kv_out", B, shape, 1, t_off)
     view = _view(k_out, v_out, t_off, "kv_out", dt)
     _check(lib.kvd_project_qkv(ctypes.byref(shape.c()), _ptr(h_new, "h_new", dt, 2), _ptr(gamma, "gamma", dt),
                                _ptr(w_q, "w_q", dt), _ptr(w_k, "w_k", dt), _ptr(w_v, "w_v", dt),
-                               _ptr(pos, "pos", torch.int32), h_new.shape[0], _ptr(q_out, "q_out", dt, 3),
+                               _ptr(pos, "pos", torch.int32), B, _ptr(q_out, "q_out", dt, 3),
                                ctypes.byref(view) if view is not None else None, _stream()))
+
+
+def kvd_project_q(shape: Shape, h_new, gamma, w_q, pos, q_out):
+    """q = RoPE(RMSNorm(h_new) W_q^T, pos) of h_new [B, d] into q_out [B, n_q, hd]."""
+    dt = shape.torch_dtype
+    if not isinstance(h_new, torch.Tensor) or h_new.dim() != 2:
+        raise ValueError("h_new must be a [B, d_model] tensor")
+    B = h_new.shape[0]
+    _extent(h_new, "h_new", (B, shape.d_model))
+    _weights_extent(shape, gamma=gamma, w_q=w_q)
+    _pos_extent(pos, "pos", B)
+    _qo_extent(q_out, "q_out", B, shape)
+    _check(lib.kvd_project_q(ctypes.byref(shape.c()), _ptr(h_new, "h_new", dt, 2), _ptr(gamma, "gamma", dt),
+                             _ptr(w_q, "w_q", dt), _ptr(pos, "pos", torch.int32), B, _ptr(q_out, "q_out", dt, 3),
+                             _stream()))
 
 
 def _attn(fn, shape, q, k, v, T, out, ws, t_off):
     dt = shape.torch_dtype
+    if not isinstance(q, torch.Tensor) or q.dim() != 3:
+        raise ValueError("q must be a [B, n_q, head_dim] tensor")
+    B = q.shape[0]
+    _qo_extent(q, "q", B, shape)
+    _qo_extent(out, "out", B, shape)
+    _kv_extent(k, v, "kv", B, shape, T, t_off)
+    if k is None:
+        raise ValueError("kv: k and v are required")
     view = _view(k, v, t_off, "kv", dt)
-    _check(fn(ctypes.byref(shape.c()), _ptr(q, "q", dt, 3), ctypes.byref(view), q.shape[0], T,
-              _ptr(out, "out", dt, 3), _ptr(ws, "ws"), ws.numel() * ws.element_size(), _stream()))
+    wp, wb = _ws(ws)
+    _check(fn(ctypes.byref(shape.c()), _ptr(q, "q", dt, 3), ctypes.byref(view), B, T,
+              _ptr(out, "out", dt, 3), wp, wb, _stream()))
 
 
 def kvd_pack_weights(shape: Shape, w):
     """A packed copy (MFMA operand order) of a row-major [rows, d_model] bf16 weight matrix."""
+    if not isinstance(w, torch.Tensor) or w.dim() != 2 or w.shape[1] != shape.d_model:
+        raise ValueError(f"w must be a [rows, d_model={shape.d_model}] tensor")
     out = torch.empty_like(w)
     _check(lib.kvd_pack_weights(ctypes.byref(shape.c()), _ptr(w, "w", torch.bfloat16, 2), w.shape[0],
                                 _ptr(out, "packed", torch.bfloat16, 2), _stream()))
@@ -235,8 +333,9 @@ def kvd_pack_weights(shape: Shape, w):
 
 def kvd_combine(shape: Shape, B: int, S: int, ws, out):
     """Merge the S split-K partials an attention call (with out=None) left in ws into out."""
-    _check(lib.kvd_combine(ctypes.byref(shape.c()), B, S, _ptr(ws, "ws"), ws.numel() * ws.element_size(),
-                           _ptr(out, "out", shape.torch_dtype, 3), _stream()))
+    _qo_extent(out, "out", B, shape)
+    wp, wb = _ws(ws)
+    _check(lib.kvd_combine(ctypes.byref(shape.c()), B, S, wp, wb, _ptr(out, "out", shape.torch_dtype, 3), _stream()))
 
 
 def kvd_decode_attn(shape: Shape, q, k, v, T: int, out, ws, t_off: int = 0):
@@ -250,21 +349,42 @@ def kvd_cached_attn(shape: Shape, q, k, v, T: int, out, ws, t_off: int = 0):
     _attn(lib.kvd_cached_attn, shape, q, k, v, T, out, ws, t_off)
 
 
+def _fused_extents(shape, q, h, T_rec, gamma, w_k, w_v, out, tail_k, tail_v, T_tail, tail_t_off):
+    if not isinstance(q, torch.Tensor) or q.dim() != 3:
+        raise ValueError("q must be a [B, n_q, head_dim] tensor")
+    B = q.shape[0]
+    _qo_extent(q, "q", B, shape)
+    _qo_extent(out, "out", B, shape)
+    if T_rec > 0:
+        if not isinstance(h, torch.Tensor) or h.dim() != 3:
+            raise ValueError("h must be a [B, h_ld, d_model] tensor")
+        _extent(h, "h", (B, h.shape[1], shape.d_model))
+        _weights_extent(shape, gamma=gamma, w_k=w_k, w_v=w_v)
+    if T_tail > 0 and tail_k is None:
+        raise ValueError("tail_k / tail_v are required when T_tail > 0")
+    _kv_extent(tail_k, tail_v, "tail", B, shape, T_tail, tail_t_off)
+    return B
+
+
 def kvd_fused_recompute_attn(shape: Shape, q, h, T_rec: int, gamma, w_k, w_v, pos0, out, ws,
                              tail_k=None, tail_v=None, T_tail: int = 0, tail_t_off: int = 0,
                              dbg_k=None, dbg_v=None, dbg_t_off: int = 0):
     """Attention of q over K/V recomputed from h rows 0..T_rec-1, followed by T_tail stored tail rows
     (out=None: partials only, merged later by kvd_combine)."""
     dt = shape.torch_dtype
+    B = _fused_extents(shape, q, h, T_rec, gamma, w_k, w_v, out, tail_k, tail_v, T_tail, tail_t_off)
+    if T_rec > 0:
+        _pos_extent(pos0, "pos0", B)
+        _kv_extent(dbg_k, dbg_v, "kv_debug", B, shape, T_rec, dbg_t_off)
     tail = _view(tail_k, tail_v, tail_t_off, "tail", dt)
     dbg = _view(dbg_k, dbg_v, dbg_t_off, "kv_debug", dt)
+    wp, wb = _ws(ws)
     _check(lib.kvd_fused_recompute_attn(
         ctypes.byref(shape.c()), _ptr(q, "q", dt, 3), _ptr(h, "h", dt, 3), h.shape[1] if h is not None else 0,
         _ptr(gamma, "gamma", dt),
-        _ptr(w_k, "w_k", dt), _ptr(w_v, "w_v", dt), _ptr(pos0, "pos0", torch.int32), q.shape[0], T_rec,
+        _ptr(w_k, "w_k", dt), _ptr(w_v, "w_v", dt), _ptr(pos0, "pos0", torch.int32), B, T_rec,
         ctypes.byref(tail) if tail is not None else None, T_tail, _ptr(out, "out", dt, 3) if out is not None else None,
-        _ptr(ws, "ws"),
-        ws.numel() * ws.element_size(), ctypes.byref(dbg) if dbg is not None else None, _stream()))
+        wp, wb, ctypes.byref(dbg) if dbg is not None else None, _stream()))
 
 
 def kvd_fused_window_attn(shape: Shape, q, h, T_rec: int, gamma, w_k, w_v, window: int, out, ws,
@@ -272,17 +392,20 @@ def kvd_fused_window_attn(shape: Shape, q, h, T_rec: int, gamma, w_k, w_v, windo
     """Sliding-window attention of q over the newest `window` of [h rows 0..T_rec-1 recomputed || T_tail stored
     tail rows], each kept key rotated by its index inside the window (out=None: partials only)."""
     dt = shape.torch_dtype
+    B = _fused_extents(shape, q, h, T_rec, gamma, w_k, w_v, out, tail_k, tail_v, T_tail, tail_t_off)
     tail = _view(tail_k, tail_v, tail_t_off, "tail", dt)
+    wp, wb = _ws(ws)
     _check(lib.kvd_fused_window_attn(
         ctypes.byref(shape.c()), _ptr(q, "q", dt, 3), _ptr(h, "h", dt, 3), h.shape[1] if h is not None else 0,
-        _ptr(gamma, "gamma", dt), _ptr(w_k, "w_k", dt), _ptr(w_v, "w_v", dt), q.shape[0], T_rec,
+        _ptr(gamma, "gamma", dt), _ptr(w_k, "w_k", dt), _ptr(w_v, "w_v", dt), B, T_rec,
         ctypes.byref(tail) if tail is not None else None, T_tail, window,
-        _ptr(out, "out", dt, 3) if out is not None else None, _ptr(ws, "ws"), ws.numel() * ws.element_size(),
-        _stream()))
+        _ptr(out, "out", dt, 3) if out is not None else None, wp, wb, _stream()))
 
 
 def kvd_pack_matrix(w):
     """A packed copy (MFMA operand order) of a row-major [rows, cols] bf16 matrix."""
+    if not isinstance(w, torch.Tensor) or w.dim() != 2:
+        raise ValueError("w must be a [rows, cols] tensor")
     out = torch.empty_like(w)
     _check(lib.kvd_pack_matrix(_ptr(w, "w", torch.bfloat16, 2), w.shape[0], w.shape[1],
                                _ptr(out, "packed", torch.bfloat16, 2), _stream()))
@@ -293,17 +416,44 @@ def kvd_block_workspace_bytes(shape: Shape, d_ff: int, B: int, T: int) -> int:
     return lib.kvd_block_workspace_bytes(ctypes.byref(shape.c()), d_ff, B, T)
 
 
-def block_weights(gamma_attn, w_q, w_k, w_v, w_o, gamma_mlp, w_gate, w_up, w_down) -> BlockWeights:
-    """The kvd_block_weights of one block (device bf16 tensors, kept alive by the caller)."""
+def block_weights(gamma_attn, w_q, w_k, w_v, w_o, gamma_mlp, w_gate, w_up, w_down, shape: Shape = None) -> BlockWeights:
+    """The kvd_block_weights of one block (device bf16 tensors, kept alive by the caller).  With `shape`,
+    every extent is checked against it: gammas [d], W_q [n_q*hd, d], W_k/W_v [n_kv*hd, d], W_o [d, n_q*hd],
+    W_gate/W_up [d_ff, d], W_down [d, d_ff]."""
     ts = (gamma_attn, w_q, w_k, w_v, w_o, gamma_mlp, w_gate, w_up, w_down)
     names = ("gamma_attn", "w_q", "w_k", "w_v", "w_o", "gamma_mlp", "w_gate", "w_up", "w_down")
+    if not isinstance(w_gate, torch.Tensor) or w_gate.dim() != 2:
+        raise ValueError("w_gate must be a [d_ff, d_model] tensor")
+    d_ff = w_gate.shape[0]
+    if shape is not None:
+        d, qd, kd = shape.d_model, shape.n_q_heads * shape.head_dim, shape.n_kv_heads * shape.head_dim
+        want = ((d,), (qd, d), (kd, d), (kd, d), (d, qd), (d,), (d_ff, d), (d_ff, d), (d, d_ff))
+        for t, n, wsh in zip(ts, names, want):
+            _extent(t, n, wsh)
     ptrs = [_ptr(t, n, torch.bfloat16) for t, n in zip(ts, names)]
-    return BlockWeights(*ptrs, w_gate.shape[0])
+    bw = BlockWeights(*ptrs, d_ff)
+    bw._extents = tuple(tuple(t.shape) for t in ts)  # checked against the shape by kvd_block_forward
+    return bw
 
 
 def kvd_block_forward(shape: Shape, weights: BlockWeights, h_in, h_out, pos0, ws):
     """h_out [B, T, d] = one pre-norm transformer block over every position of h_in [B, T, d]."""
+    if not isinstance(h_in, torch.Tensor) or h_in.dim() != 3:
+        raise ValueError("h_in must be a [B, T, d_model] tensor")
     B, T = h_in.shape[0], h_in.shape[1]
+    _extent(h_in, "h_in", (B, T, shape.d_model))
+    _extent(h_out, "h_out", (B, T, shape.d_model))
+    _pos_extent(pos0, "pos0", B)
+    ext = getattr(weights, "_extents", None)
+    if ext is not None:
+        d, qd, kd, d_ff = shape.d_model, shape.n_q_heads * shape.head_dim, shape.n_kv_heads * shape.head_dim, \
+            weights.d_ff
+        want = ((d,), (qd, d), (kd, d), (kd, d), (d, qd), (d,), (d_ff, d), (d_ff, d), (d, d_ff))
+        names = ("gamma_attn", "w_q", "w_k", "w_v", "w_o", "gamma_mlp", "w_gate", "w_up", "w_down")
+        for e, wsh, n in zip(ext, want, names):
+            if tuple(e) != wsh:
+                raise ValueError(f"{n} has shape {tuple(e)}, expected {wsh}")
+    wp, wb = _ws(ws)
     _check(lib.kvd_block_forward(ctypes.byref(shape.c()), ctypes.byref(weights), _ptr(h_in, "h_in", torch.bfloat16, 3),
                                  _ptr(h_out, "h_out", torch.bfloat16, 3), _ptr(pos0, "pos0", torch.int32), B, T,
-                                 _ptr(ws, "ws"), ws.numel() * ws.element_size(), _stream()))
+                                 wp, wb, _stream()))

@@ -148,17 +148,40 @@ def test_project_validation():
     assert f(ctypes.byref(s), FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 1, FAKE, ctypes.byref(bad), None) == kvd.KVD_ERR_SHAPE
 
 
+def _stream_splits(pairs, T, target):
+    """The bf16 stored-K/V attention's split rule as documented: about `target`
+    workgroups over the call, at most one split per 16-key block, whole blocks per split."""
+    nblk = -(-T // 16)
+    s = min(max(-(-target // pairs), 1), nblk)
+    kps = -(-nblk // s) * 16
+    return -(-T // kps)
+
+
 def test_split_policy_and_workspace():
     s = shape()
-    # one 64-key split per tile; a bf16 tail of <= 4 rows joins the fused kernel's
-    # last recomputed tile, a longer one (or any fp32 tail) adds its own tiles
-    ns = lambda sh, op, T, Tt: lib.kvd_num_splits(ctypes.byref(sh), op, 1, T, Tt)
-    assert ns(s, kvd.KVD_OP_DECODE_ATTN, 4097, 0) == 64      # 1..4 remaining keys join the last tile (bf16)
-    assert ns(s, kvd.KVD_OP_DECODE_ATTN, 4100, 0) == 64
-    assert ns(s, kvd.KVD_OP_DECODE_ATTN, 4101, 0) == 65
-    assert ns(s, kvd.KVD_OP_DECODE_ATTN, 4, 0) == 1
-    assert ns(s, kvd.KVD_OP_DECODE_ATTN, 68, 0) == 1
+    ns = lambda sh, op, T, Tt, B=1: lib.kvd_num_splits(ctypes.byref(sh), op, B, T, Tt)  # noqa: E731
+    # bf16 stored-K/V attention: contiguous key ranges, ~256 workgroups over the call
+    for B, T in [(1, 4097), (1, 2049), (8, 2049), (64, 2049), (16, 5121), (1, 1), (3, 17), (256, 100)]:
+        want = _stream_splits(B * 4, T, 256)
+        assert ns(s, kvd.KVD_OP_DECODE_ATTN, T, 0, B) == want, (B, T)
+        assert ns(s, kvd.KVD_OP_CACHED_ATTN, T, 0, B) == want, (B, T)
+    assert ns(s, kvd.KVD_OP_DECODE_ATTN, 4097, 0) == 52     # 4 (b, head) pairs: 80-key splits
+    assert ns(s, kvd.KVD_OP_DECODE_ATTN, 2049, 0, 8) == 8   # 32 pairs: 272-key splits
+    assert ns(s, kvd.KVD_OP_DECODE_ATTN, 2049, 0, 64) == 1  # 256 pairs: one split each
+    # the workgroup target moves the split count, and 0 restores the default
+    try:
+        assert lib.kvd_set_attn_workgroups(1) == 256
+        assert ns(s, kvd.KVD_OP_DECODE_ATTN, 4097, 0) == 1
+        assert lib.kvd_set_attn_workgroups(1 << 20) == 1
+        assert ns(s, kvd.KVD_OP_DECODE_ATTN, 4097, 0) == 257  # one per 16-key block at most
+    finally:
+        lib.kvd_set_attn_workgroups(0)
+    assert ns(s, kvd.KVD_OP_DECODE_ATTN, 4097, 0) == 52
+    # fp32 stored-K/V attention: one split per 64-key tile
     assert ns(shape(dtype=kvd.KVD_F32), kvd.KVD_OP_DECODE_ATTN, 4097, 0) == 65
+    assert ns(shape(dtype=kvd.KVD_F32), kvd.KVD_OP_DECODE_ATTN, 64, 0) == 1
+    # fused: one split per 64-token recompute tile; a bf16 tail of <= 4 rows joins the
+    # last recomputed tile, a longer one (or any fp32 tail) adds its own tiles
     assert ns(s, kvd.KVD_OP_FUSED, 4096, 1) == 64
     assert ns(s, kvd.KVD_OP_FUSED, 4096, 4) == 64
     assert ns(s, kvd.KVD_OP_FUSED, 4096, 5) == 65
@@ -167,7 +190,8 @@ def test_split_policy_and_workspace():
     assert ns(s, kvd.KVD_OP_FUSED, 0, 1) == 1
     assert lib.kvd_num_splits(ctypes.byref(s), kvd.KVD_OP_DECODE_ATTN, 1, 0, 0) == 0
     n = lib.kvd_workspace_bytes(ctypes.byref(s), kvd.KVD_OP_DECODE_ATTN, 2, 100, 0)
-    S = 2
+    S = _stream_splits(8, 100, 256)
+    assert S == 7
     acc = -(-2 * 8 * S * 256 * 4 // 256) * 256
     ml = -(-2 * 8 * S * 2 * 4 // 256) * 256
     done = -(-2 * 4 * 8 // 256) * 256  # split counters [B][n_kv] uint64
@@ -273,3 +297,78 @@ def test_pack_matrix_validation():
     assert f(FAKE, 64, 24, FAKE + (1 << 24), None) == kvd.KVD_ERR_SHAPE
     assert f(None, 64, 64, FAKE, None) == kvd.KVD_ERR_NULL
     assert f(FAKE, 64, 64, FAKE + 64, None) == kvd.KVD_ERR_SHAPE     # overlap
+
+
+# ------------------------------------------------------------------ binding extent checks (no GPU)
+
+def _layer_tensors(B=2, T=8, d=512, nq=8, nkv=4, hd=64, dt=None):
+    import torch
+    dt = dt or torch.bfloat16
+    return dict(h=torch.zeros(B, T, d, dtype=dt), gamma=torch.zeros(d, dtype=dt),
+                w_q=torch.zeros(nq * hd, d, dtype=dt), w_k=torch.zeros(nkv * hd, d, dtype=dt),
+                w_v=torch.zeros(nkv * hd, d, dtype=dt), pos=torch.zeros(B, dtype=torch.int32),
+                q=torch.zeros(B, nq, hd, dtype=dt), k=torch.zeros(B, nkv, T + 1, hd, dtype=dt),
+                v=torch.zeros(B, nkv, T + 1, hd, dtype=dt), h_new=torch.zeros(B, d, dtype=dt))
+
+
+SH = kvd.Shape(512, 8, 4, 64, 1e-6, 1e4, kvd.KVD_BF16)
+
+
+def _raises(match, fn, *a, **kw):
+    with pytest.raises(ValueError, match=match):
+        fn(*a, **kw)
+
+
+def test_binding_rejects_mismatched_extents_before_any_launch():
+    import torch
+    x = _layer_tensors()
+    bad_k = torch.zeros(2, 3, 9, 64, dtype=torch.bfloat16)   # 3 KV heads, the shape says 4
+    # recompute_kv
+    _raises("h has shape", kvd.kvd_recompute_kv, SH, torch.zeros(2, 8, 256, dtype=torch.bfloat16), x["gamma"],
+            x["w_k"], x["w_v"], x["pos"], 8, x["k"], x["v"])
+    _raises("gamma has shape", kvd.kvd_recompute_kv, SH, x["h"], torch.zeros(256, dtype=torch.bfloat16), x["w_k"],
+            x["w_v"], x["pos"], 8, x["k"], x["v"])
+    _raises("w_k has shape", kvd.kvd_recompute_kv, SH, x["h"], x["gamma"], x["w_q"], x["w_v"], x["pos"], 8, x["k"],
+            x["v"])
+    _raises("pos0 has shape", kvd.kvd_recompute_kv, SH, x["h"], x["gamma"], x["w_k"], x["w_v"],
+            torch.zeros(3, dtype=torch.int32), 8, x["k"], x["v"])
+    _raises("out_k has shape", kvd.kvd_recompute_kv, SH, x["h"], x["gamma"], x["w_k"], x["w_v"], x["pos"], 8, bad_k,
+            bad_k)
+    _raises("exceed t_cap", kvd.kvd_recompute_kv, SH, x["h"], x["gamma"], x["w_k"], x["w_v"], x["pos"], 8, x["k"],
+            x["v"], 2)
+    # project
+    _raises("q_out has shape", kvd.kvd_project_qkv, SH, x["h_new"], x["gamma"], x["w_q"], x["w_k"], x["w_v"], x["pos"],
+            torch.zeros(2, 4, 64, dtype=torch.bfloat16))
+    _raises("w_q has shape", kvd.kvd_project_q, SH, x["h_new"], x["gamma"], x["w_k"], x["pos"], x["q"])
+    # attention
+    _raises("out has shape", kvd.kvd_decode_attn, SH, x["q"], x["k"], x["v"], 9, torch.zeros(1, 8, 64), x["q"])
+    _raises("kv_k has shape", kvd.kvd_cached_attn, SH, x["q"], bad_k, bad_k, 9, x["q"], x["q"])
+    _raises("exceed t_cap", kvd.kvd_decode_attn, SH, x["q"], x["k"], x["v"], 10, x["q"], x["q"])
+    _raises("out has shape", kvd.kvd_combine, SH, 2, 3, x["q"], torch.zeros(2, 8, 32))
+    # fused
+    _raises("h has shape", kvd.kvd_fused_recompute_attn, SH, x["q"], torch.zeros(3, 8, 512, dtype=torch.bfloat16), 8,
+            x["gamma"], x["w_k"], x["w_v"], x["pos"], x["q"], x["q"])
+    _raises("tail_k has shape", kvd.kvd_fused_recompute_attn, SH, x["q"], x["h"], 8, x["gamma"], x["w_k"], x["w_v"],
+            x["pos"], x["q"], x["q"], bad_k, bad_k, 1)
+    _raises("tail_k / tail_v are required", kvd.kvd_fused_recompute_attn, SH, x["q"], x["h"], 8, x["gamma"], x["w_k"],
+            x["w_v"], x["pos"], x["q"], x["q"], None, None, 1)
+    _raises("kv_debug_k has shape", kvd.kvd_fused_recompute_attn, SH, x["q"], x["h"], 8, x["gamma"], x["w_k"],
+            x["w_v"], x["pos"], x["q"], x["q"], x["k"], x["v"], 1, 0, bad_k, bad_k)
+    _raises("h has shape", kvd.kvd_fused_window_attn, SH, x["q"], torch.zeros(2, 8, 64, dtype=torch.bfloat16), 8,
+            x["gamma"], x["w_k"], x["w_v"], 4, x["q"], x["q"])
+    # block forward weights against the shape
+    d_ff = 256
+    z = lambda *s: torch.zeros(*s, dtype=torch.bfloat16)  # noqa: E731
+    _raises("w_o has shape", kvd.block_weights, x["gamma"], x["w_q"], x["w_k"], x["w_v"], z(512, 256), x["gamma"],
+            z(d_ff, 512), z(d_ff, 512), z(512, d_ff), shape=SH)
+    _raises("h_out has shape", kvd.kvd_block_forward, SH, None, x["h"], z(2, 7, 512), x["pos"], x["q"])
+    with pytest.raises(ValueError, match="d_model=512"):
+        kvd.kvd_pack_weights(SH, z(64, 256))
+
+
+def test_binding_rejects_host_tensors_of_the_right_extents():
+    # extents pass; the device check then refuses host memory (still before any launch)
+    x = _layer_tensors()
+    _raises("on the GPU", kvd.kvd_recompute_kv, SH, x["h"], x["gamma"], x["w_k"], x["w_v"], x["pos"], 8, x["k"],
+            x["v"])
+    _raises("on the GPU", kvd.kvd_decode_attn, SH, x["q"], x["k"], x["v"], 9, x["q"], x["q"])
