@@ -207,6 +207,27 @@ kvd_status kvd_fused_recompute_attn(const kvd_attn_shape* shape, const void* q, 
                                     void* out, void* ws, size_t ws_bytes,
                                     const kvd_kv_view* kv_debug, void* stream);
 
+/* kvd_fused_recompute_attn without a workspace argument, for callers that
+ * cannot allocate device memory: code under HIP graph capture, tight serving
+ * loops, harnesses that forbid hipMalloc.  It allocates nothing.  Its split-K
+ * partials and counters live in a static per-device scratch array of 32 MiB
+ * (kvd_workspace_bytes(shape, KVD_OP_FUSED, B, T_rec, T_tail) must not exceed
+ * 33554432, else KVD_ERR_WORKSPACE before any launch), held by every GPU the
+ * library runs on until the process ends; its address is looked up once per
+ * device on the first call.  Each call first clears its split counters with a
+ * fill kernel, then runs exactly the kernels of kvd_fused_recompute_attn, so
+ * out is bit-identical to that call's.  out must not be NULL (the splits are
+ * always merged in the kernel); there is no kv_debug.  All calls on one GPU
+ * share the one array: calls that overlap on a GPU (concurrent streams,
+ * threads or processes' graph replays in flight together) race and give
+ * wrong results; order them on one stream.  Other arguments as in
+ * kvd_fused_recompute_attn.                                                   */
+kvd_status kvd_fused_recompute_attn_noalloc(const kvd_attn_shape* shape, const void* q, const void* h,
+                                            int32_t h_ld, const void* gamma, const void* w_k,
+                                            const void* w_v, const int32_t* pos0, int32_t B,
+                                            int32_t T_rec, const kvd_kv_view* tail, int32_t T_tail,
+                                            void* out, void* stream);
+
 /* A sliding-window layer's decode-step attention (Sec. 3.2, the sliding-window
  * boundary and Eq. sw_error; Sec. 5, the sliding-window limitation): of the
  * T = T_rec + T_tail keys that kvd_fused_recompute_attn would attend (residual

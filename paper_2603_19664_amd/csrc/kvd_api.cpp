@@ -435,6 +435,31 @@ kvd_status kvd_fused_recompute_attn(const kvd_attn_shape* shape, const void* q, 
                       stream, "kvd_fused_recompute_attn launch");
 }
 
+kvd_status kvd_fused_recompute_attn_noalloc(const kvd_attn_shape* shape, const void* q, const void* h, int32_t h_ld,
+                                            const void* gamma, const void* w_k, const void* w_v, const int32_t* pos0,
+                                            int32_t B, int32_t T_rec, const kvd_kv_view* tail, int32_t T_tail,
+                                            void* out, void* stream) {
+  KVD_TRY(check_fused_args(shape, q, h, h_ld, gamma, w_k, w_v, B, T_rec, tail, T_tail, out));
+  if (B == 0) return KVD_OK;
+  if (out == nullptr) return fail(KVD_ERR_NULL, "out is NULL (the no-allocation call always merges its splits)");
+  if (T_rec > 0 && pos0 == nullptr) return fail(KVD_ERR_NULL, "pos0 is NULL");
+  const int32_t S = splits(shape, KVD_OP_FUSED, B, T_rec, T_tail);
+  const size_t need = ws_total(shape, B, S);
+  if (need > kvd::kNoAllocScratchBytes)
+    return fail(KVD_ERR_WORKSPACE,
+                "kvd_fused_recompute_attn_noalloc: B=%d T_rec=%d T_tail=%d needs %zu bytes of scratch, more than the "
+                "%zu of the library's static scratch; call kvd_fused_recompute_attn with a workspace instead",
+                B, T_rec, T_tail, need, kvd::kNoAllocScratchBytes);
+  void* ws = nullptr;
+  KVD_TRY(device_status(kvd::noalloc_scratch(&ws), "kvd_fused_recompute_attn_noalloc scratch lookup"));
+  // the split counters [B][n_kv] start at zero: cleared by a fill kernel (a
+  // kernel node under graph capture, never a memset)
+  KVD_TRY(device_status(kvd::launch_fill_zero_u64(ws, B * shape->n_kv_heads, (hipStream_t)stream),
+                        "kvd_fused_recompute_attn_noalloc counter clear"));
+  return fused_launch(shape, q, h, h_ld, gamma, w_k, w_v, pos0, B, T_rec, tail, T_tail, out, ws,
+                      kvd::kNoAllocScratchBytes, nullptr, stream, "kvd_fused_recompute_attn_noalloc launch");
+}
+
 kvd_status kvd_fused_window_attn(const kvd_attn_shape* shape, const void* q, const void* h, int32_t h_ld,
                                  const void* gamma, const void* w_k, const void* w_v, int32_t B, int32_t T_rec,
                                  const kvd_kv_view* tail, int32_t T_tail, int32_t window, void* out, void* ws,

@@ -17,6 +17,7 @@
 #include <hip/hip_runtime.h>
 
 #include <atomic>
+#include <mutex>
 
 #include "kvd_device.hpp"
 #include "kvd_launch.h"
@@ -796,6 +797,38 @@ hipError_t launch_pack(const void* w, void* out, int rows, int d, hipStream_t st
   hipLaunchKernelGGL(pack_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, static_cast<const uint16_t*>(w),
                      static_cast<uint16_t*>(out), rows, d);
   return hipGetLastError();
+}
+
+// ------------------------------------------------------------------ static scratch
+
+// The allocation-free fused call's workspace (split counters, then partials):
+// one array per device, held until the process ends.  Host code never names
+// the array after set-up: noalloc_scratch() looks up each device's address
+// once (with that device current) and every launch, fill and copy takes that
+// pointer.
+static __device__ __align__(256) unsigned char scratch[kNoAllocScratchBytes];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices];
+}  // namespace
+
+hipError_t noalloc_scratch(void** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch_ptr[dev] == nullptr) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (p == nullptr) return hipErrorInvalidSymbol;
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return hipSuccess;
 }
 
 // ------------------------------------------------------------------ launchers

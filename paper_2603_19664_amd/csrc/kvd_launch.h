@@ -135,6 +135,11 @@ hipError_t launch_fill_zero_u64(void* dst, int n, hipStream_t st);
 size_t gemm_lds_bytes(int K);
 size_t prefill_lds_bytes(int hd);
 
+// The current device's static scratch (kNoAllocScratchBytes, 256-byte aligned):
+// its address is looked up once per device, on the first call with that device
+// current.  Allocates nothing.
+hipError_t noalloc_scratch(void** out);
+
 hipError_t launch_proj(const ProjArgs& a, int dtype_bf16, int hd, int packed, int n_units, hipStream_t st);
 // Current-token projection (T == 1): the streaming kernel for bf16, proj_kernel for fp32.
 hipError_t launch_project_current(const ProjArgs& a, int dtype_bf16, int hd, int packed, int n_units,

@@ -232,6 +232,11 @@ constexpr SaLds sa_lds(int hd, int G) {
   return L;
 }
 
+// Bytes of the static per-device scratch of kvd_fused_recompute_attn_noalloc:
+// enough for the split-K workspace of every measured workload (the largest,
+// a Gemma-3-4B layer at B = 64 and 2048 context tokens, needs ~17 MB).
+constexpr size_t kNoAllocScratchBytes = (size_t)32 << 20;
+
 // Workgroup -> work item remap that keeps the items of one XCD contiguous:
 // hardware dispatch sends workgroup w to XCD w % 8, so XCD x runs items
 // x*per .. x*per+per-1, and units that share weights land on the same L2.

@@ -71,6 +71,7 @@ def _load() -> ctypes.CDLL:
         "kvd_cached_attn": [S, VP, V, I32, I32, VP, VP, SZ, VP],
         "kvd_fused_recompute_attn": [S, VP, VP, I32, VP, VP, VP, VP, I32, I32, V, I32, VP, VP, SZ, V, VP],
         "kvd_fused_window_attn": [S, VP, VP, I32, VP, VP, VP, I32, I32, V, I32, I32, VP, VP, SZ, VP],
+        "kvd_fused_recompute_attn_noalloc": [S, VP, VP, I32, VP, VP, VP, VP, I32, I32, V, I32, VP, VP],
     }
     for name, args in sig.items():
         f = getattr(lib, name)
@@ -385,6 +386,23 @@ def kvd_fused_recompute_attn(shape: Shape, q, h, T_rec: int, gamma, w_k, w_v, po
         _ptr(w_k, "w_k", dt), _ptr(w_v, "w_v", dt), _ptr(pos0, "pos0", torch.int32), B, T_rec,
         ctypes.byref(tail) if tail is not None else None, T_tail, _ptr(out, "out", dt, 3) if out is not None else None,
         wp, wb, ctypes.byref(dbg) if dbg is not None else None, _stream()))
+
+
+def kvd_fused_recompute_attn_noalloc(shape: Shape, q, h, T_rec: int, gamma, w_k, w_v, pos0, out,
+                                     tail_k=None, tail_v=None, T_tail: int = 0, tail_t_off: int = 0):
+    """kvd_fused_recompute_attn with the library's static per-device scratch as its workspace
+    (allocates nothing; calls on one GPU must not overlap)."""
+    dt = shape.torch_dtype
+    B = _fused_extents(shape, q, h, T_rec, gamma, w_k, w_v, out, tail_k, tail_v, T_tail, tail_t_off)
+    if out is None:
+        raise ValueError("out is required")
+    if T_rec > 0:
+        _pos_extent(pos0, "pos0", B)
+    tail = _view(tail_k, tail_v, tail_t_off, "tail", dt)
+    _check(lib.kvd_fused_recompute_attn_noalloc(
+        ctypes.byref(shape.c()), _ptr(q, "q", dt, 3), _ptr(h, "h", dt, 3), h.shape[1] if h is not None else 0,
+        _ptr(gamma, "gamma", dt), _ptr(w_k, "w_k", dt), _ptr(w_v, "w_v", dt), _ptr(pos0, "pos0", torch.int32), B,
+        T_rec, ctypes.byref(tail) if tail is not None else None, T_tail, _ptr(out, "out", dt, 3), _stream()))
 
 
 def kvd_fused_window_attn(shape: Shape, q, h, T_rec: int, gamma, w_k, w_v, window: int, out, ws,

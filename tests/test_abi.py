@@ -372,3 +372,19 @@ def test_binding_rejects_host_tensors_of_the_right_extents():
     _raises("on the GPU", kvd.kvd_recompute_kv, SH, x["h"], x["gamma"], x["w_k"], x["w_v"], x["pos"], 8, x["k"],
             x["v"])
     _raises("on the GPU", kvd.kvd_decode_attn, SH, x["q"], x["k"], x["v"], 9, x["q"], x["q"])
+
+
+def test_noalloc_rejects_work_beyond_its_scratch():
+    # 64 sequences of 16384 recomputed keys need ~134 MB of split-K partials, more
+    # than the 32 MiB static scratch: refused before any HIP call
+    s = shape()
+    need = lib.kvd_workspace_bytes(ctypes.byref(s), kvd.KVD_OP_FUSED, 64, 16384, 1)
+    assert need > 32 << 20
+    tail = view(t_cap=1)
+    st = lib.kvd_fused_recompute_attn_noalloc(ctypes.byref(s), FAKE, FAKE, 16384, FAKE, FAKE, FAKE, FAKE, 64, 16384,
+                                              ctypes.byref(tail), 1, FAKE, None)
+    assert st == kvd.KVD_ERR_WORKSPACE and "static scratch" in kvd.last_error()
+    # the partial-only form has no place in it: out is required
+    st = lib.kvd_fused_recompute_attn_noalloc(ctypes.byref(s), FAKE, FAKE, 100, FAKE, FAKE, FAKE, FAKE, 1, 100,
+                                              ctypes.byref(tail), 1, None, None)
+    assert st == kvd.KVD_ERR_NULL
