@@ -180,13 +180,16 @@ kvd_status kvd_cached_attn(const kvd_attn_shape* shape, const void* q, const kvd
                            int32_t B, int32_t T, void* out, void* ws, size_t ws_bytes,
                            void* stream);
 
-/* One KV-Direct decode step's attention at cache budget 0 (Algorithm 1:
- * RECOMPUTE_KV, CONCAT, ATTENTION): keys and values are recomputed from the
- * checkpointed residuals h rows 0..T_rec-1 (positions pos0[b]+t) inside the
- * kernel and attended from LDS without being written to HBM, then
- * concatenated with T_tail stored keys (tail rows tail->t_off ..
- * tail->t_off+T_tail-1; typically the current token's own K/V from
- * kvd_project_qkv, or a window of cached recent keys).
+/* One KV-Direct decode step's attention (Algorithm 1: RECOMPUTE_KV, CONCAT,
+ * ATTENTION): keys and values are recomputed from the checkpointed residuals
+ * h rows 0..T_rec-1 (positions pos0[b]+t) inside the kernel and attended from
+ * LDS without being written to HBM, then concatenated with T_tail stored keys:
+ * the tail view's rows t_off, t_off+1, ... taken modulo tail->t_cap, so a
+ * bounded cache kept as a ring of t_cap slots is read oldest first from its
+ * oldest slot t_off (0 <= t_off < t_cap, T_tail <= t_cap; a view with
+ * t_off + T_tail <= t_cap is an ordinary contiguous block).  The tail is
+ * typically the current token's own K/V from kvd_project_qkv (cache budget 0),
+ * or Algorithm 1's bounded cache of recent tokens followed by the current one.
  *   T_rec >= 0, T_tail >= 0, T_rec + T_tail >= 1; tail may be NULL iff T_tail == 0.
  *   ws: kvd_workspace_bytes(shape, KVD_OP_FUSED, B, T_rec, T_tail) bytes.
  *   kv_debug: NULL in production.  If not NULL, the recomputed K/V are also
@@ -249,6 +252,16 @@ kvd_status kvd_fused_window_attn(const kvd_attn_shape* shape, const void* q, con
                                  const void* w_v, int32_t B, int32_t T_rec,
                                  const kvd_kv_view* tail, int32_t T_tail, int32_t window,
                                  void* out, void* ws, size_t ws_bytes, void* stream);
+
+/* STORE_RESIDUAL (Algorithm 1; Eq. res_mem): checkpoint each sequence's
+ * current residual, ckpt[b][row][:] = h_new[b][:] for b < B, in the shape
+ * dtype.  A bounded cache (Algorithm 1 with budget > 0) stores every token's
+ * residual when the token arrives, since its h^(l) exists only at that step,
+ * and recomputes from it once the token is evicted from the cache.
+ *   h_new [B][d_model].   ckpt [B][c_ld][d_model], 0 <= row < c_ld; must not
+ *   overlap h_new.   B == 0 is a no-op.                                       */
+kvd_status kvd_store_residual(const kvd_attn_shape* shape, const void* h_new, void* ckpt, int32_t c_ld,
+                              int32_t row, int32_t B, void* stream);
 
 /* Weight packing (done once per frozen weight matrix; the weights of the paper's
  * projections are fixed at inference, Sec. 3.2): rewrites a row-major

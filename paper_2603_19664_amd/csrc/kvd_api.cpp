@@ -73,6 +73,20 @@ kvd_status check_view(const kvd_kv_view* v, int32_t T, const char* name) {
   return KVD_OK;
 }
 
+// A stored tail of T rows read as a ring: rows t_off .. t_off+T-1 modulo t_cap
+// (t_off < t_cap, T <= t_cap).  A view with t_off + T <= t_cap is an ordinary
+// contiguous block.
+kvd_status check_ring_view(const kvd_kv_view* v, int32_t T, const char* name) {
+  if (v == nullptr) return fail(KVD_ERR_NULL, "%s is NULL", name);
+  std::string nk = std::string(name) + "->k", nv = std::string(name) + "->v";
+  KVD_TRY(check_ptr(v->k, nk.c_str()));
+  KVD_TRY(check_ptr(v->v, nv.c_str()));
+  if (v->t_cap < 1 || v->t_off < 0 || v->t_off >= v->t_cap || T > v->t_cap)
+    return fail(KVD_ERR_SHAPE, "%s: %d rows from slot t_off=%d of a ring of t_cap=%d slots (need 0 <= t_off < t_cap "
+                "and T <= t_cap)", name, T, v->t_off, v->t_cap);
+  return KVD_OK;
+}
+
 kvd_status check_batch(int32_t B) {
   if (B < 0 || B > 65535) return fail(KVD_ERR_SHAPE, "B=%d must be in [0, 65535]", B);
   return KVD_OK;
@@ -364,7 +378,7 @@ kvd_status check_fused_args(const kvd_attn_shape* shape, const void* q, const vo
     KVD_TRY(check_ptr(w_k, "w_k"));
     KVD_TRY(check_ptr(w_v, "w_v"));
   }
-  if (T_tail > 0) KVD_TRY(check_view(tail, T_tail, "tail"));
+  if (T_tail > 0) KVD_TRY(check_ring_view(tail, T_tail, "tail"));
   return KVD_OK;
 }
 
@@ -478,11 +492,30 @@ kvd_status kvd_fused_window_attn(const kvd_attn_shape* shape, const void* q, con
   kvd_kv_view tail_kept{};
   if (keep_tail > 0) {
     tail_kept = *tail;
-    tail_kept.t_off += drop_tail;
+    tail_kept.t_off = (int32_t)(((int64_t)tail_kept.t_off + drop_tail) % tail_kept.t_cap);
   }
   return fused_launch(shape, q, h_kept, h_ld, gamma, w_k, w_v, nullptr, B, keep_rec,
                       keep_tail > 0 ? &tail_kept : nullptr, keep_tail, out, ws, ws_bytes, nullptr, stream,
                       "kvd_fused_window_attn launch");
+}
+
+kvd_status kvd_store_residual(const kvd_attn_shape* shape, const void* h_new, void* ckpt, int32_t c_ld, int32_t row,
+                              int32_t B, void* stream) {
+  KVD_TRY(check_shape(shape));
+  KVD_TRY(check_batch(B));
+  if (c_ld < 1 || row < 0 || row >= c_ld)
+    return fail(KVD_ERR_SHAPE, "row=%d must lie in the checkpoint store's c_ld=%d rows", row, c_ld);
+  if (B == 0) return KVD_OK;
+  KVD_TRY(check_ptr(h_new, "h_new"));
+  KVD_TRY(check_ptr(ckpt, "ckpt"));
+  const size_t row_bytes = (size_t)shape->d_model * elem_size(shape);
+  const char* a = static_cast<const char*>(h_new);
+  const char* c = static_cast<const char*>(ckpt);
+  if (a < c + (size_t)B * c_ld * row_bytes && c < a + (size_t)B * row_bytes)
+    return fail(KVD_ERR_SHAPE, "ckpt must not overlap h_new");
+  return device_status(kvd::launch_copy_rows(h_new, row_bytes, static_cast<char*>(ckpt) + (size_t)row * row_bytes,
+                                             (size_t)c_ld * row_bytes, row_bytes, B, (hipStream_t)stream),
+                       "kvd_store_residual launch");
 }
 
 kvd_status kvd_pack_matrix(const void* w, int32_t rows, int32_t cols, void* packed, void* stream) {

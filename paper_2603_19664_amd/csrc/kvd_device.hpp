@@ -640,8 +640,10 @@ struct TileSetup {
 };
 
 // Rows row0 .. row0+n-1 (n <= kTile) of a stored K/V block ([B][n_kv][t_cap][HD],
-// head j of sequence b) into the LDS tile [kTile][K | V].  All loads of a thread
-// are issued before its LDS stores.
+// head j of sequence b) into the LDS tile [kTile][K | V].  Rows wrap around the
+// t_cap slots (row0 + t >= t_cap reads slot row0 + t - t_cap; callers keep
+// row0 + n <= 2 t_cap): a ring of slots reads oldest first.  All loads of a
+// thread are issued before its LDS stores.
 template <typename T, int HD, int NT>
 __device__ __forceinline__ void load_kv_tile(const T* K, const T* V, int b, int n_kv, int j, int t_cap, int row0,
                                              int n, T* kv) {
@@ -650,13 +652,15 @@ __device__ __forceinline__ void load_kv_tile(const T* K, const T* V, int b, int 
   constexpr int CPR = HD / CH;               // chunks per K (or V) row
   constexpr int HALF = kTile * CPR / NT;     // chunks per thread for the K (or V) half of a full tile
   static_assert(HALF * NT == kTile * CPR, "tile split");
-  const size_t base = ((size_t)b * n_kv + j) * t_cap + row0;
+  const size_t base = ((size_t)b * n_kv + j) * t_cap;
   u32x4_t v[2 * HALF];
 #pragma unroll
   for (int i = 0; i < 2 * HALF; ++i) {
     const int rem = threadIdx.x + NT * (i % HALF);
     const int t = rem / CPR, ch = rem % CPR;
-    const T* src = (i < HALF ? K : V) + (base + (t < n ? t : 0)) * HD + ch * CH;
+    int row = row0 + (t < n ? t : 0);
+    row -= row >= t_cap ? t_cap : 0;
+    const T* src = (i < HALF ? K : V) + (base + row) * HD + ch * CH;
     v[i] = *reinterpret_cast<const u32x4_t*>(src);
   }
 #pragma unroll

@@ -431,7 +431,9 @@ __global__ __launch_bounds__(kNtTile, 1) void fused_kernel(FusedArgs a, int per_
   const bool tail_mine = FR > 0 && tail_here && tr < a.T_tail;
   u32x4_t tail_v;
   if constexpr (FR > 0) {
-    const size_t trow = ((size_t)b * a.n_kv + j) * a.tail_t_cap + a.tail_t_off + tr;
+    int tslot = a.tail_t_off + (tail_mine ? tr : 0);  // tail rows wrap around a ring of tail_t_cap slots
+    tslot -= tslot >= a.tail_t_cap ? a.tail_t_cap : 0;
+    const size_t trow = ((size_t)b * a.n_kv + j) * a.tail_t_cap + tslot;
     const T* src = tch < TCH / 2 ? static_cast<const T*>(a.tk) + trow * HD + tch * (16 / sizeof(T))
                                  : static_cast<const T*>(a.tv) + trow * HD + (tch - TCH / 2) * (16 / sizeof(T));
     tail_v = *reinterpret_cast<const u32x4_t*>(tail_mine ? src : static_cast<const T*>(a.q));
@@ -790,6 +792,26 @@ __global__ __launch_bounds__(256) void pack_kernel(const uint16_t* w, uint16_t* 
   const long long rb = blk / (d / 16);
   const uint16_t* src = w + (size_t)(rb * 32 + l % 32) * d + 16 * kb + 8 * (l / 32);
   *reinterpret_cast<uint4*>(out + (size_t)chunk * 8) = *reinterpret_cast<const uint4*>(src);
+}
+
+// ------------------------------------------------------------------ residual checkpoint store
+
+// One workgroup per (16-byte chunk block, row b): dst row b <- src row b.
+__global__ __launch_bounds__(256) void copy_rows_kernel(const char* src, size_t src_stride, char* dst, size_t dst_stride,
+                                                        int chunks) {
+  const int c = blockIdx.x * 256 + threadIdx.x;
+  if (c >= chunks) return;
+  const size_t b = blockIdx.y;
+  *reinterpret_cast<uint4*>(dst + b * dst_stride + (size_t)c * 16) =
+      *reinterpret_cast<const uint4*>(src + b * src_stride + (size_t)c * 16);
+}
+
+hipError_t launch_copy_rows(const void* src, size_t src_stride, void* dst, size_t dst_stride, size_t row_bytes, int B,
+                            hipStream_t st) {
+  const int chunks = (int)(row_bytes / 16);
+  hipLaunchKernelGGL(copy_rows_kernel, dim3((unsigned)((chunks + 255) / 256), (unsigned)B), dim3(256), 0, st,
+                     static_cast<const char*>(src), src_stride, static_cast<char*>(dst), dst_stride, chunks);
+  return hipGetLastError();
 }
 
 hipError_t launch_pack(const void* w, void* out, int rows, int d, hipStream_t st) {

@@ -140,6 +140,10 @@ size_t prefill_lds_bytes(int hd);
 // current.  Allocates nothing.
 hipError_t noalloc_scratch(void** out);
 
+// dst + b dst_stride <- src + b src_stride, row_bytes (a multiple of 16) each, b < B.
+hipError_t launch_copy_rows(const void* src, size_t src_stride, void* dst, size_t dst_stride, size_t row_bytes, int B,
+                            hipStream_t st);
+
 hipError_t launch_proj(const ProjArgs& a, int dtype_bf16, int hd, int packed, int n_units, hipStream_t st);
 // Current-token projection (T == 1): the streaming kernel for bf16, proj_kernel for fp32.
 hipError_t launch_project_current(const ProjArgs& a, int dtype_bf16, int hd, int packed, int n_units,

@@ -77,6 +77,8 @@ def _load() -> ctypes.CDLL:
         f = getattr(lib, name)
         f.argtypes = args
         f.restype = ctypes.c_int
+    lib.kvd_store_residual.argtypes = [S, VP, VP, I32, I32, I32, VP]
+    lib.kvd_store_residual.restype = ctypes.c_int
     lib.kvd_pack_weights.argtypes = [S, VP, I32, VP, VP]
     lib.kvd_pack_weights.restype = ctypes.c_int
     lib.kvd_pack_matrix.argtypes = [VP, I32, I32, VP, VP]
@@ -186,8 +188,9 @@ def _extent(t, name, want):
         raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {tuple(want)}")
 
 
-def _kv_extent(k, v, name, B, shape: "Shape", min_rows: int, t_off: int):
-    """k, v: [B, n_kv, t_cap, head_dim] with rows t_off .. t_off + min_rows - 1 inside t_cap."""
+def _kv_extent(k, v, name, B, shape: "Shape", min_rows: int, t_off: int, ring: bool = False):
+    """k, v: [B, n_kv, t_cap, head_dim] with rows t_off .. t_off + min_rows - 1 inside t_cap
+    (ring: the rows wrap modulo t_cap, so t_off < t_cap and min_rows <= t_cap)."""
     if k is None and v is None:
         return
     if k is None or v is None or k.dim() != 4:
@@ -195,7 +198,10 @@ def _kv_extent(k, v, name, B, shape: "Shape", min_rows: int, t_off: int):
     t_cap = k.shape[2]
     _extent(k, name + "_k", (B, shape.n_kv_heads, t_cap, shape.head_dim))
     _extent(v, name + "_v", (B, shape.n_kv_heads, t_cap, shape.head_dim))
-    if t_off < 0 or t_off + min_rows > t_cap:
+    if ring:
+        if t_off < 0 or t_off >= t_cap or min_rows > t_cap:
+            raise ValueError(f"{name}: {min_rows} rows from slot {t_off} do not fit a ring of {t_cap} slots")
+    elif t_off < 0 or t_off + min_rows > t_cap:
         raise ValueError(f"{name}: rows {t_off} .. {t_off + min_rows - 1} exceed t_cap {t_cap}")
 
 
@@ -322,6 +328,20 @@ def _attn(fn, shape, q, k, v, T, out, ws, t_off):
               _ptr(out, "out", dt, 3), wp, wb, _stream()))
 
 
+def kvd_store_residual(shape: Shape, h_new, ckpt, row: int):
+    """STORE_RESIDUAL: ckpt[b, row] = h_new[b] for every sequence (h_new [B, d], ckpt [B, c_ld, d])."""
+    dt = shape.torch_dtype
+    if not isinstance(h_new, torch.Tensor) or h_new.dim() != 2:
+        raise ValueError("h_new must be a [B, d_model] tensor")
+    B = h_new.shape[0]
+    _extent(h_new, "h_new", (B, shape.d_model))
+    if not isinstance(ckpt, torch.Tensor) or ckpt.dim() != 3:
+        raise ValueError("ckpt must be a [B, c_ld, d_model] tensor")
+    _extent(ckpt, "ckpt", (B, ckpt.shape[1], shape.d_model))
+    _check(lib.kvd_store_residual(ctypes.byref(shape.c()), _ptr(h_new, "h_new", dt, 2), _ptr(ckpt, "ckpt", dt, 3),
+                                  ckpt.shape[1], row, B, _stream()))
+
+
 def kvd_pack_weights(shape: Shape, w):
     """A packed copy (MFMA operand order) of a row-major [rows, d_model] bf16 weight matrix."""
     if not isinstance(w, torch.Tensor) or w.dim() != 2 or w.shape[1] != shape.d_model:
@@ -363,7 +383,7 @@ def _fused_extents(shape, q, h, T_rec, gamma, w_k, w_v, out, tail_k, tail_v, T_t
         _weights_extent(shape, gamma=gamma, w_k=w_k, w_v=w_v)
     if T_tail > 0 and tail_k is None:
         raise ValueError("tail_k / tail_v are required when T_tail > 0")
-    _kv_extent(tail_k, tail_v, "tail", B, shape, T_tail, tail_t_off)
+    _kv_extent(tail_k, tail_v, "tail", B, shape, T_tail, tail_t_off, ring=True)
     return B
 
 
