@@ -12,10 +12,17 @@ Per layer the step runs the whole hot path through libkvd's C ABI:
                             attention over [context || current token]; the workgroup that
                             completes a (sequence, KV head) merges its partials in-kernel
 
-Printed: ONE JSON line (tokens/s of the step, ms per step, the roofline of the
-fused kernel from HIP events over the timed region, the per-op us/layer, the
-cached-K/V and unfused baselines, the recompute-vs-cached-read crossover over
-batch size, and the CPU oracle baseline).
+Printed: ONE JSON line with
+  - tokens/s of the step, ms per step, and the roofline of the fused kernel from
+    HIP events over the timed region;
+  - per-op us/layer, and the cached-K/V and unfused baselines of the same step;
+  - the recompute-vs-cached-read crossover over batch size (Gemma-3-4B layer,
+    context 2048, B = 1..64; each op timed after a cache-evicting read);
+  - workloads: the SmolLM2-135M fp32 layer, the Qwen2.5-1.5B-shaped 28-layer step
+    (B = 8, context 16384) and the Gemma-3-4B multi-turn step (B = 16, turn
+    boundaries up to 5120 tokens), fused against cached;
+  - cpu_baseline: the fp64 oracle on the host cores for the headline step, and
+    cpu_baselines: bounded oracle samples of one layer of each other workload.
 """
 from __future__ import annotations
 
@@ -50,13 +57,13 @@ def parse():
                    help="size of one untimed device-to-device copy whose HBM counters calibrate the traffic figure")
     p.add_argument("--next", action="store_true",
                    help="also measure the hybrid cache budget sweep and the recompute-vs-transfer sweep over evicted tokens")
-    p.add_argument("--only", choices=["single_checkpoint", "sliding_window", "hybrid_budget", "evicted_tokens"],
-                   help="run only this one of the --next measurements and print its JSON (no headline line; "
-                        "for profiling its kernels)")
-    p.add_argument("--extra", action="store_true",
-                   help="also measure the Qwen-1.5B-shaped step (28 layers, B=8, 16384 ctx; fused vs cached) and "
-                        "the multi-turn conversation (Gemma 3-4B shape, B=16, a decode step at each of 20 turn "
-                        "boundaries of 256 tokens) into extra_workloads")
+    p.add_argument("--only", choices=["single_checkpoint", "sliding_window", "hybrid_budget", "evicted_tokens",
+                                       "crossover", "workloads", "cpu_baselines"],
+                   help="run only this one measurement and print its JSON (no headline line; for profiling its "
+                        "kernels)")
+    p.add_argument("--no-workloads", action="store_true",
+                   help="skip the other configurations' steps (SmolLM fp32 layer, Qwen-1.5B shape, multi-turn)")
+    p.add_argument("--all-turns", action="store_true", help="time all 20 turn boundaries of the multi-turn workload")
     return p.parse_args()
 
 
@@ -123,13 +130,17 @@ def main():
     from paper_2603_19664_amd import kvd
 
     torch.cuda.set_device(0)
+    turns = tuple(range(1, 21)) if args.all_turns else (1, 5, 10, 15, 20)
     if args.only:
         op_time = op_timer(torch, np, 3)
         fn = {"single_checkpoint": lambda: run_single_checkpoint(torch, np, kvd, configs, inputs, log),
               "sliding_window": lambda: run_sliding(torch, kvd, configs, inputs, log),
               "hybrid_budget": lambda: run_hybrid(torch, np, kvd, configs, inputs, op_time, log),
               "evicted_tokens": lambda: run_evicted(torch, np, kvd, configs, inputs, op_time, log)[
-                  "evicted_tokens"]}[args.only]
+                  "evicted_tokens"],
+              "crossover": lambda: run_crossover(args, torch, np, kvd, acc, configs, inputs, op_time, log),
+              "workloads": lambda: run_workloads(args, torch, np, kvd, acc, configs, inputs, log, turns),
+              "cpu_baselines": lambda: run_cpu_baselines(args, np, torch, configs, inputs, log)}[args.only]
         print(json.dumps({args.only: fn()}), flush=True)
         return
     dev = "cuda"
@@ -282,6 +293,9 @@ def main():
             cached.append(Call(lib.kvd_cached_attn, ctypes.byref(sc), P(q), ctypes.byref(vall), B, T + 1, P(out),
                                P(ws_c), ws_c.numel(), stream))
         per_op["cached_attn_us"] = op_time(cyc(cached), iters=2 * L)
+        # the 34 layers' cached attention back to back (no event between launches)
+        b2b = _step_timer(torch, lambda: [c() for c in cached], steps=max(3, K // 2), warmup=2) / L
+        per_op["cached_attn_us_back_to_back"] = 1e3 * b2b
 
         def cached_step():
             for l in range(L):
@@ -293,6 +307,10 @@ def main():
         cbytes = acc.cached_bytes(B, T + 1, nq, nkv, hd, 2, S_c)
         baselines["cached_attn_hbm_gbs"] = cbytes / (per_op["cached_attn_us"] * 1e-6) / 1e9
         baselines["cached_attn_hbm_frac"] = baselines["cached_attn_hbm_gbs"] / MI355X_HBM_PEAK_GBS
+        baselines["cached_attn_hbm_gbs_back_to_back"] = cbytes / (b2b * 1e-3) / 1e9
+        baselines["cached_attn_hbm_frac_back_to_back"] = baselines["cached_attn_hbm_gbs_back_to_back"] / \
+            MI355X_HBM_PEAK_GBS
+        baselines["cached_attn_splits"] = S_c
 
         # unfused recompute: recompute_kv writes K/V to HBM, decode_attn reads them back
         log("[bench] unfused recompute baseline")
@@ -360,26 +378,35 @@ def main():
         "crossover": crossover,
         "cpu_baseline": cpu,
     }
-    if args.extra or args.next:
-        del layers
-        torch.cuda.empty_cache()
+    del layers
+    torch.cuda.empty_cache()
+    if not args.no_workloads:
+        res["workloads"] = run_workloads(args, torch, np, kvd, acc, configs, inputs, log, turns)
+    if not args.no_cpu_baseline:
+        res["cpu_baselines"] = run_cpu_baselines(args, np, torch, configs, inputs, log)
     if args.next:
         res["next"] = run_next(args, torch, np, kvd, configs, inputs, op_time, log)
-    if args.extra:
-        res["extra_workloads"] = run_extra(args, torch, np, kvd, acc, configs, inputs, log)
     print(json.dumps(res), flush=True)
+
+
+def cold_flush(torch):
+    """A 1 GiB read that evicts L2 and the 256 MB Infinity Cache before a timed op.  A read,
+    not a write: a write flush leaves the Infinity Cache full of dirty lines, and their
+    write-back during the timed op cost a pure-read kernel up to 40% of its bandwidth
+    (measured on MI355X), which would flatter recompute against the cached read."""
+    buf = torch.ones(1 << 28, dtype=torch.float32, device="cuda")
+    return lambda: buf.sum()
 
 
 def run_crossover(args, torch, np, kvd, acc, configs, inputs, op_time, log):
     """Fused recompute-attention vs cached-K/V attention (each with its split-K merge) for one
     Gemma-3-4B-shaped layer, context 2048 + current token, over batch size.  Each
-    measurement runs after a 512 MiB write that evicts L2 and the Infinity Cache, so
-    both sides read their inputs from HBM."""
+    measurement runs after a cache-evicting read (cold_flush), so both sides read their
+    inputs from HBM."""
     wl = configs.GEMMA3_SWEEP
     s = kvd.shape_of(wl).packed()
     T = wl.ctx
-    flush_buf = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
-    flush = lambda: flush_buf.fill_(1)  # noqa: E731
+    flush = cold_flush(torch)
     rows = []
     for B in [int(x) for x in args.sweep_batches.split(",")]:
         log(f"[bench] crossover B={B}")
@@ -400,23 +427,28 @@ def run_crossover(args, torch, np, kvd, acc, configs, inputs, op_time, log):
         fz = lambda: kvd.kvd_fused_recompute_attn(s, q, h, T, gamma, w_k, w_v, pos0, out, ws_f, tk, tv, 1)  # noqa
         cz = lambda: kvd.kvd_cached_attn(s, q, Kc, Vc, T + 1, out, ws_c)  # noqa: E731
         it = 10
-        f_us = op_time(fz, iters=it, flush=flush)
-        c_us = op_time(cz, iters=it, flush=flush)
+        f_us = op_time(fz, iters=it, flush=flush, median=True)
+        c_us = op_time(cz, iters=it, flush=flush, median=True)
         fl = acc.fused_flops(B, T, 1, wl.n_q, wl.n_kv, wl.d_model, wl.head_dim)
-        cb = acc.cached_bytes(B, T + 1, wl.n_q, wl.n_kv, wl.head_dim, 2, kvd.kvd_num_splits(
-            s, kvd.KVD_OP_CACHED_ATTN, B, T + 1))
+        S_c = kvd.kvd_num_splits(s, kvd.KVD_OP_CACHED_ATTN, B, T + 1)
+        cb = acc.cached_bytes(B, T + 1, wl.n_q, wl.n_kv, wl.head_dim, 2, S_c)
         rows.append({"B": B, "fused_us": f_us, "cached_us": c_us, "ratio_fused_over_cached": f_us / c_us,
-                     "fused_tflops": fl / (f_us * 1e-6) / 1e12, "cached_gbs": cb / (c_us * 1e-6) / 1e9})
+                     "fused_tflops": fl / (f_us * 1e-6) / 1e12,
+                     "fused_mfma_frac": fl / (f_us * 1e-6) / 1e12 / MI355X_BF16_PEAK_TFLOPS,
+                     "cached_gbs": cb / (c_us * 1e-6) / 1e9,
+                     "cached_hbm_frac": cb / (c_us * 1e-6) / 1e9 / MI355X_HBM_PEAK_GBS, "cached_splits": S_c})
+        log(f"[bench] crossover B={B}: fused {f_us:.1f} us ({rows[-1]['fused_tflops']:.0f} TFLOP/s), cached "
+            f"{c_us:.1f} us ({rows[-1]['cached_gbs']:.0f} GB/s)")
         del h, Kc, Vc
         torch.cuda.empty_cache()
     faster = [r["B"] for r in rows if r["ratio_fused_over_cached"] < 1.0]
     return {"workload": wl.name, "ctx": T, "rows": rows, "batches_where_recompute_wins": faster,
-            "note": "each op timed with HIP events after a 512 MiB cache-evicting write; both include their split-K merge"}
+            "note": "medians of 10 calls, each after a 1 GiB cache-evicting read; both include their split-K merge"}
 
 
 def run_next(args, torch, np, kvd, configs, inputs, op_time, log):
     """Two measurements on one Gemma-3-4B-shaped layer (context 4096 + the current token),
-    each op timed with HIP events after a 512 MiB write that evicts L2 and the Infinity Cache:
+    each op timed with HIP events after a cache-evicting read (cold_flush):
 
     hybrid_budget: Algorithm 1 with a cache budget of W tokens.  The W most recent context
       tokens keep stored bf16 K/V and form the fused kernel's tail with the current token;
@@ -439,16 +471,15 @@ def run_next(args, torch, np, kvd, configs, inputs, op_time, log):
 def _next_setup(torch, kvd, configs, inputs):
     wl = configs.GEMMA3_4B
     s = kvd.shape_of(wl).packed()
-    flush_buf = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
+    flush = cold_flush(torch)
     gamma, w_q, w_k, w_v = inputs.weights(wl, 0, 0, "cuda")
     w_q, w_k, w_v = (kvd.kvd_pack_weights(s, w) for w in (w_q, w_k, w_v))
-    return wl, s, flush_buf, gamma, w_q, w_k, w_v
+    return wl, s, flush, gamma, w_q, w_k, w_v
 
 
 def run_hybrid(torch, np, kvd, configs, inputs, op_time, log):
     """The hybrid cache budget sweep (see run_next)."""
-    wl, s, flush_buf, gamma, w_q, w_k, w_v = _next_setup(torch, kvd, configs, inputs)
-    flush = lambda: flush_buf.fill_(1)  # noqa: E731
+    wl, s, flush, gamma, w_q, w_k, w_v = _next_setup(torch, kvd, configs, inputs)
     T, d, nkv, hd = wl.ctx, wl.d_model, wl.n_kv, wl.head_dim
     rows = []
     for B in (1, 8):
@@ -489,8 +520,7 @@ def run_hybrid(torch, np, kvd, configs, inputs, op_time, log):
 
 def run_evicted(torch, np, kvd, configs, inputs, op_time, log):
     """Recompute vs copy of N evicted tokens' K/V (see run_next)."""
-    wl, s, flush_buf, gamma, w_q, w_k, w_v = _next_setup(torch, kvd, configs, inputs)
-    flush = lambda: flush_buf.fill_(1)  # noqa: E731
+    wl, s, flush, gamma, w_q, w_k, w_v = _next_setup(torch, kvd, configs, inputs)
     T, nkv, hd = wl.ctx, wl.n_kv, wl.head_dim
     res = {}
     log("[bench] next: evicted tokens, recompute vs HBM copy vs host copy")
@@ -522,7 +552,7 @@ def run_evicted(torch, np, kvd, configs, inputs, op_time, log):
         "workload": "gemma3-4b layer, B=1; K/V of N evicted tokens (N * 4 KiB)", "rows": erows,
         "recompute_faster_than_hbm_copy": [e["N"] for e in erows if e["recompute_us"] < e["hbm_copy_us"]],
         "recompute_faster_than_host_copy": [e["N"] for e in erows if e["recompute_us"] < e["host_copy_us"]]}
-    del h, Kc, Vc, kv_dev, kv_host, flush_buf
+    del h, Kc, Vc, kv_dev, kv_host, flush
     torch.cuda.empty_cache()
     return res
 
@@ -688,27 +718,34 @@ def _step_timer(torch, step, steps, warmup):
     return a.elapsed_time(b) / steps
 
 
-def _model_layers(wl, s, kvd, inputs, L, B, T_cap, dev):
+def _model_layers(wl, s, kvd, inputs, L, B, T_cap, dev, packed=True):
     layers = []
+    pk = (lambda w: kvd.kvd_pack_weights(s, w)) if packed else (lambda w: w)  # noqa: E731
     for l in range(L):
         gamma, w_q, w_k, w_v = inputs.weights(wl, l, 0, dev)
         h, h_new = inputs.residuals(wl, l, B, T_cap, 0, dev)
-        layers.append(dict(gamma=gamma, w_q=kvd.kvd_pack_weights(s, w_q), w_k=kvd.kvd_pack_weights(s, w_k),
-                           w_v=kvd.kvd_pack_weights(s, w_v), h=h, h_new=h_new))
+        layers.append(dict(gamma=gamma, w_q=pk(w_q), w_k=pk(w_k), w_v=pk(w_v), h=h, h_new=h_new))
         del w_q, w_k, w_v
     return layers
 
 
-def run_extra(args, torch, np, kvd, acc, configs, inputs, log):
-    """Full decode steps of the two other workloads, through the same C ABI calls as
-    the headline step (per layer: kvd_project_qkv, then kvd_fused_recompute_attn with
-    the current token as a one-row tail and the split-K merge in-kernel)."""
+def run_workloads(args, torch, np, kvd, acc, configs, inputs, log, turns=(1, 5, 10, 15, 20), c4_steps=10):
+    """The other configurations' decode steps, through the same C ABI calls as the headline
+    step (per layer: kvd_project_qkv, then kvd_fused_recompute_attn with the current token as
+    a one-row tail and the split-K merge in-kernel), HIP events around back-to-back steps:
+
+      smollm_fp32: one SmolLM2-135M-shaped layer in fp32, 256 context tokens (the parity config);
+      qwen_1_5b:   28 Qwen2.5-1.5B-shaped layers, B = 8, 16384 context tokens at per-sequence
+                   position offsets, fused step against the cached-K/V step on the same inputs;
+      multiturn:   34 Gemma-3-4B-shaped layers, B = 16, a decode step at turn boundaries of the
+                   20 x 256-token conversation (checkpoints only; the cached step at turn 20 for
+                   comparison), with the HBM footprint of each scheme."""
     lib, dev = kvd.lib, "cuda"
     stream = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
     P = lambda t: ctypes.c_void_p(t.data_ptr())  # noqa: E731
     res = {}
 
-    def fused_calls(s, sc, layers, B, T, h_ld, pos0, pos_new, q, out, tail, ws):
+    def fused_calls(sc, layers, B, T, h_ld, pos0, pos_new, q, out, tail, ws):
         calls = []
         for ly in layers:
             calls.append(Call(lib.kvd_project_qkv, ctypes.byref(sc), P(ly["h_new"]), P(ly["gamma"]), P(ly["w_q"]),
@@ -718,12 +755,55 @@ def run_extra(args, torch, np, kvd, acc, configs, inputs, log):
                               P(out), P(ws), ws.numel(), None, stream))
         return calls
 
+    def cached_calls(sc, layers, caches, B, T, pos_new, q, out, wsc):
+        calls = []
+        for ly, (Kc, Vc, vrow, vall) in zip(layers, caches):
+            calls.append(Call(lib.kvd_project_qkv, ctypes.byref(sc), P(ly["h_new"]), P(ly["gamma"]), P(ly["w_q"]),
+                              P(ly["w_k"]), P(ly["w_v"]), P(pos_new), B, P(q), ctypes.byref(vrow), stream))
+            calls.append(Call(lib.kvd_cached_attn, ctypes.byref(sc), P(q), ctypes.byref(vall), B, T + 1, P(out),
+                              P(wsc), wsc.numel(), stream))
+        return calls
+
+    def prefill(s, layers, B, T, pos0):
+        caches = []
+        for ly in layers:
+            Kc = torch.empty((B, s.n_kv_heads, T + 1, s.head_dim), dtype=torch.bfloat16, device=dev)
+            Vc = torch.empty_like(Kc)
+            kvd.kvd_recompute_kv(s, ly["h"], ly["gamma"], ly["w_k"], ly["w_v"], pos0, T, Kc, Vc, 0)
+            caches.append((Kc, Vc, kvd.KvView(Kc.data_ptr(), Vc.data_ptr(), T + 1, T),
+                           kvd.KvView(Kc.data_ptr(), Vc.data_ptr(), T + 1, 0)))
+        return caches
+
+    # ---- SmolLM2-135M layer, fp32 (the parity config): one decode step
+    wl = configs.SMOLLM_FP32
+    s = kvd.shape_of(wl)
+    sc = s.c()
+    B, T = wl.batch, wl.ctx
+    log(f"[bench] workloads: {wl.name}")
+    layers = _model_layers(wl, s, kvd, inputs, 1, B, T, dev, packed=False)
+    pos0 = torch.zeros((B,), dtype=torch.int32, device=dev)
+    pos_new = torch.full((B,), T, dtype=torch.int32, device=dev)
+    q = torch.empty((B, wl.n_q, wl.head_dim), dtype=torch.float32, device=dev)
+    out = torch.empty_like(q)
+    tk = torch.zeros((B, wl.n_kv, 1, wl.head_dim), dtype=torch.float32, device=dev)
+    tv = torch.zeros_like(tk)
+    tail = kvd.KvView(tk.data_ptr(), tv.data_ptr(), 1, 0)
+    ws = kvd.workspace(s, kvd.KVD_OP_FUSED, B, T, 1)
+    calls = fused_calls(sc, layers, B, T, T, pos0, pos_new, q, out, tail, ws)
+    ms = _step_timer(torch, lambda: [c() for c in calls], steps=50, warmup=5)
+    res["smollm_fp32"] = {"workload": wl.name, "layers": 1, "batch": B, "ctx": T, "dtype": "f32",
+                          "us_per_layer": 1e3 * ms, "tok_s": B / (ms * 1e-3),
+                          "note": "the parity config: fp32 on the vector ALUs (no fp32 MFMA path), 12 workgroups "
+                                  "of 64 keys; latency bound"}
+    del layers, calls
+    torch.cuda.empty_cache()
+
     # ---- Qwen-1.5B shape: 28 layers, B = 8, 16384 checkpointed tokens + current token
     wl = configs.QWEN_1_5B
     s = kvd.shape_of(wl).packed()
     sc = s.c()
     L, B, T = wl.layers, wl.batch, wl.ctx
-    log(f"[bench] extra: {wl.name}: generating {L} layers")
+    log(f"[bench] workloads: {wl.name}: generating {L} layers")
     layers = _model_layers(wl, s, kvd, inputs, L, B, T, dev)
     pos0 = inputs.positions(wl, B).to(dev)
     pos_new = (pos0 + T).to(torch.int32)
@@ -733,34 +813,26 @@ def run_extra(args, torch, np, kvd, acc, configs, inputs, log):
     tv = torch.zeros_like(tk)
     tail = kvd.KvView(tk.data_ptr(), tv.data_ptr(), 1, 0)
     ws = kvd.workspace(s, kvd.KVD_OP_FUSED, B, T, 1)
-    calls = fused_calls(s, sc, layers, B, T, T, pos0, pos_new, q, out, tail, ws)
-    ms = _step_timer(torch, lambda: [c() for c in calls], steps=10, warmup=2)
+    calls = fused_calls(sc, layers, B, T, T, pos0, pos_new, q, out, tail, ws)
+    ms = _step_timer(torch, lambda: [c() for c in calls], steps=c4_steps, warmup=2)
     flops = L * acc.fused_flops(B, T, 1, wl.n_q, wl.n_kv, wl.d_model, wl.head_dim)
     entry = {"workload": wl.name, "layers": L, "batch": B, "ctx": T, "ms_per_step": ms, "tok_s": B / (ms * 1e-3),
-             "us_per_layer": 1e3 * ms / L, "fused_path_tflops": flops / (ms * 1e-3) / 1e12}
-    log(f"[bench] extra: {wl.name}: fused step {ms:.3f} ms")
-    # cached-K/V step on the same inputs: per-layer bf16 caches prefilled by the library
+             "us_per_layer": 1e3 * ms / L, "fused_path_tflops": flops / (ms * 1e-3) / 1e12,
+             "fused_path_mfma_frac": flops / (ms * 1e-3) / 1e12 / MI355X_BF16_PEAK_TFLOPS}
+    log(f"[bench] workloads: {wl.name}: fused step {ms:.3f} ms")
+    caches = prefill(s, layers, B, T, pos0)
     wsc = kvd.workspace(s, kvd.KVD_OP_CACHED_ATTN, B, T + 1)
-    ccalls, caches = [], []
-    for ly in layers:
-        Kc = torch.empty((B, wl.n_kv, T + 1, wl.head_dim), dtype=torch.bfloat16, device=dev)
-        Vc = torch.empty_like(Kc)
-        kvd.kvd_recompute_kv(s, ly["h"], ly["gamma"], ly["w_k"], ly["w_v"], pos0, T, Kc, Vc, 0)
-        vrow = kvd.KvView(Kc.data_ptr(), Vc.data_ptr(), T + 1, T)
-        vall = kvd.KvView(Kc.data_ptr(), Vc.data_ptr(), T + 1, 0)
-        caches.append((Kc, Vc, vrow, vall))
-        ccalls.append(Call(lib.kvd_project_qkv, ctypes.byref(sc), P(ly["h_new"]), P(ly["gamma"]), P(ly["w_q"]),
-                           P(ly["w_k"]), P(ly["w_v"]), P(pos_new), B, P(q), ctypes.byref(vrow), stream))
-        ccalls.append(Call(lib.kvd_cached_attn, ctypes.byref(sc), P(q), ctypes.byref(vall), B, T + 1, P(out),
-                           P(wsc), wsc.numel(), stream))
-    cms = _step_timer(torch, lambda: [c() for c in ccalls], steps=10, warmup=2)
+    ccalls = cached_calls(sc, layers, caches, B, T, pos_new, q, out, wsc)
+    cms = _step_timer(torch, lambda: [c() for c in ccalls], steps=c4_steps, warmup=2)
+    catt = _step_timer(torch, lambda: [c() for c in ccalls[1::2]], steps=c4_steps, warmup=2)
     cbytes = L * acc.cached_bytes(B, T + 1, wl.n_q, wl.n_kv, wl.head_dim, 2,
                                   kvd.kvd_num_splits(s, kvd.KVD_OP_CACHED_ATTN, B, T + 1))
     entry.update({"cached_ms_per_step": cms, "cached_tok_s": B / (cms * 1e-3),
-                  "cached_path_gbs": cbytes / (cms * 1e-3) / 1e9,
+                  "cached_attn_us_per_layer": 1e3 * catt / L, "cached_attn_gbs": cbytes / (catt * 1e-3) / 1e9,
+                  "cached_attn_hbm_frac": cbytes / (catt * 1e-3) / 1e9 / MI355X_HBM_PEAK_GBS,
                   "checkpoint_bytes": L * B * T * wl.d_model * 2,
                   "kv_cache_bytes": L * B * (T + 1) * 2 * wl.n_kv * wl.head_dim * 2})
-    log(f"[bench] extra: {wl.name}: cached step {cms:.3f} ms")
+    log(f"[bench] workloads: {wl.name}: cached step {cms:.3f} ms (attention {catt:.3f} ms)")
     res["qwen_1_5b"] = entry
     del layers, caches, calls, ccalls
     torch.cuda.empty_cache()
@@ -770,7 +842,7 @@ def run_extra(args, torch, np, kvd, acc, configs, inputs, log):
     s = kvd.shape_of(wl).packed()
     sc = s.c()
     L, B, Tmax = wl.layers, wl.batch, wl.turns * wl.turn_tokens
-    log(f"[bench] extra: {wl.name}: generating {L} layers of {Tmax}-token checkpoints")
+    log(f"[bench] workloads: {wl.name}: generating {L} layers of {Tmax}-token checkpoints")
     layers = _model_layers(wl, s, kvd, inputs, L, B, Tmax, dev)
     pos0 = torch.zeros((B,), dtype=torch.int32, device=dev)
     q = torch.empty((B, wl.n_q, wl.head_dim), dtype=torch.bfloat16, device=dev)
@@ -778,25 +850,107 @@ def run_extra(args, torch, np, kvd, acc, configs, inputs, log):
     tk = torch.zeros((B, wl.n_kv, 1, wl.head_dim), dtype=torch.bfloat16, device=dev)
     tv = torch.zeros_like(tk)
     tail = kvd.KvView(tk.data_ptr(), tv.data_ptr(), 1, 0)
-    turns = []
-    for k in range(1, wl.turns + 1):
+    rows = []
+    for k in turns:
         T = k * wl.turn_tokens
         pos_new = torch.full((B,), T, dtype=torch.int32, device=dev)
         ws = kvd.workspace(s, kvd.KVD_OP_FUSED, B, T, 1)
-        calls = fused_calls(s, sc, layers, B, T, Tmax, pos0, pos_new, q, out, tail, ws)
+        calls = fused_calls(sc, layers, B, T, Tmax, pos0, pos_new, q, out, tail, ws)
         ms = _step_timer(torch, lambda: [c() for c in calls], steps=3, warmup=1)
         flops = L * acc.fused_flops(B, T, 1, wl.n_q, wl.n_kv, wl.d_model, wl.head_dim)
-        turns.append({"turn": k, "ctx": T, "ms_per_step": ms, "tok_s": B / (ms * 1e-3), "us_per_layer": 1e3 * ms / L,
-                      "fused_path_tflops": flops / (ms * 1e-3) / 1e12,
-                      "checkpoint_bytes": L * B * T * wl.d_model * 2,
-                      "kv_cache_equiv_bytes": L * B * T * 2 * wl.n_kv * wl.head_dim * 2,
-                      "single_checkpoint_bytes": B * T * wl.d_model * 2,
-                      "workspace_bytes": ws.numel()})
-        log(f"[bench] extra: turn {k} ctx {T}: {ms:.3f} ms/step")
-    res["multiturn"] = {"workload": wl.name, "layers": L, "batch": B, "turn_tokens": wl.turn_tokens, "turns": turns}
-    del layers
+        rows.append({"turn": k, "ctx": T, "ms_per_step": ms, "tok_s": B / (ms * 1e-3), "us_per_layer": 1e3 * ms / L,
+                     "fused_path_tflops": flops / (ms * 1e-3) / 1e12,
+                     "fused_path_mfma_frac": flops / (ms * 1e-3) / 1e12 / MI355X_BF16_PEAK_TFLOPS,
+                     "checkpoint_bytes": L * B * T * wl.d_model * 2,
+                     "kv_cache_equiv_bytes": L * B * T * 2 * wl.n_kv * wl.head_dim * 2,
+                     "single_checkpoint_bytes": B * T * wl.d_model * 2, "workspace_bytes": ws.numel()})
+        log(f"[bench] workloads: turn {k} ctx {T}: {ms:.3f} ms/step")
+    entry = {"workload": wl.name, "layers": L, "batch": B, "turn_tokens": wl.turn_tokens, "turns": rows}
+    # the cached-K/V step at the last turn on the same inputs (per-layer prefilled caches)
+    T = Tmax
+    pos_new = torch.full((B,), T, dtype=torch.int32, device=dev)
+    caches = prefill(s, layers, B, T, pos0)
+    wsc = kvd.workspace(s, kvd.KVD_OP_CACHED_ATTN, B, T + 1)
+    ccalls = cached_calls(sc, layers, caches, B, T, pos_new, q, out, wsc)
+    cms = _step_timer(torch, lambda: [c() for c in ccalls], steps=3, warmup=1)
+    catt = _step_timer(torch, lambda: [c() for c in ccalls[1::2]], steps=3, warmup=1)
+    cbytes = L * acc.cached_bytes(B, T + 1, wl.n_q, wl.n_kv, wl.head_dim, 2,
+                                  kvd.kvd_num_splits(s, kvd.KVD_OP_CACHED_ATTN, B, T + 1))
+    entry["cached_last_turn"] = {"ctx": T, "ms_per_step": cms, "tok_s": B / (cms * 1e-3),
+                                 "attn_us_per_layer": 1e3 * catt / L, "attn_gbs": cbytes / (catt * 1e-3) / 1e9,
+                                 "attn_hbm_frac": cbytes / (catt * 1e-3) / 1e9 / MI355X_HBM_PEAK_GBS}
+    log(f"[bench] workloads: cached step at turn {wl.turns}: {cms:.3f} ms (attention {catt:.3f} ms)")
+    res["multiturn"] = entry
+    del layers, caches, ccalls
     torch.cuda.empty_cache()
     return res
+
+
+def machine_info():
+    model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return {"nproc": os.cpu_count(), "cpu_model": model,
+            "affinity_cpus": len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else None}
+
+
+def _oracle_threads():
+    import threadpoolctl
+    return max([i.get("num_threads", 1) for i in threadpoolctl.threadpool_info()] + [1])
+
+
+def run_cpu_baselines(args, np, torch, configs, inputs, log, budget_s=2.0):
+    """The fp64 oracle on the host cores for the other configurations, each on a bounded
+    sample of one layer (one sequence of the batch, and for the 16384-token workload the
+    first 2048 of its context tokens), repeated until budget_s is spent and scaled to the
+    whole layer's keys (the oracle's work is linear in sequences x keys)."""
+    import oracle as O
+
+    out = {}
+
+    def layer_sample(wl, T_full, B_full, T_sample, name, layer=0):
+        gamma, w_q, w_k, w_v = (inputs.to_f64(t) for t in inputs.weights(wl, layer, 0, "cpu"))
+        h, h_new = inputs.residuals(wl, layer, 1, T_sample, 0, "cpu")
+        h, h_new = inputs.to_f64(h), inputs.to_f64(h_new)
+        pos = np.arange(T_sample)[None, :]
+        spent, n = 0.0, 0
+        while spent < budget_s or n == 0:
+            t0 = time.perf_counter()
+            q, kt, vt = O.project_qkv(h_new, gamma, w_q, w_k, w_v, np.array([T_sample]), wl.n_q, wl.n_kv,
+                                      wl.head_dim, wl.rms_eps, wl.rope_theta)
+            O.kv_direct_decode(q, h, gamma, w_k, w_v, pos, kt[:, :, None], vt[:, :, None], wl.n_kv, wl.head_dim,
+                               wl.rms_eps, wl.rope_theta)
+            spent += time.perf_counter() - t0
+            n += 1
+        s_per = spent / n
+        scale = (B_full * (T_full + 1)) / (T_sample + 1)
+        layer_s = s_per * scale
+        out[name] = {"workload": wl.name, "us_per_layer": layer_s * 1e6, "tok_s_per_layer": B_full / layer_s,
+                     "sample": f"one sequence, {T_sample} context tokens + current, {n} runs in {spent:.2f} s; "
+                               f"scaled x{scale:.1f} to B={B_full}, {T_full} + 1 keys"}
+        log(f"[bench] cpu oracle {name}: {layer_s * 1e3:.1f} ms per layer")
+
+    wl = configs.SMOLLM_FP32
+    layer_sample(wl, wl.ctx, 1, wl.ctx, "smollm_fp32_layer")
+    wl = configs.GEMMA3_SWEEP
+    layer_sample(wl, wl.ctx, 1, wl.ctx, "gemma_ctx2048_b1_layer")
+    out["gemma_ctx2048_b8_layer"] = dict(out["gemma_ctx2048_b1_layer"])
+    for k in ("us_per_layer",):
+        out["gemma_ctx2048_b8_layer"][k] *= 8
+    out["gemma_ctx2048_b8_layer"]["tok_s_per_layer"] = out["gemma_ctx2048_b1_layer"]["tok_s_per_layer"]
+    out["gemma_ctx2048_b8_layer"]["sample"] = "the B=1 sample above, scaled x8 (sequences are independent)"
+    wl = configs.QWEN_1_5B
+    layer_sample(wl, wl.ctx, wl.batch, 2048, "qwen_ctx16384_b8_layer")
+    wl = configs.GEMMA3_MULTITURN
+    for T in (256, 2560, 5120):
+        layer_sample(wl, T, wl.batch, T, f"multiturn_b16_ctx{T}_layer")
+    return {"kind": "oracle", "cores": _oracle_threads(), **machine_info(), "configs": out}
 
 
 def run_cpu_baseline(args, np, wl, layers, T, B, inputs, log):
@@ -826,6 +980,7 @@ def run_cpu_baseline(args, np, wl, layers, T, B, inputs, log):
     cores = max([i.get("num_threads", 1) for i in threadpoolctl.threadpool_info()] + [1])
     log(f"[bench] cpu oracle: {done} layers in {spent:.1f} s on {cores} threads")
     return {"value": B * (done / wl.layers) / spent, "unit": "tok/s", "cores": cores, "kind": "oracle",
+            **machine_info(),
             "sample": f"{done} layer evaluations ({done / wl.layers:.2f} steps of {wl.layers} layers) of the decode step (B={B}, {T} context tokens + current "
                       f"token), fp64 numpy oracle, scaled to the full step; {spent:.1f} s"}
 
