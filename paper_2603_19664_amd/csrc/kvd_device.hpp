@@ -944,15 +944,20 @@ __device__ __forceinline__ void combine_rows(const float* ws_acc, const float* w
     for (int s0 = 0, blk = 0; s0 < S; s0 += 64, ++blk) {
       const int cnt = min(64, S - s0);
       const float* a = abase + (size_t)s0 * HD;
-      // the block's accumulators: every load in flight before any wait.  Past the
-      // last split the loads repeat split cnt - 1 (in bounds, finite): their
-      // weights below are zero, and the loads stay straight-line code.
+      // the block's accumulators: every load in flight before any wait, in chunks
+      // of 8 splits (a uniform branch per chunk; within the last chunk, loads past
+      // the last split repeat split cnt - 1: in bounds and finite, weight zero)
       float x[CPT][64];
 #pragma unroll
       for (int k = 0; k < CPT; ++k) {
         if (rv[k]) {
 #pragma unroll
-          for (int e = 0; e < 64; ++e) x[k][e] = load_dev(a + (size_t)min(e, cnt - 1) * HD + aoff[k]);
+          for (int e0 = 0; e0 < 64; e0 += 8) {
+            if (e0 < cnt) {
+#pragma unroll
+              for (int e = e0; e < e0 + 8; ++e) x[k][e] = load_dev(a + (size_t)min(e, cnt - 1) * HD + aoff[k]);
+            }
+          }
         }
       }
       if (mine) {
@@ -974,13 +979,19 @@ __device__ __forceinline__ void combine_rows(const float* ws_acc, const float* w
         wsh[wave * 64 + lane] = w;
       }
       __syncthreads();
-      // w = 0 past the last split: those terms add an exact zero
+      // chunks past the last split are skipped; inside the last chunk w = 0 past
+      // the last split, so those terms add an exact zero
 #pragma unroll
       for (int k = 0; k < CPT; ++k) {
         if (rv[k]) {
           const float* wp = wsh + (rr + k * RPH) * 64;
 #pragma unroll
-          for (int e = 0; e < 64; ++e) o[k] = fmaf(x[k][e], wp[e], o[k]);
+          for (int e0 = 0; e0 < 64; e0 += 8) {
+            if (e0 < cnt) {
+#pragma unroll
+              for (int e = e0; e < e0 + 8; ++e) o[k] = fmaf(x[k][e], wp[e], o[k]);
+            }
+          }
         }
       }
       __syncthreads();

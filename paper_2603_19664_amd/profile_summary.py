@@ -3,6 +3,9 @@
     python -m paper_2603_19664_amd.profile_summary stats <run_kernel_stats.csv> "<command>" > profiles/X.md
     python -m paper_2603_19664_amd.profile_summary trace <run_kernel_trace.csv> "<command>" > profiles/X.md
     python -m paper_2603_19664_amd.profile_summary pmc <dir with p*/run_counter_collection.csv> <kernel substring> "<command>"
+    python -m paper_2603_19664_amd.profile_summary pmc_by_grid <dir>[,<dir>...] <kernel substring> "<command>"
+    python -m paper_2603_19664_amd.profile_summary pmc_seq <dir>[,<dir>...] <kernel> <block> <label,...> "<command>" [<copy kernel> <copy bytes>]
+    python -m paper_2603_19664_amd.profile_summary sweep_traffic <fetch dir> <write dir> <trace csv> <kernel> <block> <label,...> <copy kernel> <copy bytes> "<command>"
     python -m paper_2603_19664_amd.profile_summary traffic <fetch dir> <write dir> <kernel> <copy kernel> <copy bytes> <workload> "<command>"
 """
 from __future__ import annotations
@@ -56,6 +59,120 @@ def pmc(directory: str, kernel: str, command: str) -> str:
     return "\n".join(out) + "\n"
 
 
+def _rows(directory):
+    for p in sorted(glob.glob(os.path.join(directory, "**", "*counter_collection.csv"), recursive=True)):
+        yield from csv.DictReader(open(p))
+
+
+def _wgs(r):
+    grid = r.get("Grid_Size") or r.get("Grid_Size_X") or "0"
+    wg = r.get("Workgroup_Size") or r.get("Workgroup_Size_X") or "1"
+    return int(grid) // max(int(wg), 1)
+
+
+def pmc_by_grid(directories, kernel: str, command: str) -> str:
+    """Mean per dispatch of every counter of `kernel`, one row per grid size (the number
+    of workgroups tells the workload shapes of one run apart)."""
+    agg = collections.defaultdict(lambda: collections.defaultdict(list))
+    for d in directories:
+        for r in _rows(d):
+            if kernel in r["Kernel_Name"]:
+                agg[_wgs(r)][r["Counter_Name"]].append(float(r["Counter_Value"]))
+    names = sorted({c for g in agg.values() for c in g})
+    out = ["# rocprofv3 counters per grid", "", f"Kernel: `{kernel}`", "",
+           "Command (repository root, one MI355X; one rocprofv3 run per counter group):", "", "```", command, "```", "",
+           "| workgroups | dispatches | " + " | ".join(names) + " |", "|---" * (len(names) + 2) + "|"]
+    for wgs in sorted(agg):
+        g = agg[wgs]
+        n = max(len(v) for v in g.values())
+        out.append(f"| {wgs} | {n} | " + " | ".join(f"{sum(g[c]) / len(g[c]):.6g}" if g.get(c) else "-"
+                                                     for c in names) + " |")
+    return "\n".join(out) + "\n"
+
+
+def pmc_seq(directories, kernel: str, block: int, labels, command: str, copy_kernel: str = "",
+            copy_bytes: int = 0) -> str:
+    """Counters of `kernel` in dispatch order, `block` consecutive dispatches per label (a sweep
+    that launches the kernel `block` times per point, points in the order of `labels`).  With a
+    calibration copy (copy_kernel, copy_bytes: the largest dispatch of that kernel in each run),
+    FETCH_SIZE and WRITE_SIZE are also given in bytes per dispatch."""
+    agg = collections.defaultdict(lambda: collections.defaultdict(list))
+    scale = {}
+    for d in directories:
+        rows = sorted(_rows(d), key=lambda r: int(r["Dispatch_Id"]))
+        seen = collections.defaultdict(int)
+        for r in rows:
+            c = r["Counter_Name"]
+            # the calibration copy is the run's first dispatch of the copy kernel
+            if copy_kernel and copy_kernel in r["Kernel_Name"] and c in ("FETCH_SIZE", "WRITE_SIZE") and c not in scale:
+                scale[c] = float(r["Counter_Value"])
+            if kernel in r["Kernel_Name"]:
+                i = seen[c]
+                seen[c] += 1
+                if i // block < len(labels):
+                    agg[labels[i // block]][c].append(float(r["Counter_Value"]))
+    names = sorted({c for g in agg.values() for c in g})
+    extra = [f"{c} bytes" for c in ("FETCH_SIZE", "WRITE_SIZE") if c in names and c in scale]
+    out = ["# rocprofv3 counters per sweep point", "", f"Kernel: `{kernel}`, {block} dispatches per point, in order: "
+           + ", ".join(labels), "", "Command (repository root, one MI355X; one rocprofv3 run per counter group):", "",
+           "```", command, "```", ""]
+    if extra:
+        out += [f"FETCH_SIZE / WRITE_SIZE (KiB) scaled to bytes by a {copy_bytes}-byte copy in the same run "
+                f"({', '.join(f'{c} {scale[c]:.0f} KiB' for c in scale)}).", ""]
+    out += ["| point | dispatches | " + " | ".join(names + extra) + " |", "|---" * (len(names) + len(extra) + 2) + "|"]
+    for lab in labels:
+        g = agg.get(lab)
+        if not g:
+            continue
+        n = max(len(v) for v in g.values())
+        vals = [f"{sum(g[c]) / len(g[c]):.6g}" if g.get(c) else "-" for c in names]
+        for c in ("FETCH_SIZE", "WRITE_SIZE"):
+            if f"{c} bytes" in extra:
+                vals.append(f"{sum(g[c]) / len(g[c]) * copy_bytes / scale[c]:.4g}")
+        out.append(f"| {lab} | {n} | " + " | ".join(vals) + " |")
+    return "\n".join(out) + "\n"
+
+
+def sweep_traffic(fetch_dir: str, write_dir: str, trace_csv: str, kernel: str, block: int, labels, copy_kernel: str,
+                  copy_bytes: int, command: str, peak_gbs: float = 8000.0) -> str:
+    """Per sweep point (block consecutive dispatches of `kernel` per label): the kernel-trace
+    duration, FETCH_SIZE + WRITE_SIZE in bytes (scaled by the run's first copy-kernel dispatch,
+    a copy of copy_bytes), and the HBM rate they give against peak_gbs."""
+    def seq(rows, pick):
+        out = collections.defaultdict(list)
+        for i, v in enumerate(pick(r) for r in rows):
+            if i // block < len(labels):
+                out[labels[i // block]].append(v)
+        return out
+
+    def counter(directory, name):
+        rows = sorted((r for r in _rows(directory) if r["Counter_Name"] == name), key=lambda r: int(r["Dispatch_Id"]))
+        cal = next(float(r["Counter_Value"]) for r in rows if copy_kernel in r["Kernel_Name"])
+        mine = [r for r in rows if kernel in r["Kernel_Name"]]
+        return seq(mine, lambda r: float(r["Counter_Value"]) * copy_bytes / cal)
+
+    tr = sorted((r for r in csv.DictReader(open(trace_csv)) if kernel in r["Kernel_Name"]),
+                key=lambda r: int(r["Start_Timestamp"]))
+    dur = seq(tr, lambda r: (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3)
+    fe, wr = counter(fetch_dir, "FETCH_SIZE"), counter(write_dir, "WRITE_SIZE")
+    out = ["# HBM traffic and rate per sweep point", "", f"Kernel: `{kernel}`, {block} dispatches per point, in order: "
+           + ", ".join(labels), "", "Commands (repository root, one MI355X; a kernel trace and one counter run per counter):",
+           "", "```", command, "```", "",
+           f"Counter bytes are FETCH_SIZE / WRITE_SIZE scaled by the first `{copy_kernel}` dispatch of the same run (a "
+           f"{copy_bytes}-byte copy).  Rate = (fetch + write) / mean trace duration; peak {peak_gbs:.0f} GB/s.", "",
+           "| point | mean duration (us) | fetch (MB) | write (MB) | rate (GB/s) | fraction of peak |",
+           "|---|---|---|---|---|---|"]
+    for lab in labels:
+        if not dur.get(lab):
+            continue
+        d = sum(dur[lab]) / len(dur[lab])
+        f = sum(fe[lab]) / len(fe[lab])
+        w = sum(wr[lab]) / len(wr[lab])
+        gbs = (f + w) / (d * 1e-6) / 1e9
+        out.append(f"| {lab} | {d:.1f} | {f / 1e6:.2f} | {w / 1e6:.3f} | {gbs:.0f} | {gbs / peak_gbs:.3f} |")
+    return "\n".join(out) + "\n"
+
+
 def traffic(fetch_dir: str, write_dir: str, kernel: str, copy_kernel: str, copy_bytes: int, workload: str,
             source_hash: str, command: str) -> dict:
     """Per-launch HBM bytes of `kernel` from a FETCH_SIZE run and a WRITE_SIZE run, each scaled by
@@ -65,16 +182,16 @@ def traffic(fetch_dir: str, write_dir: str, kernel: str, copy_kernel: str, copy_
         for p in glob.glob(os.path.join(directory, "**", "*counter_collection.csv"), recursive=True):
             for r in csv.DictReader(open(p)):
                 if name in r["Kernel_Name"] and r["Counter_Name"] == counter:
-                    v.append(float(r["Counter_Value"]))
+                    v.append((int(r["Dispatch_Id"]), float(r["Counter_Value"])))
         if not v:
             raise SystemExit(f"no {counter} samples for {name} under {directory}")
-        return v
+        return [x for _, x in sorted(v)]
     fv = values(fetch_dir, "FETCH_SIZE", kernel)
     wv = values(write_dir, "WRITE_SIZE", kernel)
     f_k, nf, w_k, nw = sum(fv) / len(fv), len(fv), sum(wv) / len(wv), len(wv)
-    # the calibration copy is the largest dispatch of the copy kernel in the run
-    f_c = max(values(fetch_dir, "FETCH_SIZE", copy_kernel))
-    w_c = max(values(write_dir, "WRITE_SIZE", copy_kernel))
+    # the calibration copy is the run's first dispatch of the copy kernel (made before anything else)
+    f_c = values(fetch_dir, "FETCH_SIZE", copy_kernel)[0]
+    w_c = values(write_dir, "WRITE_SIZE", copy_kernel)[0]
     ff = copy_bytes / (f_c * 1024.0)
     fw = copy_bytes / (w_c * 1024.0)
     fetch = f_k * 1024.0 * ff
@@ -93,6 +210,17 @@ if __name__ == "__main__":
         sys.stdout.write(trace(sys.argv[2], sys.argv[3]))
     elif mode == "pmc":
         sys.stdout.write(pmc(sys.argv[2], sys.argv[3], sys.argv[4]))
+    elif mode == "pmc_by_grid":
+        sys.stdout.write(pmc_by_grid(sys.argv[2].split(","), sys.argv[3], sys.argv[4]))
+    elif mode == "pmc_seq":
+        dirs, kernel, block, labels, command = sys.argv[2:7]
+        copy_kernel, copy_bytes = (sys.argv[7], int(sys.argv[8])) if len(sys.argv) > 8 else ("", 0)
+        sys.stdout.write(pmc_seq(dirs.split(","), kernel, int(block), labels.split(","), command, copy_kernel,
+                                 copy_bytes))
+    elif mode == "sweep_traffic":
+        fetch_dir, write_dir, trace_csv, kernel, block, labels, copy_kernel, copy_bytes, command = sys.argv[2:11]
+        sys.stdout.write(sweep_traffic(fetch_dir, write_dir, trace_csv, kernel, int(block), labels.split(","),
+                                       copy_kernel, int(copy_bytes), command))
     elif mode == "traffic":
         import json
         fetch_dir, write_dir, kernel, copy_kernel, copy_bytes, workload, command = sys.argv[2:9]
