@@ -117,8 +117,10 @@ typedef struct {
  * over d_model per output element, one sum-of-squares order), so prefill,
  * recompute, kvd_project_qkv's K/V and the fused kernel's K/V are bit-identical
  * for the same residual row and position (Prop. reconstruction).  A bf16 call of
- * at most 64 rows (B * T) runs on the current-token projection's kernel, which
- * serves a few rows at far lower latency than the 64-row tile engine.
+ * few rows (at most 512 workgroups of 32 K/V rows x 16 tokens: 128 tokens of
+ * the Gemma-3-4B shape, 512 of the Qwen2.5-1.5B shape) runs on the
+ * current-token projection's kernel, which serves them at lower latency than
+ * the 64-token tile engine.
  *   h     [B][h_ld][d_model], h_ld >= T.      pos0  [B] int32.
  *   out   K/V view written at rows out->t_off .. out->t_off+T-1.
  * B == 0 or T == 0 is a no-op.                                                */

@@ -279,8 +279,10 @@ kvd_status kvd_recompute_kv(const kvd_attn_shape* shape, const void* h, int32_t 
   a.n_kv_units = shape->n_kv_heads;
   a.eps = shape->rms_eps;
   fill_rev(shape, a.rev);
-  if (shape->dtype == KVD_BF16 && (long long)B * T <= kvd::kStreamRecomputeMaxTokens &&
-      kvd::stream_group(shape->d_model, B * T, kLdsLimit) >= 1)
+  const int G = (long long)B * T <= INT32_MAX ? kvd::stream_group(shape->d_model, B * T, kLdsLimit) : 0;
+  const long long stream_wgs =
+      G >= 1 ? (long long)(2 * shape->n_kv_heads * shape->head_dim / 32) * (((long long)B * T + G - 1) / G) : 0;
+  if (shape->dtype == KVD_BF16 && G >= 1 && stream_wgs <= kvd::kStreamRecomputeMaxWgs)
     return device_status(kvd::launch_project_current(a, 1, shape->head_dim, shape->w_layout == KVD_W_PACKED,
                                                      a.n_kv_units, (hipStream_t)stream),
                          "kvd_recompute_kv launch");

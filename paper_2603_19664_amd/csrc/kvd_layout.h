@@ -150,10 +150,15 @@ constexpr int kStreamWaves = 5;
 constexpr int kStreamChunk = 2;
 constexpr int kStreamSlots = 4;
 constexpr int kStreamDepth = 10;
-// A bf16 recompute of at most this many token rows runs on the streaming
-// projection (its MFMA chain is the tile engine's, so the K/V are identical):
-// the tile engine takes a whole K-loop per 64-token tile whatever the count.
-constexpr int kStreamRecomputeMaxTokens = 64;
+// A bf16 recompute runs on the streaming projection (its MFMA chain is the tile
+// engine's, so the K/V are identical) while that kernel's grid, one workgroup
+// per (32 K/V rows, group of up to kProjTok tokens), has at most this many
+// workgroups: about two rounds of the chip.  The tile engine takes one whole
+// K-loop over d_model per 64-token tile whatever the count (55 us at d 2560,
+// 25 us at d 1536, measured); the streaming kernel's time grows with its rounds
+// and wins up to two of them (Gemma-3-4B shape: 128 tokens in 36 us; Qwen2.5-
+// 1.5B shape: 512 tokens in 21 us).
+constexpr long long kStreamRecomputeMaxWgs = 512;
 constexpr size_t kStreamSlotBytes = (size_t)32 * kKT * 2 * kStreamChunk;
 struct StreamLds {
   size_t rev, rinv, pos, gam, ring, hb, hs, end;

@@ -190,7 +190,8 @@ def test_prefill_equals_recompute_bitwise(dtype):
     L = make_layer(wl, B=3, T=300, seed=21, pos0=[0, 17, 4000])
     Kp, Vp = gpu_recompute(L)                     # prefill: every token at once
     # recompute of sub-ranges with odd lengths, at other offsets and capacities (in bf16,
-    # B * T <= 64 rows run on the streaming kernel, longer ones on the tile engine)
+    # calls of at most 512 streaming workgroups, here 64 per 16 rows, run on the
+    # streaming kernel: (0, 1), (66, 67), (299, 300), (100, 120); the others on the tile engine)
     for a, b in [(0, 1), (1, 66), (66, 67), (67, 299), (299, 300), (5, 250), (100, 120)]:
         Lr = dataclasses.replace(L, h=L.h[:, a:b].contiguous(), T=b - a, pos0=(L.pos0 + a).to(torch.int32))
         K, V = gpu_recompute(Lr, t_cap=b - a + 9, t_off=7)
@@ -206,6 +207,21 @@ def test_prefill_equals_recompute_bitwise(dtype):
     # run to run
     K2, V2 = gpu_recompute(L)
     assert torch.equal(_bits(K2), _bits(Kp)) and torch.equal(_bits(V2), _bits(Vp))
+
+
+def test_long_recompute_on_the_streaming_kernel_bitwise():
+    # Qwen2.5-1.5B layer shape (2 KV heads of 128: 16 streaming workgroups per 16 rows):
+    # a 500-token recompute runs on the streaming kernel (512 workgroups), the 2 x 600
+    # prefill on the tile engine; the K/V agree bit for bit
+    L = make_layer(C.QWEN_1_5B, B=2, T=600, seed=33)
+    Kp, Vp = gpu_recompute(L)
+    Lr = dataclasses.replace(L, B=1, h=L.h[1:2, 50:550].contiguous(), T=500,
+                             pos0=(L.pos0[1:2] + 50).to(torch.int32))
+    K, V = gpu_recompute(Lr, t_cap=503, t_off=3)
+    assert torch.equal(_bits(K[0, :, 3:]), _bits(Kp[1, :, 50:550]))
+    assert torch.equal(_bits(V[0, :, 3:]), _bits(Vp[1, :, 50:550]))
+    Kr, Vr = oracle_kv(Lr)
+    check("K (streaming, 500 rows) vs oracle", K[:, :, 3:], Kr, 2e-2)
 
 
 @pytest.mark.parametrize("dtype", [BF, F32])
