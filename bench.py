@@ -58,7 +58,7 @@ def parse():
     p.add_argument("--next", action="store_true",
                    help="also measure the hybrid cache budget sweep and the recompute-vs-transfer sweep over evicted tokens")
     p.add_argument("--only", choices=["single_checkpoint", "sliding_window", "hybrid_budget", "evicted_tokens",
-                                       "crossover", "workloads", "cpu_baselines"],
+                                       "bounded_cache", "crossover", "workloads", "cpu_baselines"],
                    help="run only this one measurement and print its JSON (no headline line; for profiling its "
                         "kernels)")
     p.add_argument("--no-workloads", action="store_true",
@@ -147,6 +147,7 @@ def main():
               "hybrid_budget": lambda: run_hybrid(torch, np, kvd, configs, inputs, op_time, log),
               "evicted_tokens": lambda: run_evicted(torch, np, kvd, configs, inputs, op_time, log)[
                   "evicted_tokens"],
+              "bounded_cache": lambda: run_bounded_cache(torch, np, kvd, configs, inputs, log),
               "crossover": lambda: run_crossover(args, torch, np, kvd, acc, configs, inputs, op_time, log),
               "workloads": lambda: run_workloads(args, torch, np, kvd, acc, configs, inputs, log, turns),
               "cpu_baselines": lambda: run_cpu_baselines(args, np, torch, configs, inputs, log)}[args.only]
@@ -460,7 +461,8 @@ def run_next(args, torch, np, kvd, configs, inputs, op_time, log):
       their checkpoints (kvd_recompute_kv), copied from a bf16 copy in HBM, and copied from a
       bf16 copy in pinned host memory over PCIe (token-major, so each is one contiguous copy).
       Medians of 11 calls (a PCIe copy occasionally takes far longer)."""
-    res = {"hybrid_budget": run_hybrid(torch, np, kvd, configs, inputs, op_time, log)}
+    res = {"hybrid_budget": run_hybrid(torch, np, kvd, configs, inputs, op_time, log),
+           "bounded_cache": run_bounded_cache(torch, np, kvd, configs, inputs, log)}
     res.update(run_evicted(torch, np, kvd, configs, inputs, op_time, log))
     res["sliding_window"] = run_sliding(torch, kvd, configs, inputs, log)
     res["single_checkpoint"] = run_single_checkpoint(torch, np, kvd, configs, inputs, log)
@@ -515,6 +517,66 @@ def run_hybrid(torch, np, kvd, configs, inputs, op_time, log):
                           "us_per_stored_token_read": read_per_token,
                           "us_per_recomputed_token": read_per_token - b}
     return {"workload": "gemma3-4b layer, ctx 4096 + current token", "rows": rows, "per_token_costs": slopes}
+
+
+def run_bounded_cache(torch, np, kvd, configs, inputs, log, steps=300, budgets=(0, 64, 256, 1024), start=4096):
+    """Algorithm 1's bounded cache in a decode loop (paper_2603_19664_amd.budget.BoundedCache):
+    one Gemma-3-4B-shaped layer, B = 1 and 8, a history of `start` tokens (the last `budget`
+    of them in the cache ring, the rest evicted to checkpoints), then `steps` decode steps
+    (STORE_RESIDUAL, Q/K_t/V_t into the ring, fused recompute + attention, eviction).  Reports
+    the device time per step (HIP events around the loop; the three launches of a step are
+    issued from Python) and the fused call's own time, and the memory per layer and sequence
+    against Eq. total_mem."""
+    from paper_2603_19664_amd.budget import BoundedCache
+    wl = configs.GEMMA3_4B
+    s = kvd.shape_of(wl).packed()
+    gamma, w_q, w_k, w_v = inputs.weights(wl, 0, 0, "cuda")
+    w_q, w_k, w_v = (kvd.kvd_pack_weights(s, w) for w in (w_q, w_k, w_v))
+    rows = []
+    for B in (1, 8):
+        h_all, _ = inputs.residuals(wl, 0, B, start + steps, 0, "cuda")
+        pos0 = torch.zeros((B,), dtype=torch.int32, device="cuda")
+        for budget in budgets:
+            log(f"[bench] next: bounded cache B={B} budget={budget}")
+            cache = BoundedCache(s, B, budget, start + steps, pos0)
+            st = cache.state
+            cache.ckpt[:, :start].copy_(h_all[:, :start])           # the history's checkpoints
+            st.T, st.T_rec, st.head, st.n_cached = start, start - budget, 0, budget
+            if budget > 0:                                          # the cached tokens' K/V, ring slots 0..budget-1
+                kvd.kvd_recompute_kv(s, h_all[:, start - budget:start].contiguous(), gamma, w_k, w_v,
+                                     (pos0 + start - budget).to(torch.int32), budget, cache.ring_k, cache.ring_v, 0)
+            out = torch.empty((B, s.n_q_heads, s.head_dim), dtype=torch.bfloat16, device="cuda")
+            h_steps = [h_all[:, start + i].contiguous() for i in range(steps)]
+            torch.cuda.synchronize()
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            for i in range(steps):
+                cache.step(h_steps[i], gamma, w_q, w_k, w_v, out)
+            b.record()
+            torch.cuda.synchronize()
+            step_us = a.elapsed_time(b) * 1e3 / steps
+            # the fused call alone at the final state's shape
+            ws = cache.ws
+            fz = lambda: kvd.kvd_fused_recompute_attn(s, cache.q, cache.ckpt, st.T_rec, gamma, w_k, w_v, pos0, out,  # noqa
+                                                     ws, cache.ring_k, cache.ring_v, st.n_cached + 1, st.head)
+            for _ in range(3):
+                fz()
+            ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(20)]
+            for e0, e1 in ev:
+                e0.record()
+                fz()
+                e1.record()
+            torch.cuda.synchronize()
+            fused_us = float(np.median([e0.elapsed_time(e1) for e0, e1 in ev])) * 1e3
+            m = st.memory_bytes(s.d_model, s.n_kv_heads, s.head_dim, 2)
+            rows.append({"B": B, "budget": budget, "tokens_after": st.T, "recomputed": st.T_rec,
+                         "cached": st.n_cached, "us_per_step_loop": step_us, "fused_us": fused_us,
+                         "memory_per_layer_seq": m})
+            log(f"[bench] next: bounded cache B={B} budget={budget}: {step_us:.1f} us/step, fused {fused_us:.1f} us")
+            del cache
+        del h_all
+        torch.cuda.empty_cache()
+    return {"workload": f"gemma3-4b layer, {start} tokens of history then {steps} decode steps", "rows": rows}
 
 
 def run_evicted(torch, np, kvd, configs, inputs, op_time, log):

@@ -117,10 +117,10 @@ typedef struct {
  * over d_model per output element, one sum-of-squares order), so prefill,
  * recompute, kvd_project_qkv's K/V and the fused kernel's K/V are bit-identical
  * for the same residual row and position (Prop. reconstruction).  A bf16 call of
- * few rows (at most 512 workgroups of 32 K/V rows x 16 tokens: 128 tokens of
- * the Gemma-3-4B shape, 512 of the Qwen2.5-1.5B shape) runs on the
- * current-token projection's kernel, which serves them at lower latency than
- * the 64-token tile engine.
+ * few rows (at most 512 workgroups of 32 K/V rows x up to 16 tokens, 1024 for
+ * head_dim 256: about 180 tokens of the Gemma-3-4B shape, 512 of the
+ * Qwen2.5-1.5B shape) runs on the current-token projection's kernel, which
+ * serves them at lower latency than the 64-token tile engine.
  *   h     [B][h_ld][d_model], h_ld >= T.      pos0  [B] int32.
  *   out   K/V view written at rows out->t_off .. out->t_off+T-1.
  * B == 0 or T == 0 is a no-op.                                                */
@@ -151,7 +151,8 @@ kvd_status kvd_project_q(const kvd_attn_shape* shape, const void* h_new, const v
 /* ATTENTION for one decode query per sequence and head (Eqs. attn_weights,
  * head_output) over T >= 1 stored keys: rows kv->t_off .. kv->t_off+T-1.
  * bf16: the keys of each (sequence, KV head) are cut into kvd_num_splits
- * contiguous ranges (about kvd_set_attn_workgroups workgroups over the call),
+ * contiguous ranges (about kvd_set_attn_workgroups workgroups over the call,
+ * at most 32 ranges per (sequence, KV head)),
  * each streamed by one workgroup that keeps its next 16-key block's loads in
  * flight (HBM-bound: the read is Eq. read_bytes).  fp32: one split per
  * 64-key tile.

@@ -205,7 +205,7 @@ kvd_status attn_common(const kvd_attn_shape* shape, const void* q, const kvd_kv_
   const int32_t S = splits(shape, KVD_OP_DECODE_ATTN, B, T, 0);
   KVD_TRY(check_ws(shape, B, S, ws, ws_bytes));
   kvd::AttnArgs a{};
-  if (shape->dtype == KVD_BF16) a.kps = stream_split(shape, B, T).kps;
+  if (shape->dtype == KVD_BF16) a.nblk = stream_split(shape, B, T).nblk;
   a.q = q;
   a.k = kv->k;
   a.v = kv->v;
@@ -282,7 +282,9 @@ kvd_status kvd_recompute_kv(const kvd_attn_shape* shape, const void* h, int32_t 
   const int G = (long long)B * T <= INT32_MAX ? kvd::stream_group(shape->d_model, B * T, kLdsLimit) : 0;
   const long long stream_wgs =
       G >= 1 ? (long long)(2 * shape->n_kv_heads * shape->head_dim / 32) * (((long long)B * T + G - 1) / G) : 0;
-  if (shape->dtype == KVD_BF16 && G >= 1 && stream_wgs <= kvd::kStreamRecomputeMaxWgs)
+  const long long max_wgs =
+      shape->head_dim >= 256 ? kvd::kStreamRecomputeMaxWgsHd256 : kvd::kStreamRecomputeMaxWgs;
+  if (shape->dtype == KVD_BF16 && G >= 1 && stream_wgs <= max_wgs)
     return device_status(kvd::launch_project_current(a, 1, shape->head_dim, shape->w_layout == KVD_W_PACKED,
                                                      a.n_kv_units, (hipStream_t)stream),
                          "kvd_recompute_kv launch");

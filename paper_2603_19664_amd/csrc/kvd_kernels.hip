@@ -556,8 +556,8 @@ __global__ __launch_bounds__(kNtAttn) void decode_kernel(AttnArgs a) {
 
 // ------------------------------------------------------------------ streaming stored-K/V attention (bf16)
 
-// One workgroup of kSaWaves waves per (split s, KV head j, sequence b): keys
-// k0 = s * kps .. min(T, k0 + kps) - 1 of the stored K/V, in 16-key blocks,
+// One workgroup of kSaWaves waves per (split s, KV head j, sequence b): the keys
+// of blocks sa_first_block(s) .. sa_first_block(s + 1) - 1 of the stored K/V,
 // block i to wave i % kSaWaves.  Memory traffic is the K/V rows read once
 // (Eq. read_bytes): HBM-bound, so the design keeps loads in flight rather than
 // counting flops.  Per block a wave
@@ -595,8 +595,8 @@ __global__ __launch_bounds__(64 * kSaWaves) __attribute__((amdgpu_waves_per_eu(2
   const int tid = threadIdx.x, lane = tid & 63, w = wave_id();
   const int s = blockIdx.x, j = blockIdx.y, b = blockIdx.z;
   const int g = a.n_q / a.n_kv;
-  const int k0 = s * a.kps;
-  const int nk = min(a.T - k0, a.kps);              // keys of this split, >= 1
+  const int k0 = kSaBlock * sa_first_block(s, a.nblk, a.S);
+  const int nk = min(a.T, kSaBlock * sa_first_block(s + 1, a.nblk, a.S)) - k0;  // keys of this split, >= 1
   const int nblk = (nk + kSaBlock - 1) / kSaBlock;
   const int nb = nblk > w ? (nblk - 1 - w) / NW + 1 : 0;  // this wave's blocks: w, w + NW, ...
   const size_t row0 = ((size_t)b * a.n_kv + j) * a.t_cap + a.t_off + k0;

@@ -56,8 +56,8 @@ struct FusedArgs {
 };
 
 // Split-K attention over stored K/V.  fp32: S = decode_splits(T) chunks of
-// kTile keys (decode_kernel).  bf16: S splits of kps keys (the last one
-// shorter), one streaming workgroup each (stream_attn_kernel).  out == nullptr:
+// kTile keys (decode_kernel).  bf16: S splits of the nblk 16-key blocks
+// (sa_first_block), one streaming workgroup each (stream_attn_kernel).  out == nullptr:
 // partials only; otherwise the workgroup that completes the splits of (b, KV
 // head) merges them into out (with S == 1 the one workgroup writes out
 // directly).  The same holds for FusedArgs::out.
@@ -71,7 +71,7 @@ struct AttnArgs {
   float* ws_ml;
   unsigned long long* ws_done;
   int B, T, n_q, n_kv, S;
-  int kps;  // bf16: keys per split
+  int nblk;  // bf16: 16-key blocks of the T keys
 };
 
 // Block-forward projection on the tile engine (bf16): out = epilogue(x W^T) for

@@ -159,6 +159,11 @@ constexpr int kStreamDepth = 10;
 // and wins up to two of them (Gemma-3-4B shape: 128 tokens in 36 us; Qwen2.5-
 // 1.5B shape: 512 tokens in 21 us).
 constexpr long long kStreamRecomputeMaxWgs = 512;
+// head_dim 256: the tile engine's workgroup does twice the work (512 K|V rows)
+// and takes 55-59 us at d 2560, so two more rounds of the streaming kernel still
+// win (its token groups are 11 rows there, LDS-bound: 128 tokens are 768
+// workgroups, 36 us; 192 tokens 1152 workgroups, 47 us).
+constexpr long long kStreamRecomputeMaxWgsHd256 = 1024;
 constexpr size_t kStreamSlotBytes = (size_t)32 * kKT * 2 * kStreamChunk;
 struct StreamLds {
   size_t rev, rinv, pos, gam, ring, hb, hs, end;
@@ -200,22 +205,33 @@ constexpr int kSaTargetWgs = 256;
 // 4, 6, 8, 16 that is >= g (heads g .. G-1 are computed on zero queries and
 // never stored).
 constexpr int sa_group(int g) { return g <= 4 ? g : g <= 6 ? 6 : g <= 8 ? 8 : 16; }
-// Keys per split (a multiple of kSaBlock) and the split count S for T keys and
-// `pairs` = B * n_kv (sequence, KV head) pairs: about `target` workgroups in
-// all, at most one split per block; every split holds at least one key.
+// Split count S for T keys and `pairs` = B * n_kv (sequence, KV head) pairs:
+// about `target` workgroups in all, at most kSaMaxSplits and at most one split
+// per 16-key block.  Split s
+// takes blocks sa_first_block(s) .. sa_first_block(s + 1) - 1 of the nblk, so the
+// splits' block counts differ by at most one, every split holds at least one
+// key, and S never decreases as T grows (a workspace sized for the longest call
+// serves the shorter ones).
 struct SaSplit {
-  int kps, S;
+  int nblk, S;
 };
+// At most kSaMaxSplits splits: each split adds an arrival on its (sequence, KV
+// head) counter and a partial to merge, and past 32 that cost more than the
+// parallelism gained (measured, Gemma-3-4B layer, B = 1: 4097 keys in 15.2 us
+// with 32 splits, 19.3 us with 64, 25.1 us with 128).
+constexpr int kSaMaxSplits = 32;
 constexpr SaSplit sa_split(long long pairs, int T, int target) {
-  const int nblk = (T + kSaBlock - 1) / kSaBlock;
+  SaSplit r{};
+  r.nblk = (T + kSaBlock - 1) / kSaBlock;
   long long s = pairs > 0 ? (target + pairs - 1) / pairs : 1;
   if (s < 1) s = 1;
-  if (s > nblk) s = nblk;
-  const int bps = (int)((nblk + s - 1) / s);  // blocks per split
-  SaSplit r{};
-  r.kps = bps * kSaBlock;
-  r.S = (T + r.kps - 1) / r.kps;
+  if (s > kSaMaxSplits) s = kSaMaxSplits;
+  if (s > r.nblk) s = r.nblk;
+  r.S = (int)s;
   return r;
+}
+constexpr int sa_first_block(int s, int nblk, int S) {
+  return (int)((long long)s * nblk / S);
 }
 // LDS of the streaming kernel: per wave the block's probabilities [G][16] and
 // rescale factors [16]; the waves' states [kSaWaves][G][hd] and (max, sum)

@@ -150,11 +150,9 @@ def test_project_validation():
 
 def _stream_splits(pairs, T, target):
     """The bf16 stored-K/V attention's split rule as documented: about `target`
-    workgroups over the call, at most one split per 16-key block, whole blocks per split."""
+    workgroups over the call, at most one split per 16-key block."""
     nblk = -(-T // 16)
-    s = min(max(-(-target // pairs), 1), nblk)
-    kps = -(-nblk // s) * 16
-    return -(-T // kps)
+    return min(max(-(-target // pairs), 1), 32, nblk)
 
 
 def test_split_policy_and_workspace():
@@ -165,18 +163,23 @@ def test_split_policy_and_workspace():
         want = _stream_splits(B * 4, T, 256)
         assert ns(s, kvd.KVD_OP_DECODE_ATTN, T, 0, B) == want, (B, T)
         assert ns(s, kvd.KVD_OP_CACHED_ATTN, T, 0, B) == want, (B, T)
-    assert ns(s, kvd.KVD_OP_DECODE_ATTN, 4097, 0) == 52     # 4 (b, head) pairs: 80-key splits
-    assert ns(s, kvd.KVD_OP_DECODE_ATTN, 2049, 0, 8) == 8   # 32 pairs: 272-key splits
+    assert ns(s, kvd.KVD_OP_DECODE_ATTN, 4097, 0) == 32     # 4 (b, head) pairs: 32 splits of 8-9 blocks
+    assert ns(s, kvd.KVD_OP_DECODE_ATTN, 2049, 0, 8) == 8   # 32 pairs: 8 splits each
     assert ns(s, kvd.KVD_OP_DECODE_ATTN, 2049, 0, 64) == 1  # 256 pairs: one split each
+    # the split count never falls as the key count grows (one workspace serves a growing context)
+    for B in (1, 3, 8):
+        counts = [ns(s, kvd.KVD_OP_DECODE_ATTN, T, 0, B) for T in range(1, 6000, 7)]
+        assert counts == sorted(counts)
     # the workgroup target moves the split count, and 0 restores the default
     try:
         assert lib.kvd_set_attn_workgroups(1) == 256
         assert ns(s, kvd.KVD_OP_DECODE_ATTN, 4097, 0) == 1
         assert lib.kvd_set_attn_workgroups(1 << 20) == 1
-        assert ns(s, kvd.KVD_OP_DECODE_ATTN, 4097, 0) == 257  # one per 16-key block at most
+        assert ns(s, kvd.KVD_OP_DECODE_ATTN, 4097, 0) == 32   # at most 32 per (sequence, head)
+        assert ns(s, kvd.KVD_OP_DECODE_ATTN, 100, 0) == 7     # and at most one per 16-key block
     finally:
         lib.kvd_set_attn_workgroups(0)
-    assert ns(s, kvd.KVD_OP_DECODE_ATTN, 4097, 0) == 52
+    assert ns(s, kvd.KVD_OP_DECODE_ATTN, 4097, 0) == 32
     # fp32 stored-K/V attention: one split per 64-key tile
     assert ns(shape(dtype=kvd.KVD_F32), kvd.KVD_OP_DECODE_ATTN, 4097, 0) == 65
     assert ns(shape(dtype=kvd.KVD_F32), kvd.KVD_OP_DECODE_ATTN, 64, 0) == 1

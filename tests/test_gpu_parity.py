@@ -190,8 +190,9 @@ def test_prefill_equals_recompute_bitwise(dtype):
     L = make_layer(wl, B=3, T=300, seed=21, pos0=[0, 17, 4000])
     Kp, Vp = gpu_recompute(L)                     # prefill: every token at once
     # recompute of sub-ranges with odd lengths, at other offsets and capacities (in bf16,
-    # calls of at most 512 streaming workgroups, here 64 per 16 rows, run on the
-    # streaming kernel: (0, 1), (66, 67), (299, 300), (100, 120); the others on the tile engine)
+    # calls of at most 1024 streaming workgroups at head_dim 256, here 64 per 16 rows, run
+    # on the streaming kernel: (0, 1), (1, 66), (66, 67), (299, 300), (100, 120); the
+    # others and the prefill on the tile engine)
     for a, b in [(0, 1), (1, 66), (66, 67), (67, 299), (299, 300), (5, 250), (100, 120)]:
         Lr = dataclasses.replace(L, h=L.h[:, a:b].contiguous(), T=b - a, pos0=(L.pos0 + a).to(torch.int32))
         K, V = gpu_recompute(Lr, t_cap=b - a + 9, t_off=7)
