@@ -108,12 +108,54 @@ kvd::SaSplit stream_split(const kvd_attn_shape* s, int32_t B, int32_t T) {
   return kvd::sa_split((long long)B * s->n_kv_heads, T, g_attn_target.load(std::memory_order_relaxed));
 }
 
+// Token tile of the fused call (kvd_set_fused_tokens): 0 = chosen per call.
+std::atomic<int32_t> g_fused_tokens{0};
+
+// The fused call's tiling: mt recomputed tokens per workgroup (kMtBf16 /
+// kMtF32, or kMtWide on the wide engine), n_rec recomputed tiles, n_tail
+// stored-tail tiles, S = n_rec + n_tail splits.
+struct FusedPlan {
+  int32_t mt, n_rec, n_tail, S;
+};
+
+// The wide engine exists for bf16 at head_dim 128 / 256 where its LDS fits.
+bool wide_supported(const kvd_attn_shape* s) {
+  if (s->dtype != KVD_BF16 || (s->head_dim != 128 && s->head_dim != 256)) return false;
+  return kvd::fused_wide_lds_bytes(s->n_q_heads / s->n_kv_heads, s->head_dim) + kvd::gamma_lds_bytes(s->d_model) <=
+         kvd::kLdsPerGroup;
+}
+
+FusedPlan narrow_plan(const kvd_attn_shape* s, int32_t T_rec, int32_t T_tail) {
+  FusedPlan p{};
+  p.mt = kvd::kMtBf16;
+  p.n_rec = ceil_div(T_rec, p.mt);
+  p.n_tail = s->dtype == KVD_BF16 ? kvd::fused_tail_tiles<uint16_t>(p.n_rec, T_tail)
+                                  : kvd::fused_tail_tiles<float>(p.n_rec, T_tail);
+  p.S = p.n_rec + p.n_tail;
+  return p;
+}
+
+FusedPlan wide_plan(int32_t T_rec, int32_t T_tail) {
+  FusedPlan p{};
+  p.mt = kvd::kMtWide;
+  p.n_rec = ceil_div(T_rec, p.mt);
+  p.n_tail = ceil_div(T_tail, kvd::kTile);
+  p.S = p.n_rec + p.n_tail;
+  return p;
+}
+
+// Wide tiles when supported and the call has at least kWideMinTiles of them (a
+// full round of the chip), or when forced by kvd_set_fused_tokens(128).
+FusedPlan fused_plan(const kvd_attn_shape* s, int32_t B, int32_t T_rec, int32_t T_tail) {
+  const int32_t mode = g_fused_tokens.load(std::memory_order_relaxed);
+  bool wide = T_rec > 0 && mode != kvd::kMtBf16 && wide_supported(s);
+  if (wide && mode == 0)
+    wide = (int64_t)B * s->n_kv_heads * ceil_div(T_rec, kvd::kMtWide) >= kvd::kWideMinTiles;
+  return wide ? wide_plan(T_rec, T_tail) : narrow_plan(s, T_rec, T_tail);
+}
+
 int32_t splits(const kvd_attn_shape* s, int32_t op, int32_t B, int32_t T_main, int32_t T_tail) {
-  if (op == KVD_OP_FUSED) {
-    const int32_t n_rec = ceil_div(T_main, kvd::kMtBf16);
-    return n_rec + (s->dtype == KVD_BF16 ? kvd::fused_tail_tiles<uint16_t>(n_rec, T_tail)
-                                         : kvd::fused_tail_tiles<float>(n_rec, T_tail));
-  }
+  if (op == KVD_OP_FUSED) return fused_plan(s, B, T_main, T_tail).S;
   return s->dtype == KVD_BF16 ? stream_split(s, B, T_main).S : kvd::decode_splits<float>(T_main);
 }
 
@@ -392,7 +434,8 @@ kvd_status fused_launch(const kvd_attn_shape* shape, const void* q, const void* 
                         const void* w_k, const void* w_v, const int32_t* pos0, int32_t B, int32_t T_rec,
                         const kvd_kv_view* tail, int32_t T_tail, void* out, void* ws, size_t ws_bytes,
                         const kvd_kv_view* kv_debug, void* stream, const char* name) {
-  const int32_t S = splits(shape, KVD_OP_FUSED, B, T_rec, T_tail);
+  const FusedPlan plan = fused_plan(shape, B, T_rec, T_tail);
+  const int32_t S = plan.S;
   // one workgroup per (KV head, sequence, split), indexed in 32 bits
   if ((int64_t)shape->n_kv_heads * B * S > INT32_MAX - 8)
     return fail(KVD_ERR_SHAPE, "%s: n_kv_heads * B * splits = %lld workgroups is too many", name,
@@ -428,12 +471,13 @@ kvd_status fused_launch(const kvd_attn_shape* shape, const void* q, const void* 
   a.n_kv = shape->n_kv_heads;
   a.B = B;
   a.T_rec = T_rec;
-  a.n_rec = ceil_div(T_rec, kvd::kMtBf16);
+  a.n_rec = plan.n_rec;
   a.S = S;
   a.eps = shape->rms_eps;
   fill_rev(shape, a.rev);
   return device_status(kvd::launch_fused(a, shape->dtype == KVD_BF16, shape->head_dim,
-                                         shape->w_layout == KVD_W_PACKED, (hipStream_t)stream),
+                                         shape->w_layout == KVD_W_PACKED, plan.mt == kvd::kMtWide,
+                                         (hipStream_t)stream),
                        name);
 }
 
@@ -758,9 +802,18 @@ int32_t kvd_set_attn_workgroups(int32_t target) {
   return g_attn_target.exchange(target, std::memory_order_relaxed);
 }
 
+int32_t kvd_set_fused_tokens(int32_t tokens) {
+  if (tokens != kvd::kMtBf16 && tokens != kvd::kMtWide) tokens = 0;
+  return g_fused_tokens.exchange(tokens, std::memory_order_relaxed);
+}
+
 size_t kvd_workspace_bytes(const kvd_attn_shape* shape, int32_t op, int32_t B, int32_t T_main, int32_t T_tail) {
-  const int32_t S = kvd_num_splits(shape, op, B, T_main, T_tail);
+  int32_t S = kvd_num_splits(shape, op, B, T_main, T_tail);
   if (S == 0) return 0;
+  // fused: enough for either tiling, so that the size grows with T_rec and
+  // T_tail whichever tile each call gets
+  if (op == KVD_OP_FUSED)
+    S = std::max(narrow_plan(shape, T_main, T_tail).S, wide_supported(shape) ? wide_plan(T_main, T_tail).S : 0);
   return ws_total(shape, B, S);
 }
 

@@ -464,6 +464,289 @@ struct MfmaTile {
   }
 };
 
+// ------------------------------------------------------------------ bf16 MFMA tile, 128 tokens
+
+// 8 waves (512 threads, two per SIMD) compute a [2*HD features] x [128 tokens]
+// tile, head_dim 128 or 256.  Wave w owns 32 feature rows for all 128 tokens
+// per 32-row block it holds: at head_dim 256 K rows and the same V rows
+// [32 w, 32 w + 32) (two blocks, RoPE work balanced), at head_dim 128 one block
+// of K (waves 0-3) or V (waves 4-7).  Each weight (A) fragment feeds four
+// MFMAs (one per 32-token block).  A CU reads the tile's weights once per 128
+// tokens instead of once per 64 (half the weight bytes per flop of MfmaTile),
+// and the two waves of a SIMD cover each other's staging arithmetic, fragment
+// reads and barrier waits.  The per-element arithmetic is MfmaTile's: the same
+// MFMA chain over d in K order, the same staging, 1/rms and epilogue, so the
+// K/V it produces are bit-identical.
+//
+// K-loop: weights are loaded DW = 2 K-steps ahead into A-operand registers,
+// each substep's fragments refilled right after its MFMAs; residuals one step
+// ahead into registers, staged (gamma * h -> bf16, sum of squares) two steps
+// ahead into an LDS ring of kDepth slots in B-fragment order.  One barrier
+// per step, after the second substep.  Loads go through
+// buffer resources (wave-uniform base and extent in SGPRs, a 32-bit offset per
+// lane), which keeps the addresses out of the vector registers.
+template <int HD, bool PACKED>
+struct WideTile {
+  static constexpr int NT = kNtWide;
+  static constexpr int MT = kMtWide;
+  static constexpr int NB_F = HD / 128;   // 32-row blocks per wave
+  static constexpr int NB_T = MT / 32;    // 32-token blocks (all of them)
+  static constexpr int CPT = MT * 8 / NT;  // staged 8-element chunks per thread per K-step
+  static constexpr int KLD = kv_ld<uint16_t>(HD);
+  static constexpr int DW = 2, DH = 2, DL = kDepth;
+  static constexpr int SLOT = NB_T * 4 * 512;  // elements per LDS slot (one K-step)
+  static_assert(HD == 128 || HD == 256, "wide tile: head_dim 128 or 256");
+  static_assert(DL == 4 && CPT == 2 && NT == 512, "ring and staging shape");
+
+  static __device__ __forceinline__ void block_rows(int w, int bf, int& half, int& row0) {
+    if (NB_F == 2) {
+      half = bf;
+      row0 = 32 * w;
+    } else {
+      half = w / 4;
+      row0 = 32 * (w % 4);
+    }
+  }
+
+  // As MfmaTile::run, for the n <= 128 residual rows that start at h_tile
+  // ([n][d], row stride d); the K/V tile goes to `kv`.
+  template <class Setup>
+  static __device__ __forceinline__ void run(const uint16_t* h_tile, int n, const uint16_t* gam, const uint16_t* gam_g,
+                                             int d, float eps, const Half (&halves)[2], uint16_t* hst, float* rinv,
+                                             const int* pos, const double* rev, uint16_t* kv, const Setup& setup) {
+    const int rope0 = halves[0].rope, rope1 = halves[1].rope;
+    run_with(h_tile, n, gam, gam_g, d, eps, halves, hst, rinv, setup,
+             [&](const f32x16_t (&acc)[NB_F][NB_T], const bool (&wok)[NB_F]) {
+               store_kv(acc, wok, rope0, rope1, rinv, pos, rev, kv);
+             });
+  }
+
+  // MfmaTile::store_kv for this wave layout.
+  static __device__ __forceinline__ void store_kv(const f32x16_t (&acc)[NB_F][NB_T], const bool (&wok)[NB_F],
+                                                  int rope0, int rope1, const float* rinv, const int* pos,
+                                                  const double* rev, uint16_t* kv) {
+    const int lane = threadIdx.x & 63, w = wave_id();
+#pragma unroll
+    for (int bt = 0; bt < NB_T; ++bt) {
+      const int tok = 32 * bt + (lane & 31);
+      const float ri = rinv[tok];
+      const int p = pos[tok];
+#pragma unroll
+      for (int bf = 0; bf < NB_F; ++bf) {
+        int half, row0;
+        block_rows(w, bf, half, row0);
+        float v[16];
+#pragma unroll
+        for (int r = 0; r < 16; ++r) v[r] = wok[bf] ? acc[bf][bt][r] * ri : 0.0f;
+        if (half ? rope1 : rope0) {
+#pragma unroll
+          for (int r = 0; r < 16; r += 2) {
+            const int f = row0 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+            rope_rotate(v[r], v[r + 1], p, rev[f >> 1]);
+          }
+        }
+#pragma unroll
+        for (int g4 = 0; g4 < 4; ++g4) {
+          const int col = half * HD + row0 + 8 * g4 + 4 * (lane >> 5);
+          uint2 o;
+          o.x = pack_bf16x2(v[4 * g4 + 0], v[4 * g4 + 1]);
+          o.y = pack_bf16x2(v[4 * g4 + 2], v[4 * g4 + 3]);
+          *reinterpret_cast<uint2*>(kv + (size_t)tok * KLD + col) = o;
+        }
+      }
+    }
+  }
+
+  // The K-loop and 1/rms (in rinv), then epi(acc, wok): acc[bf][bt][r] is
+  // feature row0(bf) + 8 (r / 4) + 4 (lane / 32) + r % 4 of half(bf) for token
+  // 32 bt + lane % 32.
+  template <class Setup, class Epi>
+  static __device__ __forceinline__ void run_with(const uint16_t* h_tile, int n, const uint16_t* gam,
+                                                  const uint16_t* gam_g, int d, float eps, const Half (&halves)[2],
+                                                  uint16_t* hst, float* rinv, const Setup& setup, const Epi& epi) {
+    const int tid = threadIdx.x, lane = tid & 63, sub = tid & 7;
+    const int w = wave_id();
+    const int nsteps = d / kKT;
+
+    // weights: this wave's 32 rows of each block; a half without weights reads
+    // the other half's rows (in bounds) and its results are zeros
+    const void* const hw0 = halves[0].w;
+    const void* const hw1 = halves[1].w;
+    const void* const wk = hw0 != nullptr ? hw0 : hw1;
+    const void* const wv = hw1 != nullptr ? hw1 : wk;
+    bool wok[NB_F];
+    __amdgpu_buffer_rsrc_t wres[NB_F];
+#pragma unroll
+    for (int bf = 0; bf < NB_F; ++bf) {
+      int half, row0;
+      block_rows(w, bf, half, row0);
+      wok[bf] = (half ? hw1 : hw0) != nullptr;  // uniform per wave
+      const uint16_t* wp = static_cast<const uint16_t*>(half ? wv : wk) + (size_t)row0 * d;
+      wres[bf] = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(wp), (short)0, (int)(32u * (uint32_t)d * 2u),
+                                                   0x00020000);
+    }
+    // byte offset of this lane's A-operand chunk at K-step 0, substep 0
+    const uint32_t wlane = PACKED ? 16u * lane : 2u * ((uint32_t)(lane & 31) * d + 8u * (lane >> 5));
+    // residuals: rows (tid >> 3) + 64 r; rows past n read row 0 (their MFMA
+    // columns are independent of the others and their 1/rms is zero)
+    bool valid[CPT];
+    uint32_t hoff[CPT];
+    const __amdgpu_buffer_rsrc_t hres = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint16_t*>(h_tile), (short)0, (int)((uint32_t)n * (uint32_t)d * 2u), 0x00020000);
+#pragma unroll
+    for (int r = 0; r < CPT; ++r) {
+      const int t = (tid >> 3) + 64 * r;
+      valid[r] = t < n;
+      hoff[r] = 2u * ((uint32_t)(valid[r] ? t : 0) * (uint32_t)d + 8u * sub);
+    }
+
+    f32x16_t acc[NB_F][NB_T];
+#pragma unroll
+    for (int bf = 0; bf < NB_F; ++bf)
+#pragma unroll
+      for (int bt = 0; bt < NB_T; ++bt)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) acc[bf][bt][i] = 0.0f;
+    // The accumulators live in AGPRs (the MFMAs' AGPR form): an empty asm
+    // statement that names them with the AGPR constraint tells the compiler
+    // this wave uses AGPRs, which leaves the 128 VGPRs to the operand rings.
+#pragma unroll
+    for (int bf = 0; bf < NB_F; ++bf)
+#pragma unroll
+      for (int bt = 0; bt < NB_T; ++bt) asm volatile("" : "+a"(acc[bf][bt]));
+
+    bf16x8_t A[DW][NB_F][4];
+    uint4 H[DH][CPT];
+    float ss[CPT];
+#pragma unroll
+    for (int r = 0; r < CPT; ++r) ss[r] = 0.0f;
+    // chunk r of this thread: token (tid >> 3) + 64 r = token block
+    // (tid >> 8) + 2 r, column (tid >> 3) % 32; elements 8 sub .. 8 sub + 7 of
+    // the K-step = substep sub / 2, lane half sub % 2 of the B fragment
+    const int lofs = ((tid >> 8) * 4 + (sub >> 1)) * 512 + 8 * (((tid >> 3) & 31) + 32 * (sub & 1));
+
+    auto load_wu = [&](int slot, int s, int u) {
+#pragma unroll
+      for (int bf = 0; bf < NB_F; ++bf) {
+        const u32x4_t v =
+            __builtin_amdgcn_raw_buffer_load_b128(wres[bf], (int)wlane, (int)(2u * (uint32_t)w_off<PACKED>(s, u)), 0);
+        A[slot][bf][u] = __builtin_bit_cast(bf16x8_t, v);
+      }
+    };
+    auto load_h = [&](int hslot, int s) {
+#pragma unroll
+      for (int r = 0; r < CPT; ++r) {
+        const u32x4_t v = __builtin_amdgcn_raw_buffer_load_b128(hres, (int)hoff[r], 2 * s * kKT, 0);
+        H[hslot][r] = make_uint4(v.x, v.y, v.z, v.w);
+      }
+    };
+    auto put_hv = [&](int lslot, int hslot, const uint4& gv) {
+#pragma unroll
+      for (int r = 0; r < CPT; ++r)
+        *reinterpret_cast<uint4*>(hst + (size_t)lslot * SLOT + r * 8 * 512 + lofs) =
+            stage_chunk_bf16(H[hslot][r], gv, ss[r]);
+    };
+    // B fragment of K-step slot lslot, substep u, token block bt
+    auto rd1 = [&](int lslot, int u, int bt) {
+      return *reinterpret_cast<const bf16x8_t*>(hst + (size_t)lslot * SLOT + (bt * 4 + u) * 512 + 8 * lane);
+    };
+
+    // A step is 16 units k = 4 u + bt (substep u, token block bt), each one B
+    // fragment and the NB_F MFMAs that use it.  B fragments stream through a
+    // ring of RA + 1 registers, read RA units ahead: the reads of the next
+    // step's first units come after the barrier that makes its staging visible.
+    constexpr int RA = 3;
+    constexpr int NBQ = RA + 1;
+    static_assert(16 % NBQ == 0, "unit k of every step uses ring entry k % NBQ");
+    bf16x8_t bq[NBQ];
+    // iteration s, L = s % 4: weight slot s % 2 (refilled with step s + 2), the
+    // residual registers (staged as step s + 1, then refilled with step s + 2),
+    // LDS slot L (read) and (L + 1) % 4 (written).  GUARD: the last iterations,
+    // whose step indexes are clamped into range.  Units keep their order (a
+    // scheduling fence after each lets only VALU, SALU, DS writes and
+    // transcendentals cross), so every ring register is reloaded only after its
+    // last use, and the staging arithmetic spreads over the first eight units.
+    auto iter = [&](auto lc, int s, auto guard_c) {
+      constexpr int L = decltype(lc)::value;
+      constexpr int LW = L & 1;
+      constexpr int LN = (L + 1) & 3;
+      constexpr bool GUARD = decltype(guard_c)::value;
+      const int sw = GUARD ? min(s + 2, nsteps - 1) : s + 2;
+      const int sh = GUARD ? min(s + 2, nsteps - 1) : s + 2;
+      auto unit = [&](auto kc) {
+        constexpr int k = decltype(kc)::value;
+        constexpr int u = k / 4, bt = k % 4, kk = k + RA;
+        if constexpr (kk < 16) bq[kk % NBQ] = rd1(L, kk / 4, kk % 4);
+        else bq[kk % NBQ] = rd1(LN, (kk - 16) / 4, (kk - 16) % 4);
+#pragma unroll
+        for (int bf = 0; bf < NB_F; ++bf)
+          acc[bf][bt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(A[LW][bf][u], bq[k % NBQ], acc[bf][bt], 0, 0, 0);
+        if constexpr (bt == NB_T - 1) load_wu(LW, sw, u);
+        if constexpr (k == 3) load_h(0, sh);
+        if (!GUARD) {
+          __builtin_amdgcn_sched_group_barrier(0x100, k == 0 ? 2 : 1, 0);  // DS read: B fragment (gamma)
+#pragma unroll
+          for (int bf = 0; bf < NB_F; ++bf) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);            // MFMA
+            if constexpr (k < 7) __builtin_amdgcn_sched_group_barrier(0x002, 5, 0);  // VALU: staging
+          }
+          if constexpr (k == 6) __builtin_amdgcn_sched_group_barrier(0x200, CPT, 0);  // DS write: staged chunks
+        }
+        __builtin_amdgcn_sched_barrier(0x0606);
+      };
+      __builtin_amdgcn_sched_barrier(0);
+      if (!GUARD || s + 1 < nsteps)
+        put_hv(LN, 0, *reinterpret_cast<const uint4*>(gam + (size_t)(s + 1) * kKT + 8 * sub));
+      unit(IC<0>{}); unit(IC<1>{}); unit(IC<2>{}); unit(IC<3>{});
+      unit(IC<4>{}); unit(IC<5>{}); unit(IC<6>{}); unit(IC<7>{});
+      __builtin_amdgcn_sched_barrier(0);
+      __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): this wave's staged chunks are in LDS
+      __builtin_amdgcn_s_barrier();
+      __builtin_amdgcn_sched_barrier(0);
+      unit(IC<8>{}); unit(IC<9>{}); unit(IC<10>{}); unit(IC<11>{});
+      unit(IC<12>{}); unit(IC<13>{}); unit(IC<14>{}); unit(IC<15>{});
+    };
+
+    // prologue: residual step 0 and weight steps 0, 1 in flight, the caller's
+    // setup written, step 0 staged (its gamma chunk read from global memory:
+    // the LDS copy is complete only after the barrier), step 1's residuals
+    // requested
+    load_h(0, 0);
+    const uint4 g0 = *reinterpret_cast<const uint4*>(gam_g + 8 * sub);
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int i = 0; i < DW; ++i)
+#pragma unroll
+      for (int u = 0; u < 4; ++u) load_wu(i, min(i, nsteps - 1), u);
+    setup();
+    put_hv(0, 0, g0);
+    load_h(0, min(1, nsteps - 1));
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < RA; ++k) bq[k] = rd1(0, k / 4, k % 4);
+    int s0 = 0;
+    // steady state: every step index of iterations s0 .. s0 + 3 is below nsteps
+    for (; s0 + 8 <= nsteps; s0 += 4) {
+      iter(IC<0>{}, s0, IC<0>{});
+      iter(IC<1>{}, s0 + 1, IC<0>{});
+      iter(IC<2>{}, s0 + 2, IC<0>{});
+      iter(IC<3>{}, s0 + 3, IC<0>{});
+    }
+    for (; s0 < nsteps; s0 += 4) {
+      iter(IC<0>{}, s0, IC<1>{});
+      if (s0 + 1 < nsteps) iter(IC<1>{}, s0 + 1, IC<1>{});
+      if (s0 + 2 < nsteps) iter(IC<2>{}, s0 + 2, IC<1>{});
+      if (s0 + 3 < nsteps) iter(IC<3>{}, s0 + 3, IC<1>{});
+    }
+    __syncthreads();
+
+    finish_rms<NT, CPT>(ss, valid, d, eps, rinv);
+    __syncthreads();
+
+    epi(acc, wok);
+  }
+};
+
 // ------------------------------------------------------------------ fp32 VALU tile
 
 // The same contraction in fp32 on the vector ALUs: thread (pair p, token group)

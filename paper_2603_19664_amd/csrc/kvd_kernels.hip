@@ -385,19 +385,21 @@ __global__ __launch_bounds__(64 * kStreamWaves) void stream_proj_kernel(ProjArgs
 // C = n_tail + n_rec.  Chunks c < n_tail attend stored tail tile c (64 rows;
 // partial n_rec + c) and come first, as they are short; chunk n_tail + r
 // recomputes residual rows r*MT..r*MT+MT-1 (partial r).  A folded tail (<= fold_rows<T>() rows, n_tail = 0) is attended
-// with the last recomputed chunk's keys.
+// with the last recomputed chunk's keys.  MT = kMtWide: the wide engine (bf16,
+// 4 waves, 128-key chunks, no folded tail).
 template <typename T, int HD, int MT, bool PACKED>
-__global__ __launch_bounds__(kNtTile, 1) void fused_kernel(FusedArgs a, int per_xcd, int hg) {
+__device__ __forceinline__ void fused_body(const FusedArgs& a, int per_xcd, int hg) {
   extern __shared__ __align__(16) char lds[];
-  constexpr int NT = kNtTile;
-  constexpr int FR = fold_rows<T>();
+  constexpr bool WIDE = MT == kMtWide;
+  constexpr int NT = WIDE ? kNtWide : kNtTile;
+  constexpr int FR = WIDE ? 0 : fold_rows<T>();
   constexpr ProjLds PL = proj_lds<T>(HD, MT, FR);
   constexpr int CPT = MT * 8 / NT;
   constexpr int KLD = kv_ld<T>(HD);
-  static_assert(MT == kTile, "fused chunks are attention tiles");
+  static_assert(MT == kTile || (WIDE && sizeof(T) == 2), "fused chunks: 64-key tiles, or the wide bf16 engine");
   const int tid = threadIdx.x;
-  const bool fold = fold_tail<T>(a.n_rec, a.T_tail);
-  const int n_tail = fused_tail_tiles<T>(a.n_rec, a.T_tail);
+  const bool fold = !WIDE && fold_tail<T>(a.n_rec, a.T_tail);
+  const int n_tail = WIDE ? (a.T_tail + kTile - 1) / kTile : fused_tail_tiles<T>(a.n_rec, a.T_tail);
   const int C = n_tail + a.n_rec;
   // 32-bit index arithmetic (the item count is below 2^31, checked by the host):
   // every wave runs it on the CU's one scalar unit before its first load.
@@ -470,7 +472,11 @@ __global__ __launch_bounds__(kNtTile, 1) void fused_kernel(FusedArgs a, int per_
     const size_t hd_d = (size_t)HD * a.d;
     const Half halves[2] = {Half{static_cast<const T*>(a.w_k) + j * hd_d, 1},
                             Half{static_cast<const T*>(a.w_v) + j * hd_d, 0}};
-    if constexpr (sizeof(T) == 2) {
+    if constexpr (WIDE) {
+      WideTile<HD, PACKED>::run(static_cast<const uint16_t*>(a.h) + ((size_t)b * a.h_ld + t0) * a.d, n, gam,
+                                static_cast<const uint16_t*>(a.gamma), a.d, a.eps, halves, hst, rinv, pos, rev, kv,
+                                setup);
+    } else if constexpr (sizeof(T) == 2) {
       MfmaTile<HD, MT, PACKED>::run(hrow, valid, gam, static_cast<const uint16_t*>(a.gamma), a.d, a.eps, halves, hst,
                                     rinv, pos, rev, kv, setup);
     } else {
@@ -517,6 +523,19 @@ __global__ __launch_bounds__(kNtTile, 1) void fused_kernel(FusedArgs a, int per_
       combine_rows<T, HD, NT>(a.ws_acc, a.ws_ml, static_cast<T*>(a.out), (size_t)b * a.n_q + (size_t)j * g, g, a.S,
                               reinterpret_cast<float*>(lds + AL.cmb));
   }
+}
+
+template <typename T, int HD, int MT, bool PACKED>
+__global__ __launch_bounds__(kNtTile, 1) void fused_kernel(FusedArgs a, int per_xcd, int hg) {
+  fused_body<T, HD, MT, PACKED>(a, per_xcd, hg);
+}
+
+// One workgroup of 8 waves per CU, two per SIMD: 256 registers per lane (the
+// wave's 128-token accumulators in AGPRs).
+template <int HD, bool PACKED>
+__global__ __launch_bounds__(kNtWide, 1) void fused_wide_kernel(
+    FusedArgs a, int per_xcd, int hg) {
+  fused_body<uint16_t, HD, kMtWide, PACKED>(a, per_xcd, hg);
 }
 
 // ------------------------------------------------------------------ stored-K/V attention
@@ -925,6 +944,20 @@ static hipError_t fused_t(const FusedArgs& a, hipStream_t st) {
   return hipGetLastError();
 }
 
+template <int HD, bool PACKED>
+static hipError_t fused_wide_t(const FusedArgs& a, hipStream_t st) {
+  const size_t bytes = fused_wide_lds_bytes(a.n_q / a.n_kv, HD) + gamma_lds_bytes(a.d);
+  static std::atomic<size_t> done{0};
+  auto k = fused_wide_kernel<HD, PACKED>;
+  hipError_t e = ensure_lds(k, bytes, done);
+  if (e != hipSuccess) return e;
+  const int C = (a.T_tail + kTile - 1) / kTile + a.n_rec;
+  const XcdMap m = xcd_map((long long)a.n_kv * a.B * C);
+  const int hg = a.T_tail > 0 ? 1 : fused_head_group(a.n_kv, HD, m.per);
+  hipLaunchKernelGGL(k, dim3(m.grid), dim3(kNtWide), bytes, st, a, m.per, hg);
+  return hipGetLastError();
+}
+
 template <typename T, int HD>
 static hipError_t attn_t(const AttnArgs& a, hipStream_t st) {
   const size_t bytes = decode_lds_bytes<T>(a.n_q / a.n_kv, HD);
@@ -1011,7 +1044,15 @@ hipError_t launch_project_current(const ProjArgs& a, int dtype_bf16, int hd, int
   }
 }
 
-hipError_t launch_fused(const FusedArgs& a, int dtype_bf16, int hd, int packed, hipStream_t st) {
+hipError_t launch_fused(const FusedArgs& a, int dtype_bf16, int hd, int packed, int wide, hipStream_t st) {
+  if (wide) {
+    if (!dtype_bf16) return hipErrorInvalidValue;
+    switch (hd) {
+      case 128: return packed ? fused_wide_t<128, true>(a, st) : fused_wide_t<128, false>(a, st);
+      case 256: return packed ? fused_wide_t<256, true>(a, st) : fused_wide_t<256, false>(a, st);
+      default: return hipErrorInvalidValue;
+    }
+  }
   hipError_t e;
 #define FB(H) (packed ? fused_t<uint16_t, H, true>(a, st) : fused_t<uint16_t, H, false>(a, st))
 #define FF(H) fused_t<float, H, false>(a, st)

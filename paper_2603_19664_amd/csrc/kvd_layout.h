@@ -19,6 +19,14 @@ constexpr int kDepth = 4;       // K-steps of weights / residuals in flight in t
 constexpr int kMtBf16 = 64;
 constexpr int kMtF32 = 64;
 
+// The wide bf16 engine of the fused kernel (head_dim 128 / 256): 128 tokens per
+// workgroup on 8 waves, two per SIMD.  Used when the call has at least
+// kWideMinTiles such tiles (one per CU: a full round), so that the larger tile
+// does not leave CUs idle.
+constexpr int kNtWide = 512;
+constexpr int kMtWide = 128;
+constexpr int kWideMinTiles = 256;
+
 // A stored tail of at most fold_rows<T>() rows (a decode step's current token)
 // joins the split of the last recomputed tile of a fused call: the rows are
 // copied into LDS while that tile is recomputed and attended with its keys.
@@ -136,6 +144,10 @@ constexpr size_t decode_lds_bytes(int g, int hd) {
 template <typename T>
 constexpr size_t fused_lds_bytes(int g, int hd, int mt) {
   return attn_lds(proj_lds<T>(hd, mt, fold_rows<T>()).end, g, hd, mt + fold_rows<T>()).end;
+}
+// The wide fused kernel: no folded tail (its tile already holds 128 keys).
+constexpr size_t fused_wide_lds_bytes(int g, int hd) {
+  return attn_lds(proj_lds<uint16_t>(hd, kMtWide, 0).end, g, hd, kMtWide).end;
 }
 
 // Streaming projection (current-token q/K/V): one workgroup of kStreamWaves

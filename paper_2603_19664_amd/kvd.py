@@ -95,6 +95,8 @@ def _load() -> ctypes.CDLL:
     lib.kvd_num_splits.restype = I32
     lib.kvd_set_attn_workgroups.argtypes = [I32]
     lib.kvd_set_attn_workgroups.restype = I32
+    lib.kvd_set_fused_tokens.argtypes = [I32]
+    lib.kvd_set_fused_tokens.restype = I32
     lib.kvd_status_str.argtypes = [ctypes.c_int]
     lib.kvd_status_str.restype = ctypes.c_char_p
     lib.kvd_last_error.argtypes = []
@@ -248,6 +250,12 @@ def kvd_set_attn_workgroups(target: int) -> int:
     """Workgroup target of the bf16 stored-K/V attention's split policy (0: the default);
     returns the previous value.  Process-wide; size workspaces after setting it."""
     return lib.kvd_set_attn_workgroups(int(target))
+
+
+def kvd_set_fused_tokens(tokens: int) -> int:
+    """Recomputed tokens per workgroup of the fused calls: 0 chooses per call, 128 the
+    wide engine where it exists, 64 the 64-token tiles; returns the previous setting."""
+    return lib.kvd_set_fused_tokens(int(tokens))
 
 
 def workspace(shape: Shape, op: int, B: int, T_main: int, T_tail: int = 0, device="cuda") -> torch.Tensor:

@@ -113,7 +113,7 @@ def test_fused_validation():
     assert fused(s, dbg=view(t_cap=10)) == kvd.KVD_ERR_SHAPE
     assert fused(s, B=70000) == kvd.KVD_ERR_SHAPE
     # one workgroup per (KV head, sequence, split) must stay below 2^31
-    assert fused(s, B=65535, T_rec=600000, h_ld=600000) == kvd.KVD_ERR_SHAPE
+    assert fused(s, B=65535, T_rec=1200000, h_ld=1200000) == kvd.KVD_ERR_SHAPE
     assert lib.kvd_fused_recompute_attn(ctypes.byref(s), FAKE, FAKE, 64, FAKE, FAKE, FAKE, FAKE, 1, 64, None, 1,
                                         FAKE, FAKE, 1 << 30, None, None) == kvd.KVD_ERR_NULL
 
@@ -135,8 +135,8 @@ def test_window_validation():
     assert window_call(s, tail=view(t_cap=4, t_off=4)) == kvd.KVD_ERR_SHAPE
     assert window_call(s, ws_bytes=100) == kvd.KVD_ERR_WORKSPACE
     # the kept rows set the split count: 16 kept keys need one split
-    need = lib.kvd_workspace_bytes(ctypes.byref(s), kvd.KVD_OP_FUSED, 1, 15, 1)
-    assert window_call(s, ws_bytes=need - 1) == kvd.KVD_ERR_WORKSPACE
+    assert lib.kvd_num_splits(ctypes.byref(s), kvd.KVD_OP_FUSED, 1, 15, 1) == 1
+    assert window_call(s, ws_bytes=_ws_bytes(s, 1, 1) - 1) == kvd.KVD_ERR_WORKSPACE
 
 
 def test_project_validation():
@@ -200,6 +200,56 @@ def test_split_policy_and_workspace():
     done = -(-2 * 4 * 8 // 256) * 256  # split counters [B][n_kv] uint64
     assert n == acc + ml + done
     assert lib.kvd_workspace_bytes(ctypes.byref(s), 9, 1, 10, 0) == 0
+
+
+def _fused_splits(s, B, T_rec, T_tail, tokens):
+    """The fused call's split count as documented: 64-token tiles with a bf16 tail of
+    <= 4 rows folded into the last one, or 128-token wide tiles (bf16, head_dim 128 /
+    256) when forced or when there are at least 256 of them; tails in 64-row tiles."""
+    wide_ok = s.dtype == kvd.KVD_BF16 and s.head_dim in (128, 256) and T_rec > 0
+    wide = wide_ok and (tokens == 128 or (tokens == 0 and B * s.n_kv_heads * -(-T_rec // 128) >= 256))
+    if wide:
+        return -(-T_rec // 128) + -(-T_tail // 64)
+    n_rec = -(-T_rec // 64)
+    fold = s.dtype == kvd.KVD_BF16 and n_rec > 0 and 0 < T_tail <= 4
+    return n_rec + (0 if fold else -(-T_tail // 64))
+
+
+def _ws_bytes(s, B, S):
+    up = lambda x: -(-x // 256) * 256  # noqa: E731
+    return up(B * s.n_kv_heads * 8) + up(B * s.n_q_heads * S * s.head_dim * 4) + up(B * s.n_q_heads * S * 2 * 4)
+
+
+def test_fused_tiling_policy():
+    ns = lambda sh, B, T, Tt: lib.kvd_num_splits(ctypes.byref(sh), kvd.KVD_OP_FUSED, B, T, Tt)  # noqa: E731
+    gemma, qwen = shape(), shape(d_model=1536, n_q_heads=12, n_kv_heads=2, head_dim=128)
+    others = [shape(dtype=kvd.KVD_F32), shape(head_dim=64, d_model=576, n_q_heads=9, n_kv_heads=3)]
+    # default: wide tiles only with a full round of them
+    assert ns(gemma, 1, 4096, 1) == 64        # 128 wide tiles: 64-token tiles, folded current token
+    assert ns(gemma, 2, 4096, 1) == 33        # 256 wide tiles + the tail's own split
+    assert ns(gemma, 8, 2048, 1) == 17
+    assert ns(qwen, 8, 16384, 1) == 129
+    try:
+        for tokens in (0, 64, 128):
+            assert lib.kvd_set_fused_tokens(tokens) in (0, 64, 128)
+            for sh in [gemma, qwen] + others:
+                for B, T, Tt in [(1, 4096, 1), (2, 4096, 1), (8, 2048, 1), (1, 100, 1), (1, 0, 3), (3, 130, 70),
+                                 (16, 5120, 0), (1, 64, 4), (1, 64, 5)]:
+                    S = ns(sh, B, T, Tt)
+                    assert S == _fused_splits(sh, B, T, Tt, tokens), (tokens, sh.head_dim, B, T, Tt)
+                    # the workspace covers either tiling
+                    n = lib.kvd_workspace_bytes(ctypes.byref(sh), kvd.KVD_OP_FUSED, B, T, Tt)
+                    assert n >= _ws_bytes(sh, B, S)
+                    assert n == _ws_bytes(sh, B, max(_fused_splits(sh, B, T, Tt, 64), _fused_splits(sh, B, T, Tt, 128)))
+        # the workspace size never falls as the context grows, whichever tiling a call gets
+        for B in (1, 2, 8):
+            sizes = [lib.kvd_workspace_bytes(ctypes.byref(gemma), kvd.KVD_OP_FUSED, B, T, 1) for T in range(1, 5000, 13)]
+            assert sizes == sorted(sizes)
+        assert lib.kvd_set_fused_tokens(128) == 128
+        assert lib.kvd_set_fused_tokens(77) == 128  # other values mean 0
+        assert lib.kvd_set_fused_tokens(0) == 0
+    finally:
+        lib.kvd_set_fused_tokens(0)
 
 
 def test_lds_limit_is_validated():
