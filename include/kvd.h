@@ -33,9 +33,11 @@
  *           Weights are stored [out][in], the transpose of the paper's
  *           row-vector W (h W), so head h owns rows h*head_dim ..
  *           (h+1)*head_dim-1.  shape->w_layout selects how each weight matrix
- *           is laid out in memory: KVD_W_ROWMAJOR (as above) or KVD_W_PACKED
- *           (the MFMA operand order written by kvd_pack_weights; bf16 only).
- *           Both layouts hold the same values and give bit-identical results.
+ *           is laid out in memory: KVD_W_ROWMAJOR (as above), KVD_W_PACKED
+ *           (the MFMA operand order written by kvd_pack_weights; bf16 only),
+ *           both holding the same values and giving bit-identical results, or
+ *           KVD_W_PACKED_GAMMA (kvd_pack_weights_gamma: gamma folded into the
+ *           packed weights; gamma arguments are then not read).
  * Norm.     hbar = h / sqrt(mean(h^2) + rms_eps) * gamma.
  * RoPE.     Consecutive pairs (2i, 2i+1), 0-based, are rotated by
  *           +p * rope_theta^(-2i/head_dim), p the token's absolute position.
@@ -72,8 +74,16 @@ typedef enum {
 
 typedef enum { KVD_F32 = 0, KVD_BF16 = 1 } kvd_dtype;
 
-/* Memory layout of W_q / W_k / W_v (see kvd_pack_weights). */
-typedef enum { KVD_W_ROWMAJOR = 0, KVD_W_PACKED = 1 } kvd_weight_layout;
+/* Memory layout of W_q / W_k / W_v (see kvd_pack_weights).
+ * KVD_W_PACKED_GAMMA: packed by kvd_pack_weights_gamma, with the RMSNorm weight
+ * folded in (W diag(gamma), an exact identity of Eqs. rmsnorm / k_proj: the
+ * norm's scale moves from the residual to the weights' columns).  The kernels
+ * then stage the residuals unchanged and do not read gamma (calls accept NULL
+ * for it).  K/V and q produced from folded weights differ from the other
+ * layouts' by rounding only; every producer of this layout (recompute,
+ * prefill, the current token's projection, the fused kernels) gives
+ * bit-identical values for the same residuals.                               */
+typedef enum { KVD_W_ROWMAJOR = 0, KVD_W_PACKED = 1, KVD_W_PACKED_GAMMA = 2 } kvd_weight_layout;
 
 /* Operations whose workspace size kvd_workspace_bytes reports. */
 typedef enum { KVD_OP_DECODE_ATTN = 0, KVD_OP_CACHED_ATTN = 1, KVD_OP_FUSED = 2 } kvd_op;
@@ -87,7 +97,7 @@ typedef enum { KVD_OP_DECODE_ATTN = 0, KVD_OP_CACHED_ATTN = 1, KVD_OP_FUSED = 2 
  *   rms_eps     RMSNorm epsilon, finite and >= 0.
  *   rope_theta  RoPE base, finite and > 0.
  *   dtype       a kvd_dtype.
- *   w_layout    a kvd_weight_layout; KVD_W_PACKED requires KVD_BF16.        */
+ *   w_layout    a kvd_weight_layout; the packed layouts require KVD_BF16.   */
 typedef struct {
   int32_t d_model;
   int32_t n_q_heads;
@@ -282,6 +292,17 @@ kvd_status kvd_store_residual(const kvd_attn_shape* shape, const void* h_new, vo
  * must not alias w.  shape->dtype must be KVD_BF16 (w_layout is ignored).    */
 kvd_status kvd_pack_weights(const kvd_attn_shape* shape, const void* w, int32_t rows, void* packed,
                             void* stream);
+
+/* kvd_pack_weights of W diag(gamma) for the KVD_W_PACKED_GAMMA layout: element
+ * (f, k) of the packed matrix is bf16(W[f][k] * gamma[k]) (the product of the two
+ * bf16 values is exact in fp32, then rounded to nearest even), in the block
+ * order of kvd_pack_weights.  Pack W_q, W_k and W_v of a layer with that
+ * layer's RMSNorm weight gamma ([d_model] bf16).  The RMSNorm of Eq. rmsnorm is
+ * gamma * h / rms(h); moving gamma into the weights leaves each projection's
+ * value unchanged up to rounding and lets the kernels use the residual rows as
+ * MFMA operands as they are.  packed must alias neither w nor gamma.         */
+kvd_status kvd_pack_weights_gamma(const kvd_attn_shape* shape, const void* w, const void* gamma, int32_t rows,
+                                  void* packed, void* stream);
 
 /* kvd_pack_weights for any bf16 matrix [rows][cols] (rows % 32 == 0,
  * cols % 16 == 0): block (r, c) of 32 rows x 16 columns is 512 elements at

@@ -49,9 +49,9 @@ kvd_status check_shape(const kvd_attn_shape* s) {
   if (s->n_q_heads / s->n_kv_heads > kvd::kMaxGroup)
     return fail(KVD_ERR_UNSUPPORTED, "group size %d exceeds %d", s->n_q_heads / s->n_kv_heads, kvd::kMaxGroup);
   if (!std::isfinite(s->rms_eps) || s->rms_eps < 0.0f) return fail(KVD_ERR_SHAPE, "rms_eps must be finite and >= 0");
-  if (s->w_layout != KVD_W_ROWMAJOR && s->w_layout != KVD_W_PACKED)
-    return fail(KVD_ERR_UNSUPPORTED, "w_layout %d is not KVD_W_ROWMAJOR or KVD_W_PACKED", s->w_layout);
-  if (s->w_layout == KVD_W_PACKED && s->dtype != KVD_BF16)
+  if (s->w_layout != KVD_W_ROWMAJOR && s->w_layout != KVD_W_PACKED && s->w_layout != KVD_W_PACKED_GAMMA)
+    return fail(KVD_ERR_UNSUPPORTED, "w_layout %d is not a kvd_weight_layout", s->w_layout);
+  if (s->w_layout != KVD_W_ROWMAJOR && s->dtype != KVD_BF16)
     return fail(KVD_ERR_UNSUPPORTED, "packed weights are bf16 only");
   if (!std::isfinite(s->rope_theta) || s->rope_theta <= 0.0) return fail(KVD_ERR_SHAPE, "rope_theta must be finite and > 0");
   return KVD_OK;
@@ -61,6 +61,11 @@ kvd_status check_ptr(const void* p, const char* name) {
   if (p == nullptr) return fail(KVD_ERR_NULL, "%s is NULL", name);
   if ((reinterpret_cast<uintptr_t>(p) & 15u) != 0) return fail(KVD_ERR_ALIGN, "%s is not 16-byte aligned", name);
   return KVD_OK;
+}
+
+// gamma is read unless the weights have it folded in (KVD_W_PACKED_GAMMA).
+kvd_status check_gamma(const kvd_attn_shape* s, const void* gamma) {
+  return s->w_layout == KVD_W_PACKED_GAMMA ? KVD_OK : check_ptr(gamma, "gamma");
 }
 
 kvd_status check_view(const kvd_kv_view* v, int32_t T, const char* name) {
@@ -297,7 +302,7 @@ kvd_status kvd_recompute_kv(const kvd_attn_shape* shape, const void* h, int32_t 
   if (h_ld < T) return fail(KVD_ERR_SHAPE, "h_ld=%d is smaller than T=%d", h_ld, T);
   KVD_TRY(check_lds_bytes(recompute_lds(shape), "kvd_recompute_kv"));
   KVD_TRY(check_ptr(h, "h"));
-  KVD_TRY(check_ptr(gamma, "gamma"));
+  KVD_TRY(check_gamma(shape, gamma));
   KVD_TRY(check_ptr(w_k, "w_k"));
   KVD_TRY(check_ptr(w_v, "w_v"));
   if (pos0 == nullptr) return fail(KVD_ERR_NULL, "pos0 is NULL");
@@ -327,11 +332,11 @@ kvd_status kvd_recompute_kv(const kvd_attn_shape* shape, const void* h, int32_t 
   const long long max_wgs =
       shape->head_dim >= 256 ? kvd::kStreamRecomputeMaxWgsHd256 : kvd::kStreamRecomputeMaxWgs;
   if (shape->dtype == KVD_BF16 && G >= 1 && stream_wgs <= max_wgs)
-    return device_status(kvd::launch_project_current(a, 1, shape->head_dim, shape->w_layout == KVD_W_PACKED,
-                                                     a.n_kv_units, (hipStream_t)stream),
+    return device_status(kvd::launch_project_current(a, 1, shape->head_dim, shape->w_layout, a.n_kv_units,
+                                                     (hipStream_t)stream),
                          "kvd_recompute_kv launch");
-  return device_status(kvd::launch_proj(a, shape->dtype == KVD_BF16, shape->head_dim, shape->w_layout == KVD_W_PACKED,
-                                        a.n_kv_units, (hipStream_t)stream),
+  return device_status(kvd::launch_proj(a, shape->dtype == KVD_BF16, shape->head_dim, shape->w_layout, a.n_kv_units,
+                                        (hipStream_t)stream),
                        "kvd_recompute_kv launch");
 }
 
@@ -350,7 +355,7 @@ kvd_status kvd_project_qkv(const kvd_attn_shape* shape, const void* h_new, const
   }
   if (B == 0) return KVD_OK;
   KVD_TRY(check_ptr(h_new, "h_new"));
-  KVD_TRY(check_ptr(gamma, "gamma"));
+  KVD_TRY(check_gamma(shape, gamma));
   KVD_TRY(check_ptr(w_q, "w_q"));
   KVD_TRY(check_ptr(q_out, "q_out"));
   if (pos == nullptr) return fail(KVD_ERR_NULL, "pos is NULL");
@@ -384,7 +389,7 @@ kvd_status kvd_project_qkv(const kvd_attn_shape* shape, const void* h_new, const
   fill_rev(shape, a.rev);
   const int units = a.n_kv_units + (shape->n_q_heads + 1) / 2;
   return device_status(
-      kvd::launch_project_current(a, shape->dtype == KVD_BF16, shape->head_dim, shape->w_layout == KVD_W_PACKED, units,
+      kvd::launch_project_current(a, shape->dtype == KVD_BF16, shape->head_dim, shape->w_layout, units,
                                   (hipStream_t)stream),
       "kvd_project_qkv launch");
 }
@@ -420,7 +425,7 @@ kvd_status check_fused_args(const kvd_attn_shape* shape, const void* q, const vo
   if (T_rec > 0) {
     if (h_ld < T_rec) return fail(KVD_ERR_SHAPE, "h_ld=%d is smaller than T_rec=%d", h_ld, T_rec);
     KVD_TRY(check_ptr(h, "h"));
-    KVD_TRY(check_ptr(gamma, "gamma"));
+    KVD_TRY(check_gamma(shape, gamma));
     KVD_TRY(check_ptr(w_k, "w_k"));
     KVD_TRY(check_ptr(w_v, "w_v"));
   }
@@ -476,7 +481,7 @@ kvd_status fused_launch(const kvd_attn_shape* shape, const void* q, const void* 
   a.eps = shape->rms_eps;
   fill_rev(shape, a.rev);
   return device_status(kvd::launch_fused(a, shape->dtype == KVD_BF16, shape->head_dim,
-                                         shape->w_layout == KVD_W_PACKED, plan.mt == kvd::kMtWide,
+                                         shape->w_layout, plan.mt == kvd::kMtWide,
                                          (hipStream_t)stream),
                        name);
 }
@@ -575,7 +580,7 @@ kvd_status kvd_pack_matrix(const void* w, int32_t rows, int32_t cols, void* pack
   const char* a = static_cast<const char*>(w);
   const char* b = static_cast<const char*>(packed);
   if (a < b + bytes && b < a + bytes) return fail(KVD_ERR_SHAPE, "packed must not overlap w");
-  return device_status(kvd::launch_pack(w, packed, rows, cols, (hipStream_t)stream), "kvd_pack_matrix launch");
+  return device_status(kvd::launch_pack(w, nullptr, packed, rows, cols, (hipStream_t)stream), "kvd_pack_matrix launch");
 }
 
 namespace {
@@ -611,6 +616,8 @@ kvd_status check_block(const kvd_attn_shape* shape, int32_t d_ff, int32_t B, int
   KVD_TRY(check_shape(shape));
   KVD_TRY(check_batch(B));
   if (shape->dtype != KVD_BF16) return fail(KVD_ERR_UNSUPPORTED, "the block forward runs in bf16");
+  if (shape->w_layout == KVD_W_PACKED_GAMMA)
+    return fail(KVD_ERR_UNSUPPORTED, "the block forward takes row-major or packed weights (its norms apply gamma)");
   if (shape->head_dim != 128 && shape->head_dim != 256)
     return fail(KVD_ERR_UNSUPPORTED, "the block forward supports head_dim 128 and 256 (got %d)", shape->head_dim);
   if (shape->d_model % 512 != 0)
@@ -766,7 +773,28 @@ kvd_status kvd_pack_weights(const kvd_attn_shape* shape, const void* w, int32_t 
   const char* a = static_cast<const char*>(w);
   const char* b = static_cast<const char*>(packed);
   if (a < b + bytes && b < a + bytes) return fail(KVD_ERR_SHAPE, "packed must not overlap w");
-  return device_status(kvd::launch_pack(w, packed, rows, s.d_model, (hipStream_t)stream), "kvd_pack_weights launch");
+  return device_status(kvd::launch_pack(w, nullptr, packed, rows, s.d_model, (hipStream_t)stream), "kvd_pack_weights launch");
+}
+
+kvd_status kvd_pack_weights_gamma(const kvd_attn_shape* shape, const void* w, const void* gamma, int32_t rows,
+                                  void* packed, void* stream) {
+  if (shape == nullptr) return fail(KVD_ERR_NULL, "shape is NULL");
+  kvd_attn_shape s = *shape;
+  s.w_layout = KVD_W_ROWMAJOR;
+  KVD_TRY(check_shape(&s));
+  if (s.dtype != KVD_BF16) return fail(KVD_ERR_UNSUPPORTED, "kvd_pack_weights_gamma packs bf16 weights");
+  if (rows < 32 || rows % 32 != 0) return fail(KVD_ERR_SHAPE, "rows=%d must be a positive multiple of 32", rows);
+  KVD_TRY(check_ptr(w, "w"));
+  KVD_TRY(check_ptr(gamma, "gamma"));
+  KVD_TRY(check_ptr(packed, "packed"));
+  const size_t bytes = (size_t)rows * s.d_model * 2;
+  const char* a = static_cast<const char*>(w);
+  const char* b = static_cast<const char*>(packed);
+  const char* g = static_cast<const char*>(gamma);
+  if (a < b + bytes && b < a + bytes) return fail(KVD_ERR_SHAPE, "packed must not overlap w");
+  if (g < b + bytes && b < g + (size_t)s.d_model * 2) return fail(KVD_ERR_SHAPE, "packed must not overlap gamma");
+  return device_status(kvd::launch_pack(w, gamma, packed, rows, s.d_model, (hipStream_t)stream),
+                       "kvd_pack_weights_gamma launch");
 }
 
 kvd_status kvd_combine(const kvd_attn_shape* shape, int32_t B, int32_t S, const void* ws, size_t ws_bytes, void* out,

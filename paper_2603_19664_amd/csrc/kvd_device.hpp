@@ -156,6 +156,35 @@ __device__ __forceinline__ uint4 scale_chunk_bf16(uint4 hv, uint4 gv) {
   return make_uint4(o[0], o[1], o[2], o[3]);
 }
 
+// Folded weights (W diag(gamma), kvd_pack_weights_gamma): the residual chunk is
+// staged unchanged and its sum of squares takes one dot2 per word (both
+// products exact in fp32, added to the running sum).  Every producer of folded
+// K/V runs this chain per (token, 8-element column chunk) in K order, so they
+// stay bit-identical to each other.
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ void sumsq_chunk_dot2(uint4 hv, float& ss) {
+  ss = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, hv.x), __builtin_bit_cast(bf16x2_t, hv.x), ss, false);
+  ss = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, hv.y), __builtin_bit_cast(bf16x2_t, hv.y), ss, false);
+  ss = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, hv.z), __builtin_bit_cast(bf16x2_t, hv.z), ss, false);
+  ss = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, hv.w), __builtin_bit_cast(bf16x2_t, hv.w), ss, false);
+}
+// The staged B-operand chunk and the sum of squares, for weights with gamma
+// applied by the kernel (FOLD = false: bf16(gamma * h)) or folded into them.
+template <bool FOLD>
+__device__ __forceinline__ uint4 stage_chunk(uint4 hv, uint4 gv, float& ss) {
+  if constexpr (FOLD) {
+    sumsq_chunk_dot2(hv, ss);
+    return hv;
+  } else {
+    return stage_chunk_bf16(hv, gv, ss);
+  }
+}
+template <bool FOLD>
+__device__ __forceinline__ void sumsq_chunk(uint4 hv, float& ss) {
+  if constexpr (FOLD) sumsq_chunk_dot2(hv, ss);
+  else sumsq_chunk_bf16(hv, ss);
+}
+
 // Per-token 1/rms from the per-thread partial sums: thread (row, sub) holds the
 // sum over its chunk column sub = tid & 7; the 8 partials of a row sit in 8
 // consecutive lanes and are added by a fixed xor tree.  Rows of thread tid are
@@ -187,6 +216,15 @@ __device__ __forceinline__ int wave_id() { return __builtin_amdgcn_readfirstlane
 // of the wave are outstanding (expcnt and lgkmcnt left unconstrained).
 constexpr int vmcnt_imm(int n) { return (n & 15) | ((n >> 4) << 14) | 0x0f70; }
 
+// Slot (16 bytes) of B-fragment lane lam (0..63; column lam % 32, k-half lam / 32)
+// of substep u inside its 1 KiB staged fragment.  Staging thread (token row,
+// column chunk sub) writes fragment sub / 2, lane row % 32 + 32 (sub % 2): the
+// 8 lanes of one token would all land on the same LDS banks in lane order,
+// eight-way conflicts on every staging write.  The XOR below spreads them (and
+// any 8 or 16 consecutive lanes of a write or of a fragment read) over distinct
+// banks; only addresses change, never an operand.
+__device__ __forceinline__ int bslot(int lam, int u) { return lam ^ (u << 1) ^ ((lam >> 5) * 9); }
+
 // Element offset of the MFMA A operand chunk (K-step s, 16-wide substep u) from a
 // lane's base pointer.  Row-major: base = row (row0 + lane % 32), column 8 (lane / 32);
 // packed (kvd_pack_weights): base = block row row0 + lane * 8, one 512-element
@@ -206,7 +244,7 @@ __device__ __forceinline__ size_t w_off(int s, int u) {
 // registers (each weight byte is used by exactly one wave), kDepth K-steps
 // ahead; gamma-scaled residuals are staged through LDS (shared by all waves),
 // double buffered.
-template <int HD, int MT, bool PACKED>
+template <int HD, int MT, bool PACKED, bool FOLD = false>
 struct MfmaTile {
   static constexpr int NT = kNtTile;
   static constexpr int NW = NT / 64;
@@ -339,7 +377,7 @@ struct MfmaTile {
     uint4 H[D];
     float ss[CPT] = {0.0f};
     const int row = tid >> 3;
-    const int lofs = ((row >> 5) * 4 + (sub >> 1)) * 512 + 8 * ((row & 31) + 32 * (sub & 1));
+    const int lofs = ((row >> 5) * 4 + (sub >> 1)) * 512 + 8 * bslot((row & 31) + 32 * (sub & 1), sub >> 1);
     const int bt0 = NB_T == 2 ? 0 : tw;  // first absolute token block of this wave
 
     auto load_wu = [&](int slot, int s, int u) {
@@ -351,13 +389,16 @@ struct MfmaTile {
     // Tokens past the end of a ragged tile stage a readable row's values: their
     // MFMA columns are independent of the others and their 1/rms is zero.
     auto put_hv = [&](int slot, const uint4& gv) {
-      *reinterpret_cast<uint4*>(hst + (size_t)slot * SLOT + lofs) = stage_chunk_bf16(H[slot], gv, ss[0]);
+      *reinterpret_cast<uint4*>(hst + (size_t)slot * SLOT + lofs) = stage_chunk<FOLD>(H[slot], gv, ss[0]);
     };
-    auto put_h = [&](int slot, int s) { put_hv(slot, *reinterpret_cast<const uint4*>(gam + (size_t)s * kKT + 8 * sub)); };
+    auto put_h = [&](int slot, int s) {
+      put_hv(slot, FOLD ? uint4{} : *reinterpret_cast<const uint4*>(gam + (size_t)s * kKT + 8 * sub));
+    };
     auto rd = [&](bf16x8_t (&bv)[NB_T], int slot, int u) {
 #pragma unroll
       for (int bt = 0; bt < NB_T; ++bt)
-        bv[bt] = *reinterpret_cast<const bf16x8_t*>(hst + (size_t)slot * SLOT + ((bt0 + bt) * 4 + u) * 512 + 8 * lane);
+        bv[bt] = *reinterpret_cast<const bf16x8_t*>(hst + (size_t)slot * SLOT + ((bt0 + bt) * 4 + u) * 512 +
+                                                    8 * bslot(lane, u));
     };
     auto mma = [&](int slot, int u, const bf16x8_t (&bv)[NB_T]) {
 #pragma unroll
@@ -430,7 +471,7 @@ struct MfmaTile {
     // memory: the LDS copy is complete only after the barrier)
 #pragma unroll
     for (int i = 0; i < D; ++i) load_h(i, min(i, nsteps - 1));
-    const uint4 g0 = *reinterpret_cast<const uint4*>(gam_g + 8 * sub);
+    const uint4 g0 = FOLD ? uint4{} : *reinterpret_cast<const uint4*>(gam_g + 8 * sub);
     __builtin_amdgcn_sched_barrier(0);  // keep it ahead of the weight loads (in-order waits)
 #pragma unroll
     for (int i = 0; i < D; ++i)
@@ -485,7 +526,7 @@ struct MfmaTile {
 // per step, after the second substep.  Loads go through
 // buffer resources (wave-uniform base and extent in SGPRs, a 32-bit offset per
 // lane), which keeps the addresses out of the vector registers.
-template <int HD, bool PACKED>
+template <int HD, bool PACKED, bool FOLD = false>
 struct WideTile {
   static constexpr int NT = kNtWide;
   static constexpr int MT = kMtWide;
@@ -623,7 +664,7 @@ struct WideTile {
     // chunk r of this thread: token (tid >> 3) + 64 r = token block
     // (tid >> 8) + 2 r, column (tid >> 3) % 32; elements 8 sub .. 8 sub + 7 of
     // the K-step = substep sub / 2, lane half sub % 2 of the B fragment
-    const int lofs = ((tid >> 8) * 4 + (sub >> 1)) * 512 + 8 * (((tid >> 3) & 31) + 32 * (sub & 1));
+    const int lofs = ((tid >> 8) * 4 + (sub >> 1)) * 512 + 8 * bslot(((tid >> 3) & 31) + 32 * (sub & 1), sub >> 1);
 
     auto load_wu = [&](int slot, int s, int u) {
 #pragma unroll
@@ -644,11 +685,11 @@ struct WideTile {
 #pragma unroll
       for (int r = 0; r < CPT; ++r)
         *reinterpret_cast<uint4*>(hst + (size_t)lslot * SLOT + r * 8 * 512 + lofs) =
-            stage_chunk_bf16(H[hslot][r], gv, ss[r]);
+            stage_chunk<FOLD>(H[hslot][r], gv, ss[r]);
     };
     // B fragment of K-step slot lslot, substep u, token block bt
     auto rd1 = [&](int lslot, int u, int bt) {
-      return *reinterpret_cast<const bf16x8_t*>(hst + (size_t)lslot * SLOT + (bt * 4 + u) * 512 + 8 * lane);
+      return *reinterpret_cast<const bf16x8_t*>(hst + (size_t)lslot * SLOT + (bt * 4 + u) * 512 + 8 * bslot(lane, u));
     };
 
     // A step is 16 units k = 4 u + bt (substep u, token block bt), each one B
@@ -696,7 +737,7 @@ struct WideTile {
       };
       __builtin_amdgcn_sched_barrier(0);
       if (!GUARD || s + 1 < nsteps)
-        put_hv(LN, 0, *reinterpret_cast<const uint4*>(gam + (size_t)(s + 1) * kKT + 8 * sub));
+        put_hv(LN, 0, FOLD ? uint4{} : *reinterpret_cast<const uint4*>(gam + (size_t)(s + 1) * kKT + 8 * sub));
       unit(IC<0>{}); unit(IC<1>{}); unit(IC<2>{}); unit(IC<3>{});
       unit(IC<4>{}); unit(IC<5>{}); unit(IC<6>{}); unit(IC<7>{});
       __builtin_amdgcn_sched_barrier(0);
@@ -712,7 +753,7 @@ struct WideTile {
     // the LDS copy is complete only after the barrier), step 1's residuals
     // requested
     load_h(0, 0);
-    const uint4 g0 = *reinterpret_cast<const uint4*>(gam_g + 8 * sub);
+    const uint4 g0 = FOLD ? uint4{} : *reinterpret_cast<const uint4*>(gam_g + 8 * sub);
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int i = 0; i < DW; ++i)
@@ -860,13 +901,13 @@ __device__ __forceinline__ void load_q(const T* q, int b, int n_q, int j, int g,
 }
 
 // Setup values of a recomputed tile: the KV group's query rows (WITH_Q; as load_q
-// stores them), gamma (bf16 only: the fp32 engine reads it from global memory) and the
-// RoPE inverse frequencies.  The constructor issues the loads of a thread's
+// stores them), gamma (bf16 with GAMMA, i.e. weights without gamma folded in:
+// the fp32 engine reads it from global memory) and the RoPE inverse frequencies.  The constructor issues the loads of a thread's
 // first chunks into registers with clamped indexes, unconditionally; store()
 // writes the in-range ones to LDS and copies what is left over (more than one q
 // chunk or two gamma chunks per thread) with plain loops.  Constructed before a
 // tile engine's first loads, stored by its setup(): the two latencies overlap.
-template <typename T, int HD, int NT, bool WITH_Q>
+template <typename T, int HD, int NT, bool WITH_Q, bool GAMMA = true>
 struct TileSetup {
   static constexpr int CH = 16 / sizeof(T);
   const T* qsrc;
@@ -884,7 +925,7 @@ struct TileSetup {
       qv = *reinterpret_cast<const u32x4_t*>(qsrc + CH * min(tid, nqc - 1));
     }
     rv = rev[min(tid, HD / 2 - 1)];
-    if constexpr (sizeof(T) == 2) {
+    if constexpr (sizeof(T) == 2 && GAMMA) {
       gsrc = static_cast<const uint16_t*>(gamma);
       ngc = d / 8;
       gv0 = *reinterpret_cast<const u32x4_t*>(gsrc + 8 * min(tid, ngc - 1));
@@ -913,7 +954,7 @@ struct TileSetup {
       for (int c = tid + NT; c < nqc; c += NT) put_q(c, *reinterpret_cast<const u32x4_t*>(qsrc + CH * c));
     }
     if (tid < HD / 2) revs[tid] = rv;
-    if constexpr (sizeof(T) == 2) {
+    if constexpr (sizeof(T) == 2 && GAMMA) {
       if (tid < ngc) *reinterpret_cast<u32x4_t*>(gam + 8 * tid) = gv0;
       if (tid + NT < ngc) *reinterpret_cast<u32x4_t*>(gam + 8 * (tid + NT)) = gv1;
       for (int c = tid + 2 * NT; c < ngc; c += NT)

@@ -28,7 +28,7 @@ namespace kvd {
 
 // grid: xcd_map(n_units * n_tiles) workgroups; item = unit * n_tiles + tile, so
 // the token tiles of one KV head (which share W_k / W_v) run on one XCD.
-template <typename T, int HD, int MT, bool PACKED>
+template <typename T, int HD, int MT, bool PACKED, bool FOLD>
 __global__ __launch_bounds__(kNtTile, 1) void proj_kernel(ProjArgs a, int per_xcd, int n_tiles, int n_units) {
   extern __shared__ __align__(16) char lds[];
   constexpr int NT = kNtTile;
@@ -69,7 +69,7 @@ __global__ __launch_bounds__(kNtTile, 1) void proj_kernel(ProjArgs a, int per_xc
 
   // gamma, rev and the positions reach LDS while the K-loop's first loads are in flight
   uint16_t* gam = reinterpret_cast<uint16_t*>(lds + PL.end);
-  const TileSetup<T, HD, NT, false> su(nullptr, 0, 0, 0, 0, a.gamma, a.d, a.rev);
+  const TileSetup<T, HD, NT, false, !FOLD> su(nullptr, 0, 0, 0, 0, a.gamma, a.d, a.rev);
   // position of staged token tid (tid < MT): pos0[b] + t, 0 past the end; the
   // load is issued here and its value used in setup()
   const long long pn = n0 + min(tid, MT - 1);
@@ -93,8 +93,8 @@ __global__ __launch_bounds__(kNtTile, 1) void proj_kernel(ProjArgs a, int per_xc
   }
 
   if constexpr (sizeof(T) == 2) {
-    MfmaTile<HD, MT, PACKED>::run(hrow, valid, gam, static_cast<const uint16_t*>(a.gamma), a.d, a.eps, halves, hst,
-                                  rinv, pos, rev, kv, setup);
+    MfmaTile<HD, MT, PACKED, FOLD>::run(hrow, valid, gam, static_cast<const uint16_t*>(a.gamma), a.d, a.eps, halves,
+                                        hst, rinv, pos, rev, kv, setup);
   } else {
     F32Tile<HD, MT>::run(hrow, valid, static_cast<const float*>(a.gamma), a.d, a.eps, halves, hst, rinv, pos, rev,
                          kv, setup);
@@ -143,7 +143,7 @@ __global__ __launch_bounds__(kNtTile, 1) void proj_kernel(ProjArgs a, int per_xc
 // K_t / V_t equal what recompute gives for the same row.  NCH > 0: the chunk
 // count, fixed at compile time so that the loaders' loop is straight-line code
 // (their memory-counter waits then keep every chunk in flight).
-template <int HD, bool PACKED, int NCH>
+template <int HD, bool PACKED, int NCH, bool FOLD>
 __global__ __launch_bounds__(64 * kStreamWaves) void stream_proj_kernel(ProjArgs a, int q_blocks, int k_blocks,
                                                                         int G) {
   extern __shared__ __align__(16) char lds[];
@@ -198,7 +198,9 @@ __global__ __launch_bounds__(64 * kStreamWaves) void stream_proj_kernel(ProjArgs
       *reinterpret_cast<u32x4_t*>(slot + (ld * LPW + i) * 512) = rv[i];
   };
   // gamma * h -> bf16 into hs (present rows only), by all waves between barriers A and C
+  // (folded weights: the MFMA reads the residual rows in hb as they are)
   auto scale_rows = [&]() {
+    if constexpr (FOLD) return;
     const int cpr = d / 8;
     for (int i = tid; i < nt * cpr; i += 64 * NW) {
       const int r = i / cpr, ch = i - r * cpr;
@@ -221,7 +223,7 @@ __global__ __launch_bounds__(64 * kStreamWaves) void stream_proj_kernel(ProjArgs
     // (with their share of the row scaling).
     {
       const int cpr = d / 8;  // 16-byte chunks per row
-      for (int r = ld; r <= nt; r += NW - 1) {
+      for (int r = ld; r < nt + (FOLD ? 0 : 1); r += NW - 1) {  // rows, then gamma
         const int nb = (n0 + r) / a.T, ntk = n0 + r - nb * a.T;
         const uint16_t* src = (r < nt ? static_cast<const uint16_t*>(a.h) + ((size_t)nb * a.h_ld + ntk) * d
                                       : static_cast<const uint16_t*>(a.gamma)) + 8 * lane;
@@ -261,7 +263,7 @@ __global__ __launch_bounds__(64 * kStreamWaves) void stream_proj_kernel(ProjArgs
       if (srow < nt) {
 #pragma unroll
         for (int kk = 0; kk < CK; ++kk)
-          if (c * CK + kk < nsteps) sumsq_chunk_bf16(x[kk], ss);
+          if (c * CK + kk < nsteps) sumsq_chunk<FOLD>(x[kk], ss);
       }
     };
     ss_read(0);
@@ -320,7 +322,7 @@ __global__ __launch_bounds__(64 * kStreamWaves) void stream_proj_kernel(ProjArgs
   // Columns of absent tokens read row 0 and hold unused values: MFMA output
   // columns are independent and only those of present tokens are stored.
   const int col = lane & 31;
-  const uint16_t* hcol = hs + (size_t)(col < nt ? col : 0) * HLD + 8 * (lane >> 5);
+  const uint16_t* hcol = (FOLD ? hb : hs) + (size_t)(col < nt ? col : 0) * HLD + 8 * (lane >> 5);
   {
     bf16x8_t a0[FPC], b0f[FPC], a1[FPC], b1f[FPC];  // chunk c's fragments and chunk c + 1's
     auto read_chunk = [&](bf16x8_t (&av)[FPC], bf16x8_t (&bv)[FPC], int c) {
@@ -387,7 +389,7 @@ __global__ __launch_bounds__(64 * kStreamWaves) void stream_proj_kernel(ProjArgs
 // recomputes residual rows r*MT..r*MT+MT-1 (partial r).  A folded tail (<= fold_rows<T>() rows, n_tail = 0) is attended
 // with the last recomputed chunk's keys.  MT = kMtWide: the wide engine (bf16,
 // 4 waves, 128-key chunks, no folded tail).
-template <typename T, int HD, int MT, bool PACKED>
+template <typename T, int HD, int MT, bool PACKED, bool FOLD>
 __device__ __forceinline__ void fused_body(const FusedArgs& a, int per_xcd, int hg) {
   extern __shared__ __align__(16) char lds[];
   constexpr bool WIDE = MT == kMtWide;
@@ -450,7 +452,7 @@ __device__ __forceinline__ void fused_body(const FusedArgs& a, int per_xcd, int 
     T* hst = reinterpret_cast<T*>(lds + PL.hst);
     uint16_t* gam = reinterpret_cast<uint16_t*>(lds + AL.end);
     // q, gamma and rev reach LDS while the K-loop's first loads are in flight
-    const TileSetup<T, HD, NT, true> su(static_cast<const T*>(a.q), b, a.n_q, j, g, a.gamma, a.d, a.rev);
+    const TileSetup<T, HD, NT, true, !FOLD> su(static_cast<const T*>(a.q), b, a.n_q, j, g, a.gamma, a.d, a.rev);
     // pos0[b] is read here, after the K-loop's first loads are issued: a scalar
     // load read up front holds back every address computation behind its latency
     auto setup = [&]() {
@@ -473,12 +475,12 @@ __device__ __forceinline__ void fused_body(const FusedArgs& a, int per_xcd, int 
     const Half halves[2] = {Half{static_cast<const T*>(a.w_k) + j * hd_d, 1},
                             Half{static_cast<const T*>(a.w_v) + j * hd_d, 0}};
     if constexpr (WIDE) {
-      WideTile<HD, PACKED>::run(static_cast<const uint16_t*>(a.h) + ((size_t)b * a.h_ld + t0) * a.d, n, gam,
+      WideTile<HD, PACKED, FOLD>::run(static_cast<const uint16_t*>(a.h) + ((size_t)b * a.h_ld + t0) * a.d, n, gam,
                                 static_cast<const uint16_t*>(a.gamma), a.d, a.eps, halves, hst, rinv, pos, rev, kv,
                                 setup);
     } else if constexpr (sizeof(T) == 2) {
-      MfmaTile<HD, MT, PACKED>::run(hrow, valid, gam, static_cast<const uint16_t*>(a.gamma), a.d, a.eps, halves, hst,
-                                    rinv, pos, rev, kv, setup);
+      MfmaTile<HD, MT, PACKED, FOLD>::run(hrow, valid, gam, static_cast<const uint16_t*>(a.gamma), a.d, a.eps, halves,
+                                          hst, rinv, pos, rev, kv, setup);
     } else {
       F32Tile<HD, MT>::run(hrow, valid, static_cast<const float*>(a.gamma), a.d, a.eps, halves, hst, rinv, pos, rev,
                            kv, setup);
@@ -525,17 +527,17 @@ __device__ __forceinline__ void fused_body(const FusedArgs& a, int per_xcd, int 
   }
 }
 
-template <typename T, int HD, int MT, bool PACKED>
+template <typename T, int HD, int MT, bool PACKED, bool FOLD>
 __global__ __launch_bounds__(kNtTile, 1) void fused_kernel(FusedArgs a, int per_xcd, int hg) {
-  fused_body<T, HD, MT, PACKED>(a, per_xcd, hg);
+  fused_body<T, HD, MT, PACKED, FOLD>(a, per_xcd, hg);
 }
 
 // One workgroup of 8 waves per CU, two per SIMD: 256 registers per lane (the
 // wave's 128-token accumulators in AGPRs).
-template <int HD, bool PACKED>
+template <int HD, bool PACKED, bool FOLD>
 __global__ __launch_bounds__(kNtWide, 1) void fused_wide_kernel(
     FusedArgs a, int per_xcd, int hg) {
-  fused_body<uint16_t, HD, kMtWide, PACKED>(a, per_xcd, hg);
+  fused_body<uint16_t, HD, kMtWide, PACKED, FOLD>(a, per_xcd, hg);
 }
 
 // ------------------------------------------------------------------ stored-K/V attention
@@ -801,7 +803,10 @@ __global__ __launch_bounds__(kNtAttn) void combine_kernel(const float* ws_acc, c
 // ------------------------------------------------------------------ weight packing
 
 // One thread per 16-byte chunk of the packed matrix (see kvd_pack_weights).
-__global__ __launch_bounds__(256) void pack_kernel(const uint16_t* w, uint16_t* out, int rows, int d) {
+// gamma != nullptr: each element becomes bf16(w * gamma[column]) (the exact
+// fp32 product, one round-to-nearest-even), kvd_pack_weights_gamma.
+__global__ __launch_bounds__(256) void pack_kernel(const uint16_t* w, const uint16_t* gamma, uint16_t* out, int rows,
+                                                   int d) {
   const long long chunk = (long long)blockIdx.x * 256 + threadIdx.x;
   const long long n = (long long)rows * d / 8;
   if (chunk >= n) return;
@@ -809,8 +814,17 @@ __global__ __launch_bounds__(256) void pack_kernel(const uint16_t* w, uint16_t* 
   const long long blk = chunk / 64;
   const int kb = (int)(blk % (d / 16));
   const long long rb = blk / (d / 16);
-  const uint16_t* src = w + (size_t)(rb * 32 + l % 32) * d + 16 * kb + 8 * (l / 32);
-  *reinterpret_cast<uint4*>(out + (size_t)chunk * 8) = *reinterpret_cast<const uint4*>(src);
+  const int col = 16 * kb + 8 * (l / 32);
+  const uint16_t* src = w + (size_t)(rb * 32 + l % 32) * d + col;
+  uint4 v = *reinterpret_cast<const uint4*>(src);
+  if (gamma != nullptr) {
+    const uint4 g = *reinterpret_cast<const uint4*>(gamma + col);
+    v.x = pack_bf16x2(bf_lo(v.x) * bf_lo(g.x), bf_hi(v.x) * bf_hi(g.x));
+    v.y = pack_bf16x2(bf_lo(v.y) * bf_lo(g.y), bf_hi(v.y) * bf_hi(g.y));
+    v.z = pack_bf16x2(bf_lo(v.z) * bf_lo(g.z), bf_hi(v.z) * bf_hi(g.z));
+    v.w = pack_bf16x2(bf_lo(v.w) * bf_lo(g.w), bf_hi(v.w) * bf_hi(g.w));
+  }
+  *reinterpret_cast<uint4*>(out + (size_t)chunk * 8) = v;
 }
 
 // ------------------------------------------------------------------ residual checkpoint store
@@ -833,10 +847,10 @@ hipError_t launch_copy_rows(const void* src, size_t src_stride, void* dst, size_
   return hipGetLastError();
 }
 
-hipError_t launch_pack(const void* w, void* out, int rows, int d, hipStream_t st) {
+hipError_t launch_pack(const void* w, const void* gamma, void* out, int rows, int d, hipStream_t st) {
   const long long n = (long long)rows * d / 8;
   hipLaunchKernelGGL(pack_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, static_cast<const uint16_t*>(w),
-                     static_cast<uint16_t*>(out), rows, d);
+                     static_cast<const uint16_t*>(gamma), static_cast<uint16_t*>(out), rows, d);
   return hipGetLastError();
 }
 
@@ -894,12 +908,14 @@ static hipError_t ensure_lds(K kernel, size_t bytes, std::atomic<size_t>& done) 
   return hipSuccess;
 }
 
-template <typename T, int HD, bool PACKED>
+// Launcher templates take the weight layout L: 0 row-major, 1 packed, 2 packed
+// with gamma folded in (kvd_weight_layout).
+template <typename T, int HD, int L>
 static hipError_t proj_t(const ProjArgs& a, int n_units, hipStream_t st) {
   constexpr int MT = sizeof(T) == 2 ? kMtBf16 : kMtF32;
   const size_t bytes = proj_lds<T>(HD, MT).end + gamma_lds_bytes(a.d);
   static std::atomic<size_t> done{0};
-  auto k = proj_kernel<T, HD, MT, PACKED>;
+  auto k = proj_kernel<T, HD, MT, L != 0, L == 2>;
   hipError_t e = ensure_lds(k, bytes, done);
   if (e != hipSuccess) return e;
   const long long ntok = (long long)a.B * a.T;
@@ -909,13 +925,13 @@ static hipError_t proj_t(const ProjArgs& a, int n_units, hipStream_t st) {
   return hipGetLastError();
 }
 
-template <int HD, bool PACKED, int NCH>
+template <int HD, int L, int NCH>
 static hipError_t stream_t(const ProjArgs& a, hipStream_t st) {
   const int G = stream_group(a.d, a.B * a.T, kLdsPerGroup);
   if (G < 1) return hipErrorInvalidValue;  // validated by the caller
   const size_t bytes = stream_lds(a.d, G).end;
   static std::atomic<size_t> done{0};
-  auto k = stream_proj_kernel<HD, PACKED, NCH>;
+  auto k = stream_proj_kernel<HD, L != 0, NCH, L == 2>;
   hipError_t e = ensure_lds(k, bytes, done);
   if (e != hipSuccess) return e;
   const int qb = a.q_out ? a.n_q * HD / 32 : 0;
@@ -925,12 +941,12 @@ static hipError_t stream_t(const ProjArgs& a, hipStream_t st) {
   return hipGetLastError();
 }
 
-template <typename T, int HD, bool PACKED>
+template <typename T, int HD, int L>
 static hipError_t fused_t(const FusedArgs& a, hipStream_t st) {
   constexpr int MT = sizeof(T) == 2 ? kMtBf16 : kMtF32;
   const size_t bytes = fused_lds_bytes<T>(a.n_q / a.n_kv, HD, MT) + gamma_lds_bytes(a.d);
   static std::atomic<size_t> done{0};
-  auto k = fused_kernel<T, HD, MT, PACKED>;
+  auto k = fused_kernel<T, HD, MT, L != 0, L == 2>;
   hipError_t e = ensure_lds(k, bytes, done);
   if (e != hipSuccess) return e;
   const int n_tail = fused_tail_tiles<T>(a.n_rec, a.T_tail);
@@ -944,11 +960,11 @@ static hipError_t fused_t(const FusedArgs& a, hipStream_t st) {
   return hipGetLastError();
 }
 
-template <int HD, bool PACKED>
+template <int HD, int L>
 static hipError_t fused_wide_t(const FusedArgs& a, hipStream_t st) {
   const size_t bytes = fused_wide_lds_bytes(a.n_q / a.n_kv, HD) + gamma_lds_bytes(a.d);
   static std::atomic<size_t> done{0};
-  auto k = fused_wide_kernel<HD, PACKED>;
+  auto k = fused_wide_kernel<HD, L != 0, L == 2>;
   hipError_t e = ensure_lds(k, bytes, done);
   if (e != hipSuccess) return e;
   const int C = (a.T_tail + kTile - 1) / kTile + a.n_rec;
@@ -1014,48 +1030,65 @@ static hipError_t combine_t(const float* ws_acc, const float* ws_ml, void* out, 
       return hipErrorInvalidValue;                         \
   }
 
-hipError_t launch_proj(const ProjArgs& a, int dtype_bf16, int hd, int packed, int n_units, hipStream_t st) {
-#define PB(H) (packed ? proj_t<uint16_t, H, true>(a, n_units, st) : proj_t<uint16_t, H, false>(a, n_units, st))
-#define PF(H) proj_t<float, H, false>(a, n_units, st)
+// f(IC<L>{}) for layout L in 0..2
+template <class F>
+static hipError_t with_layout(int layout, const F& f) {
+  switch (layout) {
+    case 0: return f(IC<0>{});
+    case 1: return f(IC<1>{});
+    case 2: return f(IC<2>{});
+    default: return hipErrorInvalidValue;
+  }
+}
+
+hipError_t launch_proj(const ProjArgs& a, int dtype_bf16, int hd, int layout, int n_units, hipStream_t st) {
+#define PB(H) with_layout(layout, [&](auto lc) { return proj_t<uint16_t, H, decltype(lc)::value>(a, n_units, st); })
+#define PF(H) proj_t<float, H, 0>(a, n_units, st)
   KVD_DISPATCH(dtype_bf16, hd, PB, PF)
 #undef PB
 #undef PF
 }
 
 // d = 2560 (Gemma-3-4B) and 1536 (Qwen2.5-1.5B) get a compile-time chunk count.
-template <int HD, bool PACKED>
+template <int HD, int L>
 static hipError_t stream_nch(const ProjArgs& a, hipStream_t st) {
   switch (a.d / (kKT * kStreamChunk)) {
-    case 20: if (a.d == 20 * kKT * kStreamChunk) return stream_t<HD, PACKED, 20>(a, st); break;
-    case 12: if (a.d == 12 * kKT * kStreamChunk) return stream_t<HD, PACKED, 12>(a, st); break;
+    case 20: if (a.d == 20 * kKT * kStreamChunk) return stream_t<HD, L, 20>(a, st); break;
+    case 12: if (a.d == 12 * kKT * kStreamChunk) return stream_t<HD, L, 12>(a, st); break;
     default: break;
   }
-  return stream_t<HD, PACKED, 0>(a, st);
+  return stream_t<HD, L, 0>(a, st);
 }
 
-hipError_t launch_project_current(const ProjArgs& a, int dtype_bf16, int hd, int packed, int n_units,
+hipError_t launch_project_current(const ProjArgs& a, int dtype_bf16, int hd, int layout, int n_units,
                                   hipStream_t st) {
   if (!dtype_bf16) return launch_proj(a, 0, hd, 0, n_units, st);
-  switch (hd) {
-    case 64: return packed ? stream_nch<64, true>(a, st) : stream_nch<64, false>(a, st);
-    case 128: return packed ? stream_nch<128, true>(a, st) : stream_nch<128, false>(a, st);
-    case 256: return packed ? stream_nch<256, true>(a, st) : stream_nch<256, false>(a, st);
-    default: return hipErrorInvalidValue;
-  }
-}
-
-hipError_t launch_fused(const FusedArgs& a, int dtype_bf16, int hd, int packed, int wide, hipStream_t st) {
-  if (wide) {
-    if (!dtype_bf16) return hipErrorInvalidValue;
+  return with_layout(layout, [&](auto lc) -> hipError_t {
+    constexpr int L = decltype(lc)::value;
     switch (hd) {
-      case 128: return packed ? fused_wide_t<128, true>(a, st) : fused_wide_t<128, false>(a, st);
-      case 256: return packed ? fused_wide_t<256, true>(a, st) : fused_wide_t<256, false>(a, st);
+      case 64: return stream_nch<64, L>(a, st);
+      case 128: return stream_nch<128, L>(a, st);
+      case 256: return stream_nch<256, L>(a, st);
       default: return hipErrorInvalidValue;
     }
+  });
+}
+
+hipError_t launch_fused(const FusedArgs& a, int dtype_bf16, int hd, int layout, int wide, hipStream_t st) {
+  if (wide) {
+    if (!dtype_bf16) return hipErrorInvalidValue;
+    return with_layout(layout, [&](auto lc) -> hipError_t {
+      constexpr int L = decltype(lc)::value;
+      switch (hd) {
+        case 128: return fused_wide_t<128, L>(a, st);
+        case 256: return fused_wide_t<256, L>(a, st);
+        default: return hipErrorInvalidValue;
+      }
+    });
   }
   hipError_t e;
-#define FB(H) (packed ? fused_t<uint16_t, H, true>(a, st) : fused_t<uint16_t, H, false>(a, st))
-#define FF(H) fused_t<float, H, false>(a, st)
+#define FB(H) with_layout(layout, [&](auto lc) { return fused_t<uint16_t, H, decltype(lc)::value>(a, st); })
+#define FF(H) fused_t<float, H, 0>(a, st)
   e = [&]() -> hipError_t { KVD_DISPATCH(dtype_bf16, hd, FB, FF) }();
 #undef FB
 #undef FF

@@ -144,14 +144,17 @@ hipError_t noalloc_scratch(void** out);
 hipError_t launch_copy_rows(const void* src, size_t src_stride, void* dst, size_t dst_stride, size_t row_bytes, int B,
                             hipStream_t st);
 
-hipError_t launch_proj(const ProjArgs& a, int dtype_bf16, int hd, int packed, int n_units, hipStream_t st);
+// layout: the kvd_weight_layout of the weights (0 row-major, 1 packed, 2 packed
+// with gamma folded in; 1 and 2 are bf16 only).
+hipError_t launch_proj(const ProjArgs& a, int dtype_bf16, int hd, int layout, int n_units, hipStream_t st);
 // Current-token projection (T == 1): the streaming kernel for bf16, proj_kernel for fp32.
-hipError_t launch_project_current(const ProjArgs& a, int dtype_bf16, int hd, int packed, int n_units,
+hipError_t launch_project_current(const ProjArgs& a, int dtype_bf16, int hd, int layout, int n_units,
                                   hipStream_t st);
 // wide: the 128-token engine (fused_wide_kernel; bf16, head_dim 128 / 256, a.n_rec
 // counted in 128-token tiles, the tail never folded).
-hipError_t launch_fused(const FusedArgs& a, int dtype_bf16, int hd, int packed, int wide, hipStream_t st);
-hipError_t launch_pack(const void* w, void* out, int rows, int d, hipStream_t st);
+hipError_t launch_fused(const FusedArgs& a, int dtype_bf16, int hd, int layout, int wide, hipStream_t st);
+// gamma: nullptr, or [d] bf16 folded into the packed values (bf16(w * gamma)).
+hipError_t launch_pack(const void* w, const void* gamma, void* out, int rows, int d, hipStream_t st);
 hipError_t launch_decode(const AttnArgs& a, int dtype_bf16, int hd, hipStream_t st);
 hipError_t launch_combine(const float* ws_acc, const float* ws_ml, void* out, int n_q, int B, int S, int dtype_bf16,
                           int hd, hipStream_t st);

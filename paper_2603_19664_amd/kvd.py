@@ -22,7 +22,7 @@ HEADER_PATH = os.path.join(os.path.dirname(_PKG), "include", "kvd.h")
 
 KVD_OK, KVD_ERR_NULL, KVD_ERR_SHAPE, KVD_ERR_UNSUPPORTED, KVD_ERR_WORKSPACE, KVD_ERR_ALIGN, KVD_ERR_DEVICE = range(7)
 KVD_F32, KVD_BF16 = 0, 1
-KVD_W_ROWMAJOR, KVD_W_PACKED = 0, 1
+KVD_W_ROWMAJOR, KVD_W_PACKED, KVD_W_PACKED_GAMMA = 0, 1, 2
 KVD_OP_DECODE_ATTN, KVD_OP_CACHED_ATTN, KVD_OP_FUSED = 0, 1, 2
 
 _DTYPES = {KVD_F32: torch.float32, KVD_BF16: torch.bfloat16}
@@ -81,6 +81,8 @@ def _load() -> ctypes.CDLL:
     lib.kvd_store_residual.restype = ctypes.c_int
     lib.kvd_pack_weights.argtypes = [S, VP, I32, VP, VP]
     lib.kvd_pack_weights.restype = ctypes.c_int
+    lib.kvd_pack_weights_gamma.argtypes = [S, VP, VP, I32, VP, VP]
+    lib.kvd_pack_weights_gamma.restype = ctypes.c_int
     lib.kvd_pack_matrix.argtypes = [VP, I32, I32, VP, VP]
     lib.kvd_pack_matrix.restype = ctypes.c_int
     lib.kvd_block_forward.argtypes = [S, P(BlockWeights), VP, VP, VP, I32, I32, VP, SZ, VP]
@@ -153,6 +155,10 @@ class Shape:
         """The same shape with weights in the packed MFMA layout (kvd_pack_weights)."""
         return dataclasses.replace(self, w_layout=KVD_W_PACKED)
 
+    def packed_gamma(self) -> "Shape":
+        """The same shape with gamma folded into packed weights (kvd_pack_weights_gamma)."""
+        return dataclasses.replace(self, w_layout=KVD_W_PACKED_GAMMA)
+
 
 def shape_of(wl) -> Shape:
     """The Shape of a configs.Workload."""
@@ -208,11 +214,14 @@ def _kv_extent(k, v, name, B, shape: "Shape", min_rows: int, t_off: int, ring: b
 
 
 def _weights_extent(shape: "Shape", **mats):
-    """gamma [d]; w_q [n_q*hd, d]; w_k, w_v [n_kv*hd, d] (packed weights keep these extents)."""
+    """gamma [d]; w_q [n_q*hd, d]; w_k, w_v [n_kv*hd, d] (packed weights keep these extents).
+    With gamma folded into the weights (KVD_W_PACKED_GAMMA) gamma may be None."""
     d, hd = shape.d_model, shape.head_dim
     want = {"gamma": (d,), "w_q": (shape.n_q_heads * hd, d), "w_k": (shape.n_kv_heads * hd, d),
             "w_v": (shape.n_kv_heads * hd, d)}
     for name, t in mats.items():
+        if name == "gamma" and t is None and shape.w_layout == KVD_W_PACKED_GAMMA:
+            continue
         _extent(t, name, want[name])
 
 
@@ -357,6 +366,18 @@ def kvd_pack_weights(shape: Shape, w):
     out = torch.empty_like(w)
     _check(lib.kvd_pack_weights(ctypes.byref(shape.c()), _ptr(w, "w", torch.bfloat16, 2), w.shape[0],
                                 _ptr(out, "packed", torch.bfloat16, 2), _stream()))
+    return out
+
+
+def kvd_pack_weights_gamma(shape: Shape, w, gamma):
+    """A packed copy of W diag(gamma) (bf16(w * gamma) per element) for the KVD_W_PACKED_GAMMA layout."""
+    if not isinstance(w, torch.Tensor) or w.dim() != 2 or w.shape[1] != shape.d_model:
+        raise ValueError(f"w must be a [rows, d_model={shape.d_model}] tensor")
+    _extent(gamma, "gamma", (shape.d_model,))
+    out = torch.empty_like(w)
+    _check(lib.kvd_pack_weights_gamma(ctypes.byref(shape.c()), _ptr(w, "w", torch.bfloat16, 2),
+                                      _ptr(gamma, "gamma", torch.bfloat16, 1), w.shape[0],
+                                      _ptr(out, "packed", torch.bfloat16, 2), _stream()))
     return out
 
 

@@ -51,7 +51,8 @@ class Layer:
 
 def make_layer(wl, B, T, seed=0, layer=0, w_q_std=None, pos0=None, t_cap=None, packed=None, **over) -> Layer:
     """Seeded inputs of one layer.  bf16 weights go to the library in the packed MFMA
-    layout unless packed=False (the oracle always gets the row-major values)."""
+    layout unless packed=False; packed="gamma" folds gamma into them
+    (kvd_pack_weights_gamma).  The oracle always gets the row-major values and gamma."""
     if over:
         wl = dataclasses.replace(wl, **over)
     dev = "cuda"
@@ -62,7 +63,10 @@ def make_layer(wl, B, T, seed=0, layer=0, w_q_std=None, pos0=None, t_cap=None, p
     if packed is None:
         packed = shape.dtype == kvd.KVD_BF16
     lw = (w_q, w_k, w_v)
-    if packed:
+    if packed == "gamma":
+        shape = shape.packed_gamma()
+        lw = tuple(kvd.kvd_pack_weights_gamma(shape, w, gamma) for w in lw)
+    elif packed:
         shape = shape.packed()
         lw = tuple(kvd.kvd_pack_weights(shape, w) for w in lw)
     return Layer(wl, shape, B, T, h, h_new, gamma, w_q, w_k, w_v, p0.to(dev), (p0 + T).to(torch.int32).to(dev),

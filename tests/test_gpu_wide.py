@@ -1,5 +1,5 @@
 """GPU parity of the wide fused engine (128 recomputed tokens per workgroup,
-4 waves, bf16, head_dim 128 / 256): forced with kvd_set_fused_tokens(128) on
+8 waves, bf16, head_dim 128 / 256): forced with kvd_set_fused_tokens(128) on
 small shapes that span several tiles and a ragged one, and reached by the
 automatic policy on a shape with a full round of wide tiles.
 
