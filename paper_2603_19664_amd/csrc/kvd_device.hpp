@@ -21,6 +21,7 @@
 // sum-of-squares order and the same epilogue, which is what makes their K/V
 // bit-identical (Prop. reconstruction: identical operation order).
 #pragma once
+#include <utility>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -507,12 +508,13 @@ struct MfmaTile {
 
 // ------------------------------------------------------------------ bf16 MFMA tile, 128 tokens
 
-// 8 waves (512 threads, two per SIMD) compute a [2*HD features] x [128 tokens]
-// tile, head_dim 128 or 256.  Wave w owns 32 feature rows for all 128 tokens
-// per 32-row block it holds: at head_dim 256 K rows and the same V rows
+// 8 waves (512 threads, two per SIMD) compute a [2*HD features] x [MT tokens]
+// tile (MT = 128, or 64 for grids too small for 128-token tiles), head_dim 128
+// or 256.  Wave w owns 32 feature rows for all MT tokens per 32-row block it
+// holds: at head_dim 256 K rows and the same V rows
 // [32 w, 32 w + 32) (two blocks, RoPE work balanced), at head_dim 128 one block
-// of K (waves 0-3) or V (waves 4-7).  Each weight (A) fragment feeds four
-// MFMAs (one per 32-token block).  A CU reads the tile's weights once per 128
+// of K (waves 0-3) or V (waves 4-7).  Each weight (A) fragment feeds one MFMA
+// per 32-token block.  With MT = 128 a CU reads the tile's weights once per 128
 // tokens instead of once per 64 (half the weight bytes per flop of MfmaTile),
 // and the two waves of a SIMD cover each other's staging arithmetic, fragment
 // reads and barrier waits.  The per-element arithmetic is MfmaTile's: the same
@@ -526,18 +528,18 @@ struct MfmaTile {
 // per step, after the second substep.  Loads go through
 // buffer resources (wave-uniform base and extent in SGPRs, a 32-bit offset per
 // lane), which keeps the addresses out of the vector registers.
-template <int HD, bool PACKED, bool FOLD = false>
+template <int HD, int MT, bool PACKED, bool FOLD = false>
 struct WideTile {
   static constexpr int NT = kNtWide;
-  static constexpr int MT = kMtWide;
   static constexpr int NB_F = HD / 128;   // 32-row blocks per wave
   static constexpr int NB_T = MT / 32;    // 32-token blocks (all of them)
   static constexpr int CPT = MT * 8 / NT;  // staged 8-element chunks per thread per K-step
   static constexpr int KLD = kv_ld<uint16_t>(HD);
   static constexpr int DW = 2, DH = 2, DL = kDepth;
   static constexpr int SLOT = NB_T * 4 * 512;  // elements per LDS slot (one K-step)
+  static constexpr int NU = 4 * NB_T;          // units (substep, token block) per K-step
   static_assert(HD == 128 || HD == 256, "wide tile: head_dim 128 or 256");
-  static_assert(DL == 4 && CPT == 2 && NT == 512, "ring and staging shape");
+  static_assert((MT == 64 || MT == 128) && DL == 4 && CPT == MT / 64 && NT == 512, "ring and staging shape");
 
   static __device__ __forceinline__ void block_rows(int w, int bf, int& half, int& row0) {
     if (NB_F == 2) {
@@ -549,7 +551,7 @@ struct WideTile {
     }
   }
 
-  // As MfmaTile::run, for the n <= 128 residual rows that start at h_tile
+  // As MfmaTile::run, for the n <= MT residual rows that start at h_tile
   // ([n][d], row stride d); the K/V tile goes to `kv`.
   template <class Setup>
   static __device__ __forceinline__ void run(const uint16_t* h_tile, int n, const uint16_t* gam, const uint16_t* gam_g,
@@ -692,13 +694,14 @@ struct WideTile {
       return *reinterpret_cast<const bf16x8_t*>(hst + (size_t)lslot * SLOT + (bt * 4 + u) * 512 + 8 * bslot(lane, u));
     };
 
-    // A step is 16 units k = 4 u + bt (substep u, token block bt), each one B
+    // A step is NU units k = NB_T u + bt (substep u, token block bt), each one B
     // fragment and the NB_F MFMAs that use it.  B fragments stream through a
     // ring of RA + 1 registers, read RA units ahead: the reads of the next
-    // step's first units come after the barrier that makes its staging visible.
+    // step's first units come after the barrier (after unit NU / 2 - 1) that
+    // makes its staging visible.
     constexpr int RA = 3;
     constexpr int NBQ = RA + 1;
-    static_assert(16 % NBQ == 0, "unit k of every step uses ring entry k % NBQ");
+    static_assert(NU % NBQ == 0 && RA < NU / 2, "unit k of every step uses ring entry k % NBQ");
     bf16x8_t bq[NBQ];
     // iteration s, L = s % 4: weight slot s % 2 (refilled with step s + 2), the
     // residual registers (staged as step s + 1, then refilled with step s + 2),
@@ -706,7 +709,7 @@ struct WideTile {
     // whose step indexes are clamped into range.  Units keep their order (a
     // scheduling fence after each lets only VALU, SALU, DS writes and
     // transcendentals cross), so every ring register is reloaded only after its
-    // last use, and the staging arithmetic spreads over the first eight units.
+    // last use, and the staging arithmetic spreads over the first half.
     auto iter = [&](auto lc, int s, auto guard_c) {
       constexpr int L = decltype(lc)::value;
       constexpr int LW = L & 1;
@@ -716,36 +719,36 @@ struct WideTile {
       const int sh = GUARD ? min(s + 2, nsteps - 1) : s + 2;
       auto unit = [&](auto kc) {
         constexpr int k = decltype(kc)::value;
-        constexpr int u = k / 4, bt = k % 4, kk = k + RA;
-        if constexpr (kk < 16) bq[kk % NBQ] = rd1(L, kk / 4, kk % 4);
-        else bq[kk % NBQ] = rd1(LN, (kk - 16) / 4, (kk - 16) % 4);
+        constexpr int u = k / NB_T, bt = k % NB_T, kk = k + RA;
+        if constexpr (kk < NU) bq[kk % NBQ] = rd1(L, kk / NB_T, kk % NB_T);
+        else bq[kk % NBQ] = rd1(LN, (kk - NU) / NB_T, (kk - NU) % NB_T);
 #pragma unroll
         for (int bf = 0; bf < NB_F; ++bf)
           acc[bf][bt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(A[LW][bf][u], bq[k % NBQ], acc[bf][bt], 0, 0, 0);
         if constexpr (bt == NB_T - 1) load_wu(LW, sw, u);
-        if constexpr (k == 3) load_h(0, sh);
+        if constexpr (k == NB_T - 1) load_h(0, sh);
         if (!GUARD) {
           __builtin_amdgcn_sched_group_barrier(0x100, k == 0 ? 2 : 1, 0);  // DS read: B fragment (gamma)
 #pragma unroll
           for (int bf = 0; bf < NB_F; ++bf) {
             __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);            // MFMA
-            if constexpr (k < 7) __builtin_amdgcn_sched_group_barrier(0x002, 5, 0);  // VALU: staging
+            if constexpr (k < NU / 2 - 1) __builtin_amdgcn_sched_group_barrier(0x002, 5, 0);  // VALU: staging
           }
-          if constexpr (k == 6) __builtin_amdgcn_sched_group_barrier(0x200, CPT, 0);  // DS write: staged chunks
+          if constexpr (k == NU / 2 - 2) __builtin_amdgcn_sched_group_barrier(0x200, CPT, 0);  // DS write: staged chunks
         }
         __builtin_amdgcn_sched_barrier(0x0606);
       };
       __builtin_amdgcn_sched_barrier(0);
       if (!GUARD || s + 1 < nsteps)
         put_hv(LN, 0, FOLD ? uint4{} : *reinterpret_cast<const uint4*>(gam + (size_t)(s + 1) * kKT + 8 * sub));
-      unit(IC<0>{}); unit(IC<1>{}); unit(IC<2>{}); unit(IC<3>{});
-      unit(IC<4>{}); unit(IC<5>{}); unit(IC<6>{}); unit(IC<7>{});
+      [&]<int... K>(std::integer_sequence<int, K...>) { (unit(IC<K>{}), ...); }(std::make_integer_sequence<int, NU / 2>{});
       __builtin_amdgcn_sched_barrier(0);
       __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): this wave's staged chunks are in LDS
       __builtin_amdgcn_s_barrier();
       __builtin_amdgcn_sched_barrier(0);
-      unit(IC<8>{}); unit(IC<9>{}); unit(IC<10>{}); unit(IC<11>{});
-      unit(IC<12>{}); unit(IC<13>{}); unit(IC<14>{}); unit(IC<15>{});
+      [&]<int... K>(std::integer_sequence<int, K...>) {
+        (unit(IC<K + NU / 2>{}), ...);
+      }(std::make_integer_sequence<int, NU / 2>{});
     };
 
     // prologue: residual step 0 and weight steps 0, 1 in flight, the caller's
@@ -764,7 +767,7 @@ struct WideTile {
     load_h(0, min(1, nsteps - 1));
     __syncthreads();
 #pragma unroll
-    for (int k = 0; k < RA; ++k) bq[k] = rd1(0, k / 4, k % 4);
+    for (int k = 0; k < RA; ++k) bq[k] = rd1(0, k / NB_T, k % NB_T);
     int s0 = 0;
     // steady state: every step index of iterations s0 .. s0 + 3 is below nsteps
     for (; s0 + 8 <= nsteps; s0 += 4) {

@@ -474,10 +474,10 @@ __device__ __forceinline__ void fused_body(const FusedArgs& a, int per_xcd, int 
     const size_t hd_d = (size_t)HD * a.d;
     const Half halves[2] = {Half{static_cast<const T*>(a.w_k) + j * hd_d, 1},
                             Half{static_cast<const T*>(a.w_v) + j * hd_d, 0}};
-    if constexpr (WIDE) {
-      WideTile<HD, PACKED, FOLD>::run(static_cast<const uint16_t*>(a.h) + ((size_t)b * a.h_ld + t0) * a.d, n, gam,
-                                static_cast<const uint16_t*>(a.gamma), a.d, a.eps, halves, hst, rinv, pos, rev, kv,
-                                setup);
+    if constexpr (sizeof(T) == 2 && HD >= 128) {
+      WideTile<HD, MT, PACKED, FOLD>::run(static_cast<const uint16_t*>(a.h) + ((size_t)b * a.h_ld + t0) * a.d, n, gam,
+                                          static_cast<const uint16_t*>(a.gamma), a.d, a.eps, halves, hst, rinv, pos,
+                                          rev, kv, setup);
     } else if constexpr (sizeof(T) == 2) {
       MfmaTile<HD, MT, PACKED, FOLD>::run(hrow, valid, gam, static_cast<const uint16_t*>(a.gamma), a.d, a.eps, halves,
                                           hst, rinv, pos, rev, kv, setup);
