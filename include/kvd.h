@@ -60,7 +60,7 @@
 extern "C" {
 #endif
 
-#define KVD_ABI_VERSION 7
+#define KVD_ABI_VERSION 8
 
 typedef enum {
   KVD_OK = 0,
@@ -207,16 +207,25 @@ kvd_status kvd_cached_attn(const kvd_attn_shape* shape, const void* q, const kvd
  *   ws: kvd_workspace_bytes(shape, KVD_OP_FUSED, B, T_rec, T_tail) bytes.
  *   kv_debug: NULL in production.  If not NULL, the recomputed K/V are also
  *   written to it at rows kv_debug->t_off .. +T_rec-1 (for bit-identity checks).
- * Split-K as in kvd_decode_attn, one split per recomputed tile: 64 tokens, or
- * 128 on the wide bf16 engine (head_dim 128 / 256), which a call gets when it
- * has at least 256 such tiles (B * n_kv_heads * ceil(T_rec / 128) >= 256; see
- * kvd_set_fused_tokens).  On 64-token tiles with bf16, T_rec >= 1 and
- * T_tail <= 4 (a decode step's current token) the tail joins the last tile's
- * split: its rows are copied into LDS while that tile is recomputed.
- * Otherwise the tail adds one split per 64-row tile, each attended by a
- * workgroup of its own (the hybrid cache budget: recent tokens stored, older
- * ones recomputed).  kvd_num_splits gives the count; kvd_workspace_bytes
- * covers either tiling.
+ * Split-K as in kvd_decode_attn, one split per recomputed tile, on one of
+ * three engines (see kvd_set_fused_tokens):
+ *   - wide (bf16, head_dim 128 / 256): 128-token tiles of K and V rows, when
+ *     the call has at least 256 of them (B * n_kv_heads * ceil(T_rec / 128)
+ *     >= 256: a full round of the chip);
+ *   - split (bf16, head_dim 128 / 256, T_rec >= 1, T_tail <= 4, at most 256
+ *     chunks per sequence), only when asked for with KVD_FUSED_SPLIT:
+ *     each 128-token chunk runs as two workgroups, one recomputing its K rows
+ *     and taking the scores and softmax, one recomputing its V rows and, once
+ *     the first has published the probabilities through the workspace, the
+ *     P V products.  The second waits for the first with a bounded wait
+ *     (about 0.1 s); past it that split's partial is NaN, so out shows it;
+ *   - 64-token tiles of K and V rows otherwise.
+ * With bf16, T_rec >= 1 and T_tail <= 4 (a decode step's current token) the
+ * tail joins the last tile's split on the split and 64-token engines: its
+ * rows are copied into LDS while that tile is recomputed.  Otherwise the tail
+ * adds one split per 64-row tile, each attended by a workgroup of its own (the
+ * hybrid cache budget: recent tokens stored, older ones recomputed).
+ * kvd_num_splits gives the count; kvd_workspace_bytes covers every engine.
  * The workspace's split counters follow kvd_decode_attn's contract.
  * out == NULL writes only the split-K partials (see kvd_combine).
  * Supports both dtypes.                                                       */
@@ -385,11 +394,14 @@ int32_t kvd_set_attn_workgroups(int32_t target);
 /* Tuning of kvd_fused_recompute_attn and kvd_fused_window_attn: the recomputed
  * tokens per workgroup.  0 (the default) chooses per call, 128 asks for the
  * wide engine wherever it exists (bf16, head_dim 128 / 256, its LDS within
- * the limit; elsewhere 64 is used), 64 for the 64-token tiles; other values
- * mean 0.  Returns the previous setting.  Process-wide: it changes
- * kvd_num_splits of KVD_OP_FUSED (not kvd_workspace_bytes, which covers both
- * tilings).  Both tilings give K/V bit-identical to kvd_recompute_kv; the
- * attention output differs by rounding only (other split boundaries).       */
+ * the limit; elsewhere 64 is used), KVD_FUSED_SPLIT for the split engine
+ * wherever a call can run on it (elsewhere 64), 64 for the 64-token tiles;
+ * other values mean 0.  Returns the previous setting.  Process-wide: it
+ * changes kvd_num_splits of KVD_OP_FUSED (not kvd_workspace_bytes, which
+ * covers every engine).  All engines give K/V bit-identical to
+ * kvd_recompute_kv; the attention output differs by rounding only (other
+ * split boundaries).                                                         */
+#define KVD_FUSED_SPLIT (-128)
 int32_t kvd_set_fused_tokens(int32_t tokens);
 
 const char* kvd_status_str(kvd_status status);

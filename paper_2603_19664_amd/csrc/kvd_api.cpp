@@ -116,11 +116,12 @@ kvd::SaSplit stream_split(const kvd_attn_shape* s, int32_t B, int32_t T) {
 // Token tile of the fused call (kvd_set_fused_tokens): 0 = chosen per call.
 std::atomic<int32_t> g_fused_tokens{0};
 
-// The fused call's tiling: mt recomputed tokens per workgroup (kMtBf16 /
-// kMtF32, or kMtWide on the wide engine), n_rec recomputed tiles, n_tail
-// stored-tail tiles, S = n_rec + n_tail splits.
+// The fused call's tiling: the engine (kvd::kFusedTile64 / kFusedWide /
+// kFusedSplit), mt recomputed tokens per tile (kMtBf16 / kMtF32, kMtWide or
+// kMtSplit), n_rec recomputed tiles, n_tail stored-tail tiles, S = n_rec +
+// n_tail splits.
 struct FusedPlan {
-  int32_t mt, n_rec, n_tail, S;
+  int32_t engine, mt, n_rec, n_tail, S;
 };
 
 // The wide engine exists for bf16 at head_dim 128 / 256 where its LDS fits.
@@ -132,6 +133,7 @@ bool wide_supported(const kvd_attn_shape* s) {
 
 FusedPlan narrow_plan(const kvd_attn_shape* s, int32_t T_rec, int32_t T_tail) {
   FusedPlan p{};
+  p.engine = kvd::kFusedTile64;
   p.mt = kvd::kMtBf16;
   p.n_rec = ceil_div(T_rec, p.mt);
   p.n_tail = s->dtype == KVD_BF16 ? kvd::fused_tail_tiles<uint16_t>(p.n_rec, T_tail)
@@ -142,6 +144,7 @@ FusedPlan narrow_plan(const kvd_attn_shape* s, int32_t T_rec, int32_t T_tail) {
 
 FusedPlan wide_plan(int32_t T_rec, int32_t T_tail) {
   FusedPlan p{};
+  p.engine = kvd::kFusedWide;
   p.mt = kvd::kMtWide;
   p.n_rec = ceil_div(T_rec, p.mt);
   p.n_tail = ceil_div(T_tail, kvd::kTile);
@@ -149,14 +152,43 @@ FusedPlan wide_plan(int32_t T_rec, int32_t T_tail) {
   return p;
 }
 
+// The split engine: bf16 at head_dim 128 / 256, recomputed rows, a tail that
+// folds (at most fold_rows rows), at most kSplitMaxChunks chunks per sequence,
+// and its LDS within the limit.
+bool split_supported(const kvd_attn_shape* s, int32_t T_rec, int32_t T_tail) {
+  if (s->dtype != KVD_BF16 || (s->head_dim != 128 && s->head_dim != 256)) return false;
+  if (T_rec < 1 || T_tail > kvd::fold_rows<uint16_t>() || ceil_div(T_rec, kvd::kMtSplit) > kvd::kSplitMaxChunks)
+    return false;
+  return kvd::fused_split_lds_bytes(s->n_q_heads / s->n_kv_heads, s->head_dim) +
+             kvd::gamma_lds_bytes(s->d_model) <= kvd::kLdsPerGroup;
+}
+
+FusedPlan split_plan(int32_t T_rec) {
+  FusedPlan p{};
+  p.engine = kvd::kFusedSplit;
+  p.mt = kvd::kMtSplit;
+  p.n_rec = ceil_div(T_rec, p.mt);
+  p.n_tail = 0;
+  p.S = p.n_rec;
+  return p;
+}
+
 // Wide tiles when supported and the call has at least kWideMinTiles of them (a
-// full round of the chip), or when forced by kvd_set_fused_tokens(128).
+// full round of the chip), else 64-token tiles.  The split engine runs only
+// when asked for: on MI355X, in a 34-layer decode step (Gemma-3-4B shape, B = 1,
+// 4096 keys; B = 2, 2048 keys) its launches took 58-61 us against 56-57 us on
+// 64-token tiles (its K-loop is no faster, and the K-to-V exchange adds a
+// round trip).  kvd_set_fused_tokens forces an engine (where it exists).
 FusedPlan fused_plan(const kvd_attn_shape* s, int32_t B, int32_t T_rec, int32_t T_tail) {
   const int32_t mode = g_fused_tokens.load(std::memory_order_relaxed);
-  bool wide = T_rec > 0 && mode != kvd::kMtBf16 && wide_supported(s);
-  if (wide && mode == 0)
-    wide = (int64_t)B * s->n_kv_heads * ceil_div(T_rec, kvd::kMtWide) >= kvd::kWideMinTiles;
-  return wide ? wide_plan(T_rec, T_tail) : narrow_plan(s, T_rec, T_tail);
+  const bool wide_ok = T_rec > 0 && wide_supported(s);
+  if (mode == kvd::kMtBf16) return narrow_plan(s, T_rec, T_tail);
+  if (mode == kvd::kMtWide) return wide_ok ? wide_plan(T_rec, T_tail) : narrow_plan(s, T_rec, T_tail);
+  if (mode == KVD_FUSED_SPLIT)
+    return split_supported(s, T_rec, T_tail) ? split_plan(T_rec) : narrow_plan(s, T_rec, T_tail);
+  if (wide_ok && (int64_t)B * s->n_kv_heads * ceil_div(T_rec, kvd::kMtWide) >= kvd::kWideMinTiles)
+    return wide_plan(T_rec, T_tail);
+  return narrow_plan(s, T_rec, T_tail);
 }
 
 int32_t splits(const kvd_attn_shape* s, int32_t op, int32_t B, int32_t T_main, int32_t T_tail) {
@@ -170,15 +202,27 @@ size_t ws_acc_bytes(const kvd_attn_shape* s, int32_t B, int32_t S) {
 size_t ws_ml_bytes(const kvd_attn_shape* s, int32_t B, int32_t S) {
   return kvd::align_up((size_t)B * s->n_q_heads * S * 2 * sizeof(float), 256);
 }
-size_t ws_done_bytes(const kvd_attn_shape* s, int32_t B) {
+size_t ws_ctr_bytes(const kvd_attn_shape* s, int32_t B) {
   return kvd::align_up((size_t)B * s->n_kv_heads * sizeof(uint64_t), 256);
 }
-// Workspace: split counters [B][n_kv] uint64 first (zero between calls; their
+size_t ws_done_bytes(const kvd_attn_shape* s, int32_t B) {
+  return ws_ctr_bytes(s, B) + kvd::align_up((size_t)B * s->n_kv_heads * kvd::kSplitBitWords * sizeof(uint64_t), 256);
+}
+// Workspace: split counters [B][n_kv] uint64 first, then the split engine's
+// completion words [B][n_kv][kSplitBitWords] (both zero between calls; their
 // place depends on B only, so calls with any key count can share one
 // workspace), then partial accumulators [B][n_q][S][hd] fp32 and partial
-// (max, sum) [B][n_q][S][2] fp32.
+// (max, sum) [B][n_q][S][2] fp32, then (split engine) the chunks' exchange
+// records [B][n_kv][n_rec][xf] fp32.
 size_t ws_total(const kvd_attn_shape* s, int32_t B, int32_t S) {
   return ws_done_bytes(s, B) + ws_acc_bytes(s, B, S) + ws_ml_bytes(s, B, S);
+}
+size_t ws_xch_bytes(const kvd_attn_shape* s, int32_t B, int32_t n_rec) {
+  return kvd::align_up((size_t)B * s->n_kv_heads * n_rec * kvd::split_xf(s->n_q_heads / s->n_kv_heads) * sizeof(float),
+                       256);
+}
+size_t ws_plan_bytes(const kvd_attn_shape* s, int32_t B, const FusedPlan& p) {
+  return ws_total(s, B, p.S) + (p.engine == kvd::kFusedSplit ? ws_xch_bytes(s, B, p.n_rec) : 0);
 }
 float* ws_acc_ptr(const kvd_attn_shape* s, int32_t B, void* ws) {
   return reinterpret_cast<float*>(static_cast<char*>(ws) + ws_done_bytes(s, B));
@@ -188,8 +232,8 @@ float* ws_ml_ptr(const kvd_attn_shape* s, int32_t B, int32_t S, void* ws) {
 }
 unsigned long long* ws_done_ptr(void* ws) { return static_cast<unsigned long long*>(ws); }
 
-kvd_status check_ws(const kvd_attn_shape* s, int32_t B, int32_t S, void* ws, size_t ws_bytes) {
-  const size_t need = ws_total(s, B, S);
+kvd_status check_ws(const kvd_attn_shape* s, int32_t B, int32_t S, void* ws, size_t ws_bytes, size_t extra = 0) {
+  const size_t need = ws_total(s, B, S) + extra;
   if (ws == nullptr) return fail(KVD_ERR_WORKSPACE, "workspace is NULL (%zu bytes needed)", need);
   if ((reinterpret_cast<uintptr_t>(ws) & 255u) != 0) return fail(KVD_ERR_ALIGN, "workspace is not 256-byte aligned");
   if (ws_bytes < need) return fail(KVD_ERR_WORKSPACE, "workspace holds %zu bytes, %zu needed", ws_bytes, need);
@@ -230,7 +274,9 @@ size_t recompute_lds(const kvd_attn_shape* s) {
                           : (hd == 64 ? kvd::proj_lds<float>(64, kvd::kMtF32).end
                                       : hd == 128 ? kvd::proj_lds<float>(128, kvd::kMtF32).end
                                                   : kvd::proj_lds<float>(256, kvd::kMtF32).end);
-  return base + kvd::gamma_lds_bytes(s->d_model);
+  // bf16 head_dim 128 / 256 may also run on the split engine
+  const size_t split = s->dtype == KVD_BF16 && (hd == 128 || hd == 256) ? kvd::split_lds(hd, kvd::kMtSplit).end : 0;
+  return std::max(base, split) + kvd::gamma_lds_bytes(s->d_model);
 }
 
 kvd_status device_status(hipError_t e, const char* what) {
@@ -445,7 +491,8 @@ kvd_status fused_launch(const kvd_attn_shape* shape, const void* q, const void* 
   if ((int64_t)shape->n_kv_heads * B * S > INT32_MAX - 8)
     return fail(KVD_ERR_SHAPE, "%s: n_kv_heads * B * splits = %lld workgroups is too many", name,
                 (long long)shape->n_kv_heads * B * S);
-  KVD_TRY(check_ws(shape, B, S, ws, ws_bytes));
+  const bool split = plan.engine == kvd::kFusedSplit;
+  KVD_TRY(check_ws(shape, B, S, ws, ws_bytes, split ? ws_xch_bytes(shape, B, plan.n_rec) : 0));
   kvd::FusedArgs a{};
   a.q = q;
   a.h = h;
@@ -470,6 +517,11 @@ kvd_status fused_launch(const kvd_attn_shape* shape, const void* q, const void* 
   a.ws_acc = ws_acc_ptr(shape, B, ws);
   a.ws_ml = ws_ml_ptr(shape, B, S, ws);
   a.ws_done = ws_done_ptr(ws);
+  if (split) {
+    a.ws_bits = reinterpret_cast<unsigned long long*>(static_cast<char*>(ws) + ws_ctr_bytes(shape, B));
+    a.xch = reinterpret_cast<float*>(static_cast<char*>(ws) + ws_total(shape, B, S));
+    a.xf = kvd::split_xf(shape->n_q_heads / shape->n_kv_heads);
+  }
   a.out = out;
   a.d = shape->d_model;
   a.n_q = shape->n_q_heads;
@@ -481,7 +533,7 @@ kvd_status fused_launch(const kvd_attn_shape* shape, const void* q, const void* 
   a.eps = shape->rms_eps;
   fill_rev(shape, a.rev);
   return device_status(kvd::launch_fused(a, shape->dtype == KVD_BF16, shape->head_dim,
-                                         shape->w_layout, plan.mt == kvd::kMtWide,
+                                         shape->w_layout, plan.engine,
                                          (hipStream_t)stream),
                        name);
 }
@@ -510,8 +562,7 @@ kvd_status kvd_fused_recompute_attn_noalloc(const kvd_attn_shape* shape, const v
   if (B == 0) return KVD_OK;
   if (out == nullptr) return fail(KVD_ERR_NULL, "out is NULL (the no-allocation call always merges its splits)");
   if (T_rec > 0 && pos0 == nullptr) return fail(KVD_ERR_NULL, "pos0 is NULL");
-  const int32_t S = splits(shape, KVD_OP_FUSED, B, T_rec, T_tail);
-  const size_t need = ws_total(shape, B, S);
+  const size_t need = ws_plan_bytes(shape, B, fused_plan(shape, B, T_rec, T_tail));
   if (need > kvd::kNoAllocScratchBytes)
     return fail(KVD_ERR_WORKSPACE,
                 "kvd_fused_recompute_attn_noalloc: B=%d T_rec=%d T_tail=%d needs %zu bytes of scratch, more than the "
@@ -519,9 +570,10 @@ kvd_status kvd_fused_recompute_attn_noalloc(const kvd_attn_shape* shape, const v
                 B, T_rec, T_tail, need, kvd::kNoAllocScratchBytes);
   void* ws = nullptr;
   KVD_TRY(device_status(kvd::noalloc_scratch(&ws), "kvd_fused_recompute_attn_noalloc scratch lookup"));
-  // the split counters [B][n_kv] start at zero: cleared by a fill kernel (a
-  // kernel node under graph capture, never a memset)
-  KVD_TRY(device_status(kvd::launch_fill_zero_u64(ws, B * shape->n_kv_heads, (hipStream_t)stream),
+  // the split counters and completion words start at zero: cleared by a fill
+  // kernel (a kernel node under graph capture, never a memset)
+  KVD_TRY(device_status(kvd::launch_fill_zero_u64(ws, (int)(ws_done_bytes(shape, B) / sizeof(uint64_t)),
+                                                  (hipStream_t)stream),
                         "kvd_fused_recompute_attn_noalloc counter clear"));
   return fused_launch(shape, q, h, h_ld, gamma, w_k, w_v, pos0, B, T_rec, tail, T_tail, out, ws,
                       kvd::kNoAllocScratchBytes, nullptr, stream, "kvd_fused_recompute_attn_noalloc launch");
@@ -831,7 +883,7 @@ int32_t kvd_set_attn_workgroups(int32_t target) {
 }
 
 int32_t kvd_set_fused_tokens(int32_t tokens) {
-  if (tokens != kvd::kMtBf16 && tokens != kvd::kMtWide) tokens = 0;
+  if (tokens != kvd::kMtBf16 && tokens != kvd::kMtWide && tokens != KVD_FUSED_SPLIT) tokens = 0;
   return g_fused_tokens.exchange(tokens, std::memory_order_relaxed);
 }
 
@@ -840,8 +892,12 @@ size_t kvd_workspace_bytes(const kvd_attn_shape* shape, int32_t op, int32_t B, i
   if (S == 0) return 0;
   // fused: enough for either tiling, so that the size grows with T_rec and
   // T_tail whichever tile each call gets
-  if (op == KVD_OP_FUSED)
-    S = std::max(narrow_plan(shape, T_main, T_tail).S, wide_supported(shape) ? wide_plan(T_main, T_tail).S : 0);
+  if (op == KVD_OP_FUSED) {
+    size_t n = ws_plan_bytes(shape, B, narrow_plan(shape, T_main, T_tail));
+    if (T_main > 0 && wide_supported(shape)) n = std::max(n, ws_plan_bytes(shape, B, wide_plan(T_main, T_tail)));
+    if (split_supported(shape, T_main, T_tail)) n = std::max(n, ws_plan_bytes(shape, B, split_plan(T_main)));
+    return n;
+  }
   return ws_total(shape, B, S);
 }
 

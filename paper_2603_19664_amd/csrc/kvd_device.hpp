@@ -521,6 +521,14 @@ struct MfmaTile {
 // MFMA chain over d in K order, the same staging, 1/rms and epilogue, so the
 // K/V it produces are bit-identical.
 //
+// Split layout (NTX = kNtSplit: 4 waves, one per SIMD): the tile is one half
+// only, the HD rows of halves[0] (a KV head's K rows or its V rows) for MT
+// tokens; wave w owns rows [32 NB_F w, 32 NB_F (w + 1)).  Per wave the work is
+// the 8-wave layout's (NB_F row blocks for all MT tokens), so a CU streams the
+// half's weights once per MT tokens: at MT = 128 half the weight bytes per flop
+// of a 64-token tile of both halves, over the same number of workgroups.  The
+// K/V tile then holds the half's HD columns only (row stride KLDX).
+//
 // K-loop: weights are loaded DW = 2 K-steps ahead into A-operand registers,
 // each substep's fragments refilled right after its MFMAs; residuals one step
 // ahead into registers, staged (gamma * h -> bf16, sum of squares) two steps
@@ -528,21 +536,36 @@ struct MfmaTile {
 // per step, after the second substep.  Loads go through
 // buffer resources (wave-uniform base and extent in SGPRs, a 32-bit offset per
 // lane), which keeps the addresses out of the vector registers.
-template <int HD, int MT, bool PACKED, bool FOLD = false>
+template <int HD, int MT, bool PACKED, bool FOLD = false, int NTX = kNtWide, int KLDX = kv_ld<uint16_t>(HD),
+          bool SPLITX = false>
 struct WideTile {
-  static constexpr int NT = kNtWide;
-  static constexpr int NB_F = HD / 128;   // 32-row blocks per wave
+  static constexpr int NT = NTX;
+  static constexpr int NW = NT / 64;
+  static constexpr bool SPLIT = SPLITX;   // one half per tile
+  static constexpr int NB_F = SPLIT ? HD / (32 * NW) : HD / 128;   // 32-row blocks per wave
   static constexpr int NB_T = MT / 32;    // 32-token blocks (all of them)
   static constexpr int CPT = MT * 8 / NT;  // staged 8-element chunks per thread per K-step
-  static constexpr int KLD = kv_ld<uint16_t>(HD);
-  static constexpr int DW = 2, DH = 2, DL = kDepth;
+  static constexpr int TPR = NT / 8;       // tokens staged per chunk index (one per 8 threads)
+  static constexpr int KLD = KLDX;
+  // weight K-steps in flight: a split wave of one 32-row block holds 4 (its
+  // A fragments are half the 8-wave layout's per step)
+  static constexpr int DW = SPLIT && NB_F == 1 ? 4 : 2;
+  static constexpr int DH = 2, DL = kDepth;
   static constexpr int SLOT = NB_T * 4 * 512;  // elements per LDS slot (one K-step)
   static constexpr int NU = 4 * NB_T;          // units (substep, token block) per K-step
+  // VALU instructions the schedule interleaves after each MFMA of the first
+  // half-step (the staging arithmetic of CPT chunks per thread)
+  static constexpr int VPM = SPLIT ? 5 * CPT / NB_F : 5;
   static_assert(HD == 128 || HD == 256, "wide tile: head_dim 128 or 256");
-  static_assert((MT == 64 || MT == 128) && DL == 4 && CPT == MT / 64 && NT == 512, "ring and staging shape");
+  static_assert((MT == 64 || MT == 128) && DL == 4 && CPT * NT == MT * 8 && (NT == 512 || NT == 256) &&
+                    TPR % 32 == 0 && CPT >= 1 && NB_F >= 1 && (!SPLIT || NB_F * 32 * NW == HD),
+                "ring and staging shape");
 
   static __device__ __forceinline__ void block_rows(int w, int bf, int& half, int& row0) {
-    if (NB_F == 2) {
+    if (SPLIT) {
+      half = 0;
+      row0 = 32 * (NB_F * w + bf);
+    } else if (NB_F == 2) {
       half = bf;
       row0 = 32 * w;
     } else {
@@ -638,7 +661,7 @@ struct WideTile {
         const_cast<uint16_t*>(h_tile), (short)0, (int)((uint32_t)n * (uint32_t)d * 2u), 0x00020000);
 #pragma unroll
     for (int r = 0; r < CPT; ++r) {
-      const int t = (tid >> 3) + 64 * r;
+      const int t = (tid >> 3) + TPR * r;
       valid[r] = t < n;
       hoff[r] = 2u * ((uint32_t)(valid[r] ? t : 0) * (uint32_t)d + 8u * sub);
     }
@@ -663,8 +686,8 @@ struct WideTile {
     float ss[CPT];
 #pragma unroll
     for (int r = 0; r < CPT; ++r) ss[r] = 0.0f;
-    // chunk r of this thread: token (tid >> 3) + 64 r = token block
-    // (tid >> 8) + 2 r, column (tid >> 3) % 32; elements 8 sub .. 8 sub + 7 of
+    // chunk r of this thread: token (tid >> 3) + TPR r = token block
+    // (tid >> 8) + (TPR / 32) r, column (tid >> 3) % 32; elements 8 sub .. 8 sub + 7 of
     // the K-step = substep sub / 2, lane half sub % 2 of the B fragment
     const int lofs = ((tid >> 8) * 4 + (sub >> 1)) * 512 + 8 * bslot(((tid >> 3) & 31) + 32 * (sub & 1), sub >> 1);
 
@@ -686,7 +709,7 @@ struct WideTile {
     auto put_hv = [&](int lslot, int hslot, const uint4& gv) {
 #pragma unroll
       for (int r = 0; r < CPT; ++r)
-        *reinterpret_cast<uint4*>(hst + (size_t)lslot * SLOT + r * 8 * 512 + lofs) =
+        *reinterpret_cast<uint4*>(hst + (size_t)lslot * SLOT + r * (TPR / 32) * 4 * 512 + lofs) =
             stage_chunk<FOLD>(H[hslot][r], gv, ss[r]);
     };
     // B fragment of K-step slot lslot, substep u, token block bt
@@ -712,10 +735,10 @@ struct WideTile {
     // last use, and the staging arithmetic spreads over the first half.
     auto iter = [&](auto lc, int s, auto guard_c) {
       constexpr int L = decltype(lc)::value;
-      constexpr int LW = L & 1;
+      constexpr int LW = L % DW;
       constexpr int LN = (L + 1) & 3;
       constexpr bool GUARD = decltype(guard_c)::value;
-      const int sw = GUARD ? min(s + 2, nsteps - 1) : s + 2;
+      const int sw = GUARD ? min(s + DW, nsteps - 1) : s + DW;
       const int sh = GUARD ? min(s + 2, nsteps - 1) : s + 2;
       auto unit = [&](auto kc) {
         constexpr int k = decltype(kc)::value;
@@ -732,7 +755,7 @@ struct WideTile {
 #pragma unroll
           for (int bf = 0; bf < NB_F; ++bf) {
             __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);            // MFMA
-            if constexpr (k < NU / 2 - 1) __builtin_amdgcn_sched_group_barrier(0x002, 5, 0);  // VALU: staging
+            if constexpr (k < NU / 2 - 1) __builtin_amdgcn_sched_group_barrier(0x002, VPM, 0);  // VALU: staging
           }
           if constexpr (k == NU / 2 - 2) __builtin_amdgcn_sched_group_barrier(0x200, CPT, 0);  // DS write: staged chunks
         }
@@ -1042,11 +1065,13 @@ __device__ __forceinline__ void prefetch_rows_lds(const T* K, const T* V, size_t
 
 // Moves n <= kMax K|V rows of the LDS tile from row `from` to row `to` (the
 // ranges may overlap): everything is read before anything is written.
-template <typename T, int HD, int NT, int kMax>
+// W / LD: elements per row and row stride (the K|V tile by default; one half's
+// W = HD, LD = split_ld(HD) on the split engine).
+template <typename T, int HD, int NT, int kMax, int W = 2 * HD, int LD = kv_ld<T>(HD)>
 __device__ __forceinline__ void move_rows(T* kv, int from, int to, int n) {
-  constexpr int KLD = kv_ld<T>(HD);
+  constexpr int KLD = LD;
   constexpr int CH = 16 / sizeof(T);
-  constexpr int CPR2 = 2 * HD / CH;  // 16-byte chunks of a K|V row
+  constexpr int CPR2 = W / CH;  // 16-byte chunks of a row
   static_assert(kMax * CPR2 <= NT, "one chunk per thread");
   const int r = threadIdx.x / CPR2, ch = threadIdx.x - r * CPR2;
   uint4 v{};
@@ -1072,20 +1097,24 @@ __device__ __forceinline__ void move_rows(T* kv, int from, int to, int n) {
 // For n <= 64 the second key slot adds exact zeros (max with -inf, sum with
 // 0), so KPL = 1 and KPL = 2 give bit-identical results.  rows >= n is the
 // stride of the probabilities in LDS.
-template <typename T, int HD, int NT, int KPL>
-__device__ __forceinline__ void attend_tile(const T* kv, int n, int rows, int g, char* lds, const AttnLds& L) {
-  constexpr int KLD = kv_ld<T>(HD);
+// attend_scores runs tasks 1 and 2 (K rows at kt, row stride LD), attend_pv
+// task 3 (V rows at vt); attend_tile is the two on one K|V tile.  The split
+// engine's K and V roles run one each on their halves, with the probabilities
+// and (max, sum) passed between them, and perform the same arithmetic.
+template <typename T, int HD, int NT, int KPL, int LD = kv_ld<T>(HD)>
+__device__ __forceinline__ void attend_scores(const T* kt, int n, int rows, int g, char* lds, const AttnLds& L) {
+  constexpr int KLD = LD;
   constexpr int NW = NT / 64;
   constexpr int P = HD / 64;  // 64-dim parts of a score
-  constexpr int E = HD / 64;  // output columns per lane
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = wave_id();
   const float* qs = reinterpret_cast<const float*>(lds + L.q);
   float* S = reinterpret_cast<float*>(lds + L.s);
   float* red = reinterpret_cast<float*>(lds + L.red);
   float* ml = reinterpret_cast<float*>(lds + L.ml);
+  const T* kv = kt;
 
-  static_assert(KPL == 1 || KPL == 2, "keys per lane");
+  static_assert(KPL >= 1 && KPL <= 3, "keys per lane");
   for (int kk = 0; kk < KPL && 64 * kk < n; ++kk) {  // key slot: keys 64 kk + lane
     for (int task = wave; task < g * P; task += NW) {
       const int h = task / P, p = task - h * P;
@@ -1150,7 +1179,18 @@ __device__ __forceinline__ void attend_tile(const T* kv, int n, int rows, int g,
     }
   }
   __syncthreads();
+}
 
+template <typename T, int HD, int NT, int LD = kv_ld<T>(HD)>
+__device__ __forceinline__ void attend_pv(const T* vt, int n, int rows, int g, char* lds, const AttnLds& L) {
+  constexpr int KLD = LD;
+  constexpr int NW = NT / 64;
+  constexpr int E = HD / 64;  // output columns per lane
+  const int lane = threadIdx.x & 63;
+  const int wave = wave_id();
+  const float* S = reinterpret_cast<const float*>(lds + L.s);
+  float* red = reinterpret_cast<float*>(lds + L.red);
+  const T* kv = vt;
   const int TS = attn_ts(g);
   for (int task = wave; task < g * TS; task += NW) {
     const int h = task % g, ts = task / g;
@@ -1163,7 +1203,7 @@ __device__ __forceinline__ void attend_tile(const T* kv, int n, int rows, int g,
 #pragma unroll
       for (int k = 0; k < 4; ++k) {
         pr[k] = S[h * rows + t + k * TS];
-        load_e<E>(kv + (size_t)(t + k * TS) * KLD + HD + E * lane, v[k]);
+        load_e<E>(kv + (size_t)(t + k * TS) * KLD + E * lane, v[k]);
       }
 #pragma unroll
       for (int k = 0; k < 4; ++k)
@@ -1173,7 +1213,7 @@ __device__ __forceinline__ void attend_tile(const T* kv, int n, int rows, int g,
     for (; t < n; t += TS) {
       const float pr = S[h * rows + t];
       float v[E];
-      load_e<E>(kv + (size_t)t * KLD + HD + E * lane, v);
+      load_e<E>(kv + (size_t)t * KLD + E * lane, v);
 #pragma unroll
       for (int e = 0; e < E; ++e) a[e] = fmaf(pr, v[e], a[e]);
     }
@@ -1182,6 +1222,12 @@ __device__ __forceinline__ void attend_tile(const T* kv, int n, int rows, int g,
     for (int e = 0; e < E; ++e) dst[e] = a[e];
   }
   __syncthreads();
+}
+
+template <typename T, int HD, int NT, int KPL>
+__device__ __forceinline__ void attend_tile(const T* kv, int n, int rows, int g, char* lds, const AttnLds& L) {
+  attend_scores<T, HD, NT, KPL>(kv, n, rows, g, lds, L);
+  attend_pv<T, HD, NT>(kv + HD, n, rows, g, lds, L);
 }
 
 // Device-scope (coherent across the XCDs' L2 caches) 32-bit store / load: the

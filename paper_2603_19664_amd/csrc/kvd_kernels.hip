@@ -125,6 +125,77 @@ __global__ __launch_bounds__(kNtTile, 1) void proj_kernel(ProjArgs a, int per_xc
   }
 }
 
+// ------------------------------------------------------------------ recompute / prefill, split engine
+
+// bf16, head_dim 128 / 256: one half of a unit (a KV head's K rows or its V
+// rows; query heads 2u and 2u + 1 for a q unit) for a tile of up to kMtSplit
+// tokens of one sequence, per workgroup of kNtSplit threads.  grid:
+// xcd_map(2 * n_units * B * tps) with tps = ceil(T / kMtSplit) tiles per
+// sequence; item = ((unit * B + b) * tps + tile) * 2 + half, so the two halves
+// of a tile are adjacent items on one XCD (its L2 serves the tile's residual
+// rows to both) and a unit's tiles stay on one XCD.  Per element the arithmetic
+// is the other engines' (the same MFMA chain over d, staging, 1/rms and
+// epilogue), so the K/V are bit-identical.
+template <int HD, bool PACKED, bool FOLD>
+__global__ __launch_bounds__(split_nt(HD), 1) void proj_split_kernel(ProjArgs a, int per_xcd, int tps, int n_units) {
+  extern __shared__ __align__(16) char lds[];
+  constexpr int NT = split_nt(HD), MT = kMtSplit;
+  constexpr ProjLds PL = split_lds(HD, MT);
+  constexpr int KLD = split_ld(HD);
+  const int tid = threadIdx.x;
+  const unsigned item = (blockIdx.x % kXcds) * (unsigned)per_xcd + blockIdx.x / kXcds;
+  const unsigned n_tiles = (unsigned)a.B * (unsigned)tps;
+  if (item >= 2u * (unsigned)n_units * n_tiles) return;
+  const int half = (int)(item & 1u);
+  const unsigned ut = item >> 1;
+  const int unit = (int)(ut / n_tiles);
+  const unsigned rem = ut - (unsigned)unit * n_tiles;
+  const int b = (int)(rem / (unsigned)tps);
+  const int t0 = (int)(rem - (unsigned)b * (unsigned)tps) * MT;
+  const int n = min(MT, a.T - t0);
+  const size_t hd_d = (size_t)HD * a.d;
+  const bool kv_mode = unit < a.n_kv_units;
+  const int head = kv_mode ? unit : 2 * (unit - a.n_kv_units) + half;
+  if (!kv_mode && head >= a.n_q) return;
+  const uint16_t* w = kv_mode ? static_cast<const uint16_t*>(half ? a.w_v : a.w_k) + head * hd_d
+                              : static_cast<const uint16_t*>(a.w_q) + head * hd_d;
+  const Half halves[2] = {Half{w, kv_mode ? 1 - half : 1}, Half{nullptr, 0}};
+
+  double* rev = reinterpret_cast<double*>(lds + PL.rev);
+  float* rinv = reinterpret_cast<float*>(lds + PL.rinv);
+  int* pos = reinterpret_cast<int*>(lds + PL.pos);
+  uint16_t* hst = reinterpret_cast<uint16_t*>(lds + PL.hst);
+  uint16_t* kv = reinterpret_cast<uint16_t*>(lds + PL.kv);
+  uint16_t* gam = reinterpret_cast<uint16_t*>(lds + PL.end);
+  const TileSetup<uint16_t, HD, NT, false, !FOLD> su(nullptr, 0, 0, 0, 0, a.gamma, a.d, a.rev);
+  auto setup = [&]() {
+    su.store(nullptr, gam, rev);
+    if (tid < MT) pos[tid] = a.pos0[b] + t0 + tid;
+  };
+  WideTile<HD, MT, PACKED, FOLD, NT, KLD, true>::run(static_cast<const uint16_t*>(a.h) + ((size_t)b * a.h_ld + t0) * a.d, n,
+                                               gam, static_cast<const uint16_t*>(a.gamma), a.d, a.eps, halves, hst,
+                                               rinv, pos, rev, kv, setup);
+  __syncthreads();
+
+  // store: 16-byte chunks of the tile's valid rows
+  constexpr int CPR = HD / 8;
+  uint16_t* dst0;
+  size_t row_stride;
+  if (kv_mode) {
+    dst0 = static_cast<uint16_t*>(half ? a.v_out : a.k_out) +
+           (((size_t)b * a.n_kv + head) * a.kv_t_cap + a.kv_t_off + t0) * HD;
+    row_stride = HD;
+  } else {
+    dst0 = static_cast<uint16_t*>(a.q_out) + (((size_t)b * a.T + t0) * a.n_q + head) * HD;  // [B][T][n_q][hd]
+    row_stride = (size_t)a.n_q * HD;
+  }
+  for (int c = tid; c < n * CPR; c += NT) {
+    const int row = c / CPR, ch = c - row * CPR;
+    *reinterpret_cast<uint4*>(dst0 + row * row_stride + ch * 8) =
+        *reinterpret_cast<const uint4*>(kv + (size_t)row * KLD + ch * 8);
+  }
+}
+
 // ------------------------------------------------------------------ streaming current-token projection
 
 // One workgroup of kStreamWaves waves per 32 weight rows.  blockIdx.x: a 32-row
@@ -540,6 +611,142 @@ __global__ __launch_bounds__(kNtWide, 1) void fused_wide_kernel(
   fused_body<uint16_t, HD, kMtWide, PACKED, FOLD>(a, per_xcd, hg);
 }
 
+// ------------------------------------------------------------------ fused recompute + attention, split engine
+
+// bf16, head_dim 128 / 256, for calls with too few 128-token tiles to fill the
+// chip with both halves per workgroup.  Per (KV head j, sequence b, 128-token
+// chunk c) two workgroups of split_nt(HD) threads on the split engine: the K
+// role recomputes the chunk's K rows (with RoPE) and takes tasks 1-2 of the
+// tile attention (scores, max, sum, probabilities), which it writes to the
+// chunk's exchange record before setting bit c of the (b, j) completion words;
+// the V role recomputes the V rows, waits for that bit (a bounded wait), reads
+// the record and takes task 3 (P V), then writes the chunk's split-K partial,
+// arrives at the (b, j) counter and, if last, merges.  The K role of a pair is
+// the item before its V role, on the same XCD, so it is dispatched no later
+// than the V role that waits for it and depends on nothing itself.  A folded
+// tail (T_tail <= fold rows: the current token) joins the last chunk, its K
+// rows in the K role's tile and its V rows in the V role's.  grid:
+// xcd_map(2 * n_kv * B * n_rec), items ordered as fused_body's chunks.
+template <int HD, bool PACKED, bool FOLD>
+__global__ __launch_bounds__(split_nt(HD), 1) void fused_split_kernel(FusedArgs a, int per_xcd, int hg) {
+  extern __shared__ __align__(16) char lds[];
+  constexpr int NT = split_nt(HD), MT = kMtSplit, FR = fold_rows<uint16_t>();
+  constexpr ProjLds PL = split_lds(HD, MT, FR);
+  constexpr int KLD = split_ld(HD);
+  constexpr int CPR = HD / 8;  // 16-byte chunks of a K (or V) row
+  static_assert(FR * CPR <= NT, "one folded-tail chunk per thread");
+  const int tid = threadIdx.x;
+  const int C = a.n_rec;
+  const unsigned item = (blockIdx.x % kXcds) * (unsigned)per_xcd + blockIdx.x / kXcds;
+  if (item >= 2u * (unsigned)a.n_kv * (unsigned)a.B * (unsigned)C) return;
+  const int role = (int)(item & 1u);  // 0: K rows, 1: V rows
+  const unsigned pair = item >> 1;
+  const int hg_log2 = __builtin_ctz((unsigned)hg);
+  const unsigned hgC = (unsigned)C << hg_log2;
+  const unsigned gi = pair / hgC, rem = pair - gi * hgC;
+  const int jg = (int)(gi / (unsigned)a.B);
+  const int b = (int)(gi - (unsigned)jg * (unsigned)a.B);
+  const int c = (int)(rem >> hg_log2);
+  const int j = (jg << hg_log2) + (int)(rem & (unsigned)(hg - 1));
+  const int g = a.n_q / a.n_kv;
+  constexpr int ROWS = MT + FR;
+  const AttnLds AL = attn_lds(PL.end, g, HD, ROWS);
+  uint16_t* tile = reinterpret_cast<uint16_t*>(lds + PL.kv);
+  const int t0 = c * MT;
+  const int n = min(MT, a.T_rec - t0);
+
+  // folded tail rows of this role's half, loaded with the setup values
+  const bool tail_here = a.T_tail > 0 && c == C - 1;
+  const int tr = tid / CPR, tch = tid - tr * CPR;
+  const bool tail_mine = tail_here && tr < a.T_tail;
+  u32x4_t tail_v;
+  {
+    int tslot = a.tail_t_off + (tail_mine ? tr : 0);  // a ring of tail_t_cap slots
+    tslot -= tslot >= a.tail_t_cap ? a.tail_t_cap : 0;
+    const size_t trow = ((size_t)b * a.n_kv + j) * a.tail_t_cap + tslot;
+    const uint16_t* src = static_cast<const uint16_t*>(role ? a.tv : a.tk) + trow * HD + tch * 8;
+    tail_v = *reinterpret_cast<const u32x4_t*>(tail_mine ? src : static_cast<const uint16_t*>(a.q));
+  }
+
+  double* rev = reinterpret_cast<double*>(lds + PL.rev);
+  float* rinv = reinterpret_cast<float*>(lds + PL.rinv);
+  int* pos = reinterpret_cast<int*>(lds + PL.pos);
+  uint16_t* hst = reinterpret_cast<uint16_t*>(lds + PL.hst);
+  uint16_t* gam = reinterpret_cast<uint16_t*>(lds + AL.end);
+  const TileSetup<uint16_t, HD, NT, true, !FOLD> su(static_cast<const uint16_t*>(a.q), b, a.n_q, j, g, a.gamma, a.d,
+                                                     a.rev);
+  auto setup = [&]() {
+    const int p0 = (a.pos0 != nullptr ? a.pos0[b] : 0) + t0;
+    su.store(reinterpret_cast<float*>(lds + AL.q), gam, rev);
+    if (tid < MT) pos[tid] = p0 + tid;
+    if (tail_mine) *reinterpret_cast<u32x4_t*>(tile + (size_t)(MT + tr) * KLD + tch * 8) = tail_v;
+  };
+  const size_t hd_d = (size_t)HD * a.d;
+  const Half halves[2] = {Half{static_cast<const uint16_t*>(role ? a.w_v : a.w_k) + j * hd_d, 1 - role},
+                          Half{nullptr, 0}};
+  WideTile<HD, MT, PACKED, FOLD, NT, KLD, true>::run(static_cast<const uint16_t*>(a.h) + ((size_t)b * a.h_ld + t0) * a.d,
+                                                     n, gam, static_cast<const uint16_t*>(a.gamma), a.d, a.eps, halves,
+                                                     hst, rinv, pos, rev, tile, setup);
+  __syncthreads();
+  if (a.dbg_k != nullptr) {
+    uint16_t* base = static_cast<uint16_t*>(role ? a.dbg_v : a.dbg_k);
+    uint16_t* dst = base + (((size_t)b * a.n_kv + j) * a.dbg_t_cap + a.dbg_t_off + t0) * HD;
+    for (int i = tid; i < n * CPR; i += NT) {
+      const int row = i / CPR, ch = i - row * CPR;
+      *reinterpret_cast<uint4*>(dst + (size_t)row * HD + ch * 8) =
+          *reinterpret_cast<const uint4*>(tile + (size_t)row * KLD + ch * 8);
+    }
+  }
+  int nk = n;
+  if (tail_here) {
+    if (n < MT) move_rows<uint16_t, HD, NT, FR, HD, KLD>(tile, MT, n, a.T_tail);
+    nk = n + a.T_tail;
+  }
+  float* S = reinterpret_cast<float*>(lds + AL.s);
+  float* ml = reinterpret_cast<float*>(lds + AL.ml);
+  float* xrec = a.xch + (((size_t)b * a.n_kv + j) * C + c) * a.xf;
+  unsigned long long* bits = a.ws_bits + ((size_t)b * a.n_kv + j) * kSplitBitWords;
+  if (role == 0) {
+    attend_scores<uint16_t, HD, NT, 3, KLD>(tile, nk, ROWS, g, lds, AL);
+    for (int i = tid; i < g * ROWS; i += NT) store_dev(xrec + i, S[i]);
+    if (tid < 2 * g) store_dev(xrec + g * ROWS + tid, ml[tid]);
+    __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0): this thread's record stores are complete
+    __syncthreads();
+    if (tid == 0)
+      __hip_atomic_fetch_or(bits + (c >> 6), 1ull << (c & 63), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    return;
+  }
+  int* flag = reinterpret_cast<int*>(lds + AL.ctr);
+  if (tid == 0) {
+    int ok = 0;
+    for (unsigned it = 0; it < kSplitSpinLimit; ++it) {
+      if ((__hip_atomic_load(bits + (c >> 6), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) >> (c & 63)) & 1ull) {
+        ok = 1;
+        break;
+      }
+      __builtin_amdgcn_s_sleep(2);
+    }
+    *flag = ok;
+  }
+  __syncthreads();
+  const bool ok = *flag != 0;
+  for (int i = tid; i < g * ROWS; i += NT) S[i] = load_dev(xrec + i);
+  if (tid < 2 * g) ml[tid] = ok ? load_dev(xrec + g * ROWS + tid) : __builtin_nanf("");
+  __syncthreads();
+  attend_pv<uint16_t, HD, NT, KLD>(tile, nk, ROWS, g, lds, AL);
+  write_partial<HD, NT>(lds, AL, a.ws_acc, a.ws_ml, b, a.n_q, j, g, a.S, c);
+  // every V role arrives (also without out): the last one clears the
+  // completion words for the next call
+  unsigned long long* ctr = a.ws_done + (size_t)b * a.n_kv + j;
+  const unsigned long long before = split_arrive(ctr, 1, reinterpret_cast<unsigned long long*>(lds + AL.ctr));
+  if (split_complete(ctr, before, 1, a.S)) {
+    if (tid < kSplitBitWords) __hip_atomic_store(bits + tid, 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (a.out != nullptr)
+      combine_rows<uint16_t, HD, NT>(a.ws_acc, a.ws_ml, static_cast<uint16_t*>(a.out),
+                                     (size_t)b * a.n_q + (size_t)j * g, g, a.S, reinterpret_cast<float*>(lds + AL.cmb));
+  }
+}
+
 // ------------------------------------------------------------------ stored-K/V attention
 
 template <typename T, int HD>
@@ -925,6 +1132,19 @@ static hipError_t proj_t(const ProjArgs& a, int n_units, hipStream_t st) {
   return hipGetLastError();
 }
 
+template <int HD, int L>
+static hipError_t proj_split_t(const ProjArgs& a, int n_units, hipStream_t st) {
+  const size_t bytes = split_lds(HD, kMtSplit).end + gamma_lds_bytes(a.d);
+  static std::atomic<size_t> done{0};
+  auto k = proj_split_kernel<HD, L != 0, L == 2>;
+  hipError_t e = ensure_lds(k, bytes, done);
+  if (e != hipSuccess) return e;
+  const int tps = (a.T + kMtSplit - 1) / kMtSplit;
+  const XcdMap m = xcd_map(2LL * n_units * a.B * tps);
+  hipLaunchKernelGGL(k, dim3(m.grid), dim3(split_nt(HD)), bytes, st, a, m.per, tps, n_units);
+  return hipGetLastError();
+}
+
 template <int HD, int L, int NCH>
 static hipError_t stream_t(const ProjArgs& a, hipStream_t st) {
   const int G = stream_group(a.d, a.B * a.T, kLdsPerGroup);
@@ -971,6 +1191,21 @@ static hipError_t fused_wide_t(const FusedArgs& a, hipStream_t st) {
   const XcdMap m = xcd_map((long long)a.n_kv * a.B * C);
   const int hg = a.T_tail > 0 ? 1 : fused_head_group(a.n_kv, HD, m.per);
   hipLaunchKernelGGL(k, dim3(m.grid), dim3(kNtWide), bytes, st, a, m.per, hg);
+  return hipGetLastError();
+}
+
+template <int HD, int L>
+static hipError_t fused_split_t(const FusedArgs& a, hipStream_t st) {
+  const size_t bytes = fused_split_lds_bytes(a.n_q / a.n_kv, HD) + gamma_lds_bytes(a.d);
+  static std::atomic<size_t> done{0};
+  auto k = fused_split_kernel<HD, L != 0, L == 2>;
+  hipError_t e = ensure_lds(k, bytes, done);
+  if (e != hipSuccess) return e;
+  // items in pairs: an even count per XCD keeps each pair on one XCD
+  const long long pairs = (long long)a.n_kv * a.B * a.n_rec;
+  const int per = 2 * (int)((pairs + kXcds - 1) / kXcds);
+  const int hg = fused_head_group(a.n_kv, HD, per / 2);
+  hipLaunchKernelGGL(k, dim3(kXcds * per), dim3(split_nt(HD)), bytes, st, a, per, hg);
   return hipGetLastError();
 }
 
@@ -1042,6 +1277,12 @@ static hipError_t with_layout(int layout, const F& f) {
 }
 
 hipError_t launch_proj(const ProjArgs& a, int dtype_bf16, int hd, int layout, int n_units, hipStream_t st) {
+  if (dtype_bf16 && split_prefill(hd, a.T, 2LL * n_units * a.B * ((a.T + kMtSplit - 1) / kMtSplit))) {
+    return with_layout(layout, [&](auto lc) -> hipError_t {
+      constexpr int L = decltype(lc)::value;
+      return hd == 256 ? proj_split_t<256, L>(a, n_units, st) : proj_split_t<128, L>(a, n_units, st);
+    });
+  }
 #define PB(H) with_layout(layout, [&](auto lc) { return proj_t<uint16_t, H, decltype(lc)::value>(a, n_units, st); })
 #define PF(H) proj_t<float, H, 0>(a, n_units, st)
   KVD_DISPATCH(dtype_bf16, hd, PB, PF)
@@ -1074,8 +1315,19 @@ hipError_t launch_project_current(const ProjArgs& a, int dtype_bf16, int hd, int
   });
 }
 
-hipError_t launch_fused(const FusedArgs& a, int dtype_bf16, int hd, int layout, int wide, hipStream_t st) {
-  if (wide) {
+hipError_t launch_fused(const FusedArgs& a, int dtype_bf16, int hd, int layout, int engine, hipStream_t st) {
+  if (engine == kFusedSplit) {
+    if (!dtype_bf16) return hipErrorInvalidValue;
+    return with_layout(layout, [&](auto lc) -> hipError_t {
+      constexpr int L = decltype(lc)::value;
+      switch (hd) {
+        case 128: return fused_split_t<128, L>(a, st);
+        case 256: return fused_split_t<256, L>(a, st);
+        default: return hipErrorInvalidValue;
+      }
+    });
+  }
+  if (engine == kFusedWide) {
     if (!dtype_bf16) return hipErrorInvalidValue;
     return with_layout(layout, [&](auto lc) -> hipError_t {
       constexpr int L = decltype(lc)::value;

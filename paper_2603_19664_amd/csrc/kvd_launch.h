@@ -52,6 +52,12 @@ struct FusedArgs {
   void* out;
   int d, n_q, n_kv, B, T_rec, n_rec, S;
   float eps;
+  // split engine: per (b, KV head) kSplitBitWords words of K-role completion
+  // bits (zero between calls), and per (b, KV head, chunk) xf floats of the
+  // K role's probabilities [g][kMtSplit + fold rows] and (max, sum) [g][2]
+  unsigned long long* ws_bits;
+  float* xch;
+  int xf;
   double rev[kMaxPairs];
 };
 
@@ -150,9 +156,13 @@ hipError_t launch_proj(const ProjArgs& a, int dtype_bf16, int hd, int layout, in
 // Current-token projection (T == 1): the streaming kernel for bf16, proj_kernel for fp32.
 hipError_t launch_project_current(const ProjArgs& a, int dtype_bf16, int hd, int layout, int n_units,
                                   hipStream_t st);
-// wide: the 128-token engine (fused_wide_kernel; bf16, head_dim 128 / 256, a.n_rec
-// counted in 128-token tiles, the tail never folded).
-hipError_t launch_fused(const FusedArgs& a, int dtype_bf16, int hd, int layout, int wide, hipStream_t st);
+// engine: kFusedTile64 (fused_kernel), kFusedWide (the 128-token engine,
+// fused_wide_kernel; bf16, head_dim 128 / 256, a.n_rec counted in 128-token
+// tiles, the tail never folded) or kFusedSplit (fused_split_kernel; bf16,
+// head_dim 128 / 256, 128-token chunks, a tail of at most fold_rows rows,
+// folded).
+enum { kFusedTile64 = 0, kFusedWide = 1, kFusedSplit = 2 };
+hipError_t launch_fused(const FusedArgs& a, int dtype_bf16, int hd, int layout, int engine, hipStream_t st);
 // gamma: nullptr, or [d] bf16 folded into the packed values (bf16(w * gamma)).
 hipError_t launch_pack(const void* w, const void* gamma, void* out, int rows, int d, hipStream_t st);
 hipError_t launch_decode(const AttnArgs& a, int dtype_bf16, int hd, hipStream_t st);

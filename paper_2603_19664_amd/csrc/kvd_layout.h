@@ -27,6 +27,41 @@ constexpr int kNtWide = 512;
 constexpr int kMtWide = 128;
 constexpr int kWideMinTiles = 256;
 
+// The split engine (bf16, head_dim 128 / 256): a 128-token tile of one half
+// (a KV head's K rows, or its V rows) per workgroup of 4 waves, one per SIMD.
+// The K and V halves of a tile run as two workgroups, so a grid has as many
+// workgroups as with 64-token tiles of both halves while each CU streams half
+// the weight bytes per flop.  The K/V tile in LDS holds one half: row stride
+// split_ld(hd) elements.
+constexpr int kMtSplit = 128;
+// head_dim 256: 8 waves of one 32-row block each (two per SIMD); head_dim 128:
+// 4 waves (the half has 128 rows).
+constexpr int split_nt(int hd) { return hd == 256 ? 512 : 256; }
+// The fused call on the split engine: the V role of chunk c waits for bit c of
+// its (sequence, KV head)'s completion words, which the K role sets once its
+// probabilities are out; the words are cleared by the workgroup that merges
+// the splits.  At most 64 * kSplitBitWords chunks per sequence.
+constexpr int kSplitBitWords = 4;
+constexpr int kSplitMaxChunks = 64 * kSplitBitWords;
+// Polls of the V role's bounded wait (about 0.1 s); past it the chunk's partial
+// is written as NaN, so the call's output shows the failure.
+constexpr unsigned kSplitSpinLimit = 1u << 17;
+// Floats of one chunk's exchange record for group size g (rows: kMtSplit plus
+// a folded tail of up to 4, fold_rows).
+constexpr int split_xf(int g) { return (g * (kMtSplit + 4) + 2 * g + 3) / 4 * 4; }
+constexpr int split_ld(int hd) { return hd + 8; }
+// Prefill / recompute (kvd_recompute_kv, the block forward's projections) runs
+// on the split engine for bf16 at head_dim 256, and at head_dim 128 when its
+// grid (wgs workgroups) fills at least two rounds of the chip: measured on
+// MI355X against 64-token tiles of both halves, 8-15% faster at head_dim 256
+// (Gemma-3-4B shape, 512..8192 tokens); at head_dim 128 the 4-wave layout is
+// 8-10% faster on 512-workgroup grids and 27% slower on 64 (Qwen2.5-1.5B shape).
+// Its tiles hold the tokens of one sequence, so sequences shorter than half a
+// tile stay on 64-token tiles.
+constexpr bool split_prefill(int hd, int T, long long wgs) {
+  return T >= kMtSplit / 2 && (hd == 256 || (hd == 128 && wgs >= 512));
+}
+
 // A stored tail of at most fold_rows<T>() rows (a decode step's current token)
 // joins the split of the last recomputed tile of a fused call: the rows are
 // copied into LDS while that tile is recomputed and attended with its keys.
@@ -132,6 +167,24 @@ constexpr ProjLds proj_lds(int hd, int mt, int extra = 0) {
   return L;
 }
 
+// The split engine's LDS: RoPE table, 1/rms and positions, the staging ring of
+// kDepth K-steps of mt tokens, and the one-half K/V tile [mt + extra][split_ld]
+// placed (as in proj_lds) so that its rows mt .. (filled during the K-loop)
+// stay clear of the ring.
+constexpr ProjLds split_lds(int hd, int mt, int extra = 0) {
+  ProjLds L{};
+  L.rev = 0;
+  L.rinv = align_up(L.rev + sizeof(double) * kMaxPairs, 16);
+  L.pos = align_up(L.rinv + sizeof(float) * mt, 16);
+  L.hst = align_up(L.pos + sizeof(int) * mt, 16);
+  const size_t hst_end = L.hst + sizeof(uint16_t) * kDepth * mt * kKT;
+  const size_t row = sizeof(uint16_t) * split_ld(hd);
+  L.kv = extra > 0 && L.hst + mt * row < hst_end ? hst_end - mt * row : L.hst;
+  const size_t kv_end = L.kv + row * (mt + extra);
+  L.end = align_up(hst_end > kv_end ? hst_end : kv_end, 16);
+  return L;
+}
+
 // gamma (bf16, [d]) of the bf16 recompute engine sits after a kernel's other LDS.
 constexpr size_t gamma_lds_bytes(int d) { return align_up((size_t)2 * d, 16); }
 
@@ -144,6 +197,10 @@ constexpr size_t decode_lds_bytes(int g, int hd) {
 template <typename T>
 constexpr size_t fused_lds_bytes(int g, int hd, int mt) {
   return attn_lds(proj_lds<T>(hd, mt, fold_rows<T>()).end, g, hd, mt + fold_rows<T>()).end;
+}
+// The fused kernel on the split engine: a folded tail of up to fold rows.
+constexpr size_t fused_split_lds_bytes(int g, int hd) {
+  return attn_lds(split_lds(hd, kMtSplit, 4).end, g, hd, kMtSplit + 4).end;
 }
 // The wide fused kernel: no folded tail (its tile already holds 128 keys).
 constexpr size_t fused_wide_lds_bytes(int g, int hd) {

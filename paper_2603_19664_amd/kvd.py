@@ -24,6 +24,7 @@ KVD_OK, KVD_ERR_NULL, KVD_ERR_SHAPE, KVD_ERR_UNSUPPORTED, KVD_ERR_WORKSPACE, KVD
 KVD_F32, KVD_BF16 = 0, 1
 KVD_W_ROWMAJOR, KVD_W_PACKED, KVD_W_PACKED_GAMMA = 0, 1, 2
 KVD_OP_DECODE_ATTN, KVD_OP_CACHED_ATTN, KVD_OP_FUSED = 0, 1, 2
+KVD_FUSED_SPLIT = -128  # kvd_set_fused_tokens: the split engine
 
 _DTYPES = {KVD_F32: torch.float32, KVD_BF16: torch.bfloat16}
 
@@ -263,7 +264,8 @@ def kvd_set_attn_workgroups(target: int) -> int:
 
 def kvd_set_fused_tokens(tokens: int) -> int:
     """Recomputed tokens per workgroup of the fused calls: 0 chooses per call, 128 the
-    wide engine where it exists, 64 the 64-token tiles; returns the previous setting."""
+    wide engine where it exists, KVD_FUSED_SPLIT the split engine where a call can use
+    it, 64 the 64-token tiles; returns the previous setting."""
     return lib.kvd_set_fused_tokens(int(tokens))
 
 

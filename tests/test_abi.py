@@ -24,7 +24,7 @@ def view(t_cap=16, t_off=0, k=FAKE, v=FAKE):
 
 
 def test_loads_and_version():
-    assert kvd.abi_version() == 7
+    assert kvd.abi_version() == 8
     assert kvd.status_str(kvd.KVD_ERR_ALIGN) == "KVD_ERR_ALIGN"
 
 
@@ -197,55 +197,91 @@ def test_split_policy_and_workspace():
     assert S == 7
     acc = -(-2 * 8 * S * 256 * 4 // 256) * 256
     ml = -(-2 * 8 * S * 2 * 4 // 256) * 256
-    done = -(-2 * 4 * 8 // 256) * 256  # split counters [B][n_kv] uint64
+    done = -(-2 * 4 * 8 // 256) * 256 + -(-2 * 4 * 4 * 8 // 256) * 256  # split counters, completion words
     assert n == acc + ml + done
     assert lib.kvd_workspace_bytes(ctypes.byref(s), 9, 1, 10, 0) == 0
 
 
-def _fused_splits(s, B, T_rec, T_tail, tokens):
-    """The fused call's split count as documented: 64-token tiles with a bf16 tail of
-    <= 4 rows folded into the last one, or 128-token wide tiles (bf16, head_dim 128 /
-    256) when forced or when there are at least 256 of them; tails in 64-row tiles."""
-    wide_ok = s.dtype == kvd.KVD_BF16 and s.head_dim in (128, 256) and T_rec > 0
-    wide = wide_ok and (tokens == 128 or (tokens == 0 and B * s.n_kv_heads * -(-T_rec // 128) >= 256))
-    if wide:
+def _engine(s, B, T_rec, T_tail, tokens):
+    """The fused call's engine as documented: 128-token wide tiles (bf16, head_dim 128 /
+    256) when forced or when there are at least 256 of them; the split engine (bf16,
+    head_dim 128 / 256, T_rec >= 1, T_tail <= 4, <= 256 chunks) only when forced; else
+    64-token tiles."""
+    big = s.dtype == kvd.KVD_BF16 and s.head_dim in (128, 256)
+    wide_ok = big and T_rec > 0
+    split_ok = big and T_rec > 0 and T_tail <= 4 and -(-T_rec // 128) <= 256
+    if tokens == 64:
+        return "tile64"
+    if tokens == 128:
+        return "wide" if wide_ok else "tile64"
+    if tokens == kvd.KVD_FUSED_SPLIT:
+        return "split" if split_ok else "tile64"
+    if wide_ok and B * s.n_kv_heads * -(-T_rec // 128) >= 256:
+        return "wide"
+    return "tile64"
+
+
+def _fused_splits(s, B, T_rec, T_tail, tokens, engine=None):
+    """The fused call's split count: one per recomputed tile; a bf16 tail of <= 4 rows
+    folds into the last one on the 64-token and split engines, other tails add 64-row
+    tiles."""
+    engine = engine or _engine(s, B, T_rec, T_tail, tokens)
+    if engine == "wide":
         return -(-T_rec // 128) + -(-T_tail // 64)
+    if engine == "split":
+        return -(-T_rec // 128)
     n_rec = -(-T_rec // 64)
     fold = s.dtype == kvd.KVD_BF16 and n_rec > 0 and 0 < T_tail <= 4
     return n_rec + (0 if fold else -(-T_tail // 64))
 
 
-def _ws_bytes(s, B, S):
+def _ws_bytes(s, B, S, split_chunks=0):
     up = lambda x: -(-x // 256) * 256  # noqa: E731
-    return up(B * s.n_kv_heads * 8) + up(B * s.n_q_heads * S * s.head_dim * 4) + up(B * s.n_q_heads * S * 2 * 4)
+    g = s.n_q_heads // s.n_kv_heads
+    xf = -(-(g * 132 + 2 * g) // 4) * 4
+    return (up(B * s.n_kv_heads * 8) + up(B * s.n_kv_heads * 4 * 8) + up(B * s.n_q_heads * S * s.head_dim * 4)
+            + up(B * s.n_q_heads * S * 2 * 4) + (up(B * s.n_kv_heads * split_chunks * xf * 4) if split_chunks else 0))
+
+
+def _fused_ws_bytes(s, B, T, Tt):
+    """kvd_workspace_bytes of KVD_OP_FUSED: the largest need over the engines a call can get."""
+    n = _ws_bytes(s, B, _fused_splits(s, B, T, Tt, 0, "tile64"))
+    big = s.dtype == kvd.KVD_BF16 and s.head_dim in (128, 256) and T > 0
+    if big:
+        n = max(n, _ws_bytes(s, B, _fused_splits(s, B, T, Tt, 0, "wide")))
+    if big and Tt <= 4 and -(-T // 128) <= 256:
+        n = max(n, _ws_bytes(s, B, -(-T // 128), -(-T // 128)))
+    return n
 
 
 def test_fused_tiling_policy():
     ns = lambda sh, B, T, Tt: lib.kvd_num_splits(ctypes.byref(sh), kvd.KVD_OP_FUSED, B, T, Tt)  # noqa: E731
     gemma, qwen = shape(), shape(d_model=1536, n_q_heads=12, n_kv_heads=2, head_dim=128)
     others = [shape(dtype=kvd.KVD_F32), shape(head_dim=64, d_model=576, n_q_heads=9, n_kv_heads=3)]
-    # default: wide tiles only with a full round of them
+    # default: wide tiles with a full round of them, else 64-token tiles (the split
+    # engine only when forced)
     assert ns(gemma, 1, 4096, 1) == 64        # 128 wide tiles: 64-token tiles, folded current token
     assert ns(gemma, 2, 4096, 1) == 33        # 256 wide tiles + the tail's own split
     assert ns(gemma, 8, 2048, 1) == 17
+    assert ns(gemma, 1, 4096, 5) == 65        # a 5-row tail cannot fold: 64-token tiles + a tail tile
     assert ns(qwen, 8, 16384, 1) == 129
     try:
-        for tokens in (0, 64, 128):
-            assert lib.kvd_set_fused_tokens(tokens) in (0, 64, 128)
+        for tokens in (0, 64, 128, kvd.KVD_FUSED_SPLIT):
+            assert lib.kvd_set_fused_tokens(tokens) in (0, 64, 128, kvd.KVD_FUSED_SPLIT)
             for sh in [gemma, qwen] + others:
                 for B, T, Tt in [(1, 4096, 1), (2, 4096, 1), (8, 2048, 1), (1, 100, 1), (1, 0, 3), (3, 130, 70),
-                                 (16, 5120, 0), (1, 64, 4), (1, 64, 5)]:
+                                 (16, 5120, 0), (1, 64, 4), (1, 64, 5), (1, 32769, 1)]:
                     S = ns(sh, B, T, Tt)
                     assert S == _fused_splits(sh, B, T, Tt, tokens), (tokens, sh.head_dim, B, T, Tt)
-                    # the workspace covers either tiling
+                    # the workspace covers every engine
                     n = lib.kvd_workspace_bytes(ctypes.byref(sh), kvd.KVD_OP_FUSED, B, T, Tt)
                     assert n >= _ws_bytes(sh, B, S)
-                    assert n == _ws_bytes(sh, B, max(_fused_splits(sh, B, T, Tt, 64), _fused_splits(sh, B, T, Tt, 128)))
+                    assert n == _fused_ws_bytes(sh, B, T, Tt), (tokens, sh.head_dim, B, T, Tt)
         # the workspace size never falls as the context grows, whichever tiling a call gets
         for B in (1, 2, 8):
             sizes = [lib.kvd_workspace_bytes(ctypes.byref(gemma), kvd.KVD_OP_FUSED, B, T, 1) for T in range(1, 5000, 13)]
             assert sizes == sorted(sizes)
-        assert lib.kvd_set_fused_tokens(128) == 128
+        assert lib.kvd_set_fused_tokens(128) == kvd.KVD_FUSED_SPLIT  # the loop's last setting
         assert lib.kvd_set_fused_tokens(77) == 128  # other values mean 0
         assert lib.kvd_set_fused_tokens(0) == 0
     finally:
