@@ -221,11 +221,12 @@ kvd_status kvd_cached_attn(const kvd_attn_shape* shape, const void* q, const kvd
  *     (about 0.1 s); past it that split's partial is NaN, so out shows it;
  *   - 64-token tiles of K and V rows otherwise.
  * With bf16, T_rec >= 1 and T_tail <= 4 (a decode step's current token) the
- * tail joins the last tile's split on the split and 64-token engines: its
- * rows are copied into LDS while that tile is recomputed.  Otherwise the tail
- * adds one split per 64-row tile, each attended by a workgroup of its own (the
- * hybrid cache budget: recent tokens stored, older ones recomputed).
- * kvd_num_splits gives the count; kvd_workspace_bytes covers every engine.
+ * tail joins the last tile's split on every engine: its rows are copied into
+ * LDS while that tile is recomputed.  Otherwise the tail adds one split per
+ * 64-row tile, each attended by a workgroup of its own (the hybrid cache
+ * budget: recent tokens stored, older ones recomputed); with bf16 a remainder
+ * of at most 4 rows joins the tile before it.  kvd_num_splits gives the count;
+ * kvd_workspace_bytes covers every engine.
  * The workspace's split counters follow kvd_decode_attn's contract.
  * out == NULL writes only the split-K partials (see kvd_combine).
  * Supports both dtypes.                                                       */

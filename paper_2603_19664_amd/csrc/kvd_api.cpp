@@ -147,7 +147,7 @@ FusedPlan wide_plan(int32_t T_rec, int32_t T_tail) {
   p.engine = kvd::kFusedWide;
   p.mt = kvd::kMtWide;
   p.n_rec = ceil_div(T_rec, p.mt);
-  p.n_tail = ceil_div(T_tail, kvd::kTile);
+  p.n_tail = kvd::fused_tail_tiles<uint16_t>(p.n_rec, T_tail);
   p.S = p.n_rec + p.n_tail;
   return p;
 }

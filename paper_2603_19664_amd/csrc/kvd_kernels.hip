@@ -455,24 +455,26 @@ __global__ __launch_bounds__(64 * kStreamWaves) void stream_proj_kernel(ProjArgs
 // ------------------------------------------------------------------ fused recompute + attention
 
 // grid: xcd_map(n_kv * B * C) workgroups, one per (KV head j, sequence b, chunk c),
-// C = n_tail + n_rec.  Chunks c < n_tail attend stored tail tile c (64 rows;
-// partial n_rec + c) and come first, as they are short; chunk n_tail + r
-// recomputes residual rows r*MT..r*MT+MT-1 (partial r).  A folded tail (<= fold_rows<T>() rows, n_tail = 0) is attended
-// with the last recomputed chunk's keys.  MT = kMtWide: the wide engine (bf16,
-// 4 waves, 128-key chunks, no folded tail).
+// C = n_tail + n_rec.  Chunks c < n_tail attend stored tail tile c (64 rows, the
+// last one up to 64 + fold_rows<T>(); partial n_rec + c) and come first, as they
+// are short; chunk n_tail + r recomputes residual rows r*MT..r*MT+MT-1 (partial
+// r).  A folded tail (<= fold_rows<T>() rows, n_tail = 0) is attended with the
+// last recomputed chunk's keys.  MT = kMtWide: the wide engine (bf16, 128-key
+// chunks).
 template <typename T, int HD, int MT, bool PACKED, bool FOLD>
 __device__ __forceinline__ void fused_body(const FusedArgs& a, int per_xcd, int hg) {
   extern __shared__ __align__(16) char lds[];
   constexpr bool WIDE = MT == kMtWide;
   constexpr int NT = WIDE ? kNtWide : kNtTile;
-  constexpr int FR = WIDE ? 0 : fold_rows<T>();
+  constexpr int FR = fold_rows<T>();
   constexpr ProjLds PL = proj_lds<T>(HD, MT, FR);
   constexpr int CPT = MT * 8 / NT;
   constexpr int KLD = kv_ld<T>(HD);
+  constexpr int KPL = (MT + FR + 63) / 64;  // keys per lane of the tile attention
   static_assert(MT == kTile || (WIDE && sizeof(T) == 2), "fused chunks: 64-key tiles, or the wide bf16 engine");
   const int tid = threadIdx.x;
-  const bool fold = !WIDE && fold_tail<T>(a.n_rec, a.T_tail);
-  const int n_tail = WIDE ? (a.T_tail + kTile - 1) / kTile : fused_tail_tiles<T>(a.n_rec, a.T_tail);
+  const bool fold = fold_tail<T>(a.n_rec, a.T_tail);
+  const int n_tail = fused_tail_tiles<T>(a.n_rec, a.T_tail);
   const int C = n_tail + a.n_rec;
   // 32-bit index arithmetic (the item count is below 2^31, checked by the host):
   // every wave runs it on the CU's one scalar unit before its first load.
@@ -577,16 +579,25 @@ __device__ __forceinline__ void fused_body(const FusedArgs& a, int per_xcd, int 
         nk = n + a.T_tail;
       }
     }
-    attend_tile<T, HD, NT, tile_kpl<T>()>(kv, nk, MT + FR, g, lds, AL);
+    attend_tile<T, HD, NT, KPL>(kv, nk, MT + FR, g, lds, AL);
     write_partial<HD, NT>(lds, AL, a.ws_acc, a.ws_ml, b, a.n_q, j, g, a.S, rc);
   } else {
+    // tail tile c: 64 rows, the last one the rest (up to 64 + FR rows)
     const int r0 = c * kTile;
-    const int nk = min(kTile, a.T_tail - r0);
+    const int nk = c == n_tail - 1 ? a.T_tail - r0 : kTile;
     load_q<T, HD, NT>(static_cast<const T*>(a.q), b, a.n_q, j, g, reinterpret_cast<float*>(lds + AL.q));
+    int tr0 = a.tail_t_off + r0;  // the ring's slot of row r0 (a ring of tail_t_cap slots)
+    tr0 -= tr0 >= a.tail_t_cap ? a.tail_t_cap : 0;
     load_kv_tile<T, HD, NT>(static_cast<const T*>(a.tk), static_cast<const T*>(a.tv), b, a.n_kv, j, a.tail_t_cap,
-                            a.tail_t_off + r0, nk, kv);
+                            tr0, min(nk, kTile), kv);
+    if (nk > kTile) {
+      int tr1 = tr0 + kTile;
+      tr1 -= tr1 >= a.tail_t_cap ? a.tail_t_cap : 0;
+      load_kv_tile<T, HD, NT>(static_cast<const T*>(a.tk), static_cast<const T*>(a.tv), b, a.n_kv, j, a.tail_t_cap,
+                              tr1, nk - kTile, kv + (size_t)kTile * KLD);
+    }
     __syncthreads();
-    attend_tile<T, HD, NT, tile_kpl<T>()>(kv, nk, MT + FR, g, lds, AL);
+    attend_tile<T, HD, NT, KPL>(kv, nk, MT + FR, g, lds, AL);
     write_partial<HD, NT>(lds, AL, a.ws_acc, a.ws_ml, b, a.n_q, j, g, a.S, a.n_rec + c);
   }
   if (a.out != nullptr) {
@@ -1187,9 +1198,10 @@ static hipError_t fused_wide_t(const FusedArgs& a, hipStream_t st) {
   auto k = fused_wide_kernel<HD, L != 0, L == 2>;
   hipError_t e = ensure_lds(k, bytes, done);
   if (e != hipSuccess) return e;
-  const int C = (a.T_tail + kTile - 1) / kTile + a.n_rec;
+  const int n_tail = fused_tail_tiles<uint16_t>(a.n_rec, a.T_tail);
+  const int C = n_tail + a.n_rec;
   const XcdMap m = xcd_map((long long)a.n_kv * a.B * C);
-  const int hg = a.T_tail > 0 ? 1 : fused_head_group(a.n_kv, HD, m.per);
+  const int hg = n_tail > 0 ? 1 : fused_head_group(a.n_kv, HD, m.per);
   hipLaunchKernelGGL(k, dim3(m.grid), dim3(kNtWide), bytes, st, a, m.per, hg);
   return hipGetLastError();
 }

@@ -158,7 +158,7 @@ hipError_t launch_project_current(const ProjArgs& a, int dtype_bf16, int hd, int
                                   hipStream_t st);
 // engine: kFusedTile64 (fused_kernel), kFusedWide (the 128-token engine,
 // fused_wide_kernel; bf16, head_dim 128 / 256, a.n_rec counted in 128-token
-// tiles, the tail never folded) or kFusedSplit (fused_split_kernel; bf16,
+// tiles) or kFusedSplit (fused_split_kernel; bf16,
 // head_dim 128 / 256, 128-token chunks, a tail of at most fold_rows rows,
 // folded).
 enum { kFusedTile64 = 0, kFusedWide = 1, kFusedSplit = 2 };

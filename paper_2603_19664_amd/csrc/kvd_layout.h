@@ -83,11 +83,14 @@ constexpr int decode_splits(int Tk) {
 // Keys per lane of the attention tiles (up to 64 + fold_rows<T>() keys).
 template <typename T>
 constexpr int tile_kpl() { return kTile + fold_rows<T>() > 64 ? 2 : 1; }
-// Splits of a fused call: one per recomputed tile, plus one per tail tile
-// unless the tail is folded.
+// Splits of a fused call: one per recomputed tile, plus the stored tail's tiles
+// unless the tail is folded: one per 64 rows, a remainder of at most
+// fold_rows<T>() rows joining the tile before it (as decode_splits chunks
+// stored keys), so that a stored window plus the current token adds no
+// workgroup for that one row.
 template <typename T>
 constexpr int fused_tail_tiles(int n_rec, int T_tail) {
-  return fold_tail<T>(n_rec, T_tail) ? 0 : (T_tail + kTile - 1) / kTile;
+  return fold_tail<T>(n_rec, T_tail) ? 0 : decode_splits<T>(T_tail);
 }
 
 // Streaming projection (current-token q/K/V): tokens per workgroup.
@@ -202,9 +205,10 @@ constexpr size_t fused_lds_bytes(int g, int hd, int mt) {
 constexpr size_t fused_split_lds_bytes(int g, int hd) {
   return attn_lds(split_lds(hd, kMtSplit, 4).end, g, hd, kMtSplit + 4).end;
 }
-// The wide fused kernel: no folded tail (its tile already holds 128 keys).
+// The wide fused kernel: 128-key tiles plus a folded tail.
 constexpr size_t fused_wide_lds_bytes(int g, int hd) {
-  return attn_lds(proj_lds<uint16_t>(hd, kMtWide, 0).end, g, hd, kMtWide).end;
+  return attn_lds(proj_lds<uint16_t>(hd, kMtWide, fold_rows<uint16_t>()).end, g, hd, kMtWide + fold_rows<uint16_t>())
+      .end;
 }
 
 // Streaming projection (current-token q/K/V): one workgroup of kStreamWaves

@@ -221,18 +221,28 @@ def _engine(s, B, T_rec, T_tail, tokens):
     return "tile64"
 
 
+def _tail_tiles(s, n_rec, T_tail):
+    """Stored-tail tiles: none when a bf16 tail of <= 4 rows folds into the last recomputed
+    tile; else one per 64 rows, a bf16 remainder of <= 4 rows joining the tile before it."""
+    bf = s.dtype == kvd.KVD_BF16
+    if bf and n_rec > 0 and 0 < T_tail <= 4:
+        return 0
+    r = T_tail % 64
+    if bf and T_tail > 64 and 0 < r <= 4:
+        return T_tail // 64
+    return -(-T_tail // 64)
+
+
 def _fused_splits(s, B, T_rec, T_tail, tokens, engine=None):
-    """The fused call's split count: one per recomputed tile; a bf16 tail of <= 4 rows
-    folds into the last one on the 64-token and split engines, other tails add 64-row
-    tiles."""
+    """The fused call's split count: one per recomputed tile plus the stored tail's tiles."""
     engine = engine or _engine(s, B, T_rec, T_tail, tokens)
     if engine == "wide":
-        return -(-T_rec // 128) + -(-T_tail // 64)
+        n_rec = -(-T_rec // 128)
+        return n_rec + _tail_tiles(s, n_rec, T_tail)
     if engine == "split":
         return -(-T_rec // 128)
     n_rec = -(-T_rec // 64)
-    fold = s.dtype == kvd.KVD_BF16 and n_rec > 0 and 0 < T_tail <= 4
-    return n_rec + (0 if fold else -(-T_tail // 64))
+    return n_rec + _tail_tiles(s, n_rec, T_tail)
 
 
 def _ws_bytes(s, B, S, split_chunks=0):
@@ -261,10 +271,11 @@ def test_fused_tiling_policy():
     # default: wide tiles with a full round of them, else 64-token tiles (the split
     # engine only when forced)
     assert ns(gemma, 1, 4096, 1) == 64        # 128 wide tiles: 64-token tiles, folded current token
-    assert ns(gemma, 2, 4096, 1) == 33        # 256 wide tiles + the tail's own split
-    assert ns(gemma, 8, 2048, 1) == 17
+    assert ns(gemma, 2, 4096, 1) == 32        # 256 wide tiles, folded current token
+    assert ns(gemma, 8, 2048, 1) == 16
+    assert ns(gemma, 1, 3072, 1025) == 48 + 16  # a stored window of 1024 + the current token: 16 tail tiles
     assert ns(gemma, 1, 4096, 5) == 65        # a 5-row tail cannot fold: 64-token tiles + a tail tile
-    assert ns(qwen, 8, 16384, 1) == 129
+    assert ns(qwen, 8, 16384, 1) == 128
     try:
         for tokens in (0, 64, 128, kvd.KVD_FUSED_SPLIT):
             assert lib.kvd_set_fused_tokens(tokens) in (0, 64, 128, kvd.KVD_FUSED_SPLIT)

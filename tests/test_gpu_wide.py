@@ -10,6 +10,9 @@ automatic policy on a shape with a full round of wide tiles.
   attn_weights / head_output) and the 64-token tiling to the bf16 tolerance.
 - Stored tails (Algorithm 1's bounded cache, also as a wrapped ring), the
   partials-then-kvd_combine path and sliding-window layers go through it too.
+  A tail of <= 4 rows (the current token) folds into the last 128-token chunk,
+  also a partial one; a longer tail's remainder of <= 4 rows joins its last
+  64-row tile.
 
 Tolerance (max |gpu - oracle| / max |oracle|): 2e-2 for bf16 inputs."""
 import pytest
@@ -62,7 +65,7 @@ def test_wide_kv_bitwise_and_output(hd, packed, T):
     s = L.shape
     Kp, Vp = gpu_recompute(L)
     kvd.kvd_set_fused_tokens(128)
-    assert kvd.kvd_num_splits(s, kvd.KVD_OP_FUSED, L.B, T, 1) == -(-T // 128) + 1
+    assert kvd.kvd_num_splits(s, kvd.KVD_OP_FUSED, L.B, T, 1) == -(-T // 128)  # the current token folds
     q, _, out, (dk, dv) = gpu_fused(L, kv_debug=True)
     assert torch.equal(_bits(dk), _bits(Kp)) and torch.equal(_bits(dv), _bits(Vp))
     check("wide fused vs oracle", out, oracle_decode(L))
@@ -72,10 +75,20 @@ def test_wide_kv_bitwise_and_output(hd, packed, T):
     check("wide vs 64-token tiles", out, f64(out64))
 
 
-@pytest.mark.parametrize("T_rec,T", [(130, 430), (128, 131), (256, 262), (300, 300), (1, 70)])
+def _tail_tiles(n_rec, T_tail):
+    if n_rec > 0 and 0 < T_tail <= 4:
+        return 0  # folded into the last recomputed chunk
+    return T_tail // 64 if T_tail > 64 and 0 < T_tail % 64 <= 4 else -(-T_tail // 64)
+
+
+@pytest.mark.parametrize("T_rec,T", [(130, 430), (128, 131), (256, 262), (300, 300), (1, 70), (128, 320),
+                                     (300, 302)])
 def test_wide_stored_tail(T_rec, T):
     # recompute the oldest T_rec context rows, read the rest and the current
-    # token as a stored tail (own 64-row splits on the wide engine)
+    # token as a stored tail: folded into the last chunk when it has <= 4 rows
+    # (after a full chunk (128, 131), over a partial one (300, 300), (300, 302)),
+    # else 64-row tiles of its own, a remainder of <= 4 rows joining the last
+    # of them (128, 320)
     L = _layer(256, T, seed=90 + T_rec)
     s = L.shape
     q, K, V, out_u = gpu_unfused(L)
@@ -86,7 +99,7 @@ def test_wide_stored_tail(T_rec, T):
         kvd.kvd_fused_recompute_attn(s, q, L.h, T_rec, L.gamma, L.lw_k, L.lw_v, L.pos0, out, ws, K, V, T_tail, T_rec)
 
     S = kvd.kvd_num_splits(s, kvd.KVD_OP_FUSED, L.B, T_rec, T_tail)
-    assert S == -(-T_rec // 128) + -(-T_tail // 64)
+    assert S == -(-T_rec // 128) + _tail_tiles(-(-T_rec // 128), T_tail)
     ws = kvd.workspace(s, kvd.KVD_OP_FUSED, L.B, T_rec, T_tail)
     out = torch.empty_like(q)
     fused(out, ws)
@@ -130,7 +143,7 @@ def test_wide_by_policy_on_a_full_round():
     L = make_layer(C.QWEN_1_5B, B=4, T=1024, seed=99, d_model=512, n_q=16, n_kv=8, head_dim=128,
                    pos0=[0, 300, 17, 900])
     s = L.shape
-    assert kvd.kvd_num_splits(s, kvd.KVD_OP_FUSED, L.B, L.T, 1) == 8 + 1
+    assert kvd.kvd_num_splits(s, kvd.KVD_OP_FUSED, L.B, L.T, 1) == 8
     q, _, out, _ = gpu_fused(L)
     check("auto wide vs oracle (sequences 0, 3)", out[[0, 3]], oracle_decode(L, b_sel=[0, 3]))
     kvd.kvd_set_fused_tokens(128)
