@@ -127,27 +127,33 @@ __global__ __launch_bounds__(kNtTile, 1) void proj_kernel(ProjArgs a, int per_xc
 
 // ------------------------------------------------------------------ recompute / prefill, split engine
 
-// bf16, head_dim 128 / 256: one half of a unit (a KV head's K rows or its V
-// rows; query heads 2u and 2u + 1 for a q unit) for a tile of up to kMtSplit
-// tokens of one sequence, per workgroup of kNtSplit threads.  grid:
-// xcd_map(2 * n_units * B * tps) with tps = ceil(T / kMtSplit) tiles per
-// sequence; item = ((unit * B + b) * tps + tile) * 2 + half, so the two halves
-// of a tile are adjacent items on one XCD (its L2 serves the tile's residual
-// rows to both) and a unit's tiles stay on one XCD.  Per element the arithmetic
-// is the other engines' (the same MFMA chain over d, staging, 1/rms and
-// epilogue), so the K/V are bit-identical.
-template <int HD, bool PACKED, bool FOLD>
-__global__ __launch_bounds__(split_nt(HD), 1) void proj_split_kernel(ProjArgs a, int per_xcd, int tps, int n_units) {
+// bf16, head_dim 128 / 256: RW rows of one half of a unit (a KV head's K rows
+// or its V rows; query heads 2u and 2u + 1 for a q unit) for a tile of up to MT
+// tokens of one sequence, per workgroup of NT threads: RW = HD (the split
+// engine, MT = kMtSplit) or, for calls too small to fill the chip, RW = 128 and
+// MT = 64 (the narrow tile: more, shorter workgroups).  grid: xcd_map(2 * RG *
+// n_units * B * tps) with RG = HD / RW row groups and tps = ceil(T / MT) tiles
+// per sequence; item = (((unit * B + b) * tps + tile) * 2 + half) * RG + rg, so
+// the row groups and the two halves of a tile are adjacent items on one XCD
+// (its L2 serves the tile's residual rows to all of them) and a unit's tiles
+// stay on one XCD.  Per element the arithmetic is the other engines' (the same
+// MFMA chain over d, staging, 1/rms and epilogue), so the K/V are
+// bit-identical.
+template <int HD, int MT, int NT, int RW, bool PACKED, bool FOLD>
+__global__ __launch_bounds__(NT, 1) void proj_split_kernel(ProjArgs a, int per_xcd, int tps, int n_units) {
   extern __shared__ __align__(16) char lds[];
-  constexpr int NT = split_nt(HD), MT = kMtSplit;
-  constexpr ProjLds PL = split_lds(HD, MT);
-  constexpr int KLD = split_ld(HD);
+  constexpr int RG = HD / RW;
+  constexpr ProjLds PL = split_lds(RW, MT);
+  constexpr int KLD = split_ld(RW);
+  static_assert(RG * RW == HD, "row groups");
   const int tid = threadIdx.x;
   const unsigned item = (blockIdx.x % kXcds) * (unsigned)per_xcd + blockIdx.x / kXcds;
   const unsigned n_tiles = (unsigned)a.B * (unsigned)tps;
-  if (item >= 2u * (unsigned)n_units * n_tiles) return;
-  const int half = (int)(item & 1u);
-  const unsigned ut = item >> 1;
+  if (item >= 2u * RG * (unsigned)n_units * n_tiles) return;
+  const int rg = (int)(item % RG);
+  const unsigned ih = item / RG;
+  const int half = (int)(ih & 1u);
+  const unsigned ut = ih >> 1;
   const int unit = (int)(ut / n_tiles);
   const unsigned rem = ut - (unsigned)unit * n_tiles;
   const int b = (int)(rem / (unsigned)tps);
@@ -157,8 +163,9 @@ __global__ __launch_bounds__(split_nt(HD), 1) void proj_split_kernel(ProjArgs a,
   const bool kv_mode = unit < a.n_kv_units;
   const int head = kv_mode ? unit : 2 * (unit - a.n_kv_units) + half;
   if (!kv_mode && head >= a.n_q) return;
-  const uint16_t* w = kv_mode ? static_cast<const uint16_t*>(half ? a.w_v : a.w_k) + head * hd_d
-                              : static_cast<const uint16_t*>(a.w_q) + head * hd_d;
+  const uint16_t* w = (kv_mode ? static_cast<const uint16_t*>(half ? a.w_v : a.w_k) + head * hd_d
+                               : static_cast<const uint16_t*>(a.w_q) + head * hd_d) +
+                      (size_t)rg * RW * a.d;
   const Half halves[2] = {Half{w, kv_mode ? 1 - half : 1}, Half{nullptr, 0}};
 
   double* rev = reinterpret_cast<double*>(lds + PL.rev);
@@ -172,21 +179,22 @@ __global__ __launch_bounds__(split_nt(HD), 1) void proj_split_kernel(ProjArgs a,
     su.store(nullptr, gam, rev);
     if (tid < MT) pos[tid] = a.pos0[b] + t0 + tid;
   };
-  WideTile<HD, MT, PACKED, FOLD, NT, KLD, true>::run(static_cast<const uint16_t*>(a.h) + ((size_t)b * a.h_ld + t0) * a.d, n,
+  // the row group's RoPE frequencies start at pair rg * RW / 2
+  WideTile<RW, MT, PACKED, FOLD, NT, KLD, true>::run(static_cast<const uint16_t*>(a.h) + ((size_t)b * a.h_ld + t0) * a.d, n,
                                                gam, static_cast<const uint16_t*>(a.gamma), a.d, a.eps, halves, hst,
-                                               rinv, pos, rev, kv, setup);
+                                               rinv, pos, rev + rg * (RW / 2), kv, setup);
   __syncthreads();
 
-  // store: 16-byte chunks of the tile's valid rows
-  constexpr int CPR = HD / 8;
+  // store: 16-byte chunks of the tile's valid rows (columns rg * RW ..)
+  constexpr int CPR = RW / 8;
   uint16_t* dst0;
   size_t row_stride;
   if (kv_mode) {
     dst0 = static_cast<uint16_t*>(half ? a.v_out : a.k_out) +
-           (((size_t)b * a.n_kv + head) * a.kv_t_cap + a.kv_t_off + t0) * HD;
+           (((size_t)b * a.n_kv + head) * a.kv_t_cap + a.kv_t_off + t0) * HD + rg * RW;
     row_stride = HD;
   } else {
-    dst0 = static_cast<uint16_t*>(a.q_out) + (((size_t)b * a.T + t0) * a.n_q + head) * HD;  // [B][T][n_q][hd]
+    dst0 = static_cast<uint16_t*>(a.q_out) + (((size_t)b * a.T + t0) * a.n_q + head) * HD + rg * RW;  // [B][T][n_q][hd]
     row_stride = (size_t)a.n_q * HD;
   }
   for (int c = tid; c < n * CPR; c += NT) {
@@ -1143,16 +1151,16 @@ static hipError_t proj_t(const ProjArgs& a, int n_units, hipStream_t st) {
   return hipGetLastError();
 }
 
-template <int HD, int L>
+template <int HD, int MT, int NT, int RW, int L>
 static hipError_t proj_split_t(const ProjArgs& a, int n_units, hipStream_t st) {
-  const size_t bytes = split_lds(HD, kMtSplit).end + gamma_lds_bytes(a.d);
+  const size_t bytes = split_lds(RW, MT).end + gamma_lds_bytes(a.d);
   static std::atomic<size_t> done{0};
-  auto k = proj_split_kernel<HD, L != 0, L == 2>;
+  auto k = proj_split_kernel<HD, MT, NT, RW, L != 0, L == 2>;
   hipError_t e = ensure_lds(k, bytes, done);
   if (e != hipSuccess) return e;
-  const int tps = (a.T + kMtSplit - 1) / kMtSplit;
-  const XcdMap m = xcd_map(2LL * n_units * a.B * tps);
-  hipLaunchKernelGGL(k, dim3(m.grid), dim3(split_nt(HD)), bytes, st, a, m.per, tps, n_units);
+  const int tps = (a.T + MT - 1) / MT;
+  const XcdMap m = xcd_map(2LL * (HD / RW) * n_units * a.B * tps);
+  hipLaunchKernelGGL(k, dim3(m.grid), dim3(NT), bytes, st, a, m.per, tps, n_units);
   return hipGetLastError();
 }
 
@@ -1289,10 +1297,19 @@ static hipError_t with_layout(int layout, const F& f) {
 }
 
 hipError_t launch_proj(const ProjArgs& a, int dtype_bf16, int hd, int layout, int n_units, hipStream_t st) {
+  if (dtype_bf16 && (hd == 128 || hd == 256) &&
+      narrow_prefill(2LL * (hd / kRwNarrow) * n_units * a.B * ((a.T + kMtNarrow - 1) / kMtNarrow))) {
+    return with_layout(layout, [&](auto lc) -> hipError_t {
+      constexpr int L = decltype(lc)::value;
+      return hd == 256 ? proj_split_t<256, kMtNarrow, kNtNarrow, kRwNarrow, L>(a, n_units, st)
+                       : proj_split_t<128, kMtNarrow, kNtNarrow, kRwNarrow, L>(a, n_units, st);
+    });
+  }
   if (dtype_bf16 && split_prefill(hd, a.T, 2LL * n_units * a.B * ((a.T + kMtSplit - 1) / kMtSplit))) {
     return with_layout(layout, [&](auto lc) -> hipError_t {
       constexpr int L = decltype(lc)::value;
-      return hd == 256 ? proj_split_t<256, L>(a, n_units, st) : proj_split_t<128, L>(a, n_units, st);
+      return hd == 256 ? proj_split_t<256, kMtSplit, split_nt(256), 256, L>(a, n_units, st)
+                       : proj_split_t<128, kMtSplit, split_nt(128), 128, L>(a, n_units, st);
     });
   }
 #define PB(H) with_layout(layout, [&](auto lc) { return proj_t<uint16_t, H, decltype(lc)::value>(a, n_units, st); })

@@ -61,6 +61,16 @@ constexpr int split_ld(int hd) { return hd + 8; }
 constexpr bool split_prefill(int hd, int T, long long wgs) {
   return T >= kMtSplit / 2 && (hd == 256 || (hd == 128 && wgs >= 512));
 }
+// The narrow tile of the split engine: 128 rows of one half for 64 tokens, 4
+// waves of one 32-row block each, for prefill / recompute calls whose grid of
+// narrow tiles (wgs workgroups) holds at most kNarrowMaxWgs: calls too small to
+// fill the chip with larger tiles (the evicted-token recomputes of a decode
+// step), where each workgroup's K-loop over d_model, not the work, sets the time.
+constexpr int kMtNarrow = 64;
+constexpr int kNtNarrow = 256;
+constexpr int kRwNarrow = 128;
+constexpr long long kNarrowMaxWgs = 512;
+constexpr bool narrow_prefill(long long wgs) { return wgs <= kNarrowMaxWgs; }
 
 // A stored tail of at most fold_rows<T>() rows (a decode step's current token)
 // joins the split of the last recomputed tile of a fused call: the rows are
@@ -232,11 +242,11 @@ constexpr int kStreamDepth = 10;
 // and wins up to two of them (Gemma-3-4B shape: 128 tokens in 36 us; Qwen2.5-
 // 1.5B shape: 512 tokens in 21 us).
 constexpr long long kStreamRecomputeMaxWgs = 512;
-// head_dim 256: the tile engine's workgroup does twice the work (512 K|V rows)
-// and takes 55-59 us at d 2560, so two more rounds of the streaming kernel still
-// win (its token groups are 11 rows there, LDS-bound: 128 tokens are 768
-// workgroups, 36 us; 192 tokens 1152 workgroups, 47 us).
-constexpr long long kStreamRecomputeMaxWgsHd256 = 1024;
+// head_dim 256: against the split engine's narrow tiles (about 35 us for any
+// recompute of up to ~1000 tokens at d 2560, measured) the streaming kernel
+// wins up to ~100 tokens (its token groups are 11 rows there, LDS-bound: 64
+// tokens are 384 workgroups, 24 us; 128 tokens 768 workgroups, 35 us).
+constexpr long long kStreamRecomputeMaxWgsHd256 = 640;
 constexpr size_t kStreamSlotBytes = (size_t)32 * kKT * 2 * kStreamChunk;
 struct StreamLds {
   size_t rev, rinv, pos, gam, ring, hb, hs, end;
