@@ -550,7 +550,11 @@ struct WideTile {
   // weight K-steps in flight: a split wave of one 32-row block holds 4 (its
   // A fragments are half the 8-wave layout's per step)
   static constexpr int DW = SPLIT && NB_F == 1 ? 4 : 2;
-  static constexpr int DH = 2, DL = kDepth;
+  // residual K-steps in registers: a split wave of one 32-row block has so
+  // little work per K-step that one step of lead does not cover the load
+  // latency, so it keeps two steps in flight
+  static constexpr int DH = SPLIT && NB_F == 1 ? 2 : 1;
+  static constexpr int DL = kDepth;
   static constexpr int SLOT = NB_T * 4 * 512;  // elements per LDS slot (one K-step)
   static constexpr int NU = 4 * NB_T;          // units (substep, token block) per K-step
   // VALU instructions the schedule interleaves after each MFMA of the first
@@ -739,7 +743,7 @@ struct WideTile {
       constexpr int LN = (L + 1) & 3;
       constexpr bool GUARD = decltype(guard_c)::value;
       const int sw = GUARD ? min(s + DW, nsteps - 1) : s + DW;
-      const int sh = GUARD ? min(s + 2, nsteps - 1) : s + 2;
+      const int sh = GUARD ? min(s + 1 + DH, nsteps - 1) : s + 1 + DH;
       auto unit = [&](auto kc) {
         constexpr int k = decltype(kc)::value;
         constexpr int u = k / NB_T, bt = k % NB_T, kk = k + RA;
@@ -749,7 +753,7 @@ struct WideTile {
         for (int bf = 0; bf < NB_F; ++bf)
           acc[bf][bt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(A[LW][bf][u], bq[k % NBQ], acc[bf][bt], 0, 0, 0);
         if constexpr (bt == NB_T - 1) load_wu(LW, sw, u);
-        if constexpr (k == NB_T - 1) load_h(0, sh);
+        if constexpr (k == NB_T - 1) load_h((L + 1) % DH, sh);
         if (!GUARD) {
           __builtin_amdgcn_sched_group_barrier(0x100, k == 0 ? 2 : 1, 0);  // DS read: B fragment (gamma)
 #pragma unroll
@@ -763,7 +767,7 @@ struct WideTile {
       };
       __builtin_amdgcn_sched_barrier(0);
       if (!GUARD || s + 1 < nsteps)
-        put_hv(LN, 0, FOLD ? uint4{} : *reinterpret_cast<const uint4*>(gam + (size_t)(s + 1) * kKT + 8 * sub));
+        put_hv(LN, (L + 1) % DH, FOLD ? uint4{} : *reinterpret_cast<const uint4*>(gam + (size_t)(s + 1) * kKT + 8 * sub));
       [&]<int... K>(std::integer_sequence<int, K...>) { (unit(IC<K>{}), ...); }(std::make_integer_sequence<int, NU / 2>{});
       __builtin_amdgcn_sched_barrier(0);
       __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): this wave's staged chunks are in LDS
@@ -787,7 +791,9 @@ struct WideTile {
       for (int u = 0; u < 4; ++u) load_wu(i, min(i, nsteps - 1), u);
     setup();
     put_hv(0, 0, g0);
-    load_h(0, min(1, nsteps - 1));
+    // steps 1 .. DH into slots 1 % DH .. DH % DH
+#pragma unroll
+    for (int i = 1; i <= DH; ++i) load_h(i % DH, min(i, nsteps - 1));
     __syncthreads();
 #pragma unroll
     for (int k = 0; k < RA; ++k) bq[k] = rd1(0, k / NB_T, k % NB_T);
