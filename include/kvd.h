@@ -213,8 +213,11 @@ kvd_status kvd_cached_attn(const kvd_attn_shape* shape, const void* q, const kvd
  *     the call has at least 256 of them (B * n_kv_heads * ceil(T_rec / 128)
  *     >= 256: a full round of the chip);
  *   - split (bf16, head_dim 128 / 256, T_rec >= 1, T_tail <= 4, at most 256
- *     chunks per sequence), only when asked for with KVD_FUSED_SPLIT:
- *     each 128-token chunk runs as two workgroups, one recomputing its K rows
+ *     chunks per sequence) with 64-token chunks when 64-token tiles of both
+ *     halves would fill at most 128 compute units (B * n_kv_heads *
+ *     ceil(T_rec / 64) <= 128: sliding-window layers, short contexts), or when
+ *     asked for (KVD_FUSED_SPLIT64; KVD_FUSED_SPLIT for 128-token chunks):
+ *     each chunk runs as two workgroups, one recomputing its K rows
  *     and taking the scores and softmax, one recomputing its V rows and, once
  *     the first has published the probabilities through the workspace, the
  *     P V products.  The second waits for the first with a bounded wait
@@ -395,14 +398,16 @@ int32_t kvd_set_attn_workgroups(int32_t target);
 /* Tuning of kvd_fused_recompute_attn and kvd_fused_window_attn: the recomputed
  * tokens per workgroup.  0 (the default) chooses per call, 128 asks for the
  * wide engine wherever it exists (bf16, head_dim 128 / 256, its LDS within
- * the limit; elsewhere 64 is used), KVD_FUSED_SPLIT for the split engine
- * wherever a call can run on it (elsewhere 64), 64 for the 64-token tiles;
+ * the limit; elsewhere 64 is used), KVD_FUSED_SPLIT / KVD_FUSED_SPLIT64 for
+ * the split engine with 128- / 64-token chunks wherever a call can run on it
+ * (elsewhere 64), 64 for the 64-token tiles;
  * other values mean 0.  Returns the previous setting.  Process-wide: it
  * changes kvd_num_splits of KVD_OP_FUSED (not kvd_workspace_bytes, which
  * covers every engine).  All engines give K/V bit-identical to
  * kvd_recompute_kv; the attention output differs by rounding only (other
  * split boundaries).                                                         */
 #define KVD_FUSED_SPLIT (-128)
+#define KVD_FUSED_SPLIT64 (-64)
 int32_t kvd_set_fused_tokens(int32_t tokens);
 
 const char* kvd_status_str(kvd_status status);

@@ -152,21 +152,20 @@ FusedPlan wide_plan(int32_t T_rec, int32_t T_tail) {
   return p;
 }
 
-// The split engine: bf16 at head_dim 128 / 256, recomputed rows, a tail that
-// folds (at most fold_rows rows), at most kSplitMaxChunks chunks per sequence,
-// and its LDS within the limit.
-bool split_supported(const kvd_attn_shape* s, int32_t T_rec, int32_t T_tail) {
+// The split engine with mt-token chunks: bf16 at head_dim 128 / 256,
+// recomputed rows, a tail that folds (at most fold_rows rows), at most
+// kSplitMaxChunks chunks per sequence, and its LDS within the limit.
+bool split_supported(const kvd_attn_shape* s, int32_t T_rec, int32_t T_tail, int32_t mt) {
   if (s->dtype != KVD_BF16 || (s->head_dim != 128 && s->head_dim != 256)) return false;
-  if (T_rec < 1 || T_tail > kvd::fold_rows<uint16_t>() || ceil_div(T_rec, kvd::kMtSplit) > kvd::kSplitMaxChunks)
-    return false;
-  return kvd::fused_split_lds_bytes(s->n_q_heads / s->n_kv_heads, s->head_dim) +
+  if (T_rec < 1 || T_tail > kvd::fold_rows<uint16_t>() || ceil_div(T_rec, mt) > kvd::kSplitMaxChunks) return false;
+  return kvd::fused_split_lds_bytes(s->n_q_heads / s->n_kv_heads, s->head_dim, mt) +
              kvd::gamma_lds_bytes(s->d_model) <= kvd::kLdsPerGroup;
 }
 
-FusedPlan split_plan(int32_t T_rec) {
+FusedPlan split_plan(int32_t T_rec, int32_t mt) {
   FusedPlan p{};
-  p.engine = kvd::kFusedSplit;
-  p.mt = kvd::kMtSplit;
+  p.engine = mt == 64 ? kvd::kFusedSplit64 : kvd::kFusedSplit;
+  p.mt = mt;
   p.n_rec = ceil_div(T_rec, p.mt);
   p.n_tail = 0;
   p.S = p.n_rec;
@@ -174,20 +173,29 @@ FusedPlan split_plan(int32_t T_rec) {
 }
 
 // Wide tiles when supported and the call has at least kWideMinTiles of them (a
-// full round of the chip), else 64-token tiles.  The split engine runs only
-// when asked for: on MI355X, in a 34-layer decode step (Gemma-3-4B shape, B = 1,
-// 4096 keys; B = 2, 2048 keys) its launches took 58-61 us against 56-57 us on
-// 64-token tiles (its K-loop is no faster, and the K-to-V exchange adds a
-// round trip).  kvd_set_fused_tokens forces an engine (where it exists).
+// full round of the chip); the split engine with 64-token chunks when 64-token
+// tiles of both halves would fill at most kSplit64MaxTiles CUs (twice the
+// workgroups, each with half the rows); else 64-token tiles.  With 128-token
+// chunks the split engine runs only when asked for: on MI355X, in a 34-layer
+// decode step (Gemma-3-4B shape, B = 1, 4096 keys; B = 2, 2048 keys) its
+// launches took 58-61 us against 56-57 us on 64-token tiles (its K-loop is no
+// faster, and the K-to-V exchange adds a round trip).  kvd_set_fused_tokens
+// forces an engine (where it exists).
 FusedPlan fused_plan(const kvd_attn_shape* s, int32_t B, int32_t T_rec, int32_t T_tail) {
   const int32_t mode = g_fused_tokens.load(std::memory_order_relaxed);
   const bool wide_ok = T_rec > 0 && wide_supported(s);
   if (mode == kvd::kMtBf16) return narrow_plan(s, T_rec, T_tail);
   if (mode == kvd::kMtWide) return wide_ok ? wide_plan(T_rec, T_tail) : narrow_plan(s, T_rec, T_tail);
   if (mode == KVD_FUSED_SPLIT)
-    return split_supported(s, T_rec, T_tail) ? split_plan(T_rec) : narrow_plan(s, T_rec, T_tail);
+    return split_supported(s, T_rec, T_tail, kvd::kMtSplit) ? split_plan(T_rec, kvd::kMtSplit)
+                                                             : narrow_plan(s, T_rec, T_tail);
+  if (mode == KVD_FUSED_SPLIT64)
+    return split_supported(s, T_rec, T_tail, 64) ? split_plan(T_rec, 64) : narrow_plan(s, T_rec, T_tail);
   if (wide_ok && (int64_t)B * s->n_kv_heads * ceil_div(T_rec, kvd::kMtWide) >= kvd::kWideMinTiles)
     return wide_plan(T_rec, T_tail);
+  if (split_supported(s, T_rec, T_tail, 64) &&
+      (int64_t)B * s->n_kv_heads * ceil_div(T_rec, 64) <= kvd::kSplit64MaxTiles)
+    return split_plan(T_rec, 64);
   return narrow_plan(s, T_rec, T_tail);
 }
 
@@ -217,12 +225,13 @@ size_t ws_done_bytes(const kvd_attn_shape* s, int32_t B) {
 size_t ws_total(const kvd_attn_shape* s, int32_t B, int32_t S) {
   return ws_done_bytes(s, B) + ws_acc_bytes(s, B, S) + ws_ml_bytes(s, B, S);
 }
-size_t ws_xch_bytes(const kvd_attn_shape* s, int32_t B, int32_t n_rec) {
-  return kvd::align_up((size_t)B * s->n_kv_heads * n_rec * kvd::split_xf(s->n_q_heads / s->n_kv_heads) * sizeof(float),
-                       256);
+bool is_split(const FusedPlan& p) { return p.engine == kvd::kFusedSplit || p.engine == kvd::kFusedSplit64; }
+size_t ws_xch_bytes(const kvd_attn_shape* s, int32_t B, const FusedPlan& p) {
+  return kvd::align_up(
+      (size_t)B * s->n_kv_heads * p.n_rec * kvd::split_xf(s->n_q_heads / s->n_kv_heads, p.mt) * sizeof(float), 256);
 }
 size_t ws_plan_bytes(const kvd_attn_shape* s, int32_t B, const FusedPlan& p) {
-  return ws_total(s, B, p.S) + (p.engine == kvd::kFusedSplit ? ws_xch_bytes(s, B, p.n_rec) : 0);
+  return ws_total(s, B, p.S) + (is_split(p) ? ws_xch_bytes(s, B, p) : 0);
 }
 float* ws_acc_ptr(const kvd_attn_shape* s, int32_t B, void* ws) {
   return reinterpret_cast<float*>(static_cast<char*>(ws) + ws_done_bytes(s, B));
@@ -491,8 +500,8 @@ kvd_status fused_launch(const kvd_attn_shape* shape, const void* q, const void* 
   if ((int64_t)shape->n_kv_heads * B * S > INT32_MAX - 8)
     return fail(KVD_ERR_SHAPE, "%s: n_kv_heads * B * splits = %lld workgroups is too many", name,
                 (long long)shape->n_kv_heads * B * S);
-  const bool split = plan.engine == kvd::kFusedSplit;
-  KVD_TRY(check_ws(shape, B, S, ws, ws_bytes, split ? ws_xch_bytes(shape, B, plan.n_rec) : 0));
+  const bool split = is_split(plan);
+  KVD_TRY(check_ws(shape, B, S, ws, ws_bytes, split ? ws_xch_bytes(shape, B, plan) : 0));
   kvd::FusedArgs a{};
   a.q = q;
   a.h = h;
@@ -520,7 +529,7 @@ kvd_status fused_launch(const kvd_attn_shape* shape, const void* q, const void* 
   if (split) {
     a.ws_bits = reinterpret_cast<unsigned long long*>(static_cast<char*>(ws) + ws_ctr_bytes(shape, B));
     a.xch = reinterpret_cast<float*>(static_cast<char*>(ws) + ws_total(shape, B, S));
-    a.xf = kvd::split_xf(shape->n_q_heads / shape->n_kv_heads);
+    a.xf = kvd::split_xf(shape->n_q_heads / shape->n_kv_heads, plan.mt);
   }
   a.out = out;
   a.d = shape->d_model;
@@ -883,7 +892,8 @@ int32_t kvd_set_attn_workgroups(int32_t target) {
 }
 
 int32_t kvd_set_fused_tokens(int32_t tokens) {
-  if (tokens != kvd::kMtBf16 && tokens != kvd::kMtWide && tokens != KVD_FUSED_SPLIT) tokens = 0;
+  if (tokens != kvd::kMtBf16 && tokens != kvd::kMtWide && tokens != KVD_FUSED_SPLIT && tokens != KVD_FUSED_SPLIT64)
+    tokens = 0;
   return g_fused_tokens.exchange(tokens, std::memory_order_relaxed);
 }
 
@@ -895,7 +905,9 @@ size_t kvd_workspace_bytes(const kvd_attn_shape* shape, int32_t op, int32_t B, i
   if (op == KVD_OP_FUSED) {
     size_t n = ws_plan_bytes(shape, B, narrow_plan(shape, T_main, T_tail));
     if (T_main > 0 && wide_supported(shape)) n = std::max(n, ws_plan_bytes(shape, B, wide_plan(T_main, T_tail)));
-    if (split_supported(shape, T_main, T_tail)) n = std::max(n, ws_plan_bytes(shape, B, split_plan(T_main)));
+    if (split_supported(shape, T_main, T_tail, kvd::kMtSplit))
+      n = std::max(n, ws_plan_bytes(shape, B, split_plan(T_main, kvd::kMtSplit)));
+    if (split_supported(shape, T_main, T_tail, 64)) n = std::max(n, ws_plan_bytes(shape, B, split_plan(T_main, 64)));
     return n;
   }
   return ws_total(shape, B, S);

@@ -646,10 +646,11 @@ __global__ __launch_bounds__(kNtWide, 1) void fused_wide_kernel(
 // tail (T_tail <= fold rows: the current token) joins the last chunk, its K
 // rows in the K role's tile and its V rows in the V role's.  grid:
 // xcd_map(2 * n_kv * B * n_rec), items ordered as fused_body's chunks.
-template <int HD, bool PACKED, bool FOLD>
+template <int HD, int MT, bool PACKED, bool FOLD>
 __global__ __launch_bounds__(split_nt(HD), 1) void fused_split_kernel(FusedArgs a, int per_xcd, int hg) {
   extern __shared__ __align__(16) char lds[];
-  constexpr int NT = split_nt(HD), MT = kMtSplit, FR = fold_rows<uint16_t>();
+  constexpr int NT = split_nt(HD), FR = fold_rows<uint16_t>();
+  constexpr int KPL = (MT + FR + 63) / 64;  // keys per lane of the tile attention
   constexpr ProjLds PL = split_lds(HD, MT, FR);
   constexpr int KLD = split_ld(HD);
   constexpr int CPR = HD / 8;  // 16-byte chunks of a K (or V) row
@@ -726,7 +727,7 @@ __global__ __launch_bounds__(split_nt(HD), 1) void fused_split_kernel(FusedArgs 
   float* xrec = a.xch + (((size_t)b * a.n_kv + j) * C + c) * a.xf;
   unsigned long long* bits = a.ws_bits + ((size_t)b * a.n_kv + j) * kSplitBitWords;
   if (role == 0) {
-    attend_scores<uint16_t, HD, NT, 3, KLD>(tile, nk, ROWS, g, lds, AL);
+    attend_scores<uint16_t, HD, NT, KPL, KLD>(tile, nk, ROWS, g, lds, AL);
     for (int i = tid; i < g * ROWS; i += NT) store_dev(xrec + i, S[i]);
     if (tid < 2 * g) store_dev(xrec + g * ROWS + tid, ml[tid]);
     __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0): this thread's record stores are complete
@@ -1214,11 +1215,11 @@ static hipError_t fused_wide_t(const FusedArgs& a, hipStream_t st) {
   return hipGetLastError();
 }
 
-template <int HD, int L>
+template <int HD, int MT, int L>
 static hipError_t fused_split_t(const FusedArgs& a, hipStream_t st) {
-  const size_t bytes = fused_split_lds_bytes(a.n_q / a.n_kv, HD) + gamma_lds_bytes(a.d);
+  const size_t bytes = fused_split_lds_bytes(a.n_q / a.n_kv, HD, MT) + gamma_lds_bytes(a.d);
   static std::atomic<size_t> done{0};
-  auto k = fused_split_kernel<HD, L != 0, L == 2>;
+  auto k = fused_split_kernel<HD, MT, L != 0, L == 2>;
   hipError_t e = ensure_lds(k, bytes, done);
   if (e != hipSuccess) return e;
   // items in pairs: an even count per XCD keeps each pair on one XCD
@@ -1345,13 +1346,14 @@ hipError_t launch_project_current(const ProjArgs& a, int dtype_bf16, int hd, int
 }
 
 hipError_t launch_fused(const FusedArgs& a, int dtype_bf16, int hd, int layout, int engine, hipStream_t st) {
-  if (engine == kFusedSplit) {
+  if (engine == kFusedSplit || engine == kFusedSplit64) {
     if (!dtype_bf16) return hipErrorInvalidValue;
+    const bool m64 = engine == kFusedSplit64;
     return with_layout(layout, [&](auto lc) -> hipError_t {
       constexpr int L = decltype(lc)::value;
       switch (hd) {
-        case 128: return fused_split_t<128, L>(a, st);
-        case 256: return fused_split_t<256, L>(a, st);
+        case 128: return m64 ? fused_split_t<128, 64, L>(a, st) : fused_split_t<128, kMtSplit, L>(a, st);
+        case 256: return m64 ? fused_split_t<256, 64, L>(a, st) : fused_split_t<256, kMtSplit, L>(a, st);
         default: return hipErrorInvalidValue;
       }
     });

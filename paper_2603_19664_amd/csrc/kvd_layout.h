@@ -46,9 +46,14 @@ constexpr int kSplitMaxChunks = 64 * kSplitBitWords;
 // Polls of the V role's bounded wait (about 0.1 s); past it the chunk's partial
 // is written as NaN, so the call's output shows the failure.
 constexpr unsigned kSplitSpinLimit = 1u << 17;
-// Floats of one chunk's exchange record for group size g (rows: kMtSplit plus
-// a folded tail of up to 4, fold_rows).
-constexpr int split_xf(int g) { return (g * (kMtSplit + 4) + 2 * g + 3) / 4 * 4; }
+// Floats of one chunk's exchange record for group size g and mt-token chunks
+// (rows: mt plus a folded tail of up to 4, fold_rows).
+constexpr int split_xf(int g, int mt) { return (g * (mt + 4) + 2 * g + 3) / 4 * 4; }
+// The fused call takes 64-token chunks on the split engine when its 64-token
+// grid of both halves (n_kv * B * ceil(T_rec / 64) workgroups) would fill at most
+// this many CUs (half the chip): sliding-window layers and short contexts at
+// small batch, where each workgroup's K-loop over d_model sets the time.
+constexpr long long kSplit64MaxTiles = 128;
 constexpr int split_ld(int hd) { return hd + 8; }
 // Prefill / recompute (kvd_recompute_kv, the block forward's projections) runs
 // on the split engine for bf16 at head_dim 256, and at head_dim 128 when its
@@ -212,8 +217,8 @@ constexpr size_t fused_lds_bytes(int g, int hd, int mt) {
   return attn_lds(proj_lds<T>(hd, mt, fold_rows<T>()).end, g, hd, mt + fold_rows<T>()).end;
 }
 // The fused kernel on the split engine: a folded tail of up to fold rows.
-constexpr size_t fused_split_lds_bytes(int g, int hd) {
-  return attn_lds(split_lds(hd, kMtSplit, 4).end, g, hd, kMtSplit + 4).end;
+constexpr size_t fused_split_lds_bytes(int g, int hd, int mt) {
+  return attn_lds(split_lds(hd, mt, 4).end, g, hd, mt + 4).end;
 }
 // The wide fused kernel: 128-key tiles plus a folded tail.
 constexpr size_t fused_wide_lds_bytes(int g, int hd) {

@@ -24,7 +24,8 @@ KVD_OK, KVD_ERR_NULL, KVD_ERR_SHAPE, KVD_ERR_UNSUPPORTED, KVD_ERR_WORKSPACE, KVD
 KVD_F32, KVD_BF16 = 0, 1
 KVD_W_ROWMAJOR, KVD_W_PACKED, KVD_W_PACKED_GAMMA = 0, 1, 2
 KVD_OP_DECODE_ATTN, KVD_OP_CACHED_ATTN, KVD_OP_FUSED = 0, 1, 2
-KVD_FUSED_SPLIT = -128  # kvd_set_fused_tokens: the split engine
+KVD_FUSED_SPLIT = -128  # kvd_set_fused_tokens: the split engine, 128-token chunks
+KVD_FUSED_SPLIT64 = -64  # the split engine, 64-token chunks
 
 _DTYPES = {KVD_F32: torch.float32, KVD_BF16: torch.bfloat16}
 

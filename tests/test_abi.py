@@ -205,19 +205,26 @@ def test_split_policy_and_workspace():
 def _engine(s, B, T_rec, T_tail, tokens):
     """The fused call's engine as documented: 128-token wide tiles (bf16, head_dim 128 /
     256) when forced or when there are at least 256 of them; the split engine (bf16,
-    head_dim 128 / 256, T_rec >= 1, T_tail <= 4, <= 256 chunks) only when forced; else
+    head_dim 128 / 256, T_rec >= 1, T_tail <= 4, <= 256 chunks) with 64-token chunks when
+    64-token tiles would number at most 128, or when forced (either chunk size); else
     64-token tiles."""
     big = s.dtype == kvd.KVD_BF16 and s.head_dim in (128, 256)
     wide_ok = big and T_rec > 0
-    split_ok = big and T_rec > 0 and T_tail <= 4 and -(-T_rec // 128) <= 256
+
+    def split_ok(mt):
+        return big and T_rec > 0 and T_tail <= 4 and -(-T_rec // mt) <= 256
     if tokens == 64:
         return "tile64"
     if tokens == 128:
         return "wide" if wide_ok else "tile64"
     if tokens == kvd.KVD_FUSED_SPLIT:
-        return "split" if split_ok else "tile64"
+        return "split" if split_ok(128) else "tile64"
+    if tokens == kvd.KVD_FUSED_SPLIT64:
+        return "split64" if split_ok(64) else "tile64"
     if wide_ok and B * s.n_kv_heads * -(-T_rec // 128) >= 256:
         return "wide"
+    if split_ok(64) and B * s.n_kv_heads * -(-T_rec // 64) <= 128:
+        return "split64"
     return "tile64"
 
 
@@ -241,14 +248,16 @@ def _fused_splits(s, B, T_rec, T_tail, tokens, engine=None):
         return n_rec + _tail_tiles(s, n_rec, T_tail)
     if engine == "split":
         return -(-T_rec // 128)
+    if engine == "split64":
+        return -(-T_rec // 64)
     n_rec = -(-T_rec // 64)
     return n_rec + _tail_tiles(s, n_rec, T_tail)
 
 
-def _ws_bytes(s, B, S, split_chunks=0):
+def _ws_bytes(s, B, S, split_chunks=0, mt=128):
     up = lambda x: -(-x // 256) * 256  # noqa: E731
     g = s.n_q_heads // s.n_kv_heads
-    xf = -(-(g * 132 + 2 * g) // 4) * 4
+    xf = -(-(g * (mt + 4) + 2 * g) // 4) * 4
     return (up(B * s.n_kv_heads * 8) + up(B * s.n_kv_heads * 4 * 8) + up(B * s.n_q_heads * S * s.head_dim * 4)
             + up(B * s.n_q_heads * S * 2 * 4) + (up(B * s.n_kv_heads * split_chunks * xf * 4) if split_chunks else 0))
 
@@ -261,6 +270,8 @@ def _fused_ws_bytes(s, B, T, Tt):
         n = max(n, _ws_bytes(s, B, _fused_splits(s, B, T, Tt, 0, "wide")))
     if big and Tt <= 4 and -(-T // 128) <= 256:
         n = max(n, _ws_bytes(s, B, -(-T // 128), -(-T // 128)))
+    if big and Tt <= 4 and -(-T // 64) <= 256:
+        n = max(n, _ws_bytes(s, B, -(-T // 64), -(-T // 64), mt=64))
     return n
 
 
@@ -275,10 +286,12 @@ def test_fused_tiling_policy():
     assert ns(gemma, 8, 2048, 1) == 16
     assert ns(gemma, 1, 3072, 1025) == 48 + 16  # a stored window of 1024 + the current token: 16 tail tiles
     assert ns(gemma, 1, 4096, 5) == 65        # a 5-row tail cannot fold: 64-token tiles + a tail tile
+    assert ns(gemma, 1, 2048, 1) == 32        # 128 64-token tiles: split engine, 64-token chunks
+    assert ns(gemma, 1, 1023, 1) == 16        # a sliding window at B = 1
     assert ns(qwen, 8, 16384, 1) == 128
     try:
-        for tokens in (0, 64, 128, kvd.KVD_FUSED_SPLIT):
-            assert lib.kvd_set_fused_tokens(tokens) in (0, 64, 128, kvd.KVD_FUSED_SPLIT)
+        for tokens in (0, 64, 128, kvd.KVD_FUSED_SPLIT, kvd.KVD_FUSED_SPLIT64):
+            assert lib.kvd_set_fused_tokens(tokens) in (0, 64, 128, kvd.KVD_FUSED_SPLIT, kvd.KVD_FUSED_SPLIT64)
             for sh in [gemma, qwen] + others:
                 for B, T, Tt in [(1, 4096, 1), (2, 4096, 1), (8, 2048, 1), (1, 100, 1), (1, 0, 3), (3, 130, 70),
                                  (16, 5120, 0), (1, 64, 4), (1, 64, 5), (1, 32769, 1)]:
@@ -292,7 +305,7 @@ def test_fused_tiling_policy():
         for B in (1, 2, 8):
             sizes = [lib.kvd_workspace_bytes(ctypes.byref(gemma), kvd.KVD_OP_FUSED, B, T, 1) for T in range(1, 5000, 13)]
             assert sizes == sorted(sizes)
-        assert lib.kvd_set_fused_tokens(128) == kvd.KVD_FUSED_SPLIT  # the loop's last setting
+        assert lib.kvd_set_fused_tokens(128) == kvd.KVD_FUSED_SPLIT64  # the loop's last setting
         assert lib.kvd_set_fused_tokens(77) == 128  # other values mean 0
         assert lib.kvd_set_fused_tokens(0) == 0
     finally:

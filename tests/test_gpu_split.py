@@ -1,9 +1,10 @@
 """GPU parity of the split fused engine (bf16, head_dim 128 / 256): each
 128-token chunk runs as two workgroups, one recomputing the K rows and taking
 the scores and softmax, one recomputing the V rows and taking P V once the
-first has published the probabilities.  Forced with
-kvd_set_fused_tokens(KVD_FUSED_SPLIT) on small shapes that span several chunks
-and a ragged one, and on the Gemma-3-4B layer shape.
+first has published the probabilities, with 128- or 64-token chunks.  Forced with
+kvd_set_fused_tokens(KVD_FUSED_SPLIT / KVD_FUSED_SPLIT64) on small shapes that
+span several chunks and a ragged one, and on the Gemma-3-4B layer shape; the
+64-token chunks are also reached by the automatic policy on small grids.
 
 - The K/V each role recomputes (dumped through kv_debug) are bit-identical to
   the prefill K/V of kvd_recompute_kv (Prop. reconstruction: the same MFMA
@@ -31,6 +32,7 @@ pytestmark = pytest.mark.gpu
 BF = kvd.KVD_BF16
 TOL_BF = TOL[BF]
 SPLIT = kvd.KVD_FUSED_SPLIT
+MODES = [(kvd.KVD_FUSED_SPLIT, 128), (kvd.KVD_FUSED_SPLIT64, 64)]
 
 
 @pytest.fixture(autouse=True)
@@ -66,15 +68,16 @@ def _counters_clear(ws, L):
     assert int(torch.count_nonzero(ws[:n])) == 0
 
 
+@pytest.mark.parametrize("mode,mt", MODES)
 @pytest.mark.parametrize("hd", [128, 256])
 @pytest.mark.parametrize("packed", [False, True, "gamma"])
 @pytest.mark.parametrize("T", [1, 128, 300])
-def test_split_kv_bitwise_and_output(hd, packed, T):
+def test_split_kv_bitwise_and_output(mode, mt, hd, packed, T):
     L = _layer(hd, T, seed=180 + T + hd, packed=packed)
     s = L.shape
     Kp, Vp = gpu_recompute(L)
-    kvd.kvd_set_fused_tokens(SPLIT)
-    assert kvd.kvd_num_splits(s, kvd.KVD_OP_FUSED, L.B, T, 1) == -(-T // 128)
+    kvd.kvd_set_fused_tokens(mode)
+    assert kvd.kvd_num_splits(s, kvd.KVD_OP_FUSED, L.B, T, 1) == -(-T // mt)
     q, _, out, (dk, dv) = gpu_fused(L, kv_debug=True)
     assert torch.equal(_bits(dk), _bits(Kp)) and torch.equal(_bits(dv), _bits(Vp))
     check("split fused vs oracle", out, oracle_decode(L))
@@ -84,9 +87,10 @@ def test_split_kv_bitwise_and_output(hd, packed, T):
     check("split vs 64-token tiles", out, f64(out64))
 
 
+@pytest.mark.parametrize("mode,mt", MODES)
 @pytest.mark.parametrize("hd", [128, 256])
-@pytest.mark.parametrize("T_rec,T", [(130, 133), (128, 131), (256, 257), (300, 302), (1, 4)])
-def test_split_folded_stored_tail(hd, T_rec, T):
+@pytest.mark.parametrize("T_rec,T", [(130, 133), (128, 131), (256, 257), (300, 302), (1, 4), (64, 67)])
+def test_split_folded_stored_tail(mode, mt, hd, T_rec, T):
     # recompute the oldest T_rec context rows; the newer context rows and the
     # current token (T + 1 - T_rec <= 4 rows) are a stored tail folded into the
     # last chunk, also when that chunk is partial (its rows move down in LDS)
@@ -95,13 +99,13 @@ def test_split_folded_stored_tail(hd, T_rec, T):
     q, K, V, out_u = gpu_unfused(L)
     T_tail = T - T_rec + 1
     assert T_tail <= 4
-    kvd.kvd_set_fused_tokens(SPLIT)
+    kvd.kvd_set_fused_tokens(mode)
 
     def fused(out, ws):
         kvd.kvd_fused_recompute_attn(s, q, L.h, T_rec, L.gamma, L.lw_k, L.lw_v, L.pos0, out, ws, K, V, T_tail, T_rec)
 
     S = kvd.kvd_num_splits(s, kvd.KVD_OP_FUSED, L.B, T_rec, T_tail)
-    assert S == -(-T_rec // 128)
+    assert S == -(-T_rec // mt)
     ws = kvd.workspace(s, kvd.KVD_OP_FUSED, L.B, T_rec, T_tail)
     out = torch.empty_like(q)
     fused(out, ws)
@@ -118,7 +122,8 @@ def test_split_folded_stored_tail(hd, T_rec, T):
     _counters_clear(ws, L)
 
 
-def test_split_ring_tail():
+@pytest.mark.parametrize("mode", [m for m, _ in MODES])
+def test_split_ring_tail(mode):
     # Algorithm 1's bounded cache as a ring: the 2 newest context rows and the
     # current token in a ring of 3 slots whose oldest slot is 2, so the tail
     # view wraps; the older 298 rows are recomputed on the split engine
@@ -131,7 +136,7 @@ def test_split_ring_tail():
     for i in range(n_tail):
         ring_k[:, :, (off + i) % n_tail] = K[:, :, T_rec + i]
         ring_v[:, :, (off + i) % n_tail] = V[:, :, T_rec + i]
-    kvd.kvd_set_fused_tokens(SPLIT)
+    kvd.kvd_set_fused_tokens(mode)
     out = torch.empty_like(q)
     ws = kvd.workspace(s, kvd.KVD_OP_FUSED, L.B, T_rec, n_tail)
     kvd.kvd_fused_recompute_attn(s, q, L.h, T_rec, L.gamma, L.lw_k, L.lw_v, L.pos0, out, ws, ring_k, ring_v, n_tail,
@@ -149,7 +154,8 @@ def test_split_shared_workspace_across_lengths():
     tk, tv = empty_kv(L, 1)
     q = torch.empty((L.B, s.n_q_heads, s.head_dim), dtype=s.torch_dtype, device="cuda")
     kvd.kvd_project_qkv(s, L.h_new, L.gamma, L.lw_q, L.lw_k, L.lw_v, L.pos_new, q, tk, tv, 0)
-    for mode, T_rec in [(SPLIT, 700), (64, 700), (SPLIT, 300), (128, 650), (SPLIT, 129), (SPLIT, 700)]:
+    for mode, T_rec in [(SPLIT, 700), (64, 700), (kvd.KVD_FUSED_SPLIT64, 300), (128, 650), (SPLIT, 129),
+                        (kvd.KVD_FUSED_SPLIT64, 700), (SPLIT, 700)]:
         kvd.kvd_set_fused_tokens(mode)
         out = torch.empty_like(q)
         kvd.kvd_fused_recompute_attn(s, q, L.h, T_rec, L.gamma, L.lw_k, L.lw_v, L.pos0, out, ws, tk, tv, 1)
@@ -179,8 +185,9 @@ def test_split_gemma_shape_ctx1000():
     check("split vs the default engine", out, f64(out64))
 
 
+@pytest.mark.parametrize("mode", [m for m, _ in MODES])
 @pytest.mark.parametrize("window", [130, 201, 500])
-def test_split_window(window):
+def test_split_window(mode, window):
     T = 200
     L = _layer(256, T, seed=170 + window)
     s = L.shape
@@ -189,7 +196,7 @@ def test_split_window(window):
     tk, tv = empty_kv(L, 1)
     pos = torch.full((L.B,), n_keep - 1, dtype=torch.int32, device="cuda")
     kvd.kvd_project_qkv(s, L.h_new, L.gamma, L.lw_q, L.lw_k, L.lw_v, pos, q, tk, tv, 0)
-    kvd.kvd_set_fused_tokens(SPLIT)
+    kvd.kvd_set_fused_tokens(mode)
     out = torch.empty_like(q)
     ws = kvd.workspace(s, kvd.KVD_OP_FUSED, L.B, T, 1)
     kvd.kvd_fused_window_attn(s, q, L.h, T, L.gamma, L.lw_k, L.lw_v, window, out, ws, tk, tv, 1)
@@ -197,3 +204,21 @@ def test_split_window(window):
                                   f64(L.w_v), window, s.n_q_heads, s.n_kv_heads, s.head_dim, s.rms_eps,
                                   s.rope_theta)
     check(f"split window {window} vs oracle", out, ref)
+
+
+def test_split64_by_policy_on_small_grids():
+    # a Gemma-3-4B layer at B = 1 with 1000 keys: 4 KV heads x 16 tiles of 64 = 64
+    # <= 128, so the automatic policy takes the split engine with 64-token chunks
+    L = make_layer(C.GEMMA3_4B, B=1, T=1000, seed=207, pos0=[31])
+    s = L.shape
+    assert kvd.kvd_num_splits(s, kvd.KVD_OP_FUSED, L.B, L.T, 1) == 16
+    q, _, out, (dk, dv) = gpu_fused(L, kv_debug=True)
+    check("auto split64 vs oracle", out, oracle_decode(L))
+    Kp, Vp = gpu_recompute(L)
+    assert torch.equal(_bits(dk), _bits(Kp)) and torch.equal(_bits(dv), _bits(Vp))
+    kvd.kvd_set_fused_tokens(kvd.KVD_FUSED_SPLIT64)
+    _, _, out_s, _ = gpu_fused(L, q=q)
+    assert torch.equal(_bits(out), _bits(out_s))
+    kvd.kvd_set_fused_tokens(64)
+    _, _, out64, _ = gpu_fused(L, q=q)
+    check("auto split64 vs 64-token tiles", out, f64(out64))
