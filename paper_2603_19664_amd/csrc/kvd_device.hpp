@@ -910,18 +910,17 @@ struct F32Tile {
 
 // ------------------------------------------------------------------ attention
 
-// q heads j*g .. j*g+g-1 of sequence b into LDS (fp32), pre-multiplied by
-// log2(e)/sqrt(head_dim).
+// q heads j*g .. j*g+g-1 of sequence b into LDS: fp32 pre-multiplied by
+// log2(e)/sqrt(head_dim), or for bf16 the rows as they are (the MFMA tile
+// attention scales its fp32 scores instead).
 template <typename T, int HD, int NT>
 __device__ __forceinline__ void load_q(const T* q, int b, int n_q, int j, int g, float* qs) {
   constexpr int CH = 16 / sizeof(T);
   const T* src = q + ((size_t)b * n_q + (size_t)j * g) * HD;
   for (int c = threadIdx.x; c < g * HD / CH; c += NT) {
-    float x[8];
     if constexpr (CH == 8) {
-      load8(src + CH * c, x);
-#pragma unroll
-      for (int e = 0; e < 8; ++e) qs[CH * c + e] = x[e] * ScoreScale<HD>::v;
+      *reinterpret_cast<u32x4_t*>(reinterpret_cast<uint16_t*>(qs) + CH * c) =
+          *reinterpret_cast<const u32x4_t*>(src + CH * c);
     } else {
       const float4 v = *reinterpret_cast<const float4*>(src + CH * c);
       qs[CH * c + 0] = v.x * ScoreScale<HD>::v;
@@ -970,10 +969,7 @@ struct TileSetup {
     auto put_q = [&](int c, u32x4_t v) {
       float* dst = qs + CH * c;
       if constexpr (CH == 8) {
-        const float x[8] = {bf_lo(v.x), bf_hi(v.x), bf_lo(v.y), bf_hi(v.y),
-                            bf_lo(v.z), bf_hi(v.z), bf_lo(v.w), bf_hi(v.w)};
-#pragma unroll
-        for (int e = 0; e < 8; ++e) dst[e] = x[e] * ScoreScale<HD>::v;
+        *reinterpret_cast<u32x4_t*>(reinterpret_cast<uint16_t*>(qs) + CH * c) = v;
       } else {
         dst[0] = __uint_as_float(v.x) * ScoreScale<HD>::v;
         dst[1] = __uint_as_float(v.y) * ScoreScale<HD>::v;
@@ -1230,10 +1226,154 @@ __device__ __forceinline__ void attend_pv(const T* vt, int n, int rows, int g, c
   __syncthreads();
 }
 
+// The bf16 tile attention on 16x16x32 MFMAs, in the same two halves and with
+// the same results in LDS: probabilities S[h * rows + key] and (max, sum) per
+// head from attend_scores_mfma, the tile's P V per head in `red` from
+// attend_pv_mfma (write_partial then takes one key split).  q sits in LDS as raw
+// bf16 rows.
+//  1. scores: task (16-key block, group of 16 heads): S^T = K q^T over HD / 32
+//     k-steps, A = 16 key rows of the tile, B = the heads' q rows; a lane gets
+//     4 keys of one head, scaled by log2(e)/sqrt(head_dim) in fp32;
+//  2. per head (one wave each): max, p = 2^(s - max) rounded to bf16 (the value
+//     the P V product uses), sum of the rounded p;
+//  3. P V: task (16 output columns, group of 16 heads): O^T = V^T P^T over
+//     32-key steps in key order, A = V^T fetched from the row-major V rows by
+//     two LDS transpose reads (4 keys of one column each), B = the heads'
+//     probabilities.
+// Keys past n contribute zeros: their probabilities are 0 and their V^T
+// elements are replaced by 0 before the product (LDS past the tile may hold
+// anything).  Rows past the tile are clamped to its last row for the reads.
+// Row strides of S (rows) and of the K|V tile keep every 16-byte read aligned
+// (rows and LD multiples of 4 and 8 elements).
+template <int HD, int NT, int KPL, int LD = kv_ld<uint16_t>(HD)>
+__device__ __forceinline__ void attend_scores_mfma(const uint16_t* kt, int n, int rows, int g, char* lds,
+                                                   const AttnLds& L) {
+  constexpr int NW = NT / 64;
+  constexpr int SR = 64 * KPL;  // row stride of the raw scores in `red`
+  static_assert(KPL >= 1 && KPL <= 3 && HD % 32 == 0, "keys per lane, k-steps");
+  const int lane = threadIdx.x & 63, wave = wave_id();
+  const int lq = lane & 15, lg = lane >> 4;
+  const uint16_t* qb = reinterpret_cast<const uint16_t*>(lds + L.q);
+  float* sc = reinterpret_cast<float*>(lds + L.red);
+  float* S = reinterpret_cast<float*>(lds + L.s);
+  float* ml = reinterpret_cast<float*>(lds + L.ml);
+  const int nkb = (n + 15) >> 4, nhg = (g + 15) >> 4;
+  for (int task = wave; task < nkb * nhg; task += NW) {
+    const int kb = task % nkb, hgp = task / nkb;
+    const int head = 16 * hgp + lq;
+    const uint16_t* ka = kt + (size_t)min(16 * kb + lq, rows - 1) * LD + 8 * lg;
+    const uint16_t* qa = qb + (size_t)min(head, g - 1) * HD + 8 * lg;
+    f32x4_t acc = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+    for (int ks = 0; ks < HD / 32; ++ks)
+      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(*reinterpret_cast<const bf16x8_t*>(ka + 32 * ks),
+                                                    *reinterpret_cast<const bf16x8_t*>(qa + 32 * ks), acc, 0, 0, 0);
+    if (head < g)
+      *reinterpret_cast<float4*>(sc + (size_t)head * SR + 16 * kb + 4 * lg) =
+          make_float4(acc[0] * ScoreScale<HD>::v, acc[1] * ScoreScale<HD>::v, acc[2] * ScoreScale<HD>::v,
+                      acc[3] * ScoreScale<HD>::v);
+  }
+  __syncthreads();
+
+  for (int h = wave; h < g; h += NW) {
+    float sk[KPL], pk[KPL];
+#pragma unroll
+    for (int kk = 0; kk < KPL; ++kk) {
+      const int key = 64 * kk + lane;
+      sk[kk] = key < n ? sc[(size_t)h * SR + key] : -INFINITY;
+    }
+    float mx = sk[0];
+#pragma unroll
+    for (int kk = 1; kk < KPL; ++kk) mx = fmaxf(mx, sk[kk]);
+    const float m = wave_max(mx);
+#pragma unroll
+    for (int kk = 0; kk < KPL; ++kk) pk[kk] = 64 * kk + lane < n ? bf_lo(pack_bf16x2(exp2f(sk[kk] - m), 0.0f)) : 0.0f;
+    float ps = pk[0];
+#pragma unroll
+    for (int kk = 1; kk < KPL; ++kk) ps += pk[kk];
+    const float l = wave_sum(ps);
+#pragma unroll
+    for (int kk = 0; kk < KPL; ++kk)
+      if (64 * kk + lane < rows) S[h * rows + 64 * kk + lane] = pk[kk];
+    if (lane == 0) {
+      ml[2 * h] = m;
+      ml[2 * h + 1] = l;
+    }
+  }
+  __syncthreads();
+}
+
+template <int HD, int NT, int LD = kv_ld<uint16_t>(HD)>
+__device__ __forceinline__ void attend_pv_mfma(const uint16_t* vt, int n, int rows, int g, char* lds,
+                                               const AttnLds& L) {
+  typedef short i16x4_t __attribute__((ext_vector_type(4)));
+  constexpr int NW = NT / 64;
+  constexpr int NDB = HD / 16;  // 16-column blocks of the output
+  const int lane = threadIdx.x & 63, wave = wave_id();
+  const int lq = lane & 15, lg = lane >> 4;
+  const float* S = reinterpret_cast<const float*>(lds + L.s);
+  float* red = reinterpret_cast<float*>(lds + L.red);
+  const int nks = (n + 31) >> 5, nhg = (g + 15) >> 4;
+  // transpose reads: within each group of 16 lanes, lane s reads 4 columns
+  // 4 (s % 4) .. of row s / 4 of a 4-row group; lane i then holds column i of
+  // the group's 4 rows
+  const int sr = lq >> 2, scol = 4 * (lq & 3);
+  for (int task = wave; task < NDB * nhg; task += NW) {
+    const int db = task % NDB, hgp = task / NDB;
+    const int head = 16 * hgp + lq;
+    const float* prow = S + (size_t)min(head, g - 1) * rows;
+    const uint16_t* vcol = vt + 16 * db + scol;
+    f32x4_t acc = {0.0f, 0.0f, 0.0f, 0.0f};
+    for (int ks = 0; ks < nks; ++ks) {
+      const int k0 = 32 * ks + 8 * lg;  // keys k0 .. k0 + 7 of this lane (both operands)
+      i16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+          (__attribute__((address_space(3))) i16x4_t*)(vcol + (size_t)min(k0 + sr, rows - 1) * LD));
+      i16x4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+          (__attribute__((address_space(3))) i16x4_t*)(vcol + (size_t)min(k0 + 4 + sr, rows - 1) * LD));
+      const float4 p0 = *reinterpret_cast<const float4*>(prow + k0);
+      const float4 p1 = *reinterpret_cast<const float4*>(prow + k0 + 4);
+      float pv[8] = {p0.x, p0.y, p0.z, p0.w, p1.x, p1.y, p1.z, p1.w};
+      if (k0 + 8 > n) {  // the keys past n: zero weights and zero values
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          if (k0 + e >= n) {
+            lo[e] = 0;
+            pv[e] = 0.0f;
+          }
+          if (k0 + 4 + e >= n) {
+            hi[e] = 0;
+            pv[4 + e] = 0.0f;
+          }
+        }
+      }
+      const bf16x8_t a = __builtin_bit_cast(
+          bf16x8_t, make_uint4(__builtin_bit_cast(uint2, lo).x, __builtin_bit_cast(uint2, lo).y,
+                               __builtin_bit_cast(uint2, hi).x, __builtin_bit_cast(uint2, hi).y));
+      const bf16x8_t bp = __builtin_bit_cast(bf16x8_t, make_uint4(pack_bf16x2(pv[0], pv[1]), pack_bf16x2(pv[2], pv[3]),
+                                                                  pack_bf16x2(pv[4], pv[5]), pack_bf16x2(pv[6], pv[7])));
+      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, bp, acc, 0, 0, 0);
+    }
+    if (head < g)
+      *reinterpret_cast<float4*>(red + (size_t)head * HD + 16 * db + 4 * lg) = make_float4(acc[0], acc[1], acc[2], acc[3]);
+  }
+  __syncthreads();
+}
+
+// Key splits of the P V partial sums a tile's attention leaves in `red`.
+template <typename T>
+__device__ __forceinline__ int tile_splits(int g) {
+  return sizeof(T) == 2 ? 1 : attn_ts(g);
+}
+
 template <typename T, int HD, int NT, int KPL>
 __device__ __forceinline__ void attend_tile(const T* kv, int n, int rows, int g, char* lds, const AttnLds& L) {
-  attend_scores<T, HD, NT, KPL>(kv, n, rows, g, lds, L);
-  attend_pv<T, HD, NT>(kv + HD, n, rows, g, lds, L);
+  if constexpr (sizeof(T) == 2) {
+    attend_scores_mfma<HD, NT, KPL>(kv, n, rows, g, lds, L);
+    attend_pv_mfma<HD, NT>(kv + HD, n, rows, g, lds, L);
+  } else {
+    attend_scores<T, HD, NT, KPL>(kv, n, rows, g, lds, L);
+    attend_pv<T, HD, NT>(kv + HD, n, rows, g, lds, L);
+  }
 }
 
 // Device-scope (coherent across the XCDs' L2 caches) 32-bit store / load: the
@@ -1248,14 +1388,13 @@ __device__ __forceinline__ float load_dev(const float* p) {
 
 // Split-K partial of (b, KV head j, split s) into the workspace:
 // acc [B][n_q][S][HD] fp32 followed by ml [B][n_q][S][2] fp32.  The tile's
-// output is the sum, in key-split order, of attend_tile's attn_ts(g) P V
-// partial sums in `red`; it is added here as it is written out.
+// output is the sum, in key-split order, of the TS P V partial sums the tile
+// attention left in `red` (tile_splits); it is added here as it is written out.
 template <int HD, int NT>
 __device__ __forceinline__ void write_partial(const char* lds, const AttnLds& L, float* ws_acc, float* ws_ml, int b,
-                                              int n_q, int j, int g, int S, int s) {
+                                              int n_q, int j, int g, int S, int s, int TS) {
   const float* red = reinterpret_cast<const float*>(lds + L.red);
   const float* ml = reinterpret_cast<const float*>(lds + L.ml);
-  const int TS = attn_ts(g);
   for (int i = threadIdx.x; i < g * HD; i += NT) {
     const int h = i / HD, c = i - h * HD;
     float o = 0.0f;

@@ -588,7 +588,7 @@ __device__ __forceinline__ void fused_body(const FusedArgs& a, int per_xcd, int 
       }
     }
     attend_tile<T, HD, NT, KPL>(kv, nk, MT + FR, g, lds, AL);
-    write_partial<HD, NT>(lds, AL, a.ws_acc, a.ws_ml, b, a.n_q, j, g, a.S, rc);
+    write_partial<HD, NT>(lds, AL, a.ws_acc, a.ws_ml, b, a.n_q, j, g, a.S, rc, tile_splits<T>(g));
   } else {
     // tail tile c: 64 rows, the last one the rest (up to 64 + FR rows)
     const int r0 = c * kTile;
@@ -606,7 +606,7 @@ __device__ __forceinline__ void fused_body(const FusedArgs& a, int per_xcd, int 
     }
     __syncthreads();
     attend_tile<T, HD, NT, KPL>(kv, nk, MT + FR, g, lds, AL);
-    write_partial<HD, NT>(lds, AL, a.ws_acc, a.ws_ml, b, a.n_q, j, g, a.S, a.n_rec + c);
+    write_partial<HD, NT>(lds, AL, a.ws_acc, a.ws_ml, b, a.n_q, j, g, a.S, a.n_rec + c, tile_splits<T>(g));
   }
   if (a.out != nullptr) {
     unsigned long long* ctr = a.ws_done + (size_t)b * a.n_kv + j;
@@ -727,7 +727,7 @@ __global__ __launch_bounds__(split_nt(HD), 1) void fused_split_kernel(FusedArgs 
   float* xrec = a.xch + (((size_t)b * a.n_kv + j) * C + c) * a.xf;
   unsigned long long* bits = a.ws_bits + ((size_t)b * a.n_kv + j) * kSplitBitWords;
   if (role == 0) {
-    attend_scores<uint16_t, HD, NT, KPL, KLD>(tile, nk, ROWS, g, lds, AL);
+    attend_scores_mfma<HD, NT, KPL, KLD>(tile, nk, ROWS, g, lds, AL);
     for (int i = tid; i < g * ROWS; i += NT) store_dev(xrec + i, S[i]);
     if (tid < 2 * g) store_dev(xrec + g * ROWS + tid, ml[tid]);
     __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0): this thread's record stores are complete
@@ -753,8 +753,8 @@ __global__ __launch_bounds__(split_nt(HD), 1) void fused_split_kernel(FusedArgs 
   for (int i = tid; i < g * ROWS; i += NT) S[i] = load_dev(xrec + i);
   if (tid < 2 * g) ml[tid] = ok ? load_dev(xrec + g * ROWS + tid) : __builtin_nanf("");
   __syncthreads();
-  attend_pv<uint16_t, HD, NT, KLD>(tile, nk, ROWS, g, lds, AL);
-  write_partial<HD, NT>(lds, AL, a.ws_acc, a.ws_ml, b, a.n_q, j, g, a.S, c);
+  attend_pv_mfma<HD, NT, KLD>(tile, nk, ROWS, g, lds, AL);
+  write_partial<HD, NT>(lds, AL, a.ws_acc, a.ws_ml, b, a.n_q, j, g, a.S, c, tile_splits<uint16_t>(g));
   // every V role arrives (also without out): the last one clears the
   // completion words for the next call
   unsigned long long* ctr = a.ws_done + (size_t)b * a.n_kv + j;
@@ -792,7 +792,7 @@ __global__ __launch_bounds__(kNtAttn) void decode_kernel(AttnArgs a) {
   if constexpr (FR > 0) __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0): the remainder rows are in LDS
   __syncthreads();
   attend_tile<T, HD, NT, tile_kpl<T>()>(kv, n, kTile + FR, g, lds, AL);
-  write_partial<HD, NT>(lds, AL, a.ws_acc, a.ws_ml, b, a.n_q, j, g, a.S, s);
+  write_partial<HD, NT>(lds, AL, a.ws_acc, a.ws_ml, b, a.n_q, j, g, a.S, s, tile_splits<T>(g));
   if (a.out != nullptr) {
     unsigned long long* ctr = a.ws_done + (size_t)b * a.n_kv + j;
     const unsigned long long before = split_arrive(ctr, 1, reinterpret_cast<unsigned long long*>(lds + AL.ctr));
