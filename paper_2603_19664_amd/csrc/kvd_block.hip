@@ -130,16 +130,16 @@ __global__ __launch_bounds__(kNtTile, 1) void gemm_kernel(GemmArgs a, int per_xc
 // ------------------------------------------------------------------ causal prefill attention
 
 // LDS of prefill_attn_kernel (bytes): the workgroup's query rows [128][HD + 8],
-// the key tile [64][HD + 8] and the value tile transposed [HD][64 + 8], bf16.
+// the key tile and the value tile [64][HD + 8], bf16.
 struct PrefillLds {
-  size_t qs, ks, vt, ctr, end;
+  size_t qs, ks, vs, ctr, end;
 };
 constexpr PrefillLds prefill_lds(int hd) {
   PrefillLds L{};
   L.qs = 0;
   L.ks = L.qs + (size_t)2 * 128 * (hd + 8);
-  L.vt = L.ks + (size_t)2 * 64 * (hd + 8);
-  L.ctr = L.vt + (size_t)2 * hd * (64 + 8);  // split counter broadcast
+  L.vs = L.ks + (size_t)2 * 64 * (hd + 8);
+  L.ctr = L.vs + (size_t)2 * 64 * (hd + 8);  // split counter broadcast
   L.end = L.ctr + 16;
   return L;
 }
@@ -163,6 +163,9 @@ constexpr PrefillLds prefill_lds(int hd) {
 // registers: for the 16 keys of an MFMA step, lane half h supplies the keys its
 // score registers hold (32 kh + 16 (t & 1) + 4 h + {0..3, 8..11}), and the V^T
 // operand takes the same keys, so both operands agree on the reduction order.
+// V stays row-major in LDS; each V^T operand is two LDS transpose reads (in a
+// group of 16 lanes, lane s names 4 columns of row s / 4 of a 4-key group, and
+// lane i receives column i of the 4 keys).
 // Scores are in the log2 domain (log2(e) / sqrt(hd) folded into the scale).
 template <int HD>
 __global__ __launch_bounds__(256) void prefill_attn_kernel(PrefillArgs a) {
@@ -170,13 +173,13 @@ __global__ __launch_bounds__(256) void prefill_attn_kernel(PrefillArgs a) {
   constexpr PrefillLds PL = prefill_lds(HD);
   constexpr int KS = HD / 16;              // 16-wide k-steps of a score block
   constexpr int DB = HD / 32;              // 32-row blocks of O^T (head_dim rows)
-  constexpr int KLDS = HD + 8, VLD = 64 + 8;
+  constexpr int KLDS = HD + 8;
   constexpr int CPR = HD / 8;              // 16-byte chunks per key row
-  constexpr int KCH = 64 * CPR / 256;      // key chunks per thread
-  constexpr int VGR = 16 * CPR / 256;      // value groups (4 keys x 8 columns) per thread
+  constexpr int KCH = 64 * CPR / 256;      // key (and value) chunks per thread
+  typedef short i16x4_t __attribute__((ext_vector_type(4)));
   uint16_t* Qs = reinterpret_cast<uint16_t*>(lds + PL.qs);
   uint16_t* Ks = reinterpret_cast<uint16_t*>(lds + PL.ks);
-  uint16_t* Vt = reinterpret_cast<uint16_t*>(lds + PL.vt);
+  uint16_t* Vs = reinterpret_cast<uint16_t*>(lds + PL.vs);
 
   const int tid = threadIdx.x, lane = tid & 63, w = wave_id();
   const int hl = lane >> 5;  // lane half
@@ -220,44 +223,25 @@ __global__ __launch_bounds__(256) void prefill_attn_kernel(PrefillArgs a) {
   float m_run = -INFINITY, l_run = 0.0f;
 
   // key / value block kb into registers (rows clamped to T - 1: masked below)
-  u32x4_t kc[KCH], vc[VGR][4];
+  u32x4_t kc[KCH], vc[KCH];
   auto load_kv = [&](int kb) {
 #pragma unroll
     for (int i = 0; i < KCH; ++i) {
       const int c = tid + 256 * i, row = c / CPR, ch = c - row * CPR;
-      const int t = min(64 * kb + row, a.T - 1);
-      kc[i] = *reinterpret_cast<const u32x4_t*>(kbase + (size_t)t * HD + 8 * ch);
-    }
-#pragma unroll
-    for (int i = 0; i < VGR; ++i) {
-      const int gidx = tid + 256 * i, k4 = gidx & 15, ch = gidx >> 4;
-#pragma unroll
-      for (int kk = 0; kk < 4; ++kk) {
-        const int t = min(64 * kb + 4 * k4 + kk, a.T - 1);
-        vc[i][kk] = *reinterpret_cast<const u32x4_t*>(vbase + (size_t)t * HD + 8 * ch);
-      }
+      const size_t t = min(64 * kb + row, a.T - 1);
+      kc[i] = *reinterpret_cast<const u32x4_t*>(kbase + t * HD + 8 * ch);
+      vc[i] = *reinterpret_cast<const u32x4_t*>(vbase + t * HD + 8 * ch);
     }
   };
   load_kv(kb0);
 
   for (int kb = kb0; kb < kb1; ++kb) {
-    // the registers into LDS: K as is, V transposed ([column][key])
+    // the registers into LDS, both row-major
 #pragma unroll
     for (int i = 0; i < KCH; ++i) {
       const int c = tid + 256 * i, row = c / CPR, ch = c - row * CPR;
       *reinterpret_cast<u32x4_t*>(Ks + row * KLDS + 8 * ch) = kc[i];
-    }
-#pragma unroll
-    for (int i = 0; i < VGR; ++i) {
-      const int gidx = tid + 256 * i, k4 = gidx & 15, ch = gidx >> 4;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const int word = e >> 1, sh = (e & 1) * 16;
-        uint2 pk;
-        pk.x = ((vc[i][0][word] >> sh) & 0xffffu) | (((vc[i][1][word] >> sh) & 0xffffu) << 16);
-        pk.y = ((vc[i][2][word] >> sh) & 0xffffu) | (((vc[i][3][word] >> sh) & 0xffffu) << 16);
-        *reinterpret_cast<uint2*>(Vt + (8 * ch + e) * VLD + 4 * k4) = pk;
-      }
+      *reinterpret_cast<u32x4_t*>(Vs + row * KLDS + 8 * ch) = vc[i];
     }
     __syncthreads();
     if (kb + 1 < kb1) load_kv(kb + 1);  // in flight while this block is computed
@@ -329,16 +313,24 @@ __global__ __launch_bounds__(256) void prefill_attn_kernel(PrefillArgs a) {
       }
       sum += __shfl_xor(sum, 32, 64);
       l_run += sum;
-      // O^T += V^T P^T: per 16-key step, the DB accumulators are independent
+      // O^T += V^T P^T: per 16-key step, the DB accumulators are independent.
+      // Transpose-read source of this lane: keys k0 + 4 hl + (lane % 16) / 4
+      // (+ 8 for the upper four), columns 32 db + 16 ((lane / 16) % 2) +
+      // 4 (lane % 4) .. + 3.
+      const uint16_t* vsrc = Vs + (4 * hl + ((lane & 15) >> 2)) * KLDS + 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
 #pragma unroll
       for (int t = 0; t < 4; ++t) {
         const int k0 = 32 * (t >> 1) + 16 * (t & 1);
 #pragma unroll
         for (int db = 0; db < DB; ++db) {
-          const uint16_t* vr = Vt + (32 * db + (lane & 31)) * VLD + 4 * hl + k0;
-          const uint2 lo = *reinterpret_cast<const uint2*>(vr);
-          const uint2 hi = *reinterpret_cast<const uint2*>(vr + 8);
-          const bf16x8_t vf = __builtin_bit_cast(bf16x8_t, make_uint4(lo.x, lo.y, hi.x, hi.y));
+          const uint16_t* vr = vsrc + k0 * KLDS + 32 * db;
+          const i16x4_t lo =
+              __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) i16x4_t*)vr);
+          const i16x4_t hi =
+              __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) i16x4_t*)(vr + 8 * KLDS));
+          const bf16x8_t vf = __builtin_bit_cast(
+              bf16x8_t, make_uint4(__builtin_bit_cast(uint2, lo).x, __builtin_bit_cast(uint2, lo).y,
+                                   __builtin_bit_cast(uint2, hi).x, __builtin_bit_cast(uint2, hi).y));
           o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[t], o[db], 0, 0, 0);
         }
       }
