@@ -19,15 +19,21 @@ namespace kvd {
 
 // grid: xcd_map(n_units * n_tiles) workgroups; item = unit * n_tiles + tile (the
 // token tiles of one weight block run on one XCD).  A unit is 512 rows of W
-// (kEpiResidual) or 256 rows each of W and W2 (kEpiSwiglu); a tile is 64 token rows.
-template <int EPI, bool NORM, bool PACKED>
+// (kEpiResidual) or 256 rows each of W and W2 (kEpiSwiglu); a tile is MT token
+// rows: 64 on MfmaTile, or 128 on WideTile for launches with at least a full
+// round of such tiles.  Both engines give wave w rows 32 w .. 32 w + 31 of each
+// half and run the same per-element MFMA chain, so the outputs are identical.
+template <int EPI, bool NORM, bool PACKED, int MT>
 __global__ __launch_bounds__(kNtTile, 1) void gemm_kernel(GemmArgs a, int per_xcd, int n_tiles, int n_units) {
   extern __shared__ __align__(16) char lds[];
-  constexpr int NT = kNtTile, HD = 256, MT = kMtBf16;
+  constexpr int NT = kNtTile, HD = 256;
   constexpr ProjLds PL = proj_lds<uint16_t>(HD, MT);
   constexpr int KLD = kv_ld<uint16_t>(HD);
-  using Tile = MfmaTile<HD, MT, PACKED>;
-  static_assert(Tile::NB_F == 2 && Tile::WT == 1 && Tile::NB_T == 2, "wave fw owns rows 32 fw.. of both halves");
+  using Tile = MfmaTile<HD, kMtBf16, PACKED>;
+  using Wide = WideTile<HD, 2 * kMtBf16, PACKED>;
+  static_assert(MT == kMtBf16 || MT == 2 * kMtBf16, "64- or 128-token tiles");
+  static_assert(Tile::NB_F == 2 && Tile::WT == 1 && Tile::NB_T == 2 && Wide::NB_F == 2 && NT == Wide::NT,
+                "wave w owns rows 32 w.. of both halves");
   const int tid = threadIdx.x;
   // 32-bit index arithmetic: the launch's grid bounds the item count
   const unsigned item = (blockIdx.x % kXcds) * (unsigned)per_xcd + blockIdx.x / kXcds;
@@ -57,6 +63,7 @@ __global__ __launch_bounds__(kNtTile, 1) void gemm_kernel(GemmArgs a, int per_xc
     if (!valid[0]) n = n0;  // any readable row; its column is not stored
     hrow[0] = static_cast<const uint16_t*>(a.x) + (size_t)n * K + 8 * (tid & 7);
   }
+  const int n_rows = (int)std::min<long long>(MT, a.M - n0);
   // gamma (or ones) into LDS while the K-loop's first loads are in flight
   const uint16_t* gsrc = static_cast<const uint16_t*>(a.gamma);
   const int ngc = a.K / 8;
@@ -69,10 +76,9 @@ __global__ __launch_bounds__(kNtTile, 1) void gemm_kernel(GemmArgs a, int per_xc
       *reinterpret_cast<u32x4_t*>(gam + 8 * c) = *reinterpret_cast<const u32x4_t*>(gsrc + 8 * c);
   };
   const int lane = tid & 63, fw = wave_id() % Tile::WF;
-  Tile::run_with(hrow, valid, gam, gsrc, a.K, a.eps, halves, hst, rinv, setup,
-                 [&](const f32x16_t (&acc)[2][2], const bool (&)[2]) {
+  auto epi = [&](const auto& acc, const auto&) {
 #pragma unroll
-                   for (int bt = 0; bt < 2; ++bt) {
+                   for (int bt = 0; bt < MT / 32; ++bt) {
                      const int tok = 32 * bt + (lane & 31);
                      const long long n = n0 + tok;
                      const float ri = NORM ? rinv[tok] : 1.0f;
@@ -112,7 +118,12 @@ __global__ __launch_bounds__(kNtTile, 1) void gemm_kernel(GemmArgs a, int per_xc
                        }
                      }
                    }
-                 });
+  };
+  if constexpr (MT == kMtBf16)
+    Tile::run_with(hrow, valid, gam, gsrc, a.K, a.eps, halves, hst, rinv, setup, epi);
+  else
+    Wide::run_with(static_cast<const uint16_t*>(a.x) + (size_t)n0 * K, n_rows, gam, gsrc, a.K, a.eps, halves, hst,
+                   rinv, setup, epi);
   __syncthreads();
   // store: 16-byte chunks of the valid token rows
   constexpr int NF = EPI == kEpiResidual ? 512 : 256;
@@ -444,27 +455,37 @@ static hipError_t set_lds_once(Kern k, size_t bytes, std::atomic<size_t>& done) 
   return hipSuccess;
 }
 
-template <int EPI, bool NORM, bool PACKED>
+template <int EPI, bool NORM, bool PACKED, int MT>
 static hipError_t gemm_t(const GemmArgs& a, hipStream_t st) {
-  const size_t bytes = proj_lds<uint16_t>(256, kMtBf16).end + gamma_lds_bytes(a.K);
+  const size_t bytes = gemm_lds_bytes(a.K, MT);
   static std::atomic<size_t> done{0};
-  auto k = gemm_kernel<EPI, NORM, PACKED>;
+  auto k = gemm_kernel<EPI, NORM, PACKED, MT>;
   hipError_t e = set_lds_once(k, bytes, done);
   if (e != hipSuccess) return e;
-  const int n_tiles = (a.M + kMtBf16 - 1) / kMtBf16;
+  const int n_tiles = (a.M + MT - 1) / MT;
   const int n_units = EPI == kEpiResidual ? a.N / 512 : a.N / 256;
   const XcdMap m = xcd_map((long long)n_units * n_tiles);
   hipLaunchKernelGGL(k, dim3(m.grid), dim3(kNtTile), bytes, st, a, m.per, n_tiles, n_units);
   return hipGetLastError();
 }
 
+template <int EPI, bool NORM, bool PACKED>
+static hipError_t gemm_mt(const GemmArgs& a, hipStream_t st) {
+  // 128-token tiles (twice the MFMAs per weight fragment) when they fill at
+  // least one round of the chip and their LDS fits
+  const long long units = EPI == kEpiResidual ? a.N / 512 : a.N / 256;
+  const bool wide = units * ((a.M + 2LL * kMtBf16 - 1) / (2 * kMtBf16)) >= kWideMinTiles &&
+                    gemm_lds_bytes(a.K, 2 * kMtBf16) <= kLdsPerGroup;
+  return wide ? gemm_t<EPI, NORM, PACKED, 2 * kMtBf16>(a, st) : gemm_t<EPI, NORM, PACKED, kMtBf16>(a, st);
+}
+
 hipError_t launch_gemm(const GemmArgs& a, int epi, int packed, hipStream_t st) {
   if (epi == kEpiResidual) {
-    if (a.norm) return packed ? gemm_t<kEpiResidual, true, true>(a, st) : gemm_t<kEpiResidual, true, false>(a, st);
-    return packed ? gemm_t<kEpiResidual, false, true>(a, st) : gemm_t<kEpiResidual, false, false>(a, st);
+    if (a.norm) return packed ? gemm_mt<kEpiResidual, true, true>(a, st) : gemm_mt<kEpiResidual, true, false>(a, st);
+    return packed ? gemm_mt<kEpiResidual, false, true>(a, st) : gemm_mt<kEpiResidual, false, false>(a, st);
   }
-  if (a.norm) return packed ? gemm_t<kEpiSwiglu, true, true>(a, st) : gemm_t<kEpiSwiglu, true, false>(a, st);
-  return packed ? gemm_t<kEpiSwiglu, false, true>(a, st) : gemm_t<kEpiSwiglu, false, false>(a, st);
+  if (a.norm) return packed ? gemm_mt<kEpiSwiglu, true, true>(a, st) : gemm_mt<kEpiSwiglu, true, false>(a, st);
+  return packed ? gemm_mt<kEpiSwiglu, false, true>(a, st) : gemm_mt<kEpiSwiglu, false, false>(a, st);
 }
 
 template <int HD>
@@ -525,7 +546,7 @@ PrefillSplit prefill_split(int B, int T, int n_q) {
 size_t prefill_part_floats(int hd) { return (size_t)4 * ((hd / 32) * 16 * 64 + 128); }
 
 size_t prefill_lds_bytes(int hd) { return prefill_lds(hd).end; }
-size_t gemm_lds_bytes(int K) { return proj_lds<uint16_t>(256, kMtBf16).end + gamma_lds_bytes(K); }
+size_t gemm_lds_bytes(int K, int mt) { return proj_lds<uint16_t>(256, mt).end + gamma_lds_bytes(K); }
 
 hipError_t launch_prefill_attn(const PrefillArgs& a, int hd, hipStream_t st) {
   switch (hd) {

@@ -138,7 +138,7 @@ hipError_t launch_fill_ones_bf16(void* dst, int n, hipStream_t st);
 // dst[i] = 0 (64-bit words) for i < n.
 hipError_t launch_fill_zero_u64(void* dst, int n, hipStream_t st);
 // LDS bytes of the two block-forward kernels (for host-side validation).
-size_t gemm_lds_bytes(int K);
+size_t gemm_lds_bytes(int K, int mt = kMtBf16);
 size_t prefill_lds_bytes(int hd);
 
 // The current device's static scratch (kNoAllocScratchBytes, 256-byte aligned):
