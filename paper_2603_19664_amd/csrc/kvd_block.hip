@@ -469,13 +469,17 @@ static hipError_t gemm_t(const GemmArgs& a, hipStream_t st) {
   return hipGetLastError();
 }
 
+// 128-token tiles take about 1.4-1.5x a 64-token tile's time for twice its
+// work (measured: the projections of a Gemma-3-4B-shaped block); the launch
+// takes them when its rounds of the chip (kWideMinTiles workgroups each) then
+// cost no more, and their LDS fits.
+constexpr int kGemmWideCost2 = 3;  // twice the relative time of a 128-token tile
 template <int EPI, bool NORM, bool PACKED>
 static hipError_t gemm_mt(const GemmArgs& a, hipStream_t st) {
-  // 128-token tiles (twice the MFMAs per weight fragment) when they fill at
-  // least one round of the chip and their LDS fits
   const long long units = EPI == kEpiResidual ? a.N / 512 : a.N / 256;
-  const bool wide = units * ((a.M + 2LL * kMtBf16 - 1) / (2 * kMtBf16)) >= kWideMinTiles &&
-                    gemm_lds_bytes(a.K, 2 * kMtBf16) <= kLdsPerGroup;
+  const long long r64 = (units * ((a.M + kMtBf16 - 1) / kMtBf16) + kWideMinTiles - 1) / kWideMinTiles;
+  const long long r128 = (units * ((a.M + 2LL * kMtBf16 - 1) / (2 * kMtBf16)) + kWideMinTiles - 1) / kWideMinTiles;
+  const bool wide = kGemmWideCost2 * r128 <= 2 * r64 && gemm_lds_bytes(a.K, 2 * kMtBf16) <= kLdsPerGroup;
   return wide ? gemm_t<EPI, NORM, PACKED, 2 * kMtBf16>(a, st) : gemm_t<EPI, NORM, PACKED, kMtBf16>(a, st);
 }
 
