@@ -125,6 +125,81 @@ __global__ __launch_bounds__(kNtTile, 1) void proj_kernel(ProjArgs a, int per_xc
   }
 }
 
+// ------------------------------------------------------------------ recompute / prefill, wide tiles
+
+// bf16, head_dim 128 / 256, for calls with at least a full round of 128-token
+// tiles: WideTile's 128-token tile of both halves of a unit (a KV head's K and
+// V rows, or query heads 2u and 2u + 1) for up to 128 tokens of one sequence.
+// grid: xcd_map(n_units * B * tps) with tps = ceil(T / 128); item = (unit * B +
+// b) * tps + tile, so a unit's tiles run on one XCD.  Per element the
+// arithmetic is the other engines' (the same MFMA chain over d, staging, 1/rms
+// and epilogue), so the K/V are bit-identical.
+template <int HD, bool PACKED, bool FOLD>
+__global__ __launch_bounds__(kNtWide, 1) void proj_wide_kernel(ProjArgs a, int per_xcd, int tps, int n_units) {
+  extern __shared__ __align__(16) char lds[];
+  constexpr int MT = kMtWide, NT = kNtWide;
+  constexpr ProjLds PL = proj_lds<uint16_t>(HD, MT);
+  constexpr int KLD = kv_ld<uint16_t>(HD);
+  const int tid = threadIdx.x;
+  const unsigned item = (blockIdx.x % kXcds) * (unsigned)per_xcd + blockIdx.x / kXcds;
+  const unsigned n_tiles = (unsigned)a.B * (unsigned)tps;
+  if (item >= (unsigned)n_units * n_tiles) return;
+  const int unit = (int)(item / n_tiles);
+  const unsigned rem = item - (unsigned)unit * n_tiles;
+  const int b = (int)(rem / (unsigned)tps);
+  const int t0 = (int)(rem - (unsigned)b * (unsigned)tps) * MT;
+  const int n = min(MT, a.T - t0);
+  const size_t hd_d = (size_t)HD * a.d;
+  const bool kv_mode = unit < a.n_kv_units;
+  Half halves[2];
+  int heads[2];
+  if (kv_mode) {
+    halves[0] = Half{static_cast<const uint16_t*>(a.w_k) + unit * hd_d, 1};
+    halves[1] = Half{static_cast<const uint16_t*>(a.w_v) + unit * hd_d, 0};
+    heads[0] = heads[1] = unit;
+  } else {
+    const int u = unit - a.n_kv_units;
+    heads[0] = 2 * u;
+    heads[1] = 2 * u + 1;
+    halves[0] = Half{static_cast<const uint16_t*>(a.w_q) + heads[0] * hd_d, 1};
+    halves[1] = Half{heads[1] < a.n_q ? static_cast<const uint16_t*>(a.w_q) + heads[1] * hd_d : nullptr, 1};
+  }
+
+  double* rev = reinterpret_cast<double*>(lds + PL.rev);
+  float* rinv = reinterpret_cast<float*>(lds + PL.rinv);
+  int* pos = reinterpret_cast<int*>(lds + PL.pos);
+  uint16_t* hst = reinterpret_cast<uint16_t*>(lds + PL.hst);
+  uint16_t* kv = reinterpret_cast<uint16_t*>(lds + PL.kv);
+  uint16_t* gam = reinterpret_cast<uint16_t*>(lds + PL.end);
+  const TileSetup<uint16_t, HD, NT, false, !FOLD> su(nullptr, 0, 0, 0, 0, a.gamma, a.d, a.rev);
+  auto setup = [&]() {
+    su.store(nullptr, gam, rev);
+    if (tid < MT) pos[tid] = a.pos0[b] + t0 + tid;
+  };
+  WideTile<HD, MT, PACKED, FOLD>::run(static_cast<const uint16_t*>(a.h) + ((size_t)b * a.h_ld + t0) * a.d, n, gam,
+                                      static_cast<const uint16_t*>(a.gamma), a.d, a.eps, halves, hst, rinv, pos, rev,
+                                      kv, setup);
+  __syncthreads();
+
+  // store: 16-byte chunks of each valid token row of each present half
+  constexpr int CPR = HD / 8;
+  for (int c = tid; c < 2 * n * CPR; c += NT) {
+    const int half = c / (n * CPR);
+    const int r2 = c - half * n * CPR;
+    const int row = r2 / CPR, ch = r2 - row * CPR;
+    if (half ? halves[1].w == nullptr : halves[0].w == nullptr) continue;
+    const int head = heads[half];
+    uint16_t* dst;
+    if (kv_mode) {
+      uint16_t* base = static_cast<uint16_t*>(half ? a.v_out : a.k_out);
+      dst = base + (((size_t)b * a.n_kv + head) * a.kv_t_cap + a.kv_t_off + t0 + row) * HD;
+    } else {
+      dst = static_cast<uint16_t*>(a.q_out) + (((size_t)b * a.T + t0 + row) * a.n_q + head) * HD;  // [B][T][n_q][hd]
+    }
+    *reinterpret_cast<uint4*>(dst + ch * 8) = *reinterpret_cast<const uint4*>(kv + (size_t)row * KLD + half * HD + ch * 8);
+  }
+}
+
 // ------------------------------------------------------------------ recompute / prefill, split engine
 
 // bf16, head_dim 128 / 256: RW rows of one half of a unit (a KV head's K rows
@@ -1152,6 +1227,19 @@ static hipError_t proj_t(const ProjArgs& a, int n_units, hipStream_t st) {
   return hipGetLastError();
 }
 
+template <int HD, int L>
+static hipError_t proj_wide_t(const ProjArgs& a, int n_units, hipStream_t st) {
+  const size_t bytes = proj_lds<uint16_t>(HD, kMtWide).end + gamma_lds_bytes(a.d);
+  static std::atomic<size_t> done{0};
+  auto k = proj_wide_kernel<HD, L != 0, L == 2>;
+  hipError_t e = ensure_lds(k, bytes, done);
+  if (e != hipSuccess) return e;
+  const int tps = (a.T + kMtWide - 1) / kMtWide;
+  const XcdMap m = xcd_map((long long)n_units * a.B * tps);
+  hipLaunchKernelGGL(k, dim3(m.grid), dim3(kNtWide), bytes, st, a, m.per, tps, n_units);
+  return hipGetLastError();
+}
+
 template <int HD, int MT, int NT, int RW, int L>
 static hipError_t proj_split_t(const ProjArgs& a, int n_units, hipStream_t st) {
   const size_t bytes = split_lds(RW, MT).end + gamma_lds_bytes(a.d);
@@ -1304,6 +1392,14 @@ hipError_t launch_proj(const ProjArgs& a, int dtype_bf16, int hd, int layout, in
       constexpr int L = decltype(lc)::value;
       return hd == 256 ? proj_split_t<256, kMtNarrow, kNtNarrow, kRwNarrow, L>(a, n_units, st)
                        : proj_split_t<128, kMtNarrow, kNtNarrow, kRwNarrow, L>(a, n_units, st);
+    });
+  }
+  if (dtype_bf16 && (hd == 128 || hd == 256) &&
+      wide_prefill((long long)n_units * a.B * ((a.T + kMtWide - 1) / kMtWide)) &&
+      proj_lds<uint16_t>(hd, kMtWide).end + gamma_lds_bytes(a.d) <= kLdsPerGroup) {
+    return with_layout(layout, [&](auto lc) -> hipError_t {
+      constexpr int L = decltype(lc)::value;
+      return hd == 256 ? proj_wide_t<256, L>(a, n_units, st) : proj_wide_t<128, L>(a, n_units, st);
     });
   }
   if (dtype_bf16 && split_prefill(hd, a.T, 2LL * n_units * a.B * ((a.T + kMtSplit - 1) / kMtSplit))) {

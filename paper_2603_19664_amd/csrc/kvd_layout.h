@@ -76,6 +76,10 @@ constexpr int kNtNarrow = 256;
 constexpr int kRwNarrow = 128;
 constexpr long long kNarrowMaxWgs = 512;
 constexpr bool narrow_prefill(long long wgs) { return wgs <= kNarrowMaxWgs; }
+// Prefill on WideTile's 128-token tiles of both halves: calls with at least a
+// full round of them (kWideMinTiles; each weight fragment then feeds four MFMAs
+// instead of the split engine's two), where their LDS fits.
+constexpr bool wide_prefill(long long wgs) { return wgs >= kWideMinTiles; }
 
 // A stored tail of at most fold_rows<T>() rows (a decode step's current token)
 // joins the split of the last recomputed tile of a fused call: the rows are

@@ -23,7 +23,7 @@ from paper_2603_19664_amd import configs as C
 from paper_2603_19664_amd import kvd
 
 from gpu_cases import (TOL, empty_kv, err, f64, gpu_fused, gpu_recompute, gpu_unfused, make_layer, note,
-                       oracle_decode)
+                       oracle_decode, oracle_kv)
 
 pytestmark = pytest.mark.gpu
 
@@ -173,3 +173,20 @@ def test_wide_window(window):
                                   f64(L.w_v), window, s.n_q_heads, s.n_kv_heads, s.head_dim, s.rms_eps,
                                   s.rope_theta)
     check(f"wide window {window} vs oracle", out, ref)
+
+
+@pytest.mark.parametrize("hd", [128, 256])
+def test_wide_prefill_full_round(hd):
+    # kvd_recompute_kv on a call with a full round of 128-token tiles (4 sequences
+    # x 8 KV heads x 8 tiles = 256) runs on WideTile's tiles of both halves: its
+    # K/V equal, bit for bit, the fused kernel's recomputed K/V (64-token tiles)
+    # and the oracle's within the bf16 tolerance
+    L = make_layer(C.QWEN_1_5B if hd == 128 else C.GEMMA3_4B, B=4, T=1000, seed=123 + hd, d_model=512, n_q=16,
+                   n_kv=8, head_dim=hd, pos0=[0, 300, 17, 900])
+    K, V = gpu_recompute(L)
+    kvd.kvd_set_fused_tokens(64)
+    _, _, _, (dk, dv) = gpu_fused(L, kv_debug=True)
+    assert torch.equal(_bits(K), _bits(dk)) and torch.equal(_bits(V), _bits(dv))
+    ok, ov = oracle_kv(L, b_sel=[0, 3])
+    check("wide prefill K vs oracle", K[[0, 3]], ok)
+    check("wide prefill V vs oracle", V[[0, 3]], ov)
