@@ -123,3 +123,45 @@ def test_block_forward_full_size_gemma_t4096_sampled_rows():
         hhat = hx[p] + heads @ wo.T
         ref = hhat + O.swiglu_mlp(O.rms_normalize(hhat, g_m, s.rms_eps)[None], wg, wu, wd)[0]
         check(f"block row {p} vs oracle", got[p], ref, TOL)
+
+
+def test_block_forward_wide_tiles_ragged_two_sequences():
+    # a Gemma-3-4B-shaped block (d_ff 2048) over 2 sequences of 2000 positions:
+    # 4000 token rows put the Q/K/V projection, W_o, the gate/up and the down
+    # projection on 128-token tiles whose last one is partial (32 rows) and
+    # whose tiles of the prefill stop at each sequence's end (80 rows); position
+    # offsets 0 and 37.  Sampled rows of both sequences against the oracle.
+    import oracle as O
+    from paper_2603_19664_amd import inputs
+    wl = C.GEMMA3_4B
+    d_ff, B, T = 2048, 2, 2000
+    s = kvd.shape_of(wl).packed()
+    gamma, w_q, w_k, w_v = inputs.weights(wl, 3, 0, "cuda")
+    w_o, gamma_mlp, w_gate, w_up, w_down = inputs.block_weights(wl, 3, d_ff, 0, "cuda")
+    pw = lambda w: kvd.kvd_pack_weights(s, w)  # noqa: E731
+    lw = (gamma, pw(w_q), pw(w_k), pw(w_v), kvd.kvd_pack_matrix(w_o), gamma_mlp, pw(w_gate), pw(w_up),
+          kvd.kvd_pack_matrix(w_down))
+    h, _ = inputs.residuals(wl, 3, B, T, 0, "cuda")
+    h = h.contiguous()
+    offs = [0, 37]
+    pos0 = torch.tensor(offs, dtype=torch.int32, device="cuda")
+    out = torch.empty_like(h)
+    ws = torch.empty(kvd.kvd_block_workspace_bytes(s, d_ff, B, T), dtype=torch.uint8, device="cuda")
+    kvd.kvd_block_forward(s, kvd.block_weights(*lw), h, out, pos0, ws)
+    torch.cuda.synchronize()
+    g_a, wq, wk, wv, wo, g_m, wg, wu, wd = (f64(t) for t in (gamma, w_q, w_k, w_v, w_o, gamma_mlp, w_gate, w_up,
+                                                                w_down))
+    got = f64(out)
+    for b, rows in ((0, [0, 127, 128, 1999]), (1, [0, 1919, 1920, 1968, 1999])):
+        hx = f64(h)[b]
+        last = max(rows) + 1
+        K, V = O.recompute_kv(hx[None, :last], g_a, wk, wv, offs[b] + np.arange(last)[None, :], s.n_kv_heads,
+                              s.head_dim, s.rms_eps, s.rope_theta)
+        for p in rows:
+            hb = O.rms_normalize(hx[p], g_a, s.rms_eps)
+            qp = O.apply_rope(O.project_heads(hb[None], wq, s.n_q_heads, s.head_dim), float(offs[b] + p),
+                              s.rope_theta)
+            heads = O.decode_attention(qp, K[:, :, :p + 1], V[:, :, :p + 1]).reshape(-1)
+            hhat = hx[p] + heads @ wo.T
+            ref = hhat + O.swiglu_mlp(O.rms_normalize(hhat, g_m, s.rms_eps)[None], wg, wu, wd)[0]
+            check(f"block row ({b}, {p}) vs oracle", got[b, p], ref, TOL)
