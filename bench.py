@@ -17,7 +17,8 @@ Printed: ONE JSON line with
     HIP events over the timed region;
   - per-op us/layer, and the cached-K/V and unfused baselines of the same step;
   - the recompute-vs-cached-read crossover over batch size (Gemma-3-4B layer,
-    context 2048, B = 1..64; each op timed after a cache-evicting read);
+    context 2048, B = 1..64; each op timed after a cache-evicting read), against a
+    K/V cache in HBM and against one held in pinned host memory (copied over PCIe);
   - workloads: the SmolLM2-135M fp32 layer, the Qwen2.5-1.5B-shaped 28-layer step
     (B = 8, context 16384) and the Gemma-3-4B multi-turn step (B = 16, turn
     boundaries up to 5120 tokens), fused against cached;
@@ -402,7 +403,9 @@ def run_crossover(args, torch, np, kvd, acc, configs, inputs, op_time, log):
     """Fused recompute-attention vs cached-K/V attention (each with its split-K merge) for one
     Gemma-3-4B-shaped layer, context 2048 + current token, over batch size.  Each
     measurement runs after a cache-evicting read (cold_flush), so both sides read their
-    inputs from HBM."""
+    inputs from HBM.  A third leg keeps the bf16 K/V cache in pinned host memory (a cache
+    offloaded off the GPU): its K and V are copied over PCIe into HBM, then attended by the
+    same cached-K/V kernel; the time is copy plus attention."""
     wl = configs.GEMMA3_SWEEP
     s = kvd.shape_of(wl).packed()
     T = wl.ctx
@@ -429,6 +432,17 @@ def run_crossover(args, torch, np, kvd, acc, configs, inputs, op_time, log):
         it = 10
         f_us = op_time(fz, iters=it, flush=flush, median=True)
         c_us = op_time(cz, iters=it, flush=flush, median=True)
+        Kh = torch.empty(Kc.shape, dtype=Kc.dtype, pin_memory=True)
+        Vh = torch.empty(Vc.shape, dtype=Vc.dtype, pin_memory=True)
+        Kh.copy_(Kc)
+        Vh.copy_(Vc)
+
+        def hz():
+            Kc.copy_(Kh, non_blocking=True)
+            Vc.copy_(Vh, non_blocking=True)
+            cz()
+        h_us = op_time(hz, iters=5, flush=flush, median=True)
+        kv_bytes = 2 * Kc.numel() * Kc.element_size()
         fl = acc.fused_flops(B, T, 1, wl.n_q, wl.n_kv, wl.d_model, wl.head_dim)
         S_c = kvd.kvd_num_splits(s, kvd.KVD_OP_CACHED_ATTN, B, T + 1)
         cb = acc.cached_bytes(B, T + 1, wl.n_q, wl.n_kv, wl.head_dim, 2, S_c)
@@ -436,14 +450,20 @@ def run_crossover(args, torch, np, kvd, acc, configs, inputs, op_time, log):
                      "fused_tflops": fl / (f_us * 1e-6) / 1e12,
                      "fused_mfma_frac": fl / (f_us * 1e-6) / 1e12 / MI355X_BF16_PEAK_TFLOPS,
                      "cached_gbs": cb / (c_us * 1e-6) / 1e9,
-                     "cached_hbm_frac": cb / (c_us * 1e-6) / 1e9 / MI355X_HBM_PEAK_GBS, "cached_splits": S_c})
+                     "cached_hbm_frac": cb / (c_us * 1e-6) / 1e9 / MI355X_HBM_PEAK_GBS, "cached_splits": S_c,
+                     "host_cached_us": h_us, "ratio_fused_over_host_cached": f_us / h_us,
+                     "host_copy_gbs": kv_bytes / ((h_us - c_us) * 1e-6) / 1e9})
         log(f"[bench] crossover B={B}: fused {f_us:.1f} us ({rows[-1]['fused_tflops']:.0f} TFLOP/s), cached "
-            f"{c_us:.1f} us ({rows[-1]['cached_gbs']:.0f} GB/s)")
-        del h, Kc, Vc
+            f"{c_us:.1f} us ({rows[-1]['cached_gbs']:.0f} GB/s), host-resident cache {h_us:.1f} us")
+        del h, Kc, Vc, Kh, Vh
         torch.cuda.empty_cache()
     faster = [r["B"] for r in rows if r["ratio_fused_over_cached"] < 1.0]
+    faster_host = [r["B"] for r in rows if r["ratio_fused_over_host_cached"] < 1.0]
     return {"workload": wl.name, "ctx": T, "rows": rows, "batches_where_recompute_wins": faster,
-            "note": "medians of 10 calls, each after a 1 GiB cache-evicting read; both include their split-K merge"}
+            "batches_where_recompute_beats_host_cache": faster_host,
+            "note": "medians of 10 calls (5 for the host-resident cache), each after a 1 GiB cache-evicting read; "
+                    "every leg includes its split-K merge; host_copy_gbs = K/V bytes / (host-resident time - "
+                    "cached time)"}
 
 
 def run_next(args, torch, np, kvd, configs, inputs, op_time, log):
