@@ -208,7 +208,11 @@ kvd_status kvd_cached_attn(const kvd_attn_shape* shape, const void* q, const kvd
  *   kv_debug: NULL in production.  If not NULL, the recomputed K/V are also
  *   written to it at rows kv_debug->t_off .. +T_rec-1 (for bit-identity checks).
  * Split-K as in kvd_decode_attn, one split per recomputed tile, on one of
- * three engines (see kvd_set_fused_tokens):
+ * four engines (see kvd_set_fused_tokens):
+ *   - pair (bf16, head_dim 128, an even n_kv_heads, at most 6 query heads per
+ *     KV head at common d_model): 128-token tiles of the K and V rows of two
+ *     KV heads, when the call has at least 256 of them (B * n_kv_heads / 2 *
+ *     ceil(T_rec / 128) >= 256); the same chunks and splits as wide;
  *   - wide (bf16, head_dim 128 / 256): 128-token tiles of K and V rows, when
  *     the call has at least 256 of them (B * n_kv_heads * ceil(T_rec / 128)
  *     >= 256: a full round of the chip);
@@ -398,9 +402,10 @@ int32_t kvd_set_attn_workgroups(int32_t target);
 /* Tuning of kvd_fused_recompute_attn and kvd_fused_window_attn: the recomputed
  * tokens per workgroup.  0 (the default) chooses per call, 128 asks for the
  * wide engine wherever it exists (bf16, head_dim 128 / 256, its LDS within
- * the limit; elsewhere 64 is used), KVD_FUSED_SPLIT / KVD_FUSED_SPLIT64 for
- * the split engine with 128- / 64-token chunks wherever a call can run on it
- * (elsewhere 64), 64 for the 64-token tiles;
+ * the limit; elsewhere 64 is used), KVD_FUSED_PAIR for the pair engine
+ * wherever it exists (elsewhere the wide engine, else 64), KVD_FUSED_SPLIT /
+ * KVD_FUSED_SPLIT64 for the split engine with 128- / 64-token chunks wherever
+ * a call can run on it (elsewhere 64), 64 for the 64-token tiles;
  * other values mean 0.  Returns the previous setting.  Process-wide: it
  * changes kvd_num_splits of KVD_OP_FUSED (not kvd_workspace_bytes, which
  * covers every engine).  All engines give K/V bit-identical to
@@ -408,6 +413,7 @@ int32_t kvd_set_attn_workgroups(int32_t target);
  * split boundaries).                                                         */
 #define KVD_FUSED_SPLIT (-128)
 #define KVD_FUSED_SPLIT64 (-64)
+#define KVD_FUSED_PAIR (-2)
 int32_t kvd_set_fused_tokens(int32_t tokens);
 
 const char* kvd_status_str(kvd_status status);

@@ -152,6 +152,20 @@ FusedPlan wide_plan(int32_t T_rec, int32_t T_tail) {
   return p;
 }
 
+// Two KV heads per 128-token tile: bf16 at head_dim 128 with an even n_kv,
+// where the pair tile's LDS fits.  Chunks and splits are the wide engine's.
+bool pair_supported(const kvd_attn_shape* s, int32_t T_rec) {
+  if (T_rec < 1 || s->dtype != KVD_BF16 || s->head_dim != 128 || s->n_kv_heads % 2 != 0) return false;
+  return kvd::fused_pair_lds_bytes(s->n_q_heads / s->n_kv_heads) + kvd::gamma_lds_bytes(s->d_model) <=
+         kvd::kLdsPerGroup;
+}
+
+FusedPlan pair_plan(int32_t T_rec, int32_t T_tail) {
+  FusedPlan p = wide_plan(T_rec, T_tail);
+  p.engine = kvd::kFusedPair;
+  return p;
+}
+
 // The split engine with mt-token chunks: bf16 at head_dim 128 / 256,
 // recomputed rows, a tail that folds (at most fold_rows rows), at most
 // kSplitMaxChunks chunks per sequence, and its LDS within the limit.
@@ -184,13 +198,18 @@ FusedPlan split_plan(int32_t T_rec, int32_t mt) {
 FusedPlan fused_plan(const kvd_attn_shape* s, int32_t B, int32_t T_rec, int32_t T_tail) {
   const int32_t mode = g_fused_tokens.load(std::memory_order_relaxed);
   const bool wide_ok = T_rec > 0 && wide_supported(s);
+  const bool pair_ok = pair_supported(s, T_rec);
   if (mode == kvd::kMtBf16) return narrow_plan(s, T_rec, T_tail);
   if (mode == kvd::kMtWide) return wide_ok ? wide_plan(T_rec, T_tail) : narrow_plan(s, T_rec, T_tail);
+  if (mode == KVD_FUSED_PAIR)
+    return pair_ok ? pair_plan(T_rec, T_tail) : wide_ok ? wide_plan(T_rec, T_tail) : narrow_plan(s, T_rec, T_tail);
   if (mode == KVD_FUSED_SPLIT)
     return split_supported(s, T_rec, T_tail, kvd::kMtSplit) ? split_plan(T_rec, kvd::kMtSplit)
                                                              : narrow_plan(s, T_rec, T_tail);
   if (mode == KVD_FUSED_SPLIT64)
     return split_supported(s, T_rec, T_tail, 64) ? split_plan(T_rec, 64) : narrow_plan(s, T_rec, T_tail);
+  if (pair_ok && (int64_t)B * (s->n_kv_heads / 2) * ceil_div(T_rec, kvd::kMtWide) >= kvd::kWideMinTiles)
+    return pair_plan(T_rec, T_tail);
   if (wide_ok && (int64_t)B * s->n_kv_heads * ceil_div(T_rec, kvd::kMtWide) >= kvd::kWideMinTiles)
     return wide_plan(T_rec, T_tail);
   if (split_supported(s, T_rec, T_tail, 64) &&
@@ -892,7 +911,8 @@ int32_t kvd_set_attn_workgroups(int32_t target) {
 }
 
 int32_t kvd_set_fused_tokens(int32_t tokens) {
-  if (tokens != kvd::kMtBf16 && tokens != kvd::kMtWide && tokens != KVD_FUSED_SPLIT && tokens != KVD_FUSED_SPLIT64)
+  if (tokens != kvd::kMtBf16 && tokens != kvd::kMtWide && tokens != KVD_FUSED_SPLIT && tokens != KVD_FUSED_SPLIT64 &&
+      tokens != KVD_FUSED_PAIR)
     tokens = 0;
   return g_fused_tokens.exchange(tokens, std::memory_order_relaxed);
 }

@@ -705,6 +705,161 @@ __global__ __launch_bounds__(kNtWide, 1) void fused_wide_kernel(
   fused_body<uint16_t, HD, kMtWide, PACKED, FOLD>(a, per_xcd, hg);
 }
 
+// ------------------------------------------------------------------ fused recompute + attention, KV-head pairs
+
+// bf16, head_dim 128: one workgroup per (pair of KV heads 2 jp, 2 jp + 1,
+// sequence b, chunk c) on the wide engine's head_dim 256 wave layout.  The K
+// rows of both heads are the tile's 256 "K" rows and their V rows its 256 "V"
+// rows (the heads' rows are adjacent in W_k / W_v), so each wave runs two
+// 32-row blocks for all four token blocks and every residual B fragment read
+// from LDS feeds twice the MFMAs of the head_dim 128 wide tile.  Per element
+// the MFMA chain over d, 1/rms and the RoPE epilogue are the wide engine's, and
+// the RoPE table holds head_dim 128's 64 frequencies twice (rows 128.. of a
+// half are the second head's features 0..), so K/V equal every other engine's
+// bit for bit.  The K|V tile row is [K head 0 | K head 1 | V head 0 | V head
+// 1]; the attention, partial, arrival and merge then run per head, as on the
+// wide engine, with both groups' q rows in LDS.  Chunks c < n_tail attend the
+// stored tail tiles of both heads, one after the other.
+template <bool PACKED, bool FOLD>
+__global__ __launch_bounds__(kNtWide, 1) void fused_pair_kernel(FusedArgs a, int per_xcd, int hg) {
+  extern __shared__ __align__(16) char lds[];
+  constexpr int HD = 128, MT = kMtWide, NT = kNtWide;
+  constexpr int FR = fold_rows<uint16_t>();
+  constexpr ProjLds PL = proj_lds<uint16_t>(2 * HD, MT, FR);
+  constexpr int KLD = kv_ld<uint16_t>(2 * HD);  // pair tile row stride
+  constexpr int KPL = (MT + FR + 63) / 64;
+  const int tid = threadIdx.x;
+  const bool fold = fold_tail<uint16_t>(a.n_rec, a.T_tail);
+  const int n_tail = fused_tail_tiles<uint16_t>(a.n_rec, a.T_tail);
+  const int C = n_tail + a.n_rec;
+  const int np = a.n_kv >> 1;
+  const unsigned item = (blockIdx.x % kXcds) * (unsigned)per_xcd + blockIdx.x / kXcds;
+  if (item >= (unsigned)np * (unsigned)a.B * (unsigned)C) return;
+  // items as on the wide engine, with head pairs in place of heads
+  const int hg_log2 = __builtin_ctz((unsigned)hg);
+  const unsigned hgC = (unsigned)C << hg_log2;
+  const unsigned gi = item / hgC, rem = item - gi * hgC;
+  const int pg = (int)(gi / (unsigned)a.B);
+  const int b = (int)(gi - (unsigned)pg * (unsigned)a.B);
+  const int c = (int)(rem >> hg_log2);
+  const int jp = (pg << hg_log2) + (int)(rem & (unsigned)(hg - 1));
+  const int j0 = 2 * jp;  // first KV head of the pair
+  const int rc = c - n_tail;
+  const int g = a.n_q / a.n_kv;
+  const AttnLds AL = attn_lds(PL.end, g, HD, MT + FR);
+  uint16_t* kv = reinterpret_cast<uint16_t*>(lds + PL.kv);
+  // LDS of head hh's attention: its group's q rows follow the first group's
+  auto head_lds = [&](int hh) {
+    AttnLds L = AL;
+    L.q = AL.q + (size_t)hh * g * HD * sizeof(uint16_t);
+    return L;
+  };
+  const uint16_t* const tk = static_cast<const uint16_t*>(a.tk);
+  const uint16_t* const tv = static_cast<const uint16_t*>(a.tv);
+
+  // folded tail: one 16-byte chunk of a pair row per thread (64 chunks a row),
+  // copied into LDS rows MT.. by the tile's setup
+  const bool tail_here = fold && rc == a.n_rec - 1;
+  constexpr int TCH = 4 * HD * 2 / 16;
+  static_assert(FR * TCH <= NT, "one folded-tail chunk per thread");
+
+  if (c >= n_tail) {
+    const int t0 = rc * MT;
+    const int n = min(MT, a.T_rec - t0);
+    double* rev = reinterpret_cast<double*>(lds + PL.rev);
+    float* rinv = reinterpret_cast<float*>(lds + PL.rinv);
+    int* pos = reinterpret_cast<int*>(lds + PL.pos);
+    uint16_t* hst = reinterpret_cast<uint16_t*>(lds + PL.hst);
+    uint16_t* gam = reinterpret_cast<uint16_t*>(lds + AL.end);
+    // both groups' q rows (2 g heads from head j0 * g), gamma, the 64 frequencies
+    const TileSetup<uint16_t, HD, NT, true, !FOLD> su(static_cast<const uint16_t*>(a.q), b, a.n_q, jp, 2 * g,
+                                                      a.gamma, a.d, a.rev);
+    auto setup = [&]() {
+      const int p0 = (a.pos0 != nullptr ? a.pos0[b] : 0) + t0;
+      su.store(reinterpret_cast<float*>(lds + AL.q), gam, rev);
+      if (tid >= HD / 2 && tid < HD) rev[tid] = a.rev[tid - HD / 2];  // frequency f % 64 at f
+      if (tid < MT) pos[tid] = p0 + tid;
+      const int tr = tid / TCH, tch = tid - tr * TCH;
+      if (tail_here && tr < a.T_tail) {
+        int tslot = a.tail_t_off + tr;
+        tslot -= tslot >= a.tail_t_cap ? a.tail_t_cap : 0;
+        const int part = tch >> 4;  // K head 0, K head 1, V head 0, V head 1
+        const size_t trow = ((size_t)b * a.n_kv + j0 + (part & 1)) * a.tail_t_cap + tslot;
+        *reinterpret_cast<u32x4_t*>(kv + (size_t)(MT + tr) * KLD + 8 * tch) =
+            *reinterpret_cast<const u32x4_t*>((part >= 2 ? tv : tk) + trow * HD + 8 * (tch & 15));
+      }
+    };
+    const size_t hd_d = (size_t)HD * a.d;
+    const Half halves[2] = {Half{static_cast<const uint16_t*>(a.w_k) + j0 * hd_d, 1},
+                            Half{static_cast<const uint16_t*>(a.w_v) + j0 * hd_d, 0}};
+    WideTile<2 * HD, MT, PACKED, FOLD>::run(static_cast<const uint16_t*>(a.h) + ((size_t)b * a.h_ld + t0) * a.d, n,
+                                            gam, static_cast<const uint16_t*>(a.gamma), a.d, a.eps, halves, hst, rinv,
+                                            pos, rev, kv, setup);
+    __syncthreads();
+    if (a.dbg_k != nullptr) {
+      constexpr int CPR = HD / 8;
+      for (int i = tid; i < 4 * n * CPR; i += NT) {
+        const int part = i / (n * CPR);
+        const int r2 = i - part * n * CPR;
+        const int row = r2 / CPR, ch = r2 - row * CPR;
+        uint16_t* base = static_cast<uint16_t*>(part >= 2 ? a.dbg_v : a.dbg_k);
+        uint16_t* dst = base + (((size_t)b * a.n_kv + j0 + (part & 1)) * a.dbg_t_cap + a.dbg_t_off + t0 + row) * HD;
+        *reinterpret_cast<uint4*>(dst + 8 * ch) = *reinterpret_cast<const uint4*>(kv + (size_t)row * KLD + part * HD + 8 * ch);
+      }
+    }
+    int nk = n;
+    if (tail_here) {
+      if (n < MT) move_rows<uint16_t, 2 * HD, NT, FR>(kv, MT, n, a.T_tail);
+      nk = n + a.T_tail;
+    }
+    for (int hh = 0; hh < 2; ++hh) {
+      const AttnLds L = head_lds(hh);
+      attend_scores_mfma<HD, NT, KPL, KLD>(kv + hh * HD, nk, MT + FR, g, lds, L);
+      attend_pv_mfma<HD, NT, KLD>(kv + (2 + hh) * HD, nk, MT + FR, g, lds, L);
+      write_partial<HD, NT>(lds, L, a.ws_acc, a.ws_ml, b, a.n_q, j0 + hh, g, a.S, rc, 1);
+      __syncthreads();
+    }
+  } else {
+    // tail tile c of each head in turn, on the head_dim 128 tile layout
+    const int r0 = c * kTile;
+    const int nk = c == n_tail - 1 ? a.T_tail - r0 : kTile;
+    load_q<uint16_t, HD, NT>(static_cast<const uint16_t*>(a.q), b, a.n_q, jp, 2 * g,
+                             reinterpret_cast<float*>(lds + AL.q));
+    int tr0 = a.tail_t_off + r0;
+    tr0 -= tr0 >= a.tail_t_cap ? a.tail_t_cap : 0;
+    int tr1 = tr0 + kTile;
+    tr1 -= tr1 >= a.tail_t_cap ? a.tail_t_cap : 0;
+    for (int hh = 0; hh < 2; ++hh) {
+      load_kv_tile<uint16_t, HD, NT>(tk, tv, b, a.n_kv, j0 + hh, a.tail_t_cap, tr0, min(nk, kTile), kv);
+      if (nk > kTile)
+        load_kv_tile<uint16_t, HD, NT>(tk, tv, b, a.n_kv, j0 + hh, a.tail_t_cap, tr1, nk - kTile,
+                                       kv + (size_t)kTile * kv_ld<uint16_t>(HD));
+      __syncthreads();
+      const AttnLds L = head_lds(hh);
+      attend_tile<uint16_t, HD, NT, KPL>(kv, nk, MT + FR, g, lds, L);
+      write_partial<HD, NT>(lds, L, a.ws_acc, a.ws_ml, b, a.n_q, j0 + hh, g, a.S, a.n_rec + c, 1);
+      __syncthreads();
+    }
+  }
+  if (a.out != nullptr) {
+    // arrivals at both heads' counters, then one merge of the rows of the heads
+    // this workgroup completed (rows are merged independently of each other)
+    bool last[2];
+#pragma unroll
+    for (int hh = 0; hh < 2; ++hh) {
+      unsigned long long* ctr = a.ws_done + (size_t)b * a.n_kv + j0 + hh;
+      const unsigned long long before = split_arrive(ctr, 1, reinterpret_cast<unsigned long long*>(lds + AL.ctr));
+      last[hh] = split_complete(ctr, before, 1, a.S);
+    }
+    const int first = last[0] ? 0 : 1;
+    const int cnt = (int)last[0] + (int)last[1];
+    if (cnt > 0)
+      combine_rows<uint16_t, HD, NT>(a.ws_acc, a.ws_ml, static_cast<uint16_t*>(a.out),
+                                     (size_t)b * a.n_q + (size_t)(j0 + first) * g, cnt * g, a.S,
+                                     reinterpret_cast<float*>(lds + AL.cmb));
+  }
+}
+
 // ------------------------------------------------------------------ fused recompute + attention, split engine
 
 // bf16, head_dim 128 / 256, for calls with too few 128-token tiles to fill the
@@ -1303,6 +1458,24 @@ static hipError_t fused_wide_t(const FusedArgs& a, hipStream_t st) {
   return hipGetLastError();
 }
 
+template <int L>
+static hipError_t fused_pair_t(const FusedArgs& a, hipStream_t st) {
+  if (a.n_kv % 2 != 0) return hipErrorInvalidValue;
+  const size_t bytes = fused_pair_lds_bytes(a.n_q / a.n_kv) + gamma_lds_bytes(a.d);
+  static std::atomic<size_t> done{0};
+  auto k = fused_pair_kernel<L != 0, L == 2>;
+  hipError_t e = ensure_lds(k, bytes, done);
+  if (e != hipSuccess) return e;
+  const int n_tail = fused_tail_tiles<uint16_t>(a.n_rec, a.T_tail);
+  const int C = n_tail + a.n_rec;
+  const int np = a.n_kv / 2;
+  const XcdMap m = xcd_map((long long)np * a.B * C);
+  // a pair's weight rows are a head_dim 256 head's
+  const int hg = n_tail > 0 ? 1 : fused_head_group(np, 256, m.per);
+  hipLaunchKernelGGL(k, dim3(m.grid), dim3(kNtWide), bytes, st, a, m.per, hg);
+  return hipGetLastError();
+}
+
 template <int HD, int MT, int L>
 static hipError_t fused_split_t(const FusedArgs& a, hipStream_t st) {
   const size_t bytes = fused_split_lds_bytes(a.n_q / a.n_kv, HD, MT) + gamma_lds_bytes(a.d);
@@ -1453,6 +1626,10 @@ hipError_t launch_fused(const FusedArgs& a, int dtype_bf16, int hd, int layout, 
         default: return hipErrorInvalidValue;
       }
     });
+  }
+  if (engine == kFusedPair) {
+    if (!dtype_bf16 || hd != 128) return hipErrorInvalidValue;
+    return with_layout(layout, [&](auto lc) -> hipError_t { return fused_pair_t<decltype(lc)::value>(a, st); });
   }
   if (engine == kFusedWide) {
     if (!dtype_bf16) return hipErrorInvalidValue;

@@ -158,9 +158,11 @@ hipError_t launch_project_current(const ProjArgs& a, int dtype_bf16, int hd, int
                                   hipStream_t st);
 // engine: kFusedTile64 (fused_kernel), kFusedWide (the 128-token engine,
 // fused_wide_kernel; bf16, head_dim 128 / 256, a.n_rec counted in 128-token
-// tiles) or kFusedSplit / kFusedSplit64 (fused_split_kernel; bf16, head_dim 128
-// / 256, 128- or 64-token chunks, a tail of at most fold_rows rows, folded).
-enum { kFusedTile64 = 0, kFusedWide = 1, kFusedSplit = 2, kFusedSplit64 = 3 };
+// tiles), kFusedSplit / kFusedSplit64 (fused_split_kernel; bf16, head_dim 128
+// / 256, 128- or 64-token chunks, a tail of at most fold_rows rows, folded) or
+// kFusedPair (fused_pair_kernel; bf16, head_dim 128, an even n_kv, two KV heads
+// per 128-token tile, a.n_rec as on the wide engine).
+enum { kFusedTile64 = 0, kFusedWide = 1, kFusedSplit = 2, kFusedSplit64 = 3, kFusedPair = 4 };
 hipError_t launch_fused(const FusedArgs& a, int dtype_bf16, int hd, int layout, int engine, hipStream_t st);
 // gamma: nullptr, or [d] bf16 folded into the packed values (bf16(w * gamma)).
 hipError_t launch_pack(const void* w, const void* gamma, void* out, int rows, int d, hipStream_t st);

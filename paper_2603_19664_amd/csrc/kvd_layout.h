@@ -229,6 +229,15 @@ constexpr size_t fused_wide_lds_bytes(int g, int hd) {
   return attn_lds(proj_lds<uint16_t>(hd, kMtWide, fold_rows<uint16_t>()).end, g, hd, kMtWide + fold_rows<uint16_t>())
       .end;
 }
+// The pair fused kernel (head_dim 128, two KV heads per 128-token tile): the
+// head_dim 256 wide tile's LDS, whose K|V rows hold both heads, then one head
+// group's attention scratch; its q region (g x 128 floats) holds both groups'
+// raw bf16 q rows.
+constexpr size_t fused_pair_lds_bytes(int g) {
+  return attn_lds(proj_lds<uint16_t>(256, kMtWide, fold_rows<uint16_t>()).end, g, 128,
+                  kMtWide + fold_rows<uint16_t>())
+      .end;
+}
 
 // Streaming projection (current-token q/K/V): one workgroup of kStreamWaves
 // waves per 32 weight rows.  Waves 1.. keep kStreamDepth chunks of the rows'

@@ -26,6 +26,7 @@ KVD_W_ROWMAJOR, KVD_W_PACKED, KVD_W_PACKED_GAMMA = 0, 1, 2
 KVD_OP_DECODE_ATTN, KVD_OP_CACHED_ATTN, KVD_OP_FUSED = 0, 1, 2
 KVD_FUSED_SPLIT = -128  # kvd_set_fused_tokens: the split engine, 128-token chunks
 KVD_FUSED_SPLIT64 = -64  # the split engine, 64-token chunks
+KVD_FUSED_PAIR = -2  # two KV heads per 128-token tile (bf16, head_dim 128, even n_kv_heads)
 
 _DTYPES = {KVD_F32: torch.float32, KVD_BF16: torch.bfloat16}
 
@@ -265,8 +266,9 @@ def kvd_set_attn_workgroups(target: int) -> int:
 
 def kvd_set_fused_tokens(tokens: int) -> int:
     """Recomputed tokens per workgroup of the fused calls: 0 chooses per call, 128 the
-    wide engine where it exists, KVD_FUSED_SPLIT the split engine where a call can use
-    it, 64 the 64-token tiles; returns the previous setting."""
+    wide engine where it exists, KVD_FUSED_PAIR the pair engine (two KV heads per tile)
+    where it exists, KVD_FUSED_SPLIT the split engine where a call can use it, 64 the
+    64-token tiles; returns the previous setting."""
     return lib.kvd_set_fused_tokens(int(tokens))
 
 

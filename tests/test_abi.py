@@ -215,7 +215,7 @@ def _engine(s, B, T_rec, T_tail, tokens):
         return big and T_rec > 0 and T_tail <= 4 and -(-T_rec // mt) <= 256
     if tokens == 64:
         return "tile64"
-    if tokens == 128:
+    if tokens in (128, kvd.KVD_FUSED_PAIR):  # the pair engine chunks and splits as the wide one
         return "wide" if wide_ok else "tile64"
     if tokens == kvd.KVD_FUSED_SPLIT:
         return "split" if split_ok(128) else "tile64"
@@ -290,8 +290,9 @@ def test_fused_tiling_policy():
     assert ns(gemma, 1, 1023, 1) == 16        # a sliding window at B = 1
     assert ns(qwen, 8, 16384, 1) == 128
     try:
-        for tokens in (0, 64, 128, kvd.KVD_FUSED_SPLIT, kvd.KVD_FUSED_SPLIT64):
-            assert lib.kvd_set_fused_tokens(tokens) in (0, 64, 128, kvd.KVD_FUSED_SPLIT, kvd.KVD_FUSED_SPLIT64)
+        modes = (0, 64, 128, kvd.KVD_FUSED_SPLIT, kvd.KVD_FUSED_PAIR, kvd.KVD_FUSED_SPLIT64)
+        for tokens in modes:
+            assert lib.kvd_set_fused_tokens(tokens) in modes
             for sh in [gemma, qwen] + others:
                 for B, T, Tt in [(1, 4096, 1), (2, 4096, 1), (8, 2048, 1), (1, 100, 1), (1, 0, 3), (3, 130, 70),
                                  (16, 5120, 0), (1, 64, 4), (1, 64, 5), (1, 32769, 1)]:
