@@ -54,6 +54,9 @@ def parse():
     p.add_argument("--no-baselines", action="store_true", help="skip the cached / unfused per-op timings")
     p.add_argument("--cpu-seconds", type=float, default=12.0, help="CPU oracle time budget")
     p.add_argument("--sweep-batches", default="1,2,4,8,16,32,64")
+    p.add_argument("--no-host-cache", action="store_true",
+                   help="crossover without its host-resident cache leg (profiles count the attention dispatches "
+                        "of the two HBM legs only)")
     p.add_argument("--calibration-copy-mib", type=int, default=256,
                    help="size of one untimed device-to-device copy whose HBM counters calibrate the traffic figure")
     p.add_argument("--next", action="store_true",
@@ -432,16 +435,19 @@ def run_crossover(args, torch, np, kvd, acc, configs, inputs, op_time, log):
         it = 10
         f_us = op_time(fz, iters=it, flush=flush, median=True)
         c_us = op_time(cz, iters=it, flush=flush, median=True)
-        Kh = torch.empty(Kc.shape, dtype=Kc.dtype, pin_memory=True)
-        Vh = torch.empty(Vc.shape, dtype=Vc.dtype, pin_memory=True)
-        Kh.copy_(Kc)
-        Vh.copy_(Vc)
+        h_us = None
+        if not args.no_host_cache:
+            Kh = torch.empty(Kc.shape, dtype=Kc.dtype, pin_memory=True)
+            Vh = torch.empty(Vc.shape, dtype=Vc.dtype, pin_memory=True)
+            Kh.copy_(Kc)
+            Vh.copy_(Vc)
 
-        def hz():
-            Kc.copy_(Kh, non_blocking=True)
-            Vc.copy_(Vh, non_blocking=True)
-            cz()
-        h_us = op_time(hz, iters=5, flush=flush, median=True)
+            def hz():
+                Kc.copy_(Kh, non_blocking=True)
+                Vc.copy_(Vh, non_blocking=True)
+                cz()
+            h_us = op_time(hz, iters=5, flush=flush, median=True)
+            del Kh, Vh
         kv_bytes = 2 * Kc.numel() * Kc.element_size()
         fl = acc.fused_flops(B, T, 1, wl.n_q, wl.n_kv, wl.d_model, wl.head_dim)
         S_c = kvd.kvd_num_splits(s, kvd.KVD_OP_CACHED_ATTN, B, T + 1)
@@ -451,14 +457,16 @@ def run_crossover(args, torch, np, kvd, acc, configs, inputs, op_time, log):
                      "fused_mfma_frac": fl / (f_us * 1e-6) / 1e12 / MI355X_BF16_PEAK_TFLOPS,
                      "cached_gbs": cb / (c_us * 1e-6) / 1e9,
                      "cached_hbm_frac": cb / (c_us * 1e-6) / 1e9 / MI355X_HBM_PEAK_GBS, "cached_splits": S_c,
-                     "host_cached_us": h_us, "ratio_fused_over_host_cached": f_us / h_us,
-                     "host_copy_gbs": kv_bytes / ((h_us - c_us) * 1e-6) / 1e9})
+                     "host_cached_us": h_us, "ratio_fused_over_host_cached": None if h_us is None else f_us / h_us,
+                     "host_copy_gbs": None if h_us is None else kv_bytes / ((h_us - c_us) * 1e-6) / 1e9})
         log(f"[bench] crossover B={B}: fused {f_us:.1f} us ({rows[-1]['fused_tflops']:.0f} TFLOP/s), cached "
-            f"{c_us:.1f} us ({rows[-1]['cached_gbs']:.0f} GB/s), host-resident cache {h_us:.1f} us")
-        del h, Kc, Vc, Kh, Vh
+            f"{c_us:.1f} us ({rows[-1]['cached_gbs']:.0f} GB/s)"
+            + ("" if h_us is None else f", host-resident cache {h_us:.1f} us"))
+        del h, Kc, Vc
         torch.cuda.empty_cache()
     faster = [r["B"] for r in rows if r["ratio_fused_over_cached"] < 1.0]
-    faster_host = [r["B"] for r in rows if r["ratio_fused_over_host_cached"] < 1.0]
+    faster_host = [r["B"] for r in rows
+                   if r["ratio_fused_over_host_cached"] is not None and r["ratio_fused_over_host_cached"] < 1.0]
     return {"workload": wl.name, "ctx": T, "rows": rows, "batches_where_recompute_wins": faster,
             "batches_where_recompute_beats_host_cache": faster_host,
             "note": "medians of 10 calls (5 for the host-resident cache), each after a 1 GiB cache-evicting read; "
