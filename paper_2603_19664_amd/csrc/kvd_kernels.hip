@@ -9,6 +9,12 @@
 //   fused_kernel        per (b, KV head, 64-key chunk): recompute K/V of the chunk
 //                       into LDS and emit its split-K softmax partial without writing
 //                       K/V to HBM; stored tail tiles (CONCAT) ride along.
+//   fused_wide_kernel   the same per 128-key chunk (bf16, head_dim 128 / 256).
+//   fused_pair_kernel   the same per (b, pair of KV heads, 128-key chunk) at bf16
+//                       head_dim 128, on the head_dim 256 wave layout.
+//   fused_split_kernel  the same with a chunk's K and V rows recomputed by two
+//                       workgroups (one half each).
+//   proj_split_kernel / proj_wide_kernel  prefill on the split / wide layouts.
 //   stream_attn_kernel  bf16 stored-K/V attention: per (key split, KV head, b) one
 //                       workgroup streams the split's keys in 16-key blocks, loads of
 //                       the next block in flight, and emits one split-K partial.
