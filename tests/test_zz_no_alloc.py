@@ -3,7 +3,8 @@ workspace form (kvd_fused_recompute_attn) through the C ABI: two calls in a row 
 the shared static scratch, the second with a smaller input, each output
 bit-identical to the workspace call's (the same kernels run on the same values)
 and within the bf16 tolerance (2e-2) of the fp64 oracle; then an fp32 call
-(1e-5) and one at the Gemma-3-4B headline size."""
+(1e-5), one at the Gemma-3-4B headline size and a head_dim 128 call on the pair
+engine (two KV heads per tile)."""
 import pytest
 import torch
 
@@ -32,7 +33,7 @@ def _both(L):
     return out_ws, out_na
 
 
-@pytest.mark.parametrize("case", ["bf16_two_calls_second_smaller", "fp32", "gemma_headline_size"])
+@pytest.mark.parametrize("case", ["bf16_two_calls_second_smaller", "fp32", "gemma_headline_size", "pair_engine"])
 def test_noalloc_matches_workspace_call(case):
     note(f"[gpu] noalloc {case}")
     if case == "bf16_two_calls_second_smaller":
@@ -41,6 +42,12 @@ def test_noalloc_matches_workspace_call(case):
     elif case == "fp32":
         layers = [make_layer(C.SMOLLM_FP32, B=2, T=256, seed=63, pos0=[0, 31]),
                   make_layer(C.SMOLLM_FP32, B=1, T=40, seed=64)]
+    elif case == "pair_engine":
+        # head_dim 128: 4 sequences x 4 pairs of KV heads x 16 tiles = 256 pair tiles (the
+        # pair engine), then a call too small for it
+        qw = dict(d_model=512, n_q=16, n_kv=8, head_dim=128)
+        layers = [make_layer(C.QWEN_1_5B, B=4, T=2000, seed=65, pos0=[0, 300, 17, 900], **qw),
+                  make_layer(C.QWEN_1_5B, B=1, T=300, seed=66, **qw)]
     else:
         layers = [make_layer(C.GEMMA3_4B, B=1, T=4096, layer=7), make_layer(C.GEMMA3_4B, B=1, T=1000, layer=8)]
     for i, L in enumerate(layers):
