@@ -121,7 +121,7 @@ class Call:
 def main():
     args = parse()
     if args.gpus != 1:
-        print(f"bench.py runs on one GPU only: this build has no multi-GPU path (asked for --gpus {args.gpus}). "
+        print(f"bench.py runs on one GPU only: the library has no multi-GPU path (asked for --gpus {args.gpus}). "
               "The KV-Direct hot path shards over sequences, KV heads or keys with one exchange of split-K "
               "partials per layer; that exchange is not built.", file=sys.stderr)
         sys.exit(2)

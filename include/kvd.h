@@ -66,7 +66,7 @@ typedef enum {
   KVD_OK = 0,
   KVD_ERR_NULL = 1,         /* a required pointer is NULL */
   KVD_ERR_SHAPE = 2,        /* inconsistent or out-of-range sizes */
-  KVD_ERR_UNSUPPORTED = 3,  /* valid arguments this build has no kernel for */
+  KVD_ERR_UNSUPPORTED = 3,  /* valid arguments the library has no kernel for */
   KVD_ERR_WORKSPACE = 4,    /* workspace NULL or smaller than required */
   KVD_ERR_ALIGN = 5,        /* a tensor pointer is not 16-byte aligned */
   KVD_ERR_DEVICE = 6        /* the HIP runtime reported an error */
