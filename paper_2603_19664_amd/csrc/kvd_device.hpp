@@ -552,8 +552,9 @@ struct WideTile {
   static constexpr int DW = SPLIT && NB_F == 1 ? 4 : 2;
   // residual K-steps in registers: a split wave of one 32-row block has so
   // little work per K-step that one step of lead does not cover the load
-  // latency, so it keeps two steps in flight
-  static constexpr int DH = SPLIT && NB_F == 1 ? 2 : 1;
+  // latency, so it keeps two steps in flight, and four on 64-token tiles
+  // (half the work per step again; its registers allow it without spills)
+  static constexpr int DH = SPLIT && NB_F == 1 ? (MT == 64 ? 4 : 2) : 1;
   static constexpr int DL = kDepth;
   static constexpr int SLOT = NB_T * 4 * 512;  // elements per LDS slot (one K-step)
   static constexpr int NU = 4 * NB_T;          // units (substep, token block) per K-step
