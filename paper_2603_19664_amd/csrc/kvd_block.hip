@@ -30,7 +30,7 @@ __global__ __launch_bounds__(kNtTile, 1) void gemm_kernel(GemmArgs a, int per_xc
   constexpr ProjLds PL = proj_lds<uint16_t>(HD, MT);
   constexpr int KLD = kv_ld<uint16_t>(HD);
   using Tile = MfmaTile<HD, kMtBf16, PACKED>;
-  using Wide = WideTile<HD, 2 * kMtBf16, PACKED>;
+  using Wide = WideTile<HD, 2 * kMtBf16, PACKED, false, kNtWide, kv_ld<uint16_t>(HD), false, true>;
   static_assert(MT == kMtBf16 || MT == 2 * kMtBf16, "64- or 128-token tiles");
   static_assert(Tile::NB_F == 2 && Tile::WT == 1 && Tile::NB_T == 2 && Wide::NB_F == 2 && NT == Wide::NT,
                 "wave w owns rows 32 w.. of both halves");

@@ -536,8 +536,11 @@ struct MfmaTile {
 // per step, after the second substep.  Loads go through
 // buffer resources (wave-uniform base and extent in SGPRs, a 32-bit offset per
 // lane), which keeps the addresses out of the vector registers.
+// RLEAD (tiles of both halves): residual rows two K-steps ahead and weights one
+// (instead of one and two), for the same register count; taken by the callers
+// whose tiles it measured faster (the block GEMMs, the KV-head pairs).
 template <int HD, int MT, bool PACKED, bool FOLD = false, int NTX = kNtWide, int KLDX = kv_ld<uint16_t>(HD),
-          bool SPLITX = false>
+          bool SPLITX = false, bool RLEAD = false>
 struct WideTile {
   static constexpr int NT = NTX;
   static constexpr int NW = NT / 64;
@@ -549,12 +552,13 @@ struct WideTile {
   static constexpr int KLD = KLDX;
   // weight K-steps in flight: a split wave of one 32-row block holds 4 (its
   // A fragments are half the 8-wave layout's per step)
-  static constexpr int DW = SPLIT && NB_F == 1 ? 4 : 2;
+  static constexpr int DW = SPLIT && NB_F == 1 ? 4 : (RLEAD ? 1 : 2);
   // residual K-steps in registers: a split wave of one 32-row block has so
   // little work per K-step that one step of lead does not cover the load
   // latency, so it keeps two steps in flight, and four on 64-token tiles
   // (half the work per step again; its registers allow it without spills)
-  static constexpr int DH = SPLIT && NB_F == 1 ? (MT == 64 ? 4 : 2) : 1;
+  static constexpr int DH = SPLIT && NB_F == 1 ? (MT == 64 ? 4 : 2) : (RLEAD ? 2 : 1);
+  static_assert(!RLEAD || !SPLIT, "RLEAD: tiles of both halves");
   static constexpr int DL = kDepth;
   static constexpr int SLOT = NB_T * 4 * 512;  // elements per LDS slot (one K-step)
   static constexpr int NU = 4 * NB_T;          // units (substep, token block) per K-step

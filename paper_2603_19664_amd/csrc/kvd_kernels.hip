@@ -798,7 +798,7 @@ __global__ __launch_bounds__(kNtWide, 1) void fused_pair_kernel(FusedArgs a, int
     const size_t hd_d = (size_t)HD * a.d;
     const Half halves[2] = {Half{static_cast<const uint16_t*>(a.w_k) + j0 * hd_d, 1},
                             Half{static_cast<const uint16_t*>(a.w_v) + j0 * hd_d, 0}};
-    WideTile<2 * HD, MT, PACKED, FOLD>::run(static_cast<const uint16_t*>(a.h) + ((size_t)b * a.h_ld + t0) * a.d, n,
+    WideTile<2 * HD, MT, PACKED, FOLD, NT, KLD, false, true>::run(static_cast<const uint16_t*>(a.h) + ((size_t)b * a.h_ld + t0) * a.d, n,
                                             gam, static_cast<const uint16_t*>(a.gamma), a.d, a.eps, halves, hst, rinv,
                                             pos, rev, kv, setup);
     __syncthreads();
