@@ -538,7 +538,8 @@ struct MfmaTile {
 // lane), which keeps the addresses out of the vector registers.
 // RLEAD (tiles of both halves): residual rows two K-steps ahead and weights one
 // (instead of one and two), for the same register count; taken by the callers
-// whose tiles it measured faster (the block GEMMs, the KV-head pairs).
+// whose tiles it measured faster (the block GEMMs, the KV-head pairs, the
+// 64-token fused tiles, the wide prefill), not by the wide fused engine.
 template <int HD, int MT, bool PACKED, bool FOLD = false, int NTX = kNtWide, int KLDX = kv_ld<uint16_t>(HD),
           bool SPLITX = false, bool RLEAD = false>
 struct WideTile {

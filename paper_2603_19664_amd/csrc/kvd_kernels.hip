@@ -182,9 +182,9 @@ __global__ __launch_bounds__(kNtWide, 1) void proj_wide_kernel(ProjArgs a, int p
     su.store(nullptr, gam, rev);
     if (tid < MT) pos[tid] = a.pos0[b] + t0 + tid;
   };
-  WideTile<HD, MT, PACKED, FOLD>::run(static_cast<const uint16_t*>(a.h) + ((size_t)b * a.h_ld + t0) * a.d, n, gam,
-                                      static_cast<const uint16_t*>(a.gamma), a.d, a.eps, halves, hst, rinv, pos, rev,
-                                      kv, setup);
+  WideTile<HD, MT, PACKED, FOLD, kNtWide, kv_ld<uint16_t>(HD), false, true>::run(
+      static_cast<const uint16_t*>(a.h) + ((size_t)b * a.h_ld + t0) * a.d, n, gam,
+      static_cast<const uint16_t*>(a.gamma), a.d, a.eps, halves, hst, rinv, pos, rev, kv, setup);
   __syncthreads();
 
   // store: 16-byte chunks of each valid token row of each present half
@@ -637,9 +637,10 @@ __device__ __forceinline__ void fused_body(const FusedArgs& a, int per_xcd, int 
     const Half halves[2] = {Half{static_cast<const T*>(a.w_k) + j * hd_d, 1},
                             Half{static_cast<const T*>(a.w_v) + j * hd_d, 0}};
     if constexpr (sizeof(T) == 2 && HD >= 128) {
-      WideTile<HD, MT, PACKED, FOLD>::run(static_cast<const uint16_t*>(a.h) + ((size_t)b * a.h_ld + t0) * a.d, n, gam,
-                                          static_cast<const uint16_t*>(a.gamma), a.d, a.eps, halves, hst, rinv, pos,
-                                          rev, kv, setup);
+      // residual rows two K-steps ahead on 64-token tiles (RLEAD), one on the wide engine
+      WideTile<HD, MT, PACKED, FOLD, kNtWide, kv_ld<uint16_t>(HD), false, MT == 64>::run(
+          static_cast<const uint16_t*>(a.h) + ((size_t)b * a.h_ld + t0) * a.d, n, gam,
+          static_cast<const uint16_t*>(a.gamma), a.d, a.eps, halves, hst, rinv, pos, rev, kv, setup);
     } else if constexpr (sizeof(T) == 2) {
       MfmaTile<HD, MT, PACKED, FOLD>::run(hrow, valid, gam, static_cast<const uint16_t*>(a.gamma), a.d, a.eps, halves,
                                           hst, rinv, pos, rev, kv, setup);
